@@ -1,0 +1,422 @@
+"""Checks that pin the CPU oracle to things other than itself.
+
+Each ``pin_*`` function takes the oracle module and raises AssertionError
+when the oracle disagrees with:
+  * a worked example derived by hand from the equations of Sec. III
+    (tests/golden/hand_example.json);
+  * closed forms (GELU through the standard normal CDF, tau values, the
+    round-half-even rule of Eq. block-count);
+  * brute-force enumeration on tiny layers (every subset of blocks and of
+    experts, the output as an explicit sum over channels, all in float64);
+  * reductions to textbook layers: top-k MoE (Eq. vanilla-moe-output), the
+    dense FFN (Eq. ffn-kv) and the soft MoE over all experts;
+  * the identical-expert decomposition E = sum of its blocks (Sec. III-A);
+  * the mixture-mass bound (Eq. mixture-mass-bound).
+The implementations here are written independently of the oracle (pure
+Python loops and math.erf). tests/test_oracle_mutations.py re-runs these pins
+on deliberately broken copies of the oracle to show that each mistake is
+caught.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ------------------------------------------------------------ textbook ---
+def phi(a):
+    """Standard normal CDF."""
+    return 0.5 * (1.0 + math.erf(a / math.sqrt(2.0)))
+
+
+def gelu_tb(a):
+    return a * phi(a)
+
+
+_gelu_vec = np.vectorize(gelu_tb, otypes=[np.float64])
+
+
+def tb_ffn(x, w_up, w_down):
+    """Dense FFN of Eq. ffn-kv for rows x: GELU(x K) V, with K = w_up^T and
+    V = w_down^T (float64)."""
+    return _gelu_vec(x @ w_up.T) @ w_down.T
+
+
+def tb_softmax(l):
+    e = np.exp(l - l.max(axis=-1, keepdims=True))
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def layer_cfg(d, K, B, M, **kw):
+    cfg = dict(n_tokens=0, d_model=d, n_experts=K, n_blocks=B, block_width=M,
+               dtype="f32", tau=None, mass_threshold=1.0, max_shared=B,
+               alpha_mode="adaptive", alpha_fixed=0.0, mass_mode="coupled",
+               fixed_k=1, select_mode="prototype")
+    cfg.update(kw)
+    return cfg
+
+
+def random_layer(rng, N, d, K, B, M, weight_scale=1.0, logit_scale=1.0):
+    H = B * M
+    f = np.float32
+    return dict(
+        X=rng.standard_normal((N, d)).astype(f),
+        W_router=(logit_scale * rng.standard_normal((K + 1, d)) / math.sqrt(d)).astype(f),
+        prototypes=(rng.standard_normal((B, d)) / math.sqrt(d)).astype(f),
+        W_up=(weight_scale * rng.standard_normal((K + 1, H, d))).astype(f),
+        W_down=(weight_scale * rng.standard_normal((K + 1, d, H))).astype(f))
+
+
+def _forward(O, cfg, L, valid=None):
+    cfg = dict(cfg)
+    cfg["n_tokens"] = L["X"].shape[0]
+    return O.forward(cfg, L["X"], valid, L["W_router"], L["prototypes"], L["W_up"], L["W_down"])
+
+
+def _close(a, b, rel, what):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    scale = max(1e-30, float(np.abs(b).max()))
+    err = float(np.abs(a - b).max()) / scale
+    assert err <= rel, f"{what}: relative error {err:.3e} > {rel:.1e}"
+
+
+# ---------------------------------------------------------------- pins ---
+def pin_hand_example(O):
+    with open(os.path.join(GOLDEN, "hand_example.json")) as f:
+        g = json.load(f)
+    f32 = np.float32
+    L = dict(X=np.array(g["X"], f32), W_router=np.array(g["W_router"], f32),
+             prototypes=np.array(g["prototypes"], f32), W_up=np.array(g["W_up"], f32),
+             W_down=np.array(g["W_down"], f32))
+    Y, rec = _forward(O, g["config"], L)
+    B = g["config"]["n_blocks"]
+    for e in g["expected"]:
+        t = e["token"]
+        assert abs(float(rec["alpha"][t]) - e["alpha"]) < 1e-6, ("alpha", t)
+        assert int(rec["n_shared"][t]) == e["n_shared"], ("b", t)
+        m = int(rec["shared_mask"][t])
+        assert [c for c in range(B) if m >> c & 1] == e["shared_blocks"], ("I_shr", t)
+        assert int(rec["n_res"][t]) == e["n_res"], ("k", t)
+        assert list(rec["expert_ids"][t]) == e["experts"], ("q", t)
+        assert np.allclose(rec["weights"][t], e["weights"], atol=1e-6), ("p", t)
+        bc = O.block_count(int(rec["n_shared"][t]), int(rec["n_res"][t]), B)
+        assert bc == e["block_count"], ("C_B", t)
+        assert np.allclose(Y[t], e["y"], rtol=1e-6, atol=1e-7), ("y", t, Y[t], e["y"])
+
+
+def pin_gelu(O):
+    a = np.linspace(-6.0, 6.0, 241)
+    ref = np.array([gelu_tb(v) for v in a])
+    assert np.allclose(O.gelu(a), ref, rtol=1e-12, atol=1e-15), "GELU vs a Phi(a)"
+    # GELU(a) - GELU(-a) = a (erf is odd) and GELU(0) = 0.
+    assert np.allclose(O.gelu(a) - O.gelu(-a), a, atol=1e-12), "GELU odd-part identity"
+    assert O.gelu(np.array([0.0]))[0] == 0.0
+    # Phi(1) and Phi(2) from the standard normal table.
+    assert abs(O.gelu(np.array([1.0]))[0] - 0.8413447460685429) < 1e-12
+    assert abs(O.gelu(np.array([2.0]))[0] - 2 * 0.9772498680518208) < 1e-12
+
+
+def pin_tau(O):
+    for B, num, den in ((2, 1, 4), (4, 3, 16), (8, 7, 64), (16, 15, 256), (32, 31, 1024)):
+        assert float(O.shared_offset(dict(n_blocks=B, tau=None))) == num / den, B
+
+
+def pin_round_half_even(O):
+    """Eq. block-count with a fixed alpha: B alpha on exact half-integers."""
+    rng = np.random.default_rng(5)
+    L = random_layer(rng, 1, 4, 2, 4, 1)
+    for alpha, b_expected in ((0.125, 0), (0.375, 2), (0.625, 2), (0.875, 4), (0.3, 1), (0.4, 2)):
+        cfg = layer_cfg(4, 2, 4, 1, alpha_mode="fixed", alpha_fixed=alpha)
+        _, rec = _forward(O, cfg, L)
+        assert int(rec["n_shared"][0]) == b_expected, (alpha, int(rec["n_shared"][0]))
+
+
+def pin_alpha_range(O):
+    """tau < alpha < 1 - tau and b in {1..B-1} (Sec. III-B), including
+    saturated sigmoids where B alpha lands on B - 1/2 or 1/2 (B = 2)."""
+    rng = np.random.default_rng(6)
+    for B in (2, 3, 4, 8):
+        d, K = 4, 3
+        L = random_layer(rng, 64, d, K, B, 1)
+        L["W_router"][0] *= np.float32(200.0)     # saturate sigma for most tokens
+        cfg = layer_cfg(d, K, B, 1)
+        _, rec = _forward(O, cfg, L)
+        tau = (B - 1) / B ** 2
+        a = rec["alpha"].astype(np.float64)
+        assert np.all(a >= tau - 1e-7) and np.all(a <= 1 - tau + 1e-7), B
+        b = rec["n_shared"]
+        assert b.min() >= 1 and b.max() <= B - 1, (B, b.min(), b.max())
+        if B == 2:
+            assert np.all(b == 1)
+    # z0 = 0 gives alpha = 1/2 exactly.
+    L = random_layer(rng, 1, 4, 2, 4, 1)
+    L["W_router"][0] = 0
+    _, rec = _forward(O, layer_cfg(4, 2, 4, 1), L)
+    assert float(rec["alpha"][0]) == 0.5
+
+
+def pin_rank_order(O):
+    """Order of Eq. sorted-affinity and TopK: decreasing, ties to the lower
+    index; equals a stable argsort of the negated values."""
+    rng = np.random.default_rng(7)
+    v = rng.integers(0, 4, size=(200, 9)).astype(np.float32)   # many ties
+    r = O._index_rank(v)
+    order = np.argsort(-v, axis=1, kind="stable")
+    expect = np.empty_like(order)
+    np.put_along_axis(expect, order, np.arange(9)[None, :].repeat(200, 0), axis=1)
+    assert np.array_equal(r, expect)
+
+
+def _bf_token(x, L, cfg):
+    """Brute-force float64 decisions and output of one token (tiny sizes)."""
+    d, K, B, M = cfg["d_model"], cfg["n_experts"], cfg["n_blocks"], cfg["block_width"]
+    Wr, Mu = L["W_router"].astype(float), L["prototypes"].astype(float)
+    Wu, Wd = L["W_up"].astype(float), L["W_down"].astype(float)
+    x = [float(v) for v in x]
+    dot = lambda a, b: sum(p * q for p, q in zip(a, b))
+    tau = (B - 1) / B ** 2
+    alpha = tau + (1 - 2 * tau) / (1 + math.exp(-dot(x, Wr[0])))
+    v = B * alpha
+    b = min(range(B + 1), key=lambda i: (abs(v - i), i % 2))       # nearest, ties even
+    b = min(max(b, 1), B - 1)
+    b = min(b, cfg["max_shared"])
+    u = [dot(x, Mu[c]) for c in range(B)]
+    S = max(itertools.combinations(range(B), b), key=lambda s: sum(u[c] for c in s))
+    l = [dot(x, Wr[j]) for j in range(1, K + 1)]
+    mx = max(l)
+    e = [math.exp(t - mx) for t in l]
+    s = [t / sum(e) for t in e]
+    target = min(1 - alpha, cfg["mass_threshold"])
+    for n in range(1, K + 1):
+        best = max(itertools.combinations(range(K), n), key=lambda c: sum(s[j] for j in c))
+        if sum(s[j] for j in best) >= target:
+            break
+    k = n
+    y = [0.0] * d
+    for c in range(B):
+        for h in range(c * M, (c + 1) * M):
+            if c in S:
+                g = alpha * gelu_tb(dot(x, Wu[0][h]))
+                for i in range(d):
+                    y[i] += g * Wd[0][i][h]
+            else:
+                for j in best:
+                    g = s[j] * gelu_tb(dot(x, Wu[j + 1][h]))
+                    for i in range(d):
+                        y[i] += g * Wd[j + 1][i][h]
+    # Distances of the continuous quantities to the decision boundaries.
+    us = sorted(u, reverse=True)
+    ss = sorted(s, reverse=True)
+    P = list(itertools.accumulate(ss))
+    fb = lambda r: min(min(max(r, 1), B - 1), cfg["max_shared"])
+    marg = [abs(v - (h + 0.5)) for h in range(-1, B + 1) if fb(h) != fb(h + 1)]
+    if 0 < b < B:
+        marg.append(us[b - 1] - us[b])
+    if k < K:
+        marg.append(ss[k - 1] - ss[k])
+    marg.append(abs(P[k - 1] - target))
+    if k > 1:
+        marg.append(abs(target - P[k - 2]))
+    return dict(alpha=alpha, b=b, S=tuple(sorted(S)), k=k, experts=set(j + 1 for j in best),
+                order=[j + 1 for j in sorted(range(K), key=lambda j: (-s[j], j))],
+                order_gap=min([ss[i] - ss[i + 1] for i in range(K - 1)], default=1.0),
+                y=np.array(y), margin=min(marg))
+
+
+def pin_bruteforce(O, n_layers=60, n_tok=6, seed=11):
+    rng = np.random.default_rng(seed)
+    checked = 0
+    for i in range(n_layers):
+        d = int(rng.integers(1, 5))
+        K = int(rng.integers(1, 4))
+        B = int(rng.integers(2, 5))
+        M = int(rng.integers(1, 3))
+        t = float(rng.choice([0.3, 0.6, 1.0]))
+        S_max = int(rng.integers(1, B + 1))
+        cfg = layer_cfg(d, K, B, M, mass_threshold=t, max_shared=S_max)
+        L = random_layer(rng, n_tok, d, K, B, M, logit_scale=float(rng.choice([0.5, 2.0, 6.0])))
+        Y, rec = _forward(O, cfg, L)
+        for tkn in range(n_tok):
+            ref = _bf_token(L["X"][tkn], L, cfg)
+            if ref["margin"] < 1e-4:
+                continue
+            b, S, k, q = O.decisions(rec, tkn)
+            assert abs(float(rec["alpha"][tkn]) - ref["alpha"]) < 1e-6, "alpha"
+            assert b == ref["b"], ("b", b, ref["b"])
+            assert S == ref["S"], ("I_shr", S, ref["S"])
+            assert k == ref["k"], ("k", k, ref["k"])
+            assert set(q) == ref["experts"], ("experts", q, ref["experts"])
+            if ref["order_gap"] >= 1e-4:
+                assert list(rec["expert_ids"][tkn]) == ref["order"], ("q", q, ref["order"])
+            scale = max(1e-12, float(np.abs(ref["y"]).max()))
+            err = float(np.abs(Y[tkn] - ref["y"]).max()) / scale
+            assert err < 1e-5, ("y", err)
+            checked += 1
+    assert checked >= n_layers * n_tok // 2, checked
+
+
+def pin_topk_moe(O):
+    """No shared blocks and a fixed k: the layer is the top-k MoE of Eq.
+    vanilla-moe-output over complete experts (affinities not renormalised)."""
+    rng = np.random.default_rng(12)
+    d, K, B, M, N = 8, 5, 4, 3, 40
+    L = random_layer(rng, N, d, K, B, M, weight_scale=0.3, logit_scale=3.0)
+    for kk in (1, 2, 5):
+        cfg = layer_cfg(d, K, B, M, max_shared=0, mass_mode="topk", fixed_k=kk)
+        Y, rec = _forward(O, cfg, L)
+        x = L["X"].astype(float)
+        s = tb_softmax(x @ L["W_router"][1:].astype(float).T)
+        ref = np.zeros_like(Y)
+        for j in range(K):
+            Fj = tb_ffn(x, L["W_up"][j + 1].astype(float), L["W_down"][j + 1].astype(float))
+            top = np.argsort(-s, axis=1, kind="stable")[:, :kk]
+            sel = (top == j).any(axis=1)
+            ref += (sel * s[:, j])[:, None] * Fj
+        _close(Y, ref, 1e-5, f"top-{kk} MoE")
+        assert np.all(rec["n_shared"] == 0)
+
+
+def pin_dense_ffn(O):
+    """alpha fixed at 1: every block is shared with weight 1 and the layer is
+    the shared expert's dense FFN."""
+    rng = np.random.default_rng(13)
+    d, K, B, M, N = 6, 3, 4, 2, 30
+    L = random_layer(rng, N, d, K, B, M, weight_scale=0.5)
+    cfg = layer_cfg(d, K, B, M, alpha_mode="fixed", alpha_fixed=1.0)
+    Y, rec = _forward(O, cfg, L)
+    ref = tb_ffn(L["X"].astype(float), L["W_up"][0].astype(float), L["W_down"][0].astype(float))
+    _close(Y, ref, 1e-9, "dense FFN")
+    assert np.all(rec["n_shared"] == B)
+
+
+def pin_soft_moe(O):
+    """No shared blocks and a fixed target of 1: every residual expert is
+    active with its affinity, sum_j s_j E_j(x)."""
+    rng = np.random.default_rng(14)
+    d, K, B, M, N = 6, 4, 2, 3, 30
+    L = random_layer(rng, N, d, K, B, M, weight_scale=0.5)
+    cfg = layer_cfg(d, K, B, M, max_shared=0, mass_mode="fixed", mass_threshold=1.0)
+    Y, rec = _forward(O, cfg, L)
+    x = L["X"].astype(float)
+    s = tb_softmax(x @ L["W_router"][1:].astype(float).T)
+    ref = sum(s[:, j:j + 1] * tb_ffn(x, L["W_up"][j + 1].astype(float), L["W_down"][j + 1].astype(float))
+              for j in range(K))
+    assert np.all(rec["n_res"] == K)
+    _close(Y, ref, 1e-5, "soft MoE")
+
+
+def pin_identical_experts(O):
+    """With identical experts F, y = alpha F^{I_shr}(x) + P_k F^{I_res}(x),
+    and the two block sums add up to the dense F(x) (Sec. III-A)."""
+    rng = np.random.default_rng(15)
+    d, K, B, M, N = 5, 4, 4, 2, 40
+    L = random_layer(rng, N, d, K, B, M, weight_scale=0.5)
+    L["W_up"][:] = L["W_up"][0]
+    L["W_down"][:] = L["W_down"][0]
+    cfg = layer_cfg(d, K, B, M, mass_threshold=1.0)
+    Y, rec = _forward(O, cfg, L)
+    x = L["X"].astype(float)
+    hid = _gelu_vec(x @ L["W_up"][0].astype(float).T)           # [N, H]
+    Vt = L["W_down"][0].astype(float)                            # [d, H]
+    for t in range(N):
+        m = int(rec["shared_mask"][t])
+        cols = np.array([(m >> (h // M)) & 1 for h in range(B * M)], bool)
+        Fs = Vt[:, cols] @ hid[t, cols]
+        Fr = Vt[:, ~cols] @ hid[t, ~cols]
+        assert np.allclose(Fs + Fr, Vt @ hid[t], atol=1e-9)
+        Pk = float(np.sum(rec["weights"][t, : rec["n_res"][t]].astype(float)))
+        ref = float(rec["alpha"][t]) * Fs + Pk * Fr
+        assert np.allclose(Y[t], ref, rtol=1e-9, atol=1e-9), t
+
+
+def pin_prefix_selection(O):
+    """Prefix selection (ablation): I_shr = the first b blocks."""
+    rng = np.random.default_rng(16)
+    d, K, B, M, N = 4, 3, 6, 1, 50
+    L = random_layer(rng, N, d, K, B, M)
+    cfg = layer_cfg(d, K, B, M, select_mode="prefix")
+    _, rec = _forward(O, cfg, L)
+    for t in range(N):
+        b = int(rec["n_shared"][t])
+        assert int(rec["shared_mask"][t]) == (1 << b) - 1
+
+
+def pin_mass_bound(O):
+    """Eq. mixture-mass-bound with the paper's target (t = 1):
+    beta <= P_k < beta + p_k and 1 <= alpha + P_k < 1 + p_k."""
+    rng = np.random.default_rng(17)
+    d, K, B, M, N = 16, 8, 8, 1, 500
+    L = random_layer(rng, N, d, K, B, M, logit_scale=2.0)
+    _, rec = _forward(O, layer_cfg(d, K, B, M, mass_threshold=1.0), L)
+    a = rec["alpha"].astype(float)
+    k = rec["n_res"]
+    p = rec["weights"].astype(float)
+    Pk = np.array([p[t, : k[t]].sum() for t in range(N)])
+    pk = p[np.arange(N), k - 1]
+    eps = 1e-6
+    assert np.all(1 - a <= Pk + eps) and np.all(Pk < 1 - a + pk + eps)
+    assert np.all(1 <= a + Pk + eps) and np.all(a + Pk < 1 + pk + eps)
+    assert np.all((k >= 1) & (k <= K))
+    assert np.all(np.diff(p, axis=1) <= 0)
+    assert np.allclose(p.sum(axis=1), 1.0, atol=1e-5)
+    for t in range(N):
+        assert sorted(rec["expert_ids"][t]) == list(range(1, K + 1))
+
+
+def pin_padding(O):
+    rng = np.random.default_rng(18)
+    d, K, B, M, N = 4, 3, 4, 2, 10
+    L = random_layer(rng, N, d, K, B, M)
+    valid = (np.arange(N) % 3 != 0).astype(np.uint8)
+    Y, rec = _forward(O, layer_cfg(d, K, B, M), L, valid=valid)
+    pad = valid == 0
+    assert np.all(Y[pad] == 0) and np.all(rec["n_res"][pad] == 0) and np.all(rec["alpha"][pad] == 0)
+    assert np.all(rec["expert_ids"][pad] == -1) and np.all(rec["shared_mask"][pad] == 0)
+    assert np.any(Y[~pad] != 0)
+
+
+def pin_stats(O):
+    rng = np.random.default_rng(19)
+    d, K, B, M, N = 8, 6, 4, 2, 300
+    L = random_layer(rng, N, d, K, B, M, logit_scale=2.0)
+    valid = (rng.random(N) < 0.8).astype(np.uint8)
+    cfg = layer_cfg(d, K, B, M, mass_threshold=0.7)
+    _, rec = _forward(O, cfg, L, valid=valid)
+    st = O.stats(cfg, rec)
+    v = valid.astype(bool)
+    b, k = rec["n_shared"][v], rec["n_res"][v]
+    assert st["n_valid"] == v.sum()
+    assert st["hist_b"].sum() == v.sum() and st["hist_k"].sum() == v.sum()
+    per_expert = np.zeros(K + 1, int)
+    for t in np.nonzero(v)[0]:
+        for j in rec["expert_ids"][t, : rec["n_res"][t]]:
+            per_expert[j] += 1
+    assert list(st["expert_tokens"][1:K + 1]) == list(per_expert[1:])
+    assert st["expert_tokens"][0] == v.sum()
+    cb = b + k * (B - b)
+    assert st["activated_blocks"] == cb.sum() and np.all(cb >= B)
+    assert st["activated_gemm_flops"] == 4 * d * M * cb.sum()
+
+
+def pin_margins(O):
+    """Margins agree with the brute-force float64 distances on tiny layers."""
+    rng = np.random.default_rng(20)
+    for _ in range(20):
+        d, K, B, M = 3, 3, 4, 1
+        cfg = layer_cfg(d, K, B, M, mass_threshold=0.8)
+        L = random_layer(rng, 8, d, K, B, M, logit_scale=2.0)
+        _, rec = _forward(O, cfg, L)
+        m, _ = O.margins(cfg, rec)
+        for t in range(8):
+            ref = _bf_token(L["X"][t], L, cfg)["margin"]
+            assert abs(m[t] - ref) < 1e-5, (m[t], ref)
+
+
+ALL_PINS = [pin_hand_example, pin_gelu, pin_tau, pin_round_half_even, pin_alpha_range,
+            pin_rank_order, pin_bruteforce, pin_topk_moe, pin_dense_ffn, pin_soft_moe,
+            pin_identical_experts, pin_prefix_selection, pin_mass_bound, pin_padding,
+            pin_stats, pin_margins]

@@ -1,0 +1,61 @@
+"""Planted mistakes in a copy of the oracle must be caught by the pins.
+
+Each mutant replaces one expression of the oracle's source (a dropped term,
+a wrong sign, index or comparison, a skipped step), is loaded as a separate
+module, and is run against every pin of tests/oracle_pins.py; at least one
+pin has to fail. This shows the pins constrain each step of the oracle, not
+only its overall shape. CPU only; the real oracle is untouched.
+"""
+import inspect
+import types
+
+import pytest
+
+import oracle.unif_moe_oracle as O
+from tests import oracle_pins as P
+
+MUTANTS = {
+    "sigmoid_sign": ("np.exp(-z0)", "np.exp(z0)"),
+    "tau_dropped": ("alpha = tau + one_minus_2tau * sigma", "alpha = sigma"),
+    "round_is_floor": ("np.rint(F32(B) * alpha)", "np.floor(F32(B) * alpha)"),
+    "clamp_dropped": ("b = np.clip(b, 1, B - 1)", "b = np.clip(b, 0, B)"),
+    "cap_dropped": ('b = np.minimum(b, cfg["max_shared"])', "b = b"),
+    "smallest_priorities": ("shared = _index_rank(u) < b[:, None]", "shared = _index_rank(-u) < b[:, None]"),
+    "softmax_unnormalised": ("s = e / np.cumsum(e, axis=1, dtype=F32)[:, -1:]", "s = e"),
+    "ascending_sort": ("rank = _index_rank(s)", "rank = _index_rank(-s)"),
+    "strict_mass_test": ("reached = P >= target[:, None]", "reached = P > target[:, None]"),
+    "demand_is_alpha": ("target = np.minimum(beta, t_mass)", "target = np.minimum(alpha, t_mass)"),
+    "k_off_by_one": ("reached.argmax(axis=1) + 1, K)", "np.minimum(reached.argmax(axis=1) + 2, K), K)"),
+    "expert_ids_zero_based": ('np.where(v[:, None], q + 1, -1)', 'np.where(v[:, None], q, -1)'),
+    "residual_on_shared_blocks": ("res_blocks = [c for c in range(W.B) if c not in set(shared_blocks)]",
+                                  "res_blocks = list(shared_blocks)"),
+    "shared_weight_dropped": ("y = F64(alpha) * W.selected_output(x, 0, shared_blocks)",
+                              "y = W.selected_output(x, 0, shared_blocks)"),
+    "gelu_dropped": ("return self.down[j][:, h] @ gelu(a)", "return self.down[j][:, h] @ a"),
+    "gelu_tanh": ("return 0.5 * a * (1.0 + _erf(a / math.sqrt(2.0)))", "return 0.5 * a * (1.0 + np.tanh(a))"),
+    "wrong_block_slice": ("h = slice(c * self.M, (c + 1) * self.M)", "h = slice(c, c + self.M)"),
+    "value_rows_swapped": ("a = self.up[j, h] @ x", "a = self.up[(j + 1) % self.up.shape[0], h] @ x"),
+    "margin_set_wrong": ("m_set[rows] = p[rows, k[rows] - 1] - p[rows, k[rows]]",
+                         "m_set[rows] = p[rows, 0] - p[rows, k[rows]]"),
+    "stats_cb_wrong": ("return b + k * (B - b)", "return b + k * B"),
+}
+
+
+def _mutant(name):
+    old, new = MUTANTS[name]
+    src = inspect.getsource(O)
+    assert src.count(old) == 1, f"mutation site of {name} not unique"
+    mod = types.ModuleType(f"oracle_mutant_{name}")
+    exec(compile(src.replace(old, new), mod.__name__, "exec"), mod.__dict__)
+    return mod
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name):
+    mod = _mutant(name)
+    for pin in P.ALL_PINS:
+        try:
+            pin(mod)
+        except Exception:
+            return
+    pytest.fail(f"no pin catches mutant {name}")

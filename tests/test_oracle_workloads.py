@@ -1,0 +1,83 @@
+"""Invariants of the oracle's routing on the five synthetic workloads (first
+4096 token rows each) and of the generator itself. CPU only."""
+import numpy as np
+import pytest
+
+import oracle.unif_moe_oracle as O
+from synth import config_names, generate, get_config
+from synth.generate import bf16_bits_to_f32, f32_to_bf16_bits
+
+N_SAMPLE = 4096
+
+
+@pytest.fixture(scope="module", params=config_names())
+def routed(request):
+    g = generate(request.param, n_tokens=min(N_SAMPLE, get_config(request.param)["n_tokens"]),
+                 weights=False)
+    rec = O.route(g["cfg"], g["X"], g["valid"], g["W_router"], g["prototypes"])
+    return g, rec
+
+
+def test_routing_invariants(routed):
+    g, rec = routed
+    cfg = g["cfg"]
+    K, B = cfg["n_experts"], cfg["n_blocks"]
+    v = rec["valid"]
+    tau = (B - 1) / B ** 2
+    a = rec["alpha"][v].astype(np.float64)
+    b, k = rec["n_shared"][v], rec["n_res"][v]
+    assert np.all((a > tau - 1e-7) & (a < 1 - tau + 1e-7))                 # Eq. alpha
+    assert b.min() >= 1 and b.max() <= min(B - 1, cfg["max_shared"])      # Sec. III-B
+    pop = np.array([bin(int(m)).count("1") for m in rec["shared_mask"][v]])
+    assert np.array_equal(pop, b)
+    assert k.min() >= 1 and k.max() <= K
+    p = rec["weights"][v].astype(np.float64)
+    assert np.all(np.diff(p, axis=1) <= 0)
+    assert np.allclose(p.sum(axis=1), 1, atol=1e-5)
+    ids = np.sort(rec["expert_ids"][v], axis=1)
+    assert np.all(ids == np.arange(1, K + 1)[None, :])
+    # Eq. mixture-mass-bound with the capped target: target <= P_k < target + p_k.
+    Pk = rec["P"][v][np.arange(len(k)), k - 1].astype(np.float64)
+    pk = p[np.arange(len(k)), k - 1]
+    tg = rec["target"][v].astype(np.float64)
+    assert np.all(Pk >= tg - 1e-6) and np.all(Pk < tg + pk + 1e-6)
+    cb = O.block_count(b.astype(np.int64), k.astype(np.int64), B)
+    assert np.all(cb >= B) and np.all(cb <= (K + 1) * B)                    # Eq. block-compute
+    # padded tokens
+    assert np.all(rec["n_res"][~v] == 0) and np.all(rec["expert_ids"][~v] == -1)
+
+
+def test_expected_routing_statistics(routed):
+    """Mean counts land where the workload recipes aim them."""
+    g, rec = routed
+    st = O.stats(g["cfg"], rec)
+    name = g["cfg"]["name"]
+    expect = {"tiny_f32": (1.5, 0.3), "vit_s16": (2.1, 0.2), "bert_base_padded": (2.0, 0.15),
+              "vit_b16": (3.35, 0.2), "zipf_stress": (9.0, 0.6)}[name]
+    assert abs(st["mean_k"] - expect[0]) < expect[1], st["mean_k"]
+    if name == "zipf_stress":
+        # bimodal shared demand: b is 1 or B-1 for almost every token
+        b = rec["n_shared"][rec["valid"]]
+        assert np.mean((b <= 2) | (b >= 29)) > 0.9
+
+
+def test_generator_is_prefix_stable():
+    a = generate("vit_s16", n_tokens=100, weights=False)
+    b = generate("vit_s16", n_tokens=300, weights=False)
+    assert np.array_equal(a["X"], b["X"][:100])
+    assert np.array_equal(a["W_router"], b["W_router"])
+
+
+def test_bf16_rounding():
+    v = np.array([1.0, 1 + 2 ** -8, 1 + 3 * 2 ** -8, -1 - 2 ** -9, 65504.0, 1e-30], np.float32)
+    r = bf16_bits_to_f32(f32_to_bf16_bits(v))
+    assert list(r[:4]) == [1.0, 1.0, 1 + 2 ** -6, -1.0]
+    assert np.all(np.abs(r - v) <= np.abs(v) * 2 ** -8)
+
+
+def test_padding_recipe():
+    g = generate("bert_base_padded", weights=False)
+    v = g["valid"].reshape(32, 128)
+    lengths = v.sum(axis=1)
+    assert lengths.min() >= 16 and lengths.max() <= 128
+    assert np.all(v == (np.arange(128)[None, :] < lengths[:, None]))
