@@ -1,0 +1,194 @@
+#!/usr/bin/env python3
+"""Throughput of the forward pass of one UniF-MoE feed-forward layer on one
+MI355X (bf16 expert FFNs, fp32 router), on seeded synthetic tokens.
+
+Workload: the ViT-B/16-shaped layer - 256 images x 197 tokens = 50,432 tokens,
+d = 768, K = 16 residual experts plus the shared expert, all upcycled from a
+d_ff = 3072 GELU FFN and split into B = 16 blocks of M = 192 channels,
+cumulative-mass threshold 0.6.
+
+One step = one unif_moe_layer_forward call (routing, permutation, the
+block-sparse expert GEMMs and the weighted merge) with inputs already
+resident in HBM. Prints one JSON line. Per-phase kernel durations come from
+HIP events recorded by the library itself on the launch stream during a
+second pass over the same number of steps (unif_moe_layer_forward_profiled).
+
+    python bench.py [--steps 20] [--warmup 3] [--workload vit_b16] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+PEAK_BF16_FLOPS = 2.5e15   # MI355X dense bf16 matrix-core peak
+PEAK_HBM_BYTES = 8.0e12    # MI355X HBM3E bandwidth
+METRIC = "UniF-MoE layer fwd tokens/s (bf16); MFMA util of activated FLOPs vs peak"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="vit_b16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=2048)
+    ap.add_argument("--cpu-repeats", type=int, default=3)
+    return ap.parse_args()
+
+
+def phase_bytes(cfg, st):
+    """Algorithmic HBM bytes of the non-GEMM phases (minimum traffic of each
+    step as defined, not counter readings)."""
+    N, d, K = cfg["n_tokens"], cfg["d_model"], cfg["n_experts"]
+    nv, sum_k, sum_cb = st["n_valid"], st["mean_k"] * st["n_valid"], st["activated_blocks"]
+    pairs = nv + sum_k
+    es = 2 if cfg["dtype"] == "bf16" else 4
+    routing = N * d * es + N * (4 + 4 + 8 + 4 + 8 * K)             # read X, write the record
+    permute = (N * (8 + 4) + sum_k * 4                               # read mask, k, q_1..q_k
+               + pairs * (4 + 8 + 4 + 4)                             # pair token/mask/expert, pair_of
+               + pairs * (4 + 8) + sum_cb * 4)                       # slab lists: read pairs, write rows
+    combine = pairs * d * es + pairs * 8 + N * 4 + N * d * es        # per-expert rows, weights, Y
+    return dict(routing=routing, permute=permute, combine=combine)
+
+
+def cpu_baseline(g, n_sample, repeats):
+    """The CPU oracle timed on a seeded sample of the same workload."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    import oracle.unif_moe_oracle as O
+
+    cfg = dict(g["cfg"])
+    valid_idx = np.arange(cfg["n_tokens"]) if g["valid"] is None else np.nonzero(g["valid"])[0]
+    rng = np.random.default_rng(2024)
+    sample = np.sort(rng.choice(valid_idx, size=min(n_sample, valid_idx.size), replace=False))
+    sub = dict(cfg, n_tokens=int(sample.size))
+    Xs = g["X"][sample]
+    weights = O.ExpertWeights(cfg, g["W_up"], g["W_down"])   # one-time weight preparation
+    times, cpu = [], []
+    for _ in range(repeats):
+        w0, c0 = time.perf_counter(), time.process_time()
+        O.forward(sub, Xs, None, g["W_router"], g["prototypes"], None, None, weights=weights)
+        times.append(time.perf_counter() - w0)
+        cpu.append(time.process_time() - c0)
+    med = float(np.median(times))
+    blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+    threads = int(blas[0]["num_threads"]) if blas else 1
+    return {"value": round(sample.size / med, 2), "unit": "tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{sample.size} seeded valid tokens of the same workload, routing + "
+                      f"per-token expert evaluation, median of {repeats} runs "
+                      f"({med:.2f} s each; numpy BLAS threads {threads}, "
+                      f"CPU/wall {float(np.median(cpu)) / med:.2f}; weights converted once, untimed)",
+            "host_cpu": _cpu_model(), "nproc": os.cpu_count()}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the layer forward shards by tokens with no "
+              "communication, and this build runs on a single MI355X (use --gpus 1).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2608_10392_amd import _lib
+    from paper_2608_10392_amd.layer import DeviceLayer
+    from synth import generate, layer_config
+
+    print(f"[bench] generating workload {args.workload}", file=sys.stderr, flush=True)
+    g = generate(args.workload)
+    cfg = layer_config(g["cfg"])
+    dev = DeviceLayer(cfg, g["X"], g["valid"], g["W_router"], g["prototypes"], g["W_up"], g["W_down"])
+    stream = torch.cuda.current_stream()
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        dev.forward()
+    torch.cuda.synchronize()
+    st = dev.stats()
+
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        dev.forward()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall / args.steps * 1e3
+
+    # Same steps again through the instrumented entry point: the library
+    # records six events per step on the launch stream.
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(_lib.N_PHASE_EVENTS)]
+              for _ in range(args.steps)]
+    for evs in events:
+        for ev in evs:
+            ev.record(stream)          # creates the underlying HIP event
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for evs in events:
+        _lib.layer_forward_profiled(cfg, dev.X, dev.valid, dev.W_router, dev.prototypes, dev.W_up,
+                                    dev.W_down, dev.Y, dev.ws_forward, evs, routing=dev.routing,
+                                    stream=stream)
+    torch.cuda.synchronize()
+    wall_prof = time.perf_counter() - t0
+    names = ["routing", "permute", "up_gemm", "down_gemm", "combine"]
+    phase_ms = {n: float(np.mean([evs[i].elapsed_time(evs[i + 1]) for evs in events]))
+                for i, n in enumerate(names)}
+
+    nv = st["n_valid"]
+    value = nv / (ms_per_step / 1e3)
+    act = st["activated_gemm_flops"]
+    gemm_ms = phase_ms["up_gemm"] + phase_ms["down_gemm"]
+    dom = "up_gemm" if phase_ms["up_gemm"] >= phase_ms["down_gemm"] else "down_gemm"
+    dom_flops = act / 2.0                       # each projection is half of 4 d M C_B
+    achieved = dom_flops / (phase_ms[dom] / 1e3)
+    pb = phase_bytes(cfg, st)
+    hbm = {n: pb[n] / (phase_ms[n] / 1e3) / PEAK_HBM_BYTES for n in pb}
+    hbm_all = sum(pb.values()) / ((phase_ms["routing"] + phase_ms["permute"] + phase_ms["combine"]) / 1e3)
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {cfg['n_tokens']} tokens x d={cfg['d_model']}, "
+                               f"K={cfg['n_experts']} residual + 1 shared expert, B={cfg['n_blocks']} "
+                               f"blocks of M={cfg['block_width']}, threshold {cfg['mass_threshold']}",
+                   "n_tokens": cfg["n_tokens"], "n_valid": nv, "d_model": cfg["d_model"],
+                   "n_experts": cfg["n_experts"], "n_blocks": cfg["n_blocks"],
+                   "block_width": cfg["block_width"], "mass_threshold": cfg["mass_threshold"]},
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved / 1e12, 2),
+                     "peak": PEAK_BF16_FLOPS / 1e12, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_FLOPS, 4), "traffic": None},
+        "mfma_util_activated": round(act / (gemm_ms / 1e3) / PEAK_BF16_FLOPS, 4),
+        "hbm_frac": {n: round(v, 4) for n, v in hbm.items()},
+        "hbm_frac_routing_permute_combine": round(hbm_all / PEAK_HBM_BYTES, 4),
+        "phases_ms": {n: round(v, 4) for n, v in phase_ms.items()},
+        "profiled_ms_per_step": round(wall_prof / args.steps * 1e3, 4),
+        "routing_stats": {"mean_b": round(st["mean_b"], 3), "mean_k": round(st["mean_k"], 3),
+                          "mean_cb": round(st["mean_cb"], 3),
+                          "activated_gemm_tflop": round(act / 1e12, 4)},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(g, args.cpu_sample, args.cpu_repeats)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,219 @@
+/*
+ * unif_moe.h - C ABI of the MI355X (gfx950) library for the forward pass of
+ * one UniF-MoE feed-forward layer ("Share First, Route What Remains",
+ * Sec. III).
+ *
+ * The layer holds one shared expert E_shr and K residual experts E_1..E_K,
+ * all upcycled from one FFN of width H and split into B aligned blocks of
+ * M = H / B channels (Sec. III-A). For each token x (a row of X):
+ *   alpha = tau + (1 - 2 tau) sigmoid(x W_shr), tau = (B-1)/B^2   (Eq. alpha)
+ *   b     = round(B alpha)                                         (Eq. block-count)
+ *   I_shr = the b blocks with the largest x mu_c                   (Eq. block-priority,
+ *           I_res = the other blocks                                shared-indices,
+ *                                                                   residual-indices)
+ *   s     = softmax(x W_g) over the K residual experts            (Eq. residual-router-score)
+ *   q, p  = experts by decreasing s and their affinities           (Eq. sorted-affinity)
+ *   k     = smallest n with p_1 + .. + p_n >= 1 - alpha            (Eq. beta, expert-count)
+ *   y     = alpha sum_{c in I_shr} E_shr^(c)(x)
+ *           + sum_{i <= k} p_i sum_{c in I_res} E_{q_i}^(c)(x)     (Eq. output)
+ * with E_j^(c)(x) = sum_{h in block c} GELU(x K_j[:,h]) V_j[h,:]   (Eq. block-expert-output),
+ * GELU in its exact erf form and no biases.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every tensor pointer is a DEVICE pointer owned by the caller. The
+ *   library allocates and frees nothing and keeps no state between calls.
+ * - Calls are asynchronous on `stream` (a hipStream_t; NULL is the null
+ *   stream), except unif_moe_stats, which synchronises it.
+ * - Arguments are validated on the host before any HIP call; a rejected
+ *   call launches nothing and leaves every buffer untouched.
+ * - Scratch memory comes from a caller-provided `workspace` of at least the
+ *   size reported by the matching *_workspace_size function (any alignment;
+ *   the library aligns its regions to 256 bytes inside it). Calls that share
+ *   a workspace must be ordered on one stream.
+ * - Row-major layouts. bf16 data is IEEE binary32 with the low 16 bits
+ *   dropped (bfloat16), passed as 16-bit words; conversions to bf16 round
+ *   to nearest even. The router and the block prototypes are always fp32.
+ * - Inputs must be finite (documented, not checked).
+ * - Padded tokens (valid[t] == 0) are skipped: their routing record is
+ *   alpha = 0, b = k = 0, mask = 0, expert ids -1, weights 0, their output
+ *   row is zero, and they count nowhere in the statistics.
+ */
+#ifndef UNIF_MOE_H
+#define UNIF_MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes (every entry point returns one as int32_t). */
+#define UNIF_OK            0   /* success                                        */
+#define UNIF_EINVAL       (-1) /* invalid argument: NULL pointer, bad size/mode  */
+#define UNIF_EWORKSPACE   (-2) /* workspace smaller than the reported size       */
+#define UNIF_EDEVICE      (-3) /* a HIP launch or runtime call failed            */
+#define UNIF_EUNSUPPORTED (-4) /* valid layer this build does not implement     */
+
+/* Element type of X, W_up, W_down and Y. */
+#define UNIF_F32  0
+#define UNIF_BF16 1
+
+/* alpha_mode: ADAPTIVE is Eq. alpha; FIXED uses alpha_fixed for every token
+ * (the fixed-alpha ablation, Table mechanism-ablation). */
+#define UNIF_ALPHA_ADAPTIVE 0
+#define UNIF_ALPHA_FIXED    1
+
+/* mass_mode: the target that the prefix sums P_n of Eq. expert-count must
+ * reach. COUPLED: min(1 - alpha, mass_threshold); with mass_threshold = 1
+ * this is Eq. beta / expert-count exactly. FIXED: mass_threshold for every
+ * token. TOPK: k = fixed_k (the top-k residual-activation ablation). */
+#define UNIF_MASS_COUPLED 0
+#define UNIF_MASS_FIXED   1
+#define UNIF_MASS_TOPK    2
+
+/* select_mode: PROTOTYPE is Eq. shared-indices (the b blocks of largest
+ * x mu_c, ties to the lower block index); PREFIX takes blocks 0..b-1 (the
+ * prefix-selection ablation). */
+#define UNIF_SELECT_PROTOTYPE 0
+#define UNIF_SELECT_PREFIX    1
+
+/* Layer description (Sec. III). */
+typedef struct unif_moe_config {
+    int32_t n_tokens;       /* N >= 0, rows of X                                   */
+    int32_t d_model;        /* d > 0                                               */
+    int32_t n_experts;      /* K in [1, 64] residual experts; the shared expert is
+                               stored in addition, as expert 0                     */
+    int32_t n_blocks;       /* B in [1, 64] (>= 2 in ADAPTIVE mode, Sec. III-B)    */
+    int32_t block_width;    /* M = H / B channels per block                        */
+    int32_t dtype;          /* UNIF_F32 or UNIF_BF16                               */
+    float   tau;            /* tau of Eq. alpha; NaN selects (B-1)/B^2. Must lie
+                               in [0, 1/2). 1 - 2 tau is evaluated in fp32.        */
+    float   mass_threshold; /* t in (0, 1], see mass_mode                          */
+    int32_t max_shared;     /* cap on b applied after Eq. block-count, in [0, B]   */
+    int32_t alpha_mode;     /* UNIF_ALPHA_*                                        */
+    float   alpha_fixed;    /* alpha in [0, 1] when alpha_mode == FIXED            */
+    int32_t mass_mode;      /* UNIF_MASS_*                                         */
+    int32_t fixed_k;        /* k in [1, K] when mass_mode == TOPK                  */
+    int32_t select_mode;    /* UNIF_SELECT_*                                       */
+} unif_moe_config;
+
+/* Per-token routing record, device arrays written by the library. Residual
+ * experts are numbered 1..K as E_1..E_K in the paper; index 0 of the expert
+ * weights is the shared expert.
+ *   alpha[N]          shared demand alpha (Eq. alpha), fp32
+ *   n_shared[N]       b, shared block count after clamp and cap (Eq. block-count)
+ *   shared_mask[N]    bit c set <=> block c in I_shr (Eq. shared-indices)
+ *   n_res[N]          k, residual expert count (Eq. expert-count)
+ *   expert_ids[N*K]   q_1..q_K, all K experts by decreasing affinity (ties to
+ *                     the lower index) (Eq. sorted-affinity)
+ *   weights[N*K]      p_1..p_K, their softmax affinities (fp32)            */
+typedef struct unif_moe_routing {
+    float*    alpha;
+    int32_t*  n_shared;
+    uint64_t* shared_mask;
+    int32_t*  n_res;
+    int32_t*  expert_ids;
+    float*    weights;
+} unif_moe_routing;
+
+/* Counts over valid tokens (host structure filled by unif_moe_stats). */
+typedef struct unif_moe_stats_t {
+    int64_t n_valid;
+    int64_t hist_b[65];           /* tokens with b = i                             */
+    int64_t hist_k[65];           /* tokens with k = i                             */
+    int64_t expert_tokens[65];    /* [0]: tokens on the shared expert (all valid);
+                                     [j]: tokens routed to residual expert j       */
+    int64_t activated_blocks;     /* sum of C_B = b + k (B - b) (Eq. block-compute) */
+    double  mean_b, mean_k, mean_cb;
+    double  activated_gemm_flops; /* 4 d M sum C_B: up- and down-projection FLOPs  */
+    double  routing_flops;        /* 2 d (1 + K + B) per valid token               */
+} unif_moe_stats_t;
+
+/* Workspace needed by unif_moe_route for this configuration (bytes, may be
+ * 0). Host only; no HIP call. Returns UNIF_OK, UNIF_EINVAL or
+ * UNIF_EUNSUPPORTED exactly as unif_moe_route would. */
+int32_t unif_moe_route_workspace_size(const unif_moe_config* cfg, size_t* bytes);
+
+/* Routing of Sec. III-B and III-C for every token (no expert evaluation).
+ *   X          [N, d] fp32 or bf16 (cfg->dtype)
+ *   valid      [N] uint8, nonzero = real token; NULL means all valid
+ *   W_router   [K+1, d] fp32: row 0 is W_shr, row j is W_j (the columns of
+ *              the augmented router W_g* of Eq. augmented-router)
+ *   prototypes [B, d] fp32: row c is the block prototype mu_c
+ *              (Eq. block-prototype; weight-only, so precomputed by the caller)
+ *   out        record arrays (all six required)
+ * Errors: UNIF_EINVAL, UNIF_EWORKSPACE, UNIF_EUNSUPPORTED before any launch;
+ * UNIF_EDEVICE if a launch fails. */
+int32_t unif_moe_route(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
+                       const float* W_router, const float* prototypes,
+                       const unif_moe_routing* out, void* workspace, size_t workspace_bytes,
+                       void* stream);
+
+/* Workspace needed by unif_moe_layer_forward (bytes). Host only. The size
+ * covers the worst case (every token routed to all K residual experts), so
+ * the forward never reads counts back to the host. */
+int32_t unif_moe_layer_forward_workspace_size(const unif_moe_config* cfg, size_t* bytes);
+
+/* Forward pass of the layer: routing, token permutation, block-sparse expert
+ * FFNs and the weighted merge of Eq. output.
+ *   X, valid, W_router, prototypes   as for unif_moe_route
+ *   W_up   [K+1, H, d] (cfg->dtype): expert e's row h is the key K_e[:, h]
+ *          (the [out, in] weight of the FFN's first linear layer);
+ *          expert 0 is the shared expert
+ *   W_down [K+1, d, H] (cfg->dtype): expert e's row j holds V_e[:, j], i.e.
+ *          V_e stored column-major (the [out, in] weight of the second
+ *          linear layer)
+ *   Y      [N, d] (cfg->dtype), written for every row (zero for padded rows)
+ *   routing_out  optional record (NULL: kept inside the workspace)
+ * Accumulation is fp32. In the bf16 path the GELU activations and the
+ * per-expert outputs are rounded to bf16 before the next contraction and the
+ * merge; the merge sums in a fixed order (shared expert, then q_1..q_k), so
+ * repeated calls give bitwise-identical Y.
+ * Requires, for bf16: d % 128 == 0, M % 64 == 0, M <= 256; for fp32:
+ * H = B M <= 16384. Otherwise UNIF_EUNSUPPORTED. */
+int32_t unif_moe_layer_forward(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
+                               const float* W_router, const float* prototypes,
+                               const void* W_up, const void* W_down, void* Y,
+                               const unif_moe_routing* routing_out,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Instrumented unif_moe_layer_forward for measurement: identical work and
+ * result, and additionally records the caller's events (hipEvent_t handles,
+ * created by the caller, recorded on `stream`) at the phase boundaries:
+ *   events[0] before the first launch      events[3] after the up-projection
+ *   events[1] after routing (split, route) events[4] after the down-projection
+ *   events[2] after the permutation        events[5] after the weighted merge
+ * (zero-fill, scan, scatter, slab lists)
+ * n_events must be 6. In the fp32 path events[3] and events[4] both follow
+ * the per-pair FFN. Errors as unif_moe_layer_forward; UNIF_EINVAL for a NULL
+ * event array or n_events != 6. */
+int32_t unif_moe_layer_forward_profiled(const unif_moe_config* cfg, const void* X,
+                                        const uint8_t* valid, const float* W_router,
+                                        const float* prototypes, const void* W_up,
+                                        const void* W_down, void* Y,
+                                        const unif_moe_routing* routing_out, void* workspace,
+                                        size_t workspace_bytes, void* const* events,
+                                        int32_t n_events, void* stream);
+
+/* Workspace needed by unif_moe_stats (bytes). Host only. */
+int32_t unif_moe_stats_workspace_size(const unif_moe_config* cfg, size_t* bytes);
+
+/* Counts of Sec. III-E over a routing record produced by unif_moe_route or
+ * unif_moe_layer_forward for the same cfg and valid mask: histograms of b
+ * and k, tokens per expert, C_B = b + k (B - b) (Eq. block-compute) and the
+ * activated expert-GEMM FLOPs 4 d M C_B. Reduces on the device, copies the
+ * counts to *host_out and synchronises `stream`. */
+int32_t unif_moe_stats(const unif_moe_config* cfg, const unif_moe_routing* routing,
+                       const uint8_t* valid, unif_moe_stats_t* host_out,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static text for a status code ("unknown status" for other values). */
+const char* unif_moe_status_string(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UNIF_MOE_H */

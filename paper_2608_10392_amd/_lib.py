@@ -1,0 +1,221 @@
+"""ctypes binding of libunifmoe.so (include/unif_moe.h).
+
+Argument marshalling only: every step of the layer runs in the HIP library.
+Tensors are torch device tensors (torch provides device memory and streams);
+the library never falls back to anything else, and loading fails loudly when
+the built library is missing.
+"""
+import ctypes
+import math
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libunifmoe.so")
+
+OK, EINVAL, EWORKSPACE, EDEVICE, EUNSUPPORTED = 0, -1, -2, -3, -4
+DTYPES = {"f32": 0, "bf16": 1}
+ALPHA_MODES = {"adaptive": 0, "fixed": 1}
+MASS_MODES = {"coupled": 0, "fixed": 1, "topk": 2}
+SELECT_MODES = {"prototype": 0, "prefix": 1}
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("n_tokens", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("n_experts", ctypes.c_int32), ("n_blocks", ctypes.c_int32),
+                ("block_width", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("tau", ctypes.c_float), ("mass_threshold", ctypes.c_float),
+                ("max_shared", ctypes.c_int32), ("alpha_mode", ctypes.c_int32),
+                ("alpha_fixed", ctypes.c_float), ("mass_mode", ctypes.c_int32),
+                ("fixed_k", ctypes.c_int32), ("select_mode", ctypes.c_int32)]
+
+
+class Routing(ctypes.Structure):
+    _fields_ = [("alpha", ctypes.c_void_p), ("n_shared", ctypes.c_void_p),
+                ("shared_mask", ctypes.c_void_p), ("n_res", ctypes.c_void_p),
+                ("expert_ids", ctypes.c_void_p), ("weights", ctypes.c_void_p)]
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("n_valid", ctypes.c_int64), ("hist_b", ctypes.c_int64 * 65),
+                ("hist_k", ctypes.c_int64 * 65), ("expert_tokens", ctypes.c_int64 * 65),
+                ("activated_blocks", ctypes.c_int64), ("mean_b", ctypes.c_double),
+                ("mean_k", ctypes.c_double), ("mean_cb", ctypes.c_double),
+                ("activated_gemm_flops", ctypes.c_double), ("routing_flops", ctypes.c_double)]
+
+
+EXPORTS = ("unif_moe_route_workspace_size", "unif_moe_route",
+           "unif_moe_layer_forward_workspace_size", "unif_moe_layer_forward",
+           "unif_moe_layer_forward_profiled", "unif_moe_stats_workspace_size",
+           "unif_moe_stats", "unif_moe_status_string")
+N_PHASE_EVENTS = 6
+
+
+class UnifMoeError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+
+
+_LIB = None
+
+
+def lib():
+    """The loaded HIP library (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing; build it with "
+                              "`python -m paper_2608_10392_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, sz = ctypes.c_void_p, ctypes.c_size_t
+        cfgp = ctypes.POINTER(Config)
+        L.unif_moe_route_workspace_size.argtypes = [cfgp, ctypes.POINTER(sz)]
+        L.unif_moe_layer_forward_workspace_size.argtypes = [cfgp, ctypes.POINTER(sz)]
+        L.unif_moe_stats_workspace_size.argtypes = [cfgp, ctypes.POINTER(sz)]
+        L.unif_moe_route.argtypes = [cfgp, vp, vp, vp, vp, ctypes.POINTER(Routing), vp, sz, vp]
+        L.unif_moe_layer_forward.argtypes = [cfgp, vp, vp, vp, vp, vp, vp, vp,
+                                             ctypes.POINTER(Routing), vp, sz, vp]
+        L.unif_moe_layer_forward_profiled.argtypes = [cfgp, vp, vp, vp, vp, vp, vp, vp,
+                                                      ctypes.POINTER(Routing), vp, sz,
+                                                      ctypes.POINTER(vp), ctypes.c_int32, vp]
+        L.unif_moe_stats.argtypes = [cfgp, ctypes.POINTER(Routing), vp, ctypes.POINTER(Stats),
+                                     vp, sz, vp]
+        L.unif_moe_status_string.argtypes = [ctypes.c_int32]
+        L.unif_moe_status_string.restype = ctypes.c_char_p
+        for name in EXPORTS[:-1]:
+            getattr(L, name).restype = ctypes.c_int32
+        _LIB = L
+    return _LIB
+
+
+def status_string(status):
+    return lib().unif_moe_status_string(int(status)).decode()
+
+
+def make_config(cfg):
+    """Config structure from a layer description dict (the keys of
+    synth.configs.LAYER_KEYS; modes and dtype as strings)."""
+    tau = cfg.get("tau")
+    return Config(
+        n_tokens=int(cfg["n_tokens"]), d_model=int(cfg["d_model"]),
+        n_experts=int(cfg["n_experts"]), n_blocks=int(cfg["n_blocks"]),
+        block_width=int(cfg["block_width"]), dtype=DTYPES[cfg["dtype"]],
+        tau=math.nan if tau is None else float(tau),
+        mass_threshold=float(cfg["mass_threshold"]),
+        max_shared=int(cfg["n_blocks"] if cfg.get("max_shared") is None else cfg["max_shared"]),
+        alpha_mode=ALPHA_MODES[cfg.get("alpha_mode", "adaptive")],
+        alpha_fixed=float(cfg.get("alpha_fixed", 0.0)),
+        mass_mode=MASS_MODES[cfg.get("mass_mode", "coupled")],
+        fixed_k=int(cfg.get("fixed_k", 1)),
+        select_mode=SELECT_MODES[cfg.get("select_mode", "prototype")])
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+def _check(status, where):
+    if status != OK:
+        raise UnifMoeError(status, where)
+
+
+def _size(fn, cfg):
+    c = make_config(cfg) if isinstance(cfg, dict) else cfg
+    n = ctypes.c_size_t(0)
+    _check(getattr(lib(), fn)(ctypes.byref(c), ctypes.byref(n)), fn)
+    return n.value
+
+
+def route_workspace_size(cfg):
+    return _size("unif_moe_route_workspace_size", cfg)
+
+
+def layer_forward_workspace_size(cfg):
+    return _size("unif_moe_layer_forward_workspace_size", cfg)
+
+
+def stats_workspace_size(cfg):
+    return _size("unif_moe_stats_workspace_size", cfg)
+
+
+def _routing_struct(rec):
+    if rec is None:
+        return None
+    return Routing(*(_ptr(rec[k]) for k in ("alpha", "n_shared", "shared_mask", "n_res",
+                                            "expert_ids", "weights")))
+
+
+def alloc_routing(n_tokens, n_experts, device="cuda"):
+    """Device arrays of a routing record (torch tensors)."""
+    import torch
+    N, K = int(n_tokens), int(n_experts)
+    return dict(alpha=torch.empty(N, dtype=torch.float32, device=device),
+                n_shared=torch.empty(N, dtype=torch.int32, device=device),
+                shared_mask=torch.empty(N, dtype=torch.int64, device=device),
+                n_res=torch.empty(N, dtype=torch.int32, device=device),
+                expert_ids=torch.empty((N, K), dtype=torch.int32, device=device),
+                weights=torch.empty((N, K), dtype=torch.float32, device=device))
+
+
+def alloc_workspace(nbytes, device="cuda"):
+    import torch
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def route(cfg, X, valid, W_router, prototypes, out, workspace, stream=None):
+    c = make_config(cfg)
+    r = _routing_struct(out)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().unif_moe_route(ctypes.byref(c), _ptr(X), _ptr(valid), _ptr(W_router),
+                                _ptr(prototypes), ctypes.byref(r), _ptr(workspace), ws_bytes,
+                                _stream(stream)), "unif_moe_route")
+
+
+def layer_forward(cfg, X, valid, W_router, prototypes, W_up, W_down, Y, workspace,
+                  routing=None, stream=None):
+    c = make_config(cfg)
+    r = _routing_struct(routing)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().unif_moe_layer_forward(ctypes.byref(c), _ptr(X), _ptr(valid), _ptr(W_router),
+                                        _ptr(prototypes), _ptr(W_up), _ptr(W_down), _ptr(Y),
+                                        ctypes.byref(r) if r is not None else None,
+                                        _ptr(workspace), ws_bytes, _stream(stream)),
+           "unif_moe_layer_forward")
+
+
+def layer_forward_profiled(cfg, X, valid, W_router, prototypes, W_up, W_down, Y, workspace,
+                           events, routing=None, stream=None):
+    """As layer_forward, recording the six torch.cuda.Event objects in
+    ``events`` at the phase boundaries (see the C header)."""
+    c = make_config(cfg)
+    r = _routing_struct(routing)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    handles = (ctypes.c_void_p * N_PHASE_EVENTS)(*(ev.cuda_event for ev in events))
+    _check(lib().unif_moe_layer_forward_profiled(
+        ctypes.byref(c), _ptr(X), _ptr(valid), _ptr(W_router), _ptr(prototypes), _ptr(W_up),
+        _ptr(W_down), _ptr(Y), ctypes.byref(r) if r is not None else None, _ptr(workspace),
+        ws_bytes, handles, N_PHASE_EVENTS, _stream(stream)), "unif_moe_layer_forward_profiled")
+
+
+def stats(cfg, routing, valid, workspace, stream=None):
+    c = make_config(cfg)
+    r = _routing_struct(routing)
+    s = Stats()
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().unif_moe_stats(ctypes.byref(c), ctypes.byref(r), _ptr(valid), ctypes.byref(s),
+                                _ptr(workspace), ws_bytes, _stream(stream)), "unif_moe_stats")
+    return dict(n_valid=s.n_valid, hist_b=list(s.hist_b), hist_k=list(s.hist_k),
+                expert_tokens=list(s.expert_tokens), activated_blocks=s.activated_blocks,
+                mean_b=s.mean_b, mean_k=s.mean_k, mean_cb=s.mean_cb,
+                activated_gemm_flops=s.activated_gemm_flops, routing_flops=s.routing_flops)

@@ -1,0 +1,61 @@
+// Weighted merge of Eq. output: y = alpha E_shr^S + sum_{i <= k} p_i E_{q_i}^R.
+// Each token reads its k + 1 per-expert rows (pair_of) and sums them in a
+// fixed order (shared expert first, then q_1..q_k) in fp32, so the result
+// does not depend on how pairs were scheduled. Padded rows get zeros.
+#pragma once
+#include "common.hpp"
+
+namespace unifmoe {
+
+struct CombineParams {
+    int N, d, K;
+    const void* part;
+    const int* pair_of;
+    const float* alpha;
+    const int* nres;
+    const float* wts;
+    void* Y;
+};
+
+// bf16: one thread per 8 consecutive outputs (16-byte loads and stores).
+__global__ void combine_bf16_kernel(CombineParams c) {
+    const int chunks = c.d >> 3;
+    const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (item >= (size_t)c.N * chunks) return;
+    const int t = (int)(item / chunks), ch = (int)(item - (size_t)t * chunks);
+    const int k = c.nres[t];
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    const u16* part = static_cast<const u16*>(c.part);
+    for (int i = 0; i <= k && k > 0; ++i) {
+        const float w = (i == 0) ? c.alpha[t] : c.wts[(size_t)t * c.K + i - 1];
+        const int pr = c.pair_of[(size_t)t * (c.K + 1) + i];
+        const u32x4 v = ld16(part + (size_t)pr * c.d + ch * 8);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            acc[2 * q] = fmaf(w, __uint_as_float(v[q] << 16), acc[2 * q]);
+            acc[2 * q + 1] = fmaf(w, __uint_as_float(v[q] & 0xffff0000u), acc[2 * q + 1]);
+        }
+    }
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = (uint32_t)f2bf(acc[2 * q]) | ((uint32_t)f2bf(acc[2 * q + 1]) << 16);
+    st16(static_cast<u16*>(c.Y) + (size_t)t * c.d + ch * 8, o);
+}
+
+// fp32: one thread per output element.
+__global__ void combine_f32_kernel(CombineParams c) {
+    const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (item >= (size_t)c.N * c.d) return;
+    const int t = (int)(item / c.d), j = (int)(item - (size_t)t * c.d);
+    const int k = c.nres[t];
+    const float* part = static_cast<const float*>(c.part);
+    float acc = 0.f;
+    for (int i = 0; i <= k && k > 0; ++i) {
+        const float w = (i == 0) ? c.alpha[t] : c.wts[(size_t)t * c.K + i - 1];
+        const int pr = c.pair_of[(size_t)t * (c.K + 1) + i];
+        acc = fmaf(w, part[(size_t)pr * c.d + j], acc);
+    }
+    static_cast<float*>(c.Y)[item] = acc;
+}
+
+}  // namespace unifmoe

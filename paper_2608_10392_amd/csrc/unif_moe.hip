@@ -1,0 +1,597 @@
+// Host side of the UniF-MoE layer library: argument validation, workspace
+// planning and the launch sequence of the forward pass. See include/unif_moe.h
+// for the contract of every entry point.
+//
+// Forward launch sequence (all asynchronous on the caller's stream, no
+// device-to-host traffic):
+//   fill_zero        pair / slab counters
+//   split_router     fp32 router + prototypes -> 3 bf16 parts (bf16 only)
+//   route            routing record + pair and slab counts
+//   scan             LDS prefix sums -> offsets and tile tables
+//   scatter          pair slots (expert segments sorted by block-mask key)
+//   slabfill         per-(expert, block) pair lists               (bf16)
+//   up, down         block-sparse MFMA grouped GEMMs              (bf16)
+//   pair_ffn_f32     per-pair fp32 FFN                            (fp32)
+//   combine          weighted merge in fixed order
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "../../include/unif_moe.h"
+#include "combine.hpp"
+#include "common.hpp"
+#include "ffn_bf16.hpp"
+#include "ffn_f32.hpp"
+#include "permute.hpp"
+#include "route.hpp"
+#include "stats.hpp"
+
+using namespace unifmoe;
+
+namespace {
+
+constexpr int kKeyBitsMax = 10;
+constexpr size_t kLdsLimit = 160 * 1024;
+
+struct Dims {
+    int N, d, K, B, M, H, K1, NL, NLP, lstride, key_bits, nslab, nbin;
+    bool bf16;
+    size_t elem;
+    float tau, one_minus_2tau;
+};
+
+Dims dims_of(const unif_moe_config* c) {
+    Dims m;
+    m.N = c->n_tokens;
+    m.d = c->d_model;
+    m.K = c->n_experts;
+    m.B = c->n_blocks;
+    m.M = c->block_width;
+    m.H = m.B * m.M;
+    m.K1 = m.K + 1;
+    m.NL = 1 + m.K + m.B;
+    m.NLP = ceil_div(m.NL, 16) * 16;
+    m.lstride = m.NLP + 1;
+    m.key_bits = m.B < kKeyBitsMax ? m.B : kKeyBitsMax;
+    m.nslab = m.K1 * m.B;
+    m.nbin = m.K1 << m.key_bits;
+    m.bf16 = c->dtype == UNIF_BF16;
+    m.elem = m.bf16 ? 2 : 4;
+    m.tau = std::isnan(c->tau) ? (float)((double)(m.B - 1) / ((double)m.B * (double)m.B)) : c->tau;
+    m.one_minus_2tau = 1.0f - 2.0f * m.tau;
+    return m;
+}
+
+size_t route_lds_bytes(const Dims& m) {
+    return sizeof(float) * ((size_t)kRouteTok * m.lstride + (size_t)kRouteTok * (m.K + 1) * 2 +
+                            (size_t)m.K1 * m.B);
+}
+
+// Checks shared by every entry point (host only, no HIP call).
+int32_t check_config(const unif_moe_config* c) {
+    if (c == nullptr) return UNIF_EINVAL;
+    if (c->n_tokens < 0 || c->d_model <= 0 || c->n_experts < 1 || c->n_blocks < 1 || c->block_width < 1)
+        return UNIF_EINVAL;
+    if (c->dtype != UNIF_F32 && c->dtype != UNIF_BF16) return UNIF_EINVAL;
+    if (c->alpha_mode != UNIF_ALPHA_ADAPTIVE && c->alpha_mode != UNIF_ALPHA_FIXED) return UNIF_EINVAL;
+    if (c->mass_mode != UNIF_MASS_COUPLED && c->mass_mode != UNIF_MASS_FIXED && c->mass_mode != UNIF_MASS_TOPK)
+        return UNIF_EINVAL;
+    if (c->select_mode != UNIF_SELECT_PROTOTYPE && c->select_mode != UNIF_SELECT_PREFIX) return UNIF_EINVAL;
+    if (!(c->mass_threshold > 0.0f && c->mass_threshold <= 1.0f)) return UNIF_EINVAL;
+    if (c->max_shared < 0 || c->max_shared > c->n_blocks) return UNIF_EINVAL;
+    if (c->alpha_mode == UNIF_ALPHA_ADAPTIVE && c->n_blocks < 2) return UNIF_EINVAL;
+    if (c->alpha_mode == UNIF_ALPHA_FIXED && !(c->alpha_fixed >= 0.0f && c->alpha_fixed <= 1.0f))
+        return UNIF_EINVAL;
+    if (c->mass_mode == UNIF_MASS_TOPK && (c->fixed_k < 1 || c->fixed_k > c->n_experts)) return UNIF_EINVAL;
+    if (!std::isnan(c->tau) && !(c->tau >= 0.0f && c->tau < 0.5f)) return UNIF_EINVAL;
+    if (c->n_blocks > 64 || c->n_experts > 64) return UNIF_EUNSUPPORTED;
+    const int64_t N = c->n_tokens, K = c->n_experts, B = c->n_blocks;
+    if (N * (K + 1) > INT32_MAX || N * K * B > INT32_MAX) return UNIF_EUNSUPPORTED;
+    const Dims m = dims_of(c);
+    if (route_lds_bytes(m) > kLdsLimit) return UNIF_EUNSUPPORTED;
+    if (m.bf16 && (m.d % 32) != 0) return UNIF_EUNSUPPORTED;
+    return UNIF_OK;
+}
+
+int32_t check_forward_shape(const unif_moe_config* c) {
+    const Dims m = dims_of(c);
+    if (m.bf16) {
+        if (m.d % kBN != 0 || m.M % kBK != 0 || m.M > 256) return UNIF_EUNSUPPORTED;
+        if ((int64_t)m.H * m.d * 2 > ((int64_t)1 << 40)) return UNIF_EUNSUPPORTED;
+    } else {
+        if ((int64_t)m.H > 16384) return UNIF_EUNSUPPORTED;
+    }
+    return UNIF_OK;
+}
+
+// Workspace carving: regions aligned to 256 bytes.
+struct Carver {
+    size_t cur = 0;
+    size_t take(size_t bytes) {
+        cur = (cur + 255) & ~(size_t)255;
+        const size_t o = cur;
+        cur += bytes;
+        return o;
+    }
+};
+
+struct RoutePlan {
+    size_t wsplit, total;
+};
+
+RoutePlan plan_route(const Dims& m) {
+    Carver cv;
+    RoutePlan p;
+    p.wsplit = cv.take(m.bf16 ? (size_t)3 * m.NLP * m.d * sizeof(u16) : 0);
+    p.total = cv.cur;
+    return p;
+}
+
+struct FwdPlan {
+    size_t alpha, nsh, mask, nres, eids, wts;
+    size_t wsplit;
+    size_t zero_begin, zero_end;  // bin_count, slab_count, totals
+    size_t bin_count, slab_count, totals;
+    size_t bin_cursor, slab_off, slab_cursor, seg_off, up_tile_off, down_tile_off;
+    size_t pair_token, pair_mask, pair_expert, pair_of, slab_rows, hbuf, part;
+    size_t total;
+};
+
+FwdPlan plan_forward(const Dims& m, bool own_record) {
+    Carver cv;
+    FwdPlan p;
+    const size_t N = (size_t)m.N, K = (size_t)m.K, K1 = (size_t)m.K1;
+    const size_t pmax = N * K1;
+    p.alpha = cv.take(own_record ? 4 * N : 0);
+    p.nsh = cv.take(own_record ? 4 * N : 0);
+    p.mask = cv.take(own_record ? 8 * N : 0);
+    p.nres = cv.take(own_record ? 4 * N : 0);
+    p.eids = cv.take(own_record ? 4 * N * K : 0);
+    p.wts = cv.take(own_record ? 4 * N * K : 0);
+    p.wsplit = cv.take(m.bf16 ? (size_t)3 * m.NLP * m.d * sizeof(u16) : 0);
+    p.bin_count = cv.take(4 * (size_t)m.nbin);
+    p.zero_begin = p.bin_count;
+    p.slab_count = cv.take(4 * (size_t)m.nslab);
+    p.totals = cv.take(4 * 4);
+    p.zero_end = cv.cur;
+    p.bin_cursor = cv.take(4 * (size_t)m.nbin);
+    p.slab_off = cv.take(4 * ((size_t)m.nslab + 1));
+    p.slab_cursor = cv.take(4 * (size_t)m.nslab);
+    p.seg_off = cv.take(4 * (K1 + 1));
+    p.up_tile_off = cv.take(4 * ((size_t)m.nslab + 1));
+    p.down_tile_off = cv.take(4 * (K1 + 1));
+    p.pair_token = cv.take(4 * pmax);
+    p.pair_mask = cv.take(8 * pmax);
+    p.pair_expert = cv.take(4 * pmax);
+    p.pair_of = cv.take(4 * N * K1);
+    p.slab_rows = cv.take(m.bf16 ? 4 * N * K * (size_t)m.B : 0);
+    p.hbuf = cv.take(m.bf16 ? pmax * (size_t)m.H * 2 : 0);
+    p.part = cv.take(pmax * (size_t)m.d * m.elem);
+    p.total = cv.cur + 256;  // slack for aligning an unaligned base pointer
+    return p;
+}
+
+char* align_base(void* ws) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(ws);
+    return reinterpret_cast<char*>((a + 255) & ~(uintptr_t)255);
+}
+
+int g_cu_count[64];
+
+int cu_count() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (g_cu_count[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        g_cu_count[dev] = n;
+    }
+    return g_cu_count[dev];
+}
+
+#define UNIF_LAUNCH_CHECK()                              \
+    do {                                                 \
+        if (hipGetLastError() != hipSuccess) return UNIF_EDEVICE; \
+    } while (0)
+
+template <class F>
+int32_t allow_lds(F* kernel, size_t bytes) {
+    if (bytes <= 64 * 1024) return UNIF_OK;
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)bytes) != hipSuccess)
+        return UNIF_EDEVICE;
+    return UNIF_OK;
+}
+
+RouteParams route_params(const unif_moe_config* c, const Dims& m, const void* X, const uint8_t* valid,
+                         const float* Wr, const float* mu, const u16* wsplit, float* alpha, int* nsh,
+                         uint64_t* mask, int* nres, int* eids, float* wts) {
+    RouteParams r;
+    r.N = m.N;
+    r.d = m.d;
+    r.K = m.K;
+    r.B = m.B;
+    r.NL = m.NL;
+    r.NLP = m.NLP;
+    r.lstride = m.lstride;
+    r.key_bits = m.key_bits;
+    r.tau = m.tau;
+    r.one_minus_2tau = m.one_minus_2tau;
+    r.t_mass = c->mass_threshold;
+    r.alpha_fixed = c->alpha_fixed;
+    r.max_shared = c->max_shared;
+    r.alpha_mode = c->alpha_mode;
+    r.mass_mode = c->mass_mode;
+    r.fixed_k = c->fixed_k;
+    r.select_mode = c->select_mode;
+    r.X = X;
+    r.valid = valid;
+    r.Wr = Wr;
+    r.mu = mu;
+    r.Wsplit = wsplit;
+    r.alpha = alpha;
+    r.nsh = nsh;
+    r.mask = mask;
+    r.nres = nres;
+    r.eids = eids;
+    r.wts = wts;
+    r.bin_count = nullptr;
+    r.slab_count = nullptr;
+    return r;
+}
+
+// Router logits and decisions (shared by unif_moe_route and the forward).
+int32_t launch_route(const Dims& m, const RouteParams& rp, const float* Wr, const float* mu, u16* wsplit,
+                     hipStream_t st) {
+    if (m.N == 0) return UNIF_OK;
+    if (m.bf16) {
+        const int total = m.NLP * m.d;
+        split_router_kernel<<<ceil_div(total, 256), 256, 0, st>>>(Wr, mu, m.K, m.B, m.d, m.NLP, wsplit);
+        UNIF_LAUNCH_CHECK();
+    }
+    const size_t lds = route_lds_bytes(m);
+    const int grid = ceil_div(m.N, kRouteTok);
+    if (m.bf16) {
+        if (allow_lds(route_kernel<true>, lds) != UNIF_OK) return UNIF_EDEVICE;
+        route_kernel<true><<<grid, kRouteThreads, lds, st>>>(rp);
+    } else {
+        if (allow_lds(route_kernel<false>, lds) != UNIF_OK) return UNIF_EDEVICE;
+        route_kernel<false><<<grid, kRouteThreads, lds, st>>>(rp);
+    }
+    UNIF_LAUNCH_CHECK();
+    return UNIF_OK;
+}
+
+bool record_complete(const unif_moe_routing* r) {
+    return r && r->alpha && r->n_shared && r->shared_mask && r->n_res && r->expert_ids && r->weights;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* unif_moe_status_string(int32_t s) {
+    switch (s) {
+        case UNIF_OK: return "ok";
+        case UNIF_EINVAL: return "invalid argument";
+        case UNIF_EWORKSPACE: return "workspace too small";
+        case UNIF_EDEVICE: return "HIP device error";
+        case UNIF_EUNSUPPORTED: return "unsupported layer shape";
+        default: return "unknown status";
+    }
+}
+
+int32_t unif_moe_route_workspace_size(const unif_moe_config* cfg, size_t* bytes) {
+    if (bytes == nullptr) return UNIF_EINVAL;
+    const int32_t s = check_config(cfg);
+    if (s != UNIF_OK) return s;
+    const RoutePlan p = plan_route(dims_of(cfg));
+    *bytes = p.total ? p.total + 256 : 0;
+    return UNIF_OK;
+}
+
+int32_t unif_moe_route(const unif_moe_config* cfg, const void* X, const uint8_t* valid, const float* W_router,
+                       const float* prototypes, const unif_moe_routing* out, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+    int32_t s = check_config(cfg);
+    if (s != UNIF_OK) return s;
+    if (!record_complete(out)) return UNIF_EINVAL;
+    if (cfg->n_tokens > 0 && (X == nullptr || W_router == nullptr || prototypes == nullptr)) return UNIF_EINVAL;
+    size_t need = 0;
+    unif_moe_route_workspace_size(cfg, &need);
+    if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return UNIF_EWORKSPACE;
+    const Dims m = dims_of(cfg);
+    const RoutePlan plan = plan_route(m);
+    char* ws = need ? align_base(workspace) : nullptr;
+    u16* wsplit = m.bf16 ? reinterpret_cast<u16*>(ws + plan.wsplit) : nullptr;
+    const RouteParams rp = route_params(cfg, m, X, valid, W_router, prototypes, wsplit, out->alpha,
+                                        out->n_shared, out->shared_mask, out->n_res, out->expert_ids,
+                                        out->weights);
+    return launch_route(m, rp, W_router, prototypes, wsplit, static_cast<hipStream_t>(stream));
+}
+
+int32_t unif_moe_layer_forward_workspace_size(const unif_moe_config* cfg, size_t* bytes) {
+    if (bytes == nullptr) return UNIF_EINVAL;
+    int32_t s = check_config(cfg);
+    if (s != UNIF_OK) return s;
+    s = check_forward_shape(cfg);
+    if (s != UNIF_OK) return s;
+    *bytes = plan_forward(dims_of(cfg), true).total;
+    return UNIF_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+int32_t record_event(void* const* events, int i, hipStream_t st) {
+    if (events == nullptr) return UNIF_OK;
+    return hipEventRecord(static_cast<hipEvent_t>(events[i]), st) == hipSuccess ? UNIF_OK : UNIF_EDEVICE;
+}
+
+#define UNIF_MARK(i)                                        \
+    do {                                                    \
+        if (record_event(events, (i), st) != UNIF_OK) return UNIF_EDEVICE; \
+    } while (0)
+
+int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
+                     const float* W_router, const float* prototypes, const void* W_up,
+                     const void* W_down, void* Y, const unif_moe_routing* routing_out,
+                     void* workspace, size_t workspace_bytes, void* const* events, void* stream) {
+    int32_t s = check_config(cfg);
+    if (s != UNIF_OK) return s;
+    s = check_forward_shape(cfg);
+    if (s != UNIF_OK) return s;
+    if (routing_out != nullptr && !record_complete(routing_out)) return UNIF_EINVAL;
+    if (cfg->n_tokens > 0 && (X == nullptr || W_router == nullptr || prototypes == nullptr ||
+                              W_up == nullptr || W_down == nullptr || Y == nullptr))
+        return UNIF_EINVAL;
+    const Dims m = dims_of(cfg);
+    const bool own = routing_out == nullptr;
+    const FwdPlan plan = plan_forward(m, own);
+    // The size reported by the query always includes the internal record.
+    size_t need = 0;
+    unif_moe_layer_forward_workspace_size(cfg, &need);
+    if (workspace == nullptr || workspace_bytes < need) return UNIF_EWORKSPACE;
+    if (m.N == 0) return UNIF_OK;
+
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    char* ws = align_base(workspace);
+    float* alpha = own ? reinterpret_cast<float*>(ws + plan.alpha) : routing_out->alpha;
+    int* nsh = own ? reinterpret_cast<int*>(ws + plan.nsh) : routing_out->n_shared;
+    uint64_t* mask = own ? reinterpret_cast<uint64_t*>(ws + plan.mask) : routing_out->shared_mask;
+    int* nres = own ? reinterpret_cast<int*>(ws + plan.nres) : routing_out->n_res;
+    int* eids = own ? reinterpret_cast<int*>(ws + plan.eids) : routing_out->expert_ids;
+    float* wts = own ? reinterpret_cast<float*>(ws + plan.wts) : routing_out->weights;
+    u16* wsplit = m.bf16 ? reinterpret_cast<u16*>(ws + plan.wsplit) : nullptr;
+    int* bin_count = reinterpret_cast<int*>(ws + plan.bin_count);
+    int* slab_count = reinterpret_cast<int*>(ws + plan.slab_count);
+    int* totals = reinterpret_cast<int*>(ws + plan.totals);
+
+    UNIF_MARK(0);
+    // 1. zero the counters
+    const size_t zwords = (plan.zero_end - plan.zero_begin) / 4;
+    fill_zero_kernel<<<ceil_div((int)zwords, 256), 256, 0, st>>>(reinterpret_cast<uint32_t*>(ws + plan.zero_begin),
+                                                                 zwords);
+    UNIF_LAUNCH_CHECK();
+
+    // 2. routing + counts
+    RouteParams rp = route_params(cfg, m, X, valid, W_router, prototypes, wsplit, alpha, nsh, mask, nres, eids,
+                                  wts);
+    rp.bin_count = bin_count;
+    rp.slab_count = slab_count;
+    s = launch_route(m, rp, W_router, prototypes, wsplit, st);
+    if (s != UNIF_OK) return s;
+    UNIF_MARK(1);
+
+    // 3. offsets and tile tables, pair slots, slab lists
+    PermuteParams pp;
+    pp.N = m.N;
+    pp.K = m.K;
+    pp.B = m.B;
+    pp.key_bits = m.key_bits;
+    pp.bm_up = kBM;
+    pp.bm_down = kBM;
+    pp.down_col_tiles = m.bf16 ? m.d / kBN : 1;
+    pp.mask = mask;
+    pp.nres = nres;
+    pp.eids = eids;
+    pp.bin_count = bin_count;
+    pp.bin_cursor = reinterpret_cast<int*>(ws + plan.bin_cursor);
+    pp.slab_count = slab_count;
+    pp.slab_off = reinterpret_cast<int*>(ws + plan.slab_off);
+    pp.slab_cursor = reinterpret_cast<int*>(ws + plan.slab_cursor);
+    pp.seg_off = reinterpret_cast<int*>(ws + plan.seg_off);
+    pp.up_tile_off = reinterpret_cast<int*>(ws + plan.up_tile_off);
+    pp.down_tile_off = reinterpret_cast<int*>(ws + plan.down_tile_off);
+    pp.totals = totals;
+    pp.pair_token = reinterpret_cast<int*>(ws + plan.pair_token);
+    pp.pair_mask = reinterpret_cast<uint64_t*>(ws + plan.pair_mask);
+    pp.pair_expert = reinterpret_cast<int*>(ws + plan.pair_expert);
+    pp.pair_of = reinterpret_cast<int*>(ws + plan.pair_of);
+    pp.slab_rows = m.bf16 ? reinterpret_cast<int*>(ws + plan.slab_rows) : nullptr;
+    scan_kernel<<<1, kScanThreads, 0, st>>>(pp);
+    UNIF_LAUNCH_CHECK();
+    scatter_kernel<<<ceil_div(m.N, 256), 256, 0, st>>>(pp);
+    UNIF_LAUNCH_CHECK();
+
+    const int cus = cu_count();
+    void* part = ws + plan.part;
+    if (m.bf16) {
+        slabfill_kernel<<<cus * 4, 256, 0, st>>>(pp);
+        UNIF_LAUNCH_CHECK();
+        UNIF_MARK(2);
+        // 4. block-sparse expert GEMMs
+        UpParams up;
+        up.d = m.d;
+        up.M = m.M;
+        up.B = m.B;
+        up.H = m.H;
+        up.nslab = m.nslab;
+        up.X = static_cast<const u16*>(X);
+        up.Wup = static_cast<const u16*>(W_up);
+        up.Hbuf = reinterpret_cast<u16*>(ws + plan.hbuf);
+        up.slab_rows = pp.slab_rows;
+        up.slab_off = pp.slab_off;
+        up.slab_count = slab_count;
+        up.up_tile_off = pp.up_tile_off;
+        up.totals = totals;
+        up.pair_token = pp.pair_token;
+        const size_t up_lds = (size_t)up_lds_elems(m.M) * sizeof(u16);
+        const int up_grid = cus * 2;
+        switch (m.M / 32) {
+            case 2: up_kernel<2><<<up_grid, kFfnThreads, up_lds, st>>>(up); break;
+            case 4: up_kernel<4><<<up_grid, kFfnThreads, up_lds, st>>>(up); break;
+            case 6: up_kernel<6><<<up_grid, kFfnThreads, up_lds, st>>>(up); break;
+            case 8:
+                if (allow_lds(up_kernel<8>, up_lds) != UNIF_OK) return UNIF_EDEVICE;
+                up_kernel<8><<<up_grid, kFfnThreads, up_lds, st>>>(up);
+                break;
+            default: return UNIF_EUNSUPPORTED;
+        }
+        UNIF_LAUNCH_CHECK();
+        UNIF_MARK(3);
+        DownParams dn;
+        dn.d = m.d;
+        dn.M = m.M;
+        dn.B = m.B;
+        dn.H = m.H;
+        dn.K1 = m.K1;
+        dn.Hbuf = up.Hbuf;
+        dn.Wdown = static_cast<const u16*>(W_down);
+        dn.part = static_cast<u16*>(part);
+        dn.seg_off = pp.seg_off;
+        dn.down_tile_off = pp.down_tile_off;
+        dn.totals = totals;
+        dn.pair_mask = pp.pair_mask;
+        down_kernel<<<cus * 3, kFfnThreads, (size_t)down_lds_elems() * sizeof(u16), st>>>(dn);
+        UNIF_LAUNCH_CHECK();
+        UNIF_MARK(4);
+    } else {
+        UNIF_MARK(2);
+        PairF32Params fp;
+        fp.d = m.d;
+        fp.M = m.M;
+        fp.B = m.B;
+        fp.H = m.H;
+        fp.X = static_cast<const float*>(X);
+        fp.Wup = static_cast<const float*>(W_up);
+        fp.Wdown = static_cast<const float*>(W_down);
+        fp.part = static_cast<float*>(part);
+        fp.pair_token = pp.pair_token;
+        fp.pair_expert = pp.pair_expert;
+        fp.pair_mask = pp.pair_mask;
+        fp.totals = totals;
+        const size_t lds = (size_t)m.H * sizeof(float);
+        if (allow_lds(pair_ffn_f32_kernel, lds) != UNIF_OK) return UNIF_EDEVICE;
+        pair_ffn_f32_kernel<<<cus * 4, 256, lds, st>>>(fp);
+        UNIF_LAUNCH_CHECK();
+        UNIF_MARK(3);
+        UNIF_MARK(4);
+    }
+
+    // 5. weighted merge
+    CombineParams cp;
+    cp.N = m.N;
+    cp.d = m.d;
+    cp.K = m.K;
+    cp.part = part;
+    cp.pair_of = pp.pair_of;
+    cp.alpha = alpha;
+    cp.nres = nres;
+    cp.wts = wts;
+    cp.Y = Y;
+    if (m.bf16) {
+        const size_t items = (size_t)m.N * (m.d / 8);
+        combine_bf16_kernel<<<(unsigned)((items + 255) / 256), 256, 0, st>>>(cp);
+    } else {
+        const size_t items = (size_t)m.N * m.d;
+        combine_f32_kernel<<<(unsigned)((items + 255) / 256), 256, 0, st>>>(cp);
+    }
+    UNIF_LAUNCH_CHECK();
+    UNIF_MARK(5);
+    return UNIF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t unif_moe_layer_forward(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
+                               const float* W_router, const float* prototypes, const void* W_up,
+                               const void* W_down, void* Y, const unif_moe_routing* routing_out,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+    return forward_impl(cfg, X, valid, W_router, prototypes, W_up, W_down, Y, routing_out, workspace,
+                        workspace_bytes, nullptr, stream);
+}
+
+int32_t unif_moe_layer_forward_profiled(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
+                                        const float* W_router, const float* prototypes, const void* W_up,
+                                        const void* W_down, void* Y, const unif_moe_routing* routing_out,
+                                        void* workspace, size_t workspace_bytes, void* const* events,
+                                        int32_t n_events, void* stream) {
+    if (events == nullptr || n_events != 6) return UNIF_EINVAL;
+    for (int i = 0; i < 6; ++i)
+        if (events[i] == nullptr) return UNIF_EINVAL;
+    return forward_impl(cfg, X, valid, W_router, prototypes, W_up, W_down, Y, routing_out, workspace,
+                        workspace_bytes, events, stream);
+}
+
+int32_t unif_moe_stats_workspace_size(const unif_moe_config* cfg, size_t* bytes) {
+    if (bytes == nullptr) return UNIF_EINVAL;
+    const int32_t s = check_config(cfg);
+    if (s != UNIF_OK) return s;
+    *bytes = (size_t)kStWords * 8 + 256;
+    return UNIF_OK;
+}
+
+int32_t unif_moe_stats(const unif_moe_config* cfg, const unif_moe_routing* routing, const uint8_t* valid,
+                       unif_moe_stats_t* host_out, void* workspace, size_t workspace_bytes, void* stream) {
+    const int32_t s = check_config(cfg);
+    if (s != UNIF_OK) return s;
+    if (host_out == nullptr || !record_complete(routing)) return UNIF_EINVAL;
+    size_t need = 0;
+    unif_moe_stats_workspace_size(cfg, &need);
+    if (workspace == nullptr || workspace_bytes < need) return UNIF_EWORKSPACE;
+    const Dims m = dims_of(cfg);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    unsigned long long* cnt = reinterpret_cast<unsigned long long*>(align_base(workspace));
+    fill_zero_kernel<<<1, 256, 0, st>>>(reinterpret_cast<uint32_t*>(cnt), (size_t)kStWords * 2);
+    UNIF_LAUNCH_CHECK();
+    if (m.N > 0) {
+        StatsParams sp;
+        sp.N = m.N;
+        sp.K = m.K;
+        sp.B = m.B;
+        sp.valid = valid;
+        sp.nsh = routing->n_shared;
+        sp.nres = routing->n_res;
+        sp.eids = routing->expert_ids;
+        sp.out = cnt;
+        const int grid = ceil_div(m.N, 256) < 1024 ? ceil_div(m.N, 256) : 1024;
+        stats_kernel<<<grid, 256, 0, st>>>(sp);
+        UNIF_LAUNCH_CHECK();
+    }
+    unsigned long long h[kStWords];
+    if (hipMemcpyAsync(h, cnt, sizeof(h), hipMemcpyDeviceToHost, st) != hipSuccess) return UNIF_EDEVICE;
+    if (hipStreamSynchronize(st) != hipSuccess) return UNIF_EDEVICE;
+    std::memset(host_out, 0, sizeof(*host_out));
+    host_out->n_valid = (int64_t)h[kStN];
+    for (int i = 0; i < 65; ++i) {
+        host_out->hist_b[i] = (int64_t)h[kStHistB + i];
+        host_out->hist_k[i] = (int64_t)h[kStHistK + i];
+        host_out->expert_tokens[i] = (int64_t)h[kStExp + i];
+    }
+    host_out->activated_blocks = (int64_t)h[kStSumCB];
+    const double nv = (double)h[kStN];
+    host_out->mean_b = nv > 0 ? (double)h[kStSumB] / nv : 0.0;
+    host_out->mean_k = nv > 0 ? (double)h[kStSumK] / nv : 0.0;
+    host_out->mean_cb = nv > 0 ? (double)h[kStSumCB] / nv : 0.0;
+    host_out->activated_gemm_flops = 4.0 * m.d * m.M * (double)h[kStSumCB];
+    host_out->routing_flops = 2.0 * m.d * (1.0 + m.K + m.B) * nv;
+    return UNIF_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,141 @@
+"""Parity protocol between the HIP library and the CPU oracle.
+
+Routing: every valid token whose decision margin (oracle.margins) is at least
+1e-4 must get exactly the oracle's discrete decisions (b, I_shr, k and the
+set {q_1..q_k}); the order of q is compared wherever neighbouring affinities
+differ by at least 1e-4. Tokens below the margin are counted; where their
+decisions differ, each differing decision must lie within 1e-4 of its
+boundary, and their outputs are checked against the oracle evaluated under
+the GPU's decisions (oracle.forced_forward).
+
+Outputs: max |y_gpu - y_ref| <= tol * RMS(y_ref) over the checked tokens and
+all features, with tol = 2e-2 for bf16 and 1e-4 for fp32.
+"""
+import numpy as np
+
+import oracle.unif_moe_oracle as O
+from synth.generate import bf16_bits_to_f32
+
+MARGIN = 1e-4
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+
+
+def _decision_parts(rec, t, B):
+    m = int(rec["shared_mask"][t])
+    k = int(rec["n_res"][t])
+    return (int(rec["n_shared"][t]), m, k, frozenset(int(j) for j in rec["expert_ids"][t, :k]))
+
+
+def check_routing(cfg, orec, grec):
+    """Compare records; returns a summary dict, raises AssertionError."""
+    K, B = cfg["n_experts"], cfg["n_blocks"]
+    m, parts = O.margins(cfg, orec)
+    v = orec["valid"]
+    N = len(v)
+    # padded tokens: exact record
+    pad = ~v
+    assert np.all(grec["n_res"][pad] == 0) and np.all(grec["n_shared"][pad] == 0)
+    assert np.all(grec["shared_mask"][pad] == 0) and np.all(grec["alpha"][pad] == 0)
+    assert np.all(grec["expert_ids"][pad] == -1) and np.all(grec["weights"][pad] == 0)
+
+    sure = v & (m >= MARGIN)
+    idx = np.nonzero(sure)[0]
+    bad = idx[grec["n_shared"][idx] != orec["n_shared"][idx]]
+    assert bad.size == 0, f"b differs on {bad.size} tokens with margin >= {MARGIN}, e.g. {bad[:5]}"
+    bad = idx[grec["shared_mask"][idx] != orec["shared_mask"][idx]]
+    assert bad.size == 0, f"I_shr differs on {bad.size} tokens, e.g. {bad[:5]}"
+    bad = idx[grec["n_res"][idx] != orec["n_res"][idx]]
+    assert bad.size == 0, f"k differs on {bad.size} tokens, e.g. {bad[:5]}"
+    # expert sets {q_1..q_k}
+    kk = orec["n_res"]
+    pos = np.arange(K)[None, :]
+    sel_o = np.zeros((N, K + 1), bool)
+    sel_g = np.zeros((N, K + 1), bool)
+    rows = np.repeat(np.arange(N)[:, None], K, 1)
+    live = (pos < kk[:, None]) & v[:, None]
+    np.logical_or.at(sel_o, (rows[live], orec["expert_ids"][live]), True)
+    live_g = (pos < grec["n_res"][:, None]) & v[:, None]
+    np.logical_or.at(sel_g, (rows[live_g], np.clip(grec["expert_ids"][live_g], 0, K)), True)
+    bad = idx[np.any(sel_o[idx] != sel_g[idx], axis=1)]
+    assert bad.size == 0, f"expert set differs on {bad.size} tokens, e.g. {bad[:5]}"
+    # order of q where neighbouring affinities are separated
+    p = orec["weights"].astype(np.float64)
+    gap = np.full((N, K + 1), np.inf)
+    gap[:, 1:K] = p[:, :-1] - p[:, 1:]
+    sep = (gap[:, :K] >= MARGIN) & (gap[:, 1:] >= MARGIN)
+    chk = sure[:, None] & sep
+    bad = np.nonzero(np.any(chk & (grec["expert_ids"] != orec["expert_ids"]), axis=1))[0]
+    assert bad.size == 0, f"expert order differs on {bad.size} tokens, e.g. {bad[:5]}"
+    # continuous values (diagnostics)
+    da = float(np.abs(grec["alpha"][v].astype(np.float64) - orec["alpha"][v]).max(initial=0.0))
+    dp = float(np.abs(np.sort(grec["weights"][v], axis=1).astype(np.float64)
+                      - np.sort(orec["weights"][v], axis=1)).max(initial=0.0))
+    assert da <= 1e-6, f"alpha differs by {da}"
+    assert dp <= 1e-6, f"affinities differ by {dp}"
+
+    near = np.nonzero(v & (m < MARGIN))[0]
+    differ = []
+    for t in near:
+        go, oo = _decision_parts(grec, t, B), _decision_parts(orec, t, B)
+        if go == oo:
+            continue
+        differ.append(int(t))
+        if go[0] != oo[0]:
+            assert parts["m_b"][t] < MARGIN, ("b differs away from its boundary", t)
+        elif go[1] != oo[1]:
+            assert parts["m_sel"][t] < MARGIN, ("I_shr differs away from its boundary", t)
+        if go[2] != oo[2]:
+            assert parts["m_k"][t] < MARGIN, ("k differs away from its boundary", t)
+        elif go[3] != oo[3]:
+            assert parts["m_set"][t] < MARGIN, ("expert set differs away from its boundary", t)
+    return dict(n_valid=int(v.sum()), n_checked=int(sure.sum()), n_near=int(near.size),
+                n_near_differ=len(differ), near_differ=differ, max_alpha_err=da, max_p_err=dp)
+
+
+def sample_tokens(orec, cfg, n_sample, seed=1234, near_cap=256):
+    """Seeded sample of valid tokens, plus near-tie tokens (capped) and
+    tokens with the extreme b and k."""
+    v = np.nonzero(orec["valid"])[0]
+    rng = np.random.default_rng(seed)
+    pick = set(rng.choice(v, size=min(n_sample, v.size), replace=False).tolist())
+    m, _ = O.margins(cfg, orec)
+    near = np.nonzero(orec["valid"] & (m < MARGIN))[0]
+    if near.size > near_cap:
+        near = rng.choice(near, size=near_cap, replace=False)
+    pick.update(near.tolist())
+    for key in ("n_shared", "n_res"):
+        vals = orec[key][v]
+        for target in (vals.min(), vals.max()):
+            pick.update(v[vals == target][:4].tolist())
+    return np.array(sorted(pick))
+
+
+def gpu_output_f64(Y, dtype):
+    return (bf16_bits_to_f32(Y) if dtype == "bf16" else np.asarray(Y, np.float32)).astype(np.float64)
+
+
+def check_outputs(cfg, inputs, orec, grec, Y_gpu, tokens, weights=None):
+    """Compare GPU rows against the oracle on ``tokens``; returns the
+    relative error (max abs / RMS)."""
+    if weights is None:
+        weights = O.ExpertWeights(cfg, inputs["W_up"], inputs["W_down"])
+    B = cfg["n_blocks"]
+    Yg = gpu_output_f64(Y_gpu[tokens], cfg["dtype"])
+    ref = np.zeros_like(Yg)
+    agree = [t for t in tokens if _decision_parts(grec, t, B) == _decision_parts(orec, t, B)]
+    Ya, _ = O.forward(cfg, inputs["X"], inputs["valid"], inputs["W_router"], inputs["prototypes"],
+                      None, None, tokens=agree, rec=orec, weights=weights)
+    for i, t in enumerate(tokens):
+        if not orec["valid"][t]:
+            continue
+        if _decision_parts(grec, t, B) == _decision_parts(orec, t, B):
+            ref[i] = Ya[t]
+        else:
+            b, mask, k, experts = _decision_parts(grec, t, B)
+            ref[i] = O.forced_forward(cfg, inputs["X"], orec, t,
+                                      [c for c in range(B) if mask >> c & 1], sorted(experts), weights)
+    rms = float(np.sqrt(np.mean(ref ** 2)))
+    err = float(np.abs(Yg - ref).max())
+    rel = err / rms if rms > 0 else err
+    assert rel <= TOL[cfg["dtype"]], f"output error {err:.3e} = {rel:.3e} x RMS {rms:.3e}"
+    return rel

@@ -1,0 +1,149 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads and
+exports every function include/unif_moe.h declares, the ctypes structures
+match the C layout, and invalid arguments are rejected before any HIP call.
+"""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2608_10392_amd import _lib
+from synth import config_names, get_config, layer_config
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "unif_moe.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    return _lib.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int32_t|const char\*)\s+(unif_moe_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert len(names) == 8, names
+    assert set(names) == set(_lib.EXPORTS)
+    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True, text=True).stdout
+    for n in names:
+        assert re.search(rf"\bT {n}$", out, re.M), n
+        assert getattr(L, n) is not None
+
+
+def test_struct_layout_matches_header(tmp_path):
+    src = tmp_path / "layout.c"
+    src.write_text(
+        '#include <stdio.h>\n#include <stddef.h>\n#include "unif_moe.h"\n'
+        "#define F(T, m) printf(#T \".\" #m \" %zu\\n\", offsetof(T, m))\n"
+        "int main(void) {\n"
+        ' printf("config %zu\\nrouting %zu\\nstats %zu\\n", sizeof(unif_moe_config),'
+        " sizeof(unif_moe_routing), sizeof(unif_moe_stats_t));\n"
+        " F(unif_moe_config, tau); F(unif_moe_config, select_mode);"
+        " F(unif_moe_routing, weights); F(unif_moe_stats_t, expert_tokens);"
+        " F(unif_moe_stats_t, activated_blocks); F(unif_moe_stats_t, routing_flops);\n"
+        " return 0; }\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    got = dict(l.rsplit(" ", 1) for l in subprocess.run([str(exe)], capture_output=True, text=True).stdout.splitlines())
+    assert int(got["config"]) == ctypes.sizeof(_lib.Config)
+    assert int(got["routing"]) == ctypes.sizeof(_lib.Routing)
+    assert int(got["stats"]) == ctypes.sizeof(_lib.Stats)
+    assert int(got["unif_moe_config.tau"]) == _lib.Config.tau.offset
+    assert int(got["unif_moe_config.select_mode"]) == _lib.Config.select_mode.offset
+    assert int(got["unif_moe_routing.weights"]) == _lib.Routing.weights.offset
+    assert int(got["unif_moe_stats_t.expert_tokens"]) == _lib.Stats.expert_tokens.offset
+    assert int(got["unif_moe_stats_t.activated_blocks"]) == _lib.Stats.activated_blocks.offset
+    assert int(got["unif_moe_stats_t.routing_flops"]) == _lib.Stats.routing_flops.offset
+
+
+def test_status_strings(L):
+    assert _lib.status_string(0) == "ok"
+    assert _lib.status_string(-2) == "workspace too small"
+    assert _lib.status_string(12345) == "unknown status"
+
+
+def base_cfg(**kw):
+    c = layer_config(get_config("vit_b16"))
+    c.update(kw)
+    return c
+
+
+@pytest.mark.parametrize("bad", [
+    dict(n_tokens=-1), dict(d_model=0), dict(n_experts=0), dict(n_blocks=0), dict(block_width=0),
+    dict(mass_threshold=0.0), dict(mass_threshold=1.5), dict(mass_threshold=math.nan),
+    dict(max_shared=-1), dict(max_shared=17), dict(n_blocks=1, max_shared=1),
+    dict(alpha_mode="fixed", alpha_fixed=1.5), dict(mass_mode="topk", fixed_k=0),
+    dict(mass_mode="topk", fixed_k=17), dict(tau=0.5), dict(tau=-0.1),
+])
+def test_invalid_config_rejected(bad):
+    with pytest.raises(_lib.UnifMoeError) as e:
+        _lib.layer_forward_workspace_size(base_cfg(**bad))
+    assert e.value.status == _lib.EINVAL
+
+
+@pytest.mark.parametrize("bad", [
+    dict(n_blocks=65, max_shared=65), dict(n_experts=65), dict(d_model=200),
+    dict(block_width=96), dict(block_width=320), dict(n_tokens=2 ** 30),
+])
+def test_unsupported_shapes(bad):
+    with pytest.raises(_lib.UnifMoeError) as e:
+        _lib.layer_forward_workspace_size(base_cfg(**bad))
+    assert e.value.status == _lib.EUNSUPPORTED
+
+
+def test_fixed_alpha_allows_one_block():
+    assert _lib.route_workspace_size(base_cfg(n_blocks=1, max_shared=1, alpha_mode="fixed",
+                                              block_width=3072)) > 0
+
+
+@pytest.mark.parametrize("name", config_names())
+def test_workspace_sizes_cover_worst_case(name):
+    c = layer_config(get_config(name))
+    N, d, K, H = c["n_tokens"], c["d_model"], c["n_experts"], c["n_blocks"] * c["block_width"]
+    es = 2 if c["dtype"] == "bf16" else 4
+    ws = _lib.layer_forward_workspace_size(c)
+    pairs = N * (K + 1)
+    assert ws >= pairs * d * es                      # per-expert outputs
+    if c["dtype"] == "bf16":
+        assert ws >= pairs * (H * 2 + d * 2)         # activations + outputs
+    assert _lib.stats_workspace_size(c) >= 199 * 8
+
+
+def test_calls_fail_before_touching_the_device(L):
+    """Each rejected call returns its status without any HIP call, so these
+    run on a host with no GPU."""
+    c = _lib.make_config(base_cfg(n_tokens=4))
+    r = _lib.Routing(*([1] * 6))
+    # NULL token matrix
+    assert L.unif_moe_route(ctypes.byref(c), None, None, 1, 1, ctypes.byref(r), 1, 1 << 30, None) == _lib.EINVAL
+    # incomplete record
+    r0 = _lib.Routing(1, 1, 1, None, 1, 1)
+    assert L.unif_moe_route(ctypes.byref(c), 1, None, 1, 1, ctypes.byref(r0), 1, 1 << 30, None) == _lib.EINVAL
+    # workspace too small / missing
+    assert L.unif_moe_route(ctypes.byref(c), 1, None, 1, 1, ctypes.byref(r), 1, 16, None) == _lib.EWORKSPACE
+    assert L.unif_moe_layer_forward(ctypes.byref(c), 1, None, 1, 1, 1, 1, 1, None, None, 0, None) == _lib.EWORKSPACE
+    assert L.unif_moe_layer_forward(ctypes.byref(c), 1, None, 1, 1, None, 1, 1, None, 1, 1 << 40, None) == _lib.EINVAL
+    assert L.unif_moe_layer_forward(ctypes.byref(c), 1, None, 1, 1, 1, 1, 1, ctypes.byref(r0), 1, 1 << 40, None) == _lib.EINVAL
+    s = _lib.Stats()
+    assert L.unif_moe_stats(ctypes.byref(c), ctypes.byref(r), None, None, 1, 4096, None) == _lib.EINVAL
+    assert L.unif_moe_stats(ctypes.byref(c), ctypes.byref(r), None, ctypes.byref(s), None, 0, None) == _lib.EWORKSPACE
+    assert L.unif_moe_layer_forward(None, 1, None, 1, 1, 1, 1, 1, None, 1, 1, None) == _lib.EINVAL
+    n = ctypes.c_size_t(0)
+    assert L.unif_moe_layer_forward_workspace_size(ctypes.byref(c), None) == _lib.EINVAL
+    assert L.unif_moe_layer_forward_workspace_size(ctypes.byref(c), ctypes.byref(n)) == 0 and n.value > 0
+
+
+def test_empty_batch_is_a_no_op(L):
+    """N = 0 with a large enough workspace returns OK without launching."""
+    c = _lib.make_config(base_cfg(n_tokens=0))
+    n = ctypes.c_size_t(0)
+    assert L.unif_moe_layer_forward_workspace_size(ctypes.byref(c), ctypes.byref(n)) == 0
+    assert L.unif_moe_layer_forward(ctypes.byref(c), None, None, None, None, None, None, None,
+                                    None, 1, n.value, None) == 0
