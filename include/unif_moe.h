@@ -167,10 +167,10 @@ int32_t unif_moe_layer_forward_workspace_size(const unif_moe_config* cfg, size_t
  *          linear layer)
  *   Y      [N, d] (cfg->dtype), written for every row (zero for padded rows)
  *   routing_out  optional record (NULL: kept inside the workspace)
- * Accumulation is fp32. In the bf16 path the GELU activations and the
- * per-expert outputs are rounded to bf16 before the next contraction and the
- * merge; the merge sums in a fixed order (shared expert, then q_1..q_k), so
- * repeated calls give bitwise-identical Y.
+ * Accumulation is fp32. In the bf16 path the GELU activations are rounded
+ * to bf16 before the down-projection; the per-expert outputs stay fp32 and
+ * Y is rounded once. The merge sums in a fixed order (shared expert, then
+ * q_1..q_k), so repeated calls give bitwise-identical Y.
  * Requires, for bf16: d % 128 == 0, M % 64 == 0, M <= 256; for fp32:
  * H = B M <= 16384. Otherwise UNIF_EUNSUPPORTED. */
 int32_t unif_moe_layer_forward(const unif_moe_config* cfg, const void* X, const uint8_t* valid,

@@ -9,7 +9,7 @@
 // Down-projection, one tile = 128 consecutive pairs of one expert segment x
 // 128 output columns:
 //   part[pair, n] = sum over blocks c of the pair's mask of
-//                   Hbuf[pair, block c] . V_e[block c, n]
+//                   Hbuf[pair, block c] . V_e[block c, n]        (fp32)
 // The contraction runs over the union of the tile's block masks; rows whose
 // mask lacks a block load zeros, and each 16-row MFMA group skips the blocks
 // none of its rows use. Pairs are sorted by mask key, so tiles hold similar
@@ -47,7 +47,7 @@ struct DownParams {
     int d, M, B, H, K1;
     const u16* Hbuf;
     const u16* Wdown;
-    u16* part;
+    float* part;
     const int* seg_off;
     const int* down_tile_off;
     const int* totals;
@@ -57,9 +57,7 @@ struct DownParams {
 __host__ __device__ constexpr int up_lds_elems(int M) {
     return ((kBM + M) * kLdk > kBM * (M + 8)) ? (kBM + M) * kLdk : kBM * (M + 8);
 }
-__host__ __device__ constexpr int down_lds_elems() {
-    return ((kBM + kBN) * kLdk > kBM * (kBN + 8)) ? (kBM + kBN) * kLdk : kBM * (kBN + 8);
-}
+__host__ __device__ constexpr int down_lds_elems() { return (kBM + kBN) * kLdk; }
 
 // Largest i in [0, n) with off[i] <= x (off ascending, off[0] = 0 <= x).
 __device__ __forceinline__ int upper_index(const int* off, int n, int x) {
@@ -230,24 +228,18 @@ __global__ __launch_bounds__(kFfnThreads) void down_kernel(DownParams p) {
                 __syncthreads();
             }
         }
-        constexpr int OST = kBN + 8;
-        u16* Os = lds_dn;
+        // fp32 per-expert rows; each 16-lane group writes 64 contiguous bytes.
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int r = 0; r < 4; ++r) {
+                const int row = wm * 64 + i * 16 + (lane >> 4) * 4 + r;
+                if (row < nrows) {
+                    float* dst = p.part + (size_t)(p0 + row) * p.d + n0 + wn * 64 + (lane & 15);
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int row = wm * 64 + i * 16 + (lane >> 4) * 4 + r;
-                    const int col = wn * 64 + j * 16 + (lane & 15);
-                    Os[row * OST + col] = f2bf(acc[i][j][r]);
+                    for (int j = 0; j < 4; ++j) dst[j * 16] = acc[i][j][r];
                 }
-        __syncthreads();
-        for (int i = tid; i < kBM * (kBN / 8); i += kFfnThreads) {
-            const int r = i / (kBN / 8), ch = i - (i / (kBN / 8)) * (kBN / 8);
-            if (r < nrows)
-                st16(p.part + (size_t)(p0 + r) * p.d + n0 + ch * 8, ld16(Os + r * OST + ch * 8));
-        }
+            }
     }
 }
 

@@ -168,7 +168,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.pair_of = cv.take(4 * N * K1);
     p.slab_rows = cv.take(m.bf16 ? 4 * N * K * (size_t)m.B : 0);
     p.hbuf = cv.take(m.bf16 ? pmax * (size_t)m.H * 2 : 0);
-    p.part = cv.take(pmax * (size_t)m.d * m.elem);
+    p.part = cv.take(pmax * (size_t)m.d * sizeof(float));
     p.total = cv.cur + 256;  // slack for aligning an unaligned base pointer
     return p;
 }
@@ -461,7 +461,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         dn.K1 = m.K1;
         dn.Hbuf = up.Hbuf;
         dn.Wdown = static_cast<const u16*>(W_down);
-        dn.part = static_cast<u16*>(part);
+        dn.part = static_cast<float*>(part);
         dn.seg_off = pp.seg_off;
         dn.down_tile_off = pp.down_tile_off;
         dn.totals = totals;

