@@ -98,7 +98,7 @@ int32_t check_config(const unif_moe_config* c) {
 int32_t check_forward_shape(const unif_moe_config* c) {
     const Dims m = dims_of(c);
     if (m.bf16) {
-        if (m.d % kBN != 0 || m.M % kBK != 0 || m.M > 256) return UNIF_EUNSUPPORTED;
+        if (m.d % 128 != 0 || m.M % kBK != 0 || m.M > 256) return UNIF_EUNSUPPORTED;
         if ((int64_t)m.H * m.d * 2 > ((int64_t)1 << 40)) return UNIF_EUNSUPPORTED;
     } else {
         if ((int64_t)m.H > 16384) return UNIF_EUNSUPPORTED;
@@ -203,6 +203,13 @@ int32_t allow_lds(F* kernel, size_t bytes) {
                             (int)bytes) != hipSuccess)
         return UNIF_EDEVICE;
     return UNIF_OK;
+}
+
+template <class P>
+int32_t launch_persistent(void (*kernel)(P), int grid, size_t lds, hipStream_t st, const P& prm) {
+    if (allow_lds(kernel, lds) != UNIF_OK) return UNIF_EDEVICE;
+    kernel<<<grid, kFfnThreads, lds, st>>>(prm);
+    return hipGetLastError() == hipSuccess ? UNIF_OK : UNIF_EDEVICE;
 }
 
 RouteParams route_params(const unif_moe_config* c, const Dims& m, const void* X, const uint8_t* valid,
@@ -392,9 +399,10 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.K = m.K;
     pp.B = m.B;
     pp.key_bits = m.key_bits;
-    pp.bm_up = kBM;
-    pp.bm_down = kBM;
-    pp.down_col_tiles = m.bf16 ? m.d / kBN : 1;
+    const int down_bn = 128;
+    pp.bm_up = kTM;
+    pp.bm_down = kTM;
+    pp.down_col_tiles = m.bf16 ? m.d / down_bn : 1;
     pp.mask = mask;
     pp.nres = nres;
     pp.eids = eids;
@@ -440,18 +448,15 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         up.totals = totals;
         up.pair_token = pp.pair_token;
         const size_t up_lds = (size_t)up_lds_elems(m.M) * sizeof(u16);
-        const int up_grid = cus * 2;
+        const int grid = (cus / kXcds) * kXcds;
         switch (m.M / 32) {
-            case 2: up_kernel<2><<<up_grid, kFfnThreads, up_lds, st>>>(up); break;
-            case 4: up_kernel<4><<<up_grid, kFfnThreads, up_lds, st>>>(up); break;
-            case 6: up_kernel<6><<<up_grid, kFfnThreads, up_lds, st>>>(up); break;
-            case 8:
-                if (allow_lds(up_kernel<8>, up_lds) != UNIF_OK) return UNIF_EDEVICE;
-                up_kernel<8><<<up_grid, kFfnThreads, up_lds, st>>>(up);
-                break;
+            case 2: s = launch_persistent(up_kernel<2>, grid, up_lds, st, up); break;
+            case 4: s = launch_persistent(up_kernel<4>, grid, up_lds, st, up); break;
+            case 6: s = launch_persistent(up_kernel<6>, grid, up_lds, st, up); break;
+            case 8: s = launch_persistent(up_kernel<8>, grid, up_lds, st, up); break;
             default: return UNIF_EUNSUPPORTED;
         }
-        UNIF_LAUNCH_CHECK();
+        if (s != UNIF_OK) return s;
         UNIF_MARK(3);
         DownParams dn;
         dn.d = m.d;
@@ -466,8 +471,10 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         dn.down_tile_off = pp.down_tile_off;
         dn.totals = totals;
         dn.pair_mask = pp.pair_mask;
-        down_kernel<<<cus * 3, kFfnThreads, (size_t)down_lds_elems() * sizeof(u16), st>>>(dn);
-        UNIF_LAUNCH_CHECK();
+        const size_t dn_lds = (size_t)down_lds_elems(down_bn) * sizeof(u16);
+        s = (down_bn == 256) ? launch_persistent(down_kernel<8>, grid, dn_lds, st, dn)
+                             : launch_persistent(down_kernel<4>, grid, dn_lds, st, dn);
+        if (s != UNIF_OK) return s;
         UNIF_MARK(4);
     } else {
         UNIF_MARK(2);
