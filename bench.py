@@ -35,6 +35,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=2048)
     ap.add_argument("--cpu-repeats", type=int, default=3)
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="after the timed steps, copy a buffer of this many MiB device to "
+                         "device (a known-size reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -184,6 +187,14 @@ def main():
                           "mean_cb": round(st["mean_cb"], 3),
                           "activated_gemm_tflop": round(act / 1e12, 4)},
     }
+    if args.copy_calibration_mb > 0:
+        nbytes = args.copy_calibration_mb << 20
+        src = torch.ones(nbytes, dtype=torch.uint8, device=dev.device)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = nbytes
+        del src, dst
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(g, args.cpu_sample, args.cpu_repeats)

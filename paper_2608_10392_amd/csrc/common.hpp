@@ -34,9 +34,29 @@ __device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// GELU(a) = a/2 (1 + erf(a / sqrt 2)), exact erf form.
+// GELU(a) = a/2 (1 + erf(a / sqrt 2)), exact erf form (library erff).
 __device__ __forceinline__ float gelu_erf(float a) {
     return 0.5f * a * (1.0f + erff(a * 0.7071067811865475244f));
+}
+
+// GELU through the rational-exponential erf approximation of Abramowitz and
+// Stegun, Handbook of Mathematical Functions, formula 7.1.26:
+//   erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
+//   t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7,
+// extended to x < 0 by oddness. Branch-free; used where the result is
+// rounded to bf16 (relative spacing 2^-8), far above the formula's error.
+__device__ __forceinline__ float gelu_as7126(float a) {
+    const float x = fabsf(a) * 0.7071067811865475244f;
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
+    float poly = fmaf(1.061405429f, t, -1.453152027f);
+    poly = fmaf(poly, t, 1.421413741f);
+    poly = fmaf(poly, t, -0.284496736f);
+    poly = fmaf(poly, t, 0.254829592f);
+    poly *= t;
+    const float e = __builtin_amdgcn_exp2f(-x * x * 1.4426950408889634f);
+    const float erf_abs = fmaf(-poly, e, 1.0f);
+    const float erf_x = __builtin_copysignf(erf_abs, a);
+    return 0.5f * a * (1.0f + erf_x);
 }
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
@@ -46,5 +66,24 @@ __device__ __forceinline__ uint64_t lanes_below() {
 }
 
 __host__ __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Asynchronous 16-byte copy global -> LDS (gfx950 global_load_lds_dwordx4):
+// lane l of the wave writes its 16 bytes at lds_base + 16 l, where lds_base
+// is the same for the whole wave. Completion is tracked by vmcnt only.
+__device__ __forceinline__ void dma16(const void* gsrc, void* lds_base) {
+    __builtin_amdgcn_global_load_lds(gsrc, lds_base, 16, 0, 0);
+}
+
+// Wait until at most N vector-memory operations of this wave are pending.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Wait until all LDS operations of this wave have completed.
+__device__ __forceinline__ void wait_lgkmcnt0() {
+    __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (0 << 8));
+}
 
 }  // namespace unifmoe

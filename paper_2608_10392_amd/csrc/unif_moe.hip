@@ -98,7 +98,7 @@ int32_t check_config(const unif_moe_config* c) {
 int32_t check_forward_shape(const unif_moe_config* c) {
     const Dims m = dims_of(c);
     if (m.bf16) {
-        if (m.d % 128 != 0 || m.M % kBK != 0 || m.M > 256) return UNIF_EUNSUPPORTED;
+        if (m.d % 128 != 0 || m.M % 64 != 0 || m.M > 256) return UNIF_EUNSUPPORTED;
         if ((int64_t)m.H * m.d * 2 > ((int64_t)1 << 40)) return UNIF_EUNSUPPORTED;
     } else {
         if ((int64_t)m.H > 16384) return UNIF_EUNSUPPORTED;
@@ -132,8 +132,8 @@ RoutePlan plan_route(const Dims& m) {
 struct FwdPlan {
     size_t alpha, nsh, mask, nres, eids, wts;
     size_t wsplit;
-    size_t zero_begin, zero_end;  // bin_count, slab_count, totals
-    size_t bin_count, slab_count, totals;
+    size_t zero_begin, zero_end;  // bin_count, slab_count, totals, zero page
+    size_t bin_count, slab_count, totals, zero_page;
     size_t bin_cursor, slab_off, slab_cursor, seg_off, up_tile_off, down_tile_off;
     size_t pair_token, pair_mask, pair_expert, pair_of, slab_rows, hbuf, part;
     size_t total;
@@ -155,6 +155,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.zero_begin = p.bin_count;
     p.slab_count = cv.take(4 * (size_t)m.nslab);
     p.totals = cv.take(4 * 4);
+    p.zero_page = cv.take(256);
     p.zero_end = cv.cur;
     p.bin_cursor = cv.take(4 * (size_t)m.nbin);
     p.slab_off = cv.take(4 * ((size_t)m.nslab + 1));
@@ -447,7 +448,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         up.up_tile_off = pp.up_tile_off;
         up.totals = totals;
         up.pair_token = pp.pair_token;
-        const size_t up_lds = (size_t)up_lds_elems(m.M) * sizeof(u16);
+        const size_t up_lds = (size_t)up_lds_bytes(m.M);
         const int grid = (cus / kXcds) * kXcds;
         switch (m.M / 32) {
             case 2: s = launch_persistent(up_kernel<2>, grid, up_lds, st, up); break;
@@ -467,11 +468,12 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         dn.Hbuf = up.Hbuf;
         dn.Wdown = static_cast<const u16*>(W_down);
         dn.part = static_cast<float*>(part);
+        dn.zero16 = reinterpret_cast<const u16*>(ws + plan.zero_page);
         dn.seg_off = pp.seg_off;
         dn.down_tile_off = pp.down_tile_off;
         dn.totals = totals;
         dn.pair_mask = pp.pair_mask;
-        const size_t dn_lds = (size_t)down_lds_elems(down_bn) * sizeof(u16);
+        const size_t dn_lds = (size_t)down_lds_bytes(down_bn);
         s = (down_bn == 256) ? launch_persistent(down_kernel<8>, grid, dn_lds, st, dn)
                              : launch_persistent(down_kernel<4>, grid, dn_lds, st, dn);
         if (s != UNIF_OK) return s;
