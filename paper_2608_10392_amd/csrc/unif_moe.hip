@@ -35,6 +35,22 @@ namespace {
 constexpr int kKeyBitsMax = 10;
 constexpr size_t kLdsLimit = 160 * 1024;
 
+// Expert-GEMM tile shapes. Two workgroups share each CU (kGemmOcc), so the
+// ring of one runs while the other waits at a barrier or in its epilogue.
+// Up: 128 gathered rows x the whole block width M, K staged 32 deep, 3
+// stages. Down: 128 pairs x 256 output columns (128 when d is not a
+// multiple of 256).
+constexpr int kGemmOcc = 2;
+constexpr int kUpTM = 128, kUpRB = 64, kUpNST = 3;
+constexpr int kDownTM = 128;
+constexpr int kDownBNWide = 256, kDownWideRB = 64, kDownWideNST = 3;
+constexpr int kDownBNNarrow = 128, kDownNarrowRB = 128, kDownNarrowNST = 2;
+static_assert(kGemmOcc * up_lds_bytes(kUpTM, 256, kUpRB, kUpNST) <= 160 * 1024, "up ring exceeds LDS");
+static_assert(kGemmOcc * down_lds_bytes(kDownTM, kDownBNWide, kDownWideRB, kDownWideNST) <= 160 * 1024 - 4096,
+              "down ring exceeds LDS");
+static_assert(kGemmOcc * down_lds_bytes(kDownTM, kDownBNNarrow, kDownNarrowRB, kDownNarrowNST) <= 160 * 1024 - 4096,
+              "down ring exceeds LDS");
+
 struct Dims {
     int N, d, K, B, M, H, K1, NL, NLP, lstride, key_bits, nslab, nbin;
     bool bf16;
@@ -400,9 +416,9 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.K = m.K;
     pp.B = m.B;
     pp.key_bits = m.key_bits;
-    const int down_bn = 128;
-    pp.bm_up = kTM;
-    pp.bm_down = kTM;
+    const int down_bn = (m.d % kDownBNWide == 0) ? kDownBNWide : kDownBNNarrow;
+    pp.bm_up = kUpTM;
+    pp.bm_down = kDownTM;
     pp.down_col_tiles = m.bf16 ? m.d / down_bn : 1;
     pp.mask = mask;
     pp.nres = nres;
@@ -448,13 +464,13 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         up.up_tile_off = pp.up_tile_off;
         up.totals = totals;
         up.pair_token = pp.pair_token;
-        const size_t up_lds = (size_t)up_lds_bytes(m.M);
-        const int grid = (cus / kXcds) * kXcds;
+        const size_t up_lds = (size_t)up_lds_bytes(kUpTM, m.M, kUpRB, kUpNST);
+        const int grid = (kGemmOcc * cus / kXcds) * kXcds;
         switch (m.M / 32) {
-            case 2: s = launch_persistent(up_kernel<2>, grid, up_lds, st, up); break;
-            case 4: s = launch_persistent(up_kernel<4>, grid, up_lds, st, up); break;
-            case 6: s = launch_persistent(up_kernel<6>, grid, up_lds, st, up); break;
-            case 8: s = launch_persistent(up_kernel<8>, grid, up_lds, st, up); break;
+            case 2: s = launch_persistent(up_kernel<2, kUpTM, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
+            case 4: s = launch_persistent(up_kernel<4, kUpTM, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
+            case 6: s = launch_persistent(up_kernel<6, kUpTM, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
+            case 8: s = launch_persistent(up_kernel<8, kUpTM, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
             default: return UNIF_EUNSUPPORTED;
         }
         if (s != UNIF_OK) return s;
@@ -473,9 +489,13 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         dn.down_tile_off = pp.down_tile_off;
         dn.totals = totals;
         dn.pair_mask = pp.pair_mask;
-        const size_t dn_lds = (size_t)down_lds_bytes(down_bn);
-        s = (down_bn == 256) ? launch_persistent(down_kernel<8>, grid, dn_lds, st, dn)
-                             : launch_persistent(down_kernel<4>, grid, dn_lds, st, dn);
+        if (down_bn == kDownBNWide)
+            s = launch_persistent(down_kernel<kDownBNWide / 32, kDownTM, kDownWideRB, kDownWideNST, kGemmOcc>, grid,
+                                  (size_t)down_lds_bytes(kDownTM, kDownBNWide, kDownWideRB, kDownWideNST), st, dn);
+        else
+            s = launch_persistent(down_kernel<kDownBNNarrow / 32, kDownTM, kDownNarrowRB, kDownNarrowNST, kGemmOcc>,
+                                  grid, (size_t)down_lds_bytes(kDownTM, kDownBNNarrow, kDownNarrowRB, kDownNarrowNST),
+                                  st, dn);
         if (s != UNIF_OK) return s;
         UNIF_MARK(4);
     } else {
