@@ -39,24 +39,46 @@ __device__ __forceinline__ float gelu_erf(float a) {
     return 0.5f * a * (1.0f + erff(a * 0.7071067811865475244f));
 }
 
-// GELU through the rational-exponential erf approximation of Abramowitz and
+// GELU through the rational-exponential erfc approximation of Abramowitz and
 // Stegun, Handbook of Mathematical Functions, formula 7.1.26:
-//   erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
-//   t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7,
-// extended to x < 0 by oddness. Branch-free; used where the result is
-// rounded to bf16 (relative spacing 2^-8), far above the formula's error.
+//   erfc(z) = (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-z^2),
+//   t = 1 / (1 + p z), z >= 0, |error| <= 1.5e-7.
+// With z = |a| / sqrt 2, q = erfc(z) / 2 is the upper normal tail 1 - Phi(|a|)
+// (the halving is folded into the coefficients, 1/sqrt 2 into p), and
+//   GELU(a) = a Phi(a) = a/2 + |a| (1/2 - q)
+// covers both signs without a branch or a select. The absolute error is at
+// most 0.75e-7 |a|; used where the result is rounded to bf16 (relative
+// spacing 2^-8), far above that.
 __device__ __forceinline__ float gelu_as7126(float a) {
-    const float x = fabsf(a) * 0.7071067811865475244f;
-    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
-    float poly = fmaf(1.061405429f, t, -1.453152027f);
-    poly = fmaf(poly, t, 1.421413741f);
-    poly = fmaf(poly, t, -0.284496736f);
-    poly = fmaf(poly, t, 0.254829592f);
+    const float x = fabsf(a);
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f * 0.7071067811865475244f, x, 1.0f));
+    float poly = fmaf(0.5f * 1.061405429f, t, 0.5f * -1.453152027f);
+    poly = fmaf(poly, t, 0.5f * 1.421413741f);
+    poly = fmaf(poly, t, 0.5f * -0.284496736f);
+    poly = fmaf(poly, t, 0.5f * 0.254829592f);
     poly *= t;
-    const float e = __builtin_amdgcn_exp2f(-x * x * 1.4426950408889634f);
-    const float erf_abs = fmaf(-poly, e, 1.0f);
-    const float erf_x = __builtin_copysignf(erf_abs, a);
-    return 0.5f * a * (1.0f + erf_x);
+    // exp(-a^2 / 2) = 2^(-a^2 log2(e) / 2)
+    const float e = __builtin_amdgcn_exp2f((a * a) * -0.7213475204444817f);
+    const float half_minus_q = fmaf(-poly, e, 0.5f);
+    return fmaf(x, half_minus_q, 0.5f * a);
+}
+
+// Two fp32 -> packed bf16 pair (round to nearest even, one gfx950
+// v_cvt_pk_bf16_f32); `lo` lands in the low half.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    bf16x2 v;
+    v[0] = (__bf16)lo;
+    v[1] = (__bf16)hi;
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// Load of a wave-uniform address through the constant address space, so it
+// becomes a scalar-cache load (lgkmcnt) instead of a vector load whose wait
+// would also drain in-flight vector-memory copies. Only for data that no
+// store of the running kernel touches.
+__device__ __forceinline__ int ld_uniform(const int* p) {
+    return *(const __attribute__((address_space(4))) int*)p;
 }
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
@@ -67,11 +89,40 @@ __device__ __forceinline__ uint64_t lanes_below() {
 
 __host__ __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+// Largest i in [0, n) with off[i] <= x (off ascending, off[0] = 0 <= x).
+__device__ __forceinline__ int upper_index(const int* off, int n, int x) {
+    int lo = 0, hi = n;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (off[mid] <= x) lo = mid;
+        else hi = mid;
+    }
+    return lo;
+}
+
 // Asynchronous 16-byte copy global -> LDS (gfx950 global_load_lds_dwordx4):
 // lane l of the wave writes its 16 bytes at lds_base + 16 l, where lds_base
 // is the same for the whole wave. Completion is tracked by vmcnt only.
 __device__ __forceinline__ void dma16(const void* gsrc, void* lds_base) {
     __builtin_amdgcn_global_load_lds(gsrc, lds_base, 16, 0, 0);
+}
+
+// Buffer resource over [base, base + bytes): raw (unstructured) 32-bit
+// dword format, the gfx9 descriptor word 3 for plain buffer loads. A lane
+// whose offset falls outside the range reads zeros and touches no memory.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+// Offset used to make a lane read zeros (beyond any resource size used here).
+constexpr uint32_t kOutOfRange = 0xFFFF0000u;
+
+// Asynchronous 16-byte copy, buffer form: lane l reads voff + soff in the
+// resource and writes its 16 bytes at lds_base + 16 l (lds_base uniform).
+// Lane offsets stay in VGPRs, the uniform part in an SGPR, so the copy
+// needs no per-lane address arithmetic. Completion is tracked by vmcnt.
+__device__ __forceinline__ void dma16(rsrc_t r, uint32_t voff, uint32_t soff, void* lds_base) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_base, 16, voff, soff, 0, 0);
 }
 
 // Wait until at most N vector-memory operations of this wave are pending.

@@ -9,19 +9,31 @@
 // the list of pairs that use it, which the up-projection tiles read.
 //
 //   route_kernel   counts pairs per (expert, key) and rows per slab
-//   scan_kernel    one workgroup: LDS-staged exclusive prefix sums -> bin
-//                  cursors, expert segment offsets, slab offsets, tile tables
-//   scatter_kernel one thread per token claims its pair slots
-//   slabfill_kernel one thread per pair; wave ballots reserve slab slots
+//   scan_kernel        one workgroup: LDS-staged exclusive prefix sums ->
+//                      bin cursors, expert segment offsets, slab offsets,
+//                      chunk offsets, tile tables
+//   scatter_kernel     one thread per token claims its pair slots
+//   chunk_count_kernel per chunk of kChunk pairs of one expert: pairs per block
+//   chunk_scan_kernel  per slab: exclusive scan of its chunk counts
+//   slabfill_kernel    per chunk: each pair writes itself into the slabs of
+//                      its blocks, in pair order (deterministic)
+//
+// Each slab's row list starts at a multiple of the up-projection tile height
+// bm_up and holds the slab's pairs in pair order, with their tokens beside
+// them, so a tile's gather needs no dependent lookups. Up tiles are listed
+// expert by expert, and inside an expert by row chunk j then block c: tiles
+// that run at the same time gather largely the same token rows, which then
+// come from L2.
 #pragma once
 #include "common.hpp"
 
 namespace unifmoe {
 
 constexpr int kScanThreads = 1024;
+constexpr int kChunk = 256;   // pairs per chunk of the ordered slab fill
 
 struct PermuteParams {
-    int N, K, B, key_bits, bm_up, bm_down, down_col_tiles;
+    int N, K, B, key_bits, bm_up, bm_down, down_col_tiles, up_group;
     const uint64_t* mask;
     const int* nres;
     const int* eids;
@@ -29,7 +41,6 @@ struct PermuteParams {
     int* bin_cursor;
     const int* slab_count;
     int* slab_off;
-    int* slab_cursor;
     int* seg_off;
     int* up_tile_off;
     int* down_tile_off;
@@ -38,7 +49,12 @@ struct PermuteParams {
     uint64_t* pair_mask;
     int* pair_expert;
     int* pair_of;  // [N][K+1]: pair of the shared expert, then of q_1..q_k
-    int* slab_rows;
+    int* slab_rows;     // pair of each slab row (entries past a slab's count are unused)
+    int* slab_tok;      // token of each slab row
+    int* up_tile_info;  // per up tile: slab | rows << 16
+    int* up_tile_rows;  // per up tile: first entry in slab_rows / slab_tok
+    int* chunk_off;     // [K+2] first chunk of each expert's pair segment
+    int* chunk_cnt;     // [chunks][B] pairs per block, then (scanned) first slab row
 };
 
 __global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n) {
@@ -82,16 +98,26 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
         nbin, [&](int i) { return p.bin_count[i]; }, [&](int i, int v) { p.bin_cursor[i] = v; }, lds);
     for (int e = threadIdx.x; e <= K1; e += blockDim.x)
         p.seg_off[e] = (e < K1) ? p.bin_cursor[e << p.key_bits] : P;
-    const int rows = block_exclusive_scan(
-        nslab, [&](int i) { return p.slab_count[i]; },
-        [&](int i, int v) { p.slab_off[i] = v; p.slab_cursor[i] = v; }, lds);
     const int bm = p.bm_up;
     const int nup = block_exclusive_scan(
         nslab, [&](int i) { return ceil_div(p.slab_count[i], bm); },
-        [&](int i, int v) { p.up_tile_off[i] = v; }, lds);
+        [&](int i, int v) {
+            p.up_tile_off[i] = v;
+            p.slab_off[i] = v * bm;
+        },
+        lds);
     if (threadIdx.x == 0) {
-        p.slab_off[nslab] = rows;
+        p.slab_off[nslab] = nup * bm;
         p.up_tile_off[nslab] = nup;
+        if (p.chunk_off != nullptr) {
+            int q = 0;
+            for (int e = 0; e < K1; ++e) {
+                p.chunk_off[e] = q;
+                q += ceil_div(p.seg_off[e + 1] - p.seg_off[e], kChunk);
+            }
+            p.chunk_off[K1] = q;
+            p.totals[3] = q;
+        }
         int run = 0;
         for (int e = 0; e < K1; ++e) {
             p.down_tile_off[e] = run;
@@ -129,32 +155,103 @@ __global__ void scatter_kernel(PermuteParams p) {
     }
 }
 
-// Persistent over pairs. Lanes of a wave hold consecutive pairs, which mostly
-// share an expert; for each expert present and each block, one atomic
-// reserves the slots of all lanes that use the block.
-__global__ __launch_bounds__(256) void slabfill_kernel(PermuteParams p) {
-    const int P = p.totals[0];
-    const int lane = lane_id();
-    for (int base = blockIdx.x * blockDim.x; base < P; base += gridDim.x * blockDim.x) {
-        const int pr = base + threadIdx.x;
-        const bool act = pr < P;
-        const int e = act ? p.pair_expert[pr] : -1;
-        const uint64_t m = act ? p.pair_mask[pr] : 0ull;
-        uint64_t todo = ballot(act);
-        while (todo) {
-            const int leader = __ffsll((long long)todo) - 1;
-            const int ecur = __shfl(e, leader);
-            const bool mine = act && (e == ecur);
-            todo &= ~ballot(mine);
-            for (int c = 0; c < p.B; ++c) {
-                const bool use = mine && ((m >> c) & 1ull);
-                const uint64_t bits = ballot(use);
-                if (!bits) continue;
-                int slot = 0;
-                if (lane == leader) slot = atomicAdd(&p.slab_cursor[ecur * p.B + c], __popcll(bits));
-                slot = __shfl(slot, leader);
-                if (use) p.slab_rows[slot + __popcll(bits & lanes_below())] = pr;
-            }
+// Up tile table. Tiles are listed expert by expert; inside an expert the
+// blocks are taken in groups of up_group, and inside a group by row chunk j,
+// then block c. Tile (e, g, j, c) sits at the first tile of the group
+// (up_tile_off of its first slab) + sum over the group's blocks c' of
+// min(j, tiles(e, c')) + the number of the group's blocks c' < c that have a
+// tile j. One workgroup per slab, one thread per tile of the slab.
+__global__ __launch_bounds__(256) void up_tile_kernel(PermuteParams p) {
+    __shared__ int tiles[64];
+    const int sl = blockIdx.x;
+    const int e = sl / p.B, c = sl - e * p.B;
+    const int bm = p.bm_up;
+    const int g0 = (c / p.up_group) * p.up_group, g1 = min(p.B, g0 + p.up_group);
+    if ((int)threadIdx.x < p.B) tiles[threadIdx.x] = ceil_div(p.slab_count[e * p.B + threadIdx.x], bm);
+    __syncthreads();
+    const int cnt = p.slab_count[sl], nt = tiles[c];
+    const int first = p.up_tile_off[e * p.B + g0];
+    for (int j = threadIdx.x; j < nt; j += blockDim.x) {
+        int pos = first;
+        for (int c2 = g0; c2 < g1; ++c2) pos += min(j, tiles[c2]) + ((c2 < c && tiles[c2] > j) ? 1 : 0);
+        p.up_tile_info[pos] = sl | (min(bm, cnt - j * bm) << 16);
+        p.up_tile_rows[pos] = p.slab_off[sl] + j * bm;
+    }
+}
+
+// Chunk q of expert e covers pairs [seg_off[e] + (q - chunk_off[e]) kChunk, ...)
+// of the expert's segment. One workgroup of kChunk threads per chunk, one
+// thread per pair; workgroups past the chunk count exit.
+struct ChunkView {
+    int e, lo, hi;
+};
+__device__ __forceinline__ ChunkView chunk_view(const PermuteParams& p, int q) {
+    ChunkView v;
+    v.e = upper_index(p.chunk_off, p.K + 1, q);
+    v.lo = p.seg_off[v.e] + (q - p.chunk_off[v.e]) * kChunk;
+    v.hi = min(v.lo + kChunk, p.seg_off[v.e + 1]);
+    return v;
+}
+
+// Pairs of the workgroup's waves that use each block (wave ballots).
+__device__ __forceinline__ void chunk_wave_counts(int B, uint64_t m, int (*wc)[64]) {
+    const int w = threadIdx.x >> 6;
+    for (int c = 0; c < B; ++c) {
+        const uint64_t bits = ballot(((m >> c) & 1ull) != 0ull);
+        if (lane_id() == 0) wc[w][c] = __popcll(bits);
+    }
+}
+
+__global__ __launch_bounds__(kChunk) void chunk_count_kernel(PermuteParams p) {
+    const int q = blockIdx.x;
+    if (q >= p.totals[3]) return;
+    __shared__ int wc[kChunk / 64][64];
+    const ChunkView v = chunk_view(p, q);
+    const int pr = v.lo + (int)threadIdx.x;
+    chunk_wave_counts(p.B, pr < v.hi ? p.pair_mask[pr] : 0ull, wc);
+    __syncthreads();
+    if ((int)threadIdx.x < p.B) {
+        int n = 0;
+        for (int w = 0; w < kChunk / 64; ++w) n += wc[w][threadIdx.x];
+        p.chunk_cnt[(size_t)q * p.B + threadIdx.x] = n;
+    }
+}
+
+// One workgroup per slab: its chunks' counts become the slab row at which
+// each chunk's pairs start.
+__global__ __launch_bounds__(256) void chunk_scan_kernel(PermuteParams p) {
+    __shared__ int lds[256];
+    const int sl = blockIdx.x;
+    const int e = sl / p.B, c = sl - e * p.B;
+    const int q0 = p.chunk_off[e], nq = p.chunk_off[e + 1] - q0;
+    const int base = p.slab_off[sl];
+    int* cnt = p.chunk_cnt + (size_t)q0 * p.B + c;
+    block_exclusive_scan(
+        nq, [&](int i) { return cnt[(size_t)i * p.B]; }, [&](int i, int v) { cnt[(size_t)i * p.B] = base + v; },
+        lds);
+}
+
+__global__ __launch_bounds__(kChunk) void slabfill_kernel(PermuteParams p) {
+    const int q = blockIdx.x;
+    if (q >= p.totals[3]) return;
+    __shared__ int wc[kChunk / 64][64];
+    const ChunkView v = chunk_view(p, q);
+    const int pr = v.lo + (int)threadIdx.x;
+    const bool act = pr < v.hi;
+    const uint64_t m = act ? p.pair_mask[pr] : 0ull;
+    const int tok = act ? p.pair_token[pr] : 0;
+    chunk_wave_counts(p.B, m, wc);
+    __syncthreads();
+    const int w = threadIdx.x >> 6;
+    const int* first = p.chunk_cnt + (size_t)q * p.B;
+    for (int c = 0; c < p.B; ++c) {
+        const bool use = ((m >> c) & 1ull) != 0ull;
+        const uint64_t bits = ballot(use);
+        if (use) {
+            int at = first[c] + __popcll(bits & lanes_below());
+            for (int w2 = 0; w2 < w; ++w2) at += wc[w2][c];
+            p.slab_rows[at] = pr;
+            p.slab_tok[at] = tok;
         }
     }
 }

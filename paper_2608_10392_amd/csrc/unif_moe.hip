@@ -42,10 +42,19 @@ constexpr size_t kLdsLimit = 160 * 1024;
 // multiple of 256).
 constexpr int kGemmOcc = 2;
 constexpr int kUpTM = 128, kUpRB = 64, kUpNST = 3;
+// Up tiles are ordered by expert, then by groups of this many blocks, then
+// row chunk, then block: the tiles that run together share token rows
+// (across the group's blocks) and weight slabs (within a group).
+constexpr int kUpBlockGroup = 4;
+constexpr int kUpTMWide = 64;  // M = 256: half-height tiles keep the registers in budget
+int up_tm(int M) { return M > 192 ? kUpTMWide : kUpTM; }
 constexpr int kDownTM = 128;
 constexpr int kDownBNWide = 256, kDownWideRB = 64, kDownWideNST = 3;
 constexpr int kDownBNNarrow = 128, kDownNarrowRB = 128, kDownNarrowNST = 2;
 static_assert(kGemmOcc * up_lds_bytes(kUpTM, 256, kUpRB, kUpNST) <= 160 * 1024, "up ring exceeds LDS");
+// The up kernel's pipeline needs at least 2 NST - 2 stages per tile; the
+// smallest supported d (128) gives 128 / (RB / 2).
+static_assert(128 / (kUpRB / 2) >= 2 * kUpNST - 2, "too few stages per up tile");
 static_assert(kGemmOcc * down_lds_bytes(kDownTM, kDownBNWide, kDownWideRB, kDownWideNST) <= 160 * 1024 - 4096,
               "down ring exceeds LDS");
 static_assert(kGemmOcc * down_lds_bytes(kDownTM, kDownBNNarrow, kDownNarrowRB, kDownNarrowNST) <= 160 * 1024 - 4096,
@@ -115,6 +124,10 @@ int32_t check_forward_shape(const unif_moe_config* c) {
     const Dims m = dims_of(c);
     if (m.bf16) {
         if (m.d % 128 != 0 || m.M % 64 != 0 || m.M > 256) return UNIF_EUNSUPPORTED;
+        // The expert GEMMs address X and each weight tensor with 32-bit
+        // buffer offsets.
+        if ((uint64_t)m.N * m.d * 2 >= kOutOfRange || (uint64_t)m.K1 * m.H * m.d * 2 >= kOutOfRange)
+            return UNIF_EUNSUPPORTED;
         if ((int64_t)m.H * m.d * 2 > ((int64_t)1 << 40)) return UNIF_EUNSUPPORTED;
     } else {
         if ((int64_t)m.H > 16384) return UNIF_EUNSUPPORTED;
@@ -150,10 +163,13 @@ struct FwdPlan {
     size_t wsplit;
     size_t zero_begin, zero_end;  // bin_count, slab_count, totals, zero page
     size_t bin_count, slab_count, totals, zero_page;
-    size_t bin_cursor, slab_off, slab_cursor, seg_off, up_tile_off, down_tile_off;
-    size_t pair_token, pair_mask, pair_expert, pair_of, slab_rows, hbuf, part;
+    size_t bin_cursor, slab_off, seg_off, up_tile_off, down_tile_off, chunk_off, chunk_cnt;
+    size_t pair_token, pair_mask, pair_expert, pair_of, slab_rows, slab_tok, up_tile_info, up_tile_rows, hbuf, part;
+    size_t max_chunks;
     size_t total;
 };
+
+size_t ceil_div_sz(size_t a, size_t b) { return (a + b - 1) / b; }
 
 FwdPlan plan_forward(const Dims& m, bool own_record) {
     Carver cv;
@@ -175,7 +191,6 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.zero_end = cv.cur;
     p.bin_cursor = cv.take(4 * (size_t)m.nbin);
     p.slab_off = cv.take(4 * ((size_t)m.nslab + 1));
-    p.slab_cursor = cv.take(4 * (size_t)m.nslab);
     p.seg_off = cv.take(4 * (K1 + 1));
     p.up_tile_off = cv.take(4 * ((size_t)m.nslab + 1));
     p.down_tile_off = cv.take(4 * (K1 + 1));
@@ -183,8 +198,19 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.pair_mask = cv.take(8 * pmax);
     p.pair_expert = cv.take(4 * pmax);
     p.pair_of = cv.take(4 * N * K1);
-    p.slab_rows = cv.take(m.bf16 ? 4 * N * K * (size_t)m.B : 0);
-    p.hbuf = cv.take(m.bf16 ? pmax * (size_t)m.H * 2 : 0);
+    // Slab row lists: at most K B rows per token (b + k (B - b) <= K B), each
+    // slab padded to whole up tiles.
+    const size_t tm = (size_t)up_tm(m.M);
+    const size_t up_tiles = ceil_div_sz(N * K * (size_t)m.B, tm) + (size_t)m.nslab;
+    p.slab_rows = cv.take(m.bf16 ? 4 * up_tiles * tm : 0);
+    p.slab_tok = cv.take(m.bf16 ? 4 * up_tiles * tm : 0);
+    p.up_tile_info = cv.take(m.bf16 ? 4 * up_tiles : 0);
+    p.up_tile_rows = cv.take(m.bf16 ? 4 * up_tiles : 0);
+    // Ordered slab fill: chunks of kChunk pairs inside each expert segment.
+    p.max_chunks = ceil_div_sz(pmax, kChunk) + K1;
+    p.chunk_off = cv.take(m.bf16 ? 4 * (K1 + 1) : 0);
+    p.chunk_cnt = cv.take(m.bf16 ? 4 * p.max_chunks * (size_t)m.B : 0);
+    p.hbuf = cv.take(m.bf16 ? (pmax + 1) * (size_t)m.H * 2 : 0);  // + the sink row
     p.part = cv.take(pmax * (size_t)m.d * sizeof(float));
     p.total = cv.cur + 256;  // slack for aligning an unaligned base pointer
     return p;
@@ -417,7 +443,8 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.B = m.B;
     pp.key_bits = m.key_bits;
     const int down_bn = (m.d % kDownBNWide == 0) ? kDownBNWide : kDownBNNarrow;
-    pp.bm_up = kUpTM;
+    pp.bm_up = up_tm(m.M);
+    pp.up_group = kUpBlockGroup;
     pp.bm_down = kDownTM;
     pp.down_col_tiles = m.bf16 ? m.d / down_bn : 1;
     pp.mask = mask;
@@ -427,7 +454,6 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.bin_cursor = reinterpret_cast<int*>(ws + plan.bin_cursor);
     pp.slab_count = slab_count;
     pp.slab_off = reinterpret_cast<int*>(ws + plan.slab_off);
-    pp.slab_cursor = reinterpret_cast<int*>(ws + plan.slab_cursor);
     pp.seg_off = reinterpret_cast<int*>(ws + plan.seg_off);
     pp.up_tile_off = reinterpret_cast<int*>(ws + plan.up_tile_off);
     pp.down_tile_off = reinterpret_cast<int*>(ws + plan.down_tile_off);
@@ -437,6 +463,11 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.pair_expert = reinterpret_cast<int*>(ws + plan.pair_expert);
     pp.pair_of = reinterpret_cast<int*>(ws + plan.pair_of);
     pp.slab_rows = m.bf16 ? reinterpret_cast<int*>(ws + plan.slab_rows) : nullptr;
+    pp.slab_tok = m.bf16 ? reinterpret_cast<int*>(ws + plan.slab_tok) : nullptr;
+    pp.up_tile_info = m.bf16 ? reinterpret_cast<int*>(ws + plan.up_tile_info) : nullptr;
+    pp.up_tile_rows = m.bf16 ? reinterpret_cast<int*>(ws + plan.up_tile_rows) : nullptr;
+    pp.chunk_off = m.bf16 ? reinterpret_cast<int*>(ws + plan.chunk_off) : nullptr;
+    pp.chunk_cnt = m.bf16 ? reinterpret_cast<int*>(ws + plan.chunk_cnt) : nullptr;
     scan_kernel<<<1, kScanThreads, 0, st>>>(pp);
     UNIF_LAUNCH_CHECK();
     scatter_kernel<<<ceil_div(m.N, 256), 256, 0, st>>>(pp);
@@ -445,7 +476,13 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     const int cus = cu_count();
     void* part = ws + plan.part;
     if (m.bf16) {
-        slabfill_kernel<<<cus * 4, 256, 0, st>>>(pp);
+        up_tile_kernel<<<m.nslab, 256, 0, st>>>(pp);
+        UNIF_LAUNCH_CHECK();
+        chunk_count_kernel<<<(unsigned)plan.max_chunks, kChunk, 0, st>>>(pp);
+        UNIF_LAUNCH_CHECK();
+        chunk_scan_kernel<<<m.nslab, 256, 0, st>>>(pp);
+        UNIF_LAUNCH_CHECK();
+        slabfill_kernel<<<(unsigned)plan.max_chunks, kChunk, 0, st>>>(pp);
         UNIF_LAUNCH_CHECK();
         UNIF_MARK(2);
         // 4. block-sparse expert GEMMs
@@ -454,23 +491,24 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         up.M = m.M;
         up.B = m.B;
         up.H = m.H;
-        up.nslab = m.nslab;
+        up.x_bytes = (uint32_t)((size_t)m.N * m.d * 2);
+        up.w_bytes = (uint32_t)((size_t)m.K1 * m.H * m.d * 2);
         up.X = static_cast<const u16*>(X);
         up.Wup = static_cast<const u16*>(W_up);
         up.Hbuf = reinterpret_cast<u16*>(ws + plan.hbuf);
+        up.Hsink = up.Hbuf + (size_t)m.N * m.K1 * m.H;
         up.slab_rows = pp.slab_rows;
-        up.slab_off = pp.slab_off;
-        up.slab_count = slab_count;
-        up.up_tile_off = pp.up_tile_off;
+        up.slab_tok = pp.slab_tok;
+        up.tile_info = pp.up_tile_info;
+        up.tile_rows = pp.up_tile_rows;
         up.totals = totals;
-        up.pair_token = pp.pair_token;
-        const size_t up_lds = (size_t)up_lds_bytes(kUpTM, m.M, kUpRB, kUpNST);
+        const size_t up_lds = (size_t)up_lds_bytes(up_tm(m.M), m.M, kUpRB, kUpNST);
         const int grid = (kGemmOcc * cus / kXcds) * kXcds;
         switch (m.M / 32) {
             case 2: s = launch_persistent(up_kernel<2, kUpTM, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
             case 4: s = launch_persistent(up_kernel<4, kUpTM, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
             case 6: s = launch_persistent(up_kernel<6, kUpTM, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
-            case 8: s = launch_persistent(up_kernel<8, kUpTM, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
+            case 8: s = launch_persistent(up_kernel<8, kUpTMWide, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
             default: return UNIF_EUNSUPPORTED;
         }
         if (s != UNIF_OK) return s;
