@@ -81,7 +81,15 @@ __device__ __forceinline__ int ld_uniform(const int* p) {
     return *(const __attribute__((address_space(4))) int*)p;
 }
 
+__device__ __forceinline__ uint64_t ld_uniform64(const uint64_t* p) {
+    return *(const __attribute__((address_space(4))) uint64_t*)p;
+}
+
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int mask) {
+    const uint32_t lo = __shfl_xor((uint32_t)v, mask), hi = __shfl_xor((uint32_t)(v >> 32), mask);
+    return ((uint64_t)hi << 32) | lo;
+}
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 __device__ __forceinline__ uint64_t lanes_below() {
     return (lane_id() == 0) ? 0ull : (~0ull >> (kWave - lane_id()));
@@ -105,6 +113,12 @@ __device__ __forceinline__ int upper_index(const int* off, int n, int x) {
 // is the same for the whole wave. Completion is tracked by vmcnt only.
 __device__ __forceinline__ void dma16(const void* gsrc, void* lds_base) {
     __builtin_amdgcn_global_load_lds(gsrc, lds_base, 16, 0, 0);
+}
+
+// Same with 4 bytes per lane (lane l writes lds_base + 4 l); only 4-byte
+// alignment is needed.
+__device__ __forceinline__ void dma4(const void* gsrc, void* lds_base) {
+    __builtin_amdgcn_global_load_lds(gsrc, lds_base, 4, 0, 0);
 }
 
 // Buffer resource over [base, base + bytes): raw (unstructured) 32-bit

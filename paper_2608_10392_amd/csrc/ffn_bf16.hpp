@@ -66,15 +66,17 @@ struct UpParams {
 };
 
 struct DownParams {
-    int d, M, B, H, K1;
+    int d, M, B, H, ncol;        // ncol: column tiles per row tile
+    uint32_t w_bytes;            // size of W_down (below 4 GiB)
     const u16* Hbuf;
     const u16* Wdown;
-    const u16* zero16;   // 16 zero bytes in device memory
     float* part;
-    const int* seg_off;
-    const int* down_tile_off;
-    const int* totals;
-    const uint64_t* pair_mask;
+    float* part_sink;            // one d row that absorbs the stores of unused tile rows
+    const int4* rt_info;         // per row tile: first pair, rows, expert
+    const uint64_t* rt_masks;    // per row tile: block-mask union of each 16-row group, then of the tile
+    const uint64_t* pair_mask;   // readable for a whole tile past the last pair
+    const int* tiles;            // per down tile: row tile << 8 | column tile
+    const int* totals;           // [2]: down tiles
 };
 
 // Staged-row geometry: RB bytes per row, K = RB/2 bf16 per stage.
@@ -98,10 +100,10 @@ __device__ __forceinline__ int group_col(int g, int m) {
     return 32 * (g >> 1) + 8 * (m >> 2) + (m & 3) + 4 * (g & 1);
 }
 
-// Dynamic LDS bytes of the two kernels: the stage ring; for up also the
-// row lists (tokens, pairs) of the current and the next tile.
+// Dynamic LDS bytes of the two kernels: the stage ring, plus the row lists
+// of the current and the next tile (up: tokens and pairs; down: block masks).
 __host__ __device__ constexpr int up_lds_bytes(int TM, int M, int RB, int NST) { return NST * (TM + M) * RB + 16 * TM; }
-__host__ __device__ constexpr int down_lds_bytes(int TM, int BN, int RB, int NST) { return NST * (TM + BN) * RB; }
+__host__ __device__ constexpr int down_lds_bytes(int TM, int BN, int RB, int NST) { return NST * (TM + BN) * RB + 16 * TM; }
 
 // Tile handled by this workgroup in persistent round `round`: a contiguous
 // range of tiles per XCD. gridDim.x is a multiple of kXcds.
@@ -110,28 +112,17 @@ __device__ __forceinline__ int xcd_tile(int round) {
     return round * gridDim.x + (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
 }
 
-// Wait for stage s of n given that stages up to min(n-1, s+NST-2) were
-// issued, L loads per stage per wave; then make it visible to all waves.
-template <int L, int NST>
-__device__ __forceinline__ void stage_ready(int s, int n) {
-    const int ahead = min(n - 1 - s, NST - 2);
-    if (NST >= 4 && ahead >= 2) wait_vmcnt<(NST >= 4 ? 2 * L : 0)>();
-    else if (NST >= 3 && ahead >= 1) wait_vmcnt<(NST >= 3 ? L : 0)>();
-    else wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-}
-
 // Wait until at most n vector-memory operations of this wave are pending,
 // for the few counts the GEMM pipelines use (anything else waits for all).
-template <int L, int E>
+template <int L, int E, int F>
 __device__ __forceinline__ void wait_vm_after(int n) {
     if (n == L) wait_vmcnt<L>();
-    else if (n == L + 1) wait_vmcnt<L + 1>();
+    else if (n == L + F) wait_vmcnt<L + F>();
     else if (n == L + E) wait_vmcnt<L + E>();
-    else if (n == L + E + 1) wait_vmcnt<L + E + 1>();
+    else if (n == L + E + F) wait_vmcnt<L + E + F>();
     else if (n == E) wait_vmcnt<E>();
-    else if (n == E + 1) wait_vmcnt<E + 1>();
-    else if (n == 1) wait_vmcnt<1>();
+    else if (n == E + F) wait_vmcnt<E + F>();
+    else if (n == F) wait_vmcnt<F>();
     else wait_vmcnt<0>();
 }
 
@@ -165,7 +156,8 @@ void up_kernel(UpParams p) {
     static_assert(LA >= 1 && LB >= 1, "tile too small for one copy per wave");
     static_assert(TM * 4 <= 32 * 16, "a row list must fit one half-wave copy");
     static_assert(NST == 3, "the wait accounting is written for a 3-stage ring");
-    static_assert(L + NEPI + 1 < 64, "vmcnt range");
+    constexpr int NFETCH = 1;                         // copies per wave for a tile's row lists
+    static_assert(L + NEPI + NFETCH < 64, "vmcnt range");
     extern __shared__ __attribute__((aligned(16))) char lds_up[];
     // rows[par][0] tokens, rows[par][1] pairs of the tile with parity par
     int* rows = reinterpret_cast<int*>(lds_up + RING);
@@ -280,8 +272,8 @@ void up_kernel(UpParams p) {
         auto step = [&](auto first, int s, u32x4 (&A)[RG], u32x4 (&Bw)[MW], u32x4 (&A2)[RG],
                         u32x4 (&B2)[MW]) {
             if constexpr (decltype(first)::value) {
-                const int n_after = L + (after_epi ? NEPI : 0) + ((s == 1 && has_next) ? 1 : 0);
-                wait_vm_after<L, NEPI>(n_after);
+                const int n_after = L + (after_epi ? NEPI : 0) + ((s == 1 && has_next) ? NFETCH : 0);
+                wait_vm_after<L, NEPI, NFETCH>(n_after);
             } else {
                 wait_vmcnt<L>();
             }
@@ -359,137 +351,234 @@ void up_kernel(UpParams p) {
     wait_vmcnt<0>();
 }
 
+// Down-projection on the same engine as the up kernel (ring of buffer
+// loads, fragments read one stage ahead, pipelined across tiles). A tile is
+// TM consecutive pairs of one expert x BN output columns; its stages walk
+// the blocks of the tile's mask union, M/32 stages per block. A row whose
+// mask lacks the stage's block reads zeros (an out-of-range offset), and a
+// 16-row MFMA group whose rows all lack it skips its MFMAs. Tiles with fewer
+// than NST + 1 stages are padded with empty stages (no MFMAs), so the ring
+// never runs more than one tile ahead.
 template <int NW, int TM, int RB, int NST, int OCC>
 __global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
 void down_kernel(DownParams p) {
     using S = Stage<RB>;
+    static_assert(S::KSTEPS == 1, "one MFMA k step per stage");
     constexpr int BN = NW * 32;
-    constexpr int RG = TM / 32;
+    constexpr int RG = TM / 32;                       // MFMA row groups per wave
+    constexpr int G = TM / 16;                        // 16-row groups per tile
     constexpr int LA = TM / S::ROWS_PER_DMA / 4;
     constexpr int LB = BN / S::ROWS_PER_DMA / 4;
-    constexpr int A_BYTES = TM * RB, STAGE = (TM + BN) * RB;
-    static_assert(LA >= 1 && LB >= 1, "tile too small for one DMA per wave");
+    constexpr int L = LA + LB;
+    constexpr int NEPI = RG * NW;                     // epilogue stores per wave
+    constexpr int A_BYTES = TM * RB, STAGE = (TM + BN) * RB, RING = NST * STAGE;
+    static_assert(LA >= 1 && LB >= 1, "tile too small for one copy per wave");
+    constexpr int NFETCH = TM * 8 / 256;              // 4-byte copies per wave for a tile's row masks
+    static_assert(NST == 3, "the wait accounting is written for a 3-stage ring");
+    static_assert(L + NEPI + NFETCH < 64, "vmcnt range");
     extern __shared__ __attribute__((aligned(16))) char lds_dn[];
-    __shared__ uint64_t row_mask[TM];
-    __shared__ uint64_t sub_mask[TM / 16];
-    __shared__ int blist[64];
-    __shared__ int nblocks;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    uint64_t* rmask = reinterpret_cast<uint64_t*>(lds_dn + RING);   // [2][TM]
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
-    const int ncol = p.d / BN;
-    const int kc_per_block = p.M / S::SK;
-    const int n_tiles = p.totals[2];
-    for (int round = 0; round * (int)gridDim.x < n_tiles; ++round) {
-        const int tile = xcd_tile(round);
-        if (tile >= n_tiles) continue;
-        const int e = upper_index(p.down_tile_off, p.K1, tile);
-        const int local = tile - p.down_tile_off[e];
-        const int rt = local / ncol, ct = local - rt * ncol;
-        const int p0 = p.seg_off[e] + rt * TM;
-        const int nrows = min(TM, p.seg_off[e + 1] - p0);
-        const int n0 = ct * BN;
-        wait_vmcnt<0>();          // previous tile's stores are done
-        __syncthreads();
-        for (int t = tid; t < TM; t += kFfnThreads) row_mask[t] = (t < nrows) ? p.pair_mask[p0 + t] : 0ull;
-        __syncthreads();
-        if (tid < TM / 16) {
-            uint64_t m = 0;
-            for (int r = 0; r < 16; ++r) m |= row_mask[tid * 16 + r];
-            sub_mask[tid] = m;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            uint64_t m = 0;
-            for (int g = 0; g < TM / 16; ++g) m |= sub_mask[g];
-            int n = 0;
-            for (int cc = 0; cc < p.B; ++cc)
-                if ((m >> cc) & 1ull) blist[n++] = cc;
-            nblocks = n;
-        }
-        __syncthreads();
-        // Block masks of this wave's 16-row groups, as scalars (wave-uniform).
-        uint32_t wsub_lo[RG], wsub_hi[RG];
+    const int n_tiles = ld_uniform(p.totals + 2);
+    const int kcpb = p.M / S::SK;   // stages per block (even: M is a multiple of 64)
+    int tile = xcd_tile(0);
+    if (tile >= n_tiles) return;
+
+    const int lr = lane & 15, lg = lane >> 4;
+    const uint32_t fa = S::off(wm * (TM / 2) + lr, lg);
+    const uint32_t fb = A_BYTES + S::off(wn * (BN / 2) + lr, lg);
+    const uint32_t hrow = (uint32_t)p.H * 2;
+    const rsrc_t wr = make_rsrc(p.Wdown, p.w_bytes);
+    uint32_t voffB[LB], vA[LA];
+    int rA[LA];
 #pragma unroll
-        for (int i = 0; i < RG; ++i) {
-            const uint64_t m = sub_mask[wm * RG + i];
-            wsub_lo[i] = __builtin_amdgcn_readfirstlane((uint32_t)m);
-            wsub_hi[i] = __builtin_amdgcn_readfirstlane((uint32_t)(m >> 32));
+    for (int j = 0; j < LB; ++j) {
+        int r, ch;
+        S::slot((wave * LB + j) * S::ROWS_PER_DMA, lane, r, ch);
+        voffB[j] = (uint32_t)group_col(r >> 4, r & 15) * hrow + ch * 16;
+    }
+#pragma unroll
+    for (int j = 0; j < LA; ++j) {
+        int ch;
+        S::slot((wave * LA + j) * S::ROWS_PER_DMA, lane, rA[j], ch);
+        vA[j] = (uint32_t)rA[j] * hrow + ch * 16;
+    }
+
+    // Uniform description of a tile.
+    struct Desc {
+        int p0, nrows, e, ct, nst, nreal;
+        uint64_t all, gm[RG];
+    };
+    auto describe = [&](int t) {
+        Desc D;
+        const int rc = ld_uniform(p.tiles + t);
+        const int rt = rc >> 8;
+        D.ct = rc & 255;
+        const int* inf = reinterpret_cast<const int*>(p.rt_info + rt);
+        D.p0 = ld_uniform(inf);
+        D.nrows = ld_uniform(inf + 1);
+        D.e = ld_uniform(inf + 2);
+        const uint64_t* ms = p.rt_masks + (size_t)rt * (G + 1);
+        D.all = ld_uniform64(ms + G);
+#pragma unroll
+        for (int i = 0; i < RG; ++i) D.gm[i] = ld_uniform64(ms + wm * RG + i);
+        D.nreal = __popcll(D.all) * kcpb;
+        D.nst = max(D.nreal, NST + 1);
+        return D;
+    };
+    // A tile's row masks (TM u64) are copied to LDS by every wave, in
+    // 4-byte pieces (a tile's first pair can be any index).
+    auto fetch_masks = [&](Desc D, int par) {
+        const uint32_t* src = reinterpret_cast<const uint32_t*>(p.pair_mask + D.p0);
+#pragma unroll
+        for (int q = 0; q < NFETCH; ++q) dma4(src + q * 64 + lane, rmask + par * TM + q * 32);
+    };
+
+    // Issue side: the tile whose stages are being copied.
+    rsrc_t hr = make_rsrc(p.Hbuf, 0);
+    uint64_t mrow[LA];
+    uint32_t wbase = 0;
+    uint64_t rem_w = 0;
+    int cb_w = 0, kc_w = 0, st_w = 0, nreal_w = 0;
+    auto issue_tile = [&](Desc D, int par) {
+        hr = make_rsrc(p.Hbuf + (size_t)D.p0 * p.H, (uint32_t)TM * hrow);
+#pragma unroll
+        for (int j = 0; j < LA; ++j) mrow[j] = (rA[j] < D.nrows) ? rmask[par * TM + rA[j]] : 0ull;
+        wbase = ((uint32_t)D.e * (uint32_t)p.d + (uint32_t)D.ct * BN) * hrow;
+        rem_w = D.all;
+        cb_w = rem_w ? __builtin_ctzll(rem_w) : 0;
+        kc_w = 0;
+        st_w = 0;
+        nreal_w = D.nreal;
+    };
+    int slot_w = 0, slot_r = 0, issued = 0;
+    auto issue = [&]() {
+        char* base = lds_dn + slot_w * STAGE;
+        const bool real = st_w < nreal_w;
+        const uint32_t soff = (uint32_t)(cb_w * p.M + kc_w * S::SK) * 2;
+#pragma unroll
+        for (int j = 0; j < LA; ++j)
+            dma16(hr, (real && ((mrow[j] >> cb_w) & 1ull)) ? vA[j] : kOutOfRange, soff, base + (wave * LA + j) * 1024);
+#pragma unroll
+        for (int j = 0; j < LB; ++j) dma16(wr, voffB[j], wbase + soff, base + A_BYTES + (wave * LB + j) * 1024);
+        slot_w = (slot_w == NST - 1) ? 0 : slot_w + 1;
+        ++issued;
+        ++st_w;
+        if (++kc_w == kcpb) {
+            kc_w = 0;
+            rem_w &= rem_w - 1;
+            cb_w = rem_w ? __builtin_ctzll(rem_w) : 0;
         }
-        // Per-lane sources: A rows are pairs p0 + r (or the zero page when the
-        // row's mask lacks the stage's block), B rows are output columns n0 + r.
-        const u16* srcA[LA];
-        uint64_t mA[LA];
-        const u16* srcB[LB];
-        const u16* W = p.Wdown + ((size_t)e * p.d + n0) * p.H;
+    };
+    u32x4 a0[RG], b0[NW], a1[RG], b1[NW];
+    auto load_frags = [&](u32x4 (&A)[RG], u32x4 (&Bw)[NW]) {
+        const char* st = lds_dn + slot_r * STAGE;
 #pragma unroll
-        for (int j = 0; j < LA; ++j) {
-            int r, ch;
-            S::slot((wave * LA + j) * S::ROWS_PER_DMA, lane, r, ch);
-            srcA[j] = p.Hbuf + (size_t)(p0 + r) * p.H + ch * 8;
-            mA[j] = row_mask[r];
-        }
+        for (int j = 0; j < NW; ++j) Bw[j] = ld16(st + fb + j * 16 * RB);
 #pragma unroll
-        for (int j = 0; j < LB; ++j) {
-            int r, ch;
-            S::slot((wave * LB + j) * S::ROWS_PER_DMA, lane, r, ch);
-            srcB[j] = W + (size_t)group_col(r >> 4, r & 15) * p.H + ch * 8;
-        }
-        const int nst = nblocks * kc_per_block;
-        auto issue = [&](int st) {
-            char* base = lds_dn + (st % NST) * STAGE;
-            const int cb = blist[st / kc_per_block];
-            const int col = cb * p.M + (st - (st / kc_per_block) * kc_per_block) * S::SK;
-#pragma unroll
-            for (int j = 0; j < LA; ++j) {
-                const u16* src = ((mA[j] >> cb) & 1ull) ? srcA[j] + col : p.zero16;
-                dma16(src, base + (wave * LA + j) * 1024);
-            }
-#pragma unroll
-            for (int j = 0; j < LB; ++j) dma16(srcB[j] + col, base + A_BYTES + (wave * LB + j) * 1024);
-        };
-        f32x4 acc[RG][NW];
+        for (int i = 0; i < RG; ++i) A[i] = ld16(st + fa + i * 16 * RB);
+        slot_r = (slot_r == NST - 1) ? 0 : slot_r + 1;
+    };
+    f32x4 acc[RG][NW];
+
+    int par = 0;
+    Desc cur = describe(tile);
+    fetch_masks(cur, 0);
+    wait_vmcnt<0>();
+    __syncthreads();
+    issue_tile(cur, 0);
+    for (int q = 0; q < NST; ++q) issue();
+    wait_vmcnt<(NST - 1) * L>();
+    __builtin_amdgcn_s_barrier();
+    load_frags(a0, b0);
+    wait_lgkmcnt0();
+    bool after_epi = false;
+    for (int round = 0;; ++round) {
+        const int next = xcd_tile(round + 1);
+        const bool has_next = next < n_tiles;
+        Desc nxt;
+        if (has_next) nxt = describe(next);
 #pragma unroll
         for (int i = 0; i < RG; ++i)
 #pragma unroll
             for (int j = 0; j < NW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int st = 0; st < NST - 1 && st < nst; ++st) issue(st);
-        for (int st = 0; st < nst; ++st) {
-            stage_ready<LA + LB, NST>(st, nst);
-            if (st + NST - 1 < nst) issue(st + NST - 1);
-            const int cb = __builtin_amdgcn_readfirstlane(blist[st / kc_per_block]);
-            const char* As = lds_dn + (st % NST) * STAGE;
-            const char* Bs = As + A_BYTES;
+        // Read side: block and stage of the stage in registers.
+        uint64_t rem_r = cur.all;
+        int cb_r = rem_r ? __builtin_ctzll(rem_r) : 0, kc_r = 0;
+        const int nst = cur.nst;
+        // Same step as the up kernel; the MFMAs of a row group run only if
+        // one of its rows uses the stage's block.
+        auto step = [&](auto first, int s, u32x4 (&A)[RG], u32x4 (&Bw)[NW], u32x4 (&A2)[RG],
+                        u32x4 (&B2)[NW]) {
+            if constexpr (decltype(first)::value) {
+                const int n_after = L + (after_epi ? NEPI : 0) + ((s == 1 && has_next) ? NFETCH : 0);
+                wait_vm_after<L, NEPI, NFETCH>(n_after);
+            } else {
+                wait_vmcnt<L>();
+            }
+            __builtin_amdgcn_s_barrier();
+            if (s == 0 && has_next) fetch_masks(nxt, par ^ 1);
+            if (s + NST == nst) {
+                // From here on the stages issued belong to the next tile (or,
+                // past the last tile, re-read this tile's first stages into
+                // the free slot). The next tile's row masks were copied at
+                // s == 0, before stage NST, waited for when s >= NST - 1.
+                if (has_next && s < NST - 1) {
+                    wait_vmcnt<0>();
+                    __builtin_amdgcn_s_barrier();
+                }
+                Desc D = cur;
+                if (has_next) D = nxt;
+                issue_tile(D, has_next ? par ^ 1 : par);
+            }
+            issue();
+            load_frags(A2, B2);
+            const bool real = s < cur.nreal;
 #pragma unroll
-            for (int kk = 0; kk < S::KSTEPS; ++kk) {
-                bf16x8 bw[NW];
+            for (int i = 0; i < RG; ++i) {
+                if (real && ((cur.gm[i] >> cb_r) & 1ull)) {
 #pragma unroll
-                for (int j = 0; j < NW; ++j)
-                    bw[j] = as_bf16x8(ld16(Bs + S::off(wn * (BN / 2) + j * 16 + (lane & 15), kk * 4 + (lane >> 4))));
-#pragma unroll
-                for (int i = 0; i < RG; ++i) {
-                    if ((((cb < 32) ? wsub_lo[i] >> cb : wsub_hi[i] >> (cb - 32)) & 1u) != 0u) {
-                        const bf16x8 af = as_bf16x8(
-                            ld16(As + S::off(wm * (TM / 2) + i * 16 + (lane & 15), kk * 4 + (lane >> 4))));
-#pragma unroll
-                        for (int j = 0; j < NW; ++j) acc[i][j] = mfma16x16x32(bw[j], af, acc[i][j]);
-                    }
+                    for (int j = 0; j < NW; ++j)
+                        acc[i][j] = mfma16x16x32(as_bf16x8(Bw[j]), as_bf16x8(A[i]), acc[i][j]);
                 }
             }
+            if (++kc_r == kcpb) {
+                kc_r = 0;
+                rem_r &= rem_r - 1;
+                cb_r = rem_r ? __builtin_ctzll(rem_r) : 0;
+            }
+            // The fragments just read must be in registers before the next
+            // barrier lets another wave refill their slot.
             wait_lgkmcnt0();
+        };
+        step(std::true_type{}, 0, a0, b0, a1, b1);
+        step(std::true_type{}, 1, a1, b1, a0, b0);
+        for (int s = 2; s < nst; s += 2) {
+            step(std::false_type{}, s, a0, b0, a1, b1);
+            step(std::false_type{}, s + 1, a1, b1, a0, b0);
         }
         // fp32 per-expert rows; lane stores 8 consecutive columns of its row.
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
-            const int row = wm * (TM / 2) + i * 16 + (lane & 15);
-            if (row >= nrows) continue;
-            float* dst = p.part + (size_t)(p0 + row) * p.d + n0 + wn * (BN / 2) + 8 * (lane >> 4);
+            const int r = wm * (TM / 2) + i * 16 + lr;
+            float* dst = (r < cur.nrows) ? p.part + (size_t)(cur.p0 + r) * p.d + (size_t)cur.ct * BN : p.part_sink;
+            dst += wn * (BN / 2) + 8 * lg;
 #pragma unroll
             for (int J = 0; J < NW / 2; ++J) {
                 st16(dst + 32 * J, __builtin_bit_cast(u32x4, acc[i][2 * J]));
                 st16(dst + 32 * J + 4, __builtin_bit_cast(u32x4, acc[i][2 * J + 1]));
             }
         }
+        if (!has_next) break;
+        cur = nxt;
+        par ^= 1;
+        after_epi = true;
     }
+    // The re-reads issued past the last tile land in LDS: let them finish
+    // before the workgroup's LDS is released.
+    wait_vmcnt<0>();
 }
 
 }  // namespace unifmoe

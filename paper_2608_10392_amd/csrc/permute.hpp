@@ -43,8 +43,8 @@ struct PermuteParams {
     int* slab_off;
     int* seg_off;
     int* up_tile_off;
-    int* down_tile_off;
-    int* totals;  // [0] pairs P, [1] up-projection tiles, [2] down-projection tiles
+    int* down_tile_off;  // [K+2] first down row tile of each expert segment
+    int* totals;  // [0] pairs P, [1] up tiles, [2] down tiles, [3] fill chunks, [4] down row tiles
     int* pair_token;
     uint64_t* pair_mask;
     int* pair_expert;
@@ -55,6 +55,9 @@ struct PermuteParams {
     int* up_tile_rows;  // per up tile: first entry in slab_rows / slab_tok
     int* chunk_off;     // [K+2] first chunk of each expert's pair segment
     int* chunk_cnt;     // [chunks][B] pairs per block, then (scanned) first slab row
+    int4* rt_info;      // per down row tile: first pair, rows, expert
+    uint64_t* rt_masks; // per down row tile: mask union of each 16-row group, then of the tile
+    int* down_tiles;    // per down tile: row tile << 8 | column tile
 };
 
 __global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n) {
@@ -121,12 +124,13 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
         int run = 0;
         for (int e = 0; e < K1; ++e) {
             p.down_tile_off[e] = run;
-            run += ceil_div(p.seg_off[e + 1] - p.seg_off[e], p.bm_down) * p.down_col_tiles;
+            run += ceil_div(p.seg_off[e + 1] - p.seg_off[e], p.bm_down);
         }
         p.down_tile_off[K1] = run;
         p.totals[0] = P;
         p.totals[1] = nup;
-        p.totals[2] = run;
+        p.totals[2] = run * p.down_col_tiles;
+        p.totals[4] = run;
     }
 }
 
@@ -177,6 +181,38 @@ __global__ __launch_bounds__(256) void up_tile_kernel(PermuteParams p) {
         p.up_tile_info[pos] = sl | (min(bm, cnt - j * bm) << 16);
         p.up_tile_rows[pos] = p.slab_off[sl] + j * bm;
     }
+}
+
+// Down row tiles: bm_down consecutive pairs of one expert segment. One wave
+// per row tile records its first pair, row count and expert, and the union
+// of the block masks of each 16-row group and of the whole tile. Down tiles
+// (row tile x column tile of d) are listed expert by expert, column tile
+// outer: the tiles that run together read one column slice of the expert's
+// V, which then stays in L2.
+__global__ __launch_bounds__(64) void down_rowtile_kernel(PermuteParams p) {
+    const int rt = blockIdx.x;
+    if (rt >= p.totals[4]) return;
+    const int e = upper_index(p.down_tile_off, p.K + 1, rt);
+    const int p0 = p.seg_off[e] + (rt - p.down_tile_off[e]) * p.bm_down;
+    const int nrows = min(p.bm_down, p.seg_off[e + 1] - p0);
+    const int lane = threadIdx.x, G = p.bm_down / 16;
+    uint64_t* out = p.rt_masks + (size_t)rt * (G + 1);
+    uint64_t all = 0;
+    for (int h = 0; h * 64 < p.bm_down; ++h) {
+        const int r = h * 64 + lane;
+        uint64_t m = r < nrows ? p.pair_mask[p0 + r] : 0ull;
+        for (int o = 1; o < 16; o <<= 1) m |= shfl_xor64(m, o);
+        if ((lane & 15) == 0) out[h * 4 + (lane >> 4)] = m;
+        all |= m;
+    }
+    for (int o = 16; o < 64; o <<= 1) all |= shfl_xor64(all, o);
+    if (lane == 0) {
+        out[G] = all;
+        p.rt_info[rt] = make_int4(p0, nrows, e, 0);
+    }
+    const int r0 = p.down_tile_off[e], nrt = p.down_tile_off[e + 1] - r0;
+    for (int ct = lane; ct < p.down_col_tiles; ct += 64)
+        p.down_tiles[(size_t)r0 * p.down_col_tiles + (size_t)ct * nrt + (rt - r0)] = (rt << 8) | ct;
 }
 
 // Chunk q of expert e covers pairs [seg_off[e] + (q - chunk_off[e]) kChunk, ...)

@@ -50,7 +50,7 @@ constexpr int kUpTMWide = 64;  // M = 256: half-height tiles keep the registers 
 int up_tm(int M) { return M > 192 ? kUpTMWide : kUpTM; }
 constexpr int kDownTM = 128;
 constexpr int kDownBNWide = 256, kDownWideRB = 64, kDownWideNST = 3;
-constexpr int kDownBNNarrow = 128, kDownNarrowRB = 128, kDownNarrowNST = 2;
+constexpr int kDownBNNarrow = 128, kDownNarrowRB = 64, kDownNarrowNST = 3;
 static_assert(kGemmOcc * up_lds_bytes(kUpTM, 256, kUpRB, kUpNST) <= 160 * 1024, "up ring exceeds LDS");
 // The up kernel's pipeline needs at least 2 NST - 2 stages per tile; the
 // smallest supported d (128) gives 128 / (RB / 2).
@@ -128,6 +128,9 @@ int32_t check_forward_shape(const unif_moe_config* c) {
         // buffer offsets.
         if ((uint64_t)m.N * m.d * 2 >= kOutOfRange || (uint64_t)m.K1 * m.H * m.d * 2 >= kOutOfRange)
             return UNIF_EUNSUPPORTED;
+        // Down tiles are encoded as row tile << 8 | column tile.
+        if (m.d / kDownBNNarrow > 255 || (int64_t)m.N * m.K1 / kDownTM + m.K1 >= ((int64_t)1 << 23))
+            return UNIF_EUNSUPPORTED;
         if ((int64_t)m.H * m.d * 2 > ((int64_t)1 << 40)) return UNIF_EUNSUPPORTED;
     } else {
         if ((int64_t)m.H > 16384) return UNIF_EUNSUPPORTED;
@@ -162,10 +165,10 @@ struct FwdPlan {
     size_t alpha, nsh, mask, nres, eids, wts;
     size_t wsplit;
     size_t zero_begin, zero_end;  // bin_count, slab_count, totals, zero page
-    size_t bin_count, slab_count, totals, zero_page;
+    size_t bin_count, slab_count, totals;
     size_t bin_cursor, slab_off, seg_off, up_tile_off, down_tile_off, chunk_off, chunk_cnt;
     size_t pair_token, pair_mask, pair_expert, pair_of, slab_rows, slab_tok, up_tile_info, up_tile_rows, hbuf, part;
-    size_t max_chunks;
+    size_t max_chunks, max_row_tiles, rt_info, rt_masks, down_tiles;
     size_t total;
 };
 
@@ -186,8 +189,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.bin_count = cv.take(4 * (size_t)m.nbin);
     p.zero_begin = p.bin_count;
     p.slab_count = cv.take(4 * (size_t)m.nslab);
-    p.totals = cv.take(4 * 4);
-    p.zero_page = cv.take(256);
+    p.totals = cv.take(4 * 8);
     p.zero_end = cv.cur;
     p.bin_cursor = cv.take(4 * (size_t)m.nbin);
     p.slab_off = cv.take(4 * ((size_t)m.nslab + 1));
@@ -195,7 +197,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.up_tile_off = cv.take(4 * ((size_t)m.nslab + 1));
     p.down_tile_off = cv.take(4 * (K1 + 1));
     p.pair_token = cv.take(4 * pmax);
-    p.pair_mask = cv.take(8 * pmax);
+    p.pair_mask = cv.take(8 * (pmax + kDownTM));   // a whole down tile is readable past the last pair
     p.pair_expert = cv.take(4 * pmax);
     p.pair_of = cv.take(4 * N * K1);
     // Slab row lists: at most K B rows per token (b + k (B - b) <= K B), each
@@ -211,7 +213,11 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.chunk_off = cv.take(m.bf16 ? 4 * (K1 + 1) : 0);
     p.chunk_cnt = cv.take(m.bf16 ? 4 * p.max_chunks * (size_t)m.B : 0);
     p.hbuf = cv.take(m.bf16 ? (pmax + 1) * (size_t)m.H * 2 : 0);  // + the sink row
-    p.part = cv.take(pmax * (size_t)m.d * sizeof(float));
+    p.part = cv.take((pmax + 1) * (size_t)m.d * sizeof(float));   // + the sink row
+    p.max_row_tiles = ceil_div_sz(pmax, kDownTM) + K1;
+    p.rt_info = cv.take(m.bf16 ? 16 * p.max_row_tiles : 0);
+    p.rt_masks = cv.take(m.bf16 ? 8 * (kDownTM / 16 + 1) * p.max_row_tiles : 0);
+    p.down_tiles = cv.take(m.bf16 ? 4 * p.max_row_tiles * (size_t)(m.d / kDownBNNarrow) : 0);
     p.total = cv.cur + 256;  // slack for aligning an unaligned base pointer
     return p;
 }
@@ -468,6 +474,9 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.up_tile_rows = m.bf16 ? reinterpret_cast<int*>(ws + plan.up_tile_rows) : nullptr;
     pp.chunk_off = m.bf16 ? reinterpret_cast<int*>(ws + plan.chunk_off) : nullptr;
     pp.chunk_cnt = m.bf16 ? reinterpret_cast<int*>(ws + plan.chunk_cnt) : nullptr;
+    pp.rt_info = m.bf16 ? reinterpret_cast<int4*>(ws + plan.rt_info) : nullptr;
+    pp.rt_masks = m.bf16 ? reinterpret_cast<uint64_t*>(ws + plan.rt_masks) : nullptr;
+    pp.down_tiles = m.bf16 ? reinterpret_cast<int*>(ws + plan.down_tiles) : nullptr;
     scan_kernel<<<1, kScanThreads, 0, st>>>(pp);
     UNIF_LAUNCH_CHECK();
     scatter_kernel<<<ceil_div(m.N, 256), 256, 0, st>>>(pp);
@@ -477,6 +486,8 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     void* part = ws + plan.part;
     if (m.bf16) {
         up_tile_kernel<<<m.nslab, 256, 0, st>>>(pp);
+        UNIF_LAUNCH_CHECK();
+        down_rowtile_kernel<<<(unsigned)plan.max_row_tiles, 64, 0, st>>>(pp);
         UNIF_LAUNCH_CHECK();
         chunk_count_kernel<<<(unsigned)plan.max_chunks, kChunk, 0, st>>>(pp);
         UNIF_LAUNCH_CHECK();
@@ -518,15 +529,17 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         dn.M = m.M;
         dn.B = m.B;
         dn.H = m.H;
-        dn.K1 = m.K1;
+        dn.ncol = pp.down_col_tiles;
+        dn.w_bytes = up.w_bytes;
         dn.Hbuf = up.Hbuf;
         dn.Wdown = static_cast<const u16*>(W_down);
         dn.part = static_cast<float*>(part);
-        dn.zero16 = reinterpret_cast<const u16*>(ws + plan.zero_page);
-        dn.seg_off = pp.seg_off;
-        dn.down_tile_off = pp.down_tile_off;
-        dn.totals = totals;
+        dn.part_sink = dn.part + (size_t)m.N * m.K1 * m.d;
+        dn.rt_info = pp.rt_info;
+        dn.rt_masks = pp.rt_masks;
         dn.pair_mask = pp.pair_mask;
+        dn.tiles = pp.down_tiles;
+        dn.totals = totals;
         if (down_bn == kDownBNWide)
             s = launch_persistent(down_kernel<kDownBNWide / 32, kDownTM, kDownWideRB, kDownWideNST, kGemmOcc>, grid,
                                   (size_t)down_lds_bytes(kDownTM, kDownBNWide, kDownWideRB, kDownWideNST), st, dn);
