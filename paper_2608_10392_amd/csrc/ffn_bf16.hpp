@@ -53,7 +53,6 @@ constexpr int kXcds = 8;
 
 struct UpParams {
     int d, M, B, H;
-    uint32_t x_bytes, w_bytes;   // sizes of X and W_up (each below 4 GiB)
     const u16* X;
     const u16* Wup;
     u16* Hbuf;
@@ -67,8 +66,8 @@ struct UpParams {
 
 struct DownParams {
     int d, M, B, H, ncol;        // ncol: column tiles per row tile
-    uint32_t w_bytes;            // size of W_down (below 4 GiB)
     const u16* Hbuf;
+    const u16* zero16;           // 16 zero bytes: the source of rows that lack a block
     const u16* Wdown;
     float* part;
     float* part_sink;            // one d row that absorbs the stores of unused tile rows
@@ -175,12 +174,11 @@ void up_kernel(UpParams p) {
     const int lr = lane & 15, lg = lane >> 4;
     const uint32_t fa = S::off(wm * (TM / 2) + lr, lg);
     const uint32_t fb = A_BYTES + S::off(wn * (M / 2) + lr, lg);
-    // Copy sources: buffer loads with per-lane offsets fixed for a tile and
-    // the k position (and the weight slab) in the scalar offset. Token rows
-    // past the tile's count read zeros.
+    // Copy sources: per-lane addresses fixed for a tile, plus the k position
+    // (and, for weights, the slab) as a uniform byte offset. Token rows past
+    // the tile's count read token 0; their results go to the sink row.
     const uint32_t row_bytes = (uint32_t)p.d * 2;
-    const rsrc_t xr = make_rsrc(p.X, p.x_bytes);
-    const rsrc_t wr = make_rsrc(p.Wup, p.w_bytes);
+    const char* const wup = reinterpret_cast<const char*>(p.Wup);
     uint32_t voffB[LB];
 #pragma unroll
     for (int j = 0; j < LB; ++j) {
@@ -188,8 +186,8 @@ void up_kernel(UpParams p) {
         S::slot((wave * LB + j) * S::ROWS_PER_DMA, lane, r, ch);
         voffB[j] = (uint32_t)group_col(r >> 4, r & 15) * row_bytes + ch * 16;
     }
-    uint32_t voffA[LA];   // token rows of the tile being issued
-    uint32_t wslab = 0;   // byte offset of that tile's weight slab
+    const char* srcA[LA];   // token rows of the tile being issued
+    size_t wslab = 0;       // byte offset of that tile's weight slab
 
     // A tile's token and pair lists (TM ints each) are copied by waves 0/2
     // and 1/3 (both copies of a list land on the same bytes), so that every
@@ -204,12 +202,13 @@ void up_kernel(UpParams p) {
     auto sources = [&](int par, int inf) {
         const int sl = inf & 0xffff, nrows = inf >> 16;
         const int e = sl / p.B, c = sl - e * p.B;
-        wslab = ((uint32_t)e * (uint32_t)p.H + (uint32_t)c * M) * row_bytes;
+        wslab = ((size_t)e * p.H + (size_t)c * M) * row_bytes;
 #pragma unroll
         for (int j = 0; j < LA; ++j) {
             int r, ch;
             S::slot((wave * LA + j) * S::ROWS_PER_DMA, lane, r, ch);
-            voffA[j] = (r < nrows) ? (uint32_t)rows[par * 2 * TM + r] * row_bytes + ch * 16 : kOutOfRange;
+            const int tok = (r < nrows) ? rows[par * 2 * TM + r] : 0;
+            srcA[j] = reinterpret_cast<const char*>(p.X) + (size_t)tok * row_bytes + ch * 16;
         }
     };
     // Ring slots of the next stage to issue and of the next stage to read,
@@ -217,15 +216,22 @@ void up_kernel(UpParams p) {
     int slot_w = 0, slot_r = 0;
     uint32_t k_w = 0;
     int issued = 0;
-    auto issue = [&]() {
+    // The copies of one stage (q < LA: token rows, the rest weight rows),
+    // issued one at a time between MFMAs (see step).
+    auto issue_one = [&](int q) {
         char* base = lds_up + slot_w * STAGE;
-#pragma unroll
-        for (int j = 0; j < LA; ++j) dma16(xr, voffA[j], k_w, base + (wave * LA + j) * 1024);
-#pragma unroll
-        for (int j = 0; j < LB; ++j) dma16(wr, voffB[j], wslab + k_w, base + A_BYTES + (wave * LB + j) * 1024);
+        if (q < LA) dma16(srcA[q] + k_w, base + (wave * LA + q) * 1024);
+        else dma16(wup + (wslab + k_w) + voffB[q - LA], base + A_BYTES + (wave * LB + q - LA) * 1024);
+    };
+    auto issue_end = [&]() {
         slot_w = (slot_w == NST - 1) ? 0 : slot_w + 1;
         k_w += S::SK * 2;
         ++issued;
+    };
+    auto issue = [&]() {
+#pragma unroll
+        for (int q = 0; q < L; ++q) issue_one(q);
+        issue_end();
     };
     // Fragments are kept as raw 32-bit words (bf16 vectors in loop-carried
     // registers make the compiler split them into halves).
@@ -292,26 +298,18 @@ void up_kernel(UpParams p) {
                 }
                 k_w = 0;
             }
-            issue();
             load_frags(A2, B2);
+            // MFMAs by row group, with the stage's copies spread between them.
 #pragma unroll
-            for (int i = 0; i < RG; ++i)
+            for (int i = 0; i < RG; ++i) {
 #pragma unroll
                 for (int j = 0; j < MW; ++j) acc[i][j] = mfma16x16x32(as_bf16x8(Bw[j]), as_bf16x8(A[i]), acc[i][j]);
-            // Interleave the copies and fragment reads with the MFMAs.
 #pragma unroll
-            for (int q = 0; q < L; ++q) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+                for (int q = 0; q < L; ++q)
+                    if (q * RG / L == i) issue_one(q);
+                __builtin_amdgcn_sched_barrier(0);
             }
-#pragma unroll
-            for (int q = L; q < RG + MW; ++q) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            }
-            __builtin_amdgcn_sched_group_barrier(0x008, RG * MW - (RG + MW > L ? RG + MW : L), 0);
-            __builtin_amdgcn_sched_barrier(0);
+            issue_end();
             // The fragments just read must be in registers before the next
             // barrier lets another wave refill their slot.
             wait_lgkmcnt0();
@@ -390,7 +388,7 @@ void down_kernel(DownParams p) {
     const uint32_t fa = S::off(wm * (TM / 2) + lr, lg);
     const uint32_t fb = A_BYTES + S::off(wn * (BN / 2) + lr, lg);
     const uint32_t hrow = (uint32_t)p.H * 2;
-    const rsrc_t wr = make_rsrc(p.Wdown, p.w_bytes);
+    const char* const wdn = reinterpret_cast<const char*>(p.Wdown);
     uint32_t voffB[LB], vA[LA];
     int rA[LA];
 #pragma unroll
@@ -437,16 +435,16 @@ void down_kernel(DownParams p) {
     };
 
     // Issue side: the tile whose stages are being copied.
-    rsrc_t hr = make_rsrc(p.Hbuf, 0);
+    const char* hbase = reinterpret_cast<const char*>(p.Hbuf);
     uint64_t mrow[LA];
-    uint32_t wbase = 0;
+    size_t wbase = 0;
     uint64_t rem_w = 0;
     int cb_w = 0, kc_w = 0, st_w = 0, nreal_w = 0;
     auto issue_tile = [&](Desc D, int par) {
-        hr = make_rsrc(p.Hbuf + (size_t)D.p0 * p.H, (uint32_t)TM * hrow);
+        hbase = reinterpret_cast<const char*>(p.Hbuf + (size_t)D.p0 * p.H);
 #pragma unroll
         for (int j = 0; j < LA; ++j) mrow[j] = (rA[j] < D.nrows) ? rmask[par * TM + rA[j]] : 0ull;
-        wbase = ((uint32_t)D.e * (uint32_t)p.d + (uint32_t)D.ct * BN) * hrow;
+        wbase = ((size_t)D.e * p.d + (size_t)D.ct * BN) * hrow;
         rem_w = D.all;
         cb_w = rem_w ? __builtin_ctzll(rem_w) : 0;
         kc_w = 0;
@@ -454,15 +452,25 @@ void down_kernel(DownParams p) {
         nreal_w = D.nreal;
     };
     int slot_w = 0, slot_r = 0, issued = 0;
-    auto issue = [&]() {
-        char* base = lds_dn + slot_w * STAGE;
-        const bool real = st_w < nreal_w;
-        const uint32_t soff = (uint32_t)(cb_w * p.M + kc_w * S::SK) * 2;
-#pragma unroll
-        for (int j = 0; j < LA; ++j)
-            dma16(hr, (real && ((mrow[j] >> cb_w) & 1ull)) ? vA[j] : kOutOfRange, soff, base + (wave * LA + j) * 1024);
-#pragma unroll
-        for (int j = 0; j < LB; ++j) dma16(wr, voffB[j], wbase + soff, base + A_BYTES + (wave * LB + j) * 1024);
+    // The copies of one stage: copy q < LA fills A rows, the rest B rows.
+    // They are issued one at a time between MFMAs (see step), so that a
+    // copy held up at the texture unit never leaves the matrix cores idle.
+    char* cp_base = lds_dn;
+    uint32_t cp_soff = 0;
+    bool cp_real = false;
+    auto issue_begin = [&]() {
+        cp_base = lds_dn + slot_w * STAGE;
+        cp_real = st_w < nreal_w;
+        cp_soff = (uint32_t)(cb_w * p.M + kc_w * S::SK) * 2;
+    };
+    auto issue_one = [&](int q) {
+        if (q < LA)
+            dma16((cp_real && ((mrow[q] >> cb_w) & 1ull)) ? hbase + (vA[q] + cp_soff) : reinterpret_cast<const char*>(p.zero16),
+                  cp_base + (wave * LA + q) * 1024);
+        else
+            dma16(wdn + (wbase + cp_soff) + voffB[q - LA], cp_base + A_BYTES + (wave * LB + q - LA) * 1024);
+    };
+    auto issue_end = [&]() {
         slot_w = (slot_w == NST - 1) ? 0 : slot_w + 1;
         ++issued;
         ++st_w;
@@ -471,6 +479,12 @@ void down_kernel(DownParams p) {
             rem_w &= rem_w - 1;
             cb_w = rem_w ? __builtin_ctzll(rem_w) : 0;
         }
+    };
+    auto issue = [&]() {
+        issue_begin();
+#pragma unroll
+        for (int q = 0; q < L; ++q) issue_one(q);
+        issue_end();
     };
     u32x4 a0[RG], b0[NW], a1[RG], b1[NW];
     auto load_frags = [&](u32x4 (&A)[RG], u32x4 (&Bw)[NW]) {
@@ -533,7 +547,7 @@ void down_kernel(DownParams p) {
                 if (has_next) D = nxt;
                 issue_tile(D, has_next ? par ^ 1 : par);
             }
-            issue();
+            issue_begin();
             load_frags(A2, B2);
             const bool real = s < cur.nreal;
 #pragma unroll
@@ -543,7 +557,12 @@ void down_kernel(DownParams p) {
                     for (int j = 0; j < NW; ++j)
                         acc[i][j] = mfma16x16x32(as_bf16x8(Bw[j]), as_bf16x8(A[i]), acc[i][j]);
                 }
+#pragma unroll
+                for (int q = 0; q < L; ++q)
+                    if (q * RG / L == i) issue_one(q);
+                __builtin_amdgcn_sched_barrier(0);
             }
+            issue_end();
             if (++kc_r == kcpb) {
                 kc_r = 0;
                 rem_r &= rem_r - 1;

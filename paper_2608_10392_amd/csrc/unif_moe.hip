@@ -124,10 +124,6 @@ int32_t check_forward_shape(const unif_moe_config* c) {
     const Dims m = dims_of(c);
     if (m.bf16) {
         if (m.d % 128 != 0 || m.M % 64 != 0 || m.M > 256) return UNIF_EUNSUPPORTED;
-        // The expert GEMMs address X and each weight tensor with 32-bit
-        // buffer offsets.
-        if ((uint64_t)m.N * m.d * 2 >= kOutOfRange || (uint64_t)m.K1 * m.H * m.d * 2 >= kOutOfRange)
-            return UNIF_EUNSUPPORTED;
         // Down tiles are encoded as row tile << 8 | column tile.
         if (m.d / kDownBNNarrow > 255 || (int64_t)m.N * m.K1 / kDownTM + m.K1 >= ((int64_t)1 << 23))
             return UNIF_EUNSUPPORTED;
@@ -165,7 +161,7 @@ struct FwdPlan {
     size_t alpha, nsh, mask, nres, eids, wts;
     size_t wsplit;
     size_t zero_begin, zero_end;  // bin_count, slab_count, totals, zero page
-    size_t bin_count, slab_count, totals;
+    size_t bin_count, slab_count, totals, zero_page;
     size_t bin_cursor, slab_off, seg_off, up_tile_off, down_tile_off, chunk_off, chunk_cnt;
     size_t pair_token, pair_mask, pair_expert, pair_of, slab_rows, slab_tok, up_tile_info, up_tile_rows, hbuf, part;
     size_t max_chunks, max_row_tiles, rt_info, rt_masks, down_tiles;
@@ -190,6 +186,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.zero_begin = p.bin_count;
     p.slab_count = cv.take(4 * (size_t)m.nslab);
     p.totals = cv.take(4 * 8);
+    p.zero_page = cv.take(256);
     p.zero_end = cv.cur;
     p.bin_cursor = cv.take(4 * (size_t)m.nbin);
     p.slab_off = cv.take(4 * ((size_t)m.nslab + 1));
@@ -502,8 +499,6 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         up.M = m.M;
         up.B = m.B;
         up.H = m.H;
-        up.x_bytes = (uint32_t)((size_t)m.N * m.d * 2);
-        up.w_bytes = (uint32_t)((size_t)m.K1 * m.H * m.d * 2);
         up.X = static_cast<const u16*>(X);
         up.Wup = static_cast<const u16*>(W_up);
         up.Hbuf = reinterpret_cast<u16*>(ws + plan.hbuf);
@@ -530,7 +525,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         dn.B = m.B;
         dn.H = m.H;
         dn.ncol = pp.down_col_tiles;
-        dn.w_bytes = up.w_bytes;
+        dn.zero16 = reinterpret_cast<const u16*>(ws + plan.zero_page);
         dn.Hbuf = up.Hbuf;
         dn.Wdown = static_cast<const u16*>(W_down);
         dn.part = static_cast<float*>(part);
