@@ -115,6 +115,15 @@ __device__ __forceinline__ void route_logits_f32(const RouteParams& p, float* L,
     }
 }
 
+// Total-order key of a float for ranking: for non-NaN values it orders as
+// the float comparison does (-0 is first mapped to +0, so the two tie), and
+// a NaN gets a fixed place, so ranks computed with it always form a
+// permutation, whatever the inputs hold.
+__device__ __forceinline__ uint32_t rank_key(float f) {
+    const uint32_t u = __float_as_uint(f + 0.0f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
 // Decisions for token tok0 + threadIdx.x (threads 0..127, i.e. waves 0, 1).
 __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, float* PS, int* QS,
                                              int* slab_lds, int tok0) {
@@ -137,17 +146,18 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
             alpha = p.alpha_fixed;
         }
         // Eq. block-count, half to even; clamp to [1, B-1] (adaptive), cap.
-        int b = (int)rintf(__fmul_rn((float)B, alpha));
+        // (fminf/fmaxf drop a NaN alpha, so b stays in range for any input.)
+        int b = (int)rintf(fminf(fmaxf(__fmul_rn((float)B, alpha), 0.0f), (float)B));
         if (p.alpha_mode == 0) b = min(max(b, 1), B - 1);
         b = min(b, p.max_shared);
         // Eq. block-priority / shared-indices: the b largest x mu_c.
         if (p.select_mode == 0) {
             const float* u = row + 1 + K;
             for (int c = 0; c < B; ++c) {
-                const float uc = u[c];
+                const uint32_t uc = rank_key(u[c]);
                 int rank = 0;
                 for (int c2 = 0; c2 < B; ++c2) {
-                    const float u2 = u[c2];
+                    const uint32_t u2 = rank_key(u[c2]);
                     rank += (u2 > uc) || (u2 == uc && c2 < c);
                 }
                 if (rank < b) mask |= 1ull << c;
@@ -169,10 +179,11 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
         // Eq. sorted-affinity: rank by decreasing affinity, ties to lower index.
         for (int j = 0; j < K; ++j) {
             const float sj = l[j];
+            const uint32_t kj = rank_key(sj);
             int rank = 0;
             for (int j2 = 0; j2 < K; ++j2) {
-                const float s2 = l[j2];
-                rank += (s2 > sj) || (s2 == sj && j2 < j);
+                const uint32_t k2 = rank_key(l[j2]);
+                rank += (k2 > kj) || (k2 == kj && j2 < j);
             }
             ps[rank] = sj;
             qs[rank] = j + 1;

@@ -162,6 +162,47 @@ FULL_SAMPLE = {"tiny_f32": None, "vit_s16": 2048, "bert_base_padded": 2048, "vit
                "zipf_stress": 1024}
 
 
+def test_nonfinite_tokens_keep_routing_in_range():
+    """Tokens holding NaN or infinities (a fault upstream of the layer) get a
+    well-formed routing record - expert ids a permutation of 1..K, 1 <= k <=
+    K, 1 <= b <= B - 1, a mask of b of the B blocks - so every index the
+    permutation derives from them stays in range, and the other tokens'
+    routing and outputs match the oracle run on those tokens alone."""
+    cfg = get_config("vit_s16", n_tokens=1500, d_model=256, n_experts=6, n_blocks=8,
+                     block_width=64, max_shared=8)
+    g = generate(cfg)
+    N, K, B = cfg["n_tokens"], cfg["n_experts"], cfg["n_blocks"]
+    X = g["X"].copy()
+    bad = np.arange(7, N, 11)
+    X[bad[0::4]] = 0x7FC0                       # whole row NaN
+    X[bad[1::4], 5] = 0x7F80                    # one +inf
+    X[bad[2::4], 17] = 0xFF80                   # one -inf
+    X[bad[3::4], :] = 0x7F80                    # whole row +inf
+    g = dict(g, X=X)
+    dev = _device_layer(g)
+    dev.forward()
+    torch.cuda.synchronize()
+    grec, Y = dev.routing_numpy(), dev.output_numpy()
+    for t in bad:
+        ids = grec["expert_ids"][t]
+        assert sorted(ids.tolist()) == list(range(1, K + 1)), f"token {t}: expert ids {ids}"
+        assert 1 <= grec["n_res"][t] <= K
+        b = int(grec["n_shared"][t])
+        assert 1 <= b <= B - 1
+        m = int(grec["shared_mask"][t])
+        assert m < (1 << B) and bin(m).count("1") == b
+    good = np.setdiff1d(np.arange(N), bad)
+    sub_cfg = dict(cfg, n_tokens=int(good.size))
+    sub = dict(g, cfg=sub_cfg, X=X[good], valid=None)
+    orec = O.route(sub_cfg, sub["X"], None, g["W_router"], g["prototypes"])
+    gsub = {k: v[good] for k, v in grec.items()}
+    parity.check_routing(sub_cfg, orec, gsub)
+    rel, raw = parity.check_outputs(sub_cfg, sub, orec, gsub, Y[good], np.arange(good.size))
+    print(f"[gpu] non-finite rows: {bad.size} rows well-formed; others output err {rel:.2e} x RMS",
+          flush=True)
+    _free()
+
+
 @pytest.mark.parametrize("name", config_names())
 def test_full_workload(name):
     g = generate(name)
