@@ -11,13 +11,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "csrc", "unif_moe.hip")
 LIB = os.path.join(HERE, "libunifmoe.so")
 
-# Packed fp32 VALU instructions are switched off for all device code. MFMA
-# accumulators are kept in VGPRs: the down-projection's per-row-group skips
-# otherwise make the register allocator shuttle every accumulator between
-# AGPRs and VGPRs on each K step.
+# Packed fp32 VALU instructions are switched off for all device code.
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
-               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-               "-mllvm", "-amdgpu-mfma-vgpr-form"]
+               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
 def hipcc():

@@ -34,6 +34,14 @@ __device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// D = A(32x16) * B(16x32) + C on the matrix cores. Lane l supplies row
+// (A) / column (B) l % 32 and the 8 consecutive k of group l / 32; element
+// 4 j + i of the accumulator holds D[8 j + 4 (l / 32) + i][l % 32].
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+__device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
 // GELU(a) = a/2 (1 + erf(a / sqrt 2)), exact erf form (library erff).
 __device__ __forceinline__ float gelu_erf(float a) {
     return 0.5f * a * (1.0f + erff(a * 0.7071067811865475244f));

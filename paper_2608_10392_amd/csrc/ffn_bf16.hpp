@@ -11,34 +11,31 @@
 //   part[pair, n] = sum over blocks c of the pair's mask of
 //                   Hbuf[pair, block c] . V_e[block c, n]        (fp32)
 // The contraction runs over the union of the tile's block masks; rows whose
-// mask lacks a block read a zero page instead, and each 16-row MFMA group
+// mask lacks a block read a zero page instead, and each 32-row MFMA group
 // skips the blocks none of its rows use. Pairs are sorted by mask key, so
 // tiles hold similar masks.
 //
 // Engine shared by both kernels:
-//  * 4 waves in a 2 x 2 arrangement; each wave owns TM/2 rows and half of
-//    the tile's columns, in 16 x 16 MFMA groups (v_mfma_f32_16x16x32_bf16).
+//  * One workgroup of 4 waves per CU, 2 x 2: each wave owns TM/2 rows and
+//    half of the tile's columns, in 32 x 32 MFMA groups
+//    (v_mfma_f32_32x32x16_bf16: one wave per SIMD keeps the matrix core
+//    busier with these than with 16 x 16 groups, and the 32-cycle issue
+//    shadow hides the copies, LDS reads and bookkeeping).
 //  * The product is formed transposed, weights as the MFMA A operand and
-//    token rows as B, so each lane accumulates consecutive output columns of
-//    one row. The weight rows are placed in LDS so that 16-column groups 2J
-//    and 2J + 1 interleave in blocks of 4: lane l then holds columns
-//    32 J + 8 (l / 16) + 0..7 of row l % 16, written as one 16-byte store
-//    (8 bf16 after GELU in the up kernel, 2 x 4 fp32 in the down kernel)
-//    with no LDS staging.
-//  * K is staged RB/2 deep: a stage holds RB-byte rows (64 or 128), and the
-//    16-byte chunk c of row r sits at slot c ^ ((r >> 1) & (RB/16 - 1)).
-//    Measured with the LDS bank-conflict counter on gfx950, both variants
-//    make the fragment reads (16 rows x 4 chunks per instruction)
-//    conflict-free at 4 cycles per 1 KB; the unswizzled layouts and a padded
-//    144-byte stride run at half that rate or worse.
+//    token rows as B, so each lane accumulates output columns of one row.
+//    Weight rows are placed in LDS so that lane l of a 32-column group holds
+//    columns 16 (l / 32) + 0..15 (see wcol): 16 consecutive values of one
+//    row, written as 16-byte stores with no LDS staging.
+//  * K is staged 64 deep: a stage holds one 128-byte line per row, so every
+//    L2 request of the copies is a whole line (half-line requests ran at
+//    half the bytes per clock on gfx950). The 16-byte chunk c of row r sits
+//    at slot c ^ ((r >> 1) & 7), which keeps the fragment reads (32 rows x 2
+//    chunks per instruction) free of LDS bank conflicts.
 //  * Stages are filled by global_load_lds_dwordx4 (no register staging): one
-//    instruction fills 1024/RB rows, each lane fetching the global chunk that
+//    instruction fills 8 rows, each lane fetching the global chunk that
 //    belongs in its swizzled slot. NST stages rotate; NST - 1 are in flight
 //    while one is consumed. Waits are explicit vmcnt counts followed by a
 //    bare s_barrier (a __syncthreads fence would drain every load).
-//  * Tiles are sized so that two workgroups share a CU (OCC = 2): while one
-//    waits on a barrier or runs its epilogue, the other keeps the matrix
-//    cores busy.
 //  * Persistent over a device-built tile table, with consecutive tiles mapped
 //    to workgroups of the same XCD (dispatch is round-robin over 8 XCDs), so
 //    co-running tiles share weight slabs in that XCD's L2.
@@ -78,31 +75,31 @@ struct DownParams {
     const int* totals;           // [2]: down tiles
 };
 
-// Staged-row geometry: RB bytes per row, K = RB/2 bf16 per stage.
-template <int RB>
+// Staged-row geometry: one 128-byte line (64 bf16 of k) per row and stage.
 struct Stage {
-    static constexpr int SK = RB / 2;
-    static constexpr int CH = RB / 16;             // 16-byte chunks per row
-    static constexpr int ROWS_PER_DMA = 1024 / RB;
-    static constexpr int KSTEPS = SK / 32;          // MFMA K steps per stage
-    __device__ static __forceinline__ int off(int r, int c) { return r * RB + ((c ^ ((r >> 1) & (CH - 1))) << 4); }
-    // Row r and chunk c that lane `lane` fills when one DMA covers rows r0..
+    static constexpr int RB = 128;
+    static constexpr int SK = 64;                  // k per stage
+    static constexpr int CH = 8;                   // 16-byte chunks per row
+    static constexpr int ROWS_PER_DMA = 8;         // rows filled by one 1-KB copy
+    static constexpr int KSTEPS = 4;               // 16-deep MFMA steps per stage
+    __device__ static __forceinline__ uint32_t off(int r, int c) { return r * RB + ((c ^ ((r >> 1) & 7)) << 4); }
+    // Row r and chunk c that lane `lane` fills when one copy covers rows r0..
     __device__ static __forceinline__ void slot(int r0, int lane, int& r, int& c) {
         r = r0 + lane / CH;
-        c = (lane % CH) ^ ((r >> 1) & (CH - 1));
+        c = (lane % CH) ^ ((r >> 1) & 7);
     }
 };
 
-// Output column held by row m of 16-column MFMA group g (see the engine
-// notes): groups 2J and 2J + 1 interleave in blocks of 4 columns.
-__device__ __forceinline__ int group_col(int g, int m) {
-    return 32 * (g >> 1) + 8 * (m >> 2) + (m & 3) + 4 * (g & 1);
-}
+// Output column (within its 32-column group) of the weight row staged at
+// position r of the group. The MFMA gives lane l the D rows
+// 8 j + 4 (l / 32) + i in accumulator element 4 j + i; with this order those
+// rows are the columns 16 (l / 32) + 4 j + i.
+__device__ __forceinline__ int wcol(int r) { return 16 * ((r >> 2) & 1) + 4 * (r >> 3) + (r & 3); }
 
 // Dynamic LDS bytes of the two kernels: the stage ring, plus the row lists
 // of the current and the next tile (up: tokens and pairs; down: block masks).
-__host__ __device__ constexpr int up_lds_bytes(int TM, int M, int RB, int NST) { return NST * (TM + M) * RB + 16 * TM; }
-__host__ __device__ constexpr int down_lds_bytes(int TM, int BN, int RB, int NST) { return NST * (TM + BN) * RB + 16 * TM; }
+__host__ __device__ constexpr int up_lds_bytes(int TM, int M, int NST) { return NST * (TM + M) * Stage::RB + 16 * TM; }
+__host__ __device__ constexpr int down_lds_bytes(int TM, int BN, int NST) { return NST * (TM + BN) * Stage::RB + 16 * TM; }
 
 // Tile handled by this workgroup in persistent round `round`: a contiguous
 // range of tiles per XCD. gridDim.x is a multiple of kXcds.
@@ -125,12 +122,27 @@ __device__ __forceinline__ void wait_vm_after(int n) {
     else wait_vmcnt<0>();
 }
 
+// Wait before step s of a tile reads stage s + 1. Issued after that stage:
+// the later stages still in flight (NST - 2 of them), and in the first
+// NST - 1 steps also the previous tile's epilogue stores (issued after stage
+// NST - 1) and, from step 1 on, the next tile's row-list copy (issued at
+// step 0, before stage NST).
+template <int NST, int L, int NEPI, int NFETCH>
+__device__ __forceinline__ void wait_stage(bool first, int s, bool after_epi, bool has_next) {
+    if (first && s <= NST - 2) {
+        const int n = (NST - 2) * L + (after_epi ? NEPI : 0) + ((s >= 1 && has_next) ? NFETCH : 0);
+        wait_vm_after<(NST - 2) * L, NEPI, NFETCH>(n);
+    } else {
+        wait_vmcnt<(NST - 2) * L>();
+    }
+}
+
 // Up-projection, persistent and pipelined across tiles.
-//  * Ring of NST stages filled by buffer loads into LDS; a stage's
-//    fragments are read into registers one stage ahead (two register sets),
-//    so the matrix cores never wait on LDS latency and a slot is refilled as
-//    soon as its fragments are in registers: NST - 1 stages stay in flight
-//    while the next one is read.
+//  * Ring of NST stages filled by copies into LDS; a stage's fragments are
+//    read into registers one stage ahead (two register sets), so the matrix
+//    cores never wait on LDS latency and a slot is refilled as soon as its
+//    fragments are in registers: NST - 1 stages stay in flight while the
+//    next one is read.
 //  * The ring runs on from one tile into the next: the next tile's first
 //    stages are issued during the current tile's last iterations, and its
 //    row lists (tokens, pairs) are copied to LDS at the current tile's first
@@ -140,23 +152,26 @@ __device__ __forceinline__ void wait_vm_after(int n) {
 //    previous tile's epilogue stores, a row-list copy) may be outstanding.
 //    Every epilogue store is issued (rows past the tile's count write the
 //    sink row), so the count is exact.
-template <int MW, int TM, int RB, int NST, int OCC>
-__global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
+//  * A tile has nk = d / 64 stages; tiles shorter than NST + 1 stages are
+//    padded with stages that re-read k = 0.. and run no MFMAs.
+template <int MG, int TM, int NST>
+__global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void up_kernel(UpParams p) {
-    using S = Stage<RB>;
-    static_assert(S::KSTEPS == 1, "one MFMA k step per stage");
-    constexpr int M = MW * 32;
-    constexpr int RG = TM / 32;                       // MFMA row groups per wave
-    constexpr int LA = TM / S::ROWS_PER_DMA / 4;      // A copies per wave per stage
-    constexpr int LB = M / S::ROWS_PER_DMA / 4;       // B copies per wave per stage
+    using S = Stage;
+    constexpr int RB = S::RB, KS = S::KSTEPS;
+    constexpr int M = MG * 64;                        // MG 32-column groups per wave
+    constexpr int RG = TM / 64;                       // 32-row groups per wave
+    constexpr int LA = TM / S::ROWS_PER_DMA / 4;      // token-row copies per wave per stage
+    constexpr int LB = M / S::ROWS_PER_DMA / 4;       // weight-row copies per wave per stage
     constexpr int L = LA + LB;
-    constexpr int NEPI = RG * (MW / 2);               // epilogue stores per wave
+    constexpr int NEPI = RG * MG * 2;                 // epilogue stores per wave
     constexpr int A_BYTES = TM * RB, STAGE = (TM + M) * RB, RING = NST * STAGE;
+    constexpr int NU = KS * RG;                       // MFMA units per stage
     static_assert(LA >= 1 && LB >= 1, "tile too small for one copy per wave");
     static_assert(TM * 4 <= 32 * 16, "a row list must fit one half-wave copy");
-    static_assert(NST == 3, "the wait accounting is written for a 3-stage ring");
+    static_assert(NST >= 3 && NST <= 5, "ring depth");
     constexpr int NFETCH = 1;                         // copies per wave for a tile's row lists
-    static_assert(L + NEPI + NFETCH < 64, "vmcnt range");
+    static_assert((NST - 2) * L + NEPI + NFETCH < 64, "vmcnt range");
     extern __shared__ __attribute__((aligned(16))) char lds_up[];
     // rows[par][0] tokens, rows[par][1] pairs of the tile with parity par
     int* rows = reinterpret_cast<int*>(lds_up + RING);
@@ -164,16 +179,21 @@ void up_kernel(UpParams p) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     const int n_tiles = ld_uniform(p.totals + 1);
-    const int nk = p.d / S::SK;     // stages per tile: even, and >= NST + 1 (d >= 128)
+    const int nk = p.d / S::SK;                       // real stages per tile (even)
+    const int nst = (max(nk, NST + 1) + 1) & ~1;      // stages per tile, padding included (even)
     int tile = xcd_tile(0);
     if (tile >= n_tiles) return;
 
-    // Fragment addresses inside a stage: lane (lr, lg) reads row base + lr,
-    // chunk lg; 16-row steps keep the swizzle, so row groups are constant
-    // offsets from these.
-    const int lr = lane & 15, lg = lane >> 4;
-    const uint32_t fa = S::off(wm * (TM / 2) + lr, lg);
-    const uint32_t fb = A_BYTES + S::off(wn * (M / 2) + lr, lg);
+    // Fragment addresses inside a stage: lane (lr, lh) reads row base + lr,
+    // chunk 2 k + lh of k step k; 32-row steps keep the swizzle, so row
+    // groups are constant offsets from these.
+    const int lr = lane & 31, lh = lane >> 5;
+    uint32_t fx[KS], fw[KS];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+        fx[k] = S::off(wm * (TM / 2) + lr, 2 * k + lh);
+        fw[k] = A_BYTES + S::off(wn * (M / 2) + lr, 2 * k + lh);
+    }
     // Copy sources: per-lane addresses fixed for a tile, plus the k position
     // (and, for weights, the slab) as a uniform byte offset. Token rows past
     // the tile's count read token 0; their results go to the sink row.
@@ -184,10 +204,10 @@ void up_kernel(UpParams p) {
     for (int j = 0; j < LB; ++j) {
         int r, ch;
         S::slot((wave * LB + j) * S::ROWS_PER_DMA, lane, r, ch);
-        voffB[j] = (uint32_t)group_col(r >> 4, r & 15) * row_bytes + ch * 16;
+        voffB[j] = (uint32_t)(32 * (r >> 5) + wcol(r & 31)) * row_bytes + ch * 16;
     }
     const char* srcA[LA];   // token rows of the tile being issued
-    size_t wslab = 0;       // byte offset of that tile's weight slab
+    const char* wslab = wup;
 
     // A tile's token and pair lists (TM ints each) are copied by waves 0/2
     // and 1/3 (both copies of a list land on the same bytes), so that every
@@ -202,7 +222,7 @@ void up_kernel(UpParams p) {
     auto sources = [&](int par, int inf) {
         const int sl = inf & 0xffff, nrows = inf >> 16;
         const int e = sl / p.B, c = sl - e * p.B;
-        wslab = ((size_t)e * p.H + (size_t)c * M) * row_bytes;
+        wslab = wup + ((size_t)e * p.H + (size_t)c * M) * row_bytes;
 #pragma unroll
         for (int j = 0; j < LA; ++j) {
             int r, ch;
@@ -211,22 +231,19 @@ void up_kernel(UpParams p) {
             srcA[j] = reinterpret_cast<const char*>(p.X) + (size_t)tok * row_bytes + ch * 16;
         }
     };
-    // Ring slots of the next stage to issue and of the next stage to read,
-    // and the k offset (bytes) of the next stage to issue.
-    int slot_w = 0, slot_r = 0;
+    // Ring slot (byte offset) of the next stage to issue and of the next
+    // stage to read, and the k offset (bytes) of the next stage to issue.
+    uint32_t slot_w = 0, slot_r = 0;
     uint32_t k_w = 0;
-    int issued = 0;
-    // The copies of one stage (q < LA: token rows, the rest weight rows),
-    // issued one at a time between MFMAs (see step).
     auto issue_one = [&](int q) {
-        char* base = lds_up + slot_w * STAGE;
+        char* base = lds_up + slot_w;
         if (q < LA) dma16(srcA[q] + k_w, base + (wave * LA + q) * 1024);
-        else dma16(wup + (wslab + k_w) + voffB[q - LA], base + A_BYTES + (wave * LB + q - LA) * 1024);
+        else dma16(wslab + k_w + voffB[q - LA], base + A_BYTES + (wave * LB + q - LA) * 1024);
     };
     auto issue_end = [&]() {
-        slot_w = (slot_w == NST - 1) ? 0 : slot_w + 1;
-        k_w += S::SK * 2;
-        ++issued;
+        slot_w = (slot_w == (NST - 1) * STAGE) ? 0u : slot_w + STAGE;
+        k_w += RB;
+        if (k_w == row_bytes) k_w = 0;    // padding stages re-read the row start
     };
     auto issue = [&]() {
 #pragma unroll
@@ -235,16 +252,22 @@ void up_kernel(UpParams p) {
     };
     // Fragments are kept as raw 32-bit words (bf16 vectors in loop-carried
     // registers make the compiler split them into halves).
-    u32x4 a0[RG], b0[MW], a1[RG], b1[MW];
-    auto load_frags = [&](u32x4 (&A)[RG], u32x4 (&Bw)[MW]) {
-        const char* st = lds_up + slot_r * STAGE;
-#pragma unroll
-        for (int j = 0; j < MW; ++j) Bw[j] = ld16(st + fb + j * 16 * RB);
-#pragma unroll
-        for (int i = 0; i < RG; ++i) A[i] = ld16(st + fa + i * 16 * RB);
-        slot_r = (slot_r == NST - 1) ? 0 : slot_r + 1;
+    u32x4 x0[KS][RG], w0[KS][MG], x1[KS][RG], w1[KS][MG];
+    // Fragment read r of a stage: k step r / (MG + RG), then its MG weight
+    // and RG token fragments.
+    constexpr int NR = KS * (MG + RG);
+    auto read_one = [&](const char* st, int r, u32x4 (&X)[KS][RG], u32x4 (&W)[KS][MG]) {
+        const int k = r / (MG + RG), t = r % (MG + RG);
+        if (t < MG) W[k][t] = ld16(st + fw[k] + t * 32 * RB);
+        else X[k][t - MG] = ld16(st + fx[k] + (t - MG) * 32 * RB);
     };
-    f32x4 acc[RG][MW];
+    auto next_slot_r = [&]() { slot_r = (slot_r == (NST - 1) * STAGE) ? 0u : slot_r + STAGE; };
+    auto load_frags = [&](u32x4 (&X)[KS][RG], u32x4 (&W)[KS][MG]) {
+#pragma unroll
+        for (int r = 0; r < NR; ++r) read_one(lds_up + slot_r, r, X, W);
+        next_slot_r();
+    };
+    f32x16 acc[RG][MG];
 
     int par = 0;
     int info = ld_uniform(p.tile_info + tile);
@@ -255,7 +278,7 @@ void up_kernel(UpParams p) {
     for (int ks = 0; ks < NST; ++ks) issue();
     wait_vmcnt<(NST - 1) * L>();
     __builtin_amdgcn_s_barrier();
-    load_frags(a0, b0);
+    load_frags(x0, w0);
     wait_lgkmcnt0();
     bool after_epi = false;
     for (int round = 0;; ++round) {
@@ -265,27 +288,24 @@ void up_kernel(UpParams p) {
 #pragma unroll
         for (int i = 0; i < RG; ++i)
 #pragma unroll
-            for (int j = 0; j < MW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        // Fragments of tile stage s are in (A, Bw): wait for stage s + 1,
+            for (int j = 0; j < MG; ++j) acc[i][j] = f32x16{};
+        // Fragments of tile stage s are in (X, W): wait for stage s + 1,
         // refill the slot freed by stage s with the stage NST ahead (of this
         // tile, of the next tile, or - past the last tile - a harmless
         // re-read of this tile's first stages into the free slot, which
         // keeps every iteration's copy count the same), read stage s + 1
-        // into (A2, B2), then run stage s.
+        // into (X2, W2), then run stage s.
         // FIRST marks s = 0 and 1, where the previous tile's epilogue stores
         // (issued after stages 0..NST-1 of this tile) and the row-list copy
         // (issued at s = 0, before stage NST) sit behind the awaited stage.
-        auto step = [&](auto first, int s, u32x4 (&A)[RG], u32x4 (&Bw)[MW], u32x4 (&A2)[RG],
-                        u32x4 (&B2)[MW]) {
-            if constexpr (decltype(first)::value) {
-                const int n_after = L + (after_epi ? NEPI : 0) + ((s == 1 && has_next) ? NFETCH : 0);
-                wait_vm_after<L, NEPI, NFETCH>(n_after);
-            } else {
-                wait_vmcnt<L>();
-            }
+        auto step = [&](auto first, int s, u32x4 (&X)[KS][RG], u32x4 (&W)[KS][MG], u32x4 (&X2)[KS][RG],
+                        u32x4 (&W2)[KS][MG]) {
+            wait_stage<NST, L, NEPI, NFETCH>(decltype(first)::value, s, after_epi, has_next);
             __builtin_amdgcn_s_barrier();
-            if (s == 0 && has_next) fetch_rows(next, par ^ 1);
-            if (s + NST == nk) {
+            if constexpr (decltype(first)::value) {
+                if (s == 0 && has_next) fetch_rows(next, par ^ 1);
+            }
+            if (s + NST == nst) {
                 // From here on the stages issued belong to the next tile.
                 // Its row lists were copied at s == 0, before stage NST,
                 // which has been waited for when s >= NST - 1.
@@ -298,15 +318,27 @@ void up_kernel(UpParams p) {
                 }
                 k_w = 0;
             }
-            load_frags(A2, B2);
-            // MFMAs by row group, with the stage's copies spread between them.
+            const char* st2 = lds_up + slot_r;
+            next_slot_r();
+            const bool real = s < nk;
+            // MFMAs by (k step, row group), with the reads of stage s + 1's
+            // fragments and the copies of stage s + NST spread between them
+            // (no reads after the last group, so they have landed by the
+            // step's end).
 #pragma unroll
-            for (int i = 0; i < RG; ++i) {
+            for (int u = 0; u < NU; ++u) {
+                const int k = u / RG, i = u % RG;
+                if (real) {
 #pragma unroll
-                for (int j = 0; j < MW; ++j) acc[i][j] = mfma16x16x32(as_bf16x8(Bw[j]), as_bf16x8(A[i]), acc[i][j]);
+                    for (int j = 0; j < MG; ++j)
+                        acc[i][j] = mfma32x32x16(as_bf16x8(W[k][j]), as_bf16x8(X[k][i]), acc[i][j]);
+                }
+#pragma unroll
+                for (int r = 0; r < NR; ++r)
+                    if (r * (NU - 1) / NR == u) read_one(st2, r, X2, W2);
 #pragma unroll
                 for (int q = 0; q < L; ++q)
-                    if (q * RG / L == i) issue_one(q);
+                    if (q * NU / L == u) issue_one(q);
                 __builtin_amdgcn_sched_barrier(0);
             }
             issue_end();
@@ -314,29 +346,40 @@ void up_kernel(UpParams p) {
             // barrier lets another wave refill their slot.
             wait_lgkmcnt0();
         };
-        step(std::true_type{}, 0, a0, b0, a1, b1);
-        step(std::true_type{}, 1, a1, b1, a0, b0);
-        for (int s = 2; s < nk; s += 2) {
-            step(std::false_type{}, s, a0, b0, a1, b1);
-            step(std::false_type{}, s + 1, a1, b1, a0, b0);
+        // Steps 0 .. NST - 2 carry the first-steps wait accounting; nst is
+        // even and at least NST + 1.
+        step(std::true_type{}, 0, x0, w0, x1, w1);
+        step(std::true_type{}, 1, x1, w1, x0, w0);
+        int s = 2;
+        if constexpr (NST >= 4) {
+            step(std::true_type{}, 2, x0, w0, x1, w1);
+            step(std::true_type{}, 3, x1, w1, x0, w0);
+            s = 4;
         }
-        // GELU, round to bf16; lane stores 8 consecutive columns of its row.
+        for (; s < nst; s += 2) {
+            step(std::false_type{}, s, x0, w0, x1, w1);
+            step(std::false_type{}, s + 1, x1, w1, x0, w0);
+        }
+        // GELU, round to bf16; lane stores 16 consecutive columns of its row
+        // per 32-column group.
         const int sl = info & 0xffff, nrows = info >> 16;
         const int c = sl - (sl / p.B) * p.B;
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
-            const int r = wm * (TM / 2) + i * 16 + (lane & 15);
+            const int r = wm * (TM / 2) + i * 32 + lr;
             u16* dst = (r < nrows) ? p.Hbuf + (size_t)rows[(par * 2 + 1) * TM + r] * p.H + (size_t)c * M : p.Hsink;
-            dst += wn * (M / 2) + 8 * (lane >> 4);
+            dst += wn * (M / 2) + 16 * lh;
 #pragma unroll
-            for (int J = 0; J < MW / 2; ++J) {
-                const f32x4 lo = acc[i][2 * J], hi = acc[i][2 * J + 1];
-                u32x4 v;
-                v[0] = pack_bf16x2(gelu_as7126(lo[0]), gelu_as7126(lo[1]));
-                v[1] = pack_bf16x2(gelu_as7126(lo[2]), gelu_as7126(lo[3]));
-                v[2] = pack_bf16x2(gelu_as7126(hi[0]), gelu_as7126(hi[1]));
-                v[3] = pack_bf16x2(gelu_as7126(hi[2]), gelu_as7126(hi[3]));
-                st16(dst + 32 * J, v);
+            for (int j = 0; j < MG; ++j) {
+                const f32x16 v = acc[i][j];
+                u32x4 lo, hi;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    lo[t] = pack_bf16x2(gelu_as7126(v[2 * t]), gelu_as7126(v[2 * t + 1]));
+                    hi[t] = pack_bf16x2(gelu_as7126(v[8 + 2 * t]), gelu_as7126(v[9 + 2 * t]));
+                }
+                st16(dst + 32 * j, lo);
+                st16(dst + 32 * j + 8, hi);
             }
         }
         if (!has_next) break;
@@ -349,53 +392,60 @@ void up_kernel(UpParams p) {
     wait_vmcnt<0>();
 }
 
-// Down-projection on the same engine as the up kernel (ring of buffer
-// loads, fragments read one stage ahead, pipelined across tiles). A tile is
-// TM consecutive pairs of one expert x BN output columns; its stages walk
-// the blocks of the tile's mask union, M/32 stages per block. A row whose
-// mask lacks the stage's block reads zeros (an out-of-range offset), and a
-// 16-row MFMA group whose rows all lack it skips its MFMAs. Tiles with fewer
-// than NST + 1 stages are padded with empty stages (no MFMAs), so the ring
-// never runs more than one tile ahead.
-template <int NW, int TM, int RB, int NST, int OCC>
-__global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
+// Down-projection on the same engine as the up kernel (ring of copies,
+// fragments read one stage ahead, pipelined across tiles). A tile is TM
+// consecutive pairs of one expert x BN output columns; its stages walk the
+// blocks of the tile's mask union, M/64 stages per block. A row whose mask
+// lacks the stage's block reads the zero page, and a 32-row MFMA group whose
+// rows all lack it skips its MFMAs. Tiles are padded to an even number of at
+// least NST + 1 stages with empty stages (no MFMAs), so the ring never runs
+// more than one tile ahead.
+template <int NG, int TM, int NST>
+__global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void down_kernel(DownParams p) {
-    using S = Stage<RB>;
-    static_assert(S::KSTEPS == 1, "one MFMA k step per stage");
-    constexpr int BN = NW * 32;
-    constexpr int RG = TM / 32;                       // MFMA row groups per wave
-    constexpr int G = TM / 16;                        // 16-row groups per tile
+    using S = Stage;
+    constexpr int RB = S::RB, KS = S::KSTEPS;
+    constexpr int BN = NG * 64;                       // NG 32-column groups per wave
+    constexpr int RG = TM / 64;                       // 32-row groups per wave
+    constexpr int G16 = TM / 16;                      // 16-row mask groups per tile
     constexpr int LA = TM / S::ROWS_PER_DMA / 4;
     constexpr int LB = BN / S::ROWS_PER_DMA / 4;
     constexpr int L = LA + LB;
-    constexpr int NEPI = RG * NW;                     // epilogue stores per wave
+    constexpr int NEPI = RG * NG * 4;                 // epilogue stores per wave
     constexpr int A_BYTES = TM * RB, STAGE = (TM + BN) * RB, RING = NST * STAGE;
+    constexpr int NU = KS * RG;
     static_assert(LA >= 1 && LB >= 1, "tile too small for one copy per wave");
     constexpr int NFETCH = TM * 8 / 256;              // 4-byte copies per wave for a tile's row masks
-    static_assert(NST == 3, "the wait accounting is written for a 3-stage ring");
-    static_assert(L + NEPI + NFETCH < 64, "vmcnt range");
+    static_assert(NST >= 3 && NST <= 5, "ring depth");
+    static_assert((NST - 2) * L + NEPI + NFETCH < 64, "vmcnt range");
     extern __shared__ __attribute__((aligned(16))) char lds_dn[];
     uint64_t* rmask = reinterpret_cast<uint64_t*>(lds_dn + RING);   // [2][TM]
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     const int n_tiles = ld_uniform(p.totals + 2);
-    const int kcpb = p.M / S::SK;   // stages per block (even: M is a multiple of 64)
+    const int kcpb = p.M / S::SK;   // stages per block
     int tile = xcd_tile(0);
     if (tile >= n_tiles) return;
 
-    const int lr = lane & 15, lg = lane >> 4;
-    const uint32_t fa = S::off(wm * (TM / 2) + lr, lg);
-    const uint32_t fb = A_BYTES + S::off(wn * (BN / 2) + lr, lg);
+    const int lr = lane & 31, lh = lane >> 5;
+    uint32_t fx[KS], fw[KS];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+        fx[k] = S::off(wm * (TM / 2) + lr, 2 * k + lh);
+        fw[k] = A_BYTES + S::off(wn * (BN / 2) + lr, 2 * k + lh);
+    }
     const uint32_t hrow = (uint32_t)p.H * 2;
+    const uint32_t blk_bytes = (uint32_t)p.M * 2;
     const char* const wdn = reinterpret_cast<const char*>(p.Wdown);
+    const char* const zero = reinterpret_cast<const char*>(p.zero16);
     uint32_t voffB[LB], vA[LA];
     int rA[LA];
 #pragma unroll
     for (int j = 0; j < LB; ++j) {
         int r, ch;
         S::slot((wave * LB + j) * S::ROWS_PER_DMA, lane, r, ch);
-        voffB[j] = (uint32_t)group_col(r >> 4, r & 15) * hrow + ch * 16;
+        voffB[j] = (uint32_t)(32 * (r >> 5) + wcol(r & 31)) * hrow + ch * 16;
     }
 #pragma unroll
     for (int j = 0; j < LA; ++j) {
@@ -404,7 +454,8 @@ void down_kernel(DownParams p) {
         vA[j] = (uint32_t)rA[j] * hrow + ch * 16;
     }
 
-    // Uniform description of a tile.
+    // Uniform description of a tile; gm[i]: block mask of this wave's
+    // 32-row group i.
     struct Desc {
         int p0, nrows, e, ct, nst, nreal;
         uint64_t all, gm[RG];
@@ -418,12 +469,15 @@ void down_kernel(DownParams p) {
         D.p0 = ld_uniform(inf);
         D.nrows = ld_uniform(inf + 1);
         D.e = ld_uniform(inf + 2);
-        const uint64_t* ms = p.rt_masks + (size_t)rt * (G + 1);
-        D.all = ld_uniform64(ms + G);
+        const uint64_t* ms = p.rt_masks + (size_t)rt * (G16 + 1);
+        D.all = ld_uniform64(ms + G16);
 #pragma unroll
-        for (int i = 0; i < RG; ++i) D.gm[i] = ld_uniform64(ms + wm * RG + i);
+        for (int i = 0; i < RG; ++i) {
+            const int g = 2 * (wm * RG + i);
+            D.gm[i] = ld_uniform64(ms + g) | ld_uniform64(ms + g + 1);
+        }
         D.nreal = __popcll(D.all) * kcpb;
-        D.nst = max(D.nreal, NST + 1);
+        D.nst = (max(D.nreal, NST + 1) + 1) & ~1;
         return D;
     };
     // A tile's row masks (TM u64) are copied to LDS by every wave, in
@@ -434,68 +488,80 @@ void down_kernel(DownParams p) {
         for (int q = 0; q < NFETCH; ++q) dma4(src + q * 64 + lane, rmask + par * TM + q * 32);
     };
 
-    // Issue side: the tile whose stages are being copied.
-    const char* hbase = reinterpret_cast<const char*>(p.Hbuf);
+    // Issue side. Per block, each H-row copy either walks its row (one
+    // stage of k per stage) or re-reads the zero page (stride 0); the weight
+    // copies walk the expert's rows from a uniform base. Past the last block
+    // of the union (padding stages) the H copies read the zero page and the
+    // weight copies re-read block 0 (in range, never used).
+    const char* hbase = nullptr;
+    const char* wtile = wdn;
     uint64_t mrow[LA];
-    size_t wbase = 0;
+    const char* pa[LA];
+    uint32_t sa[LA];
+    const char* pb = wdn;
     uint64_t rem_w = 0;
-    int cb_w = 0, kc_w = 0, st_w = 0, nreal_w = 0;
+    int kc_w = 0;
+    auto set_block_w = [&]() {
+        const uint64_t low = rem_w & (0ull - rem_w);
+        const int cb = rem_w ? __builtin_ctzll(rem_w) : 0;
+        pb = wtile + (size_t)cb * blk_bytes;
+#pragma unroll
+        for (int q = 0; q < LA; ++q) {
+            const bool on = (mrow[q] & low) != 0;
+            pa[q] = on ? hbase + (vA[q] + (uint32_t)cb * blk_bytes) : zero;
+            sa[q] = on ? (uint32_t)RB : 0u;
+        }
+    };
     auto issue_tile = [&](Desc D, int par) {
         hbase = reinterpret_cast<const char*>(p.Hbuf + (size_t)D.p0 * p.H);
 #pragma unroll
         for (int j = 0; j < LA; ++j) mrow[j] = (rA[j] < D.nrows) ? rmask[par * TM + rA[j]] : 0ull;
-        wbase = ((size_t)D.e * p.d + (size_t)D.ct * BN) * hrow;
+        // Settle the mask reads here, so that no later use waits on them
+        // behind the fragment reads of a step.
+        wait_lgkmcnt0();
+        wtile = wdn + ((size_t)D.e * p.d + (size_t)D.ct * BN) * hrow;
         rem_w = D.all;
-        cb_w = rem_w ? __builtin_ctzll(rem_w) : 0;
         kc_w = 0;
-        st_w = 0;
-        nreal_w = D.nreal;
+        set_block_w();
     };
-    int slot_w = 0, slot_r = 0, issued = 0;
-    // The copies of one stage: copy q < LA fills A rows, the rest B rows.
-    // They are issued one at a time between MFMAs (see step), so that a
-    // copy held up at the texture unit never leaves the matrix cores idle.
-    char* cp_base = lds_dn;
-    uint32_t cp_soff = 0;
-    bool cp_real = false;
-    auto issue_begin = [&]() {
-        cp_base = lds_dn + slot_w * STAGE;
-        cp_real = st_w < nreal_w;
-        cp_soff = (uint32_t)(cb_w * p.M + kc_w * S::SK) * 2;
-    };
+    uint32_t slot_w = 0, slot_r = 0;
+    // The copies of one stage: copy q < LA fills H rows, the rest weight
+    // rows. They are issued one at a time between MFMAs (see step).
     auto issue_one = [&](int q) {
-        if (q < LA)
-            dma16((cp_real && ((mrow[q] >> cb_w) & 1ull)) ? hbase + (vA[q] + cp_soff) : reinterpret_cast<const char*>(p.zero16),
-                  cp_base + (wave * LA + q) * 1024);
-        else
-            dma16(wdn + (wbase + cp_soff) + voffB[q - LA], cp_base + A_BYTES + (wave * LB + q - LA) * 1024);
+        char* base = lds_dn + slot_w;
+        if (q < LA) dma16(pa[q], base + (wave * LA + q) * 1024);
+        else dma16(pb + voffB[q - LA], base + A_BYTES + (wave * LB + q - LA) * 1024);
     };
     auto issue_end = [&]() {
-        slot_w = (slot_w == NST - 1) ? 0 : slot_w + 1;
-        ++issued;
-        ++st_w;
+        slot_w = (slot_w == (NST - 1) * STAGE) ? 0u : slot_w + STAGE;
+#pragma unroll
+        for (int q = 0; q < LA; ++q) pa[q] += sa[q];
+        pb += RB;
         if (++kc_w == kcpb) {
             kc_w = 0;
             rem_w &= rem_w - 1;
-            cb_w = rem_w ? __builtin_ctzll(rem_w) : 0;
+            set_block_w();
         }
     };
     auto issue = [&]() {
-        issue_begin();
 #pragma unroll
         for (int q = 0; q < L; ++q) issue_one(q);
         issue_end();
     };
-    u32x4 a0[RG], b0[NW], a1[RG], b1[NW];
-    auto load_frags = [&](u32x4 (&A)[RG], u32x4 (&Bw)[NW]) {
-        const char* st = lds_dn + slot_r * STAGE;
-#pragma unroll
-        for (int j = 0; j < NW; ++j) Bw[j] = ld16(st + fb + j * 16 * RB);
-#pragma unroll
-        for (int i = 0; i < RG; ++i) A[i] = ld16(st + fa + i * 16 * RB);
-        slot_r = (slot_r == NST - 1) ? 0 : slot_r + 1;
+    u32x4 x0[KS][RG], w0[KS][NG], x1[KS][RG], w1[KS][NG];
+    constexpr int NR = KS * (NG + RG);
+    auto read_one = [&](const char* st, int r, u32x4 (&X)[KS][RG], u32x4 (&W)[KS][NG]) {
+        const int k = r / (NG + RG), t = r % (NG + RG);
+        if (t < NG) W[k][t] = ld16(st + fw[k] + t * 32 * RB);
+        else X[k][t - NG] = ld16(st + fx[k] + (t - NG) * 32 * RB);
     };
-    f32x4 acc[RG][NW];
+    auto next_slot_r = [&]() { slot_r = (slot_r == (NST - 1) * STAGE) ? 0u : slot_r + STAGE; };
+    auto load_frags = [&](u32x4 (&X)[KS][RG], u32x4 (&W)[KS][NG]) {
+#pragma unroll
+        for (int r = 0; r < NR; ++r) read_one(lds_dn + slot_r, r, X, W);
+        next_slot_r();
+    };
+    f32x16 acc[RG][NG];
 
     int par = 0;
     Desc cur = describe(tile);
@@ -506,7 +572,7 @@ void down_kernel(DownParams p) {
     for (int q = 0; q < NST; ++q) issue();
     wait_vmcnt<(NST - 1) * L>();
     __builtin_amdgcn_s_barrier();
-    load_frags(a0, b0);
+    load_frags(x0, w0);
     wait_lgkmcnt0();
     bool after_epi = false;
     for (int round = 0;; ++round) {
@@ -517,23 +583,28 @@ void down_kernel(DownParams p) {
 #pragma unroll
         for (int i = 0; i < RG; ++i)
 #pragma unroll
-            for (int j = 0; j < NW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        // Read side: block and stage of the stage in registers.
+            for (int j = 0; j < NG; ++j) acc[i][j] = f32x16{};
+        // Read side: which of this wave's row groups use the block of the
+        // stage in registers (bit i: group i), and the stage within it.
+        // After the last block the set is empty (padding stages).
         uint64_t rem_r = cur.all;
-        int cb_r = rem_r ? __builtin_ctzll(rem_r) : 0, kc_r = 0;
+        int kc_r = 0;
+        auto groups = [&]() {
+            const uint64_t low = rem_r & (0ull - rem_r);
+            uint32_t g = 0;
+#pragma unroll
+            for (int i = 0; i < RG; ++i) g |= ((cur.gm[i] & low) != 0 ? 1u : 0u) << i;
+            return g;
+        };
+        uint32_t gset = groups();
         const int nst = cur.nst;
-        // Same step as the up kernel; the MFMAs of a row group run only if
-        // one of its rows uses the stage's block.
-        auto step = [&](auto first, int s, u32x4 (&A)[RG], u32x4 (&Bw)[NW], u32x4 (&A2)[RG],
-                        u32x4 (&B2)[NW]) {
-            if constexpr (decltype(first)::value) {
-                const int n_after = L + (after_epi ? NEPI : 0) + ((s == 1 && has_next) ? NFETCH : 0);
-                wait_vm_after<L, NEPI, NFETCH>(n_after);
-            } else {
-                wait_vmcnt<L>();
-            }
+        auto step = [&](auto first, int s, u32x4 (&X)[KS][RG], u32x4 (&W)[KS][NG], u32x4 (&X2)[KS][RG],
+                        u32x4 (&W2)[KS][NG]) {
+            wait_stage<NST, L, NEPI, NFETCH>(decltype(first)::value, s, after_epi, has_next);
             __builtin_amdgcn_s_barrier();
-            if (s == 0 && has_next) fetch_masks(nxt, par ^ 1);
+            if constexpr (decltype(first)::value) {
+                if (s == 0 && has_next) fetch_masks(nxt, par ^ 1);
+            }
             if (s + NST == nst) {
                 // From here on the stages issued belong to the next tile (or,
                 // past the last tile, re-read this tile's first stages into
@@ -547,47 +618,67 @@ void down_kernel(DownParams p) {
                 if (has_next) D = nxt;
                 issue_tile(D, has_next ? par ^ 1 : par);
             }
-            issue_begin();
-            load_frags(A2, B2);
-            const bool real = s < cur.nreal;
+            const char* st2 = lds_dn + slot_r;
+            next_slot_r();
 #pragma unroll
-            for (int i = 0; i < RG; ++i) {
-                if (real && ((cur.gm[i] >> cb_r) & 1ull)) {
+            for (int u = 0; u < NU; ++u) {
+                const int k = u / RG, i = u % RG;
+                if (gset & (1u << i)) {
 #pragma unroll
-                    for (int j = 0; j < NW; ++j)
-                        acc[i][j] = mfma16x16x32(as_bf16x8(Bw[j]), as_bf16x8(A[i]), acc[i][j]);
+                    for (int j = 0; j < NG; ++j)
+                        acc[i][j] = mfma32x32x16(as_bf16x8(W[k][j]), as_bf16x8(X[k][i]), acc[i][j]);
                 }
 #pragma unroll
+                for (int r = 0; r < NR; ++r)
+                    if (r * (NU - 1) / NR == u) read_one(st2, r, X2, W2);
+#pragma unroll
                 for (int q = 0; q < L; ++q)
-                    if (q * RG / L == i) issue_one(q);
+                    if (q * NU / L == u) issue_one(q);
                 __builtin_amdgcn_sched_barrier(0);
             }
             issue_end();
             if (++kc_r == kcpb) {
                 kc_r = 0;
                 rem_r &= rem_r - 1;
-                cb_r = rem_r ? __builtin_ctzll(rem_r) : 0;
+                gset = groups();
             }
             // The fragments just read must be in registers before the next
             // barrier lets another wave refill their slot.
             wait_lgkmcnt0();
         };
-        step(std::true_type{}, 0, a0, b0, a1, b1);
-        step(std::true_type{}, 1, a1, b1, a0, b0);
-        for (int s = 2; s < nst; s += 2) {
-            step(std::false_type{}, s, a0, b0, a1, b1);
-            step(std::false_type{}, s + 1, a1, b1, a0, b0);
+        // Steps 0 .. NST - 2 carry the first-steps wait accounting; nst is
+        // even and at least NST + 1.
+        step(std::true_type{}, 0, x0, w0, x1, w1);
+        step(std::true_type{}, 1, x1, w1, x0, w0);
+        int s = 2;
+        if constexpr (NST >= 4) {
+            step(std::true_type{}, 2, x0, w0, x1, w1);
+            step(std::true_type{}, 3, x1, w1, x0, w0);
+            s = 4;
         }
-        // fp32 per-expert rows; lane stores 8 consecutive columns of its row.
+        for (; s < nst; s += 2) {
+            step(std::false_type{}, s, x0, w0, x1, w1);
+            step(std::false_type{}, s + 1, x1, w1, x0, w0);
+        }
+        // fp32 per-expert rows; lane stores 16 consecutive columns of its row
+        // per 32-column group.
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
-            const int r = wm * (TM / 2) + i * 16 + lr;
+            const int r = wm * (TM / 2) + i * 32 + lr;
             float* dst = (r < cur.nrows) ? p.part + (size_t)(cur.p0 + r) * p.d + (size_t)cur.ct * BN : p.part_sink;
-            dst += wn * (BN / 2) + 8 * lg;
+            dst += wn * (BN / 2) + 16 * lh;
 #pragma unroll
-            for (int J = 0; J < NW / 2; ++J) {
-                st16(dst + 32 * J, __builtin_bit_cast(u32x4, acc[i][2 * J]));
-                st16(dst + 32 * J + 4, __builtin_bit_cast(u32x4, acc[i][2 * J + 1]));
+            for (int j = 0; j < NG; ++j) {
+                const f32x16 v = acc[i][j];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    u32x4 w;
+                    w[0] = __float_as_uint(v[4 * t]);
+                    w[1] = __float_as_uint(v[4 * t + 1]);
+                    w[2] = __float_as_uint(v[4 * t + 2]);
+                    w[3] = __float_as_uint(v[4 * t + 3]);
+                    st16(dst + 32 * j + 4 * t, w);
+                }
             }
         }
         if (!has_next) break;

@@ -35,30 +35,18 @@ namespace {
 constexpr int kKeyBitsMax = 10;
 constexpr size_t kLdsLimit = 160 * 1024;
 
-// Expert-GEMM tile shapes. Two workgroups share each CU (kGemmOcc), so the
-// ring of one runs while the other waits at a barrier or in its epilogue.
-// Up: 128 gathered rows x the whole block width M, K staged 32 deep, 3
-// stages. Down: 128 pairs x 256 output columns (128 when d is not a
-// multiple of 256).
-constexpr int kGemmOcc = 2;
-constexpr int kUpTM = 128, kUpRB = 64, kUpNST = 3;
+// Expert-GEMM tile shapes, one workgroup per CU. Up: 128 gathered rows x
+// the whole block width M. Down: 128 pairs x 256 output columns (128 when d
+// is not a multiple of 256). Both stage K 64 deep in a 3-stage ring.
+constexpr int kUpTM = 128, kGemmNST = 3;
 // Up tiles are ordered by expert, then by groups of this many blocks, then
 // row chunk, then block: the tiles that run together share token rows
 // (across the group's blocks) and weight slabs (within a group).
 constexpr int kUpBlockGroup = 4;
-constexpr int kUpTMWide = 64;  // M = 256: half-height tiles keep the registers in budget
-int up_tm(int M) { return M > 192 ? kUpTMWide : kUpTM; }
 constexpr int kDownTM = 128;
-constexpr int kDownBNWide = 256, kDownWideRB = 64, kDownWideNST = 3;
-constexpr int kDownBNNarrow = 128, kDownNarrowRB = 64, kDownNarrowNST = 3;
-static_assert(kGemmOcc * up_lds_bytes(kUpTM, 256, kUpRB, kUpNST) <= 160 * 1024, "up ring exceeds LDS");
-// The up kernel's pipeline needs at least 2 NST - 2 stages per tile; the
-// smallest supported d (128) gives 128 / (RB / 2).
-static_assert(128 / (kUpRB / 2) >= 2 * kUpNST - 2, "too few stages per up tile");
-static_assert(kGemmOcc * down_lds_bytes(kDownTM, kDownBNWide, kDownWideRB, kDownWideNST) <= 160 * 1024 - 4096,
-              "down ring exceeds LDS");
-static_assert(kGemmOcc * down_lds_bytes(kDownTM, kDownBNNarrow, kDownNarrowRB, kDownNarrowNST) <= 160 * 1024 - 4096,
-              "down ring exceeds LDS");
+constexpr int kDownBNWide = 256, kDownBNNarrow = 128;
+static_assert(up_lds_bytes(kUpTM, 256, kGemmNST) <= 160 * 1024, "up ring exceeds LDS");
+static_assert(down_lds_bytes(kDownTM, kDownBNWide, kGemmNST) <= 160 * 1024, "down ring exceeds LDS");
 
 struct Dims {
     int N, d, K, B, M, H, K1, NL, NLP, lstride, key_bits, nslab, nbin;
@@ -199,7 +187,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.pair_of = cv.take(4 * N * K1);
     // Slab row lists: at most K B rows per token (b + k (B - b) <= K B), each
     // slab padded to whole up tiles.
-    const size_t tm = (size_t)up_tm(m.M);
+    const size_t tm = (size_t)kUpTM;
     const size_t up_tiles = ceil_div_sz(N * K * (size_t)m.B, tm) + (size_t)m.nslab;
     p.slab_rows = cv.take(m.bf16 ? 4 * up_tiles * tm : 0);
     p.slab_tok = cv.take(m.bf16 ? 4 * up_tiles * tm : 0);
@@ -446,7 +434,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.B = m.B;
     pp.key_bits = m.key_bits;
     const int down_bn = (m.d % kDownBNWide == 0) ? kDownBNWide : kDownBNNarrow;
-    pp.bm_up = up_tm(m.M);
+    pp.bm_up = kUpTM;
     pp.up_group = kUpBlockGroup;
     pp.bm_down = kDownTM;
     pp.down_col_tiles = m.bf16 ? m.d / down_bn : 1;
@@ -508,13 +496,13 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         up.tile_info = pp.up_tile_info;
         up.tile_rows = pp.up_tile_rows;
         up.totals = totals;
-        const size_t up_lds = (size_t)up_lds_bytes(up_tm(m.M), m.M, kUpRB, kUpNST);
-        const int grid = (kGemmOcc * cus / kXcds) * kXcds;
-        switch (m.M / 32) {
-            case 2: s = launch_persistent(up_kernel<2, kUpTM, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
-            case 4: s = launch_persistent(up_kernel<4, kUpTM, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
-            case 6: s = launch_persistent(up_kernel<6, kUpTM, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
-            case 8: s = launch_persistent(up_kernel<8, kUpTMWide, kUpRB, kUpNST, kGemmOcc>, grid, up_lds, st, up); break;
+        const size_t up_lds = (size_t)up_lds_bytes(kUpTM, m.M, kGemmNST);
+        const int grid = (cus / kXcds) * kXcds;
+        switch (m.M / 64) {
+            case 1: s = launch_persistent(up_kernel<1, kUpTM, kGemmNST>, grid, up_lds, st, up); break;
+            case 2: s = launch_persistent(up_kernel<2, kUpTM, kGemmNST>, grid, up_lds, st, up); break;
+            case 3: s = launch_persistent(up_kernel<3, kUpTM, kGemmNST>, grid, up_lds, st, up); break;
+            case 4: s = launch_persistent(up_kernel<4, kUpTM, kGemmNST>, grid, up_lds, st, up); break;
             default: return UNIF_EUNSUPPORTED;
         }
         if (s != UNIF_OK) return s;
@@ -536,12 +524,11 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         dn.tiles = pp.down_tiles;
         dn.totals = totals;
         if (down_bn == kDownBNWide)
-            s = launch_persistent(down_kernel<kDownBNWide / 32, kDownTM, kDownWideRB, kDownWideNST, kGemmOcc>, grid,
-                                  (size_t)down_lds_bytes(kDownTM, kDownBNWide, kDownWideRB, kDownWideNST), st, dn);
+            s = launch_persistent(down_kernel<kDownBNWide / 64, kDownTM, kGemmNST>, grid,
+                                  (size_t)down_lds_bytes(kDownTM, kDownBNWide, kGemmNST), st, dn);
         else
-            s = launch_persistent(down_kernel<kDownBNNarrow / 32, kDownTM, kDownNarrowRB, kDownNarrowNST, kGemmOcc>,
-                                  grid, (size_t)down_lds_bytes(kDownTM, kDownBNNarrow, kDownNarrowRB, kDownNarrowNST),
-                                  st, dn);
+            s = launch_persistent(down_kernel<kDownBNNarrow / 64, kDownTM, kGemmNST>, grid,
+                                  (size_t)down_lds_bytes(kDownTM, kDownBNNarrow, kGemmNST), st, dn);
         if (s != UNIF_OK) return s;
         UNIF_MARK(4);
     } else {
