@@ -17,8 +17,8 @@ struct CombineParams {
     void* Y;
 };
 
-// bf16 output: one thread per 8 consecutive outputs; fp32 per-expert rows
-// (two 16-byte loads each), one 16-byte store.
+// bf16 path: one thread per 8 consecutive outputs; bf16 per-expert rows
+// (one 16-byte load each), one 16-byte store.
 __global__ void combine_bf16_kernel(CombineParams c) {
     const int chunks = c.d >> 3;
     const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -26,16 +26,15 @@ __global__ void combine_bf16_kernel(CombineParams c) {
     const int t = (int)(item / chunks), ch = (int)(item - (size_t)t * chunks);
     const int k = c.nres[t];
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    const float* part = static_cast<const float*>(c.part);
+    const u16* part = static_cast<const u16*>(c.part);
     for (int i = 0; i <= k && k > 0; ++i) {
         const float w = (i == 0) ? c.alpha[t] : c.wts[(size_t)t * c.K + i - 1];
         const int pr = c.pair_of[(size_t)t * (c.K + 1) + i];
-        const float* src = part + (size_t)pr * c.d + ch * 8;
-        const u32x4 v0 = ld16(src), v1 = ld16(src + 4);
+        const u32x4 v = ld16(part + (size_t)pr * c.d + ch * 8);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            acc[q] = fmaf(w, __uint_as_float(v0[q]), acc[q]);
-            acc[4 + q] = fmaf(w, __uint_as_float(v1[q]), acc[4 + q]);
+            acc[2 * q] = fmaf(w, __uint_as_float(v[q] << 16), acc[2 * q]);
+            acc[2 * q + 1] = fmaf(w, __uint_as_float(v[q] & 0xffff0000u), acc[2 * q + 1]);
         }
     }
     u32x4 o;

@@ -16,11 +16,11 @@
 // tiles hold similar masks.
 //
 // Engine shared by both kernels:
-//  * One workgroup of 4 waves per CU, 2 x 2: each wave owns TM/2 rows and
-//    half of the tile's columns, in 32 x 32 MFMA groups
-//    (v_mfma_f32_32x32x16_bf16: one wave per SIMD keeps the matrix core
-//    busier with these than with 16 x 16 groups, and the 32-cycle issue
-//    shadow hides the copies, LDS reads and bookkeeping).
+//  * One workgroup of 8 waves per CU (two per SIMD), 4 x 2: each wave owns
+//    64 of the tile's 256 rows and half of its columns, in 32 x 32 MFMA
+//    groups (v_mfma_f32_32x32x16_bf16). The 256-row tile is what the copy
+//    path of a CU can feed: the bytes staged per MFMA flop fall by a third
+//    against 128-row tiles.
 //  * The product is formed transposed, weights as the MFMA A operand and
 //    token rows as B, so each lane accumulates output columns of one row.
 //    Weight rows are placed in LDS so that lane l of a 32-column group holds
@@ -33,9 +33,13 @@
 //    chunks per instruction) free of LDS bank conflicts.
 //  * Stages are filled by global_load_lds_dwordx4 (no register staging): one
 //    instruction fills 8 rows, each lane fetching the global chunk that
-//    belongs in its swizzled slot. NST stages rotate; NST - 1 are in flight
-//    while one is consumed. Waits are explicit vmcnt counts followed by a
-//    bare s_barrier (a __syncthreads fence would drain every load).
+//    belongs in its swizzled slot. Two stage slots alternate. Fragments are
+//    read from LDS one 16-deep k step ahead into two register sets; before
+//    the last k step of stage s the waves wait for stage s + 1 and meet at
+//    a barrier, after which every wave holds all of stage s in registers, so
+//    its slot is refilled with stage s + 2 while stage s + 1 is consumed.
+//    Waits are explicit vmcnt counts followed by a bare s_barrier (a
+//    __syncthreads fence would drain every load).
 //  * Persistent over a device-built tile table, with consecutive tiles mapped
 //    to workgroups of the same XCD (dispatch is round-robin over 8 XCDs), so
 //    co-running tiles share weight slabs in that XCD's L2.
@@ -45,7 +49,9 @@
 
 namespace unifmoe {
 
-constexpr int kFfnThreads = 256;
+constexpr int kFfnThreads = 512;
+constexpr int kFfnWaves = 8;
+constexpr int kFfnTM = 256;   // rows per tile (4 waves x 2 groups of 32)
 constexpr int kXcds = 8;
 
 struct UpParams {
@@ -66,8 +72,8 @@ struct DownParams {
     const u16* Hbuf;
     const u16* zero16;           // 16 zero bytes: the source of rows that lack a block
     const u16* Wdown;
-    float* part;
-    float* part_sink;            // one d row that absorbs the stores of unused tile rows
+    u16* part;                   // per-pair output rows, bf16
+    u16* part_sink;              // one d row that absorbs the stores of unused tile rows
     const int4* rt_info;         // per row tile: first pair, rows, expert
     const uint64_t* rt_masks;    // per row tile: block-mask union of each 16-row group, then of the tile
     const uint64_t* pair_mask;   // readable for a whole tile past the last pair
@@ -96,10 +102,10 @@ struct Stage {
 // rows are the columns 16 (l / 32) + 4 j + i.
 __device__ __forceinline__ int wcol(int r) { return 16 * ((r >> 2) & 1) + 4 * (r >> 3) + (r & 3); }
 
-// Dynamic LDS bytes of the two kernels: the stage ring, plus the row lists
+// Dynamic LDS bytes of the two kernels: two stage slots, plus the row lists
 // of the current and the next tile (up: tokens and pairs; down: block masks).
-__host__ __device__ constexpr int up_lds_bytes(int TM, int M, int NST) { return NST * (TM + M) * Stage::RB + 16 * TM; }
-__host__ __device__ constexpr int down_lds_bytes(int TM, int BN, int NST) { return NST * (TM + BN) * Stage::RB + 16 * TM; }
+__host__ __device__ constexpr int up_lds_bytes(int M) { return 2 * (kFfnTM + M) * Stage::RB + 16 * kFfnTM; }
+__host__ __device__ constexpr int down_lds_bytes(int BN) { return 2 * (kFfnTM + BN) * Stage::RB + 16 * kFfnTM; }
 
 // Tile handled by this workgroup in persistent round `round`: a contiguous
 // range of tiles per XCD. gridDim.x is a multiple of kXcds.
@@ -122,56 +128,43 @@ __device__ __forceinline__ void wait_vm_after(int n) {
     else wait_vmcnt<0>();
 }
 
-// Wait before step s of a tile reads stage s + 1. Issued after that stage:
-// the later stages still in flight (NST - 2 of them), and in the first
-// NST - 1 steps also the previous tile's epilogue stores (issued after stage
-// NST - 1) and, from step 1 on, the next tile's row-list copy (issued at
-// step 0, before stage NST).
-template <int NST, int L, int NEPI, int NFETCH>
-__device__ __forceinline__ void wait_stage(bool first, int s, bool after_epi, bool has_next) {
-    if (first && s <= NST - 2) {
-        const int n = (NST - 2) * L + (after_epi ? NEPI : 0) + ((s >= 1 && has_next) ? NFETCH : 0);
-        wait_vm_after<(NST - 2) * L, NEPI, NFETCH>(n);
-    } else {
-        wait_vmcnt<(NST - 2) * L>();
-    }
+// Wait at the barrier of stage s of a tile, for stage s + 1. Only stage
+// s + 1 is in flight then, plus what was issued after it: at s = 0 the
+// previous tile's epilogue stores, at s = 1 the next tile's row-list copy.
+template <int NEPI, int NFETCH>
+__device__ __forceinline__ void wait_stage(int s, bool after_epi, bool has_next) {
+    const int n = (s == 0 && after_epi) ? NEPI : ((s == 1 && has_next) ? NFETCH : 0);
+    wait_vm_after<0, NEPI, NFETCH>(n);
 }
 
 // Up-projection, persistent and pipelined across tiles.
-//  * Ring of NST stages filled by copies into LDS; a stage's fragments are
-//    read into registers one stage ahead (two register sets), so the matrix
-//    cores never wait on LDS latency and a slot is refilled as soon as its
-//    fragments are in registers: NST - 1 stages stay in flight while the
-//    next one is read.
-//  * The ring runs on from one tile into the next: the next tile's first
-//    stages are issued during the current tile's last iterations, and its
-//    row lists (tokens, pairs) are copied to LDS at the current tile's first
-//    iteration, so there is no cold prologue between tiles.
-//  * Vector-memory operations complete in issue order for vmcnt: before a
-//    stage is read, at most the loads issued after it (later stages, the
-//    previous tile's epilogue stores, a row-list copy) may be outstanding.
-//    Every epilogue store is issued (rows past the tile's count write the
-//    sink row), so the count is exact.
-//  * A tile has nk = d / 64 stages; tiles shorter than NST + 1 stages are
-//    padded with stages that re-read k = 0.. and run no MFMAs.
-template <int MG, int TM, int NST>
-__global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+//  * The copies run on from one tile into the next: the next tile's first
+//    two stages are issued during the current tile's last two stages, and
+//    its row lists (tokens, pairs) are copied to LDS during stage 0, so
+//    there is no cold prologue between tiles.
+//  * Vector-memory operations complete in issue order for vmcnt; every
+//    epilogue store is issued (rows past the tile's count write the sink
+//    row), so the counts are exact.
+//  * A tile has nk = d / 64 stages; tiles shorter than 4 stages are padded
+//    with stages that re-read k = 0.. and run no MFMAs (the row-list copy of
+//    stage 0 is waited for at the barrier of stage 2).
+template <int MG>
+__global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void up_kernel(UpParams p) {
     using S = Stage;
-    constexpr int RB = S::RB, KS = S::KSTEPS;
+    constexpr int RB = S::RB, KS = S::KSTEPS, TM = kFfnTM, NWV = kFfnWaves;
     constexpr int M = MG * 64;                        // MG 32-column groups per wave
-    constexpr int RG = TM / 64;                       // 32-row groups per wave
-    constexpr int LA = TM / S::ROWS_PER_DMA / 4;      // token-row copies per wave per stage
-    constexpr int LB = M / S::ROWS_PER_DMA / 4;       // weight-row copies per wave per stage
+    constexpr int RG = 2;                             // 32-row groups per wave
+    constexpr int LA = TM / S::ROWS_PER_DMA / NWV;    // token-row copies per wave per stage
+    constexpr int LB = M / S::ROWS_PER_DMA / NWV;     // weight-row copies per wave per stage
     constexpr int L = LA + LB;
     constexpr int NEPI = RG * MG * 2;                 // epilogue stores per wave
-    constexpr int A_BYTES = TM * RB, STAGE = (TM + M) * RB, RING = NST * STAGE;
-    constexpr int NU = KS * RG;                       // MFMA units per stage
-    static_assert(LA >= 1 && LB >= 1, "tile too small for one copy per wave");
-    static_assert(TM * 4 <= 32 * 16, "a row list must fit one half-wave copy");
-    static_assert(NST >= 3 && NST <= 5, "ring depth");
+    constexpr int A_BYTES = TM * RB, STAGE = (TM + M) * RB, RING = 2 * STAGE;
     constexpr int NFETCH = 1;                         // copies per wave for a tile's row lists
-    static_assert((NST - 2) * L + NEPI + NFETCH < 64, "vmcnt range");
+    constexpr int NR = RG + MG;                       // fragment reads per k step
+    static_assert(LA >= 1 && LB >= 1, "tile too small for one copy per wave");
+    static_assert(2 * TM * 4 == NWV * 64 * 4, "row lists: one 4-byte copy per wave");
+    static_assert(NEPI + NFETCH + L < 64, "vmcnt range");
     extern __shared__ __attribute__((aligned(16))) char lds_up[];
     // rows[par][0] tokens, rows[par][1] pairs of the tile with parity par
     int* rows = reinterpret_cast<int*>(lds_up + RING);
@@ -179,8 +172,8 @@ void up_kernel(UpParams p) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     const int n_tiles = ld_uniform(p.totals + 1);
-    const int nk = p.d / S::SK;                       // real stages per tile (even)
-    const int nst = (max(nk, NST + 1) + 1) & ~1;      // stages per tile, padding included (even)
+    const int nk = p.d / S::SK;                       // real stages per tile
+    const int nst = max(nk, 4);                       // stages per tile, padding included
     int tile = xcd_tile(0);
     if (tile >= n_tiles) return;
 
@@ -191,7 +184,7 @@ void up_kernel(UpParams p) {
     uint32_t fx[KS], fw[KS];
 #pragma unroll
     for (int k = 0; k < KS; ++k) {
-        fx[k] = S::off(wm * (TM / 2) + lr, 2 * k + lh);
+        fx[k] = S::off(wm * 64 + lr, 2 * k + lh);
         fw[k] = A_BYTES + S::off(wn * (M / 2) + lr, 2 * k + lh);
     }
     // Copy sources: per-lane addresses fixed for a tile, plus the k position
@@ -209,15 +202,12 @@ void up_kernel(UpParams p) {
     const char* srcA[LA];   // token rows of the tile being issued
     const char* wslab = wup;
 
-    // A tile's token and pair lists (TM ints each) are copied by waves 0/2
-    // and 1/3 (both copies of a list land on the same bytes), so that every
-    // wave issues the same number of vector-memory operations.
+    // A tile's token and pair lists (TM ints each): each wave copies 256
+    // bytes, so that every wave issues the same number of operations.
     auto fetch_rows = [&](int t, int par) {
-        if (lane < TM / 4) {
-            const int which = wave & 1;
-            const int* src = (which == 0 ? p.slab_tok : p.slab_rows) + ld_uniform(p.tile_rows + t) + lane * 4;
-            dma16(src, rows + (par * 2 + which) * TM);
-        }
+        const int which = wave >> 2, part = wave & 3;
+        const int* src = (which == 0 ? p.slab_tok : p.slab_rows) + ld_uniform(p.tile_rows + t) + part * 64 + lane;
+        dma4(src, rows + (par * 2 + which) * TM + part * 64);
     };
     auto sources = [&](int par, int inf) {
         const int sl = inf & 0xffff, nrows = inf >> 16;
@@ -231,41 +221,24 @@ void up_kernel(UpParams p) {
             srcA[j] = reinterpret_cast<const char*>(p.X) + (size_t)tok * row_bytes + ch * 16;
         }
     };
-    // Ring slot (byte offset) of the next stage to issue and of the next
-    // stage to read, and the k offset (bytes) of the next stage to issue.
-    uint32_t slot_w = 0, slot_r = 0;
+    // k offset (bytes) of the next stage to issue.
     uint32_t k_w = 0;
-    auto issue_one = [&](int q) {
-        char* base = lds_up + slot_w;
+    auto issue_one = [&](uint32_t slot, int q) {
+        char* base = lds_up + slot;
         if (q < LA) dma16(srcA[q] + k_w, base + (wave * LA + q) * 1024);
         else dma16(wslab + k_w + voffB[q - LA], base + A_BYTES + (wave * LB + q - LA) * 1024);
     };
     auto issue_end = [&]() {
-        slot_w = (slot_w == (NST - 1) * STAGE) ? 0u : slot_w + STAGE;
         k_w += RB;
         if (k_w == row_bytes) k_w = 0;    // padding stages re-read the row start
     };
-    auto issue = [&]() {
-#pragma unroll
-        for (int q = 0; q < L; ++q) issue_one(q);
-        issue_end();
-    };
     // Fragments are kept as raw 32-bit words (bf16 vectors in loop-carried
     // registers make the compiler split them into halves).
-    u32x4 x0[KS][RG], w0[KS][MG], x1[KS][RG], w1[KS][MG];
-    // Fragment read r of a stage: k step r / (MG + RG), then its MG weight
-    // and RG token fragments.
-    constexpr int NR = KS * (MG + RG);
-    auto read_one = [&](const char* st, int r, u32x4 (&X)[KS][RG], u32x4 (&W)[KS][MG]) {
-        const int k = r / (MG + RG), t = r % (MG + RG);
-        if (t < MG) W[k][t] = ld16(st + fw[k] + t * 32 * RB);
-        else X[k][t - MG] = ld16(st + fx[k] + (t - MG) * 32 * RB);
-    };
-    auto next_slot_r = [&]() { slot_r = (slot_r == (NST - 1) * STAGE) ? 0u : slot_r + STAGE; };
-    auto load_frags = [&](u32x4 (&X)[KS][RG], u32x4 (&W)[KS][MG]) {
-#pragma unroll
-        for (int r = 0; r < NR; ++r) read_one(lds_up + slot_r, r, X, W);
-        next_slot_r();
+    u32x4 fxa[RG], fwa[MG], fxb[RG], fwb[MG];
+    auto read_one = [&](uint32_t slot, int k, int r, u32x4 (&X)[RG], u32x4 (&W)[MG]) {
+        const char* st = lds_up + slot;
+        if (r < MG) W[r] = ld16(st + fw[k] + r * 32 * RB);
+        else X[r - MG] = ld16(st + fx[k] + (r - MG) * 32 * RB);
     };
     f32x16 acc[RG][MG];
 
@@ -275,11 +248,17 @@ void up_kernel(UpParams p) {
     wait_vmcnt<0>();
     __syncthreads();
     sources(0, info);
-    for (int ks = 0; ks < NST; ++ks) issue();
-    wait_vmcnt<(NST - 1) * L>();
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+        for (int q = 0; q < L; ++q) issue_one(st * STAGE, q);
+        issue_end();
+    }
+    wait_vmcnt<L>();
     __builtin_amdgcn_s_barrier();
-    load_frags(x0, w0);
-    wait_lgkmcnt0();
+#pragma unroll
+    for (int r = 0; r < NR; ++r) read_one(0, 0, r, fxa, fwa);
+    uint32_t slot = 0;          // slot of the stage being computed
     bool after_epi = false;
     for (int round = 0;; ++round) {
         const int next = xcd_tile(round + 1);
@@ -289,76 +268,53 @@ void up_kernel(UpParams p) {
         for (int i = 0; i < RG; ++i)
 #pragma unroll
             for (int j = 0; j < MG; ++j) acc[i][j] = f32x16{};
-        // Fragments of tile stage s are in (X, W): wait for stage s + 1,
-        // refill the slot freed by stage s with the stage NST ahead (of this
-        // tile, of the next tile, or - past the last tile - a harmless
-        // re-read of this tile's first stages into the free slot, which
-        // keeps every iteration's copy count the same), read stage s + 1
-        // into (X2, W2), then run stage s.
-        // FIRST marks s = 0 and 1, where the previous tile's epilogue stores
-        // (issued after stages 0..NST-1 of this tile) and the row-list copy
-        // (issued at s = 0, before stage NST) sit behind the awaited stage.
-        auto step = [&](auto first, int s, u32x4 (&X)[KS][RG], u32x4 (&W)[KS][MG], u32x4 (&X2)[KS][RG],
-                        u32x4 (&W2)[KS][MG]) {
-            wait_stage<NST, L, NEPI, NFETCH>(decltype(first)::value, s, after_epi, has_next);
-            __builtin_amdgcn_s_barrier();
-            if constexpr (decltype(first)::value) {
-                if (s == 0 && has_next) fetch_rows(next, par ^ 1);
-            }
-            if (s + NST == nst) {
-                // From here on the stages issued belong to the next tile.
-                // Its row lists were copied at s == 0, before stage NST,
-                // which has been waited for when s >= NST - 1.
-                if (has_next) {
-                    if (s < NST - 1) {
-                        wait_vmcnt<0>();
-                        __builtin_amdgcn_s_barrier();
+        for (int s = 0; s < nst; ++s) {
+            const bool real = s < nk;
+            const uint32_t other = slot ^ STAGE;
+            // k step k: reads of the next k step into (X2, W2) first (a
+            // whole k step of MFMAs covers their latency), then the MFMAs on
+            // (X, W) by row group; the last k step also issues stage s + 2
+            // into this stage's slot, between the row groups.
+            auto kstep = [&](int k, u32x4 (&X)[RG], u32x4 (&W)[MG], u32x4 (&X2)[RG], u32x4 (&W2)[MG]) {
+                const uint32_t rslot = (k == KS - 1) ? other : slot;
+                const int rk = (k == KS - 1) ? 0 : k + 1;
+#pragma unroll
+                for (int r = 0; r < NR; ++r) read_one(rslot, rk, r, X2, W2);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int i = 0; i < RG; ++i) {
+                    if (real) {
+#pragma unroll
+                        for (int j = 0; j < MG; ++j)
+                            acc[i][j] = mfma32x32x16(as_bf16x8(W[j]), as_bf16x8(X[i]), acc[i][j]);
                     }
-                    sources(par ^ 1, next_info);
+                    if (k == KS - 1) {
+#pragma unroll
+                        for (int q = 0; q < L; ++q)
+                            if (q * RG / L == i) issue_one(slot, q);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
+            };
+            kstep(0, fxa, fwa, fxb, fwb);
+            kstep(1, fxb, fwb, fxa, fwa);
+            kstep(2, fxa, fwa, fxb, fwb);
+            // Stage s is in registers once the k step 3 reads land; stage
+            // s + 1 once this wave's copies of it have, and for all waves
+            // after the barrier.
+            wait_lgkmcnt0();
+            wait_stage<NEPI, NFETCH>(s, after_epi, has_next);
+            __builtin_amdgcn_s_barrier();
+            if (s + 2 == nst) {
+                // The stages issued from here on belong to the next tile, or,
+                // past the last tile, re-read this tile's first ones.
+                sources(has_next ? par ^ 1 : par, has_next ? next_info : info);
                 k_w = 0;
             }
-            const char* st2 = lds_up + slot_r;
-            next_slot_r();
-            const bool real = s < nk;
-            // MFMAs by (k step, row group), with the reads of stage s + 1's
-            // fragments and the copies of stage s + NST spread between them
-            // (no reads after the last group, so they have landed by the
-            // step's end).
-#pragma unroll
-            for (int u = 0; u < NU; ++u) {
-                const int k = u / RG, i = u % RG;
-                if (real) {
-#pragma unroll
-                    for (int j = 0; j < MG; ++j)
-                        acc[i][j] = mfma32x32x16(as_bf16x8(W[k][j]), as_bf16x8(X[k][i]), acc[i][j]);
-                }
-#pragma unroll
-                for (int r = 0; r < NR; ++r)
-                    if (r * (NU - 1) / NR == u) read_one(st2, r, X2, W2);
-#pragma unroll
-                for (int q = 0; q < L; ++q)
-                    if (q * NU / L == u) issue_one(q);
-                __builtin_amdgcn_sched_barrier(0);
-            }
+            kstep(3, fxb, fwb, fxa, fwa);
             issue_end();
-            // The fragments just read must be in registers before the next
-            // barrier lets another wave refill their slot.
-            wait_lgkmcnt0();
-        };
-        // Steps 0 .. NST - 2 carry the first-steps wait accounting; nst is
-        // even and at least NST + 1.
-        step(std::true_type{}, 0, x0, w0, x1, w1);
-        step(std::true_type{}, 1, x1, w1, x0, w0);
-        int s = 2;
-        if constexpr (NST >= 4) {
-            step(std::true_type{}, 2, x0, w0, x1, w1);
-            step(std::true_type{}, 3, x1, w1, x0, w0);
-            s = 4;
-        }
-        for (; s < nst; s += 2) {
-            step(std::false_type{}, s, x0, w0, x1, w1);
-            step(std::false_type{}, s + 1, x1, w1, x0, w0);
+            if (s == 0 && has_next) fetch_rows(next, par ^ 1);
+            slot = other;
         }
         // GELU, round to bf16; lane stores 16 consecutive columns of its row
         // per 32-column group.
@@ -366,7 +322,7 @@ void up_kernel(UpParams p) {
         const int c = sl - (sl / p.B) * p.B;
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
-            const int r = wm * (TM / 2) + i * 32 + lr;
+            const int r = wm * 64 + i * 32 + lr;
             u16* dst = (r < nrows) ? p.Hbuf + (size_t)rows[(par * 2 + 1) * TM + r] * p.H + (size_t)c * M : p.Hsink;
             dst += wn * (M / 2) + 16 * lh;
 #pragma unroll
@@ -392,32 +348,31 @@ void up_kernel(UpParams p) {
     wait_vmcnt<0>();
 }
 
-// Down-projection on the same engine as the up kernel (ring of copies,
-// fragments read one stage ahead, pipelined across tiles). A tile is TM
+// Down-projection on the same engine as the up kernel (two stage slots,
+// fragments read one k step ahead, pipelined across tiles). A tile is 256
 // consecutive pairs of one expert x BN output columns; its stages walk the
 // blocks of the tile's mask union, M/64 stages per block. A row whose mask
 // lacks the stage's block reads the zero page, and a 32-row MFMA group whose
-// rows all lack it skips its MFMAs. Tiles are padded to an even number of at
-// least NST + 1 stages with empty stages (no MFMAs), so the ring never runs
-// more than one tile ahead.
-template <int NG, int TM, int NST>
-__global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+// rows all lack it skips its MFMAs. Tiles are padded to at least 4 stages
+// with empty stages (no MFMAs).
+template <int NG>
+__global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void down_kernel(DownParams p) {
     using S = Stage;
-    constexpr int RB = S::RB, KS = S::KSTEPS;
+    constexpr int RB = S::RB, KS = S::KSTEPS, TM = kFfnTM, NWV = kFfnWaves;
     constexpr int BN = NG * 64;                       // NG 32-column groups per wave
-    constexpr int RG = TM / 64;                       // 32-row groups per wave
+    constexpr int RG = 2;                             // 32-row groups per wave
     constexpr int G16 = TM / 16;                      // 16-row mask groups per tile
-    constexpr int LA = TM / S::ROWS_PER_DMA / 4;
-    constexpr int LB = BN / S::ROWS_PER_DMA / 4;
+    constexpr int LA = TM / S::ROWS_PER_DMA / NWV;
+    constexpr int LB = BN / S::ROWS_PER_DMA / NWV;
     constexpr int L = LA + LB;
-    constexpr int NEPI = RG * NG * 4;                 // epilogue stores per wave
-    constexpr int A_BYTES = TM * RB, STAGE = (TM + BN) * RB, RING = NST * STAGE;
-    constexpr int NU = KS * RG;
+    constexpr int NEPI = RG * NG * 2;                 // epilogue stores per wave
+    constexpr int A_BYTES = TM * RB, STAGE = (TM + BN) * RB, RING = 2 * STAGE;
+    constexpr int NFETCH = 1;                         // 4-byte copies per wave for a tile's row masks
+    constexpr int NR = RG + NG;
     static_assert(LA >= 1 && LB >= 1, "tile too small for one copy per wave");
-    constexpr int NFETCH = TM * 8 / 256;              // 4-byte copies per wave for a tile's row masks
-    static_assert(NST >= 3 && NST <= 5, "ring depth");
-    static_assert((NST - 2) * L + NEPI + NFETCH < 64, "vmcnt range");
+    static_assert(TM * 8 == NWV * 64 * 4, "row masks: one 4-byte copy per wave");
+    static_assert(NEPI + NFETCH + L < 64, "vmcnt range");
     extern __shared__ __attribute__((aligned(16))) char lds_dn[];
     uint64_t* rmask = reinterpret_cast<uint64_t*>(lds_dn + RING);   // [2][TM]
     const int tid = threadIdx.x, lane = tid & 63;
@@ -432,7 +387,7 @@ void down_kernel(DownParams p) {
     uint32_t fx[KS], fw[KS];
 #pragma unroll
     for (int k = 0; k < KS; ++k) {
-        fx[k] = S::off(wm * (TM / 2) + lr, 2 * k + lh);
+        fx[k] = S::off(wm * 64 + lr, 2 * k + lh);
         fw[k] = A_BYTES + S::off(wn * (BN / 2) + lr, 2 * k + lh);
     }
     const uint32_t hrow = (uint32_t)p.H * 2;
@@ -477,15 +432,14 @@ void down_kernel(DownParams p) {
             D.gm[i] = ld_uniform64(ms + g) | ld_uniform64(ms + g + 1);
         }
         D.nreal = __popcll(D.all) * kcpb;
-        D.nst = (max(D.nreal, NST + 1) + 1) & ~1;
+        D.nst = max(D.nreal, 4);
         return D;
     };
-    // A tile's row masks (TM u64) are copied to LDS by every wave, in
+    // A tile's row masks (TM u64, 2 KB): each wave copies 256 bytes in
     // 4-byte pieces (a tile's first pair can be any index).
     auto fetch_masks = [&](Desc D, int par) {
         const uint32_t* src = reinterpret_cast<const uint32_t*>(p.pair_mask + D.p0);
-#pragma unroll
-        for (int q = 0; q < NFETCH; ++q) dma4(src + q * 64 + lane, rmask + par * TM + q * 32);
+        dma4(src + wave * 64 + lane, rmask + par * TM + wave * 32);
     };
 
     // Issue side. Per block, each H-row copy either walks its row (one
@@ -517,23 +471,20 @@ void down_kernel(DownParams p) {
 #pragma unroll
         for (int j = 0; j < LA; ++j) mrow[j] = (rA[j] < D.nrows) ? rmask[par * TM + rA[j]] : 0ull;
         // Settle the mask reads here, so that no later use waits on them
-        // behind the fragment reads of a step.
+        // behind the fragment reads of a k step.
         wait_lgkmcnt0();
         wtile = wdn + ((size_t)D.e * p.d + (size_t)D.ct * BN) * hrow;
         rem_w = D.all;
         kc_w = 0;
         set_block_w();
     };
-    uint32_t slot_w = 0, slot_r = 0;
-    // The copies of one stage: copy q < LA fills H rows, the rest weight
-    // rows. They are issued one at a time between MFMAs (see step).
-    auto issue_one = [&](int q) {
-        char* base = lds_dn + slot_w;
+    // The copies of one stage: copy q < LA fills H rows, the rest weight rows.
+    auto issue_one = [&](uint32_t slot, int q) {
+        char* base = lds_dn + slot;
         if (q < LA) dma16(pa[q], base + (wave * LA + q) * 1024);
         else dma16(pb + voffB[q - LA], base + A_BYTES + (wave * LB + q - LA) * 1024);
     };
     auto issue_end = [&]() {
-        slot_w = (slot_w == (NST - 1) * STAGE) ? 0u : slot_w + STAGE;
 #pragma unroll
         for (int q = 0; q < LA; ++q) pa[q] += sa[q];
         pb += RB;
@@ -543,23 +494,11 @@ void down_kernel(DownParams p) {
             set_block_w();
         }
     };
-    auto issue = [&]() {
-#pragma unroll
-        for (int q = 0; q < L; ++q) issue_one(q);
-        issue_end();
-    };
-    u32x4 x0[KS][RG], w0[KS][NG], x1[KS][RG], w1[KS][NG];
-    constexpr int NR = KS * (NG + RG);
-    auto read_one = [&](const char* st, int r, u32x4 (&X)[KS][RG], u32x4 (&W)[KS][NG]) {
-        const int k = r / (NG + RG), t = r % (NG + RG);
-        if (t < NG) W[k][t] = ld16(st + fw[k] + t * 32 * RB);
-        else X[k][t - NG] = ld16(st + fx[k] + (t - NG) * 32 * RB);
-    };
-    auto next_slot_r = [&]() { slot_r = (slot_r == (NST - 1) * STAGE) ? 0u : slot_r + STAGE; };
-    auto load_frags = [&](u32x4 (&X)[KS][RG], u32x4 (&W)[KS][NG]) {
-#pragma unroll
-        for (int r = 0; r < NR; ++r) read_one(lds_dn + slot_r, r, X, W);
-        next_slot_r();
+    u32x4 fxa[RG], fwa[NG], fxb[RG], fwb[NG];
+    auto read_one = [&](uint32_t slot, int k, int r, u32x4 (&X)[RG], u32x4 (&W)[NG]) {
+        const char* st = lds_dn + slot;
+        if (r < NG) W[r] = ld16(st + fw[k] + r * 32 * RB);
+        else X[r - NG] = ld16(st + fx[k] + (r - NG) * 32 * RB);
     };
     f32x16 acc[RG][NG];
 
@@ -569,11 +508,17 @@ void down_kernel(DownParams p) {
     wait_vmcnt<0>();
     __syncthreads();
     issue_tile(cur, 0);
-    for (int q = 0; q < NST; ++q) issue();
-    wait_vmcnt<(NST - 1) * L>();
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+        for (int q = 0; q < L; ++q) issue_one(st * STAGE, q);
+        issue_end();
+    }
+    wait_vmcnt<L>();
     __builtin_amdgcn_s_barrier();
-    load_frags(x0, w0);
-    wait_lgkmcnt0();
+#pragma unroll
+    for (int r = 0; r < NR; ++r) read_one(0, 0, r, fxa, fwa);
+    uint32_t slot = 0;
     bool after_epi = false;
     for (int round = 0;; ++round) {
         const int next = xcd_tile(round + 1);
@@ -585,7 +530,7 @@ void down_kernel(DownParams p) {
 #pragma unroll
             for (int j = 0; j < NG; ++j) acc[i][j] = f32x16{};
         // Read side: which of this wave's row groups use the block of the
-        // stage in registers (bit i: group i), and the stage within it.
+        // stage being computed (bit i: group i), and the stage within it.
         // After the last block the set is empty (padding stages).
         uint64_t rem_r = cur.all;
         int kc_r = 0;
@@ -598,87 +543,73 @@ void down_kernel(DownParams p) {
         };
         uint32_t gset = groups();
         const int nst = cur.nst;
-        auto step = [&](auto first, int s, u32x4 (&X)[KS][RG], u32x4 (&W)[KS][NG], u32x4 (&X2)[KS][RG],
-                        u32x4 (&W2)[KS][NG]) {
-            wait_stage<NST, L, NEPI, NFETCH>(decltype(first)::value, s, after_epi, has_next);
-            __builtin_amdgcn_s_barrier();
-            if constexpr (decltype(first)::value) {
-                if (s == 0 && has_next) fetch_masks(nxt, par ^ 1);
-            }
-            if (s + NST == nst) {
-                // From here on the stages issued belong to the next tile (or,
-                // past the last tile, re-read this tile's first stages into
-                // the free slot). The next tile's row masks were copied at
-                // s == 0, before stage NST, waited for when s >= NST - 1.
-                if (has_next && s < NST - 1) {
-                    wait_vmcnt<0>();
-                    __builtin_amdgcn_s_barrier();
+        for (int s = 0; s < nst; ++s) {
+            const uint32_t other = slot ^ STAGE;
+            auto kstep = [&](int k, u32x4 (&X)[RG], u32x4 (&W)[NG], u32x4 (&X2)[RG], u32x4 (&W2)[NG]) {
+                const uint32_t rslot = (k == KS - 1) ? other : slot;
+                const int rk = (k == KS - 1) ? 0 : k + 1;
+#pragma unroll
+                for (int r = 0; r < NR; ++r) read_one(rslot, rk, r, X2, W2);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int i = 0; i < RG; ++i) {
+                    if (gset & (1u << i)) {
+#pragma unroll
+                        for (int j = 0; j < NG; ++j)
+                            acc[i][j] = mfma32x32x16(as_bf16x8(W[j]), as_bf16x8(X[i]), acc[i][j]);
+                    }
+                    if (k == KS - 1) {
+#pragma unroll
+                        for (int q = 0; q < L; ++q)
+                            if (q * RG / L == i) issue_one(slot, q);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
+            };
+            kstep(0, fxa, fwa, fxb, fwb);
+            kstep(1, fxb, fwb, fxa, fwa);
+            kstep(2, fxa, fwa, fxb, fwb);
+            wait_lgkmcnt0();
+            wait_stage<NEPI, NFETCH>(s, after_epi, has_next);
+            __builtin_amdgcn_s_barrier();
+            if (s + 2 == nst) {
+                // The stages issued from here on belong to the next tile (or,
+                // past the last tile, re-read this tile's first stages). Its
+                // row masks were copied at stage 0 and waited for at the
+                // barrier of stage 2 (s >= 2 here).
                 Desc D = cur;
                 if (has_next) D = nxt;
                 issue_tile(D, has_next ? par ^ 1 : par);
             }
-            const char* st2 = lds_dn + slot_r;
-            next_slot_r();
-#pragma unroll
-            for (int u = 0; u < NU; ++u) {
-                const int k = u / RG, i = u % RG;
-                if (gset & (1u << i)) {
-#pragma unroll
-                    for (int j = 0; j < NG; ++j)
-                        acc[i][j] = mfma32x32x16(as_bf16x8(W[k][j]), as_bf16x8(X[k][i]), acc[i][j]);
-                }
-#pragma unroll
-                for (int r = 0; r < NR; ++r)
-                    if (r * (NU - 1) / NR == u) read_one(st2, r, X2, W2);
-#pragma unroll
-                for (int q = 0; q < L; ++q)
-                    if (q * NU / L == u) issue_one(q);
-                __builtin_amdgcn_sched_barrier(0);
-            }
+            kstep(3, fxb, fwb, fxa, fwa);
             issue_end();
+            if (s == 0 && has_next) fetch_masks(nxt, par ^ 1);
             if (++kc_r == kcpb) {
                 kc_r = 0;
                 rem_r &= rem_r - 1;
                 gset = groups();
             }
-            // The fragments just read must be in registers before the next
-            // barrier lets another wave refill their slot.
-            wait_lgkmcnt0();
-        };
-        // Steps 0 .. NST - 2 carry the first-steps wait accounting; nst is
-        // even and at least NST + 1.
-        step(std::true_type{}, 0, x0, w0, x1, w1);
-        step(std::true_type{}, 1, x1, w1, x0, w0);
-        int s = 2;
-        if constexpr (NST >= 4) {
-            step(std::true_type{}, 2, x0, w0, x1, w1);
-            step(std::true_type{}, 3, x1, w1, x0, w0);
-            s = 4;
+            slot = other;
         }
-        for (; s < nst; s += 2) {
-            step(std::false_type{}, s, x0, w0, x1, w1);
-            step(std::false_type{}, s + 1, x1, w1, x0, w0);
-        }
-        // fp32 per-expert rows; lane stores 16 consecutive columns of its row
-        // per 32-column group.
+        // Per-expert rows, rounded to bf16 (the combine weighs and sums them
+        // in fp32); lane stores 16 consecutive columns of its row per
+        // 32-column group.
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
-            const int r = wm * (TM / 2) + i * 32 + lr;
-            float* dst = (r < cur.nrows) ? p.part + (size_t)(cur.p0 + r) * p.d + (size_t)cur.ct * BN : p.part_sink;
+            const int r = wm * 64 + i * 32 + lr;
+            u16* dst = (r < cur.nrows) ? p.part + (size_t)(cur.p0 + r) * p.d + (size_t)cur.ct * BN : p.part_sink;
             dst += wn * (BN / 2) + 16 * lh;
 #pragma unroll
             for (int j = 0; j < NG; ++j) {
                 const f32x16 v = acc[i][j];
+                u32x4 lo, hi;
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    u32x4 w;
-                    w[0] = __float_as_uint(v[4 * t]);
-                    w[1] = __float_as_uint(v[4 * t + 1]);
-                    w[2] = __float_as_uint(v[4 * t + 2]);
-                    w[3] = __float_as_uint(v[4 * t + 3]);
-                    st16(dst + 32 * j + 4 * t, w);
+                    lo[t] = pack_bf16x2(v[2 * t], v[2 * t + 1]);
+                    hi[t] = pack_bf16x2(v[8 + 2 * t], v[9 + 2 * t]);
                 }
+                st16(dst + 32 * j, lo);
+                st16(dst + 32 * j + 8, hi);
             }
         }
         if (!has_next) break;

@@ -35,18 +35,18 @@ namespace {
 constexpr int kKeyBitsMax = 10;
 constexpr size_t kLdsLimit = 160 * 1024;
 
-// Expert-GEMM tile shapes, one workgroup per CU. Up: 128 gathered rows x
-// the whole block width M. Down: 128 pairs x 256 output columns (128 when d
-// is not a multiple of 256). Both stage K 64 deep in a 3-stage ring.
-constexpr int kUpTM = 128, kGemmNST = 3;
+// Expert-GEMM tile shapes, one workgroup of 8 waves per CU. Up: 256
+// gathered rows x the whole block width M. Down: 256 pairs x 256 output
+// columns (128 when d is not a multiple of 256).
+constexpr int kUpTM = kFfnTM;
 // Up tiles are ordered by expert, then by groups of this many blocks, then
 // row chunk, then block: the tiles that run together share token rows
 // (across the group's blocks) and weight slabs (within a group).
 constexpr int kUpBlockGroup = 4;
-constexpr int kDownTM = 128;
+constexpr int kDownTM = kFfnTM;
 constexpr int kDownBNWide = 256, kDownBNNarrow = 128;
-static_assert(up_lds_bytes(kUpTM, 256, kGemmNST) <= 160 * 1024, "up ring exceeds LDS");
-static_assert(down_lds_bytes(kDownTM, kDownBNWide, kGemmNST) <= 160 * 1024, "down ring exceeds LDS");
+static_assert(up_lds_bytes(256) <= 160 * 1024, "up stages exceed LDS");
+static_assert(down_lds_bytes(kDownBNWide) <= 160 * 1024, "down stages exceed LDS");
 
 struct Dims {
     int N, d, K, B, M, H, K1, NL, NLP, lstride, key_bits, nslab, nbin;
@@ -198,7 +198,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.chunk_off = cv.take(m.bf16 ? 4 * (K1 + 1) : 0);
     p.chunk_cnt = cv.take(m.bf16 ? 4 * p.max_chunks * (size_t)m.B : 0);
     p.hbuf = cv.take(m.bf16 ? (pmax + 1) * (size_t)m.H * 2 : 0);  // + the sink row
-    p.part = cv.take((pmax + 1) * (size_t)m.d * sizeof(float));   // + the sink row
+    p.part = cv.take((pmax + 1) * (size_t)m.d * (m.bf16 ? 2 : sizeof(float)));   // + the sink row
     p.max_row_tiles = ceil_div_sz(pmax, kDownTM) + K1;
     p.rt_info = cv.take(m.bf16 ? 16 * p.max_row_tiles : 0);
     p.rt_masks = cv.take(m.bf16 ? 8 * (kDownTM / 16 + 1) * p.max_row_tiles : 0);
@@ -496,13 +496,13 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         up.tile_info = pp.up_tile_info;
         up.tile_rows = pp.up_tile_rows;
         up.totals = totals;
-        const size_t up_lds = (size_t)up_lds_bytes(kUpTM, m.M, kGemmNST);
+        const size_t up_lds = (size_t)up_lds_bytes(m.M);
         const int grid = (cus / kXcds) * kXcds;
         switch (m.M / 64) {
-            case 1: s = launch_persistent(up_kernel<1, kUpTM, kGemmNST>, grid, up_lds, st, up); break;
-            case 2: s = launch_persistent(up_kernel<2, kUpTM, kGemmNST>, grid, up_lds, st, up); break;
-            case 3: s = launch_persistent(up_kernel<3, kUpTM, kGemmNST>, grid, up_lds, st, up); break;
-            case 4: s = launch_persistent(up_kernel<4, kUpTM, kGemmNST>, grid, up_lds, st, up); break;
+            case 1: s = launch_persistent(up_kernel<1>, grid, up_lds, st, up); break;
+            case 2: s = launch_persistent(up_kernel<2>, grid, up_lds, st, up); break;
+            case 3: s = launch_persistent(up_kernel<3>, grid, up_lds, st, up); break;
+            case 4: s = launch_persistent(up_kernel<4>, grid, up_lds, st, up); break;
             default: return UNIF_EUNSUPPORTED;
         }
         if (s != UNIF_OK) return s;
@@ -516,7 +516,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         dn.zero16 = reinterpret_cast<const u16*>(ws + plan.zero_page);
         dn.Hbuf = up.Hbuf;
         dn.Wdown = static_cast<const u16*>(W_down);
-        dn.part = static_cast<float*>(part);
+        dn.part = static_cast<u16*>(part);
         dn.part_sink = dn.part + (size_t)m.N * m.K1 * m.d;
         dn.rt_info = pp.rt_info;
         dn.rt_masks = pp.rt_masks;
@@ -524,11 +524,9 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         dn.tiles = pp.down_tiles;
         dn.totals = totals;
         if (down_bn == kDownBNWide)
-            s = launch_persistent(down_kernel<kDownBNWide / 64, kDownTM, kGemmNST>, grid,
-                                  (size_t)down_lds_bytes(kDownTM, kDownBNWide, kGemmNST), st, dn);
+            s = launch_persistent(down_kernel<kDownBNWide / 64>, grid, (size_t)down_lds_bytes(kDownBNWide), st, dn);
         else
-            s = launch_persistent(down_kernel<kDownBNNarrow / 64, kDownTM, kGemmNST>, grid,
-                                  (size_t)down_lds_bytes(kDownTM, kDownBNNarrow, kGemmNST), st, dn);
+            s = launch_persistent(down_kernel<kDownBNNarrow / 64>, grid, (size_t)down_lds_bytes(kDownBNNarrow), st, dn);
         if (s != UNIF_OK) return s;
         UNIF_MARK(4);
     } else {
