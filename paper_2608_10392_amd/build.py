@@ -11,9 +11,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "csrc", "unif_moe.hip")
 LIB = os.path.join(HERE, "libunifmoe.so")
 
-# Packed fp32 VALU instructions are switched off for all device code.
+# Packed fp32 VALU instructions are switched off for all device code. The
+# atomic optimizer is off: it turns a one-lane atomic with return (the GEMM
+# tile queues) into a wave-wide one whose result is broadcast at once, which
+# drains every copy in flight.
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
-               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+               "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]
 
 
 def hipcc():

@@ -12,6 +12,10 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
+// Copies of the per-(expert, block) row counts that the routing kernel's
+// workgroups add into (spreading same-address atomics); the permutation
+// sums them.
+constexpr int kSlabCopies = 8;
 
 __device__ __forceinline__ float bf2f(u16 v) { return __uint_as_float(((uint32_t)v) << 16); }
 

@@ -40,9 +40,12 @@
 //    its slot is refilled with stage s + 2 while stage s + 1 is consumed.
 //    Waits are explicit vmcnt counts followed by a bare s_barrier (a
 //    __syncthreads fence would drain every load).
-//  * Persistent over a device-built tile table, with consecutive tiles mapped
-//    to workgroups of the same XCD (dispatch is round-robin over 8 XCDs), so
-//    co-running tiles share weight slabs in that XCD's L2.
+//  * Persistent over a device-built tile table. Each XCD (dispatch is
+//    round-robin over 8 XCDs) owns one contiguous eighth of the table, and
+//    its workgroups take the next tile from a per-XCD counter as they free
+//    up, so consecutive tiles run side by side on one XCD and share its L2
+//    (weight slabs, and the H rows a row tile's column tiles all read).
+//    Which workgroup computes a tile does not change its result.
 #pragma once
 #include <type_traits>
 #include "common.hpp"
@@ -65,6 +68,7 @@ struct UpParams {
     const int* tile_info;    // slab | rows << 16
     const int* tile_rows;    // first entry of the tile's rows in slab_rows / slab_tok
     const int* totals;
+    int* queue;              // 8 per-XCD tile counters, zero at launch
 };
 
 struct DownParams {
@@ -79,6 +83,7 @@ struct DownParams {
     const uint64_t* pair_mask;   // readable for a whole tile past the last pair
     const int* tiles;            // per down tile: row tile << 8 | column tile
     const int* totals;           // [2]: down tiles
+    int* queue;                  // 8 per-XCD tile counters, zero at launch
 };
 
 // Staged-row geometry: one 128-byte line (64 bf16 of k) per row and stage.
@@ -104,15 +109,26 @@ __device__ __forceinline__ int wcol(int r) { return 16 * ((r >> 2) & 1) + 4 * (r
 
 // Dynamic LDS bytes of the two kernels: two stage slots, plus the row lists
 // of the current and the next tile (up: tokens and pairs; down: block masks).
-__host__ __device__ constexpr int up_lds_bytes(int M) { return 2 * (kFfnTM + M) * Stage::RB + 16 * kFfnTM; }
-__host__ __device__ constexpr int down_lds_bytes(int BN) { return 2 * (kFfnTM + BN) * Stage::RB + 16 * kFfnTM; }
+// The last 16 bytes pass tile indices between waves.
+__host__ __device__ constexpr int up_lds_bytes(int M) { return 2 * (kFfnTM + M) * Stage::RB + 16 * kFfnTM + 16; }
+__host__ __device__ constexpr int down_lds_bytes(int TM, int BN) { return 2 * (TM + BN) * Stage::RB + 16 * TM + 16; }
 
-// Tile handled by this workgroup in persistent round `round`: a contiguous
-// range of tiles per XCD. gridDim.x is a multiple of kXcds.
-__device__ __forceinline__ int xcd_tile(int round) {
-    const int per = gridDim.x / kXcds;
-    return round * gridDim.x + (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
-}
+// Per-XCD tile queue: XCD x (= blockIdx.x % 8) owns tiles [lo, hi) of the
+// table and hands them out in order through counter queue[x]. Indices past
+// hi mean "no tile". gridDim.x is a multiple of kXcds.
+struct TileQueue {
+    int* ctr;
+    int lo, hi;
+    __device__ TileQueue(int* queue, int n_tiles) {
+        const int x = blockIdx.x % kXcds;
+        ctr = queue + x;
+        lo = (int)((int64_t)x * n_tiles / kXcds);
+        hi = (int)((int64_t)(x + 1) * n_tiles / kXcds);
+    }
+    // One lane only (a vector atomic with return); the result is an offset
+    // from lo.
+    __device__ int take(int n) const { return atomicAdd(ctr, n); }
+};
 
 // Wait until at most n vector-memory operations of this wave are pending,
 // for the few counts the GEMM pipelines use (anything else waits for all).
@@ -174,8 +190,20 @@ void up_kernel(UpParams p) {
     const int n_tiles = ld_uniform(p.totals + 1);
     const int nk = p.d / S::SK;                       // real stages per tile
     const int nst = max(nk, 4);                       // stages per tile, padding included
-    int tile = xcd_tile(0);
-    if (tile >= n_tiles) return;
+    const TileQueue tq(p.queue, n_tiles);
+    // ctl[0], ctl[1]: the first two tiles; ctl[2]: the tile after next,
+    // taken at stage 0 of each tile, written at stage 1, read after stage 2.
+    int* ctl = reinterpret_cast<int*>(lds_up + RING + 16 * TM);
+    if (tid == 0) {
+        const int t = tq.take(2);
+        ctl[0] = t;
+        ctl[1] = t + 1;
+    }
+    __syncthreads();
+    int tile = tq.lo + __builtin_amdgcn_readfirstlane(ctl[0]);
+    int next = tq.lo + __builtin_amdgcn_readfirstlane(ctl[1]);
+    if (tile >= tq.hi) return;
+    int taken = 0;
 
     // Fragment addresses inside a stage: lane (lr, lh) reads row base + lr,
     // chunk 2 k + lh of k step k; 32-row steps keep the swizzle, so row
@@ -260,9 +288,8 @@ void up_kernel(UpParams p) {
     for (int r = 0; r < NR; ++r) read_one(0, 0, r, fxa, fwa);
     uint32_t slot = 0;          // slot of the stage being computed
     bool after_epi = false;
-    for (int round = 0;; ++round) {
-        const int next = xcd_tile(round + 1);
-        const bool has_next = next < n_tiles;
+    for (;;) {
+        const bool has_next = next < tq.hi;
         const int next_info = has_next ? ld_uniform(p.tile_info + next) : 0;
 #pragma unroll
         for (int i = 0; i < RG; ++i)
@@ -305,6 +332,10 @@ void up_kernel(UpParams p) {
             wait_lgkmcnt0();
             wait_stage<NEPI, NFETCH>(s, after_epi, has_next);
             __builtin_amdgcn_s_barrier();
+            // The atomic is issued before stage s + 2's copies, so the wait
+            // of stage 1 (for stage 2) covers it.
+            if (s == 0 && has_next && tid == 0) taken = tq.take(1);
+            if (s == 1 && has_next && tid == 0) ctl[2] = taken;
             if (s + 2 == nst) {
                 // The stages issued from here on belong to the next tile, or,
                 // past the last tile, re-read this tile's first ones.
@@ -339,6 +370,8 @@ void up_kernel(UpParams p) {
             }
         }
         if (!has_next) break;
+        tile = next;
+        next = tq.lo + __builtin_amdgcn_readfirstlane(ctl[2]);
         info = next_info;
         par ^= 1;
         after_epi = true;
@@ -349,18 +382,22 @@ void up_kernel(UpParams p) {
 }
 
 // Down-projection on the same engine as the up kernel (two stage slots,
-// fragments read one k step ahead, pipelined across tiles). A tile is 256
-// consecutive pairs of one expert x BN output columns; its stages walk the
+// fragments read one k step ahead, pipelined across tiles). The 8 waves sit
+// WM x (8 / WM); a tile is TM = 64 WM consecutive pairs of one expert x
+// BN = (8 / WM) NG 32 output columns (wide tiles read each pair's H row for
+// fewer column tiles, tall ones each weight slab for fewer rows); its stages walk the
 // blocks of the tile's mask union, M/64 stages per block. A row whose mask
 // lacks the stage's block reads the zero page, and a 32-row MFMA group whose
 // rows all lack it skips its MFMAs. Tiles are padded to at least 4 stages
 // with empty stages (no MFMAs).
-template <int NG>
+template <int WM, int NG>
 __global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void down_kernel(DownParams p) {
     using S = Stage;
-    constexpr int RB = S::RB, KS = S::KSTEPS, TM = kFfnTM, NWV = kFfnWaves;
-    constexpr int BN = NG * 64;                       // NG 32-column groups per wave
+    constexpr int RB = S::RB, KS = S::KSTEPS, NWV = kFfnWaves;
+    constexpr int WN = NWV / WM;
+    constexpr int TM = WM * 64;
+    constexpr int BN = WN * NG * 32;                  // NG 32-column groups per wave
     constexpr int RG = 2;                             // 32-row groups per wave
     constexpr int G16 = TM / 16;                      // 16-row mask groups per tile
     constexpr int LA = TM / S::ROWS_PER_DMA / NWV;
@@ -371,24 +408,35 @@ void down_kernel(DownParams p) {
     constexpr int NFETCH = 1;                         // 4-byte copies per wave for a tile's row masks
     constexpr int NR = RG + NG;
     static_assert(LA >= 1 && LB >= 1, "tile too small for one copy per wave");
-    static_assert(TM * 8 == NWV * 64 * 4, "row masks: one 4-byte copy per wave");
+    static_assert(TM % 32 == 0 && TM / 4 <= 64, "row masks: one 4-byte copy per wave");
     static_assert(NEPI + NFETCH + L < 64, "vmcnt range");
     extern __shared__ __attribute__((aligned(16))) char lds_dn[];
     uint64_t* rmask = reinterpret_cast<uint64_t*>(lds_dn + RING);   // [2][TM]
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
     const int n_tiles = ld_uniform(p.totals + 2);
     const int kcpb = p.M / S::SK;   // stages per block
-    int tile = xcd_tile(0);
-    if (tile >= n_tiles) return;
+    const TileQueue tq(p.queue, n_tiles);
+    // ctl as in the up kernel.
+    int* ctl = reinterpret_cast<int*>(lds_dn + RING + 16 * TM);
+    if (tid == 0) {
+        const int t = tq.take(2);
+        ctl[0] = t;
+        ctl[1] = t + 1;
+    }
+    __syncthreads();
+    int tile = tq.lo + __builtin_amdgcn_readfirstlane(ctl[0]);
+    int next = tq.lo + __builtin_amdgcn_readfirstlane(ctl[1]);
+    if (tile >= tq.hi) return;
+    int taken = 0;
 
     const int lr = lane & 31, lh = lane >> 5;
     uint32_t fx[KS], fw[KS];
 #pragma unroll
     for (int k = 0; k < KS; ++k) {
         fx[k] = S::off(wm * 64 + lr, 2 * k + lh);
-        fw[k] = A_BYTES + S::off(wn * (BN / 2) + lr, 2 * k + lh);
+        fw[k] = A_BYTES + S::off(wn * (BN / WN) + lr, 2 * k + lh);
     }
     const uint32_t hrow = (uint32_t)p.H * 2;
     const uint32_t blk_bytes = (uint32_t)p.M * 2;
@@ -435,11 +483,11 @@ void down_kernel(DownParams p) {
         D.nst = max(D.nreal, 4);
         return D;
     };
-    // A tile's row masks (TM u64, 2 KB): each wave copies 256 bytes in
-    // 4-byte pieces (a tile's first pair can be any index).
+    // A tile's row masks (TM u64): each wave copies TM bytes in 4-byte
+    // pieces (a tile's first pair can be any index).
     auto fetch_masks = [&](Desc D, int par) {
         const uint32_t* src = reinterpret_cast<const uint32_t*>(p.pair_mask + D.p0);
-        dma4(src + wave * 64 + lane, rmask + par * TM + wave * 32);
+        if (lane < TM / 4) dma4(src + wave * (TM / 4) + lane, rmask + par * TM + wave * (TM / 8));
     };
 
     // Issue side. Per block, each H-row copy either walks its row (one
@@ -520,9 +568,8 @@ void down_kernel(DownParams p) {
     for (int r = 0; r < NR; ++r) read_one(0, 0, r, fxa, fwa);
     uint32_t slot = 0;
     bool after_epi = false;
-    for (int round = 0;; ++round) {
-        const int next = xcd_tile(round + 1);
-        const bool has_next = next < n_tiles;
+    for (;;) {
+        const bool has_next = next < tq.hi;
         Desc nxt;
         if (has_next) nxt = describe(next);
 #pragma unroll
@@ -572,6 +619,8 @@ void down_kernel(DownParams p) {
             wait_lgkmcnt0();
             wait_stage<NEPI, NFETCH>(s, after_epi, has_next);
             __builtin_amdgcn_s_barrier();
+            if (s == 0 && has_next && tid == 0) taken = tq.take(1);
+            if (s == 1 && has_next && tid == 0) ctl[2] = taken;
             if (s + 2 == nst) {
                 // The stages issued from here on belong to the next tile (or,
                 // past the last tile, re-read this tile's first stages). Its
@@ -598,7 +647,7 @@ void down_kernel(DownParams p) {
         for (int i = 0; i < RG; ++i) {
             const int r = wm * 64 + i * 32 + lr;
             u16* dst = (r < cur.nrows) ? p.part + (size_t)(cur.p0 + r) * p.d + (size_t)cur.ct * BN : p.part_sink;
-            dst += wn * (BN / 2) + 16 * lh;
+            dst += wn * (BN / WN) + 16 * lh;
 #pragma unroll
             for (int j = 0; j < NG; ++j) {
                 const f32x16 v = acc[i][j];
@@ -613,6 +662,8 @@ void down_kernel(DownParams p) {
             }
         }
         if (!has_next) break;
+        tile = next;
+        next = tq.lo + __builtin_amdgcn_readfirstlane(ctl[2]);
         cur = nxt;
         par ^= 1;
         after_epi = true;

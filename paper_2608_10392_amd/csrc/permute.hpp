@@ -94,21 +94,76 @@ __device__ int block_exclusive_scan(int n, Get get, Put put, int* lds) {
     return total;
 }
 
+// The same for long inputs: pieces of up to kScanStage values are loaded
+// into LDS with consecutive (coalesced, independent) reads, scanned there,
+// and written back the same way, so the global latency is paid a few times
+// per piece instead of once per value of a thread's chunk.
+constexpr int kScanStage = 16384;
+template <class Get, class Put>
+__device__ int staged_exclusive_scan(int n, Get get, Put put, int* stage, int* lds) {
+    const int tid = threadIdx.x, T = blockDim.x;
+    int carry = 0;
+    for (int base = 0; base < n; base += kScanStage) {
+        const int cnt = min(kScanStage, n - base);
+        for (int i = tid; i < cnt; i += T) stage[i] = get(base + i);
+        __syncthreads();
+        const int per = ceil_div(cnt, T);
+        const int beg = min(cnt, tid * per), end = min(cnt, beg + per);
+        int s = 0;
+        for (int i = beg; i < end; ++i) s += stage[i];
+        lds[tid] = s;
+        __syncthreads();
+        for (int off = 1; off < T; off <<= 1) {
+            const int v = (tid >= off) ? lds[tid - off] : 0;
+            __syncthreads();
+            lds[tid] += v;
+            __syncthreads();
+        }
+        int run = carry + lds[tid] - s;
+        const int total = lds[T - 1];
+        for (int i = beg; i < end; ++i) {
+            const int c = stage[i];
+            stage[i] = run;
+            run += c;
+        }
+        __syncthreads();
+        for (int i = tid; i < cnt; i += T) put(base + i, stage[i]);
+        carry += total;
+        __syncthreads();
+    }
+    return carry;
+}
+
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
     __shared__ int lds[kScanThreads];
+    __shared__ int stage[kScanStage];
+    __shared__ int segs[66];   // K + 2 <= 66
     const int K1 = p.K + 1, nbin = K1 << p.key_bits, nslab = K1 * p.B;
-    const int P = block_exclusive_scan(
-        nbin, [&](int i) { return p.bin_count[i]; }, [&](int i, int v) { p.bin_cursor[i] = v; }, lds);
-    for (int e = threadIdx.x; e <= K1; e += blockDim.x)
-        p.seg_off[e] = (e < K1) ? p.bin_cursor[e << p.key_bits] : P;
+    // The routing kernel leaves the row counts in kSlabCopies copies: sum
+    // them into the first.
+    int* slab_count = const_cast<int*>(p.slab_count);
+    for (int i = threadIdx.x; i < nslab; i += blockDim.x) {
+        int n = 0;
+        for (int c = 0; c < kSlabCopies; ++c) n += slab_count[(size_t)c * nslab + i];
+        slab_count[i] = n;
+    }
+    __syncthreads();
+    const int P = staged_exclusive_scan(
+        nbin, [&](int i) { return p.bin_count[i]; }, [&](int i, int v) { p.bin_cursor[i] = v; }, stage, lds);
+    // Segment offsets, also kept in LDS for the per-expert loops below.
+    for (int e = threadIdx.x; e <= K1; e += blockDim.x) {
+        const int o = (e < K1) ? p.bin_cursor[e << p.key_bits] : P;
+        p.seg_off[e] = o;
+        segs[e] = o;
+    }
     const int bm = p.bm_up;
-    const int nup = block_exclusive_scan(
+    const int nup = staged_exclusive_scan(
         nslab, [&](int i) { return ceil_div(p.slab_count[i], bm); },
         [&](int i, int v) {
             p.up_tile_off[i] = v;
             p.slab_off[i] = v * bm;
         },
-        lds);
+        stage, lds);
     if (threadIdx.x == 0) {
         p.slab_off[nslab] = nup * bm;
         p.up_tile_off[nslab] = nup;
@@ -116,7 +171,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
             int q = 0;
             for (int e = 0; e < K1; ++e) {
                 p.chunk_off[e] = q;
-                q += ceil_div(p.seg_off[e + 1] - p.seg_off[e], kChunk);
+                q += ceil_div(segs[e + 1] - segs[e], kChunk);
             }
             p.chunk_off[K1] = q;
             p.totals[3] = q;
@@ -124,7 +179,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
         int run = 0;
         for (int e = 0; e < K1; ++e) {
             p.down_tile_off[e] = run;
-            run += ceil_div(p.seg_off[e + 1] - p.seg_off[e], p.bm_down);
+            run += ceil_div(segs[e + 1] - segs[e], p.bm_down);
         }
         p.down_tile_off[K1] = run;
         p.totals[0] = P;
@@ -134,28 +189,69 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
     }
 }
 
+constexpr int kScatterBatch = 8;
 __global__ void scatter_kernel(PermuteParams p) {
     const int t = blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= p.N) return;
-    const int k = p.nres[t];
-    if (k == 0) return;  // padded token (valid tokens have k >= 1)
+    const int k = t < p.N ? p.nres[t] : 0;
+    const bool act = k > 0;   // padded tokens (and lanes past N) have k == 0
     const int B = p.B, kb = p.key_bits, K1 = p.K + 1;
     const uint64_t full = (B == 64) ? ~0ull : ((1ull << B) - 1ull);
-    const uint64_t m = p.mask[t], rm = ~m & full;
+    const uint64_t m = act ? p.mask[t] : 0ull, rm = ~m & full;
     const int ks = (int)(B > kb ? (m >> (B - kb)) : m);
     const int kr = (int)(B > kb ? (rm >> (B - kb)) : rm);
-    int pr = atomicAdd(&p.bin_cursor[ks], 1);
+    // Shared-expert pairs: block masks concentrate on few keys, so the lanes
+    // of a wave with the same key are grouped first; each group's first lane
+    // takes the group's slots with one atomic (all groups at once), and the
+    // lanes take consecutive slots in lane order.
+    const int lane = lane_id();
+    int leader = lane;
+    uint64_t grp = 0;
+    for (uint64_t pend = ballot(act); pend;) {
+        const int l0 = __builtin_ctzll(pend);
+        const int key = __shfl(ks, l0);
+        const uint64_t same = ballot(act && ks == key);
+        if (act && ks == key) {
+            leader = l0;
+            grp = same;
+        }
+        pend &= ~same;
+    }
+    int base = 0;
+    if (act && leader == lane) base = atomicAdd(&p.bin_cursor[ks], __popcll(grp));
+    // Residual pairs, kScatterBatch at a time: all slots of a batch are taken
+    // before any is used, so the atomics' latencies overlap.
+    int ex[kScatterBatch], slot[kScatterBatch];
+    const int* eid = p.eids + (size_t)t * p.K;
+#pragma unroll
+    for (int i = 0; i < kScatterBatch; ++i) {
+        ex[i] = (i < k) ? eid[i] : 0;
+        slot[i] = (i < k) ? atomicAdd(&p.bin_cursor[(ex[i] << kb) + kr], 1) : 0;
+    }
+    base = __shfl(base, leader);
+    if (!act) return;
+    const int pr = base + __popcll(grp & lanes_below());
     p.pair_token[pr] = t;
     p.pair_mask[pr] = m;
     p.pair_expert[pr] = 0;
     p.pair_of[(size_t)t * K1] = pr;
-    for (int i = 0; i < k; ++i) {
-        const int e = p.eids[(size_t)t * p.K + i];
-        pr = atomicAdd(&p.bin_cursor[(e << kb) + kr], 1);
-        p.pair_token[pr] = t;
-        p.pair_mask[pr] = rm;
-        p.pair_expert[pr] = e;
-        p.pair_of[(size_t)t * K1 + 1 + i] = pr;
+    for (int i0 = 0; i0 < k; i0 += kScatterBatch) {
+        if (i0 > 0) {
+#pragma unroll
+            for (int i = 0; i < kScatterBatch; ++i) {
+                ex[i] = (i0 + i < k) ? eid[i0 + i] : 0;
+                slot[i] = (i0 + i < k) ? atomicAdd(&p.bin_cursor[(ex[i] << kb) + kr], 1) : 0;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < kScatterBatch; ++i) {
+            if (i0 + i < k) {
+                const int q = slot[i];
+                p.pair_token[q] = t;
+                p.pair_mask[q] = rm;
+                p.pair_expert[q] = ex[i];
+                p.pair_of[(size_t)t * K1 + 1 + i0 + i] = q;
+            }
+        }
     }
 }
 
@@ -186,9 +282,9 @@ __global__ __launch_bounds__(256) void up_tile_kernel(PermuteParams p) {
 // Down row tiles: bm_down consecutive pairs of one expert segment. One wave
 // per row tile records its first pair, row count and expert, and the union
 // of the block masks of each 16-row group and of the whole tile. Down tiles
-// (row tile x column tile of d) are listed expert by expert, column tile
-// outer: the tiles that run together read one column slice of the expert's
-// V, which then stays in L2.
+// (row tile x column tile of d) are listed row tile by row tile: the column
+// tiles of one row tile run side by side on one XCD and read its H rows
+// from HBM once.
 __global__ __launch_bounds__(64) void down_rowtile_kernel(PermuteParams p) {
     const int rt = blockIdx.x;
     if (rt >= p.totals[4]) return;
@@ -210,9 +306,8 @@ __global__ __launch_bounds__(64) void down_rowtile_kernel(PermuteParams p) {
         out[G] = all;
         p.rt_info[rt] = make_int4(p0, nrows, e, 0);
     }
-    const int r0 = p.down_tile_off[e], nrt = p.down_tile_off[e + 1] - r0;
     for (int ct = lane; ct < p.down_col_tiles; ct += 64)
-        p.down_tiles[(size_t)r0 * p.down_col_tiles + (size_t)ct * nrt + (rt - r0)] = (rt << 8) | ct;
+        p.down_tiles[(size_t)rt * p.down_col_tiles + ct] = (rt << 8) | ct;
 }
 
 // Chunk q of expert e covers pairs [seg_off[e] + (q - chunk_off[e]) kChunk, ...)

@@ -3,35 +3,37 @@
 // cumulative-mass expert count, and the per-(expert, block) counts that the
 // permutation needs.
 //
-// One workgroup routes 128 tokens. Phase 1 computes the 1 + K + B logits of
-// each token (x W_shr, x W_1..x W_K, x mu_1..x mu_B) into LDS:
-//   * bf16 tokens: on the matrix cores. The fp32 router and prototype
-//     weights are pre-split into three bf16 parts (hi + mid + lo carries all
-//     24 significand bits), so every bf16 x bf16 product is exact and only
-//     the fp32 accumulation order differs from a sequential dot product.
+// One workgroup of two waves routes 128 tokens. Phase 1 computes the
+// 1 + K + B logits of each token (x W_shr, x W_1..x W_K, x mu_1..x mu_B)
+// into LDS:
+//   * bf16 tokens: x W_1.., x mu_1.. on the matrix cores. The fp32 router
+//     and prototype weights are pre-split into three bf16 parts (hi + mid +
+//     lo carries all 24 significand bits), so every bf16 x bf16 product is
+//     exact and only the fp32 accumulation order differs from a sequential
+//     dot product. x W_shr is an fp32 dot product on the vector units.
 //   * fp32 tokens: sequential fp32 FMA dot products.
-// Phase 2 takes one token per lane (waves 0 and 1) and runs the decisions in
-// the paper's order in fp32 with explicitly rounded operations; ties break
-// toward the lower index. The per-(expert, block) row counts are gathered
-// with wave ballots into LDS, then added to global memory once per group.
+// Phase 2 takes one token per lane and runs the decisions in the paper's
+// order in fp32 with explicitly rounded operations; ties break toward the
+// lower index. The per-(expert, block) row counts are gathered with wave
+// ballots into LDS, then added to global memory once per workgroup.
 #pragma once
 #include "common.hpp"
 
 namespace unifmoe {
 
 constexpr int kRouteTok = 128;
-constexpr int kRouteThreads = 256;
-constexpr int kRouteMaxColTiles = 9;  // 1 + K + B <= 144 logits
+constexpr int kRouteThreads = 128;    // 2 waves: 64 tokens each in the logits, one token per thread after
 
 struct RouteParams {
     int N, d, K, B, NL, NLP, lstride, key_bits;
+    int key_stride;     // words per token of the LDS ranking keys, 0 if none
     float tau, one_minus_2tau, t_mass, alpha_fixed;
     int max_shared, alpha_mode, mass_mode, fixed_k, select_mode;
     const void* X;
     const uint8_t* valid;
     const float* Wr;    // fp32 logits: [K+1][d]
     const float* mu;    // fp32 logits: [B][d]
-    const u16* Wsplit;  // bf16 logits: [3][NLP][d], rows W_shr, W_1..W_K, mu_1..mu_B, 0...
+    const u16* Wsplit;  // bf16 logits: [3][NLP][d], rows W_1..W_K, mu_1..mu_B, 0...
     float* alpha;
     int* nsh;
     uint64_t* mask;
@@ -39,7 +41,7 @@ struct RouteParams {
     int* eids;
     float* wts;
     int* bin_count;   // [(K+1) << key_bits] pairs per (expert, mask key), or null
-    int* slab_count;  // [(K+1) * B] rows per (expert, block), or null
+    int* slab_count;  // [kSlabCopies][(K+1) * B] rows per (expert, block), or null
 };
 
 // Exact three-way split of an fp32 value into bf16 parts.
@@ -50,8 +52,8 @@ __global__ void split_router_kernel(const float* __restrict__ Wr, const float* _
     if (i >= total) return;
     const int j = i / d, k = i - (i / d) * d;
     float w = 0.f;
-    if (j <= K) w = Wr[(size_t)j * d + k];
-    else if (j <= K + B) w = mu[(size_t)(j - 1 - K) * d + k];
+    if (j < K) w = Wr[(size_t)(j + 1) * d + k];
+    else if (j < K + B) w = mu[(size_t)(j - K) * d + k];
     const u16 hi = f2bf(w);
     const float r1 = w - bf2f(hi);
     const u16 mid = f2bf(r1);
@@ -61,45 +63,101 @@ __global__ void split_router_kernel(const float* __restrict__ Wr, const float* _
     out[2 * total + i] = f2bf(r2);
 }
 
+// Logits of the bf16 path. Each wave takes 64 tokens (four 16-row MFMA
+// fragments), so every weight fragment it loads serves four MFMAs.
+//  * The K + B expert and prototype logits run on the matrix cores in NCT
+//    16-column tiles, three exact bf16 parts per weight.
+//  * The shared-demand logit x W_shr is a plain fp32 dot product on the
+//    vector units, in the shadow of the MFMAs: each lane sums its 8 k of
+//    every k step, then the four lane groups of a row are added.
+// Every operand of a k step is loaded together, D - 1 k steps ahead of its
+// use, so the loads overlap each other and the MFMAs of earlier steps.
+template <int NCT>
 __device__ __forceinline__ void route_logits_bf16(const RouteParams& p, float* L, int tok0) {
+    constexpr int RT = 4;                    // 16-row fragments per wave
+    constexpr int D = (NCT <= 2) ? 3 : 2;    // register sets in the ring
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int nct = p.NLP / 16;
     const u16* X = static_cast<const u16*>(p.X);
-    f32x4 acc[2][kRouteMaxColTiles];
+    f32x4 acc[RT][NCT];
+    float sh[RT];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < RT; ++i) {
+        sh[i] = 0.f;
 #pragma unroll
-        for (int j = 0; j < kRouteMaxColTiles; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int r0 = tok0 + w * 32 + (lane & 15);
-    const int r1 = r0 + 16;
+        for (int j = 0; j < NCT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
     const int kof = (lane >> 4) * 8;
-    for (int k0 = 0; k0 < p.d; k0 += 32) {
-        u32x4 va = {0u, 0u, 0u, 0u}, vb = {0u, 0u, 0u, 0u};
-        if (r0 < p.N) va = ld16(X + (size_t)r0 * p.d + k0 + kof);
-        if (r1 < p.N) vb = ld16(X + (size_t)r1 * p.d + k0 + kof);
-        const bf16x8 a0 = as_bf16x8(va), a1 = as_bf16x8(vb);
+    const u16* xr[RT];
 #pragma unroll
-        for (int ct = 0; ct < kRouteMaxColTiles; ++ct) {
-            if (ct < nct) {
+    for (int i = 0; i < RT; ++i) {
+        // Rows past N read row N - 1; their logits are never used.
+        const int r = min(tok0 + w * 64 + i * 16 + (lane & 15), p.N - 1);
+        xr[i] = X + (size_t)r * p.d + kof;
+    }
+    const u16* wb = p.Wsplit + (size_t)(lane & 15) * p.d + kof;
+    const float* wsh = p.Wr + kof;           // row 0 of the fp32 router: W_shr
+    const size_t part_stride = (size_t)p.NLP * p.d, ct_stride = (size_t)16 * p.d;
+    const int nks = p.d / 32;
+    struct Set {
+        u32x4 a[RT], b[3][NCT], s0, s1;
+    };
+    Set ring[D];
+    auto load = [&](int ks, Set& S) {
+        const int k0 = ks * 32;
 #pragma unroll
-                for (int part = 0; part < 3; ++part) {
-                    const bf16x8 b = as_bf16x8(ld16(
-                        p.Wsplit + (size_t)(part * p.NLP + ct * 16 + (lane & 15)) * p.d + k0 + kof));
-                    acc[0][ct] = mfma16x16x32(a0, b, acc[0][ct]);
-                    acc[1][ct] = mfma16x16x32(a1, b, acc[1][ct]);
-                }
+        for (int i = 0; i < RT; ++i) S.a[i] = ld16(xr[i] + k0);
+#pragma unroll
+        for (int part = 0; part < 3; ++part)
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) S.b[part][ct] = ld16(wb + part * part_stride + ct * ct_stride + k0);
+        S.s0 = ld16(wsh + k0);
+        S.s1 = ld16(wsh + k0 + 4);
+    };
+    auto compute = [&](const Set& S) {
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int part = 0; part < 3; ++part) {
+                const bf16x8 b = as_bf16x8(S.b[part][ct]);
+#pragma unroll
+                for (int i = 0; i < RT; ++i) acc[i][ct] = mfma16x16x32(as_bf16x8(S.a[i]), b, acc[i][ct]);
+            }
+#pragma unroll
+        for (int i = 0; i < RT; ++i) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t u = S.a[i][q];
+                sh[i] = fmaf(__uint_as_float(u << 16), __uint_as_float(q < 2 ? S.s0[2 * q] : S.s1[2 * q - 4]), sh[i]);
+                sh[i] = fmaf(__uint_as_float(u & 0xffff0000u),
+                             __uint_as_float(q < 2 ? S.s0[2 * q + 1] : S.s1[2 * q - 3]), sh[i]);
+            }
+        }
+    };
+#pragma unroll
+    for (int i = 0; i < D - 1; ++i)
+        if (i < nks) load(i, ring[i]);
+    for (int ks = 0; ks < nks; ks += D) {
+#pragma unroll
+        for (int i = 0; i < D; ++i) {
+            if (ks + i < nks) {
+                if (ks + i + D - 1 < nks) load(ks + i + D - 1, ring[(i + D - 1) % D]);
+                compute(ring[i]);
             }
         }
     }
+    // Column 0: the shared-demand logit; columns 1..: the MFMA tiles.
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
+    for (int i = 0; i < RT; ++i) {
+        float v = sh[i];
+        v += __shfl_xor(v, 16);
+        v += __shfl_xor(v, 32);
+        if (lane < 16) L[(w * 64 + i * 16 + lane) * p.lstride] = v;
 #pragma unroll
-        for (int ct = 0; ct < kRouteMaxColTiles; ++ct)
-            if (ct < nct)
+        for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    L[(w * 32 + rt * 16 + (lane >> 4) * 4 + r) * p.lstride + ct * 16 + (lane & 15)] =
-                        acc[rt][ct][r];
+            for (int r = 0; r < 4; ++r)
+                L[(w * 64 + i * 16 + (lane >> 4) * 4 + r) * p.lstride + 1 + ct * 16 + (lane & 15)] = acc[i][ct][r];
+    }
 }
 
 __device__ __forceinline__ void route_logits_f32(const RouteParams& p, float* L, int tok0) {
@@ -115,6 +173,9 @@ __device__ __forceinline__ void route_logits_f32(const RouteParams& p, float* L,
     }
 }
 
+// Words per token of the ranking keys: max(K, B) rounded up to 4.
+__host__ __device__ __forceinline__ int key_row(int K, int B) { return ((K > B ? K : B) + 3) & ~3; }
+
 // Total-order key of a float for ranking: for non-NaN values it orders as
 // the float comparison does (-0 is first mapped to +0, so the two tie), and
 // a NaN gets a fixed place, so ranks computed with it always form a
@@ -124,8 +185,34 @@ __device__ __forceinline__ uint32_t rank_key(float f) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Rank of entry j among the n keys of a row (16-byte aligned, zero-padded to
+// a multiple of 4): the number of entries that come before it in decreasing
+// key order, ties to the lower index. Padding keys are 0 and sit at indices
+// >= n, so they never come first.
+__device__ __forceinline__ int rank_in_row(const uint32_t* keys, int n, int j) {
+    const uint32_t kj = keys[j];
+    int rank = 0;
+    for (int c = 0; c < n; c += 4) {
+        const u32x4 k4 = *reinterpret_cast<const u32x4*>(keys + c);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) rank += (k4[q] > kj) || (k4[q] == kj && c + q < j);
+    }
+    return rank;
+}
+
+// The same from the float values (no key row).
+__device__ __forceinline__ int rank_in_values(const float* v, int n, int j) {
+    const uint32_t kj = rank_key(v[j]);
+    int rank = 0;
+    for (int c = 0; c < n; ++c) {
+        const uint32_t kc = rank_key(v[c]);
+        rank += (kc > kj) || (kc == kj && c < j);
+    }
+    return rank;
+}
+
 // Decisions for token tok0 + threadIdx.x (threads 0..127, i.e. waves 0, 1).
-__device__ __forceinline__ void route_decide(const RouteParams& p, float* L, float* PS, int* QS,
+__device__ __forceinline__ void route_decide(const RouteParams& p, float* L, float* PS, int* QS, uint32_t* KEYS,
                                              int* slab_lds, int tok0) {
     const int tid = threadIdx.x;
     const int K = p.K, B = p.B, tok = tok0 + tid;
@@ -134,6 +221,10 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
     float* row = L + tid * p.lstride;
     float* ps = PS + tid * (K + 1);
     int* qs = QS + tid * (K + 1);
+    // Ranking keys: a 16-byte-aligned row per token when the workgroup's
+    // LDS has room for them (kp > 0), else ranked straight from the values.
+    const int kp = p.key_stride;
+    uint32_t* keys = KEYS + tid * kp;
     uint64_t mask = 0, sel = 0;
     int k = 0;
     if (v) {
@@ -153,14 +244,13 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
         // Eq. block-priority / shared-indices: the b largest x mu_c.
         if (p.select_mode == 0) {
             const float* u = row + 1 + K;
-            for (int c = 0; c < B; ++c) {
-                const uint32_t uc = rank_key(u[c]);
-                int rank = 0;
-                for (int c2 = 0; c2 < B; ++c2) {
-                    const uint32_t u2 = rank_key(u[c2]);
-                    rank += (u2 > uc) || (u2 == uc && c2 < c);
-                }
-                if (rank < b) mask |= 1ull << c;
+            if (kp > 0) {
+                for (int c = 0; c < kp; ++c) keys[c] = c < B ? rank_key(u[c]) : 0u;
+                for (int c = 0; c < B; ++c)
+                    if (rank_in_row(keys, B, c) < b) mask |= 1ull << c;
+            } else {
+                for (int c = 0; c < B; ++c)
+                    if (rank_in_values(u, B, c) < b) mask |= 1ull << c;
             }
         } else {
             mask = (b >= 64) ? ~0ull : ((1ull << b) - 1ull);
@@ -177,18 +267,11 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
         }
         for (int j = 0; j < K; ++j) l[j] = __fdiv_rn(l[j], S);
         // Eq. sorted-affinity: rank by decreasing affinity, ties to lower index.
+        for (int j = 0; j < kp; ++j) keys[j] = j < K ? rank_key(l[j]) : 0u;
         for (int j = 0; j < K; ++j) {
-            const float sj = l[j];
-            const uint32_t kj = rank_key(sj);
-            int rank = 0;
-            for (int j2 = 0; j2 < K; ++j2) {
-                const uint32_t k2 = rank_key(l[j2]);
-                rank += (k2 > kj) || (k2 == kj && j2 < j);
-            }
-            ps[rank] = sj;
+            const int rank = kp > 0 ? rank_in_row(keys, K, j) : rank_in_values(l, K, j);
+            ps[rank] = l[j];
             qs[rank] = j + 1;
-            p.eids[(size_t)tok * K + rank] = j + 1;
-            p.wts[(size_t)tok * K + rank] = sj;
         }
         // Eq. beta / expert-count: smallest prefix reaching the target.
         if (p.mass_mode == 2) {
@@ -217,8 +300,8 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
         p.mask[tok] = 0;
         p.nres[tok] = 0;
         for (int j = 0; j < K; ++j) {
-            p.eids[(size_t)tok * K + j] = -1;
-            p.wts[(size_t)tok * K + j] = 0.f;
+            ps[j] = 0.f;
+            qs[j] = -1;
         }
     }
     if (p.bin_count == nullptr) return;
@@ -227,15 +310,23 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
     // k residual pairs per valid token.
     const uint64_t full = (B == 64) ? ~0ull : ((1ull << B) - 1ull);
     const int kb = p.key_bits;
-    if (v) {
-        const uint64_t rmask = ~mask & full;
-        const int ks = (int)(B > kb ? (mask >> (B - kb)) : mask);
-        const int kr = (int)(B > kb ? (rmask >> (B - kb)) : rmask);
-        atomicAdd(&p.bin_count[ks], 1);
-        for (int i = 0; i < k; ++i) atomicAdd(&p.bin_count[(qs[i] << kb) + kr], 1);
-    }
-    // Rows per (expert, block): shared expert on I_shr, residual experts on I_res.
     const int lane = lane_id();
+    const uint64_t rmask = ~mask & full;
+    const int ks = (int)(B > kb ? (mask >> (B - kb)) : mask);
+    const int kr = (int)(B > kb ? (rmask >> (B - kb)) : rmask);
+    // Shared-expert pairs: every valid token has one, and block masks
+    // concentrate on few keys, so the lanes of a wave with the same key are
+    // merged first (one global atomic per distinct key, not per token).
+    for (uint64_t pend = ballot(v); pend;) {
+        const int leader = __builtin_ctzll(pend);
+        const int key = __shfl(ks, leader);
+        const uint64_t same = ballot(v && ks == key);
+        if (lane == leader) atomicAdd(&p.bin_count[key], __popcll(same));
+        pend &= ~same;
+    }
+    if (v)
+        for (int i = 0; i < k; ++i) atomicAdd(&p.bin_count[(qs[i] << kb) + kr], 1);
+    // Rows per (expert, block): shared expert on I_shr, residual experts on I_res.
     for (int c = 0; c < B; ++c) {
         const uint64_t bits = ballot(v && ((mask >> c) & 1ull));
         if (lane == 0 && bits) atomicAdd(&slab_lds[c], __popcll(bits));
@@ -250,25 +341,43 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
     }
 }
 
-template <bool kBF16>
+// NCT: 16-column logit tiles of the bf16 path (1 + K + B <= 16 NCT); 0 for
+// fp32 tokens.
+template <int NCT>
 __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteParams p) {
     extern __shared__ float lds_route[];
     float* L = lds_route;
     float* PS = L + kRouteTok * p.lstride;
     int* QS = reinterpret_cast<int*>(PS + kRouteTok * (p.K + 1));
-    int* slab_lds = QS + kRouteTok * (p.K + 1);
+    uint32_t* KEYS = reinterpret_cast<uint32_t*>(QS + kRouteTok * (p.K + 1));   // 16-byte aligned
+    int* slab_lds = reinterpret_cast<int*>(KEYS + kRouteTok * p.key_stride);
     const int tok0 = blockIdx.x * kRouteTok;
     const int nslab = (p.K + 1) * p.B;
     if (p.slab_count)
         for (int i = threadIdx.x; i < nslab; i += blockDim.x) slab_lds[i] = 0;
-    if (kBF16) route_logits_bf16(p, L, tok0);
+    if constexpr (NCT > 0) route_logits_bf16<NCT>(p, L, tok0);
     else route_logits_f32(p, L, tok0);
     __syncthreads();
-    if (threadIdx.x < kRouteTok) route_decide(p, L, PS, QS, slab_lds, tok0);
+    if (threadIdx.x < kRouteTok) route_decide(p, L, PS, QS, KEYS, slab_lds, tok0);
     __syncthreads();
-    if (p.slab_count)
+    // Sorted expert ids and weights of the workgroup's tokens: one contiguous
+    // range of each output, written from LDS with consecutive addresses.
+    {
+        const int K = p.K, ntok = min(kRouteTok, p.N - tok0);
+        const size_t base = (size_t)tok0 * K;
+        for (int i = threadIdx.x; i < ntok * K; i += blockDim.x) {
+            const int t = i / K, r = i - t * K;
+            p.eids[base + i] = QS[t * (K + 1) + r];
+            p.wts[base + i] = PS[t * (K + 1) + r];
+        }
+    }
+    // Workgroup totals go to one of kSlabCopies copies of the counts, which
+    // spreads the same-address atomics; the permutation sums the copies.
+    if (p.slab_count) {
+        int* dst = p.slab_count + (size_t)(blockIdx.x % kSlabCopies) * nslab;
         for (int i = threadIdx.x; i < nslab; i += blockDim.x)
-            if (slab_lds[i]) atomicAdd(&p.slab_count[i], slab_lds[i]);
+            if (slab_lds[i]) atomicAdd(&dst[i], slab_lds[i]);
+    }
 }
 
 }  // namespace unifmoe

@@ -43,10 +43,20 @@ constexpr int kUpTM = kFfnTM;
 // row chunk, then block: the tiles that run together share token rows
 // (across the group's blocks) and weight slabs (within a group).
 constexpr int kUpBlockGroup = 4;
-constexpr int kDownTM = kFfnTM;
-constexpr int kDownBNWide = 256, kDownBNNarrow = 128;
+// Down tiles: 256 pairs x 256 columns when d is a multiple of 256, else
+// 128 x 384 when d is a multiple of 384 (d = 384: one column tile), else
+// 256 x 128.
+constexpr int kDownTMMin = 128, kDownTMMax = 256;
+constexpr int kDownBNNarrow = 128;
+struct DownShape { int tm, bn; };
+DownShape down_shape(int d) {
+    if (d % 256 == 0) return {256, 256};
+    if (d % 384 == 0) return {128, 384};
+    return {256, 128};
+}
 static_assert(up_lds_bytes(256) <= 160 * 1024, "up stages exceed LDS");
-static_assert(down_lds_bytes(kDownBNWide) <= 160 * 1024, "down stages exceed LDS");
+static_assert(down_lds_bytes(128, 384) <= 160 * 1024 && down_lds_bytes(256, 256) <= 160 * 1024,
+              "down stages exceed LDS");
 
 struct Dims {
     int N, d, K, B, M, H, K1, NL, NLP, lstride, key_bits, nslab, nbin;
@@ -65,8 +75,8 @@ Dims dims_of(const unif_moe_config* c) {
     m.H = m.B * m.M;
     m.K1 = m.K + 1;
     m.NL = 1 + m.K + m.B;
-    m.NLP = ceil_div(m.NL, 16) * 16;
-    m.lstride = m.NLP + 1;
+    m.NLP = ceil_div(m.K + m.B, 16) * 16;   // matrix-core logit rows (bf16 path)
+    m.lstride = m.NLP + 1;                  // LDS row: x W_shr, then those
     m.key_bits = m.B < kKeyBitsMax ? m.B : kKeyBitsMax;
     m.nslab = m.K1 * m.B;
     m.nbin = m.K1 << m.key_bits;
@@ -77,10 +87,16 @@ Dims dims_of(const unif_moe_config* c) {
     return m;
 }
 
-size_t route_lds_bytes(const Dims& m) {
-    return sizeof(float) * ((size_t)kRouteTok * m.lstride + (size_t)kRouteTok * (m.K + 1) * 2 +
-                            (size_t)m.K1 * m.B);
+// Routing LDS: logits, sorted weights and ids, ranking keys (16-byte
+// aligned; left out when they would not fit), row counts.
+size_t route_lds_bytes_with(const Dims& m, int key_stride) {
+    const size_t head = (size_t)kRouteTok * m.lstride + (size_t)kRouteTok * (m.K + 1) * 2;
+    return sizeof(float) * (((head + 3) & ~(size_t)3) + (size_t)kRouteTok * key_stride + (size_t)m.K1 * m.B);
 }
+int route_key_stride(const Dims& m) {
+    return route_lds_bytes_with(m, key_row(m.K, m.B)) <= kLdsLimit ? key_row(m.K, m.B) : 0;
+}
+size_t route_lds_bytes(const Dims& m) { return route_lds_bytes_with(m, route_key_stride(m)); }
 
 // Checks shared by every entry point (host only, no HIP call).
 int32_t check_config(const unif_moe_config* c) {
@@ -113,7 +129,7 @@ int32_t check_forward_shape(const unif_moe_config* c) {
     if (m.bf16) {
         if (m.d % 128 != 0 || m.M % 64 != 0 || m.M > 256) return UNIF_EUNSUPPORTED;
         // Down tiles are encoded as row tile << 8 | column tile.
-        if (m.d / kDownBNNarrow > 255 || (int64_t)m.N * m.K1 / kDownTM + m.K1 >= ((int64_t)1 << 23))
+        if (m.d / kDownBNNarrow > 255 || (int64_t)m.N * m.K1 / kDownTMMin + m.K1 >= ((int64_t)1 << 23))
             return UNIF_EUNSUPPORTED;
         if ((int64_t)m.H * m.d * 2 > ((int64_t)1 << 40)) return UNIF_EUNSUPPORTED;
     } else {
@@ -149,7 +165,7 @@ struct FwdPlan {
     size_t alpha, nsh, mask, nres, eids, wts;
     size_t wsplit;
     size_t zero_begin, zero_end;  // bin_count, slab_count, totals, zero page
-    size_t bin_count, slab_count, totals, zero_page;
+    size_t bin_count, slab_count, totals, queues, zero_page;
     size_t bin_cursor, slab_off, seg_off, up_tile_off, down_tile_off, chunk_off, chunk_cnt;
     size_t pair_token, pair_mask, pair_expert, pair_of, slab_rows, slab_tok, up_tile_info, up_tile_rows, hbuf, part;
     size_t max_chunks, max_row_tiles, rt_info, rt_masks, down_tiles;
@@ -172,8 +188,9 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.wsplit = cv.take(m.bf16 ? (size_t)3 * m.NLP * m.d * sizeof(u16) : 0);
     p.bin_count = cv.take(4 * (size_t)m.nbin);
     p.zero_begin = p.bin_count;
-    p.slab_count = cv.take(4 * (size_t)m.nslab);
+    p.slab_count = cv.take(4 * (size_t)m.nslab * kSlabCopies);
     p.totals = cv.take(4 * 8);
+    p.queues = cv.take(4 * 16);   // per-XCD tile counters: up, then down
     p.zero_page = cv.take(256);
     p.zero_end = cv.cur;
     p.bin_cursor = cv.take(4 * (size_t)m.nbin);
@@ -182,7 +199,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.up_tile_off = cv.take(4 * ((size_t)m.nslab + 1));
     p.down_tile_off = cv.take(4 * (K1 + 1));
     p.pair_token = cv.take(4 * pmax);
-    p.pair_mask = cv.take(8 * (pmax + kDownTM));   // a whole down tile is readable past the last pair
+    p.pair_mask = cv.take(8 * (pmax + kDownTMMax));   // a whole down tile is readable past the last pair
     p.pair_expert = cv.take(4 * pmax);
     p.pair_of = cv.take(4 * N * K1);
     // Slab row lists: at most K B rows per token (b + k (B - b) <= K B), each
@@ -199,9 +216,9 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.chunk_cnt = cv.take(m.bf16 ? 4 * p.max_chunks * (size_t)m.B : 0);
     p.hbuf = cv.take(m.bf16 ? (pmax + 1) * (size_t)m.H * 2 : 0);  // + the sink row
     p.part = cv.take((pmax + 1) * (size_t)m.d * (m.bf16 ? 2 : sizeof(float)));   // + the sink row
-    p.max_row_tiles = ceil_div_sz(pmax, kDownTM) + K1;
+    p.max_row_tiles = ceil_div_sz(pmax, kDownTMMin) + K1;
     p.rt_info = cv.take(m.bf16 ? 16 * p.max_row_tiles : 0);
-    p.rt_masks = cv.take(m.bf16 ? 8 * (kDownTM / 16 + 1) * p.max_row_tiles : 0);
+    p.rt_masks = cv.take(m.bf16 ? 8 * (kDownTMMax / 16 + 1) * p.max_row_tiles : 0);
     p.down_tiles = cv.take(m.bf16 ? 4 * p.max_row_tiles * (size_t)(m.d / kDownBNNarrow) : 0);
     p.total = cv.cur + 256;  // slack for aligning an unaligned base pointer
     return p;
@@ -257,6 +274,7 @@ RouteParams route_params(const unif_moe_config* c, const Dims& m, const void* X,
     r.NL = m.NL;
     r.NLP = m.NLP;
     r.lstride = m.lstride;
+    r.key_stride = route_key_stride(m);
     r.key_bits = m.key_bits;
     r.tau = m.tau;
     r.one_minus_2tau = m.one_minus_2tau;
@@ -294,13 +312,22 @@ int32_t launch_route(const Dims& m, const RouteParams& rp, const float* Wr, cons
     }
     const size_t lds = route_lds_bytes(m);
     const int grid = ceil_div(m.N, kRouteTok);
+    void (*kern)(RouteParams) = route_kernel<0>;
     if (m.bf16) {
-        if (allow_lds(route_kernel<true>, lds) != UNIF_OK) return UNIF_EDEVICE;
-        route_kernel<true><<<grid, kRouteThreads, lds, st>>>(rp);
-    } else {
-        if (allow_lds(route_kernel<false>, lds) != UNIF_OK) return UNIF_EDEVICE;
-        route_kernel<false><<<grid, kRouteThreads, lds, st>>>(rp);
+        switch (m.NLP / 16) {
+            case 1: kern = route_kernel<1>; break;
+            case 2: kern = route_kernel<2>; break;
+            case 3: kern = route_kernel<3>; break;
+            case 4: kern = route_kernel<4>; break;
+            case 5: kern = route_kernel<5>; break;
+            case 6: kern = route_kernel<6>; break;
+            case 7: kern = route_kernel<7>; break;
+            case 8: kern = route_kernel<8>; break;
+            default: return UNIF_EUNSUPPORTED;
+        }
     }
+    if (allow_lds(kern, lds) != UNIF_OK) return UNIF_EDEVICE;
+    kern<<<grid, kRouteThreads, lds, st>>>(rp);
     UNIF_LAUNCH_CHECK();
     return UNIF_OK;
 }
@@ -433,11 +460,11 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.K = m.K;
     pp.B = m.B;
     pp.key_bits = m.key_bits;
-    const int down_bn = (m.d % kDownBNWide == 0) ? kDownBNWide : kDownBNNarrow;
+    const DownShape dsh = down_shape(m.d);
     pp.bm_up = kUpTM;
     pp.up_group = kUpBlockGroup;
-    pp.bm_down = kDownTM;
-    pp.down_col_tiles = m.bf16 ? m.d / down_bn : 1;
+    pp.bm_down = dsh.tm;
+    pp.down_col_tiles = m.bf16 ? m.d / dsh.bn : 1;
     pp.mask = mask;
     pp.nres = nres;
     pp.eids = eids;
@@ -496,6 +523,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         up.tile_info = pp.up_tile_info;
         up.tile_rows = pp.up_tile_rows;
         up.totals = totals;
+        up.queue = reinterpret_cast<int*>(ws + plan.queues);
         const size_t up_lds = (size_t)up_lds_bytes(m.M);
         const int grid = (cus / kXcds) * kXcds;
         switch (m.M / 64) {
@@ -523,10 +551,13 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         dn.pair_mask = pp.pair_mask;
         dn.tiles = pp.down_tiles;
         dn.totals = totals;
-        if (down_bn == kDownBNWide)
-            s = launch_persistent(down_kernel<kDownBNWide / 64>, grid, (size_t)down_lds_bytes(kDownBNWide), st, dn);
+        dn.queue = reinterpret_cast<int*>(ws + plan.queues) + 8;
+        if (dsh.bn == 384)
+            s = launch_persistent(down_kernel<2, 3>, grid, (size_t)down_lds_bytes(128, 384), st, dn);
+        else if (dsh.bn == 256)
+            s = launch_persistent(down_kernel<4, 4>, grid, (size_t)down_lds_bytes(256, 256), st, dn);
         else
-            s = launch_persistent(down_kernel<kDownBNNarrow / 64>, grid, (size_t)down_lds_bytes(kDownBNNarrow), st, dn);
+            s = launch_persistent(down_kernel<4, 2>, grid, (size_t)down_lds_bytes(256, 128), st, dn);
         if (s != UNIF_OK) return s;
         UNIF_MARK(4);
     } else {
