@@ -56,6 +56,41 @@ def phase_bytes(cfg, st):
     return dict(routing=routing, permute=permute, combine=combine)
 
 
+COUNTERS_PROFILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                                "gemm_vit_b16_hbm_counters.md")
+
+
+def library_source_hash():
+    """SHA-256 over the library's kernel sources and build flags."""
+    import hashlib
+    base = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_10392_amd")
+    files = sorted(os.path.join("paper_2608_10392_amd", "csrc", f) for f in os.listdir(os.path.join(base, "csrc")))
+    files.append(os.path.join("paper_2608_10392_amd", "build.py"))
+    h = hashlib.sha256()
+    root = os.path.dirname(base)
+    for f in files:
+        h.update(f.encode())
+        with open(os.path.join(root, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def committed_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (FETCH_SIZE and WRITE_SIZE scaled by a same-run copy of known size), or
+    None when the summary is missing or the sources changed since."""
+    try:
+        with open(COUNTERS_PROFILE) as f:
+            line = next(l for l in f if l.startswith("counters-json:"))
+        c = json.loads(line.split(":", 1)[1])
+        if c.get("source_sha256") != library_source_hash():
+            return None
+        k = c["kernels"][kernel]
+        return int(k["read_bytes_per_launch"] + k["write_bytes_per_launch"])
+    except (OSError, StopIteration, ValueError, KeyError):
+        return None
+
+
 def cpu_baseline(g, n_sample, repeats):
     """The CPU oracle timed on a seeded sample of the same workload."""
     import numpy as np
@@ -177,7 +212,7 @@ def main():
                    "block_width": cfg["block_width"], "mass_threshold": cfg["mass_threshold"]},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved / 1e12, 2),
                      "peak": PEAK_BF16_FLOPS / 1e12, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_FLOPS, 4), "traffic": None},
+                     "frac": round(achieved / PEAK_BF16_FLOPS, 4), "traffic": committed_traffic(dom)},
         "mfma_util_activated": round(act / (gemm_ms / 1e3) / PEAK_BF16_FLOPS, 4),
         "hbm_frac": {n: round(v, 4) for n, v in hbm.items()},
         "hbm_frac_routing_permute_combine": round(hbm_all / PEAK_HBM_BYTES, 4),
