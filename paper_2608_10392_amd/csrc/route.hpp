@@ -22,7 +22,9 @@
 namespace unifmoe {
 
 constexpr int kRouteTok = 128;
-constexpr int kRouteThreads = 128;    // 2 waves: 64 tokens each in the logits, one token per thread after
+// 4 waves: in the logits, wave w takes tokens 64 (w & 1).. and half (w >> 1)
+// of the k range; then waves 0 and 1 take one token per thread.
+constexpr int kRouteThreads = 256;
 
 struct RouteParams {
     int N, d, K, B, NL, NLP, lstride, key_bits;
@@ -76,7 +78,8 @@ template <int NCT>
 __device__ __forceinline__ void route_logits_bf16(const RouteParams& p, float* L, int tok0) {
     constexpr int RT = 4;                    // 16-row fragments per wave
     constexpr int D = (NCT <= 2) ? 3 : 2;    // register sets in the ring
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int w = wave & 1, kh = wave >> 1;  // token half, k half
     const u16* X = static_cast<const u16*>(p.X);
     f32x4 acc[RT][NCT];
     float sh[RT];
@@ -97,13 +100,15 @@ __device__ __forceinline__ void route_logits_bf16(const RouteParams& p, float* L
     const u16* wb = p.Wsplit + (size_t)(lane & 15) * p.d + kof;
     const float* wsh = p.Wr + kof;           // row 0 of the fp32 router: W_shr
     const size_t part_stride = (size_t)p.NLP * p.d, ct_stride = (size_t)16 * p.d;
-    const int nks = p.d / 32;
+    const int nks_all = p.d / 32;
+    const int ks0 = kh ? nks_all / 2 : 0;
+    const int nks = kh ? nks_all - nks_all / 2 : nks_all / 2;
     struct Set {
         u32x4 a[RT], b[3][NCT], s0, s1;
     };
     Set ring[D];
     auto load = [&](int ks, Set& S) {
-        const int k0 = ks * 32;
+        const int k0 = (ks0 + ks) * 32;
 #pragma unroll
         for (int i = 0; i < RT; ++i) S.a[i] = ld16(xr[i] + k0);
 #pragma unroll
@@ -145,18 +150,35 @@ __device__ __forceinline__ void route_logits_bf16(const RouteParams& p, float* L
             }
         }
     }
-    // Column 0: the shared-demand logit; columns 1..: the MFMA tiles.
+    // Column 0: the shared-demand logit; columns 1..: the MFMA tiles. The
+    // second k half is written first; the first adds it to its own sums
+    // (same order for every token).
 #pragma unroll
     for (int i = 0; i < RT; ++i) {
         float v = sh[i];
         v += __shfl_xor(v, 16);
         v += __shfl_xor(v, 32);
-        if (lane < 16) L[(w * 64 + i * 16 + lane) * p.lstride] = v;
+        sh[i] = v;
+    }
+    for (int half = 1; half >= 0; --half) {
+        if (kh == half) {
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct)
+            for (int i = 0; i < RT; ++i) {
+                float* row0 = L + (size_t)(w * 64 + i * 16) * p.lstride;
+                if (lane < 16) {
+                    float* d0 = row0 + lane * p.lstride;
+                    *d0 = half ? sh[i] : sh[i] + *d0;
+                }
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-                L[(w * 64 + i * 16 + (lane >> 4) * 4 + r) * p.lstride + 1 + ct * 16 + (lane & 15)] = acc[i][ct][r];
+                for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        float* d = row0 + ((lane >> 4) * 4 + r) * p.lstride + 1 + ct * 16 + (lane & 15);
+                        *d = half ? acc[i][ct][r] : acc[i][ct][r] + *d;
+                    }
+            }
+        }
+        __syncthreads();
     }
 }
 
@@ -211,6 +233,9 @@ __device__ __forceinline__ int rank_in_values(const float* v, int n, int j) {
     return rank;
 }
 
+// Rankings of at most this many entries run on registers.
+constexpr int kSmallRank = 16;
+
 // Decisions for token tok0 + threadIdx.x (threads 0..127, i.e. waves 0, 1).
 __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, float* PS, int* QS, uint32_t* KEYS,
                                              int* slab_lds, int tok0) {
@@ -244,7 +269,19 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
         // Eq. block-priority / shared-indices: the b largest x mu_c.
         if (p.select_mode == 0) {
             const float* u = row + 1 + K;
-            if (kp > 0) {
+            if (B <= kSmallRank) {
+                // All keys in registers; padding keys 0 never come first.
+                uint32_t uk[kSmallRank];
+#pragma unroll
+                for (int c = 0; c < kSmallRank; ++c) uk[c] = c < B ? rank_key(u[c]) : 0u;
+#pragma unroll
+                for (int c = 0; c < kSmallRank; ++c) {
+                    int rank = 0;
+#pragma unroll
+                    for (int c2 = 0; c2 < kSmallRank; ++c2) rank += (uk[c2] > uk[c]) || (uk[c2] == uk[c] && c2 < c);
+                    if (c < B && rank < b) mask |= 1ull << c;
+                }
+            } else if (kp > 0) {
                 for (int c = 0; c < kp; ++c) keys[c] = c < B ? rank_key(u[c]) : 0u;
                 for (int c = 0; c < B; ++c)
                     if (rank_in_row(keys, B, c) < b) mask |= 1ull << c;
@@ -257,6 +294,65 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
         }
         // Eq. residual-router-score: max-subtracted softmax, index-order sum.
         float* l = row + 1;
+        if (K <= kSmallRank) {
+            // The same steps on registers: softmax, ranks, then the sorted
+            // weights back from LDS for the prefix of Eq. expert-count.
+            float lv[kSmallRank];
+#pragma unroll
+            for (int j = 0; j < kSmallRank; ++j) lv[j] = j < K ? l[j] : 0.f;
+            float m = lv[0];
+#pragma unroll
+            for (int j = 1; j < kSmallRank; ++j) m = j < K ? fmaxf(m, lv[j]) : m;
+            float S = 0.f;
+#pragma unroll
+            for (int j = 0; j < kSmallRank; ++j) {
+                lv[j] = j < K ? expf(__fsub_rn(lv[j], m)) : 0.f;
+                S = j < K ? __fadd_rn(S, lv[j]) : S;
+            }
+            uint32_t ek[kSmallRank];
+#pragma unroll
+            for (int j = 0; j < kSmallRank; ++j) {
+                lv[j] = __fdiv_rn(lv[j], S);
+                ek[j] = j < K ? rank_key(lv[j]) : 0u;
+            }
+            int rk[kSmallRank];
+#pragma unroll
+            for (int j = 0; j < kSmallRank; ++j) {
+                int rank = 0;
+#pragma unroll
+                for (int j2 = 0; j2 < kSmallRank; ++j2) rank += (ek[j2] > ek[j]) || (ek[j2] == ek[j] && j2 < j);
+                rk[j] = rank;
+                if (j < K) {
+                    ps[rank] = lv[j];
+                    qs[rank] = j + 1;
+                }
+            }
+            if (p.mass_mode == 2) {
+                k = p.fixed_k;
+            } else {
+                const float beta = __fsub_rn(1.0f, alpha);
+                const float target = (p.mass_mode == 0) ? fminf(beta, p.t_mass) : p.t_mass;
+                float sv[kSmallRank];
+#pragma unroll
+                for (int n = 0; n < kSmallRank; ++n) sv[n] = n < K ? ps[n] : 0.f;
+                float P = 0.f;
+                k = K;
+                bool found = false;
+#pragma unroll
+                for (int n = 0; n < kSmallRank; ++n) {
+                    if (n < K && !found) {
+                        P = __fadd_rn(P, sv[n]);
+                        if (P >= target) {
+                            k = n + 1;
+                            found = true;
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kSmallRank; ++j)
+                if (j < K && rk[j] < k) sel |= 1ull << j;
+        } else {
         float m = l[0];
         for (int j = 1; j < K; ++j) m = fmaxf(m, l[j]);
         float S = 0.f;
@@ -290,6 +386,7 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
             }
         }
         for (int i = 0; i < k; ++i) sel |= 1ull << (qs[i] - 1);
+        }
         p.alpha[tok] = alpha;
         p.nsh[tok] = b;
         p.mask[tok] = mask;
