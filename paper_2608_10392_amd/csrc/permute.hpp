@@ -13,7 +13,9 @@
 //                      bin cursors, expert segment offsets, slab offsets,
 //                      chunk offsets, tile tables
 //   scatter_kernel     one thread per token claims its pair slots
-//   chunk_count_kernel per chunk of kChunk pairs of one expert: pairs per block
+//   tables_kernel      up tile table (per slab), down row tiles (per row
+//                      tile), and per chunk of kChunk pairs of one expert:
+//                      pairs per block
 //   chunk_scan_kernel  per slab: exclusive scan of its chunk counts
 //   slabfill_kernel    per chunk: each pair writes itself into the slabs of
 //                      its blocks, in pair order (deterministic)
@@ -21,9 +23,8 @@
 // Each slab's row list starts at a multiple of the up-projection tile height
 // bm_up and holds the slab's pairs in pair order, with their tokens beside
 // them, so a tile's gather needs no dependent lookups. Up tiles are listed
-// expert by expert, and inside an expert by row chunk j then block c: tiles
-// that run at the same time gather largely the same token rows, which then
-// come from L2.
+// expert by expert, and inside an expert by groups of blocks, row chunk j,
+// then block c (see up_tiles_of_slab).
 #pragma once
 #include "common.hpp"
 
@@ -261,9 +262,7 @@ __global__ void scatter_kernel(PermuteParams p) {
 // (up_tile_off of its first slab) + sum over the group's blocks c' of
 // min(j, tiles(e, c')) + the number of the group's blocks c' < c that have a
 // tile j. One workgroup per slab, one thread per tile of the slab.
-__global__ __launch_bounds__(256) void up_tile_kernel(PermuteParams p) {
-    __shared__ int tiles[64];
-    const int sl = blockIdx.x;
+__device__ __forceinline__ void up_tiles_of_slab(const PermuteParams& p, int sl, int* tiles) {
     const int e = sl / p.B, c = sl - e * p.B;
     const int bm = p.bm_up;
     const int g0 = (c / p.up_group) * p.up_group, g1 = min(p.B, g0 + p.up_group);
@@ -285,13 +284,11 @@ __global__ __launch_bounds__(256) void up_tile_kernel(PermuteParams p) {
 // (row tile x column tile of d) are listed row tile by row tile: the column
 // tiles of one row tile run side by side on one XCD and read its H rows
 // from HBM once.
-__global__ __launch_bounds__(64) void down_rowtile_kernel(PermuteParams p) {
-    const int rt = blockIdx.x;
-    if (rt >= p.totals[4]) return;
+__device__ __forceinline__ void down_rowtile(const PermuteParams& p, int rt) {
     const int e = upper_index(p.down_tile_off, p.K + 1, rt);
     const int p0 = p.seg_off[e] + (rt - p.down_tile_off[e]) * p.bm_down;
     const int nrows = min(p.bm_down, p.seg_off[e + 1] - p0);
-    const int lane = threadIdx.x, G = p.bm_down / 16;
+    const int lane = threadIdx.x & 63, G = p.bm_down / 16;
     uint64_t* out = p.rt_masks + (size_t)rt * (G + 1);
     uint64_t all = 0;
     for (int h = 0; h * 64 < p.bm_down; ++h) {
@@ -309,6 +306,8 @@ __global__ __launch_bounds__(64) void down_rowtile_kernel(PermuteParams p) {
     for (int ct = lane; ct < p.down_col_tiles; ct += 64)
         p.down_tiles[(size_t)rt * p.down_col_tiles + ct] = (rt << 8) | ct;
 }
+
+
 
 // Chunk q of expert e covers pairs [seg_off[e] + (q - chunk_off[e]) kChunk, ...)
 // of the expert's segment. One workgroup of kChunk threads per chunk, one
@@ -333,18 +332,36 @@ __device__ __forceinline__ void chunk_wave_counts(int B, uint64_t m, int (*wc)[6
     }
 }
 
-__global__ __launch_bounds__(kChunk) void chunk_count_kernel(PermuteParams p) {
-    const int q = blockIdx.x;
-    if (q >= p.totals[3]) return;
+// The three tables that only need the scatter's output, in one launch
+// (each is small; a kernel launch costs more than their work): workgroups
+// [0, nslab) build the up tiles of one slab each, the next g1 workgroups the
+// down row tiles (one wave per row tile), the rest count the chunks' rows
+// per block.
+__global__ __launch_bounds__(256) void tables_kernel(PermuteParams p, int g1) {
+    static_assert(kChunk == 256, "one thread per chunk pair");
+    __shared__ int tiles[64];
     __shared__ int wc[kChunk / 64][64];
-    const ChunkView v = chunk_view(p, q);
-    const int pr = v.lo + (int)threadIdx.x;
-    chunk_wave_counts(p.B, pr < v.hi ? p.pair_mask[pr] : 0ull, wc);
-    __syncthreads();
-    if ((int)threadIdx.x < p.B) {
-        int n = 0;
-        for (int w = 0; w < kChunk / 64; ++w) n += wc[w][threadIdx.x];
-        p.chunk_cnt[(size_t)q * p.B + threadIdx.x] = n;
+    const int nslab = (p.K + 1) * p.B;
+    const int b = blockIdx.x;
+    if (b < nslab) {
+        up_tiles_of_slab(p, b, tiles);
+    } else if (b < nslab + g1) {
+        const int nrt = p.totals[4];
+        for (int rt = (b - nslab) * 4 + (threadIdx.x >> 6); rt < nrt; rt += g1 * 4) down_rowtile(p, rt);
+    } else {
+        const int g2 = gridDim.x - nslab - g1, nq = p.totals[3];
+        for (int q = b - nslab - g1; q < nq; q += g2) {
+            const ChunkView v = chunk_view(p, q);
+            const int pr = v.lo + (int)threadIdx.x;
+            chunk_wave_counts(p.B, pr < v.hi ? p.pair_mask[pr] : 0ull, wc);
+            __syncthreads();
+            if ((int)threadIdx.x < p.B) {
+                int n = 0;
+                for (int w = 0; w < kChunk / 64; ++w) n += wc[w][threadIdx.x];
+                p.chunk_cnt[(size_t)q * p.B + threadIdx.x] = n;
+            }
+            __syncthreads();
+        }
     }
 }
 
@@ -362,10 +379,7 @@ __global__ __launch_bounds__(256) void chunk_scan_kernel(PermuteParams p) {
         lds);
 }
 
-__global__ __launch_bounds__(kChunk) void slabfill_kernel(PermuteParams p) {
-    const int q = blockIdx.x;
-    if (q >= p.totals[3]) return;
-    __shared__ int wc[kChunk / 64][64];
+__device__ __forceinline__ void slabfill_chunk(const PermuteParams& p, int q, int (*wc)[64]) {
     const ChunkView v = chunk_view(p, q);
     const int pr = v.lo + (int)threadIdx.x;
     const bool act = pr < v.hi;
@@ -384,6 +398,15 @@ __global__ __launch_bounds__(kChunk) void slabfill_kernel(PermuteParams p) {
             p.slab_rows[at] = pr;
             p.slab_tok[at] = tok;
         }
+    }
+}
+
+__global__ __launch_bounds__(kChunk) void slabfill_kernel(PermuteParams p) {
+    __shared__ int wc[kChunk / 64][64];
+    const int nq = p.totals[3];
+    for (int q = blockIdx.x; q < nq; q += gridDim.x) {
+        slabfill_chunk(p, q, wc);
+        __syncthreads();
     }
 }
 

@@ -9,12 +9,14 @@
 //   route            routing record + pair and slab counts
 //   scan             LDS prefix sums -> offsets and tile tables
 //   scatter          pair slots (expert segments sorted by block-mask key)
-//   slabfill         per-(expert, block) pair lists               (bf16)
+//   tables, chunk_scan, slabfill
+//                    tile tables, per-(expert, block) pair lists  (bf16)
 //   up, down         block-sparse MFMA grouped GEMMs              (bf16)
 //   pair_ffn_f32     per-pair fp32 FFN                            (fp32)
 //   combine          weighted merge in fixed order
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -497,15 +499,16 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     const int cus = cu_count();
     void* part = ws + plan.part;
     if (m.bf16) {
-        up_tile_kernel<<<m.nslab, 256, 0, st>>>(pp);
-        UNIF_LAUNCH_CHECK();
-        down_rowtile_kernel<<<(unsigned)plan.max_row_tiles, 64, 0, st>>>(pp);
-        UNIF_LAUNCH_CHECK();
-        chunk_count_kernel<<<(unsigned)plan.max_chunks, kChunk, 0, st>>>(pp);
+        // The grid-stride loops below are sized for the worst case only up to
+        // a few workgroups per CU; the real counts are on the device.
+        const unsigned gs = (unsigned)(4 * cus);
+        const unsigned g1 = std::min((unsigned)ceil_div_sz(plan.max_row_tiles, 4), gs);
+        const unsigned g2 = std::min((unsigned)plan.max_chunks, gs);
+        tables_kernel<<<(unsigned)m.nslab + g1 + g2, 256, 0, st>>>(pp, (int)g1);
         UNIF_LAUNCH_CHECK();
         chunk_scan_kernel<<<m.nslab, 256, 0, st>>>(pp);
         UNIF_LAUNCH_CHECK();
-        slabfill_kernel<<<(unsigned)plan.max_chunks, kChunk, 0, st>>>(pp);
+        slabfill_kernel<<<std::min((unsigned)plan.max_chunks, gs), kChunk, 0, st>>>(pp);
         UNIF_LAUNCH_CHECK();
         UNIF_MARK(2);
         // 4. block-sparse expert GEMMs
