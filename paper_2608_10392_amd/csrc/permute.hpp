@@ -8,11 +8,12 @@
 // each other for the down-projection tiles. Each (expert, block) "slab" gets
 // the list of pairs that use it, which the up-projection tiles read.
 //
-//   route_kernel   counts pairs per (expert, key) and rows per slab
+//   route_kernel       counts pairs per (expert, key), taking each pair's slot
+//                      in its bin, and rows per slab
 //   scan_kernel        one workgroup: LDS-staged exclusive prefix sums ->
 //                      bin cursors, expert segment offsets, slab offsets,
 //                      chunk offsets, tile tables
-//   scatter_kernel     one thread per token claims its pair slots
+//   scatter_kernel     one thread per token writes its pairs at their slots
 //   tables_kernel      up tile table (per slab), down row tiles (per row
 //                      tile), and per chunk of kChunk pairs of one expert:
 //                      pairs per block
@@ -106,7 +107,15 @@ __device__ int staged_exclusive_scan(int n, Get get, Put put, int* stage, int* l
     int carry = 0;
     for (int base = 0; base < n; base += kScanStage) {
         const int cnt = min(kScanStage, n - base);
-        for (int i = tid; i < cnt; i += T) stage[i] = get(base + i);
+        // Loads in batches of 8 per thread, all issued before any is stored.
+        for (int i0 = tid; i0 < cnt; i0 += 8 * T) {
+            int v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = (i0 + u * T < cnt) ? get(base + i0 + u * T) : 0;
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (i0 + u * T < cnt) stage[i0 + u * T] = v[u];
+        }
         __syncthreads();
         const int per = ceil_div(cnt, T);
         const int beg = min(cnt, tid * per), end = min(cnt, beg + per);
@@ -144,8 +153,12 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
     // them into the first.
     int* slab_count = const_cast<int*>(p.slab_count);
     for (int i = threadIdx.x; i < nslab; i += blockDim.x) {
+        int v[kSlabCopies];
+#pragma unroll
+        for (int c = 0; c < kSlabCopies; ++c) v[c] = slab_count[(size_t)c * nslab + i];
         int n = 0;
-        for (int c = 0; c < kSlabCopies; ++c) n += slab_count[(size_t)c * nslab + i];
+#pragma unroll
+        for (int c = 0; c < kSlabCopies; ++c) n += v[c];
         slab_count[i] = n;
     }
     __syncthreads();
@@ -190,69 +203,32 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
     }
 }
 
-constexpr int kScatterBatch = 8;
+// One thread per token writes its pairs at bin start + the slot the routing
+// kernel took for each (stored in pair_of, overwritten here with the pair).
 __global__ void scatter_kernel(PermuteParams p) {
     const int t = blockIdx.x * blockDim.x + threadIdx.x;
-    const int k = t < p.N ? p.nres[t] : 0;
-    const bool act = k > 0;   // padded tokens (and lanes past N) have k == 0
+    if (t >= p.N) return;
+    const int k = p.nres[t];
+    if (k == 0) return;  // padded token (valid tokens have k >= 1)
     const int B = p.B, kb = p.key_bits, K1 = p.K + 1;
     const uint64_t full = (B == 64) ? ~0ull : ((1ull << B) - 1ull);
-    const uint64_t m = act ? p.mask[t] : 0ull, rm = ~m & full;
+    const uint64_t m = p.mask[t], rm = ~m & full;
     const int ks = (int)(B > kb ? (m >> (B - kb)) : m);
     const int kr = (int)(B > kb ? (rm >> (B - kb)) : rm);
-    // Shared-expert pairs: block masks concentrate on few keys, so the lanes
-    // of a wave with the same key are grouped first; each group's first lane
-    // takes the group's slots with one atomic (all groups at once), and the
-    // lanes take consecutive slots in lane order.
-    const int lane = lane_id();
-    int leader = lane;
-    uint64_t grp = 0;
-    for (uint64_t pend = ballot(act); pend;) {
-        const int l0 = __builtin_ctzll(pend);
-        const int key = __shfl(ks, l0);
-        const uint64_t same = ballot(act && ks == key);
-        if (act && ks == key) {
-            leader = l0;
-            grp = same;
-        }
-        pend &= ~same;
-    }
-    int base = 0;
-    if (act && leader == lane) base = atomicAdd(&p.bin_cursor[ks], __popcll(grp));
-    // Residual pairs, kScatterBatch at a time: all slots of a batch are taken
-    // before any is used, so the atomics' latencies overlap.
-    int ex[kScatterBatch], slot[kScatterBatch];
+    int* of = p.pair_of + (size_t)t * K1;
     const int* eid = p.eids + (size_t)t * p.K;
-#pragma unroll
-    for (int i = 0; i < kScatterBatch; ++i) {
-        ex[i] = (i < k) ? eid[i] : 0;
-        slot[i] = (i < k) ? atomicAdd(&p.bin_cursor[(ex[i] << kb) + kr], 1) : 0;
-    }
-    base = __shfl(base, leader);
-    if (!act) return;
-    const int pr = base + __popcll(grp & lanes_below());
+    const int pr = p.bin_cursor[ks] + of[0];
     p.pair_token[pr] = t;
     p.pair_mask[pr] = m;
     p.pair_expert[pr] = 0;
-    p.pair_of[(size_t)t * K1] = pr;
-    for (int i0 = 0; i0 < k; i0 += kScatterBatch) {
-        if (i0 > 0) {
-#pragma unroll
-            for (int i = 0; i < kScatterBatch; ++i) {
-                ex[i] = (i0 + i < k) ? eid[i0 + i] : 0;
-                slot[i] = (i0 + i < k) ? atomicAdd(&p.bin_cursor[(ex[i] << kb) + kr], 1) : 0;
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < kScatterBatch; ++i) {
-            if (i0 + i < k) {
-                const int q = slot[i];
-                p.pair_token[q] = t;
-                p.pair_mask[q] = rm;
-                p.pair_expert[q] = ex[i];
-                p.pair_of[(size_t)t * K1 + 1 + i0 + i] = q;
-            }
-        }
+    of[0] = pr;
+    for (int i = 0; i < k; ++i) {
+        const int e = eid[i];
+        const int q = p.bin_cursor[(e << kb) + kr] + of[1 + i];
+        p.pair_token[q] = t;
+        p.pair_mask[q] = rm;
+        p.pair_expert[q] = e;
+        of[1 + i] = q;
     }
 }
 

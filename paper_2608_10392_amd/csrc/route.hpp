@@ -44,6 +44,7 @@ struct RouteParams {
     float* wts;
     int* bin_count;   // [(K+1) << key_bits] pairs per (expert, mask key), or null
     int* slab_count;  // [kSlabCopies][(K+1) * B] rows per (expert, block), or null
+    int* pair_rank;   // [N][K+1]: slot of each pair within its (expert, key) bin (with bin_count)
 };
 
 // Exact three-way split of an fp32 value into bf16 parts.
@@ -233,6 +234,8 @@ __device__ __forceinline__ int rank_in_values(const float* v, int n, int j) {
     return rank;
 }
 
+constexpr int kRankBatch = 8;   // residual-pair atomics in flight per token
+
 // Rankings of at most this many entries run on registers.
 constexpr int kSmallRank = 16;
 
@@ -411,18 +414,41 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
     const uint64_t rmask = ~mask & full;
     const int ks = (int)(B > kb ? (mask >> (B - kb)) : mask);
     const int kr = (int)(B > kb ? (rmask >> (B - kb)) : rmask);
+    // The count of a bin taken before a pair adds itself is the pair's slot
+    // within the bin (pair_rank), so the scatter needs no atomics.
     // Shared-expert pairs: every valid token has one, and block masks
     // concentrate on few keys, so the lanes of a wave with the same key are
-    // merged first (one global atomic per distinct key, not per token).
+    // grouped first; each group's first lane adds the group at once and the
+    // lanes take consecutive slots in lane order.
+    int leader = lane;
+    uint64_t grp = 0;
     for (uint64_t pend = ballot(v); pend;) {
-        const int leader = __builtin_ctzll(pend);
-        const int key = __shfl(ks, leader);
+        const int l0 = __builtin_ctzll(pend);
+        const int key = __shfl(ks, l0);
         const uint64_t same = ballot(v && ks == key);
-        if (lane == leader) atomicAdd(&p.bin_count[key], __popcll(same));
+        if (v && ks == key) {
+            leader = l0;
+            grp = same;
+        }
         pend &= ~same;
     }
-    if (v)
-        for (int i = 0; i < k; ++i) atomicAdd(&p.bin_count[(qs[i] << kb) + kr], 1);
+    int sbase = 0;
+    if (v && leader == lane) sbase = atomicAdd(&p.bin_count[ks], __popcll(grp));
+    int* rank = p.pair_rank + (size_t)(v ? tok : 0) * (K + 1);
+    // Residual pairs: the atomics of kRankBatch pairs are issued before any
+    // result is used, so their latencies overlap.
+    for (int i0 = 0; i0 < K; i0 += kRankBatch) {
+        if (!ballot(v && i0 < k)) break;
+        int r[kRankBatch];
+#pragma unroll
+        for (int u = 0; u < kRankBatch; ++u)
+            r[u] = (v && i0 + u < k) ? atomicAdd(&p.bin_count[(qs[i0 + u] << kb) + kr], 1) : 0;
+#pragma unroll
+        for (int u = 0; u < kRankBatch; ++u)
+            if (v && i0 + u < k) rank[1 + i0 + u] = r[u];
+    }
+    sbase = __shfl(sbase, leader);
+    if (v) rank[0] = sbase + __popcll(grp & lanes_below());
     // Rows per (expert, block): shared expert on I_shr, residual experts on I_res.
     for (int c = 0; c < B; ++c) {
         const uint64_t bits = ballot(v && ((mask >> c) & 1ull));

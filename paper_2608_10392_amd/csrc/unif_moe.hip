@@ -300,6 +300,7 @@ RouteParams route_params(const unif_moe_config* c, const Dims& m, const void* X,
     r.wts = wts;
     r.bin_count = nullptr;
     r.slab_count = nullptr;
+    r.pair_rank = nullptr;
     return r;
 }
 
@@ -452,6 +453,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
                                   wts);
     rp.bin_count = bin_count;
     rp.slab_count = slab_count;
+    rp.pair_rank = reinterpret_cast<int*>(ws + plan.pair_of);
     s = launch_route(m, rp, W_router, prototypes, wsplit, st);
     if (s != UNIF_OK) return s;
     UNIF_MARK(1);
