@@ -17,6 +17,8 @@ struct CombineParams {
     void* Y;
 };
 
+constexpr int kCombineBatch = 6;
+
 // bf16 path: one thread per 8 consecutive outputs; bf16 per-expert rows
 // (one 16-byte load each), one 16-byte store.
 __global__ void combine_bf16_kernel(CombineParams c) {
@@ -27,14 +29,33 @@ __global__ void combine_bf16_kernel(CombineParams c) {
     const int k = c.nres[t];
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     const u16* part = static_cast<const u16*>(c.part);
-    for (int i = 0; i <= k && k > 0; ++i) {
-        const float w = (i == 0) ? c.alpha[t] : c.wts[(size_t)t * c.K + i - 1];
-        const int pr = c.pair_of[(size_t)t * (c.K + 1) + i];
-        const u32x4 v = ld16(part + (size_t)pr * c.d + ch * 8);
+    const int* of = c.pair_of + (size_t)t * (c.K + 1);
+    const float* wt = c.wts + (size_t)t * c.K;
+    // Rows in batches of kCombineBatch: the weights and pair indices of a
+    // batch, then its rows, are loaded before any is used (the latencies
+    // overlap); the sum still runs in the fixed order.
+    for (int i0 = 0; i0 <= k && k > 0; i0 += kCombineBatch) {
+        float w[kCombineBatch];
+        int pr[kCombineBatch];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            acc[2 * q] = fmaf(w, __uint_as_float(v[q] << 16), acc[2 * q]);
-            acc[2 * q + 1] = fmaf(w, __uint_as_float(v[q] & 0xffff0000u), acc[2 * q + 1]);
+        for (int u = 0; u < kCombineBatch; ++u) {
+            const int i = i0 + u;
+            w[u] = (i > k) ? 0.f : (i == 0 ? c.alpha[t] : wt[i - 1]);
+            pr[u] = (i > k) ? 0 : of[i];
+        }
+        u32x4 v[kCombineBatch];
+#pragma unroll
+        for (int u = 0; u < kCombineBatch; ++u)
+            v[u] = (i0 + u <= k) ? ld16(part + (size_t)pr[u] * c.d + ch * 8) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int u = 0; u < kCombineBatch; ++u) {
+            if (i0 + u <= k) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    acc[2 * q] = fmaf(w[u], __uint_as_float(v[u][q] << 16), acc[2 * q]);
+                    acc[2 * q + 1] = fmaf(w[u], __uint_as_float(v[u][q] & 0xffff0000u), acc[2 * q + 1]);
+                }
+            }
         }
     }
     u32x4 o;
