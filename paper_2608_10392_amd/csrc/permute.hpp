@@ -10,9 +10,9 @@
 //
 //   route_kernel       counts pairs per (expert, key), taking each pair's slot
 //                      in its bin, and rows per slab
-//   scan_kernel        one workgroup: LDS-staged exclusive prefix sums ->
-//                      bin cursors, expert segment offsets, slab offsets,
-//                      chunk offsets, tile tables
+//   scan_kernel        one workgroup per expert: LDS-staged exclusive prefix
+//                      sums -> bin cursors, expert segment offsets, slab
+//                      offsets, chunk offsets, tile tables
 //   scatter_kernel     one thread per token writes its pairs at their slots
 //   tables_kernel      up tile table (per slab), down row tiles (per row
 //                      tile), and per chunk of kChunk pairs of one expert:
@@ -144,32 +144,55 @@ __device__ int staged_exclusive_scan(int n, Get get, Put put, int* stage, int* l
     return carry;
 }
 
+// One workgroup per expert. The routing kernel leaves the row counts per
+// slab and the pair counts per expert in kSlabCopies copies (slab_count:
+// [copy][nslab + K + 1]). Every workgroup sums the expert counts into the
+// segment offsets; workgroup e scans its expert's bins from its segment
+// start; workgroup 0 also builds the slab offsets and the tile tables.
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
     __shared__ int lds[kScanThreads];
     __shared__ int stage[kScanStage];
     __shared__ int segs[66];   // K + 2 <= 66
-    const int K1 = p.K + 1, nbin = K1 << p.key_bits, nslab = K1 * p.B;
-    // The routing kernel leaves the row counts in kSlabCopies copies: sum
-    // them into the first.
-    int* slab_count = const_cast<int*>(p.slab_count);
-    for (int i = threadIdx.x; i < nslab; i += blockDim.x) {
+    const int K1 = p.K + 1, nslab = K1 * p.B, ncnt = nslab + K1, nb = 1 << p.key_bits;
+    const int e = blockIdx.x;
+    int* cnt = const_cast<int*>(p.slab_count);
+    if ((int)threadIdx.x < K1) {
         int v[kSlabCopies];
 #pragma unroll
-        for (int c = 0; c < kSlabCopies; ++c) v[c] = slab_count[(size_t)c * nslab + i];
+        for (int c = 0; c < kSlabCopies; ++c) v[c] = cnt[(size_t)c * ncnt + nslab + threadIdx.x];
         int n = 0;
 #pragma unroll
         for (int c = 0; c < kSlabCopies; ++c) n += v[c];
-        slab_count[i] = n;
+        lds[threadIdx.x] = n;
     }
     __syncthreads();
-    const int P = staged_exclusive_scan(
-        nbin, [&](int i) { return p.bin_count[i]; }, [&](int i, int v) { p.bin_cursor[i] = v; }, stage, lds);
-    // Segment offsets, also kept in LDS for the per-expert loops below.
-    for (int e = threadIdx.x; e <= K1; e += blockDim.x) {
-        const int o = (e < K1) ? p.bin_cursor[e << p.key_bits] : P;
-        p.seg_off[e] = o;
-        segs[e] = o;
+    if (threadIdx.x == 0) {
+        int run = 0;
+        for (int x = 0; x < K1; ++x) {
+            segs[x] = run;
+            run += lds[x];
+        }
+        segs[K1] = run;
     }
+    __syncthreads();
+    const int base = segs[e];
+    staged_exclusive_scan(
+        nb, [&](int i) { return p.bin_count[(size_t)e * nb + i]; },
+        [&](int i, int v) { p.bin_cursor[(size_t)e * nb + i] = base + v; }, stage, lds);
+    if (e != 0) return;
+    for (int x = threadIdx.x; x <= K1; x += blockDim.x) p.seg_off[x] = segs[x];
+    const int P = segs[K1];
+    // Row counts per slab: sum the copies into the first.
+    for (int i = threadIdx.x; i < nslab; i += blockDim.x) {
+        int v[kSlabCopies];
+#pragma unroll
+        for (int c = 0; c < kSlabCopies; ++c) v[c] = cnt[(size_t)c * ncnt + i];
+        int n = 0;
+#pragma unroll
+        for (int c = 0; c < kSlabCopies; ++c) n += v[c];
+        cnt[i] = n;
+    }
+    __syncthreads();
     const int bm = p.bm_up;
     const int nup = staged_exclusive_scan(
         nslab, [&](int i) { return ceil_div(p.slab_count[i], bm); },
@@ -183,17 +206,17 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
         p.up_tile_off[nslab] = nup;
         if (p.chunk_off != nullptr) {
             int q = 0;
-            for (int e = 0; e < K1; ++e) {
-                p.chunk_off[e] = q;
-                q += ceil_div(segs[e + 1] - segs[e], kChunk);
+            for (int x = 0; x < K1; ++x) {
+                p.chunk_off[x] = q;
+                q += ceil_div(segs[x + 1] - segs[x], kChunk);
             }
             p.chunk_off[K1] = q;
             p.totals[3] = q;
         }
         int run = 0;
-        for (int e = 0; e < K1; ++e) {
-            p.down_tile_off[e] = run;
-            run += ceil_div(segs[e + 1] - segs[e], p.bm_down);
+        for (int x = 0; x < K1; ++x) {
+            p.down_tile_off[x] = run;
+            run += ceil_div(segs[x + 1] - segs[x], p.bm_down);
         }
         p.down_tile_off[K1] = run;
         p.totals[0] = P;

@@ -43,7 +43,7 @@ struct RouteParams {
     int* eids;
     float* wts;
     int* bin_count;   // [(K+1) << key_bits] pairs per (expert, mask key), or null
-    int* slab_count;  // [kSlabCopies][(K+1) * B] rows per (expert, block), or null
+    int* slab_count;  // [kSlabCopies][(K+1) B + K+1]: rows per (expert, block), then pairs per expert; or null
     int* pair_rank;   // [N][K+1]: slot of each pair within its (expert, key) bin (with bin_count)
 };
 
@@ -449,6 +449,12 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
     }
     sbase = __shfl(sbase, leader);
     if (v) rank[0] = sbase + __popcll(grp & lanes_below());
+    // Pairs per expert, after the row counts in slab_lds.
+    int* ecnt = slab_lds + (K + 1) * B;
+    {
+        const uint64_t vb = ballot(v);
+        if (lane == 0 && vb) atomicAdd(&ecnt[0], __popcll(vb));
+    }
     // Rows per (expert, block): shared expert on I_shr, residual experts on I_res.
     for (int c = 0; c < B; ++c) {
         const uint64_t bits = ballot(v && ((mask >> c) & 1ull));
@@ -456,7 +462,9 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
     }
     for (int e = 1; e <= K; ++e) {
         const bool has = v && ((sel >> (e - 1)) & 1ull);
-        if (!ballot(has)) continue;
+        const uint64_t hb = ballot(has);
+        if (!hb) continue;
+        if (lane == 0) atomicAdd(&ecnt[e], __popcll(hb));
         for (int c = 0; c < B; ++c) {
             const uint64_t bits = ballot(has && !((mask >> c) & 1ull));
             if (lane == 0 && bits) atomicAdd(&slab_lds[e * B + c], __popcll(bits));
@@ -476,8 +484,10 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteParams p) {
     int* slab_lds = reinterpret_cast<int*>(KEYS + kRouteTok * p.key_stride);
     const int tok0 = blockIdx.x * kRouteTok;
     const int nslab = (p.K + 1) * p.B;
+    // slab_lds: rows per slab, then pairs per expert.
+    const int ncnt = nslab + p.K + 1;
     if (p.slab_count)
-        for (int i = threadIdx.x; i < nslab; i += blockDim.x) slab_lds[i] = 0;
+        for (int i = threadIdx.x; i < ncnt; i += blockDim.x) slab_lds[i] = 0;
     if constexpr (NCT > 0) route_logits_bf16<NCT>(p, L, tok0);
     else route_logits_f32(p, L, tok0);
     __syncthreads();
@@ -497,8 +507,8 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteParams p) {
     // Workgroup totals go to one of kSlabCopies copies of the counts, which
     // spreads the same-address atomics; the permutation sums the copies.
     if (p.slab_count) {
-        int* dst = p.slab_count + (size_t)(blockIdx.x % kSlabCopies) * nslab;
-        for (int i = threadIdx.x; i < nslab; i += blockDim.x)
+        int* dst = p.slab_count + (size_t)(blockIdx.x % kSlabCopies) * ncnt;
+        for (int i = threadIdx.x; i < ncnt; i += blockDim.x)
             if (slab_lds[i]) atomicAdd(&dst[i], slab_lds[i]);
     }
 }

@@ -93,7 +93,7 @@ Dims dims_of(const unif_moe_config* c) {
 // aligned; left out when they would not fit), row counts.
 size_t route_lds_bytes_with(const Dims& m, int key_stride) {
     const size_t head = (size_t)kRouteTok * m.lstride + (size_t)kRouteTok * (m.K + 1) * 2;
-    return sizeof(float) * (((head + 3) & ~(size_t)3) + (size_t)kRouteTok * key_stride + (size_t)m.K1 * m.B);
+    return sizeof(float) * (((head + 3) & ~(size_t)3) + (size_t)kRouteTok * key_stride + (size_t)m.K1 * m.B + m.K1);
 }
 int route_key_stride(const Dims& m) {
     return route_lds_bytes_with(m, key_row(m.K, m.B)) <= kLdsLimit ? key_row(m.K, m.B) : 0;
@@ -190,7 +190,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.wsplit = cv.take(m.bf16 ? (size_t)3 * m.NLP * m.d * sizeof(u16) : 0);
     p.bin_count = cv.take(4 * (size_t)m.nbin);
     p.zero_begin = p.bin_count;
-    p.slab_count = cv.take(4 * (size_t)m.nslab * kSlabCopies);
+    p.slab_count = cv.take(4 * ((size_t)m.nslab + K1) * kSlabCopies);
     p.totals = cv.take(4 * 8);
     p.queues = cv.take(4 * 16);   // per-XCD tile counters: up, then down
     p.zero_page = cv.take(256);
@@ -493,7 +493,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.rt_info = m.bf16 ? reinterpret_cast<int4*>(ws + plan.rt_info) : nullptr;
     pp.rt_masks = m.bf16 ? reinterpret_cast<uint64_t*>(ws + plan.rt_masks) : nullptr;
     pp.down_tiles = m.bf16 ? reinterpret_cast<int*>(ws + plan.down_tiles) : nullptr;
-    scan_kernel<<<1, kScanThreads, 0, st>>>(pp);
+    scan_kernel<<<m.K1, kScanThreads, 0, st>>>(pp);
     UNIF_LAUNCH_CHECK();
     scatter_kernel<<<ceil_div(m.N, 256), 256, 0, st>>>(pp);
     UNIF_LAUNCH_CHECK();
