@@ -109,6 +109,18 @@ __device__ __forceinline__ uint64_t lanes_below() {
 
 __host__ __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+// Sort key of a B-bit block mask: its top kb bits (kb <= 16), replaced by
+// their rank in the reflected Gray code sequence, so that key order puts
+// masks that differ in one block next to each other.
+__device__ __forceinline__ int mask_key(uint64_t mask, int B, int kb) {
+    uint32_t v = (uint32_t)(B > kb ? (mask >> (B - kb)) : mask);
+    v ^= v >> 1;
+    v ^= v >> 2;
+    v ^= v >> 4;
+    v ^= v >> 8;
+    return (int)v;
+}
+
 // Largest i in [0, n) with off[i] <= x (off ascending, off[0] = 0 <= x).
 __device__ __forceinline__ int upper_index(const int* off, int n, int x) {
     int lo = 0, hi = n;

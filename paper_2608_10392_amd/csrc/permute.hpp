@@ -3,10 +3,11 @@
 // A "pair" is one (token, expert) evaluation: the shared expert on the
 // token's blocks I_shr, or one of its k residual experts on I_res
 // (Eq. selected-shared-output, selected-residual-output). Pairs are laid out
-// grouped by expert and, inside an expert, by the top key_bits bits of their
-// block mask (a counting sort), so that pairs that share blocks sit next to
-// each other for the down-projection tiles. Each (expert, block) "slab" gets
-// the list of pairs that use it, which the up-projection tiles read.
+// grouped by expert and, inside an expert, by the Gray-code rank of the top
+// key_bits bits of their block mask (a counting sort, see mask_key), so that
+// pairs that share blocks sit next to each other for the down-projection
+// tiles. Each (expert, block) "slab" gets the list of pairs that use it,
+// which the up-projection tiles read.
 //
 //   route_kernel       counts pairs per (expert, key), taking each pair's slot
 //                      in its bin, and rows per slab
@@ -14,18 +15,18 @@
 //                      sums -> bin cursors, expert segment offsets, slab
 //                      offsets, chunk offsets, tile tables
 //   scatter_kernel     one thread per token writes its pairs at their slots
-//   tables_kernel      up tile table (per slab), down row tiles (per row
-//                      tile), and per chunk of kChunk pairs of one expert:
-//                      pairs per block
+//   tables_kernel      down row tiles (per row tile), and per chunk of
+//                      kChunk pairs of one expert: pairs per block
 //   chunk_scan_kernel  per slab: exclusive scan of its chunk counts
 //   slabfill_kernel    per chunk: each pair writes itself into the slabs of
-//                      its blocks, in pair order (deterministic)
+//                      its blocks, in pair order (deterministic); per
+//                      (expert, block group): the up tile table
 //
 // Each slab's row list starts at a multiple of the up-projection tile height
 // bm_up and holds the slab's pairs in pair order, with their tokens beside
 // them, so a tile's gather needs no dependent lookups. Up tiles are listed
-// expert by expert, and inside an expert by groups of blocks, row chunk j,
-// then block c (see up_tiles_of_slab).
+// expert by expert, and inside an expert by groups of blocks, then by the
+// stretch of the expert's pairs they cover (see up_tiles_of_group).
 #pragma once
 #include "common.hpp"
 
@@ -236,8 +237,8 @@ __global__ void scatter_kernel(PermuteParams p) {
     const int B = p.B, kb = p.key_bits, K1 = p.K + 1;
     const uint64_t full = (B == 64) ? ~0ull : ((1ull << B) - 1ull);
     const uint64_t m = p.mask[t], rm = ~m & full;
-    const int ks = (int)(B > kb ? (m >> (B - kb)) : m);
-    const int kr = (int)(B > kb ? (rm >> (B - kb)) : rm);
+    const int ks = mask_key(m, B, kb);
+    const int kr = mask_key(rm, B, kb);
     int* of = p.pair_of + (size_t)t * K1;
     const int* eid = p.eids + (size_t)t * p.K;
     const int pr = p.bin_cursor[ks] + of[0];
@@ -255,26 +256,49 @@ __global__ void scatter_kernel(PermuteParams p) {
     }
 }
 
-// Up tile table. Tiles are listed expert by expert; inside an expert the
-// blocks are taken in groups of up_group, and inside a group by row chunk j,
-// then block c. Tile (e, g, j, c) sits at the first tile of the group
-// (up_tile_off of its first slab) + sum over the group's blocks c' of
-// min(j, tiles(e, c')) + the number of the group's blocks c' < c that have a
-// tile j. One workgroup per slab, one thread per tile of the slab.
-__device__ __forceinline__ void up_tiles_of_slab(const PermuteParams& p, int sl, int* tiles) {
-    const int e = sl / p.B, c = sl - e * p.B;
-    const int bm = p.bm_up;
-    const int g0 = (c / p.up_group) * p.up_group, g1 = min(p.B, g0 + p.up_group);
-    if ((int)threadIdx.x < p.B) tiles[threadIdx.x] = ceil_div(p.slab_count[e * p.B + threadIdx.x], bm);
+// Up tile table, built once the slab rows of every chunk are known. Tiles
+// are listed expert by expert; inside an expert the blocks are taken in
+// groups of up_group, and inside a group tile j of block c is placed by the
+// chunk q of the expert's pairs in which its first row falls, then by c,
+// then by j. Tiles that run close together in this order gather the token
+// rows of the same stretch of the expert's pairs, which a group's weight
+// slabs share in L2. One workgroup per (expert, group); each thread takes a
+// contiguous range of the expert's chunks. tile_lo(i, c) is the first tile
+// of slab c whose first row is at or after chunk i's first slab row.
+__device__ __forceinline__ void up_tiles_of_group(const PermuteParams& p, int grp, int* lds) {
+    const int ngr = ceil_div(p.B, p.up_group);
+    const int e = grp / ngr, g = grp - e * ngr;
+    const int c0 = g * p.up_group, c1 = min(p.B, c0 + p.up_group);
+    const int q0 = p.chunk_off[e], nq = p.chunk_off[e + 1] - q0;
+    const int bm = p.bm_up, sl0 = e * p.B;
+    auto tile_lo = [&](int i, int c) {
+        const int sl = sl0 + c;
+        const int r = (i < nq) ? p.chunk_cnt[(size_t)(q0 + i) * p.B + c] - p.slab_off[sl] : p.slab_count[sl];
+        return ceil_div(r, bm);
+    };
+    const int tid = threadIdx.x, T = blockDim.x;
+    const int per = ceil_div(nq, T);
+    const int qa = min(nq, tid * per), qb = min(nq, qa + per);
+    int n = 0;
+    for (int c = c0; c < c1; ++c) n += tile_lo(qb, c) - tile_lo(qa, c);
+    lds[tid] = n;
     __syncthreads();
-    const int cnt = p.slab_count[sl], nt = tiles[c];
-    const int first = p.up_tile_off[e * p.B + g0];
-    for (int j = threadIdx.x; j < nt; j += blockDim.x) {
-        int pos = first;
-        for (int c2 = g0; c2 < g1; ++c2) pos += min(j, tiles[c2]) + ((c2 < c && tiles[c2] > j) ? 1 : 0);
-        p.up_tile_info[pos] = sl | (min(bm, cnt - j * bm) << 16);
-        p.up_tile_rows[pos] = p.slab_off[sl] + j * bm;
+    for (int off = 1; off < T; off <<= 1) {
+        const int v = (tid >= off) ? lds[tid - off] : 0;
+        __syncthreads();
+        lds[tid] += v;
+        __syncthreads();
     }
+    int pos = p.up_tile_off[sl0 + c0] + lds[tid] - n;
+    for (int i = qa; i < qb; ++i)
+        for (int c = c0; c < c1; ++c) {
+            const int sl = sl0 + c, cnt = p.slab_count[sl];
+            for (int j = tile_lo(i, c), je = tile_lo(i + 1, c); j < je; ++j, ++pos) {
+                p.up_tile_info[pos] = sl | (min(bm, cnt - j * bm) << 16);
+                p.up_tile_rows[pos] = p.slab_off[sl] + j * bm;
+            }
+        }
+    __syncthreads();
 }
 
 // Down row tiles: bm_down consecutive pairs of one expert segment. One wave
@@ -331,25 +355,20 @@ __device__ __forceinline__ void chunk_wave_counts(int B, uint64_t m, int (*wc)[6
     }
 }
 
-// The three tables that only need the scatter's output, in one launch
-// (each is small; a kernel launch costs more than their work): workgroups
-// [0, nslab) build the up tiles of one slab each, the next g1 workgroups the
-// down row tiles (one wave per row tile), the rest count the chunks' rows
-// per block.
+// The two tables that only need the scatter's output, in one launch (each
+// is small; a kernel launch costs more than their work): workgroups [0, g1)
+// build the down row tiles (one wave per row tile), the rest count the
+// chunks' rows per block.
 __global__ __launch_bounds__(256) void tables_kernel(PermuteParams p, int g1) {
     static_assert(kChunk == 256, "one thread per chunk pair");
-    __shared__ int tiles[64];
     __shared__ int wc[kChunk / 64][64];
-    const int nslab = (p.K + 1) * p.B;
     const int b = blockIdx.x;
-    if (b < nslab) {
-        up_tiles_of_slab(p, b, tiles);
-    } else if (b < nslab + g1) {
+    if (b < g1) {
         const int nrt = p.totals[4];
-        for (int rt = (b - nslab) * 4 + (threadIdx.x >> 6); rt < nrt; rt += g1 * 4) down_rowtile(p, rt);
+        for (int rt = b * 4 + (threadIdx.x >> 6); rt < nrt; rt += g1 * 4) down_rowtile(p, rt);
     } else {
-        const int g2 = gridDim.x - nslab - g1, nq = p.totals[3];
-        for (int q = b - nslab - g1; q < nq; q += g2) {
+        const int g2 = gridDim.x - g1, nq = p.totals[3];
+        for (int q = b - g1; q < nq; q += g2) {
             const ChunkView v = chunk_view(p, q);
             const int pr = v.lo + (int)threadIdx.x;
             chunk_wave_counts(p.B, pr < v.hi ? p.pair_mask[pr] : 0ull, wc);
@@ -400,10 +419,17 @@ __device__ __forceinline__ void slabfill_chunk(const PermuteParams& p, int q, in
     }
 }
 
-__global__ __launch_bounds__(kChunk) void slabfill_kernel(PermuteParams p) {
+// Workgroups [0, n_groups) build the up tile table of one (expert, block
+// group) each; the rest fill the chunks' slab rows.
+__global__ __launch_bounds__(kChunk) void slabfill_kernel(PermuteParams p, int n_groups) {
     __shared__ int wc[kChunk / 64][64];
+    const int b = blockIdx.x;
+    if (b < n_groups) {
+        up_tiles_of_group(p, b, &wc[0][0]);
+        return;
+    }
     const int nq = p.totals[3];
-    for (int q = blockIdx.x; q < nq; q += gridDim.x) {
+    for (int q = b - n_groups; q < nq; q += gridDim.x - n_groups) {
         slabfill_chunk(p, q, wc);
         __syncthreads();
     }

@@ -412,8 +412,8 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
     const int kb = p.key_bits;
     const int lane = lane_id();
     const uint64_t rmask = ~mask & full;
-    const int ks = (int)(B > kb ? (mask >> (B - kb)) : mask);
-    const int kr = (int)(B > kb ? (rmask >> (B - kb)) : rmask);
+    const int ks = mask_key(mask, B, kb);
+    const int kr = mask_key(rmask, B, kb);
     // The count of a bin taken before a pair adds itself is the pair's slot
     // within the bin (pair_rank), so the scatter needs no atomics.
     // Shared-expert pairs: every valid token has one, and block masks

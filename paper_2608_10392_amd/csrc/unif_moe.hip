@@ -41,10 +41,16 @@ constexpr size_t kLdsLimit = 160 * 1024;
 // gathered rows x the whole block width M. Down: 256 pairs x 256 output
 // columns (128 when d is not a multiple of 256).
 constexpr int kUpTM = kFfnTM;
-// Up tiles are ordered by expert, then by groups of this many blocks, then
-// row chunk, then block: the tiles that run together share token rows
-// (across the group's blocks) and weight slabs (within a group).
-constexpr int kUpBlockGroup = 4;
+// Up tiles are ordered by expert, then by groups of blocks, then by the
+// stretch of the expert's pairs they cover: the tiles that run together on
+// one XCD share token rows (across the group's blocks) and weight slabs
+// (within a group). A group's weight slabs take at most this many bytes,
+// about 60% of one XCD's 4 MB L2.
+constexpr size_t kUpGroupWeightBytes = (size_t)5 << 19;
+int up_block_group(int d, int M, int B) {
+    const size_t slab = (size_t)2 * d * M;
+    return (int)std::max<size_t>(1, std::min<size_t>((size_t)B, kUpGroupWeightBytes / slab));
+}
 // Down tiles: 256 pairs x 256 columns when d is a multiple of 256, else
 // 128 x 384 when d is a multiple of 384 (d = 384: one column tile), else
 // 256 x 128.
@@ -466,7 +472,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.key_bits = m.key_bits;
     const DownShape dsh = down_shape(m.d);
     pp.bm_up = kUpTM;
-    pp.up_group = kUpBlockGroup;
+    pp.up_group = up_block_group(m.d, m.M, m.B);
     pp.bm_down = dsh.tm;
     pp.down_col_tiles = m.bf16 ? m.d / dsh.bn : 1;
     pp.mask = mask;
@@ -506,11 +512,12 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         const unsigned gs = (unsigned)(4 * cus);
         const unsigned g1 = std::min((unsigned)ceil_div_sz(plan.max_row_tiles, 4), gs);
         const unsigned g2 = std::min((unsigned)plan.max_chunks, gs);
-        tables_kernel<<<(unsigned)m.nslab + g1 + g2, 256, 0, st>>>(pp, (int)g1);
+        tables_kernel<<<g1 + g2, 256, 0, st>>>(pp, (int)g1);
         UNIF_LAUNCH_CHECK();
         chunk_scan_kernel<<<m.nslab, 256, 0, st>>>(pp);
         UNIF_LAUNCH_CHECK();
-        slabfill_kernel<<<std::min((unsigned)plan.max_chunks, gs), kChunk, 0, st>>>(pp);
+        const int up_groups = m.K1 * ceil_div(m.B, pp.up_group);
+        slabfill_kernel<<<(unsigned)up_groups + std::min((unsigned)plan.max_chunks, gs), kChunk, 0, st>>>(pp, up_groups);
         UNIF_LAUNCH_CHECK();
         UNIF_MARK(2);
         // 4. block-sparse expert GEMMs
