@@ -362,8 +362,8 @@ void up_kernel(UpParams p) {
                 u32x4 lo, hi;
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    lo[t] = pack_bf16x2(gelu_as7126(v[2 * t]), gelu_as7126(v[2 * t + 1]));
-                    hi[t] = pack_bf16x2(gelu_as7126(v[8 + 2 * t]), gelu_as7126(v[9 + 2 * t]));
+                    lo[t] = pack_bf16x2(gelu_exp2poly(v[2 * t]), gelu_exp2poly(v[2 * t + 1]));
+                    hi[t] = pack_bf16x2(gelu_exp2poly(v[8 + 2 * t]), gelu_exp2poly(v[9 + 2 * t]));
                 }
                 st16(dst + 32 * j, lo);
                 st16(dst + 32 * j + 8, hi);

@@ -47,9 +47,18 @@ struct RouteParams {
     int* pair_rank;   // [N][K+1]: slot of each pair within its (expert, key) bin (with bin_count)
 };
 
-// Exact three-way split of an fp32 value into bf16 parts.
+// Exact three-way split of an fp32 value into bf16 parts, in workgroups
+// [0, nsplit); the workgroups after them zero zwords words at zero (the
+// forward's counters, in the same launch).
 __global__ void split_router_kernel(const float* __restrict__ Wr, const float* __restrict__ mu,
-                                    int K, int B, int d, int NLP, u16* __restrict__ out) {
+                                    int K, int B, int d, int NLP, u16* __restrict__ out, int nsplit,
+                                    uint32_t* __restrict__ zero, size_t zwords) {
+    if ((int)blockIdx.x >= nsplit) {
+        const size_t stride = (size_t)(gridDim.x - nsplit) * blockDim.x;
+        for (size_t i = (size_t)(blockIdx.x - nsplit) * blockDim.x + threadIdx.x; i < zwords; i += stride)
+            zero[i] = 0u;
+        return;
+    }
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     const int total = NLP * d;
     if (i >= total) return;

@@ -311,12 +311,16 @@ RouteParams route_params(const unif_moe_config* c, const Dims& m, const void* X,
 }
 
 // Router logits and decisions (shared by unif_moe_route and the forward).
+// The forward's counters (zwords words at zero) are cleared in the launch
+// that splits the router weights.
 int32_t launch_route(const Dims& m, const RouteParams& rp, const float* Wr, const float* mu, u16* wsplit,
-                     hipStream_t st) {
+                     hipStream_t st, uint32_t* zero = nullptr, size_t zwords = 0) {
     if (m.N == 0) return UNIF_OK;
-    if (m.bf16) {
-        const int total = m.NLP * m.d;
-        split_router_kernel<<<ceil_div(total, 256), 256, 0, st>>>(Wr, mu, m.K, m.B, m.d, m.NLP, wsplit);
+    const int nsplit = m.bf16 ? ceil_div(m.NLP * m.d, 256) : 0;
+    const int nzero = zwords ? (int)std::min<size_t>(ceil_div_sz(zwords, 256), 1024) : 0;
+    if (nsplit + nzero > 0) {
+        split_router_kernel<<<nsplit + nzero, 256, 0, st>>>(Wr, mu, m.K, m.B, m.d, m.NLP, wsplit, nsplit, zero,
+                                                           zwords);
         UNIF_LAUNCH_CHECK();
     }
     const size_t lds = route_lds_bytes(m);
@@ -448,19 +452,15 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     int* totals = reinterpret_cast<int*>(ws + plan.totals);
 
     UNIF_MARK(0);
-    // 1. zero the counters
+    // 1. zero the counters (in the launch before routing) and 2. routing + counts
     const size_t zwords = (plan.zero_end - plan.zero_begin) / 4;
-    fill_zero_kernel<<<ceil_div((int)zwords, 256), 256, 0, st>>>(reinterpret_cast<uint32_t*>(ws + plan.zero_begin),
-                                                                 zwords);
-    UNIF_LAUNCH_CHECK();
-
-    // 2. routing + counts
     RouteParams rp = route_params(cfg, m, X, valid, W_router, prototypes, wsplit, alpha, nsh, mask, nres, eids,
                                   wts);
     rp.bin_count = bin_count;
     rp.slab_count = slab_count;
     rp.pair_rank = reinterpret_cast<int*>(ws + plan.pair_of);
-    s = launch_route(m, rp, W_router, prototypes, wsplit, st);
+    s = launch_route(m, rp, W_router, prototypes, wsplit, st, reinterpret_cast<uint32_t*>(ws + plan.zero_begin),
+                     zwords);
     if (s != UNIF_OK) return s;
     UNIF_MARK(1);
 

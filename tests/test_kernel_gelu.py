@@ -1,0 +1,81 @@
+"""The bf16 up-projection's GELU approximation (csrc/common.hpp, gelu_exp2poly).
+
+Host-side check of the kernel's arithmetic: the coefficients in the header
+are the ones the committed fit script prints, and the formula, evaluated in
+fp32 steps here, stays within its stated error of x Phi(x) (scipy's normal
+CDF in fp64). No GPU needed.
+"""
+import os
+import re
+import sys
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2608_10392_amd", "csrc")
+special = pytest.importorskip("scipy.special")
+
+
+def header_coefficients():
+    text = open(os.path.join(CSRC, "common.hpp")).read()
+    body = re.search(r"kGeluQ\[8\]\s*=\s*\{([^}]*)\}", text).group(1)
+    ymax = float(re.search(r"kGeluQMax\s*=\s*([0-9.eE+-]+)f", text).group(1))
+    return [float(v.strip().rstrip("f")) for v in body.split(",")], ymax
+
+
+def f32(v):
+    return np.asarray(v, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+def fma32(a, b, c):
+    # fp32 operands: the product is exact in fp64, so this rounds once more
+    # than a fused fp32 fma at most in rare halfway cases.
+    return f32(np.asarray(a, np.float64) * b + c)
+
+
+def gelu_kernel(x, c, ymax):
+    x = f32(x)
+    y = np.minimum(np.abs(x), ymax)
+    q = fma32(c[7], y, c[6])
+    for i in range(5, -1, -1):
+        q = fma32(q, y, c[i])
+    e = f32(np.exp2(q))
+    return fma32(np.abs(x), f32(0.5 - e), f32(0.5 * x))
+
+
+def test_header_matches_fit_script():
+    sys.path.insert(0, CSRC)
+    try:
+        import gelu_coeffs
+    finally:
+        sys.path.pop(0)
+    c, ymax = header_coefficients()
+    assert ymax == gelu_coeffs.Y
+    np.testing.assert_array_equal(np.float32(c), np.float32(gelu_coeffs.coefficients()))
+
+
+def test_error_bounds():
+    c, ymax = header_coefficients()
+    x = np.concatenate([np.linspace(-12, 12, 480001), [0.0, 1e-30, -1e-30, 1e-6, -1e-6, 6.0, -6.0]])
+    x = f32(x)
+    exact = x * special.ndtr(x)
+    got = gelu_kernel(x, c, ymax)
+    err = np.abs(got - exact)
+    assert err.max() < 5e-7
+    # Relative 1e-5 from the fit, plus the rounding of 1/2 - Phi(-|a|) to
+    # fp32 (at most 2^-25 |a|), which dominates in the far negative tail.
+    inside = np.abs(x) < ymax
+    assert (err[inside] <= 1e-5 * np.abs(exact[inside]) + 3e-8 * np.abs(x[inside])).all()
+    pos = x > -2
+    assert (err[pos] <= 1e-5 * np.abs(exact[pos])).all()
+    # GELU(0) = 0 and the signs of the two branches.
+    assert gelu_kernel(np.array([0.0]), c, ymax)[0] == 0.0
+    assert (got[x > 0] > 0).all() and (got[x < 0] <= 0).all()
+
+
+def test_infinities_and_nan():
+    c, ymax = header_coefficients()
+    with np.errstate(invalid="ignore"):
+        v = gelu_kernel(np.array([np.inf, np.nan]), c, ymax)
+    assert v[0] == np.inf and np.isnan(v[1])
