@@ -163,8 +163,9 @@ __device__ __forceinline__ void wait_stage(int s, bool after_epi, bool has_next)
 //    row), so the counts are exact.
 //  * A tile has nk = d / 64 stages; tiles shorter than 4 stages are padded
 //    with stages that re-read k = 0.. and run no MFMAs (the row-list copy of
-//    stage 0 is waited for at the barrier of stage 2).
-template <int MG>
+//    stage 0 is waited for at the barrier of stage 2). PAD: whether d < 256
+//    (else no stage is padding and the MFMAs need no per-stage test).
+template <int MG, bool PAD>
 __global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void up_kernel(UpParams p) {
     using S = Stage;
@@ -296,7 +297,7 @@ void up_kernel(UpParams p) {
 #pragma unroll
             for (int j = 0; j < MG; ++j) acc[i][j] = f32x16{};
         for (int s = 0; s < nst; ++s) {
-            const bool real = s < nk;
+            const bool real = !PAD || s < nk;
             const uint32_t other = slot ^ STAGE;
             // k step k: reads of the next k step into (X2, W2) first (a
             // whole k step of MFMAs covers their latency), then the MFMAs on

@@ -538,11 +538,24 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         up.queue = reinterpret_cast<int*>(ws + plan.queues);
         const size_t up_lds = (size_t)up_lds_bytes(m.M);
         const int grid = (cus / kXcds) * kXcds;
+        const bool pad = m.d / 64 < 4;   // tiles padded to 4 stages
         switch (m.M / 64) {
-            case 1: s = launch_persistent(up_kernel<1>, grid, up_lds, st, up); break;
-            case 2: s = launch_persistent(up_kernel<2>, grid, up_lds, st, up); break;
-            case 3: s = launch_persistent(up_kernel<3>, grid, up_lds, st, up); break;
-            case 4: s = launch_persistent(up_kernel<4>, grid, up_lds, st, up); break;
+            case 1:
+                s = pad ? launch_persistent(up_kernel<1, true>, grid, up_lds, st, up)
+                        : launch_persistent(up_kernel<1, false>, grid, up_lds, st, up);
+                break;
+            case 2:
+                s = pad ? launch_persistent(up_kernel<2, true>, grid, up_lds, st, up)
+                        : launch_persistent(up_kernel<2, false>, grid, up_lds, st, up);
+                break;
+            case 3:
+                s = pad ? launch_persistent(up_kernel<3, true>, grid, up_lds, st, up)
+                        : launch_persistent(up_kernel<3, false>, grid, up_lds, st, up);
+                break;
+            case 4:
+                s = pad ? launch_persistent(up_kernel<4, true>, grid, up_lds, st, up)
+                        : launch_persistent(up_kernel<4, false>, grid, up_lds, st, up);
+                break;
             default: return UNIF_EUNSUPPORTED;
         }
         if (s != UNIF_OK) return s;
