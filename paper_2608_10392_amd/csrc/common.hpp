@@ -134,20 +134,39 @@ __device__ __forceinline__ int upper_index(const int* off, int n, int x) {
     return lo;
 }
 
-// Asynchronous 16-byte copy global -> LDS (gfx950 global_load_lds_dwordx4):
-// lane l of the wave writes its 16 bytes at lds_base + 16 l, where lds_base
-// is the same for the whole wave. Completion is tracked by vmcnt only.
-// (Measured on gfx950 interleaved with MFMAs, this form sustains more copy
-// bandwidth at less MFMA cost than the buffer-load form of the same copy.)
+// Asynchronous copies global -> LDS (gfx950 global_load_lds_dword[x4]): lane
+// l of the wave writes its 4 or 16 bytes at lds_base + 4 l or + 16 l, where
+// lds_base (in M0) is the same for the whole wave. Completion is tracked by
+// vmcnt only. (Measured on gfx950 interleaved with MFMAs, this form sustains
+// more copy bandwidth at less MFMA cost than the buffer-load form of the same
+// copy.)
+// They are issued as inline assembly, so the compiler does not model them:
+// a compiler-visible LDS copy makes it wait for every LDS read in flight
+// (lgkmcnt(0)) wherever a fragment read is consumed, which defeats reading
+// the next k step's fragments ahead. Every consumer of the copied data
+// therefore waits explicitly (wait_vmcnt, then a barrier); the compiler's
+// own vmcnt waits for its loads can only over-count the copies. M0 is set
+// by each copy and used by nothing else in these kernels.
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+// (M0 is a reserved register: clang warns that clobbering it is not
+// tracked; the kernels keep no value in M0 across a copy.)
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(const void* gsrc, void* lds_base) {
-    __builtin_amdgcn_global_load_lds(gsrc, lds_base, 16, 0, 0);
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(gsrc), "s"(lds_offset(lds_base))
+                 : "memory", "m0");
 }
-
-// Same with 4 bytes per lane (lane l writes lds_base + 4 l); only 4-byte
-// alignment is needed.
 __device__ __forceinline__ void dma4(const void* gsrc, void* lds_base) {
-    __builtin_amdgcn_global_load_lds(gsrc, lds_base, 4, 0, 0);
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+                 :
+                 : "v"(gsrc), "s"(lds_offset(lds_base))
+                 : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
 // Wait until at most N vector-memory operations of this wave are pending.
 template <int N>

@@ -233,9 +233,9 @@ void up_kernel(UpParams p) {
 
     // A tile's token and pair lists (TM ints each): each wave copies 256
     // bytes, so that every wave issues the same number of operations.
-    auto fetch_rows = [&](int t, int par) {
+    auto fetch_rows = [&](int first, int par) {
         const int which = wave >> 2, part = wave & 3;
-        const int* src = (which == 0 ? p.slab_tok : p.slab_rows) + ld_uniform(p.tile_rows + t) + part * 64 + lane;
+        const int* src = (which == 0 ? p.slab_tok : p.slab_rows) + first + part * 64 + lane;
         dma4(src, rows + (par * 2 + which) * TM + part * 64);
     };
     auto sources = [&](int par, int inf) {
@@ -273,7 +273,7 @@ void up_kernel(UpParams p) {
 
     int par = 0;
     int info = ld_uniform(p.tile_info + tile);
-    fetch_rows(tile, 0);
+    fetch_rows(ld_uniform(p.tile_rows + tile), 0);
     wait_vmcnt<0>();
     __syncthreads();
     sources(0, info);
@@ -292,6 +292,11 @@ void up_kernel(UpParams p) {
     for (;;) {
         const bool has_next = next < tq.hi;
         const int next_info = has_next ? ld_uniform(p.tile_info + next) : 0;
+        const int next_rows = has_next ? ld_uniform(p.tile_rows + next) : 0;
+        // No scalar load may be in flight in the stage loop: the compiler
+        // can then wait for the fragment reads of one k step only (lgkmcnt
+        // also counts scalar loads, which complete out of order).
+        wait_lgkmcnt0();
 #pragma unroll
         for (int i = 0; i < RG; ++i)
 #pragma unroll
@@ -345,7 +350,7 @@ void up_kernel(UpParams p) {
             }
             kstep(3, fxb, fwb, fxa, fwa);
             issue_end();
-            if (s == 0 && has_next) fetch_rows(next, par ^ 1);
+            if (s == 0 && has_next) fetch_rows(next_rows, par ^ 1);
             slot = other;
         }
         // GELU, round to bf16; lane stores 16 consecutive columns of its row
@@ -573,6 +578,8 @@ void down_kernel(DownParams p) {
         const bool has_next = next < tq.hi;
         Desc nxt;
         if (has_next) nxt = describe(next);
+        // No scalar load may be in flight in the stage loop (see up_kernel).
+        wait_lgkmcnt0();
 #pragma unroll
         for (int i = 0; i < RG; ++i)
 #pragma unroll
