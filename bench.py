@@ -64,7 +64,9 @@ def library_source_hash():
     """SHA-256 over the library's kernel sources and build flags."""
     import hashlib
     base = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_10392_amd")
-    files = sorted(os.path.join("paper_2608_10392_amd", "csrc", f) for f in os.listdir(os.path.join(base, "csrc")))
+    csrc = os.path.join(base, "csrc")
+    files = sorted(os.path.join("paper_2608_10392_amd", "csrc", f) for f in os.listdir(csrc)
+                   if os.path.isfile(os.path.join(csrc, f)) and f.endswith((".hip", ".hpp", ".h", ".py")))
     files.append(os.path.join("paper_2608_10392_amd", "build.py"))
     h = hashlib.sha256()
     root = os.path.dirname(base)

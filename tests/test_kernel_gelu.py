@@ -46,9 +46,12 @@ def gelu_kernel(x, c, ymax):
 
 def test_header_matches_fit_script():
     sys.path.insert(0, CSRC)
+    dont_write = sys.dont_write_bytecode
+    sys.dont_write_bytecode = True   # no cache files beside the kernel sources
     try:
         import gelu_coeffs
     finally:
+        sys.dont_write_bytecode = dont_write
         sys.path.pop(0)
     c, ymax = header_coefficients()
     assert ymax == gelu_coeffs.Y
