@@ -33,16 +33,20 @@ __global__ void combine_bf16_kernel(CombineParams c) {
     const float* wt = c.wts + (size_t)t * c.K;
     // Rows in batches of kCombineBatch: the weights and pair indices of a
     // batch, then its rows, are loaded before any is used (the latencies
-    // overlap); the sum still runs in the fixed order.
-    for (int i0 = 0; i0 <= k && k > 0; i0 += kCombineBatch) {
+    // overlap); the sum still runs in the fixed order. The first batch's
+    // weights and indices do not wait for k: entries up to K are always
+    // readable, and those past k are not used.
+    for (int i0 = 0; i0 == 0 || (i0 <= k && k > 0); i0 += kCombineBatch) {
         float w[kCombineBatch];
         int pr[kCombineBatch];
 #pragma unroll
         for (int u = 0; u < kCombineBatch; ++u) {
             const int i = i0 + u;
-            w[u] = (i > k) ? 0.f : (i == 0 ? c.alpha[t] : wt[i - 1]);
-            pr[u] = (i > k) ? 0 : of[i];
+            const bool in = (i0 == 0) ? i <= c.K : i <= k;
+            w[u] = in ? (i == 0 ? c.alpha[t] : wt[i - 1]) : 0.f;
+            pr[u] = in ? of[i] : 0;
         }
+        if (k == 0) break;
         u32x4 v[kCombineBatch];
 #pragma unroll
         for (int u = 0; u < kCombineBatch; ++u)

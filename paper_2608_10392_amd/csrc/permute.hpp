@@ -242,17 +242,35 @@ __global__ void scatter_kernel(PermuteParams p) {
     int* of = p.pair_of + (size_t)t * K1;
     const int* eid = p.eids + (size_t)t * p.K;
     const int pr = p.bin_cursor[ks] + of[0];
-    p.pair_token[pr] = t;
-    p.pair_mask[pr] = m;
-    p.pair_expert[pr] = 0;
-    of[0] = pr;
-    for (int i = 0; i < k; ++i) {
-        const int e = eid[i];
-        const int q = p.bin_cursor[(e << kb) + kr] + of[1 + i];
-        p.pair_token[q] = t;
-        p.pair_mask[q] = rm;
-        p.pair_expert[q] = e;
-        of[1 + i] = q;
+    // Residual pairs in batches: every load of a batch (experts, slots, bin
+    // cursors) is issued before its stores, which the compiler may not move
+    // loads across.
+    constexpr int kBatch = 8;
+    for (int i0 = 0; i0 < k; i0 += kBatch) {
+        int e[kBatch], q[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            e[u] = (i0 + u < k) ? eid[i0 + u] : 0;
+            q[u] = (i0 + u < k) ? of[1 + i0 + u] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+            if (i0 + u < k) q[u] += p.bin_cursor[(e[u] << kb) + kr];
+        if (i0 == 0) {
+            p.pair_token[pr] = t;
+            p.pair_mask[pr] = m;
+            p.pair_expert[pr] = 0;
+            of[0] = pr;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (i0 + u < k) {
+                p.pair_token[q[u]] = t;
+                p.pair_mask[q[u]] = rm;
+                p.pair_expert[q[u]] = e[u];
+                of[1 + i0 + u] = q[u];
+            }
+        }
     }
 }
 
@@ -397,16 +415,18 @@ __global__ __launch_bounds__(256) void chunk_scan_kernel(PermuteParams p) {
         lds);
 }
 
-__device__ __forceinline__ void slabfill_chunk(const PermuteParams& p, int q, int (*wc)[64]) {
+// first[c]: the chunk's first row in slab c, staged in LDS so that the
+// store loop below carries no global loads.
+__device__ __forceinline__ void slabfill_chunk(const PermuteParams& p, int q, int (*wc)[64], int* first) {
     const ChunkView v = chunk_view(p, q);
     const int pr = v.lo + (int)threadIdx.x;
     const bool act = pr < v.hi;
     const uint64_t m = act ? p.pair_mask[pr] : 0ull;
     const int tok = act ? p.pair_token[pr] : 0;
+    if ((int)threadIdx.x < p.B) first[threadIdx.x] = p.chunk_cnt[(size_t)q * p.B + threadIdx.x];
     chunk_wave_counts(p.B, m, wc);
     __syncthreads();
     const int w = threadIdx.x >> 6;
-    const int* first = p.chunk_cnt + (size_t)q * p.B;
     for (int c = 0; c < p.B; ++c) {
         const bool use = ((m >> c) & 1ull) != 0ull;
         const uint64_t bits = ballot(use);
@@ -423,6 +443,7 @@ __device__ __forceinline__ void slabfill_chunk(const PermuteParams& p, int q, in
 // group) each; the rest fill the chunks' slab rows.
 __global__ __launch_bounds__(kChunk) void slabfill_kernel(PermuteParams p, int n_groups) {
     __shared__ int wc[kChunk / 64][64];
+    __shared__ int first[64];
     const int b = blockIdx.x;
     if (b < n_groups) {
         up_tiles_of_group(p, b, &wc[0][0]);
@@ -430,7 +451,7 @@ __global__ __launch_bounds__(kChunk) void slabfill_kernel(PermuteParams p, int n
     }
     const int nq = p.totals[3];
     for (int q = b - n_groups; q < nq; q += gridDim.x - n_groups) {
-        slabfill_chunk(p, q, wc);
+        slabfill_chunk(p, q, wc, first);
         __syncthreads();
     }
 }
