@@ -1,4 +1,4 @@
-"""The five synthetic layer workloads and their generator recipes.
+"""The synthetic layer workloads and their generator recipes.
 
 Shapes follow the backbones the paper evaluates (Sec. IV-A and App. A-B):
 DeiT/ViT patch tokens (197 per image) and BERT sequences of at most 128
@@ -54,6 +54,21 @@ CONFIGS = {
         index=5, seed=4, n_tokens=131072, d_model=1024, n_experts=32,
         n_blocks=32, block_width=128, dtype="bf16", mass_threshold=0.8,
         tokens="bimodal", router="zipf_bimodal"),
+    # The paper's own operating points (Sec. IV-A and the architecture
+    # details of the appendix), with the cumulative target exactly Eq. beta
+    # (t = 1). Vision: DeiT-S/16 (d=384, H=1536) with K=6 residual experts
+    # and B=8 blocks, evaluation batch 64 x 197 tokens. Language: BERT-large
+    # (d=1024, H=4096) with K=16, B=16, evaluation batch 32 x 128 slots with
+    # dynamic padding (valid lengths U{16..128}).
+    "paper_vision": dict(
+        index=6, seed=5, n_tokens=64 * 197, d_model=384, n_experts=6,
+        n_blocks=8, block_width=192, dtype="bf16", mass_threshold=1.0,
+        tokens="normal_ln", router="default"),
+    "paper_language": dict(
+        index=7, seed=6, n_tokens=32 * 128, d_model=1024, n_experts=16,
+        n_blocks=16, block_width=256, dtype="bf16", mass_threshold=1.0,
+        tokens="normal_ln", padding=dict(n_seq=32, seq_len=128, lo=16, hi=128),
+        router="default"),
 }
 
 for _c in CONFIGS.values():

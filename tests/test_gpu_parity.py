@@ -159,7 +159,7 @@ def test_stats_match_oracle():
 
 
 FULL_SAMPLE = {"tiny_f32": None, "vit_s16": 2048, "bert_base_padded": 2048, "vit_b16": 2048,
-               "zipf_stress": 1024}
+               "zipf_stress": 1024, "paper_vision": 2048, "paper_language": 1024}
 
 
 def test_nonfinite_tokens_keep_routing_in_range():

@@ -1,4 +1,4 @@
-"""Invariants of the oracle's routing on the five synthetic workloads (first
+"""Invariants of the oracle's routing on the synthetic workloads (first
 4096 token rows each) and of the generator itself. CPU only."""
 import numpy as np
 import pytest
@@ -53,7 +53,9 @@ def test_expected_routing_statistics(routed):
     st = O.stats(g["cfg"], rec)
     name = g["cfg"]["name"]
     expect = {"tiny_f32": (1.5, 0.3), "vit_s16": (2.1, 0.2), "bert_base_padded": (2.0, 0.15),
-              "vit_b16": (3.35, 0.2), "zipf_stress": (9.0, 0.6)}[name]
+              "vit_b16": (3.35, 0.2), "zipf_stress": (9.0, 0.6)}.get(name)
+    if expect is None:
+        pytest.skip(f"{name}: the recipe aims at no particular expert count (paper settings, t = 1)")
     assert abs(st["mean_k"] - expect[0]) < expect[1], st["mean_k"]
     if name == "zipf_stress":
         # bimodal shared demand: b is 1 or B-1 for almost every token
