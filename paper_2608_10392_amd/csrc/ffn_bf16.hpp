@@ -110,7 +110,7 @@ __device__ __forceinline__ int wcol(int r) { return 16 * ((r >> 2) & 1) + 4 * (r
 // Dynamic LDS bytes of the two kernels: two stage slots, plus the row lists
 // of the current and the next tile (up: tokens and pairs; down: block masks).
 // The last 16 bytes pass tile indices between waves.
-__host__ __device__ constexpr int up_lds_bytes(int M) { return 2 * (kFfnTM + M) * Stage::RB + 16 * kFfnTM + 16; }
+__host__ __device__ constexpr int up_lds_bytes(int M, int TM) { return 2 * (TM + M) * Stage::RB + 16 * TM + 16; }
 __host__ __device__ constexpr int down_lds_bytes(int TM, int BN) { return 2 * (TM + BN) * Stage::RB + 16 * TM + 16; }
 
 // Per-XCD tile queue: XCD x (= blockIdx.x % 8) owns tiles [lo, hi) of the
@@ -165,22 +165,25 @@ __device__ __forceinline__ void wait_stage(int s, bool after_epi, bool has_next)
 //    with stages that re-read k = 0.. and run no MFMAs (the row-list copy of
 //    stage 0 is waited for at the barrier of stage 2). PAD: whether d < 256
 //    (else no stage is padding and the MFMAs need no per-stage test).
-template <int MG, bool PAD>
+template <int MG, bool PAD, int TM>
 __global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void up_kernel(UpParams p) {
     using S = Stage;
-    constexpr int RB = S::RB, KS = S::KSTEPS, TM = kFfnTM, NWV = kFfnWaves;
+    constexpr int RB = S::RB, KS = S::KSTEPS, NWV = kFfnWaves;
     constexpr int M = MG * 64;                        // MG 32-column groups per wave
-    constexpr int RG = 2;                             // 32-row groups per wave
+    constexpr int RG = TM / 128;                      // 32-row groups per wave (4 row waves)
+    static_assert(TM == 256 || TM == 384, "tile heights with whole row-list copies");
     constexpr int LA = TM / S::ROWS_PER_DMA / NWV;    // token-row copies per wave per stage
     constexpr int LB = M / S::ROWS_PER_DMA / NWV;     // weight-row copies per wave per stage
     constexpr int L = LA + LB;
     constexpr int NEPI = RG * MG * 2;                 // epilogue stores per wave
     constexpr int A_BYTES = TM * RB, STAGE = (TM + M) * RB, RING = 2 * STAGE;
-    constexpr int NFETCH = 1;                         // copies per wave for a tile's row lists
+    // 4-byte copies per wave for a tile's row lists (2 TM ints): one of 64
+    // ints per wave, and for TM = 384 one more of 32.
+    constexpr int NFETCH = (2 * TM > NWV * 64) ? 2 : 1;
     constexpr int NR = RG + MG;                       // fragment reads per k step
     static_assert(LA >= 1 && LB >= 1, "tile too small for one copy per wave");
-    static_assert(2 * TM * 4 == NWV * 64 * 4, "row lists: one 4-byte copy per wave");
+    static_assert(2 * TM == NWV * 64 || 2 * TM == NWV * 96, "row lists: one or one and a half copies per wave");
     static_assert(NEPI + NFETCH + L < 64, "vmcnt range");
     extern __shared__ __attribute__((aligned(16))) char lds_up[];
     // rows[par][0] tokens, rows[par][1] pairs of the tile with parity par
@@ -213,7 +216,7 @@ void up_kernel(UpParams p) {
     uint32_t fx[KS], fw[KS];
 #pragma unroll
     for (int k = 0; k < KS; ++k) {
-        fx[k] = S::off(wm * 64 + lr, 2 * k + lh);
+        fx[k] = S::off(wm * (TM / 4) + lr, 2 * k + lh);
         fw[k] = A_BYTES + S::off(wn * (M / 2) + lr, 2 * k + lh);
     }
     // Copy sources: per-lane addresses fixed for a tile, plus the k position
@@ -231,12 +234,18 @@ void up_kernel(UpParams p) {
     const char* srcA[LA];   // token rows of the tile being issued
     const char* wslab = wup;
 
-    // A tile's token and pair lists (TM ints each): each wave copies 256
-    // bytes, so that every wave issues the same number of operations.
+    // A tile's token and pair lists (TM ints each, stored back to back):
+    // wave w copies ints 64 w .. 64 w + 63 of the two lists, and for TM = 384
+    // also ints 512 + 32 w .. (pairs 128 + 32 w ..), so that every wave issues
+    // the same number of operations.
     auto fetch_rows = [&](int first, int par) {
-        const int which = wave >> 2, part = wave & 3;
-        const int* src = (which == 0 ? p.slab_tok : p.slab_rows) + first + part * 64 + lane;
-        dma4(src, rows + (par * 2 + which) * TM + part * 64);
+        int* dst = rows + par * 2 * TM;
+        const int i0 = wave * 64;   // the list boundary TM is a multiple of 64
+        dma4((i0 < TM ? p.slab_tok + first + i0 : p.slab_rows + first + (i0 - TM)) + lane, dst + i0);
+        if constexpr (NFETCH == 2) {
+            const int i1 = NWV * 64 + wave * 32;
+            if (lane < 32) dma4(p.slab_rows + first + (i1 - TM) + lane, dst + i1);
+        }
     };
     auto sources = [&](int par, int inf) {
         const int sl = inf & 0xffff, nrows = inf >> 16;
@@ -359,7 +368,7 @@ void up_kernel(UpParams p) {
         const int c = sl - (sl / p.B) * p.B;
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
-            const int r = wm * 64 + i * 32 + lr;
+            const int r = wm * (TM / 4) + i * 32 + lr;
             u16* dst = (r < nrows) ? p.Hbuf + (size_t)rows[(par * 2 + 1) * TM + r] * p.H + (size_t)c * M : p.Hsink;
             dst += wn * (M / 2) + 16 * lh;
 #pragma unroll

@@ -40,7 +40,10 @@ constexpr size_t kLdsLimit = 160 * 1024;
 // Expert-GEMM tile shapes, one workgroup of 8 waves per CU. Up: 256
 // gathered rows x the whole block width M. Down: 256 pairs x 256 output
 // columns (128 when d is not a multiple of 256).
-constexpr int kUpTM = kFfnTM;
+// Up tiles are 384 rows when the block is at most 192 wide and no stage is
+// padding (d >= 256): their accumulators and fragments then still fit two
+// waves per SIMD without spills. Else 256.
+int up_tm(int M, int d) { return (M <= 192 && d >= 256) ? 384 : 256; }
 // Up tiles are ordered by expert, then by groups of blocks, then by the
 // stretch of the expert's pairs they cover: the tiles that run together on
 // one XCD share token rows (across the group's blocks) and weight slabs
@@ -62,7 +65,7 @@ DownShape down_shape(int d) {
     if (d % 384 == 0) return {128, 384};
     return {256, 128};
 }
-static_assert(up_lds_bytes(256) <= 160 * 1024, "up stages exceed LDS");
+static_assert(up_lds_bytes(192, 384) <= 160 * 1024 && up_lds_bytes(256, 256) <= 160 * 1024, "up stages exceed LDS");
 static_assert(down_lds_bytes(128, 384) <= 160 * 1024 && down_lds_bytes(256, 256) <= 160 * 1024,
               "down stages exceed LDS");
 
@@ -212,7 +215,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.pair_of = cv.take(4 * N * K1);
     // Slab row lists: at most K B rows per token (b + k (B - b) <= K B), each
     // slab padded to whole up tiles.
-    const size_t tm = (size_t)kUpTM;
+    const size_t tm = (size_t)up_tm(m.M, m.d);
     const size_t up_tiles = ceil_div_sz(N * K * (size_t)m.B, tm) + (size_t)m.nslab;
     p.slab_rows = cv.take(m.bf16 ? 4 * up_tiles * tm : 0);
     p.slab_tok = cv.take(m.bf16 ? 4 * up_tiles * tm : 0);
@@ -471,7 +474,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.B = m.B;
     pp.key_bits = m.key_bits;
     const DownShape dsh = down_shape(m.d);
-    pp.bm_up = kUpTM;
+    pp.bm_up = up_tm(m.M, m.d);
     pp.up_group = up_block_group(m.d, m.M, m.B);
     pp.bm_down = dsh.tm;
     pp.down_col_tiles = m.bf16 ? m.d / dsh.bn : 1;
@@ -536,25 +539,25 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         up.tile_rows = pp.up_tile_rows;
         up.totals = totals;
         up.queue = reinterpret_cast<int*>(ws + plan.queues);
-        const size_t up_lds = (size_t)up_lds_bytes(m.M);
+        const size_t up_lds = (size_t)up_lds_bytes(m.M, up_tm(m.M, m.d));
         const int grid = (cus / kXcds) * kXcds;
         const bool pad = m.d / 64 < 4;   // tiles padded to 4 stages
         switch (m.M / 64) {
             case 1:
-                s = pad ? launch_persistent(up_kernel<1, true>, grid, up_lds, st, up)
-                        : launch_persistent(up_kernel<1, false>, grid, up_lds, st, up);
+                s = pad ? launch_persistent(up_kernel<1, true, 256>, grid, up_lds, st, up)
+                        : launch_persistent(up_kernel<1, false, 384>, grid, up_lds, st, up);
                 break;
             case 2:
-                s = pad ? launch_persistent(up_kernel<2, true>, grid, up_lds, st, up)
-                        : launch_persistent(up_kernel<2, false>, grid, up_lds, st, up);
+                s = pad ? launch_persistent(up_kernel<2, true, 256>, grid, up_lds, st, up)
+                        : launch_persistent(up_kernel<2, false, 384>, grid, up_lds, st, up);
                 break;
             case 3:
-                s = pad ? launch_persistent(up_kernel<3, true>, grid, up_lds, st, up)
-                        : launch_persistent(up_kernel<3, false>, grid, up_lds, st, up);
+                s = pad ? launch_persistent(up_kernel<3, true, 256>, grid, up_lds, st, up)
+                        : launch_persistent(up_kernel<3, false, 384>, grid, up_lds, st, up);
                 break;
             case 4:
-                s = pad ? launch_persistent(up_kernel<4, true>, grid, up_lds, st, up)
-                        : launch_persistent(up_kernel<4, false>, grid, up_lds, st, up);
+                s = pad ? launch_persistent(up_kernel<4, true, 256>, grid, up_lds, st, up)
+                        : launch_persistent(up_kernel<4, false, 256>, grid, up_lds, st, up);
                 break;
             default: return UNIF_EUNSUPPORTED;
         }
