@@ -248,10 +248,10 @@ constexpr int kRankBatch = 8;   // residual-pair atomics in flight per token
 // Rankings of at most this many entries run on registers.
 constexpr int kSmallRank = 16;
 
-// Decisions for token tok0 + threadIdx.x (threads 0..127, i.e. waves 0, 1).
+// Decisions for token tok0 + tid, one token per lane of whole waves (the
+// counting below merges the lanes of a wave).
 __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, float* PS, int* QS, uint32_t* KEYS,
-                                             int* slab_lds, int tok0) {
-    const int tid = threadIdx.x;
+                                             int* slab_lds, int tok0, int tid) {
     const int K = p.K, B = p.B, tok = tok0 + tid;
     const bool in_range = tok < p.N;
     const bool v = in_range && (p.valid == nullptr || p.valid[tok] != 0);
@@ -500,7 +500,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteParams p) {
     if constexpr (NCT > 0) route_logits_bf16<NCT>(p, L, tok0);
     else route_logits_f32(p, L, tok0);
     __syncthreads();
-    if (threadIdx.x < kRouteTok) route_decide(p, L, PS, QS, KEYS, slab_lds, tok0);
+    if (threadIdx.x < kRouteTok) route_decide(p, L, PS, QS, KEYS, slab_lds, tok0, threadIdx.x);
     __syncthreads();
     // Sorted expert ids and weights of the workgroup's tokens: one contiguous
     // range of each output, written from LDS with consecutive addresses.
@@ -518,6 +518,156 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteParams p) {
     if (p.slab_count) {
         int* dst = p.slab_count + (size_t)(blockIdx.x % kSlabCopies) * ncnt;
         for (int i = threadIdx.x; i < ncnt; i += blockDim.x)
+            if (slab_lds[i]) atomicAdd(&dst[i], slab_lds[i]);
+    }
+}
+
+// Persistent routing for bf16 tokens when the router fits in registers
+// (1 + K + B <= 32 columns, d <= 768, K, B <= 16). One workgroup of 8 waves
+// takes the 64-token tiles blockIdx.x, blockIdx.x + gridDim.x, ... (at most
+// kRpMaxTiles). Wave w owns k steps [w nks / 8, (w + 1) nks / 8) of the
+// logits and keeps the router's three bf16 parts and W_shr for them in
+// registers for all its tiles, so only token rows stream from memory; each
+// tile's partial logits go to LDS and are summed over the 8 k slices in a
+// fixed order. Then wave i takes the decisions of tile i (one token per lane),
+// the tiles' decisions running side by side.
+constexpr int kRpTok = 64;
+constexpr int kRpWaves = 8;
+constexpr int kRpThreads = kRpWaves * 64;
+constexpr int kRpMaxTiles = 4;
+
+template <int NCT, int KPW>
+__global__ __launch_bounds__(kRpThreads) void route_persist_kernel(RouteParams p) {
+    constexpr int RT = kRpTok / 16;          // 16-row fragments per tile
+    extern __shared__ float lds_route[];
+    const int K = p.K, ls = p.lstride;
+    const int ncols = 1 + 16 * NCT;
+    float* Lb = lds_route;                                       // [kRpMaxTiles][64][ls]
+    float* U = Lb + kRpMaxTiles * kRpTok * ls;                   // union: partials, then PS/QS
+    float* Pbuf = U;                                             // [8][64][ls]
+    float* PS = U;                                               // [kRpMaxTiles][64][K+1]
+    int* QS = reinterpret_cast<int*>(PS + kRpMaxTiles * kRpTok * (K + 1));
+    const int ufloats = max(kRpWaves * kRpTok * ls, 2 * kRpMaxTiles * kRpTok * (K + 1));
+    int* slab_lds = reinterpret_cast<int*>(U + ufloats);
+    const int nslab = (K + 1) * p.B, ncnt = nslab + K + 1;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int ntile_all = (p.N + kRpTok - 1) / kRpTok;
+    const int nt = min(kRpMaxTiles, (ntile_all - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x);
+    if (p.slab_count)
+        for (int i = tid; i < ncnt; i += blockDim.x) slab_lds[i] = 0;
+
+    // This wave's k steps (32 deep) and the router parts for them.
+    const int nks = p.d / 32;
+    const int kb = wave * nks / kRpWaves, kn = (wave + 1) * nks / kRpWaves - kb;   // kn <= KPW
+    const int kof = (lane >> 4) * 8;
+    const u16* wb = p.Wsplit + (size_t)(lane & 15) * p.d + kof;
+    const size_t part_stride = (size_t)p.NLP * p.d, ct_stride = (size_t)16 * p.d;
+    u32x4 W[KPW][3][NCT], S0[KPW], S1[KPW];
+#pragma unroll
+    for (int j = 0; j < KPW; ++j) {
+        const int k0 = (kb + (j < kn ? j : 0)) * 32;
+#pragma unroll
+        for (int part = 0; part < 3; ++part)
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) W[j][part][ct] = ld16(wb + part * part_stride + ct * ct_stride + k0);
+        S0[j] = ld16(p.Wr + kof + k0);
+        S1[j] = ld16(p.Wr + kof + k0 + 4);
+    }
+    const u16* X = static_cast<const u16*>(p.X);
+    u32x4 xa[KPW][RT];
+    auto load_x = [&](int i) {
+        const int tok0 = ((int)blockIdx.x + i * (int)gridDim.x) * kRpTok;
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            // Rows past N read row N - 1; their logits are never used.
+            const u16* xr = X + (size_t)min(tok0 + r * 16 + (lane & 15), p.N - 1) * p.d + kof;
+#pragma unroll
+            for (int j = 0; j < KPW; ++j) xa[j][r] = ld16(xr + (kb + (j < kn ? j : 0)) * 32);
+        }
+    };
+    if (nt > 0) load_x(0);
+    for (int i = 0; i < nt; ++i) {
+        f32x4 acc[RT][NCT];
+        float sh[RT];
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            sh[r] = 0.f;
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) acc[r][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int j = 0; j < KPW; ++j) {
+            if (j < kn) {
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                    for (int part = 0; part < 3; ++part)
+#pragma unroll
+                        for (int r = 0; r < RT; ++r)
+                            acc[r][ct] = mfma16x16x32(as_bf16x8(xa[j][r]), as_bf16x8(W[j][part][ct]), acc[r][ct]);
+#pragma unroll
+                for (int r = 0; r < RT; ++r)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const uint32_t u = xa[j][r][q];
+                        sh[r] = fmaf(__uint_as_float(u << 16), __uint_as_float(q < 2 ? S0[j][2 * q] : S1[j][2 * q - 4]), sh[r]);
+                        sh[r] = fmaf(__uint_as_float(u & 0xffff0000u),
+                                     __uint_as_float(q < 2 ? S0[j][2 * q + 1] : S1[j][2 * q - 3]), sh[r]);
+                    }
+            }
+        }
+        // The next tile's rows are in flight during the reduction.
+        if (i + 1 < nt) load_x(i + 1);
+        // This wave's partial logits: column 0 the shared demand, columns
+        // 1.. the MFMA tiles.
+        float* P = Pbuf + wave * kRpTok * ls;
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            float v = sh[r];
+            v += __shfl_xor(v, 16);
+            v += __shfl_xor(v, 32);
+            if (lane < 16) P[(r * 16 + lane) * ls] = v;
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    P[(r * 16 + (lane >> 4) * 4 + e) * ls + 1 + ct * 16 + (lane & 15)] = acc[r][ct][e];
+        }
+        lds_barrier();
+        // Sum of the 8 k slices, in wave order.
+        float* L = Lb + i * kRpTok * ls;
+        for (int e = tid; e < kRpTok * ncols; e += blockDim.x) {
+            const int t = e / ncols, c = e - t * ncols;
+            float v = 0.f;
+#pragma unroll
+            for (int w = 0; w < kRpWaves; ++w) v += Pbuf[(w * kRpTok + t) * ls + c];
+            L[t * ls + c] = v;
+        }
+        lds_barrier();
+    }
+    // Decisions: wave i takes tile i (the partial buffer is reused as PS/QS).
+    if (wave < nt) {
+        const int tok0 = ((int)blockIdx.x + wave * (int)gridDim.x) * kRpTok;
+        route_decide(p, Lb + wave * kRpTok * ls, PS + wave * kRpTok * (K + 1), QS + wave * kRpTok * (K + 1),
+                     nullptr, slab_lds, tok0, lane);
+    }
+    __syncthreads();
+    for (int i = 0; i < nt; ++i) {
+        const int tok0 = ((int)blockIdx.x + i * (int)gridDim.x) * kRpTok;
+        const int ntok = min(kRpTok, p.N - tok0);
+        const size_t base = (size_t)tok0 * K;
+        const float* ps = PS + i * kRpTok * (K + 1);
+        const int* qs = QS + i * kRpTok * (K + 1);
+        for (int e = tid; e < ntok * K; e += blockDim.x) {
+            const int t = e / K, r = e - t * K;
+            p.eids[base + e] = qs[t * (K + 1) + r];
+            p.wts[base + e] = ps[t * (K + 1) + r];
+        }
+    }
+    if (p.slab_count) {
+        int* dst = p.slab_count + (size_t)(blockIdx.x % kSlabCopies) * ncnt;
+        for (int i = tid; i < ncnt; i += blockDim.x)
             if (slab_lds[i]) atomicAdd(&dst[i], slab_lds[i]);
     }
 }

@@ -326,6 +326,36 @@ int32_t launch_route(const Dims& m, const RouteParams& rp, const float* Wr, cons
                                                            zwords);
         UNIF_LAUNCH_CHECK();
     }
+    // Persistent routing with the router in registers where it fits.
+    const int nct = m.NLP / 16, kpw = ceil_div(m.d / 32, kRpWaves);
+    if (m.bf16 && nct <= 2 && kpw <= 3 && m.K <= kSmallRank && m.B <= kSmallRank) {
+        const size_t ls = (size_t)m.lstride, K1 = (size_t)m.K1;
+        const size_t lds = sizeof(float) * (kRpMaxTiles * kRpTok * ls +
+                                            std::max(kRpWaves * kRpTok * ls, 2 * kRpMaxTiles * kRpTok * K1) +
+                                            (size_t)m.nslab + K1);
+        if (lds <= kLdsLimit) {
+            void (*pk)(RouteParams) = nullptr;
+            switch (nct * 4 + kpw) {
+                case 5: pk = route_persist_kernel<1, 1>; break;
+                case 6: pk = route_persist_kernel<1, 2>; break;
+                case 7: pk = route_persist_kernel<1, 3>; break;
+                case 9: pk = route_persist_kernel<2, 1>; break;
+                case 10: pk = route_persist_kernel<2, 2>; break;
+                case 11: pk = route_persist_kernel<2, 3>; break;
+                default: break;
+            }
+            if (pk != nullptr) {
+                RouteParams rq = rp;
+                rq.key_stride = 0;   // rankings of <= 16 entries run on registers
+                const int ntiles = ceil_div(m.N, kRpTok);
+                const int grid = std::max(std::min(cu_count(), ntiles), ceil_div(ntiles, kRpMaxTiles));
+                if (allow_lds(pk, lds) != UNIF_OK) return UNIF_EDEVICE;
+                pk<<<grid, kRpThreads, lds, st>>>(rq);
+                UNIF_LAUNCH_CHECK();
+                return UNIF_OK;
+            }
+        }
+    }
     const size_t lds = route_lds_bytes(m);
     const int grid = ceil_div(m.N, kRouteTok);
     void (*kern)(RouteParams) = route_kernel<0>;
