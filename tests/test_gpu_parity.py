@@ -108,6 +108,17 @@ def test_all_padded_and_partly_padded():
     _free()
 
 
+def test_route_more_tiles_than_four_per_cu():
+    """70,000 tokens with a router that fits in registers: the persistent
+    routing kernel then runs more workgroups than CUs (at most four 64-token
+    tiles each), with a ragged last tile; every token's routing is checked."""
+    cfg = get_config("vit_s16", n_tokens=70_001, d_model=256, n_experts=8, n_blocks=8,
+                     block_width=64, max_shared=8)
+    g = generate(cfg)
+    run_case(g, "70001 tokens", n_sample=1024)
+    _free()
+
+
 def test_fp32_path_small_padded():
     cfg = get_config("tiny_f32", n_tokens=333, d_model=96, n_experts=5, n_blocks=3,
                      block_width=40, max_shared=3)
