@@ -424,28 +424,13 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
     const int ks = mask_key(mask, B, kb);
     const int kr = mask_key(rmask, B, kb);
     // The count of a bin taken before a pair adds itself is the pair's slot
-    // within the bin (pair_rank), so the scatter needs no atomics.
-    // Shared-expert pairs: every valid token has one, and block masks
-    // concentrate on few keys, so the lanes of a wave with the same key are
-    // grouped first; each group's first lane adds the group at once and the
-    // lanes take consecutive slots in lane order.
-    int leader = lane;
-    uint64_t grp = 0;
-    for (uint64_t pend = ballot(v); pend;) {
-        const int l0 = __builtin_ctzll(pend);
-        const int key = __shfl(ks, l0);
-        const uint64_t same = ballot(v && ks == key);
-        if (v && ks == key) {
-            leader = l0;
-            grp = same;
-        }
-        pend &= ~same;
-    }
-    int sbase = 0;
-    if (v && leader == lane) sbase = atomicAdd(&p.bin_count[ks], __popcll(grp));
+    // within the bin (pair_rank), so the scatter needs no atomics. The order
+    // of the slots inside a bin is whatever order the atomics land in; no
+    // result depends on it (every GEMM row is computed from its own pair).
+    // The shared pair's atomic and those of the first kRankBatch residual
+    // pairs are issued before any result is used, so their latencies overlap.
     int* rank = p.pair_rank + (size_t)(v ? tok : 0) * (K + 1);
-    // Residual pairs: the atomics of kRankBatch pairs are issued before any
-    // result is used, so their latencies overlap.
+    const int r0 = v ? atomicAdd(&p.bin_count[ks], 1) : 0;
     for (int i0 = 0; i0 < K; i0 += kRankBatch) {
         if (!ballot(v && i0 < k)) break;
         int r[kRankBatch];
@@ -456,27 +441,32 @@ __device__ __forceinline__ void route_decide(const RouteParams& p, float* L, flo
         for (int u = 0; u < kRankBatch; ++u)
             if (v && i0 + u < k) rank[1 + i0 + u] = r[u];
     }
-    sbase = __shfl(sbase, leader);
-    if (v) rank[0] = sbase + __popcll(grp & lanes_below());
-    // Pairs per expert, after the row counts in slab_lds.
+    if (v) rank[0] = r0;
+    // Pairs per expert and rows per (expert, block), after the row counts in
+    // slab_lds: lane c (< B) holds the ballot of the tokens whose shared
+    // blocks include c, so expert e's rows on block c (the shared expert on
+    // I_shr, a residual expert on I_res) are one popcount, and each expert
+    // needs one LDS add per block lane.
     int* ecnt = slab_lds + (K + 1) * B;
-    {
-        const uint64_t vb = ballot(v);
-        if (lane == 0 && vb) atomicAdd(&ecnt[0], __popcll(vb));
-    }
-    // Rows per (expert, block): shared expert on I_shr, residual experts on I_res.
+    uint64_t mb = 0;
     for (int c = 0; c < B; ++c) {
         const uint64_t bits = ballot(v && ((mask >> c) & 1ull));
-        if (lane == 0 && bits) atomicAdd(&slab_lds[c], __popcll(bits));
+        if (lane == c) mb = bits;
+    }
+    const uint64_t vb = ballot(v);
+    if (!vb) return;
+    if (lane == 0) atomicAdd(&ecnt[0], __popcll(vb));
+    if (lane < B) {
+        const int n = __popcll(mb);
+        if (n) atomicAdd(&slab_lds[lane], n);
     }
     for (int e = 1; e <= K; ++e) {
-        const bool has = v && ((sel >> (e - 1)) & 1ull);
-        const uint64_t hb = ballot(has);
+        const uint64_t hb = ballot(v && ((sel >> (e - 1)) & 1ull));
         if (!hb) continue;
         if (lane == 0) atomicAdd(&ecnt[e], __popcll(hb));
-        for (int c = 0; c < B; ++c) {
-            const uint64_t bits = ballot(has && !((mask >> c) & 1ull));
-            if (lane == 0 && bits) atomicAdd(&slab_lds[e * B + c], __popcll(bits));
+        if (lane < B) {
+            const int n = __popcll(hb & ~mb);
+            if (n) atomicAdd(&slab_lds[e * B + lane], n);
         }
     }
 }
