@@ -78,11 +78,12 @@ struct DownParams {
     const u16* Wdown;
     u16* part;                   // per-pair output rows, bf16
     u16* part_sink;              // one d row that absorbs the stores of unused tile rows
-    const int4* rt_info;         // per row tile: first pair, rows, expert
+    const int4* rt_info;         // per row tile: first pair, rows, expert, cost
     const uint64_t* rt_masks;    // per row tile: block-mask union of each 16-row group, then of the tile
     const uint64_t* pair_mask;   // readable for a whole tile past the last pair
     const int* tiles;            // per down tile: row tile << 8 | column tile
     const int* totals;           // [2]: down tiles
+    const int* slices;           // [9]: first tile of each XCD's slice, then the count
     int* queue;                  // 8 per-XCD tile counters, zero at launch
 };
 
@@ -124,6 +125,13 @@ struct TileQueue {
         ctr = queue + x;
         lo = (int)((int64_t)x * n_tiles / kXcds);
         hi = (int)((int64_t)(x + 1) * n_tiles / kXcds);
+    }
+    // Slices given by the table: XCD x owns [slices[x], slices[x + 1]).
+    __device__ TileQueue(int* queue, const int* slices) {
+        const int x = blockIdx.x % kXcds;
+        ctr = queue + x;
+        lo = ld_uniform(slices + x);
+        hi = ld_uniform(slices + x + 1);
     }
     // One lane only (a vector atomic with return); the result is an offset
     // from lo.
@@ -430,9 +438,8 @@ void down_kernel(DownParams p) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WN, wn = wave % WN;
-    const int n_tiles = ld_uniform(p.totals + 2);
     const int kcpb = p.M / S::SK;   // stages per block
-    const TileQueue tq(p.queue, n_tiles);
+    const TileQueue tq(p.queue, p.slices);
     // ctl as in the up kernel.
     int* ctl = reinterpret_cast<int*>(lds_dn + RING + 16 * TM);
     if (tid == 0) {

@@ -34,6 +34,7 @@ namespace unifmoe {
 
 constexpr int kScanThreads = 1024;
 constexpr int kChunk = 256;   // pairs per chunk of the ordered slab fill
+constexpr int kXcdSlices = 8; // the down tile table is split into one slice per XCD
 
 struct PermuteParams {
     int N, K, B, key_bits, bm_up, bm_down, down_col_tiles, up_group;
@@ -58,9 +59,10 @@ struct PermuteParams {
     int* up_tile_rows;  // per up tile: first entry in slab_rows / slab_tok
     int* chunk_off;     // [K+2] first chunk of each expert's pair segment
     int* chunk_cnt;     // [chunks][B] pairs per block, then (scanned) first slab row
-    int4* rt_info;      // per down row tile: first pair, rows, expert
+    int4* rt_info;      // per down row tile: first pair, rows, expert, cost (see down_rowtile)
     uint64_t* rt_masks; // per down row tile: mask union of each 16-row group, then of the tile
     int* down_tiles;    // per down tile: row tile << 8 | column tile
+    int* down_slices;   // [9]: first down tile of each XCD's slice of the table, then the count
 };
 
 __global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n) {
@@ -332,17 +334,24 @@ __device__ __forceinline__ void down_rowtile(const PermuteParams& p, int rt) {
     const int lane = threadIdx.x & 63, G = p.bm_down / 16;
     uint64_t* out = p.rt_masks + (size_t)rt * (G + 1);
     uint64_t all = 0;
+    int groups = 0;   // blocks summed over the 32-row MFMA groups (lanes 0 and 32)
     for (int h = 0; h * 64 < p.bm_down; ++h) {
         const int r = h * 64 + lane;
         uint64_t m = r < nrows ? p.pair_mask[p0 + r] : 0ull;
         for (int o = 1; o < 16; o <<= 1) m |= shfl_xor64(m, o);
         if ((lane & 15) == 0) out[h * 4 + (lane >> 4)] = m;
         all |= m;
+        const uint64_t m32 = m | shfl_xor64(m, 16);
+        if ((lane & 31) == 0) groups += __popcll(m32);
     }
     for (int o = 16; o < 64; o <<= 1) all |= shfl_xor64(all, o);
+    groups += __shfl_xor(groups, 32);
     if (lane == 0) {
         out[G] = all;
-        p.rt_info[rt] = make_int4(p0, nrows, e, 0);
+        // Cost estimate for balancing the XCD slices: the MFMA work (blocks
+        // over the 32-row groups) plus a per-stage share for the copies
+        // every stage of the tile's union makes.
+        p.rt_info[rt] = make_int4(p0, nrows, e, groups + 4 * __popcll(all));
     }
     for (int ct = lane; ct < p.down_col_tiles; ct += 64)
         p.down_tiles[(size_t)rt * p.down_col_tiles + ct] = (rt << 8) | ct;
@@ -401,10 +410,42 @@ __global__ __launch_bounds__(256) void tables_kernel(PermuteParams p, int g1) {
     }
 }
 
+// The down tile table is split into one contiguous slice per XCD with equal
+// estimated cost (rt_info[].w per tile of a row tile), not equal tile
+// counts: the shared expert's row tiles, listed first, are cheaper. Slice x
+// starts at the first tile whose preceding cost reaches x/8 of the total.
+__device__ __forceinline__ void down_slices(const PermuteParams& p, int* lds) {
+    const int nrt = p.totals[4], ncol = p.down_col_tiles;
+    const int total = block_exclusive_scan(
+        nrt, [&](int i) { return p.rt_info[i].w * ncol; }, [&](int, int) {}, lds);
+    if (threadIdx.x == 0) {
+        p.down_slices[0] = 0;
+        p.down_slices[kXcdSlices] = nrt * ncol;
+        for (int x = 1; x < kXcdSlices; ++x)
+            if ((int64_t)x * total / kXcdSlices == 0) p.down_slices[x] = 0;
+    }
+    block_exclusive_scan(
+        nrt, [&](int i) { return p.rt_info[i].w * ncol; },
+        [&](int i, int v) {
+            const int c = p.rt_info[i].w;
+            for (int x = 1; x < kXcdSlices; ++x) {
+                const int target = (int)((int64_t)x * total / kXcdSlices);
+                if (target > v && target <= v + ncol * c)
+                    p.down_slices[x] = i * ncol + (target - v + c - 1) / c;
+            }
+        },
+        lds);
+}
+
 // One workgroup per slab: its chunks' counts become the slab row at which
-// each chunk's pairs start.
+// each chunk's pairs start. One more workgroup splits the down tile table
+// into the XCD slices.
 __global__ __launch_bounds__(256) void chunk_scan_kernel(PermuteParams p) {
     __shared__ int lds[256];
+    if ((int)blockIdx.x == (p.K + 1) * p.B) {
+        down_slices(p, lds);
+        return;
+    }
     const int sl = blockIdx.x;
     const int e = sl / p.B, c = sl - e * p.B;
     const int q0 = p.chunk_off[e], nq = p.chunk_off[e + 1] - q0;

@@ -179,7 +179,7 @@ struct FwdPlan {
     size_t bin_count, slab_count, totals, queues, zero_page;
     size_t bin_cursor, slab_off, seg_off, up_tile_off, down_tile_off, chunk_off, chunk_cnt;
     size_t pair_token, pair_mask, pair_expert, pair_of, slab_rows, slab_tok, up_tile_info, up_tile_rows, hbuf, part;
-    size_t max_chunks, max_row_tiles, rt_info, rt_masks, down_tiles;
+    size_t max_chunks, max_row_tiles, rt_info, rt_masks, down_tiles, down_slices;
     size_t total;
 };
 
@@ -231,6 +231,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.rt_info = cv.take(m.bf16 ? 16 * p.max_row_tiles : 0);
     p.rt_masks = cv.take(m.bf16 ? 8 * (kDownTMMax / 16 + 1) * p.max_row_tiles : 0);
     p.down_tiles = cv.take(m.bf16 ? 4 * p.max_row_tiles * (size_t)(m.d / kDownBNNarrow) : 0);
+    p.down_slices = cv.take(m.bf16 ? 4 * 16 : 0);
     p.total = cv.cur + 256;  // slack for aligning an unaligned base pointer
     return p;
 }
@@ -532,6 +533,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.rt_info = m.bf16 ? reinterpret_cast<int4*>(ws + plan.rt_info) : nullptr;
     pp.rt_masks = m.bf16 ? reinterpret_cast<uint64_t*>(ws + plan.rt_masks) : nullptr;
     pp.down_tiles = m.bf16 ? reinterpret_cast<int*>(ws + plan.down_tiles) : nullptr;
+    pp.down_slices = m.bf16 ? reinterpret_cast<int*>(ws + plan.down_slices) : nullptr;
     scan_kernel<<<m.K1, kScanThreads, 0, st>>>(pp);
     UNIF_LAUNCH_CHECK();
     scatter_kernel<<<ceil_div(m.N, 256), 256, 0, st>>>(pp);
@@ -547,7 +549,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         const unsigned g2 = std::min((unsigned)plan.max_chunks, gs);
         tables_kernel<<<g1 + g2, 256, 0, st>>>(pp, (int)g1);
         UNIF_LAUNCH_CHECK();
-        chunk_scan_kernel<<<m.nslab, 256, 0, st>>>(pp);
+        chunk_scan_kernel<<<m.nslab + 1, 256, 0, st>>>(pp);   // + the down slices
         UNIF_LAUNCH_CHECK();
         const int up_groups = m.K1 * ceil_div(m.B, pp.up_group);
         slabfill_kernel<<<(unsigned)up_groups + std::min((unsigned)plan.max_chunks, gs), kChunk, 0, st>>>(pp, up_groups);
@@ -606,6 +608,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         dn.part_sink = dn.part + (size_t)m.N * m.K1 * m.d;
         dn.rt_info = pp.rt_info;
         dn.rt_masks = pp.rt_masks;
+        dn.slices = pp.down_slices;
         dn.pair_mask = pp.pair_mask;
         dn.tiles = pp.down_tiles;
         dn.totals = totals;
