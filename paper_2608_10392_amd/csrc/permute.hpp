@@ -11,9 +11,9 @@
 //
 //   route_kernel       counts pairs per (expert, key), taking each pair's slot
 //                      in its bin, and rows per slab
-//   scan_kernel        one workgroup per expert: LDS-staged exclusive prefix
-//                      sums -> bin cursors, expert segment offsets, slab
-//                      offsets, chunk offsets, tile tables
+//   scan_kernel        one workgroup per expert and one more: LDS-staged
+//                      exclusive prefix sums -> bin cursors, expert segment
+//                      offsets, slab offsets, chunk offsets, tile offsets
 //   scatter_kernel     one thread per token writes its pairs at their slots
 //   tables_kernel      down row tiles (per row tile), and per chunk of
 //                      kChunk pairs of one expert: pairs per block
@@ -147,11 +147,12 @@ __device__ int staged_exclusive_scan(int n, Get get, Put put, int* stage, int* l
     return carry;
 }
 
-// One workgroup per expert. The routing kernel leaves the row counts per
-// slab and the pair counts per expert in kSlabCopies copies (slab_count:
-// [copy][nslab + K + 1]). Every workgroup sums the expert counts into the
-// segment offsets; workgroup e scans its expert's bins from its segment
-// start; workgroup 0 also builds the slab offsets and the tile tables.
+// One workgroup per expert, and one more. The routing kernel leaves the row
+// counts per slab and the pair counts per expert in kSlabCopies copies
+// (slab_count: [copy][nslab + K + 1]). Every workgroup sums the expert
+// counts into the segment offsets; workgroup e <= K scans its expert's bins
+// from its segment start; workgroup K + 1 builds the slab offsets and the
+// tile offsets meanwhile.
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
     __shared__ int lds[kScanThreads];
     __shared__ int stage[kScanStage];
@@ -178,11 +179,13 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
         segs[K1] = run;
     }
     __syncthreads();
-    const int base = segs[e];
-    staged_exclusive_scan(
-        nb, [&](int i) { return p.bin_count[(size_t)e * nb + i]; },
-        [&](int i, int v) { p.bin_cursor[(size_t)e * nb + i] = base + v; }, stage, lds);
-    if (e != 0) return;
+    if (e < K1) {
+        const int base = segs[e];
+        staged_exclusive_scan(
+            nb, [&](int i) { return p.bin_count[(size_t)e * nb + i]; },
+            [&](int i, int v) { p.bin_cursor[(size_t)e * nb + i] = base + v; }, stage, lds);
+        return;
+    }
     for (int x = threadIdx.x; x <= K1; x += blockDim.x) p.seg_off[x] = segs[x];
     const int P = segs[K1];
     // Row counts per slab: sum the copies into the first.

@@ -534,7 +534,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     pp.rt_masks = m.bf16 ? reinterpret_cast<uint64_t*>(ws + plan.rt_masks) : nullptr;
     pp.down_tiles = m.bf16 ? reinterpret_cast<int*>(ws + plan.down_tiles) : nullptr;
     pp.down_slices = m.bf16 ? reinterpret_cast<int*>(ws + plan.down_slices) : nullptr;
-    scan_kernel<<<m.K1, kScanThreads, 0, st>>>(pp);
+    scan_kernel<<<m.K1 + 1, kScanThreads, 0, st>>>(pp);
     UNIF_LAUNCH_CHECK();
     scatter_kernel<<<ceil_div(m.N, 256), 256, 0, st>>>(pp);
     UNIF_LAUNCH_CHECK();
