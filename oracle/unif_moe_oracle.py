@@ -38,8 +38,21 @@ Readings where the paper is silent (each is listed in the design notes):
   * The workloads' cumulative-mass threshold t caps the target:
     min(beta, t) ("coupled"); t = 1 is the paper exactly. "fixed" uses t
     alone; "topk" uses a fixed k (the ablation's top-k residual activation).
-  * GELU is the exact erf form; there are no biases.
+  * GELU is the exact erf form; the layer itself has no biases.
   * The selected residual experts keep their raw affinities p_i.
+
+The surrounding transformer block (the paper leaves biases out of its
+equations and converts layers of pre-LN DeiT and post-LN BERT backbones) is
+``block_forward``. Its readings:
+  * b1 enters each channel before the GELU: GELU(x K_j[:, h] + b1_j[h]).
+  * b2 of expert j is split over the blocks in proportion: a pathway that
+    runs the set C of blocks of expert j adds (|C| / B) b2_j, so the shared
+    and residual parts of one expert add up to its full FFN (bias included).
+  * LayerNorm uses the biased variance over d and its eps inside the square
+    root. Pre-LN: y = x + F(LN(x)), LN(x) rounded once to the layer's format
+    (it is the FFN's input, routing included). Post-LN: y = LN(x + F(x)).
+    The residual add can be switched off (then y = F(..) or LN(F(x))).
+  * Padded tokens have F = 0 (no biases); the rest of the block applies.
 
 Parity pins: every function here is checked by tests marked "not gpu"
 against brute-force enumeration, closed forms, the textbook top-k MoE /
@@ -209,24 +222,33 @@ def decisions(rec, t):
 class ExpertWeights:
     """Expert weights as float64 (exact copies of the bf16 / fp32 inputs)."""
 
-    def __init__(self, cfg, W_up, W_down):
+    def __init__(self, cfg, W_up, W_down, b_up=None, b_down=None):
         self.M = cfg["block_width"]
         self.B = cfg["n_blocks"]
         self.up = _as_f32(W_up, cfg["dtype"]).astype(F64)      # [K+1, H, d]
         self.down = _as_f32(W_down, cfg["dtype"]).astype(F64)  # [K+1, d, H]
+        # Optional FFN biases (float32 inputs): b1 [K+1, H], b2 [K+1, d].
+        self.b_up = None if b_up is None else np.asarray(b_up, F32).astype(F64)
+        self.b_down = None if b_down is None else np.asarray(b_down, F32).astype(F64)
 
     def block_output(self, x, j, c):
-        """E_j^(c)(x) of Eq. block-expert-output, float64 [d]."""
+        """E_j^(c)(x) of Eq. block-expert-output, float64 [d] (with b1 when
+        the block has biases)."""
         h = slice(c * self.M, (c + 1) * self.M)
         a = self.up[j, h] @ x                 # x K_j[:, h] for the M channels
+        if self.b_up is not None:
+            a = a + self.b_up[j, h]
         return self.down[j][:, h] @ gelu(a)   # sum_h GELU(.) V_j[h, :]
 
     def selected_output(self, x, j, blocks):
         """Sum of E_j^(c)(x) over the given blocks (Eq. selected-shared-output,
-        selected-residual-output)."""
+        selected-residual-output), plus the blocks' share |blocks| / B of b2_j
+        when the block has biases."""
         y = np.zeros(self.down.shape[1], F64)
         for c in blocks:
             y += self.block_output(x, j, c)
+        if self.b_down is not None:
+            y = y + (len(blocks) / self.B) * self.b_down[j]
         return y
 
 
@@ -275,6 +297,84 @@ def forced_forward(cfg, X, rec, t, shared_blocks, experts, weights):
     x = _as_f32(X[t], cfg["dtype"]).astype(F64)
     residual = [(j, rec["s"][t, j - 1]) for j in experts]
     return _token_output(weights, x, rec["alpha"][t], list(shared_blocks), residual)
+
+
+# ----------------------------------------------------- transformer block ---
+NORM_MODES = ("none", "pre", "post")
+
+
+def layer_norm(v, gamma, beta, eps):
+    """LayerNorm over the last axis, float64: (v - mean) / sqrt(var + eps)
+    gamma + beta with the biased variance; gamma, beta and eps are float32
+    inputs."""
+    v = np.asarray(v, F64)
+    mu = v.mean(axis=-1, keepdims=True)
+    var = np.mean((v - mu) ** 2, axis=-1, keepdims=True)
+    g = np.asarray(gamma, F32).astype(F64)
+    b = np.asarray(beta, F32).astype(F64)
+    return (v - mu) / np.sqrt(var + F64(F32(eps))) * g + b
+
+
+def to_format(v, dtype):
+    """float64 -> the layer's format, rounded once to nearest, ties to even:
+    bf16 bit patterns (uint16) or float32. (bf16: exact for values in the
+    normal range and zero.)"""
+    v = np.asarray(v, F64)
+    if dtype == "f32":
+        return v.astype(F32)
+    m, e = np.frexp(v)                                   # v = m 2^e, 1/2 <= |m| < 1
+    r = np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)         # 8 significant bits
+    return (r.astype(F32).view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def rounding_slack(v, dtype):
+    """Distance (float64) of each value to the nearest point where its
+    rounding to the layer's format changes (a midpoint between two
+    neighbours)."""
+    v = np.asarray(v, F64)
+    bits = 8 if dtype == "bf16" else 24
+    m, e = np.frexp(v)
+    s = np.ldexp(np.abs(m), bits)
+    return np.ldexp(np.abs(s - (np.floor(s) + 0.5)), e - bits)
+
+
+def block_weights(cfg, blk, W_up, W_down):
+    return ExpertWeights(cfg, W_up, W_down, blk.get("b_up"), blk.get("b_down"))
+
+
+def block_input(cfg, blk, X):
+    """The FFN's input: LN(x) rounded to the layer's format (pre-LN), else X."""
+    if blk["norm"] != "pre":
+        return X
+    x = _as_f32(X, cfg["dtype"]).astype(F64)
+    return to_format(layer_norm(x, blk["ln_gamma"], blk["ln_beta"], blk["ln_eps"]), cfg["dtype"])
+
+
+def block_finish(cfg, blk, X, F):
+    """Residual add and post-LN around FFN outputs F (float64 rows of the
+    tokens in X)."""
+    z = F + _as_f32(X, cfg["dtype"]).astype(F64) if blk["residual"] else F
+    if blk["norm"] == "post":
+        z = layer_norm(z, blk["ln_gamma"], blk["ln_beta"], blk["ln_eps"])
+    return z
+
+
+def block_forward(cfg, blk, X, valid, W_router, prototypes, W_up, W_down, tokens=None,
+                  weights=None):
+    """Transformer-block output around the layer (float64 [N, d]), the
+    routing record and the FFN input.
+
+    ``blk``: norm ("none", "pre", "post"), residual (bool), ln_gamma and
+    ln_beta [d] and ln_eps (float32), b_up [K+1, H] and b_down [K+1, d]
+    (float32 or None). With ``tokens`` only those rows are block outputs.
+    """
+    if blk["norm"] not in NORM_MODES:
+        raise ValueError("unknown norm mode")
+    Xin = block_input(cfg, blk, X)
+    W = weights if weights is not None else block_weights(cfg, blk, W_up, W_down)
+    F, rec = forward(cfg, Xin, valid, W_router, prototypes, None, None, tokens=tokens,
+                     weights=W)
+    return block_finish(cfg, blk, X, F), rec, Xin
 
 
 # ------------------------------------------------------------- margins ---

@@ -7,7 +7,10 @@ first n token rows of a workload do not depend on the total token count.
 
 Stream tags: 0 token draws, 1 base up-projection, 2 base down-projection,
 3 router, 4 block prototypes, 5 padding lengths, 6 skewed-router directions,
-7 bimodal token signs, 10 + e expert e's perturbation (up, then down).
+7 bimodal token signs, 10 + e expert e's perturbation (up, then down);
+for the transformer block around the layer: 200 LayerNorm gain, 201 LayerNorm
+shift, 202 up-projection biases, 203 down-projection biases, 204 residual-
+stream scales and offsets.
 
 Values are drawn in float64. Router and prototypes are cast to float32;
 tokens and expert weights to float32 (fp32 workloads) or to bfloat16 with
@@ -175,3 +178,33 @@ def generate(name_or_cfg, n_tokens=None, weights=True, router_scales=None, **ove
 def as_f32(a, dtype):
     """Array of a workload (bf16 bits or float32) as float32 values."""
     return bf16_bits_to_f32(a) if dtype == "bf16" else np.asarray(a, dtype=np.float32)
+
+
+def block_inputs(gen, norm, residual=True, biases=True, eps=1e-5):
+    """Parameters of the transformer block around a generated layer, and its
+    residual-stream input.
+
+    Returns (blk, X): ``blk`` holds norm ("none", "pre" or "post"), residual,
+    ln_eps, ln_gamma [d] ~ 1 + 0.2 N(0, 1), ln_beta [d] ~ 0.1 N(0, 1),
+    b_up [K+1, H] ~ 0.3 N(0, 1) and b_down [K+1, d] ~ 0.05 N(0, 1) (float32;
+    None without biases). X is the workload's tokens with a per-token scale
+    U(0.5, 2.5) and a per-feature offset 0.3 N(0, 1), in the layer's format:
+    the un-normalised residual stream that LayerNorm sees.
+    """
+    cfg = gen["cfg"]
+    d, K = cfg["d_model"], cfg["n_experts"]
+    H = cfg["n_blocks"] * cfg["block_width"]
+    n = gen["X"].shape[0]
+    seed = cfg["seed"]
+    blk = dict(norm=norm, residual=bool(residual), ln_eps=np.float32(eps),
+               ln_gamma=(1.0 + 0.2 * _rng(seed, 200).standard_normal(d)).astype(np.float32),
+               ln_beta=(0.1 * _rng(seed, 201).standard_normal(d)).astype(np.float32),
+               b_up=None, b_down=None)
+    if biases:
+        blk["b_up"] = (0.3 * _rng(seed, 202).standard_normal((K + 1, H))).astype(np.float32)
+        blk["b_down"] = (0.05 * _rng(seed, 203).standard_normal((K + 1, d))).astype(np.float32)
+    r = _rng(seed, 204)
+    offset = 0.3 * r.standard_normal(d)
+    scale = r.uniform(0.5, 2.5, size=n)
+    x = as_f32(gen["X"], cfg["dtype"]).astype(np.float64) * scale[:, None] + offset[None, :]
+    return blk, _cast(x, cfg["dtype"])

@@ -416,7 +416,157 @@ def pin_margins(O):
             assert abs(m[t] - ref) < 1e-5, (m[t], ref)
 
 
+# ------------------------------------------------ the block around it ---
+def tb_layer_norm_row(v, gamma, beta, eps):
+    """LayerNorm of one row in plain Python floats (biased variance)."""
+    n = len(v)
+    mu = math.fsum(v) / n
+    var = math.fsum((a - mu) ** 2 for a in v) / n
+    r = 1.0 / math.sqrt(var + float(eps))
+    return [(a - mu) * r * float(g) + float(b) for a, g, b in zip(v, gamma, beta)]
+
+
+def tb_layer_norm(x, gamma, beta, eps):
+    return np.array([tb_layer_norm_row(list(map(float, row)), gamma, beta, eps) for row in x])
+
+
+def tb_bf16(v):
+    """Nearest bfloat16 to v (ties to even), by exact rational arithmetic."""
+    from fractions import Fraction
+    if v == 0:
+        return 0.0
+    q = Fraction(v)
+    e = math.floor(math.log2(abs(v)))
+    while Fraction(2) ** e > abs(q):
+        e -= 1
+    while Fraction(2) ** (e + 1) <= abs(q):
+        e += 1
+    ulp = Fraction(2) ** (e - 7)
+    lo = math.floor(q / ulp)
+    rem = q / ulp - lo
+    n = lo + 1 if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and lo % 2 == 1) else lo
+    return float(n * ulp)
+
+
+def _block(d, K, B, M, rng, norm, residual, biases=True, eps=1e-5):
+    H = B * M
+    f = np.float32
+    return dict(norm=norm, residual=residual, ln_eps=f(eps),
+                ln_gamma=(1.0 + 0.3 * rng.standard_normal(d)).astype(f),
+                ln_beta=(0.2 * rng.standard_normal(d)).astype(f),
+                b_up=(0.5 * rng.standard_normal((K + 1, H))).astype(f) if biases else None,
+                b_down=(0.5 * rng.standard_normal((K + 1, d))).astype(f) if biases else None)
+
+
+def _block_forward(O, cfg, blk, L, valid=None):
+    cfg = dict(cfg)
+    cfg["n_tokens"] = L["X"].shape[0]
+    return O.block_forward(cfg, blk, L["X"], valid, L["W_router"], L["prototypes"],
+                           L["W_up"], L["W_down"])
+
+
+def pin_layer_norm(O):
+    """A row worked by hand, and random rows against plain-Python LayerNorm."""
+    x = np.array([[1.0, 2.0, 3.0, 4.0]])
+    # mean 5/2, biased variance 5/4, eps 11/4: the scale is 1 / sqrt(4) = 1/2
+    y = O.layer_norm(x, [1.0, 2.0, -1.0, 0.5], [0.0, 1.0, 0.0, -1.0], 2.75)
+    assert np.array_equal(y, [[-0.75, 0.5, -0.25, -0.625]]), y
+    rng = np.random.default_rng(30)
+    x = 3.0 * rng.standard_normal((20, 7)) + 5.0
+    g = (1 + rng.standard_normal(7)).astype(np.float32)
+    b = rng.standard_normal(7).astype(np.float32)
+    _close(O.layer_norm(x, g, b, np.float32(1e-3)), tb_layer_norm(x, g, b, np.float32(1e-3)), 1e-12,
+           "LayerNorm")
+
+
+def pin_bf16_rounding(O):
+    """Rounding to bf16 against exact rational rounding, including ties and
+    values just off a tie (where rounding through float32 first goes wrong)."""
+    one = 1.0
+    vals = [one, one + 2.0 ** -8, one + 3 * 2.0 ** -8, one + 2.0 ** -8 + 2.0 ** -40,
+            -(one + 2.0 ** -8 + 2.0 ** -40), 3.0 * 2.0 ** -100, -7.99, 1e30, 0.0]
+    rng = np.random.default_rng(31)
+    vals += list(rng.standard_normal(200) * 10.0 ** rng.integers(-6, 6, 200))
+    got = O.to_format(np.array(vals), "bf16")
+    got_f = (got.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    for v, g in zip(vals, got_f):
+        assert g == tb_bf16(v), (v, g, tb_bf16(v))
+    assert np.array_equal(O.to_format(np.array(vals), "f32"), np.array(vals, np.float32))
+
+
+def pin_block_dense(O):
+    """alpha fixed at 1, pre-LN, biases and residual: the textbook pre-LN
+    block x + GELU(LN(x) K + b1) V + b2 of the shared expert (LN(x) rounded
+    to the layer's float32 format)."""
+    rng = np.random.default_rng(32)
+    d, K, B, M, N = 6, 3, 4, 2, 25
+    L = random_layer(rng, N, d, K, B, M, weight_scale=0.5)
+    L["X"] = (2.0 * L["X"] + 1.0).astype(np.float32)
+    blk = _block(d, K, B, M, rng, "pre", True)
+    cfg = layer_cfg(d, K, B, M, alpha_mode="fixed", alpha_fixed=1.0)
+    Y, rec, Xin = _block_forward(O, cfg, blk, L)
+    xn = tb_layer_norm(L["X"], blk["ln_gamma"], blk["ln_beta"], blk["ln_eps"]).astype(np.float32)
+    a = xn.astype(float) @ L["W_up"][0].astype(float).T + blk["b_up"][0].astype(float)
+    ref = L["X"].astype(float) + _gelu_vec(a) @ L["W_down"][0].astype(float).T + blk["b_down"][0]
+    _close(Y, ref, 1e-9, "pre-LN dense block")
+    assert np.array_equal(Xin, xn)
+
+
+def pin_block_bias_split(O):
+    """Zero expert weights leave only the biases: GELU(0 + b1) meets zero
+    values, and expert j's b2 enters with its pathway's share of the blocks,
+    alpha (b / B) b2_shr + sum_i p_i ((B - b) / B) b2_{q_i}."""
+    rng = np.random.default_rng(33)
+    d, K, B, M, N = 5, 4, 4, 2, 40
+    L = random_layer(rng, N, d, K, B, M, logit_scale=2.0)
+    L["W_up"][:] = 0
+    L["W_down"][:] = 0
+    blk = _block(d, K, B, M, rng, "none", False)
+    cfg = layer_cfg(d, K, B, M, mass_threshold=0.8)
+    Y, rec, _ = _block_forward(O, cfg, blk, L)
+    b2 = blk["b_down"].astype(float)
+    for t in range(N):
+        b, k = int(rec["n_shared"][t]), int(rec["n_res"][t])
+        ref = float(rec["alpha"][t]) * (b / B) * b2[0]
+        for i in range(k):
+            ref = ref + float(rec["weights"][t, i]) * ((B - b) / B) * b2[rec["expert_ids"][t, i]]
+        _close(Y[t], ref, 1e-12, f"bias split, token {t}")
+
+
+def pin_block_post_ln(O):
+    """Post-LN block: LN(x + F(x)) with F the layer itself; and without the
+    residual add, LN(F(x))."""
+    rng = np.random.default_rng(34)
+    d, K, B, M, N = 6, 3, 4, 2, 20
+    L = random_layer(rng, N, d, K, B, M, weight_scale=0.5)
+    for residual in (True, False):
+        blk = _block(d, K, B, M, rng, "post", residual, biases=False)
+        Y, _, Xin = _block_forward(O, layer_cfg(d, K, B, M), blk, L)
+        F, _ = _forward(O, layer_cfg(d, K, B, M), L)
+        z = F + L["X"].astype(float) if residual else F
+        _close(Y, tb_layer_norm(z, blk["ln_gamma"], blk["ln_beta"], blk["ln_eps"]), 1e-12,
+               "post-LN block")
+        assert Xin is L["X"]
+
+
+def pin_block_padding(O):
+    """Padded tokens have no FFN term: pre-LN + residual gives x, post-LN +
+    residual gives LN(x)."""
+    rng = np.random.default_rng(35)
+    d, K, B, M, N = 4, 3, 4, 2, 12
+    L = random_layer(rng, N, d, K, B, M)
+    valid = (np.arange(N) % 3 != 0).astype(np.uint8)
+    pad = valid == 0
+    for norm in ("pre", "post"):
+        blk = _block(d, K, B, M, rng, norm, True)
+        Y, _, _ = _block_forward(O, layer_cfg(d, K, B, M), blk, L, valid=valid)
+        x = L["X"][pad].astype(float)
+        ref = x if norm == "pre" else tb_layer_norm(x, blk["ln_gamma"], blk["ln_beta"], blk["ln_eps"])
+        _close(Y[pad], ref, 1e-12, f"padded rows ({norm})")
+
+
 ALL_PINS = [pin_hand_example, pin_gelu, pin_tau, pin_round_half_even, pin_alpha_range,
             pin_rank_order, pin_bruteforce, pin_topk_moe, pin_dense_ffn, pin_soft_moe,
             pin_identical_experts, pin_prefix_selection, pin_mass_bound, pin_padding,
-            pin_stats, pin_margins]
+            pin_stats, pin_margins, pin_layer_norm, pin_bf16_rounding, pin_block_dense,
+            pin_block_bias_split, pin_block_post_ln, pin_block_padding]

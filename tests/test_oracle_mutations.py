@@ -38,6 +38,19 @@ MUTANTS = {
     "margin_set_wrong": ("m_set[rows] = p[rows, k[rows] - 1] - p[rows, k[rows]]",
                          "m_set[rows] = p[rows, 0] - p[rows, k[rows]]"),
     "stats_cb_wrong": ("return b + k * (B - b)", "return b + k * B"),
+    "b1_dropped": ("a = a + self.b_up[j, h]", "a = a"),
+    "b2_unsplit": ("y = y + (len(blocks) / self.B) * self.b_down[j]", "y = y + self.b_down[j]"),
+    "b2_on_shared_row": ("y = y + (len(blocks) / self.B) * self.b_down[j]",
+                         "y = y + (len(blocks) / self.B) * self.b_down[0]"),
+    "ln_unbiased_variance": ("var = np.mean((v - mu) ** 2, axis=-1, keepdims=True)",
+                             "var = np.sum((v - mu) ** 2, axis=-1, keepdims=True) / (v.shape[-1] - 1)"),
+    "ln_eps_outside_root": ("(v - mu) / np.sqrt(var + F64(F32(eps)))", "(v - mu) / (np.sqrt(var) + F64(F32(eps)))"),
+    "ln_shift_dropped": ("* g + b\n", "* g\n"),
+    "bf16_through_f32": ("r = np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)",
+                         "r = np.ldexp(np.rint(np.ldexp(m.astype(F32).astype(F64), 8)), e - 8)"),
+    "bf16_truncated": ("np.rint(np.ldexp(m, 8))", "np.trunc(np.ldexp(m, 8))"),
+    "pre_ln_on_output": ('if blk["norm"] == "post":', 'if blk["norm"] in ("pre", "post"):'),
+    "residual_dropped": ('z = F + _as_f32(X, cfg["dtype"]).astype(F64) if blk["residual"] else F', "z = F"),
 }
 
 
