@@ -197,6 +197,65 @@ int32_t unif_moe_layer_forward_profiled(const unif_moe_config* cfg, const void* 
                                         size_t workspace_bytes, void* const* events,
                                         int32_t n_events, void* stream);
 
+/* The transformer block around the layer (the paper converts FFN layers of
+ * a pre-LN DeiT and a post-LN BERT backbone; its equations leave biases
+ * out). With F the layer above plus FFN biases:
+ *   UNIF_NORM_NONE  y = [x +] F(x)
+ *   UNIF_NORM_PRE   y = [x +] F(LN(x))     (pre-LN block, as in DeiT)
+ *   UNIF_NORM_POST  y = LN([x +] F(x))     (post-LN block, as in BERT)
+ * where [x +] is the residual add (switched by `residual`) and
+ *   LN(v) = (v - mean(v)) / sqrt(var(v) + eps) * gamma + beta
+ * with the biased variance over the d features. Biases (readings, since the
+ * paper does not define them per block):
+ *   b_up (b1) enters every active channel before the GELU:
+ *     GELU(x K_j[:, h] + b1_j[h]);
+ *   b_down (b2) of expert j is split over its blocks in proportion: a
+ *     pathway that runs the set C of blocks adds (|C| / B) b2_j, so the
+ *     shared part (alpha-weighted, C = I_shr) and the residual part
+ *     (p_i-weighted, C = I_res) of one expert sum to its whole FFN.
+ * Padded tokens have F = 0 (no bias terms); the rest of the block applies. */
+#define UNIF_NORM_NONE 0
+#define UNIF_NORM_PRE  1
+#define UNIF_NORM_POST 2
+
+typedef struct unif_moe_block {
+    int32_t      norm;      /* UNIF_NORM_*                                         */
+    int32_t      residual;  /* nonzero: add the block input x                      */
+    float        ln_eps;    /* eps > 0, finite (unused for UNIF_NORM_NONE)         */
+    const float* ln_gamma;  /* [d] fp32 device array (required unless NONE)        */
+    const float* ln_beta;   /* [d] fp32 device array (required unless NONE)        */
+    const float* b_up;      /* [K+1, H] fp32 device array, row e = b1 of expert e;
+                               NULL: no up-projection bias                         */
+    const float* b_down;    /* [K+1, d] fp32 device array, row e = b2 of expert e;
+                               NULL: no down-projection bias                       */
+} unif_moe_block;
+
+/* Workspace needed by unif_moe_block_forward (bytes). Host only. Returns
+ * UNIF_OK, UNIF_EINVAL or UNIF_EUNSUPPORTED exactly as the forward would
+ * before its pointer checks. */
+int32_t unif_moe_block_forward_workspace_size(const unif_moe_config* cfg,
+                                              const unif_moe_block* blk, size_t* bytes);
+
+/* Forward pass of the block around the layer (see unif_moe_block): the
+ * layer's routing, permutation and block-sparse FFNs run on the FFN input
+ * (LN(x) for UNIF_NORM_PRE, else x), with the biases of `blk`; the merge of
+ * Eq. output then adds the b2 shares, the residual x and, for
+ * UNIF_NORM_POST, the LayerNorm. Arguments as unif_moe_layer_forward, plus
+ * `blk` (host structure holding device pointers).
+ * Precision: LN statistics and the normalisation run in fp64 and are rounded
+ * once to the layer's format (to nearest even; for bf16 through
+ * round-to-odd fp32, which equals direct rounding for normal results).
+ * Pre-LN: LN(x) is stored in the layer's format, as the FFN's input.
+ * Requires what unif_moe_layer_forward requires, and d <= 40960 for
+ * UNIF_NORM_POST (one fp32 row in LDS); otherwise UNIF_EUNSUPPORTED.
+ * Errors: UNIF_EINVAL (also for a NULL blk, an unknown norm, a bad eps or a
+ * missing gamma/beta), UNIF_EWORKSPACE, UNIF_EUNSUPPORTED, UNIF_EDEVICE. */
+int32_t unif_moe_block_forward(const unif_moe_config* cfg, const unif_moe_block* blk,
+                               const void* X, const uint8_t* valid, const float* W_router,
+                               const float* prototypes, const void* W_up, const void* W_down,
+                               void* Y, const unif_moe_routing* routing_out, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
 /* Workspace needed by unif_moe_stats (bytes). Host only. */
 int32_t unif_moe_stats_workspace_size(const unif_moe_config* cfg, size_t* bytes);
 

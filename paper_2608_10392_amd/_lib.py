@@ -43,9 +43,20 @@ class Stats(ctypes.Structure):
                 ("activated_gemm_flops", ctypes.c_double), ("routing_flops", ctypes.c_double)]
 
 
+NORM_MODES = {"none": 0, "pre": 1, "post": 2}
+
+
+class Block(ctypes.Structure):
+    _fields_ = [("norm", ctypes.c_int32), ("residual", ctypes.c_int32),
+                ("ln_eps", ctypes.c_float), ("ln_gamma", ctypes.c_void_p),
+                ("ln_beta", ctypes.c_void_p), ("b_up", ctypes.c_void_p),
+                ("b_down", ctypes.c_void_p)]
+
+
 EXPORTS = ("unif_moe_route_workspace_size", "unif_moe_route",
            "unif_moe_layer_forward_workspace_size", "unif_moe_layer_forward",
-           "unif_moe_layer_forward_profiled", "unif_moe_stats_workspace_size",
+           "unif_moe_layer_forward_profiled", "unif_moe_block_forward_workspace_size",
+           "unif_moe_block_forward", "unif_moe_stats_workspace_size",
            "unif_moe_stats", "unif_moe_status_string")
 N_PHASE_EVENTS = 6
 
@@ -80,6 +91,10 @@ def lib():
                                                       ctypes.POINTER(vp), ctypes.c_int32, vp]
         L.unif_moe_stats.argtypes = [cfgp, ctypes.POINTER(Routing), vp, ctypes.POINTER(Stats),
                                      vp, sz, vp]
+        blkp = ctypes.POINTER(Block)
+        L.unif_moe_block_forward_workspace_size.argtypes = [cfgp, blkp, ctypes.POINTER(sz)]
+        L.unif_moe_block_forward.argtypes = [cfgp, blkp, vp, vp, vp, vp, vp, vp, vp,
+                                             ctypes.POINTER(Routing), vp, sz, vp]
         L.unif_moe_status_string.argtypes = [ctypes.c_int32]
         L.unif_moe_status_string.restype = ctypes.c_char_p
         for name in EXPORTS[:-1]:
@@ -206,6 +221,39 @@ def layer_forward_profiled(cfg, X, valid, W_router, prototypes, W_up, W_down, Y,
         ctypes.byref(c), _ptr(X), _ptr(valid), _ptr(W_router), _ptr(prototypes), _ptr(W_up),
         _ptr(W_down), _ptr(Y), ctypes.byref(r) if r is not None else None, _ptr(workspace),
         ws_bytes, handles, N_PHASE_EVENTS, _stream(stream)), "unif_moe_layer_forward_profiled")
+
+
+def make_block(blk):
+    """Block structure from a dict: norm ("none", "pre", "post"), residual,
+    ln_eps, and device tensors (or None) ln_gamma, ln_beta, b_up, b_down."""
+    return Block(norm=NORM_MODES[blk["norm"]], residual=1 if blk["residual"] else 0,
+                 ln_eps=float(blk["ln_eps"]), ln_gamma=_ptr(blk.get("ln_gamma")),
+                 ln_beta=_ptr(blk.get("ln_beta")), b_up=_ptr(blk.get("b_up")),
+                 b_down=_ptr(blk.get("b_down")))
+
+
+def block_forward_workspace_size(cfg, blk):
+    c = make_config(cfg) if isinstance(cfg, dict) else cfg
+    b = make_block(blk) if isinstance(blk, dict) else blk
+    n = ctypes.c_size_t(0)
+    _check(lib().unif_moe_block_forward_workspace_size(ctypes.byref(c), ctypes.byref(b),
+                                                       ctypes.byref(n)),
+           "unif_moe_block_forward_workspace_size")
+    return n.value
+
+
+def block_forward(cfg, blk, X, valid, W_router, prototypes, W_up, W_down, Y, workspace,
+                  routing=None, stream=None):
+    c = make_config(cfg)
+    b = make_block(blk)
+    r = _routing_struct(routing)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().unif_moe_block_forward(ctypes.byref(c), ctypes.byref(b), _ptr(X), _ptr(valid),
+                                        _ptr(W_router), _ptr(prototypes), _ptr(W_up),
+                                        _ptr(W_down), _ptr(Y),
+                                        ctypes.byref(r) if r is not None else None,
+                                        _ptr(workspace), ws_bytes, _stream(stream)),
+           "unif_moe_block_forward")
 
 
 def stats(cfg, routing, valid, workspace, stream=None):

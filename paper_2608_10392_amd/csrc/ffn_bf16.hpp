@@ -69,6 +69,7 @@ struct UpParams {
     const int* tile_rows;    // first entry of the tile's rows in slab_rows / slab_tok
     const int* totals;
     int* queue;              // 8 per-XCD tile counters, zero at launch
+    const float* b_up;       // [K+1, H] fp32 biases added before the GELU (BIAS kernels only)
 };
 
 struct DownParams {
@@ -173,7 +174,7 @@ __device__ __forceinline__ void wait_stage(int s, bool after_epi, bool has_next)
 //    with stages that re-read k = 0.. and run no MFMAs (the row-list copy of
 //    stage 0 is waited for at the barrier of stage 2). PAD: whether d < 256
 //    (else no stage is padding and the MFMAs need no per-stage test).
-template <int MG, bool PAD, int TM>
+template <int MG, bool PAD, int TM, bool BIAS = false>
 __global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void up_kernel(UpParams p) {
     using S = Stage;
@@ -381,7 +382,20 @@ void up_kernel(UpParams p) {
             dst += wn * (M / 2) + 16 * lh;
 #pragma unroll
             for (int j = 0; j < MG; ++j) {
-                const f32x16 v = acc[i][j];
+                f32x16 v = acc[i][j];
+                if constexpr (BIAS) {
+                    // b1 of the lane's 16 columns (Eq. block-expert-output
+                    // with the FFN's first bias). The compiler's wait for
+                    // these loads also covers the copies in flight: an
+                    // over-wait, never an early one.
+                    const float* bb = p.b_up + (size_t)(sl / p.B) * p.H + (size_t)c * M + wn * (M / 2) + 16 * lh + 32 * j;
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const f32x4 b4 = *reinterpret_cast<const f32x4*>(bb + 4 * u);
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) v[4 * u + q] += b4[q];
+                    }
+                }
                 u32x4 lo, hi;
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {

@@ -19,6 +19,7 @@ struct PairF32Params {
     const int* pair_expert;
     const uint64_t* pair_mask;
     const int* totals;
+    const float* b_up;   // [K+1][H] biases added before the GELU, or null
 };
 
 __global__ __launch_bounds__(256) void pair_ffn_f32_kernel(PairF32Params p) {
@@ -35,6 +36,7 @@ __global__ __launch_bounds__(256) void pair_ffn_f32_kernel(PairF32Params p) {
             if ((m >> (h / p.M)) & 1ull) {
                 const float* w = Wu + (size_t)h * p.d;
                 for (int i = 0; i < p.d; ++i) a = fmaf(x[i], w[i], a);
+                if (p.b_up != nullptr) a += p.b_up[(size_t)e * p.H + h];
                 a = gelu_erf(a);
             }
             g_act[h] = a;

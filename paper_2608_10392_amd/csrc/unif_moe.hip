@@ -14,6 +14,8 @@
 //   up, down         block-sparse MFMA grouped GEMMs              (bf16)
 //   pair_ffn_f32     per-pair fp32 FFN                            (fp32)
 //   combine          weighted merge in fixed order
+// The block forward adds a LayerNorm pass before routing (pre-LN) and
+// replaces the merge by the block's merge (biases, residual, post-LN).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -22,6 +24,7 @@
 #include <cstring>
 
 #include "../../include/unif_moe.h"
+#include "block.hpp"
 #include "combine.hpp"
 #include "common.hpp"
 #include "ffn_bf16.hpp"
@@ -149,6 +152,31 @@ int32_t check_forward_shape(const unif_moe_config* c) {
     return UNIF_OK;
 }
 
+// Block description: mode, eps and the shape limit of the post-LN merge
+// (checked by the workspace query too).
+constexpr int kPostLnMaxD = (int)(kLdsLimit / sizeof(float));   // one fp32 row in LDS
+int32_t check_block_shape(const unif_moe_config* c, const unif_moe_block* b) {
+    if (b == nullptr) return UNIF_EINVAL;
+    if (b->norm != UNIF_NORM_NONE && b->norm != UNIF_NORM_PRE && b->norm != UNIF_NORM_POST) return UNIF_EINVAL;
+    if (b->norm != UNIF_NORM_NONE && !(b->ln_eps > 0.0f && std::isfinite(b->ln_eps))) return UNIF_EINVAL;
+    if (b->norm == UNIF_NORM_POST && c->d_model > kPostLnMaxD) return UNIF_EUNSUPPORTED;
+    return UNIF_OK;
+}
+
+// Pointer checks of the block forward.
+int32_t check_block_pointers(const unif_moe_config* c, const unif_moe_block* b) {
+    if (b->norm != UNIF_NORM_NONE && (b->ln_gamma == nullptr || b->ln_beta == nullptr)) return UNIF_EINVAL;
+    // The bf16 up-projection reads b1 in 16-byte pieces.
+    if (c->dtype == UNIF_BF16 && b->b_up != nullptr && reinterpret_cast<uintptr_t>(b->b_up) % 16 != 0)
+        return UNIF_EINVAL;
+    return UNIF_OK;
+}
+
+size_t block_xn_bytes(const unif_moe_config* c, const unif_moe_block* b) {
+    if (b == nullptr || b->norm != UNIF_NORM_PRE) return 0;
+    return (size_t)c->n_tokens * (size_t)c->d_model * (c->dtype == UNIF_BF16 ? 2 : 4);
+}
+
 // Workspace carving: regions aligned to 256 bytes.
 struct Carver {
     size_t cur = 0;
@@ -180,12 +208,13 @@ struct FwdPlan {
     size_t bin_cursor, slab_off, seg_off, up_tile_off, down_tile_off, chunk_off, chunk_cnt;
     size_t pair_token, pair_mask, pair_expert, pair_of, slab_rows, slab_tok, up_tile_info, up_tile_rows, hbuf, part;
     size_t max_chunks, max_row_tiles, rt_info, rt_masks, down_tiles, down_slices;
+    size_t xn;   // LN(X), the FFN input of a pre-LN block
     size_t total;
 };
 
 size_t ceil_div_sz(size_t a, size_t b) { return (a + b - 1) / b; }
 
-FwdPlan plan_forward(const Dims& m, bool own_record) {
+FwdPlan plan_forward(const Dims& m, bool own_record, size_t xn_bytes = 0) {
     Carver cv;
     FwdPlan p;
     const size_t N = (size_t)m.N, K = (size_t)m.K, K1 = (size_t)m.K1;
@@ -232,6 +261,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record) {
     p.rt_masks = cv.take(m.bf16 ? 8 * (kDownTMMax / 16 + 1) * p.max_row_tiles : 0);
     p.down_tiles = cv.take(m.bf16 ? 4 * p.max_row_tiles * (size_t)(m.d / kDownBNNarrow) : 0);
     p.down_slices = cv.take(m.bf16 ? 4 * 16 : 0);
+    p.xn = cv.take(xn_bytes);
     p.total = cv.cur + 256;  // slack for aligning an unaligned base pointer
     return p;
 }
@@ -451,24 +481,54 @@ int32_t record_event(void* const* events, int i, hipStream_t st) {
         if (record_event(events, (i), st) != UNIF_OK) return UNIF_EDEVICE; \
     } while (0)
 
-int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
-                     const float* W_router, const float* prototypes, const void* W_up,
-                     const void* W_down, void* Y, const unif_moe_routing* routing_out,
-                     void* workspace, size_t workspace_bytes, void* const* events, void* stream) {
+// Up-projection launch for the layer's block width (BIAS: b1 before GELU).
+template <bool BIAS>
+int32_t launch_up(const Dims& m, int grid, size_t lds, hipStream_t st, const UpParams& up) {
+    const bool pad = m.d / 64 < 4;   // tiles padded to 4 stages
+    switch (m.M / 64) {
+        case 1:
+            return pad ? launch_persistent(up_kernel<1, true, 256, BIAS>, grid, lds, st, up)
+                       : launch_persistent(up_kernel<1, false, 384, BIAS>, grid, lds, st, up);
+        case 2:
+            return pad ? launch_persistent(up_kernel<2, true, 256, BIAS>, grid, lds, st, up)
+                       : launch_persistent(up_kernel<2, false, 384, BIAS>, grid, lds, st, up);
+        case 3:
+            return pad ? launch_persistent(up_kernel<3, true, 256, BIAS>, grid, lds, st, up)
+                       : launch_persistent(up_kernel<3, false, 384, BIAS>, grid, lds, st, up);
+        case 4:
+            return pad ? launch_persistent(up_kernel<4, true, 256, BIAS>, grid, lds, st, up)
+                       : launch_persistent(up_kernel<4, false, 256, BIAS>, grid, lds, st, up);
+        default: return UNIF_EUNSUPPORTED;
+    }
+}
+
+// The layer forward (blk == nullptr) or the block forward around it.
+int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, const void* X,
+                     const uint8_t* valid, const float* W_router, const float* prototypes,
+                     const void* W_up, const void* W_down, void* Y,
+                     const unif_moe_routing* routing_out, void* workspace, size_t workspace_bytes,
+                     void* const* events, void* stream) {
     int32_t s = check_config(cfg);
     if (s != UNIF_OK) return s;
     s = check_forward_shape(cfg);
     if (s != UNIF_OK) return s;
+    if (blk != nullptr) {
+        s = check_block_shape(cfg, blk);
+        if (s != UNIF_OK) return s;
+        s = check_block_pointers(cfg, blk);
+        if (s != UNIF_OK) return s;
+    }
     if (routing_out != nullptr && !record_complete(routing_out)) return UNIF_EINVAL;
     if (cfg->n_tokens > 0 && (X == nullptr || W_router == nullptr || prototypes == nullptr ||
                               W_up == nullptr || W_down == nullptr || Y == nullptr))
         return UNIF_EINVAL;
     const Dims m = dims_of(cfg);
     const bool own = routing_out == nullptr;
-    const FwdPlan plan = plan_forward(m, own);
+    const FwdPlan plan = plan_forward(m, own, block_xn_bytes(cfg, blk));
     // The size reported by the query always includes the internal record.
     size_t need = 0;
-    unif_moe_layer_forward_workspace_size(cfg, &need);
+    if (blk != nullptr) unif_moe_block_forward_workspace_size(cfg, blk, &need);
+    else unif_moe_layer_forward_workspace_size(cfg, &need);
     if (workspace == nullptr || workspace_bytes < need) return UNIF_EWORKSPACE;
     if (m.N == 0) return UNIF_OK;
 
@@ -486,9 +546,26 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
     int* totals = reinterpret_cast<int*>(ws + plan.totals);
 
     UNIF_MARK(0);
+    // 0. the FFN input: LN(X) for a pre-LN block, else X
+    const void* Xf = X;
+    if (blk != nullptr && blk->norm == UNIF_NORM_PRE) {
+        LayerNormParams ln;
+        ln.N = m.N;
+        ln.d = m.d;
+        ln.X = X;
+        ln.Xn = ws + plan.xn;
+        ln.gamma = blk->ln_gamma;
+        ln.beta = blk->ln_beta;
+        ln.eps = (double)blk->ln_eps;
+        const unsigned g = (unsigned)ceil_div(m.N, 4);
+        if (m.bf16) layernorm_rows_kernel<true><<<g, 256, 0, st>>>(ln);
+        else layernorm_rows_kernel<false><<<g, 256, 0, st>>>(ln);
+        UNIF_LAUNCH_CHECK();
+        Xf = ln.Xn;
+    }
     // 1. zero the counters (in the launch before routing) and 2. routing + counts
     const size_t zwords = (plan.zero_end - plan.zero_begin) / 4;
-    RouteParams rp = route_params(cfg, m, X, valid, W_router, prototypes, wsplit, alpha, nsh, mask, nres, eids,
+    RouteParams rp = route_params(cfg, m, Xf, valid, W_router, prototypes, wsplit, alpha, nsh, mask, nres, eids,
                                   wts);
     rp.bin_count = bin_count;
     rp.slab_count = slab_count;
@@ -561,7 +638,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         up.M = m.M;
         up.B = m.B;
         up.H = m.H;
-        up.X = static_cast<const u16*>(X);
+        up.X = static_cast<const u16*>(Xf);
         up.Wup = static_cast<const u16*>(W_up);
         up.Hbuf = reinterpret_cast<u16*>(ws + plan.hbuf);
         up.Hsink = up.Hbuf + (size_t)m.N * m.K1 * m.H;
@@ -571,28 +648,10 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         up.tile_rows = pp.up_tile_rows;
         up.totals = totals;
         up.queue = reinterpret_cast<int*>(ws + plan.queues);
+        up.b_up = blk != nullptr ? blk->b_up : nullptr;
         const size_t up_lds = (size_t)up_lds_bytes(m.M, up_tm(m.M, m.d));
         const int grid = (cus / kXcds) * kXcds;
-        const bool pad = m.d / 64 < 4;   // tiles padded to 4 stages
-        switch (m.M / 64) {
-            case 1:
-                s = pad ? launch_persistent(up_kernel<1, true, 256>, grid, up_lds, st, up)
-                        : launch_persistent(up_kernel<1, false, 384>, grid, up_lds, st, up);
-                break;
-            case 2:
-                s = pad ? launch_persistent(up_kernel<2, true, 256>, grid, up_lds, st, up)
-                        : launch_persistent(up_kernel<2, false, 384>, grid, up_lds, st, up);
-                break;
-            case 3:
-                s = pad ? launch_persistent(up_kernel<3, true, 256>, grid, up_lds, st, up)
-                        : launch_persistent(up_kernel<3, false, 384>, grid, up_lds, st, up);
-                break;
-            case 4:
-                s = pad ? launch_persistent(up_kernel<4, true, 256>, grid, up_lds, st, up)
-                        : launch_persistent(up_kernel<4, false, 256>, grid, up_lds, st, up);
-                break;
-            default: return UNIF_EUNSUPPORTED;
-        }
+        s = up.b_up != nullptr ? launch_up<true>(m, grid, up_lds, st, up) : launch_up<false>(m, grid, up_lds, st, up);
         if (s != UNIF_OK) return s;
         UNIF_MARK(3);
         DownParams dn;
@@ -628,7 +687,8 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         fp.M = m.M;
         fp.B = m.B;
         fp.H = m.H;
-        fp.X = static_cast<const float*>(X);
+        fp.X = static_cast<const float*>(Xf);
+        fp.b_up = blk != nullptr ? blk->b_up : nullptr;
         fp.Wup = static_cast<const float*>(W_up);
         fp.Wdown = static_cast<const float*>(W_down);
         fp.part = static_cast<float*>(part);
@@ -644,7 +704,43 @@ int32_t forward_impl(const unif_moe_config* cfg, const void* X, const uint8_t* v
         UNIF_MARK(4);
     }
 
-    // 5. weighted merge
+    // 5. weighted merge (the block's merge around it)
+    if (blk != nullptr) {
+        BlockCombineParams bc;
+        bc.N = m.N;
+        bc.d = m.d;
+        bc.K = m.K;
+        bc.B = m.B;
+        bc.part = part;
+        bc.pair_of = pp.pair_of;
+        bc.alpha = alpha;
+        bc.nsh = nsh;
+        bc.nres = nres;
+        bc.eids = eids;
+        bc.wts = wts;
+        bc.b_down = blk->b_down;
+        bc.X = blk->residual ? X : nullptr;
+        bc.post = blk->norm == UNIF_NORM_POST;
+        bc.gamma = blk->ln_gamma;
+        bc.beta = blk->ln_beta;
+        bc.eps = (double)blk->ln_eps;
+        bc.Y = Y;
+        // Post-LN keeps one fp32 row per wave in LDS: 4 rows per workgroup
+        // while that fits in 64 KB, else one.
+        const int rows = (!bc.post || (size_t)16 * m.d <= 65536) ? 4 : 1;
+        const size_t lds = bc.post ? (size_t)rows * m.d * sizeof(float) : 0;
+        const unsigned g = (unsigned)ceil_div(m.N, rows);
+        if (m.bf16) {
+            if (allow_lds(combine_block_kernel<true>, lds) != UNIF_OK) return UNIF_EDEVICE;
+            combine_block_kernel<true><<<g, 64 * rows, lds, st>>>(bc);
+        } else {
+            if (allow_lds(combine_block_kernel<false>, lds) != UNIF_OK) return UNIF_EDEVICE;
+            combine_block_kernel<false><<<g, 64 * rows, lds, st>>>(bc);
+        }
+        UNIF_LAUNCH_CHECK();
+        UNIF_MARK(5);
+        return UNIF_OK;
+    }
     CombineParams cp;
     cp.N = m.N;
     cp.d = m.d;
@@ -675,7 +771,30 @@ int32_t unif_moe_layer_forward(const unif_moe_config* cfg, const void* X, const 
                                const float* W_router, const float* prototypes, const void* W_up,
                                const void* W_down, void* Y, const unif_moe_routing* routing_out,
                                void* workspace, size_t workspace_bytes, void* stream) {
-    return forward_impl(cfg, X, valid, W_router, prototypes, W_up, W_down, Y, routing_out, workspace,
+    return forward_impl(cfg, nullptr, X, valid, W_router, prototypes, W_up, W_down, Y, routing_out,
+                        workspace, workspace_bytes, nullptr, stream);
+}
+
+int32_t unif_moe_block_forward_workspace_size(const unif_moe_config* cfg, const unif_moe_block* blk,
+                                              size_t* bytes) {
+    if (bytes == nullptr) return UNIF_EINVAL;
+    int32_t s = check_config(cfg);
+    if (s != UNIF_OK) return s;
+    s = check_forward_shape(cfg);
+    if (s != UNIF_OK) return s;
+    s = check_block_shape(cfg, blk);
+    if (s != UNIF_OK) return s;
+    *bytes = plan_forward(dims_of(cfg), true, block_xn_bytes(cfg, blk)).total;
+    return UNIF_OK;
+}
+
+int32_t unif_moe_block_forward(const unif_moe_config* cfg, const unif_moe_block* blk, const void* X,
+                               const uint8_t* valid, const float* W_router, const float* prototypes,
+                               const void* W_up, const void* W_down, void* Y,
+                               const unif_moe_routing* routing_out, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+    if (blk == nullptr) return UNIF_EINVAL;
+    return forward_impl(cfg, blk, X, valid, W_router, prototypes, W_up, W_down, Y, routing_out, workspace,
                         workspace_bytes, nullptr, stream);
 }
 
@@ -687,7 +806,7 @@ int32_t unif_moe_layer_forward_profiled(const unif_moe_config* cfg, const void* 
     if (events == nullptr || n_events != 6) return UNIF_EINVAL;
     for (int i = 0; i < 6; ++i)
         if (events[i] == nullptr) return UNIF_EINVAL;
-    return forward_impl(cfg, X, valid, W_router, prototypes, W_up, W_down, Y, routing_out, workspace,
+    return forward_impl(cfg, nullptr, X, valid, W_router, prototypes, W_up, W_down, Y, routing_out, workspace,
                         workspace_bytes, events, stream);
 }
 

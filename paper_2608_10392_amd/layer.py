@@ -53,6 +53,22 @@ class DeviceLayer:
                            routing=self.routing if routing else None, stream=stream)
         return self.Y
 
+    def block_forward(self, blk, X=None, stream=None, routing=True):
+        """The transformer block around the layer (``blk`` as
+        synth.block_inputs returns it: numpy parameters, moved to the device
+        on each call). ``X`` replaces the layer input (the residual stream)."""
+        dt = self.cfg["dtype"]
+        Xd = self.X if X is None else to_device(X, dt, self.device)
+        b = dict(norm=blk["norm"], residual=blk["residual"], ln_eps=blk["ln_eps"])
+        for k in ("ln_gamma", "ln_beta", "b_up", "b_down"):
+            b[k] = None if blk.get(k) is None else to_device(np.asarray(blk[k], np.float32), "f32",
+                                                              self.device)
+        ws = _lib.alloc_workspace(_lib.block_forward_workspace_size(self.cfg, b), self.device)
+        _lib.block_forward(self.cfg, b, Xd, self.valid, self.W_router, self.prototypes,
+                           self.W_up, self.W_down, self.Y, ws,
+                           routing=self.routing if routing else None, stream=stream)
+        return self.Y
+
     def route(self, out=None, stream=None):
         if self.ws_route is None:
             self.ws_route = _lib.alloc_workspace(_lib.route_workspace_size(self.cfg), self.device)

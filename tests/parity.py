@@ -32,19 +32,25 @@ def _decision_parts(rec, t, B):
     return (int(rec["n_shared"][t]), m, k, frozenset(int(j) for j in rec["expert_ids"][t, :k]))
 
 
-def check_routing(cfg, orec, grec):
-    """Compare records; returns a summary dict, raises AssertionError."""
+def check_routing(cfg, orec, grec, loose=None):
+    """Compare records; returns a summary dict, raises AssertionError.
+
+    ``loose`` marks tokens whose routing input itself may differ between the
+    two sides (see block_loose_tokens): they are checked like near-ties,
+    without the boundary condition."""
     K, B = cfg["n_experts"], cfg["n_blocks"]
     m, parts = O.margins(cfg, orec)
     v = orec["valid"]
     N = len(v)
+    if loose is None:
+        loose = np.zeros(N, bool)
     # padded tokens: exact record
     pad = ~v
     assert np.all(grec["n_res"][pad] == 0) and np.all(grec["n_shared"][pad] == 0)
     assert np.all(grec["shared_mask"][pad] == 0) and np.all(grec["alpha"][pad] == 0)
     assert np.all(grec["expert_ids"][pad] == -1) and np.all(grec["weights"][pad] == 0)
 
-    sure = v & (m >= MARGIN)
+    sure = v & (m >= MARGIN) & ~loose
     idx = np.nonzero(sure)[0]
     bad = idx[grec["n_shared"][idx] != orec["n_shared"][idx]]
     assert bad.size == 0, f"b differs on {bad.size} tokens with margin >= {MARGIN}, e.g. {bad[:5]}"
@@ -73,9 +79,10 @@ def check_routing(cfg, orec, grec):
     bad = np.nonzero(np.any(chk & (grec["expert_ids"] != orec["expert_ids"]), axis=1))[0]
     assert bad.size == 0, f"expert order differs on {bad.size} tokens, e.g. {bad[:5]}"
     # continuous values (diagnostics)
-    da = float(np.abs(grec["alpha"][v].astype(np.float64) - orec["alpha"][v]).max(initial=0.0))
-    dp = float(np.abs(np.sort(grec["weights"][v], axis=1).astype(np.float64)
-                      - np.sort(orec["weights"][v], axis=1)).max(initial=0.0))
+    vs = v & ~loose
+    da = float(np.abs(grec["alpha"][vs].astype(np.float64) - orec["alpha"][vs]).max(initial=0.0))
+    dp = float(np.abs(np.sort(grec["weights"][vs], axis=1).astype(np.float64)
+                      - np.sort(orec["weights"][vs], axis=1)).max(initial=0.0))
     # Logits differ from the correctly rounded ones by the fp32 accumulation
     # order: about sqrt(d) ulp of the partial sums, <= 1e-5 for |z| <= 30 and
     # d <= 1024; alpha and p move by at most 1/4 of that (sigmoid and softmax
@@ -83,13 +90,15 @@ def check_routing(cfg, orec, grec):
     assert da <= 1e-5, f"alpha differs by {da}"
     assert dp <= 1e-5, f"affinities differ by {dp}"
 
-    near = np.nonzero(v & (m < MARGIN))[0]
+    near = np.nonzero(v & ((m < MARGIN) | loose))[0]
     differ = []
     for t in near:
         go, oo = _decision_parts(grec, t, B), _decision_parts(orec, t, B)
         if go == oo:
             continue
         differ.append(int(t))
+        if loose[t]:
+            continue
         if go[0] != oo[0]:
             assert parts["m_b"][t] < MARGIN, ("b differs away from its boundary", t)
         elif go[1] != oo[1]:
@@ -132,6 +141,60 @@ def gpu_output_f64(Y, dtype):
     return (bf16_bits_to_f32(Y) if dtype == "bf16" else np.asarray(Y, np.float32)).astype(np.float64)
 
 
+def _output_error(cfg, Yg, ref):
+    rms = float(np.sqrt(np.mean(ref ** 2)))
+    raw = float(np.abs(Yg - ref).max())
+    excess = float(np.maximum(np.abs(Yg - ref) - half_ulp(ref, cfg["dtype"]), 0.0).max())
+    rel = excess / rms if rms > 0 else excess
+    raw_rel = raw / rms if rms > 0 else raw
+    assert rel <= TOL[cfg["dtype"]], (f"output error beyond the output format's half ulp "
+                                      f"{excess:.3e} = {rel:.3e} x RMS {rms:.3e} (raw {raw_rel:.3e})")
+    return rel, raw_rel
+
+
+# ------------------------------------------------ the block around it ---
+# The two sides compute LN(x) in fp64 (a few ulps apart) and round it to the
+# layer's format; an element within this distance of a rounding midpoint may
+# round differently, and its token's routing input with it.
+LN_SLACK = 1e-9
+
+
+def block_loose_tokens(cfg, blk, X):
+    """Tokens whose pre-LN FFN input has an element within LN_SLACK (x (1 +
+    |v|)) of a rounding midpoint of the layer's format."""
+    N = X.shape[0]
+    if blk["norm"] != "pre":
+        return np.zeros(N, bool)
+    x = O._as_f32(X, cfg["dtype"]).astype(np.float64)
+    v = O.layer_norm(x, blk["ln_gamma"], blk["ln_beta"], blk["ln_eps"])
+    return np.any(O.rounding_slack(v, cfg["dtype"]) < LN_SLACK * (1.0 + np.abs(v)), axis=1)
+
+
+def check_block_outputs(cfg, blk, inputs, Xin, orec, grec, Y_gpu, tokens, weights=None):
+    """As check_outputs, for the block forward: the oracle's FFN part under
+    the agreed (or the GPU's) decisions on the FFN input Xin, then the
+    residual add and post-LN of oracle.block_finish."""
+    if weights is None:
+        weights = O.block_weights(cfg, blk, inputs["W_up"], inputs["W_down"])
+    B = cfg["n_blocks"]
+    Yg = gpu_output_f64(Y_gpu[tokens], cfg["dtype"])
+    agree = [t for t in tokens if _decision_parts(grec, t, B) == _decision_parts(orec, t, B)]
+    Fa, _ = O.forward(cfg, Xin, inputs["valid"], inputs["W_router"], inputs["prototypes"],
+                      None, None, tokens=agree, rec=orec, weights=weights)
+    F = np.zeros_like(Yg)
+    for i, t in enumerate(tokens):
+        if not orec["valid"][t]:
+            continue
+        if _decision_parts(grec, t, B) == _decision_parts(orec, t, B):
+            F[i] = Fa[t]
+        else:
+            b, mask, k, experts = _decision_parts(grec, t, B)
+            F[i] = O.forced_forward(cfg, Xin, orec, t, [c for c in range(B) if mask >> c & 1],
+                                    sorted(experts), weights)
+    ref = O.block_finish(cfg, blk, inputs["X"][tokens], F)
+    return _output_error(cfg, Yg, ref)
+
+
 def check_outputs(cfg, inputs, orec, grec, Y_gpu, tokens, weights=None):
     """Compare GPU rows against the oracle on ``tokens``; returns the
     relative error (max abs / RMS)."""
@@ -152,11 +215,4 @@ def check_outputs(cfg, inputs, orec, grec, Y_gpu, tokens, weights=None):
             b, mask, k, experts = _decision_parts(grec, t, B)
             ref[i] = O.forced_forward(cfg, inputs["X"], orec, t,
                                       [c for c in range(B) if mask >> c & 1], sorted(experts), weights)
-    rms = float(np.sqrt(np.mean(ref ** 2)))
-    raw = float(np.abs(Yg - ref).max())
-    excess = float(np.maximum(np.abs(Yg - ref) - half_ulp(ref, cfg["dtype"]), 0.0).max())
-    rel = excess / rms if rms > 0 else excess
-    raw_rel = raw / rms if rms > 0 else raw
-    assert rel <= TOL[cfg["dtype"]], (f"output error beyond the output format's half ulp "
-                                      f"{excess:.3e} = {rel:.3e} x RMS {rms:.3e} (raw {raw_rel:.3e})")
-    return rel, raw_rel
+    return _output_error(cfg, Yg, ref)

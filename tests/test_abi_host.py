@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 8, names
+    assert len(names) == 10, names
     assert set(names) == set(_lib.EXPORTS)
     out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True, text=True).stdout
     for n in names:
@@ -43,11 +43,12 @@ def test_struct_layout_matches_header(tmp_path):
         '#include <stdio.h>\n#include <stddef.h>\n#include "unif_moe.h"\n'
         "#define F(T, m) printf(#T \".\" #m \" %zu\\n\", offsetof(T, m))\n"
         "int main(void) {\n"
-        ' printf("config %zu\\nrouting %zu\\nstats %zu\\n", sizeof(unif_moe_config),'
-        " sizeof(unif_moe_routing), sizeof(unif_moe_stats_t));\n"
+        ' printf("config %zu\\nrouting %zu\\nstats %zu\\nblock %zu\\n", sizeof(unif_moe_config),'
+        " sizeof(unif_moe_routing), sizeof(unif_moe_stats_t), sizeof(unif_moe_block));\n"
         " F(unif_moe_config, tau); F(unif_moe_config, select_mode);"
         " F(unif_moe_routing, weights); F(unif_moe_stats_t, expert_tokens);"
         " F(unif_moe_stats_t, activated_blocks); F(unif_moe_stats_t, routing_flops);\n"
+        " F(unif_moe_block, ln_eps); F(unif_moe_block, ln_gamma); F(unif_moe_block, b_down);\n"
         " return 0; }\n")
     exe = tmp_path / "layout"
     subprocess.run(["gcc", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
@@ -61,6 +62,10 @@ def test_struct_layout_matches_header(tmp_path):
     assert int(got["unif_moe_stats_t.expert_tokens"]) == _lib.Stats.expert_tokens.offset
     assert int(got["unif_moe_stats_t.activated_blocks"]) == _lib.Stats.activated_blocks.offset
     assert int(got["unif_moe_stats_t.routing_flops"]) == _lib.Stats.routing_flops.offset
+    assert int(got["block"]) == ctypes.sizeof(_lib.Block)
+    assert int(got["unif_moe_block.ln_eps"]) == _lib.Block.ln_eps.offset
+    assert int(got["unif_moe_block.ln_gamma"]) == _lib.Block.ln_gamma.offset
+    assert int(got["unif_moe_block.b_down"]) == _lib.Block.b_down.offset
 
 
 def test_status_strings(L):
@@ -147,3 +152,52 @@ def test_empty_batch_is_a_no_op(L):
     assert L.unif_moe_layer_forward_workspace_size(ctypes.byref(c), ctypes.byref(n)) == 0
     assert L.unif_moe_layer_forward(ctypes.byref(c), None, None, None, None, None, None, None,
                                     None, 1, n.value, None) == 0
+
+
+def _blk(**kw):
+    b = dict(norm="pre", residual=True, ln_eps=1e-6, ln_gamma=1, ln_beta=1, b_up=None, b_down=None)
+    b.update(kw)
+    return b
+
+
+def test_block_workspace_adds_the_normalised_input():
+    c = base_cfg(n_tokens=1000)
+    layer = _lib.layer_forward_workspace_size(c)
+    assert _lib.block_forward_workspace_size(c, _blk(norm="none")) == layer
+    assert _lib.block_forward_workspace_size(c, _blk(norm="post")) == layer
+    pre = _lib.block_forward_workspace_size(c, _blk(norm="pre"))
+    assert layer + 1000 * 768 * 2 <= pre <= layer + 1000 * 768 * 2 + 256
+
+
+@pytest.mark.parametrize("bad, status", [
+    (dict(norm="pre", ln_eps=0.0), _lib.EINVAL), (dict(norm="post", ln_eps=-1.0), _lib.EINVAL),
+    (dict(norm="pre", ln_eps=math.inf), _lib.EINVAL), (dict(norm="post", ln_eps=math.nan), _lib.EINVAL),
+])
+def test_block_invalid_rejected(bad, status):
+    with pytest.raises(_lib.UnifMoeError) as e:
+        _lib.block_forward_workspace_size(base_cfg(), _blk(**bad))
+    assert e.value.status == status
+
+
+def test_block_calls_fail_before_touching_the_device(L):
+    c = _lib.make_config(base_cfg(n_tokens=4))
+    n = ctypes.c_size_t(0)
+    good = _lib.make_block(_blk())
+    assert L.unif_moe_block_forward_workspace_size(ctypes.byref(c), None, ctypes.byref(n)) == _lib.EINVAL
+    assert L.unif_moe_block_forward_workspace_size(ctypes.byref(c), ctypes.byref(good), ctypes.byref(n)) == 0
+    big = 1 << 40
+    args = (1, None, 1, 1, 1, 1, 1, None, 1, big, None)
+    assert L.unif_moe_block_forward(ctypes.byref(c), None, *args) == _lib.EINVAL
+    bad_norm = _lib.Block(norm=7, residual=1, ln_eps=1e-6, ln_gamma=1, ln_beta=1)
+    assert L.unif_moe_block_forward(ctypes.byref(c), ctypes.byref(bad_norm), *args) == _lib.EINVAL
+    no_gamma = _lib.make_block(_blk(ln_gamma=None))
+    assert L.unif_moe_block_forward(ctypes.byref(c), ctypes.byref(no_gamma), *args) == _lib.EINVAL
+    odd_bias = _lib.make_block(_blk(b_up=4))          # bf16 layers read b1 in 16-byte pieces
+    assert L.unif_moe_block_forward(ctypes.byref(c), ctypes.byref(odd_bias), *args) == _lib.EINVAL
+    no_ln = _lib.make_block(_blk(norm="none", ln_gamma=None, ln_beta=None, ln_eps=0.0))
+    assert L.unif_moe_block_forward(ctypes.byref(c), ctypes.byref(no_ln), 1, None, 1, 1, 1, 1, 1, None,
+                                    None, 0, None) == _lib.EWORKSPACE
+    post_wide = _lib.make_config(base_cfg(n_tokens=4, d_model=40960 + 128))
+    post = _lib.make_block(_blk(norm="post"))
+    assert L.unif_moe_block_forward_workspace_size(ctypes.byref(post_wide), ctypes.byref(post),
+                                                   ctypes.byref(n)) == _lib.EUNSUPPORTED
