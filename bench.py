@@ -14,11 +14,13 @@ HIP events recorded by the library itself on the launch stream during a
 second pass over the same number of steps (unif_moe_layer_forward_profiled).
 
     python bench.py [--steps 20] [--warmup 3] [--workload vit_b16] [--no-cpu-baseline]
-                    [--no-paper-exact]
+                    [--no-paper-exact] [--no-block]
 
 Unless --no-paper-exact, a second, shorter run repeats the workload with the
 cumulative target exactly Eq. beta (t = 1) and reports it under
-"paper_exact_t1" (whole-step time only).
+"paper_exact_t1" (whole-step time only). Unless --no-block, a third repeats
+it as the pre-LN transformer block around the layer (LayerNorm, FFN biases,
+residual add; unif_moe_block_forward) and reports it under "block_pre_ln".
 """
 import argparse
 import json
@@ -40,6 +42,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-paper-exact", action="store_true",
                     help="skip the second, shorter run at cumulative target t = 1")
+    ap.add_argument("--no-block", action="store_true",
+                    help="skip the pre-LN block run")
     ap.add_argument("--cpu-sample", type=int, default=2048)
     ap.add_argument("--cpu-repeats", type=int, default=3)
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
@@ -252,6 +256,39 @@ def main():
             "activated_gemm_tflop": round(st1["activated_gemm_flops"] / 1e12, 4),
             "activated_tflops_per_s": round(st1["activated_gemm_flops"] / (ms1 / 1e3) / 1e12, 1)}
         del dev1
+    if not args.no_block:
+        # The pre-LN block (as in DeiT) around the same layer: LN(x) feeds
+        # routing and experts, b1 and b2 are added, and x is added back.
+        from synth import block_inputs
+        blk, Xb = block_inputs(g, "pre", residual=True, eps=1e-6)
+        dev.X = None
+        torch.cuda.empty_cache()
+        Xd = torch.from_numpy(Xb.view(np.int16)).view(torch.bfloat16).to(dev.device)
+        bd = dict(norm="pre", residual=True, ln_eps=float(blk["ln_eps"]))
+        for k in ("ln_gamma", "ln_beta", "b_up", "b_down"):
+            bd[k] = torch.from_numpy(blk[k]).to(dev.device)
+        wsb = _lib.alloc_workspace(_lib.block_forward_workspace_size(cfg, bd), dev.device)
+        dev.ws_forward = None
+        torch.cuda.empty_cache()
+        stepsb = max(1, args.steps // 2)
+
+        def block_step():
+            _lib.block_forward(cfg, bd, Xd, dev.valid, dev.W_router, dev.prototypes, dev.W_up,
+                               dev.W_down, dev.Y, wsb, routing=dev.routing, stream=stream)
+        for _ in range(args.warmup):
+            block_step()
+        torch.cuda.synchronize()
+        stb = dev.stats()
+        t0 = time.perf_counter()
+        for _ in range(stepsb):
+            block_step()
+        torch.cuda.synchronize()
+        msb = (time.perf_counter() - t0) / stepsb * 1e3
+        out["block_pre_ln"] = {
+            "ms_per_step": round(msb, 4), "tokens_per_s": round(stb["n_valid"] / (msb / 1e3), 1),
+            "steps": stepsb, "mean_cb": round(stb["mean_cb"], 3),
+            "over_layer_ms": round(msb - ms_per_step, 4)}
+        del Xd, wsb, bd
     if args.copy_calibration_mb > 0:
         nbytes = args.copy_calibration_mb << 20
         src = torch.ones(nbytes, dtype=torch.uint8, device=dev.device)

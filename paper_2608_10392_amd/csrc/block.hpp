@@ -40,45 +40,79 @@ struct LayerNormParams {
     double eps;
 };
 
-__device__ __forceinline__ float load_elem(const void* row, int j, bool bf16) {
-    return bf16 ? bf2f(static_cast<const u16*>(row)[j]) : static_cast<const float*>(row)[j];
-}
-
-__device__ __forceinline__ void store_elem(void* row, int j, double v, bool bf16) {
-    if (bf16) static_cast<u16*>(row)[j] = f64_to_bf16(v);
-    else static_cast<float*>(row)[j] = (float)v;
-}
-
-// mean and 1 / sqrt(var + eps) of a row read through get(j) (fp64).
-template <typename G>
-__device__ __forceinline__ void row_moments(G get, int d, double eps, double& mu, double& rstd) {
-    const int lane = lane_id();
-    double s = 0.0;
-    for (int j = lane; j < d; j += kWave) s += (double)get(j);
-    mu = wave_sum_f64(s) / d;
-    double q = 0.0;
-    for (int j = lane; j < d; j += kWave) {
-        const double c = (double)get(j) - mu;
-        q = fma(c, c, q);
+// Rows are walked in chunks: 8 bf16 (one 16-byte access) or one fp32
+// element; lane l takes chunks l, l + 64, ...
+template <bool BF16>
+struct Chunk {
+    static constexpr int E = BF16 ? 8 : 1;
+    float v[E];
+    __device__ __forceinline__ void load(const void* row, int ch) {
+        if constexpr (BF16) {
+            const u32x4 q = ld16(static_cast<const u16*>(row) + ch * 8);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                v[2 * i] = __uint_as_float(q[i] << 16);
+                v[2 * i + 1] = __uint_as_float(q[i] & 0xffff0000u);
+            }
+        } else {
+            v[0] = static_cast<const float*>(row)[ch];
+        }
     }
-    rstd = 1.0 / sqrt(wave_sum_f64(q) / d + eps);
+};
+
+template <bool BF16>
+__device__ __forceinline__ void store_chunk(void* row, int ch, const double (&y)[Chunk<BF16>::E]) {
+    if constexpr (BF16) {
+        u32x4 q;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            q[i] = (uint32_t)f64_to_bf16(y[2 * i]) | ((uint32_t)f64_to_bf16(y[2 * i + 1]) << 16);
+        st16(static_cast<u16*>(row) + ch * 8, q);
+    } else {
+        static_cast<float*>(row)[ch] = (float)y[0];
+    }
 }
 
-// Pre-LN: Xn = LN(X), one wave per row (the row is re-read from cache by
-// each pass).
+// Pre-LN: Xn = LN(X), one wave per row; the three passes (mean, variance,
+// output) re-read the row from cache.
 template <bool BF16>
 __global__ __launch_bounds__(256) void layernorm_rows_kernel(LayerNormParams p) {
-    const int t = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+    using C = Chunk<BF16>;
+    const int t = blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (t >= p.N) return;
+    const int lane = lane_id(), nch = p.d / C::E;
     const size_t esz = BF16 ? 2 : 4;
     const char* xr = static_cast<const char*>(p.X) + (size_t)t * p.d * esz;
     char* yr = static_cast<char*>(p.Xn) + (size_t)t * p.d * esz;
-    auto get = [&](int j) { return load_elem(xr, j, BF16); };
-    double mu, rstd;
-    row_moments(get, p.d, p.eps, mu, rstd);
-    for (int j = lane_id(); j < p.d; j += kWave) {
-        const double v = ((double)get(j) - mu) * rstd * (double)p.gamma[j] + (double)p.beta[j];
-        store_elem(yr, j, v, BF16);
+    double s = 0.0;
+    for (int ch = lane; ch < nch; ch += kWave) {
+        C c;
+        c.load(xr, ch);
+#pragma unroll
+        for (int e = 0; e < C::E; ++e) s += (double)c.v[e];
+    }
+    const double mu = wave_sum_f64(s) / p.d;
+    double q = 0.0;
+    for (int ch = lane; ch < nch; ch += kWave) {
+        C c;
+        c.load(xr, ch);
+#pragma unroll
+        for (int e = 0; e < C::E; ++e) {
+            const double u = (double)c.v[e] - mu;
+            q = fma(u, u, q);
+        }
+    }
+    const double rstd = 1.0 / sqrt(wave_sum_f64(q) / p.d + p.eps);
+    for (int ch = lane; ch < nch; ch += kWave) {
+        C c;
+        c.load(xr, ch);
+        double y[C::E];
+#pragma unroll
+        for (int e = 0; e < C::E; ++e) {
+            const int j = ch * C::E + e;
+            y[e] = ((double)c.v[e] - mu) * rstd * (double)p.gamma[j] + (double)p.beta[j];
+        }
+        store_chunk<BF16>(yr, ch, y);
     }
 }
 
@@ -100,18 +134,23 @@ struct BlockCombineParams {
     void* Y;
 };
 
+constexpr int kBlockCombineBatch = 4;
+
 // One wave per token. z_j = alpha E_shr^S + sum_{i <= k} p_i E_{q_i}^R
-// (the expert rows in the layer's fixed order, fp32), then the b2 shares
-// alpha (b/B) b2_shr + sum_i p_i ((B-b)/B) b2_{q_i}, then x_j. Post-LN keeps
-// z in LDS (d floats per wave) for the LayerNorm.
+// (the expert rows in the layer's fixed order, fp32; rows loaded in
+// batches), then the b2 shares alpha (b/B) b2_shr + sum_i p_i ((B-b)/B)
+// b2_{q_i}, then x_j. Post-LN keeps z in LDS (d floats per wave; each lane
+// reads back only what it wrote) for the LayerNorm.
 template <bool BF16>
 __global__ __launch_bounds__(256) void combine_block_kernel(BlockCombineParams c) {
+    using C = Chunk<BF16>;
+    constexpr int E = C::E;
     extern __shared__ float zrow_all[];
-    const int w = threadIdx.x >> 6;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int t = blockIdx.x * (blockDim.x >> 6) + w;
     if (t >= c.N) return;
     float* zrow = zrow_all + (size_t)w * c.d;
-    const int lane = lane_id();
+    const int lane = lane_id(), nch = c.d / E;
     const int k = c.nres[t];
     const int b = c.nsh[t];
     const float a = c.alpha[t];
@@ -124,39 +163,73 @@ __global__ __launch_bounds__(256) void combine_block_kernel(BlockCombineParams c
     char* yr = static_cast<char*>(c.Y) + (size_t)t * c.d * esz;
     const char* part = static_cast<const char*>(c.part);
     double s = 0.0;
-    for (int j = lane; j < c.d; j += kWave) {
-        float z = 0.f;
-        if (k > 0) {
-            for (int i = 0; i <= k; ++i) {
-                const float wi = (i == 0) ? a : wt[i - 1];
-                z = fmaf(wi, load_elem(part + (size_t)of[i] * c.d * esz, j, BF16), z);
-            }
-            if (c.b_down != nullptr) {
-                z = fmaf(a * share_s, c.b_down[j], z);
-                for (int i = 1; i <= k; ++i) z = fmaf(wt[i - 1] * share_r, c.b_down[(size_t)q[i - 1] * c.d + j], z);
+    for (int ch = lane; ch < nch; ch += kWave) {
+        float z[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) z[e] = 0.f;
+        for (int i0 = 0; i0 <= k && k > 0; i0 += kBlockCombineBatch) {
+            C r[kBlockCombineBatch];
+#pragma unroll
+            for (int u = 0; u < kBlockCombineBatch; ++u)
+                if (i0 + u <= k) r[u].load(part + (size_t)of[i0 + u] * c.d * esz, ch);
+#pragma unroll
+            for (int u = 0; u < kBlockCombineBatch; ++u) {
+                if (i0 + u <= k) {
+                    const float wi = (i0 + u == 0) ? a : wt[i0 + u - 1];
+#pragma unroll
+                    for (int e = 0; e < E; ++e) z[e] = fmaf(wi, r[u].v[e], z[e]);
+                }
             }
         }
-        if (xr != nullptr) z += load_elem(xr, j, BF16);
+        if (c.b_down != nullptr && k > 0) {
+            const float* b0 = c.b_down + ch * E;
+#pragma unroll
+            for (int e = 0; e < E; ++e) z[e] = fmaf(a * share_s, b0[e], z[e]);
+            for (int i = 1; i <= k; ++i) {
+                const float* bq = c.b_down + (size_t)q[i - 1] * c.d + ch * E;
+                const float f = wt[i - 1] * share_r;
+#pragma unroll
+                for (int e = 0; e < E; ++e) z[e] = fmaf(f, bq[e], z[e]);
+            }
+        }
+        if (xr != nullptr) {
+            C x;
+            x.load(xr, ch);
+#pragma unroll
+            for (int e = 0; e < E; ++e) z[e] += x.v[e];
+        }
         if (c.post) {
-            zrow[j] = z;
-            s += (double)z;
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                zrow[ch * E + e] = z[e];
+                s += (double)z[e];
+            }
         } else {
-            store_elem(yr, j, (double)z, BF16);
+            double y[E];
+#pragma unroll
+            for (int e = 0; e < E; ++e) y[e] = (double)z[e];
+            store_chunk<BF16>(yr, ch, y);
         }
     }
     if (!c.post) return;
-    // Each lane reads back only the entries it wrote (j = lane + 64 i), so
-    // no barrier is needed between the passes.
     const double mu = wave_sum_f64(s) / c.d;
     double sq = 0.0;
-    for (int j = lane; j < c.d; j += kWave) {
-        const double e = (double)zrow[j] - mu;
-        sq = fma(e, e, sq);
+    for (int ch = lane; ch < nch; ch += kWave) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const double u = (double)zrow[ch * E + e] - mu;
+            sq = fma(u, u, sq);
+        }
     }
     const double rstd = 1.0 / sqrt(wave_sum_f64(sq) / c.d + c.eps);
-    for (int j = lane; j < c.d; j += kWave) {
-        const double v = ((double)zrow[j] - mu) * rstd * (double)c.gamma[j] + (double)c.beta[j];
-        store_elem(yr, j, v, BF16);
+    for (int ch = lane; ch < nch; ch += kWave) {
+        double y[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int j = ch * E + e;
+            y[e] = ((double)zrow[j] - mu) * rstd * (double)c.gamma[j] + (double)c.beta[j];
+        }
+        store_chunk<BF16>(yr, ch, y);
     }
 }
 

@@ -187,9 +187,11 @@ def block_inputs(gen, norm, residual=True, biases=True, eps=1e-5):
     Returns (blk, X): ``blk`` holds norm ("none", "pre" or "post"), residual,
     ln_eps, ln_gamma [d] ~ 1 + 0.2 N(0, 1), ln_beta [d] ~ 0.1 N(0, 1),
     b_up [K+1, H] ~ 0.3 N(0, 1) and b_down [K+1, d] ~ 0.05 N(0, 1) (float32;
-    None without biases). X is the workload's tokens with a per-token scale
-    U(0.5, 2.5) and a per-feature offset 0.3 N(0, 1), in the layer's format:
-    the un-normalised residual stream that LayerNorm sees.
+    None without biases). X is the block input in the layer's format: for
+    "pre", the workload's tokens with a per-token scale U(0.5, 2.5) and a
+    per-feature offset 0.3 N(0, 1) (the un-normalised residual stream that
+    the pre-FFN LayerNorm sees); otherwise the workload's tokens as they are
+    (in a post-LN block the FFN input is the previous LayerNorm's output).
     """
     cfg = gen["cfg"]
     d, K = cfg["d_model"], cfg["n_experts"]
@@ -203,6 +205,8 @@ def block_inputs(gen, norm, residual=True, biases=True, eps=1e-5):
     if biases:
         blk["b_up"] = (0.3 * _rng(seed, 202).standard_normal((K + 1, H))).astype(np.float32)
         blk["b_down"] = (0.05 * _rng(seed, 203).standard_normal((K + 1, d))).astype(np.float32)
+    if norm != "pre":
+        return blk, gen["X"].copy()
     r = _rng(seed, 204)
     offset = 0.3 * r.standard_normal(d)
     scale = r.uniform(0.5, 2.5, size=n)
