@@ -225,9 +225,11 @@ typedef struct unif_moe_block {
     const float* ln_gamma;  /* [d] fp32 device array (required unless NONE)        */
     const float* ln_beta;   /* [d] fp32 device array (required unless NONE)        */
     const float* b_up;      /* [K+1, H] fp32 device array, row e = b1 of expert e;
-                               NULL: no up-projection bias                         */
+                               NULL: no up-projection bias. 16-byte aligned for
+                               bf16 layers                                         */
     const float* b_down;    /* [K+1, d] fp32 device array, row e = b2 of expert e;
-                               NULL: no down-projection bias                       */
+                               NULL: no down-projection bias. 16-byte aligned
+                               for bf16 layers                                     */
 } unif_moe_block;
 
 /* Workspace needed by unif_moe_block_forward (bytes). Host only. Returns
@@ -248,8 +250,9 @@ int32_t unif_moe_block_forward_workspace_size(const unif_moe_config* cfg,
  * Pre-LN: LN(x) is stored in the layer's format, as the FFN's input.
  * Requires what unif_moe_layer_forward requires, and d <= 40960 for
  * UNIF_NORM_POST (one fp32 row in LDS); otherwise UNIF_EUNSUPPORTED.
- * Errors: UNIF_EINVAL (also for a NULL blk, an unknown norm, a bad eps or a
- * missing gamma/beta), UNIF_EWORKSPACE, UNIF_EUNSUPPORTED, UNIF_EDEVICE. */
+ * Errors: UNIF_EINVAL (also for a NULL blk, an unknown norm, a bad eps, a
+ * missing gamma/beta or a misaligned bias), UNIF_EWORKSPACE,
+ * UNIF_EUNSUPPORTED, UNIF_EDEVICE. */
 int32_t unif_moe_block_forward(const unif_moe_config* cfg, const unif_moe_block* blk,
                                const void* X, const uint8_t* valid, const float* W_router,
                                const float* prototypes, const void* W_up, const void* W_down,

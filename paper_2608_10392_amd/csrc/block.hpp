@@ -13,7 +13,7 @@
 
 namespace unifmoe {
 
-// Both kernels take one row per wave and blockDim.x / 64 rows per workgroup.
+// The row kernels take one row per wave and blockDim.x / 64 rows per workgroup.
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
 #pragma unroll
@@ -73,9 +73,10 @@ __device__ __forceinline__ void store_chunk(void* row, int ch, const double (&y)
     }
 }
 
-// Pre-LN: Xn = LN(X), one wave per row; the three passes (mean, variance,
-// output) re-read the row from cache.
-template <bool BF16>
+// Pre-LN: Xn = LN(X), one wave per row. Rows of at most 64 MAXC chunks
+// stay in registers (one read); longer rows are re-read from cache by each
+// of the three passes (mean, variance, output).
+template <bool BF16, int MAXC>
 __global__ __launch_bounds__(256) void layernorm_rows_kernel(LayerNormParams p) {
     using C = Chunk<BF16>;
     const int t = blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -84,18 +85,35 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(LayerNormParams p) 
     const size_t esz = BF16 ? 2 : 4;
     const char* xr = static_cast<const char*>(p.X) + (size_t)t * p.d * esz;
     char* yr = static_cast<char*>(p.Xn) + (size_t)t * p.d * esz;
-    double s = 0.0;
-    for (int ch = lane; ch < nch; ch += kWave) {
+    const bool cached = nch <= kWave * MAXC;
+    C cache[MAXC];
+    if (cached) {
+#pragma unroll
+        for (int i = 0; i < MAXC; ++i)
+            if (lane + kWave * i < nch) cache[i].load(xr, lane + kWave * i);
+    }
+    // Chunk ch = lane + 64 i of the row, from registers or from memory.
+    auto chunk = [&](int i, int ch) {
         C c;
-        c.load(xr, ch);
+        if (cached) {
+#pragma unroll
+            for (int j = 0; j < MAXC; ++j)
+                if (j == i) c = cache[j];
+        } else {
+            c.load(xr, ch);
+        }
+        return c;
+    };
+    double s = 0.0;
+    for (int i = 0, ch = lane; ch < nch; ++i, ch += kWave) {
+        const C c = chunk(i, ch);
 #pragma unroll
         for (int e = 0; e < C::E; ++e) s += (double)c.v[e];
     }
     const double mu = wave_sum_f64(s) / p.d;
     double q = 0.0;
-    for (int ch = lane; ch < nch; ch += kWave) {
-        C c;
-        c.load(xr, ch);
+    for (int i = 0, ch = lane; ch < nch; ++i, ch += kWave) {
+        const C c = chunk(i, ch);
 #pragma unroll
         for (int e = 0; e < C::E; ++e) {
             const double u = (double)c.v[e] - mu;
@@ -103,9 +121,8 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(LayerNormParams p) 
         }
     }
     const double rstd = 1.0 / sqrt(wave_sum_f64(q) / p.d + p.eps);
-    for (int ch = lane; ch < nch; ch += kWave) {
-        C c;
-        c.load(xr, ch);
+    for (int i = 0, ch = lane; ch < nch; ++i, ch += kWave) {
+        const C c = chunk(i, ch);
         double y[C::E];
 #pragma unroll
         for (int e = 0; e < C::E; ++e) {
@@ -136,82 +153,109 @@ struct BlockCombineParams {
 
 constexpr int kBlockCombineBatch = 4;
 
-// One wave per token. z_j = alpha E_shr^S + sum_{i <= k} p_i E_{q_i}^R
-// (the expert rows in the layer's fixed order, fp32; rows loaded in
+// z over one chunk of token t's row: alpha E_shr^S + sum_{i <= k} p_i
+// E_{q_i}^R (the expert rows in the layer's fixed order, fp32, loaded in
 // batches), then the b2 shares alpha (b/B) b2_shr + sum_i p_i ((B-b)/B)
-// b2_{q_i}, then x_j. Post-LN keeps z in LDS (d floats per wave; each lane
-// reads back only what it wrote) for the LayerNorm.
+// b2_{q_i}, then x.
 template <bool BF16>
-__global__ __launch_bounds__(256) void combine_block_kernel(BlockCombineParams c) {
+__device__ __forceinline__ void block_chunk_sum(const BlockCombineParams& c, int t, int ch,
+                                                float (&z)[Chunk<BF16>::E]) {
     using C = Chunk<BF16>;
     constexpr int E = C::E;
+    const int k = c.nres[t];
+    const float a = c.alpha[t];
+    const int* of = c.pair_of + (size_t)t * (c.K + 1);
+    const float* wt = c.wts + (size_t)t * c.K;
+    const size_t esz = BF16 ? 2 : 4;
+    const char* part = static_cast<const char*>(c.part);
+#pragma unroll
+    for (int e = 0; e < E; ++e) z[e] = 0.f;
+    for (int i0 = 0; i0 <= k && k > 0; i0 += kBlockCombineBatch) {
+        C r[kBlockCombineBatch];
+#pragma unroll
+        for (int u = 0; u < kBlockCombineBatch; ++u)
+            if (i0 + u <= k) r[u].load(part + (size_t)of[i0 + u] * c.d * esz, ch);
+#pragma unroll
+        for (int u = 0; u < kBlockCombineBatch; ++u) {
+            if (i0 + u <= k) {
+                const float wi = (i0 + u == 0) ? a : wt[i0 + u - 1];
+#pragma unroll
+                for (int e = 0; e < E; ++e) z[e] = fmaf(wi, r[u].v[e], z[e]);
+            }
+        }
+    }
+    if (c.b_down != nullptr && k > 0) {
+        const int b = c.nsh[t];
+        const float share_s = (float)b / (float)c.B, share_r = (float)(c.B - b) / (float)c.B;
+        const int* q = c.eids + (size_t)t * c.K;
+        // b2 rows: E consecutive floats (16-byte aligned for bf16 layers).
+        auto add_b2 = [&](const float* row, float f) {
+            if constexpr (BF16) {
+#pragma unroll
+                for (int h = 0; h < E / 4; ++h) {
+                    const f32x4 b4 = *reinterpret_cast<const f32x4*>(row + 4 * h);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) z[4 * h + e] = fmaf(f, b4[e], z[4 * h + e]);
+                }
+            } else {
+                z[0] = fmaf(f, row[0], z[0]);
+            }
+        };
+        add_b2(c.b_down + ch * E, a * share_s);
+        for (int i = 1; i <= k; ++i) add_b2(c.b_down + (size_t)q[i - 1] * c.d + ch * E, wt[i - 1] * share_r);
+    }
+    if (c.X != nullptr) {
+        C x;
+        x.load(static_cast<const char*>(c.X) + (size_t)t * c.d * esz, ch);
+#pragma unroll
+        for (int e = 0; e < E; ++e) z[e] += x.v[e];
+    }
+}
+
+// No post-LN: one thread per chunk of the whole output (the layer's
+// combine layout).
+template <bool BF16>
+__global__ __launch_bounds__(256) void combine_block_flat_kernel(BlockCombineParams c) {
+    constexpr int E = Chunk<BF16>::E;
+    const int nch = c.d / E;
+    const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (item >= (size_t)c.N * nch) return;
+    const int t = (int)(item / nch), ch = (int)(item - (size_t)t * nch);
+    float z[E];
+    block_chunk_sum<BF16>(c, t, ch, z);
+    // One rounding from fp32 (what f64_to_bf16 gives for an fp32 value).
+    if constexpr (BF16) {
+        u32x4 o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = (uint32_t)f2bf(z[2 * i]) | ((uint32_t)f2bf(z[2 * i + 1]) << 16);
+        st16(static_cast<u16*>(c.Y) + (size_t)t * c.d + ch * 8, o);
+    } else {
+        static_cast<float*>(c.Y)[(size_t)t * c.d + ch] = z[0];
+    }
+}
+
+// Post-LN: one wave per token; z stays in LDS (d floats per wave; each lane
+// reads back only what it wrote) for the LayerNorm.
+template <bool BF16>
+__global__ __launch_bounds__(256) void combine_block_post_kernel(BlockCombineParams c) {
+    constexpr int E = Chunk<BF16>::E;
     extern __shared__ float zrow_all[];
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int t = blockIdx.x * (blockDim.x >> 6) + w;
     if (t >= c.N) return;
     float* zrow = zrow_all + (size_t)w * c.d;
     const int lane = lane_id(), nch = c.d / E;
-    const int k = c.nres[t];
-    const int b = c.nsh[t];
-    const float a = c.alpha[t];
-    const float share_s = (float)b / (float)c.B, share_r = (float)(c.B - b) / (float)c.B;
-    const int* of = c.pair_of + (size_t)t * (c.K + 1);
-    const int* q = c.eids + (size_t)t * c.K;
-    const float* wt = c.wts + (size_t)t * c.K;
-    const size_t esz = BF16 ? 2 : 4;
-    const char* xr = c.X ? static_cast<const char*>(c.X) + (size_t)t * c.d * esz : nullptr;
-    char* yr = static_cast<char*>(c.Y) + (size_t)t * c.d * esz;
-    const char* part = static_cast<const char*>(c.part);
+    char* yr = static_cast<char*>(c.Y) + (size_t)t * c.d * (BF16 ? 2 : 4);
     double s = 0.0;
     for (int ch = lane; ch < nch; ch += kWave) {
         float z[E];
+        block_chunk_sum<BF16>(c, t, ch, z);
 #pragma unroll
-        for (int e = 0; e < E; ++e) z[e] = 0.f;
-        for (int i0 = 0; i0 <= k && k > 0; i0 += kBlockCombineBatch) {
-            C r[kBlockCombineBatch];
-#pragma unroll
-            for (int u = 0; u < kBlockCombineBatch; ++u)
-                if (i0 + u <= k) r[u].load(part + (size_t)of[i0 + u] * c.d * esz, ch);
-#pragma unroll
-            for (int u = 0; u < kBlockCombineBatch; ++u) {
-                if (i0 + u <= k) {
-                    const float wi = (i0 + u == 0) ? a : wt[i0 + u - 1];
-#pragma unroll
-                    for (int e = 0; e < E; ++e) z[e] = fmaf(wi, r[u].v[e], z[e]);
-                }
-            }
-        }
-        if (c.b_down != nullptr && k > 0) {
-            const float* b0 = c.b_down + ch * E;
-#pragma unroll
-            for (int e = 0; e < E; ++e) z[e] = fmaf(a * share_s, b0[e], z[e]);
-            for (int i = 1; i <= k; ++i) {
-                const float* bq = c.b_down + (size_t)q[i - 1] * c.d + ch * E;
-                const float f = wt[i - 1] * share_r;
-#pragma unroll
-                for (int e = 0; e < E; ++e) z[e] = fmaf(f, bq[e], z[e]);
-            }
-        }
-        if (xr != nullptr) {
-            C x;
-            x.load(xr, ch);
-#pragma unroll
-            for (int e = 0; e < E; ++e) z[e] += x.v[e];
-        }
-        if (c.post) {
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                zrow[ch * E + e] = z[e];
-                s += (double)z[e];
-            }
-        } else {
-            double y[E];
-#pragma unroll
-            for (int e = 0; e < E; ++e) y[e] = (double)z[e];
-            store_chunk<BF16>(yr, ch, y);
+        for (int e = 0; e < E; ++e) {
+            zrow[ch * E + e] = z[e];
+            s += (double)z[e];
         }
     }
-    if (!c.post) return;
     const double mu = wave_sum_f64(s) / c.d;
     double sq = 0.0;
     for (int ch = lane; ch < nch; ch += kWave) {

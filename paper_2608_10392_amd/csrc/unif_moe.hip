@@ -166,8 +166,9 @@ int32_t check_block_shape(const unif_moe_config* c, const unif_moe_block* b) {
 // Pointer checks of the block forward.
 int32_t check_block_pointers(const unif_moe_config* c, const unif_moe_block* b) {
     if (b->norm != UNIF_NORM_NONE && (b->ln_gamma == nullptr || b->ln_beta == nullptr)) return UNIF_EINVAL;
-    // The bf16 up-projection reads b1 in 16-byte pieces.
-    if (c->dtype == UNIF_BF16 && b->b_up != nullptr && reinterpret_cast<uintptr_t>(b->b_up) % 16 != 0)
+    // The bf16 kernels read b1 and b2 in 16-byte pieces.
+    if (c->dtype == UNIF_BF16 && ((b->b_up != nullptr && reinterpret_cast<uintptr_t>(b->b_up) % 16 != 0) ||
+                                  (b->b_down != nullptr && reinterpret_cast<uintptr_t>(b->b_down) % 16 != 0)))
         return UNIF_EINVAL;
     return UNIF_OK;
 }
@@ -558,8 +559,9 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         ln.beta = blk->ln_beta;
         ln.eps = (double)blk->ln_eps;
         const unsigned g = (unsigned)ceil_div(m.N, 4);
-        if (m.bf16) layernorm_rows_kernel<true><<<g, 256, 0, st>>>(ln);
-        else layernorm_rows_kernel<false><<<g, 256, 0, st>>>(ln);
+        // Rows of up to 1024 bf16 (128 fp32) stay in registers.
+        if (m.bf16) layernorm_rows_kernel<true, 2><<<g, 256, 0, st>>>(ln);
+        else layernorm_rows_kernel<false, 2><<<g, 256, 0, st>>>(ln);
         UNIF_LAUNCH_CHECK();
         Xf = ln.Xn;
     }
@@ -725,17 +727,24 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         bc.beta = blk->ln_beta;
         bc.eps = (double)blk->ln_eps;
         bc.Y = Y;
-        // Post-LN keeps one fp32 row per wave in LDS: 4 rows per workgroup
-        // while that fits in 64 KB, else one.
-        const int rows = (!bc.post || (size_t)16 * m.d <= 65536) ? 4 : 1;
-        const size_t lds = bc.post ? (size_t)rows * m.d * sizeof(float) : 0;
-        const unsigned g = (unsigned)ceil_div(m.N, rows);
-        if (m.bf16) {
-            if (allow_lds(combine_block_kernel<true>, lds) != UNIF_OK) return UNIF_EDEVICE;
-            combine_block_kernel<true><<<g, 64 * rows, lds, st>>>(bc);
+        if (!bc.post) {
+            const int nch = m.bf16 ? m.d / 8 : m.d;
+            const unsigned g = (unsigned)(((size_t)m.N * nch + 255) / 256);
+            if (m.bf16) combine_block_flat_kernel<true><<<g, 256, 0, st>>>(bc);
+            else combine_block_flat_kernel<false><<<g, 256, 0, st>>>(bc);
         } else {
-            if (allow_lds(combine_block_kernel<false>, lds) != UNIF_OK) return UNIF_EDEVICE;
-            combine_block_kernel<false><<<g, 64 * rows, lds, st>>>(bc);
+            // One fp32 row per wave in LDS: 4 rows per workgroup while that
+            // fits in 64 KB, else one.
+            const int rows = ((size_t)16 * m.d <= 65536) ? 4 : 1;
+            const size_t lds = (size_t)rows * m.d * sizeof(float);
+            const unsigned g = (unsigned)ceil_div(m.N, rows);
+            if (m.bf16) {
+                if (allow_lds(combine_block_post_kernel<true>, lds) != UNIF_OK) return UNIF_EDEVICE;
+                combine_block_post_kernel<true><<<g, 64 * rows, lds, st>>>(bc);
+            } else {
+                if (allow_lds(combine_block_post_kernel<false>, lds) != UNIF_OK) return UNIF_EDEVICE;
+                combine_block_post_kernel<false><<<g, 64 * rows, lds, st>>>(bc);
+            }
         }
         UNIF_LAUNCH_CHECK();
         UNIF_MARK(5);

@@ -192,7 +192,9 @@ def test_block_calls_fail_before_touching_the_device(L):
     assert L.unif_moe_block_forward(ctypes.byref(c), ctypes.byref(bad_norm), *args) == _lib.EINVAL
     no_gamma = _lib.make_block(_blk(ln_gamma=None))
     assert L.unif_moe_block_forward(ctypes.byref(c), ctypes.byref(no_gamma), *args) == _lib.EINVAL
-    odd_bias = _lib.make_block(_blk(b_up=4))          # bf16 layers read b1 in 16-byte pieces
+    odd_bias = _lib.make_block(_blk(b_up=4))          # bf16 layers read b1 and b2 in 16-byte pieces
+    assert L.unif_moe_block_forward(ctypes.byref(c), ctypes.byref(odd_bias), *args) == _lib.EINVAL
+    odd_bias = _lib.make_block(_blk(b_down=20))
     assert L.unif_moe_block_forward(ctypes.byref(c), ctypes.byref(odd_bias), *args) == _lib.EINVAL
     no_ln = _lib.make_block(_blk(norm="none", ln_gamma=None, ln_beta=None, ln_eps=0.0))
     assert L.unif_moe_block_forward(ctypes.byref(c), ctypes.byref(no_ln), 1, None, 1, 1, 1, 1, 1, None,
