@@ -54,6 +54,10 @@ equations and converts layers of pre-LN DeiT and post-LN BERT backbones) is
     The residual add can be switched off (then y = F(..) or LN(F(x))).
   * Padded tokens have F = 0 (no biases); the rest of the block applies.
 
+The backward pass of the layer (``backward``, decisions held fixed) and the
+Gram diversity loss of Eq. diversity-loss (``diversity_loss``) are here too,
+for the training step.
+
 Parity pins: every function here is checked by tests marked "not gpu"
 against brute-force enumeration, closed forms, the textbook top-k MoE /
 dense FFN / soft MoE reductions, the mixture-mass bound of Eq.
@@ -375,6 +379,94 @@ def block_forward(cfg, blk, X, valid, W_router, prototypes, W_up, W_down, tokens
     F, rec = forward(cfg, Xin, valid, W_router, prototypes, None, None, tokens=tokens,
                      weights=W)
     return block_finish(cfg, blk, X, F), rec, Xin
+
+
+# ---------------------------------------------------------- backward pass ---
+def gelu_grad(a):
+    """d GELU / da = Phi(a) + a phi(a), float64."""
+    a = np.asarray(a, dtype=F64)
+    return 0.5 * (1.0 + _erf(a / math.sqrt(2.0))) + a * np.exp(-0.5 * a * a) / math.sqrt(2.0 * math.pi)
+
+
+def backward(cfg, X, valid, W_router, prototypes, W_up, W_down, dY, rec=None, weights=None):
+    """Gradients of sum(dY * Y) for the layer's forward (float64).
+
+    Readings (the paper does not give gradients): the discrete decisions b,
+    I_shr, the expert order q and k are held fixed (they are piecewise
+    constant); gradients flow through alpha (Eq. alpha, to W_shr and x;
+    none in fixed-alpha mode), through the affinities p_i of the selected
+    experts (the softmax of Eq. residual-router-score, to W_1..W_K and x) and
+    through the expert FFNs (Eq. block-expert-output). The prototypes mu get
+    no gradient (they only enter TopK). alpha and the softmax derivatives are
+    taken at the record's float32 values.
+
+    Returns dict(dX [N, d], dW_up [K+1, H, d], dW_down [K+1, d, H],
+    dW_router [K+1, d], dprototypes [B, d] (zeros)).
+    """
+    if rec is None:
+        rec = route(cfg, X, valid, W_router, prototypes)
+    W = weights if weights is not None else ExpertWeights(cfg, W_up, W_down)
+    N, d = X.shape
+    K, B, M = cfg["n_experts"], cfg["n_blocks"], cfg["block_width"]
+    Wr = np.asarray(W_router, dtype=F32).astype(F64)
+    dY = np.asarray(dY, dtype=F64)
+    tau = F64(shared_offset(cfg))
+    dX = np.zeros((N, d), F64)
+    dWup = np.zeros_like(W.up)
+    dWdown = np.zeros_like(W.down)
+    dWr = np.zeros_like(Wr)
+    for t in range(N):
+        if not rec["valid"][t]:
+            continue
+        x = _as_f32(X[t], cfg["dtype"]).astype(F64)
+        g = dY[t]
+        b, shared_blocks, k, q = decisions(rec, t)
+        res_blocks = [c for c in range(B) if c not in set(shared_blocks)]
+        pathways = [(0, shared_blocks, F64(rec["alpha"][t]))]
+        pathways += [(q[i], res_blocks, F64(rec["weights"][t, i])) for i in range(k)]
+        dcoef = []
+        for j, blocks, w in pathways:
+            E = np.zeros(d, F64)
+            dE = w * g                                   # gradient of the pathway output
+            for c in blocks:
+                h = slice(c * M, (c + 1) * M)
+                a = W.up[j, h] @ x
+                act = gelu(a)
+                E += W.down[j][:, h] @ act
+                dWdown[j][:, h] += np.outer(dE, act)
+                da = (W.down[j][:, h].T @ dE) * gelu_grad(a)
+                dWup[j, h] += np.outer(da, x)
+                dX[t] += W.up[j, h].T @ da
+            dcoef.append(g @ E)                          # d loss / d (pathway weight)
+        # alpha = tau + (1 - 2 tau) sigma(z0), z0 = x W_shr
+        if cfg["alpha_mode"] == "adaptive":
+            sig = 1.0 / (1.0 + math.exp(-F64(rec["z0"][t])))
+            dz0 = dcoef[0] * (1.0 - 2.0 * tau) * sig * (1.0 - sig)
+            dWr[0] += dz0 * x
+            dX[t] += dz0 * Wr[0]
+        # p_i = s_{q_i}, s = softmax(l), l_j = x W_j: ds/dl = diag(s) - s s^T
+        dp = np.zeros(K, F64)
+        for i in range(k):
+            dp[q[i] - 1] += dcoef[1 + i]
+        sv = rec["s"][t].astype(F64)
+        dl = sv * (dp - sv @ dp)
+        dWr[1:] += np.outer(dl, x)
+        dX[t] += dl @ Wr[1:]
+    return dict(dX=dX, dW_up=dWup, dW_down=dWdown, dW_router=dWr,
+                dprototypes=np.zeros((B, d), F64))
+
+
+def diversity_loss(W_router):
+    """L_div = || W* ^T W* - I_{K+1} ||_F (Eq. diversity-loss), W* = the
+    augmented router with columns W_shr, W_1..W_K (rows of W_router), and
+    its gradient with respect to W_router: (2 / L_div) (G - I) W_router with
+    G = W_router W_router^T (zero where L_div = 0). float64."""
+    Wr = np.asarray(W_router, dtype=F64)
+    G = Wr @ Wr.T
+    D = G - np.eye(Wr.shape[0])
+    L = math.sqrt(float(np.sum(D * D)))
+    grad = np.zeros_like(Wr) if L == 0.0 else (2.0 / L) * (D @ Wr)
+    return L, grad
 
 
 # ------------------------------------------------------------- margins ---

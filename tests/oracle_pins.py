@@ -565,8 +565,141 @@ def pin_block_padding(O):
         _close(Y[pad], ref, 1e-12, f"padded rows ({norm})")
 
 
+# ------------------------------------------------------ backward pass ---
+def _fixed_decision_forward(cfg, rec, X, Wr, Wup, Wdown):
+    """Layer output in float64 with the record's discrete decisions held
+    fixed and alpha, s recomputed in float64 from the parameters (pure
+    Python over channels)."""
+    N, d = X.shape
+    K, B, M = cfg["n_experts"], cfg["n_blocks"], cfg["block_width"]
+    tau = (B - 1) / (B * B) if cfg.get("tau") is None else cfg["tau"]
+    Y = np.zeros((N, d))
+    for t in range(N):
+        x = X[t]
+        z = Wr @ x
+        if cfg["alpha_mode"] == "adaptive":
+            alpha = tau + (1 - 2 * tau) / (1 + math.exp(-z[0]))
+        else:
+            alpha = cfg["alpha_fixed"]
+        s = tb_softmax(z[1:])
+        mask = int(rec["shared_mask"][t])
+        shared = [c for c in range(B) if mask >> c & 1]
+        resid = [c for c in range(B) if not mask >> c & 1]
+        paths = [(0, shared, alpha)]
+        for i in range(int(rec["n_res"][t])):
+            j = int(rec["expert_ids"][t, i])
+            paths.append((j, resid, s[j - 1]))
+        for j, blocks, w in paths:
+            for c in blocks:
+                for h in range(c * M, (c + 1) * M):
+                    Y[t] += w * gelu_tb(float(Wup[j, h] @ x)) * Wdown[j][:, h]
+    return Y
+
+
+def pin_backward_finite_differences(O):
+    """Every gradient against central differences of sum(dY * Y) with the
+    decisions fixed (float64 forward, step 1e-6)."""
+    rng = np.random.default_rng(40)
+    d, K, B, M, N = 4, 3, 4, 2, 6
+    L = random_layer(rng, N, d, K, B, M, weight_scale=0.7, logit_scale=2.0)
+    cfg = layer_cfg(d, K, B, M, mass_threshold=0.8, n_tokens=N)
+    _, rec = _forward(O, cfg, L)
+    dY = rng.standard_normal((N, d))
+    G = O.backward(cfg, L["X"], None, L["W_router"], L["prototypes"], L["W_up"], L["W_down"], dY, rec=rec)
+    P = {k: L[k].astype(np.float64) for k in ("X", "W_router", "W_up", "W_down")}
+    names = dict(X="dX", W_router="dW_router", W_up="dW_up", W_down="dW_down")
+
+    def loss():
+        return float(np.sum(dY * _fixed_decision_forward(cfg, rec, P["X"], P["W_router"], P["W_up"], P["W_down"])))
+    h = 1e-6
+    for key, gname in names.items():
+        fd = np.zeros_like(P[key])
+        for idx in np.ndindex(P[key].shape):
+            v = P[key][idx]
+            P[key][idx] = v + h
+            lp = loss()
+            P[key][idx] = v - h
+            lm = loss()
+            P[key][idx] = v
+            fd[idx] = (lp - lm) / (2 * h)
+        _close(G[gname], fd, 2e-5, f"gradient {gname}")
+        assert np.any(fd != 0), gname
+    assert np.all(G["dprototypes"] == 0)
+
+
+def pin_backward_dense_torch(O):
+    """alpha fixed at 1: the gradients of the dense FFN, from torch autograd."""
+    import torch
+    rng = np.random.default_rng(41)
+    d, K, B, M, N = 6, 3, 4, 2, 20
+    L = random_layer(rng, N, d, K, B, M, weight_scale=0.5)
+    cfg = layer_cfg(d, K, B, M, alpha_mode="fixed", alpha_fixed=1.0, n_tokens=N)
+    dY = rng.standard_normal((N, d))
+    G = O.backward(cfg, L["X"], None, L["W_router"], L["prototypes"], L["W_up"], L["W_down"], dY)
+    x = torch.tensor(L["X"], dtype=torch.float64, requires_grad=True)
+    wu = torch.tensor(L["W_up"][0], dtype=torch.float64, requires_grad=True)
+    wd = torch.tensor(L["W_down"][0], dtype=torch.float64, requires_grad=True)
+    y = torch.nn.functional.gelu(x @ wu.T) @ wd.T
+    (y * torch.tensor(dY)).sum().backward()
+    _close(G["dX"], x.grad.numpy(), 1e-10, "dense dX")
+    _close(G["dW_up"][0], wu.grad.numpy(), 1e-10, "dense dW_up")
+    _close(G["dW_down"][0], wd.grad.numpy(), 1e-10, "dense dW_down")
+    assert np.all(G["dW_up"][1:] == 0) and np.all(G["dW_router"] == 0)
+
+
+def pin_backward_soft_moe_torch(O):
+    """No shared blocks and target 1: y = sum_j s_j E_j(x) with s the softmax
+    of the router; every gradient (router included) from torch autograd."""
+    import torch
+    rng = np.random.default_rng(42)
+    d, K, B, M, N = 6, 4, 2, 3, 16
+    L = random_layer(rng, N, d, K, B, M, weight_scale=0.5)
+    cfg = layer_cfg(d, K, B, M, max_shared=0, mass_mode="fixed", mass_threshold=1.0, n_tokens=N)
+    _, rec = _forward(O, cfg, L)
+    assert np.all(rec["n_res"] == K)
+    dY = rng.standard_normal((N, d))
+    G = O.backward(cfg, L["X"], None, L["W_router"], L["prototypes"], L["W_up"], L["W_down"], dY, rec=rec)
+    x = torch.tensor(L["X"], dtype=torch.float64, requires_grad=True)
+    wr = torch.tensor(L["W_router"], dtype=torch.float64, requires_grad=True)
+    wu = torch.tensor(L["W_up"], dtype=torch.float64, requires_grad=True)
+    wd = torch.tensor(L["W_down"], dtype=torch.float64, requires_grad=True)
+    s = torch.softmax(x @ wr[1:].T, dim=1)
+    y = sum(s[:, j - 1:j] * (torch.nn.functional.gelu(x @ wu[j].T) @ wd[j].T) for j in range(1, K + 1))
+    (y * torch.tensor(dY)).sum().backward()
+    # the oracle takes the softmax derivative at the float32 affinities
+    _close(G["dX"], x.grad.numpy(), 1e-6, "soft MoE dX")
+    _close(G["dW_router"], wr.grad.numpy(), 1e-6, "soft MoE dW_router")
+    _close(G["dW_up"], wu.grad.numpy(), 1e-6, "soft MoE dW_up")
+    _close(G["dW_down"], wd.grad.numpy(), 1e-6, "soft MoE dW_down")
+
+
+def pin_diversity_loss(O):
+    """L_div vanishes at orthonormal router columns (exactly, with the zero
+    subgradient, for unit vectors); at a random router, its value and
+    gradient against torch (Frobenius norm, autograd)."""
+    import torch
+    rng = np.random.default_rng(43)
+    Q, _ = np.linalg.qr(rng.standard_normal((8, 5)))
+    assert O.diversity_loss(Q.T)[0] < 1e-12
+    L0, g0 = O.diversity_loss(np.eye(8)[:5])
+    assert L0 == 0.0 and np.all(g0 == 0)
+    # an orthogonal pair of norm 2 columns: G - I = 3 I, L = 3 sqrt(2)
+    L2, g2 = O.diversity_loss(2.0 * np.eye(4)[:2])
+    assert abs(L2 - 3.0 * math.sqrt(2.0)) < 1e-12
+    _close(g2, (2.0 / L2) * 3.0 * 2.0 * np.eye(4)[:2], 1e-12, "L_div gradient, scaled pair")
+    W = rng.standard_normal((5, 8))
+    Lv, g = O.diversity_loss(W)
+    w = torch.tensor(W, requires_grad=True)
+    lt = torch.linalg.matrix_norm(w @ w.T - torch.eye(5, dtype=torch.float64), "fro")
+    lt.backward()
+    assert abs(Lv - lt.item()) < 1e-10 * lt.item()
+    _close(g, w.grad.numpy(), 1e-10, "L_div gradient")
+
+
 ALL_PINS = [pin_hand_example, pin_gelu, pin_tau, pin_round_half_even, pin_alpha_range,
             pin_rank_order, pin_bruteforce, pin_topk_moe, pin_dense_ffn, pin_soft_moe,
             pin_identical_experts, pin_prefix_selection, pin_mass_bound, pin_padding,
             pin_stats, pin_margins, pin_layer_norm, pin_bf16_rounding, pin_block_dense,
-            pin_block_bias_split, pin_block_post_ln, pin_block_padding]
+            pin_block_bias_split, pin_block_post_ln, pin_block_padding,
+            pin_backward_finite_differences, pin_backward_dense_torch, pin_backward_soft_moe_torch,
+            pin_diversity_loss]

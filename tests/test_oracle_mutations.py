@@ -51,6 +51,15 @@ MUTANTS = {
     "bf16_truncated": ("np.rint(np.ldexp(m, 8))", "np.trunc(np.ldexp(m, 8))"),
     "pre_ln_on_output": ('if blk["norm"] == "post":', 'if blk["norm"] in ("pre", "post"):'),
     "residual_dropped": ('z = F + _as_f32(X, cfg["dtype"]).astype(F64) if blk["residual"] else F', "z = F"),
+    "gelu_grad_missing_density": ("+ a * np.exp(-0.5 * a * a) / math.sqrt(2.0 * math.pi)", "+ 0.0"),
+    "sigmoid_slope_dropped": ("dz0 = dcoef[0] * (1.0 - 2.0 * tau) * sig * (1.0 - sig)", "dz0 = dcoef[0] * sig"),
+    "softmax_jacobian_sign": ("dl = sv * (dp - sv @ dp)", "dl = sv * (dp + sv @ dp)"),
+    "router_dx_dropped": ("dX[t] += dl @ Wr[1:]", "dX[t] += 0.0 * (dl @ Wr[1:])"),
+    "dWdown_from_preactivation": ("dWdown[j][:, h] += np.outer(dE, act)", "dWdown[j][:, h] += np.outer(dE, a)"),
+    "pathway_weight_dropped": ("dE = w * g ", "dE = g "),
+    "dWup_transposed_input": ("dWup[j, h] += np.outer(da, x)", "dWup[j, h] += np.outer(da, x[::-1])"),
+    "div_grad_factor": ("(2.0 / L) * (D @ Wr)", "(1.0 / L) * (D @ Wr)"),
+    "div_squared": ("L = math.sqrt(float(np.sum(D * D)))", "L = float(np.sum(D * D))"),
 }
 
 
