@@ -6,14 +6,16 @@
 // variance over the d features. Statistics and the normalisation run in
 // fp64 (sums of d terms; the result then differs from the exact value by a
 // few fp64 ulps, so rounding it to the layer's format almost never lands on
-// the other side of a rounding midpoint). One wave per row; every lane ends
-// a butterfly reduction with the same (commutative) sums.
+// the other side of a rounding midpoint). Row sums are butterfly
+// reductions over the lanes of a row, after which every one of those lanes
+// holds the same (commutative) sums.
 #pragma once
 #include "common.hpp"
 
 namespace unifmoe {
 
-// The row kernels take one row per wave and blockDim.x / 64 rows per workgroup.
+// The post-LN merge takes one row per wave and blockDim.x / 64 rows per
+// workgroup; the LayerNorm pass takes LPR lanes per row.
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
 #pragma unroll
@@ -73,26 +75,36 @@ __device__ __forceinline__ void store_chunk(void* row, int ch, const double (&y)
     }
 }
 
-// Pre-LN: Xn = LN(X), one wave per row. Rows of at most 64 MAXC chunks
-// stay in registers (one read); longer rows are re-read from cache by each
-// of the three passes (mean, variance, output).
-template <bool BF16, int MAXC>
+// Sum over the LPR consecutive lanes that share a row (LPR a power of two
+// <= 64); every lane of the group ends with the same sum.
+template <int LPR>
+__device__ __forceinline__ double group_sum_f64(double v) {
+#pragma unroll
+    for (int o = LPR / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+// Pre-LN: Xn = LN(X), LPR lanes per row (several rows per wave, so each
+// wave keeps more loads in flight). Rows of at most LPR MAXC chunks stay in
+// registers (one read); longer rows are re-read from cache by each of the
+// three passes (mean, variance, output).
+template <bool BF16, int MAXC, int LPR>
 __global__ __launch_bounds__(256) void layernorm_rows_kernel(LayerNormParams p) {
     using C = Chunk<BF16>;
-    const int t = blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int t = (int)((blockIdx.x * blockDim.x + threadIdx.x) / LPR);
     if (t >= p.N) return;
-    const int lane = lane_id(), nch = p.d / C::E;
+    const int sub = threadIdx.x % LPR, nch = p.d / C::E;
     const size_t esz = BF16 ? 2 : 4;
     const char* xr = static_cast<const char*>(p.X) + (size_t)t * p.d * esz;
     char* yr = static_cast<char*>(p.Xn) + (size_t)t * p.d * esz;
-    const bool cached = nch <= kWave * MAXC;
+    const bool cached = nch <= LPR * MAXC;
     C cache[MAXC];
     if (cached) {
 #pragma unroll
         for (int i = 0; i < MAXC; ++i)
-            if (lane + kWave * i < nch) cache[i].load(xr, lane + kWave * i);
+            if (sub + LPR * i < nch) cache[i].load(xr, sub + LPR * i);
     }
-    // Chunk ch = lane + 64 i of the row, from registers or from memory.
+    // Chunk ch = sub + LPR i of the row, from registers or from memory.
     auto chunk = [&](int i, int ch) {
         C c;
         if (cached) {
@@ -105,14 +117,14 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(LayerNormParams p) 
         return c;
     };
     double s = 0.0;
-    for (int i = 0, ch = lane; ch < nch; ++i, ch += kWave) {
+    for (int i = 0, ch = sub; ch < nch; ++i, ch += LPR) {
         const C c = chunk(i, ch);
 #pragma unroll
         for (int e = 0; e < C::E; ++e) s += (double)c.v[e];
     }
-    const double mu = wave_sum_f64(s) / p.d;
+    const double mu = group_sum_f64<LPR>(s) / p.d;
     double q = 0.0;
-    for (int i = 0, ch = lane; ch < nch; ++i, ch += kWave) {
+    for (int i = 0, ch = sub; ch < nch; ++i, ch += LPR) {
         const C c = chunk(i, ch);
 #pragma unroll
         for (int e = 0; e < C::E; ++e) {
@@ -120,8 +132,8 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(LayerNormParams p) 
             q = fma(u, u, q);
         }
     }
-    const double rstd = 1.0 / sqrt(wave_sum_f64(q) / p.d + p.eps);
-    for (int i = 0, ch = lane; ch < nch; ++i, ch += kWave) {
+    const double rstd = 1.0 / sqrt(group_sum_f64<LPR>(q) / p.d + p.eps);
+    for (int i = 0, ch = sub; ch < nch; ++i, ch += LPR) {
         const C c = chunk(i, ch);
         double y[C::E];
 #pragma unroll

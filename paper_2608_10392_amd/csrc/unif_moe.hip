@@ -558,10 +558,11 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         ln.gamma = blk->ln_gamma;
         ln.beta = blk->ln_beta;
         ln.eps = (double)blk->ln_eps;
-        const unsigned g = (unsigned)ceil_div(m.N, 4);
-        // Rows of up to 1024 bf16 (128 fp32) stay in registers.
-        if (m.bf16) layernorm_rows_kernel<true, 2><<<g, 256, 0, st>>>(ln);
-        else layernorm_rows_kernel<false, 2><<<g, 256, 0, st>>>(ln);
+        // 16 lanes per row, 16 rows per workgroup; rows of up to 1024 bf16
+        // (128 fp32) stay in registers.
+        const unsigned g = (unsigned)ceil_div(m.N, 16);
+        if (m.bf16) layernorm_rows_kernel<true, 8, 16><<<g, 256, 0, st>>>(ln);
+        else layernorm_rows_kernel<false, 8, 16><<<g, 256, 0, st>>>(ln);
         UNIF_LAUNCH_CHECK();
         Xf = ln.Xn;
     }
