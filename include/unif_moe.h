@@ -259,6 +259,39 @@ int32_t unif_moe_block_forward(const unif_moe_config* cfg, const unif_moe_block*
                                void* Y, const unif_moe_routing* routing_out, void* workspace,
                                size_t workspace_bytes, void* stream);
 
+/* Workspace needed by unif_moe_layer_backward (bytes). Host only. It holds
+ * the forward's workspace plus fp32 per-pair intermediates sized for the
+ * worst case: 4 (2 H + d + 1) N (K+1) bytes and the forward output. */
+int32_t unif_moe_layer_backward_workspace_size(const unif_moe_config* cfg, size_t* bytes);
+
+/* Backward pass of the layer for a training step: the gradients of
+ * sum(dY * Y) with Y the output of unif_moe_layer_forward for the same
+ * arguments. The forward is recomputed inside (same kernels, so the same
+ * discrete decisions). Readings, since the paper gives no gradients: the
+ * decisions b, I_shr, the expert order q and k are held fixed (they are
+ * piecewise constant); gradients flow through alpha (Eq. alpha) to W_shr and
+ * x, through the selected affinities p_i (softmax of Eq.
+ * residual-router-score) to W_1..W_K and x, and through the expert FFNs of
+ * Eq. block-expert-output; the prototypes get none. Padded tokens get
+ * dX = 0 and contribute nothing.
+ *   dY         [N, d] (cfg->dtype)
+ *   dX         [N, d] fp32, written
+ *   dW_up      [K+1, H, d] fp32, written (layout of W_up)
+ *   dW_down    [K+1, d, H] fp32, written (layout of W_down)
+ *   dW_router  [K+1, d] fp32, written (layout of W_router)
+ * All arithmetic is fp32 (bf16 inputs are exact in fp32). A first
+ * implementation on the vector units: per-pair recompute of the activations,
+ * tiled fp32 reductions for the weight gradients. Requires what
+ * unif_moe_layer_forward requires and 4 (2 d + 2 H + 16) <= 160 KB (LDS of
+ * the per-pair kernel); otherwise UNIF_EUNSUPPORTED. Errors as
+ * unif_moe_layer_forward. The Gram diversity loss of Eq. diversity-loss is a
+ * (K+1) x (K+1) product of the router with itself and is left to the caller. */
+int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
+                                const float* W_router, const float* prototypes, const void* W_up,
+                                const void* W_down, const void* dY, float* dX, float* dW_up,
+                                float* dW_down, float* dW_router, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
 /* Workspace needed by unif_moe_stats (bytes). Host only. */
 int32_t unif_moe_stats_workspace_size(const unif_moe_config* cfg, size_t* bytes);
 

@@ -56,7 +56,8 @@ class Block(ctypes.Structure):
 EXPORTS = ("unif_moe_route_workspace_size", "unif_moe_route",
            "unif_moe_layer_forward_workspace_size", "unif_moe_layer_forward",
            "unif_moe_layer_forward_profiled", "unif_moe_block_forward_workspace_size",
-           "unif_moe_block_forward", "unif_moe_stats_workspace_size",
+           "unif_moe_block_forward", "unif_moe_layer_backward_workspace_size",
+           "unif_moe_layer_backward", "unif_moe_stats_workspace_size",
            "unif_moe_stats", "unif_moe_status_string")
 N_PHASE_EVENTS = 6
 
@@ -91,6 +92,9 @@ def lib():
                                                       ctypes.POINTER(vp), ctypes.c_int32, vp]
         L.unif_moe_stats.argtypes = [cfgp, ctypes.POINTER(Routing), vp, ctypes.POINTER(Stats),
                                      vp, sz, vp]
+        L.unif_moe_layer_backward_workspace_size.argtypes = [cfgp, ctypes.POINTER(sz)]
+        L.unif_moe_layer_backward.argtypes = [cfgp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                              vp, sz, vp]
         blkp = ctypes.POINTER(Block)
         L.unif_moe_block_forward_workspace_size.argtypes = [cfgp, blkp, ctypes.POINTER(sz)]
         L.unif_moe_block_forward.argtypes = [cfgp, blkp, vp, vp, vp, vp, vp, vp, vp,
@@ -254,6 +258,21 @@ def block_forward(cfg, blk, X, valid, W_router, prototypes, W_up, W_down, Y, wor
                                         ctypes.byref(r) if r is not None else None,
                                         _ptr(workspace), ws_bytes, _stream(stream)),
            "unif_moe_block_forward")
+
+
+def layer_backward_workspace_size(cfg):
+    return _size("unif_moe_layer_backward_workspace_size", cfg)
+
+
+def layer_backward(cfg, X, valid, W_router, prototypes, W_up, W_down, dY, dX, dW_up, dW_down,
+                   dW_router, workspace, stream=None):
+    c = make_config(cfg)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().unif_moe_layer_backward(ctypes.byref(c), _ptr(X), _ptr(valid), _ptr(W_router),
+                                         _ptr(prototypes), _ptr(W_up), _ptr(W_down), _ptr(dY),
+                                         _ptr(dX), _ptr(dW_up), _ptr(dW_down), _ptr(dW_router),
+                                         _ptr(workspace), ws_bytes, _stream(stream)),
+           "unif_moe_layer_backward")
 
 
 def stats(cfg, routing, valid, workspace, stream=None):

@@ -15,7 +15,8 @@
 //   pair_ffn_f32     per-pair fp32 FFN                            (fp32)
 //   combine          weighted merge in fixed order
 // The block forward adds a LayerNorm pass before routing (pre-LN) and
-// replaces the merge by the block's merge (biases, residual, post-LN).
+// replaces the merge by the block's merge (biases, residual, post-LN). The
+// backward runs the forward into its workspace, then the backward kernels.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -24,6 +25,7 @@
 #include <cstring>
 
 #include "../../include/unif_moe.h"
+#include "backward.hpp"
 #include "block.hpp"
 #include "combine.hpp"
 #include "common.hpp"
@@ -818,6 +820,150 @@ int32_t unif_moe_layer_forward_profiled(const unif_moe_config* cfg, const void* 
         if (events[i] == nullptr) return UNIF_EINVAL;
     return forward_impl(cfg, nullptr, X, valid, W_router, prototypes, W_up, W_down, Y, routing_out, workspace,
                         workspace_bytes, events, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Backward workspace: the forward's (record and pair tables kept), then the
+// forward output and the per-pair intermediates.
+struct BwdPlan {
+    size_t fwd, y, act, da, dcoef, dxp, dz, total;
+};
+
+BwdPlan plan_backward(const Dims& m) {
+    BwdPlan b;
+    b.fwd = plan_forward(m, true).total;   // includes its own 256 bytes of alignment slack
+    const size_t pmax = (size_t)m.N * m.K1;
+    Carver cv;
+    cv.cur = b.fwd;
+    b.y = cv.take((size_t)m.N * m.d * m.elem);
+    b.act = cv.take(pmax * m.H * sizeof(float));
+    b.da = cv.take(pmax * m.H * sizeof(float));
+    b.dcoef = cv.take(pmax * sizeof(float));
+    b.dxp = cv.take(pmax * m.d * sizeof(float));
+    b.dz = cv.take((size_t)m.N * m.K1 * sizeof(float));
+    b.total = cv.cur + 256;
+    return b;
+}
+
+size_t bwd_pair_lds(const Dims& m) { return (size_t)(2 * m.d + 2 * m.H + 16) * sizeof(float); }
+
+int32_t check_backward_shape(const unif_moe_config* c) {
+    int32_t s = check_config(c);
+    if (s != UNIF_OK) return s;
+    s = check_forward_shape(c);
+    if (s != UNIF_OK) return s;
+    if (bwd_pair_lds(dims_of(c)) > kLdsLimit) return UNIF_EUNSUPPORTED;
+    return UNIF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t unif_moe_layer_backward_workspace_size(const unif_moe_config* cfg, size_t* bytes) {
+    if (bytes == nullptr) return UNIF_EINVAL;
+    const int32_t s = check_backward_shape(cfg);
+    if (s != UNIF_OK) return s;
+    *bytes = plan_backward(dims_of(cfg)).total;
+    return UNIF_OK;
+}
+
+int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
+                                const float* W_router, const float* prototypes, const void* W_up,
+                                const void* W_down, const void* dY, float* dX, float* dW_up, float* dW_down,
+                                float* dW_router, void* workspace, size_t workspace_bytes, void* stream) {
+    int32_t s = check_backward_shape(cfg);
+    if (s != UNIF_OK) return s;
+    if (cfg->n_tokens > 0 && (X == nullptr || W_router == nullptr || prototypes == nullptr || W_up == nullptr ||
+                              W_down == nullptr || dY == nullptr || dX == nullptr))
+        return UNIF_EINVAL;
+    if (dW_up == nullptr || dW_down == nullptr || dW_router == nullptr) return UNIF_EINVAL;
+    const Dims m = dims_of(cfg);
+    const BwdPlan bp = plan_backward(m);
+    if (workspace == nullptr || workspace_bytes < bp.total) return UNIF_EWORKSPACE;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int cus = cu_count();
+    BwdParams p;
+    p.N = m.N;
+    p.d = m.d;
+    p.K = m.K;
+    p.B = m.B;
+    p.M = m.M;
+    p.H = m.H;
+    p.alpha_adaptive = cfg->alpha_mode == UNIF_ALPHA_ADAPTIVE;
+    p.tau = m.tau;
+    p.one_minus_2tau = m.one_minus_2tau;
+    p.X = X;
+    p.dY = dY;
+    p.Wup = W_up;
+    p.Wdown = W_down;
+    p.Wr = W_router;
+    p.dX = dX;
+    p.dWup = dW_up;
+    p.dWdown = dW_down;
+    p.dWr = dW_router;
+    const int tiles_h = ceil_div(m.H, 64), tiles_d = ceil_div(m.d, 64);
+    const dim3 wg_grid((unsigned)(tiles_h * tiles_d), 2, (unsigned)m.K1);
+    // 1. the forward (routing record, pair tables) into the front of the workspace
+    char* ws = align_base(workspace);
+    const FwdPlan fp = plan_forward(m, true);
+    void* Yscratch = ws + bp.y;
+    if (m.N > 0) {
+        s = forward_impl(cfg, nullptr, X, valid, W_router, prototypes, W_up, W_down, Yscratch, nullptr, ws,
+                         bp.fwd, nullptr, stream);
+        if (s != UNIF_OK) return s;
+    }
+    p.alpha = reinterpret_cast<const float*>(ws + fp.alpha);
+    p.nres = reinterpret_cast<const int*>(ws + fp.nres);
+    p.eids = reinterpret_cast<const int*>(ws + fp.eids);
+    p.wts = reinterpret_cast<const float*>(ws + fp.wts);
+    p.pair_token = reinterpret_cast<const int*>(ws + fp.pair_token);
+    p.pair_expert = reinterpret_cast<const int*>(ws + fp.pair_expert);
+    p.pair_mask = reinterpret_cast<const uint64_t*>(ws + fp.pair_mask);
+    p.pair_of = reinterpret_cast<const int*>(ws + fp.pair_of);
+    p.seg_off = reinterpret_cast<const int*>(ws + fp.seg_off);
+    p.totals = reinterpret_cast<const int*>(ws + fp.totals);
+    p.act = reinterpret_cast<float*>(ws + bp.act);
+    p.da = reinterpret_cast<float*>(ws + bp.da);
+    p.dcoef = reinterpret_cast<float*>(ws + bp.dcoef);
+    p.dxp = reinterpret_cast<float*>(ws + bp.dxp);
+    p.dz = reinterpret_cast<float*>(ws + bp.dz);
+    if (m.N == 0) {
+        // No tokens: the forward built no tables; the weight gradients are zero.
+        const size_t nw[3] = {(size_t)m.K1 * m.H * m.d, (size_t)m.K1 * m.d * m.H, (size_t)m.K1 * m.d};
+        float* const outs[3] = {dW_up, dW_down, dW_router};
+        for (int i = 0; i < 3; ++i) {
+            const unsigned g = (unsigned)std::min<size_t>((nw[i] + 255) / 256, (size_t)cus * 16);
+            fill_zero_kernel<<<g, 256, 0, st>>>(reinterpret_cast<uint32_t*>(outs[i]), nw[i]);
+            UNIF_LAUNCH_CHECK();
+        }
+        return UNIF_OK;
+    }
+    // 2. per pair, 3. per token, 4. router and expert weight gradients
+    const size_t lds = bwd_pair_lds(m);
+    if (m.bf16) {
+        if (allow_lds(bwd_pair_kernel<true>, lds) != UNIF_OK) return UNIF_EDEVICE;
+        bwd_pair_kernel<true><<<cus * 4, 256, lds, st>>>(p);
+    } else {
+        if (allow_lds(bwd_pair_kernel<false>, lds) != UNIF_OK) return UNIF_EDEVICE;
+        bwd_pair_kernel<false><<<cus * 4, 256, lds, st>>>(p);
+    }
+    UNIF_LAUNCH_CHECK();
+    bwd_token_kernel<<<(unsigned)ceil_div(m.N, 4), 256, 0, st>>>(p);
+    UNIF_LAUNCH_CHECK();
+    const unsigned rg = (unsigned)ceil_div(m.K1 * m.d, 256);
+    if (m.bf16) {
+        bwd_router_kernel<true><<<rg, 256, 0, st>>>(p);
+        bwd_wgrad_kernel<true><<<wg_grid, 256, 0, st>>>(p, tiles_h, tiles_d);
+    } else {
+        bwd_router_kernel<false><<<rg, 256, 0, st>>>(p);
+        bwd_wgrad_kernel<false><<<wg_grid, 256, 0, st>>>(p, tiles_h, tiles_d);
+    }
+    UNIF_LAUNCH_CHECK();
+    return UNIF_OK;
 }
 
 int32_t unif_moe_stats_workspace_size(const unif_moe_config* cfg, size_t* bytes) {

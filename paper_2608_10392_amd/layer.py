@@ -69,6 +69,23 @@ class DeviceLayer:
                            routing=self.routing if routing else None, stream=stream)
         return self.Y
 
+    def backward(self, dY, stream=None):
+        """Gradients of sum(dY * Y) (numpy dY in the layer's format): dict of
+        fp32 device tensors dX, dW_up, dW_down, dW_router."""
+        import torch
+        c = self.cfg
+        N, d, K = c["n_tokens"], c["d_model"], c["n_experts"]
+        H = c["n_blocks"] * c["block_width"]
+        f = dict(dtype=torch.float32, device=self.device)
+        g = dict(dX=torch.empty((N, d), **f), dW_up=torch.empty((K + 1, H, d), **f),
+                 dW_down=torch.empty((K + 1, d, H), **f), dW_router=torch.empty((K + 1, d), **f))
+        dYd = to_device(dY, c["dtype"], self.device)
+        ws = _lib.alloc_workspace(_lib.layer_backward_workspace_size(c), self.device)
+        _lib.layer_backward(c, self.X, self.valid, self.W_router, self.prototypes, self.W_up,
+                            self.W_down, dYd, g["dX"], g["dW_up"], g["dW_down"], g["dW_router"], ws,
+                            stream=stream)
+        return g
+
     def route(self, out=None, stream=None):
         if self.ws_route is None:
             self.ws_route = _lib.alloc_workspace(_lib.route_workspace_size(self.cfg), self.device)

@@ -7,9 +7,9 @@ layer's routing (router scales for two workloads) are read from
 ``calibration.json``, which ``oracle/calibrate.py`` writes.
 """
 from .configs import CONFIGS, config_names, get_config, layer_config
-from .generate import generate, block_inputs, bf16_bits_to_f32, f32_to_bf16_bits
+from .generate import generate, block_inputs, upstream_grad, bf16_bits_to_f32, f32_to_bf16_bits
 
 __all__ = [
-    "CONFIGS", "config_names", "get_config", "layer_config", "generate", "block_inputs",
+    "CONFIGS", "config_names", "get_config", "layer_config", "generate", "block_inputs", "upstream_grad",
     "bf16_bits_to_f32", "f32_to_bf16_bits",
 ]

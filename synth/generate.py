@@ -10,7 +10,7 @@ Stream tags: 0 token draws, 1 base up-projection, 2 base down-projection,
 7 bimodal token signs, 10 + e expert e's perturbation (up, then down);
 for the transformer block around the layer: 200 LayerNorm gain, 201 LayerNorm
 shift, 202 up-projection biases, 203 down-projection biases, 204 residual-
-stream scales and offsets.
+stream scales and offsets; 205 the upstream gradient dY of a training step.
 
 Values are drawn in float64. Router and prototypes are cast to float32;
 tokens and expert weights to float32 (fp32 workloads) or to bfloat16 with
@@ -212,3 +212,11 @@ def block_inputs(gen, norm, residual=True, biases=True, eps=1e-5):
     scale = r.uniform(0.5, 2.5, size=n)
     x = as_f32(gen["X"], cfg["dtype"]).astype(np.float64) * scale[:, None] + offset[None, :]
     return blk, _cast(x, cfg["dtype"])
+
+
+def upstream_grad(gen):
+    """Seeded upstream gradient dY [N, d] ~ N(0, 1) of a generated layer, in
+    the layer's format (tag 205)."""
+    cfg = gen["cfg"]
+    n, d = gen["X"].shape
+    return _cast(_rng(cfg["seed"], 205).standard_normal((n, d)), cfg["dtype"])

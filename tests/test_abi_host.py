@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 10, names
+    assert len(names) == 12, names
     assert set(names) == set(_lib.EXPORTS)
     out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True, text=True).stdout
     for n in names:
@@ -203,3 +203,20 @@ def test_block_calls_fail_before_touching_the_device(L):
     post = _lib.make_block(_blk(norm="post"))
     assert L.unif_moe_block_forward_workspace_size(ctypes.byref(post_wide), ctypes.byref(post),
                                                    ctypes.byref(n)) == _lib.EUNSUPPORTED
+
+
+def test_backward_workspace_and_validation(L):
+    c = base_cfg(n_tokens=1000)
+    N, d, K, H = 1000, 768, 16, 3072
+    ws = _lib.layer_backward_workspace_size(c)
+    assert ws >= _lib.layer_forward_workspace_size(c) + 4 * (2 * H + d + 1) * N * (K + 1)
+    cc = _lib.make_config(c)
+    big = 1 << 45
+    # NULL dY, NULL gradient outputs, small workspace: rejected before any HIP call
+    assert L.unif_moe_layer_backward(ctypes.byref(cc), 1, None, 1, 1, 1, 1, None, 1, 1, 1, 1, 1, big, None) == _lib.EINVAL
+    assert L.unif_moe_layer_backward(ctypes.byref(cc), 1, None, 1, 1, 1, 1, 1, 1, None, 1, 1, 1, big, None) == _lib.EINVAL
+    assert L.unif_moe_layer_backward(ctypes.byref(cc), 1, None, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 16, None) == _lib.EWORKSPACE
+    # the per-pair kernel keeps 2 d + 2 H floats in LDS
+    with pytest.raises(_lib.UnifMoeError) as e:
+        _lib.layer_backward_workspace_size(base_cfg(n_blocks=64, max_shared=64, block_width=256, d_model=4096))
+    assert e.value.status == _lib.EUNSUPPORTED

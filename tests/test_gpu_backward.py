@@ -1,0 +1,73 @@
+"""Parity of the backward pass (unif_moe_layer_backward) with the CPU
+oracle's backward (MI355X only).
+
+The gradients of sum(dY * Y) are compared tensor by tensor: max |g_gpu -
+g_ref| <= 1e-4 x max |g_ref| (the library computes in fp32 from inputs that
+are exact in fp32; the oracle in fp64). The decisions are held fixed, so
+tokens whose routing margin is below 1e-4 (where the two sides may take
+different decisions) are marked padded in the input; padded tokens must get
+dX = 0.
+"""
+import numpy as np
+import pytest
+
+import oracle.unif_moe_oracle as O
+from synth import generate, get_config, layer_config, upstream_grad
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+TOL = 1e-4
+
+
+def run_backward(g, label):
+    cfg = g["cfg"]
+    N = cfg["n_tokens"]
+    rec0 = O.route(cfg, g["X"], g["valid"], g["W_router"], g["prototypes"])
+    m, _ = O.margins(cfg, rec0)
+    valid = np.ones(N, np.uint8) if g["valid"] is None else g["valid"].copy()
+    valid[m < parity.MARGIN] = 0
+    dY = upstream_grad(g)
+    print(f"\n[gpu] backward {label}: N={N} ({int(valid.sum())} valid) d={cfg['d_model']} "
+          f"K={cfg['n_experts']} B={cfg['n_blocks']} M={cfg['block_width']} {cfg['dtype']}", flush=True)
+    from paper_2608_10392_amd.layer import DeviceLayer
+    dev = DeviceLayer(layer_config(cfg), g["X"], valid, g["W_router"], g["prototypes"],
+                      g["W_up"], g["W_down"])
+    got = {k: v.cpu().numpy().astype(np.float64) for k, v in dev.backward(dY).items()}
+    dYf = O._as_f32(dY, cfg["dtype"]).astype(np.float64)
+    ref = O.backward(cfg, g["X"], valid, g["W_router"], g["prototypes"], g["W_up"], g["W_down"], dYf)
+    errs = {}
+    for k in ("dX", "dW_up", "dW_down", "dW_router"):
+        scale = float(np.abs(ref[k]).max())
+        err = float(np.abs(got[k] - ref[k]).max()) / scale
+        errs[k] = err
+        assert err <= TOL, f"{k}: error {err:.2e} x max |ref| ({scale:.3e})"
+    assert np.all(got["dX"][valid == 0] == 0)
+    print(f"[gpu] backward {label}: " + ", ".join(f"{k} {v:.1e}" for k, v in errs.items())
+          + " x max |ref|", flush=True)
+    del dev
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+CASES = {
+    "bf16_m64": ("vit_s16", dict(n_tokens=300, d_model=128, n_experts=4, n_blocks=4,
+                                 block_width=64, max_shared=4)),
+    "bf16_m192": ("vit_s16", dict(n_tokens=600, d_model=384, n_experts=8, n_blocks=8,
+                                  block_width=192, max_shared=8)),
+    "bf16_fixed_alpha_top2": ("vit_s16", dict(n_tokens=300, d_model=128, n_experts=5, n_blocks=4,
+                                              block_width=64, max_shared=4, alpha_mode="fixed",
+                                              alpha_fixed=0.4, mass_mode="topk", fixed_k=2)),
+    "bf16_padded": ("bert_base_padded", dict(n_tokens=384, d_model=256, n_experts=6, n_blocks=8,
+                                             block_width=64, max_shared=8)),
+    "f32": ("tiny_f32", dict(n_tokens=200, d_model=64, n_experts=4, n_blocks=4, block_width=32,
+                             max_shared=4)),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_backward(name):
+    base, over = CASES[name]
+    run_backward(generate(get_config(base, **over)), name)
