@@ -14,13 +14,16 @@ HIP events recorded by the library itself on the launch stream during a
 second pass over the same number of steps (unif_moe_layer_forward_profiled).
 
     python bench.py [--steps 20] [--warmup 3] [--workload vit_b16] [--no-cpu-baseline]
-                    [--no-paper-exact] [--no-block]
+                    [--no-paper-exact] [--no-block] [--no-backward]
 
 Unless --no-paper-exact, a second, shorter run repeats the workload with the
 cumulative target exactly Eq. beta (t = 1) and reports it under
 "paper_exact_t1" (whole-step time only). Unless --no-block, a third repeats
 it as the pre-LN transformer block around the layer (LayerNorm, FFN biases,
 residual add; unif_moe_block_forward) and reports it under "block_pre_ln".
+Unless --no-backward, the training step's backward pass (unif_moe_layer_backward,
+a first fp32 version on the vector units) is timed on the same workload and
+reported under "backward" against the fp32 vector peak.
 """
 import argparse
 import json
@@ -30,6 +33,7 @@ import time
 
 PEAK_BF16_FLOPS = 2.5e15   # MI355X dense bf16 matrix-core peak
 PEAK_HBM_BYTES = 8.0e12    # MI355X HBM3E bandwidth
+PEAK_FP32_VECTOR = 157.3e12  # MI355X fp32 vector peak
 METRIC = "UniF-MoE layer fwd tokens/s (bf16); MFMA util of activated FLOPs vs peak"
 
 
@@ -44,6 +48,8 @@ def parse():
                     help="skip the second, shorter run at cumulative target t = 1")
     ap.add_argument("--no-block", action="store_true",
                     help="skip the pre-LN block run")
+    ap.add_argument("--no-backward", action="store_true",
+                    help="skip the backward-pass run")
     ap.add_argument("--cpu-sample", type=int, default=2048)
     ap.add_argument("--cpu-repeats", type=int, default=3)
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
@@ -289,6 +295,44 @@ def main():
             "steps": stepsb, "mean_cb": round(stb["mean_cb"], 3),
             "over_layer_ms": round(msb - ms_per_step, 4)}
         del Xd, wsb, bd
+    if not args.no_backward:
+        # Gradients of sum(dY * Y) for the layer (forward recomputed inside).
+        # Algorithmic work: four products of 2 d M per activated block (dh,
+        # dx, dW_up, dW_down), i.e. 8 d M sum(C_B).
+        from synth import upstream_grad
+        if dev.X is None:
+            dev.X = torch.from_numpy(g["X"].view(np.int16)).view(torch.bfloat16).to(dev.device)
+        dY = upstream_grad(g)
+        dYd = torch.from_numpy(dY.view(np.int16)).view(torch.bfloat16).to(dev.device)
+        N, d, K = cfg["n_tokens"], cfg["d_model"], cfg["n_experts"]
+        H = cfg["n_blocks"] * cfg["block_width"]
+        f32 = dict(dtype=torch.float32, device=dev.device)
+        gr = dict(dX=torch.empty((N, d), **f32), dW_up=torch.empty((K + 1, H, d), **f32),
+                  dW_down=torch.empty((K + 1, d, H), **f32), dW_router=torch.empty((K + 1, d), **f32))
+        wsg = _lib.alloc_workspace(_lib.layer_backward_workspace_size(cfg), dev.device)
+
+        def bwd_step():
+            _lib.layer_backward(cfg, dev.X, dev.valid, dev.W_router, dev.prototypes, dev.W_up,
+                                dev.W_down, dYd, gr["dX"], gr["dW_up"], gr["dW_down"],
+                                gr["dW_router"], wsg, stream=stream)
+        print("[bench] backward", file=sys.stderr, flush=True)
+        bwd_step()
+        torch.cuda.synchronize()
+        stepsg = 2
+        t0 = time.perf_counter()
+        for _ in range(stepsg):
+            bwd_step()
+        torch.cuda.synchronize()
+        msg = (time.perf_counter() - t0) / stepsg * 1e3
+        bflops = 8.0 * cfg["d_model"] * cfg["block_width"] * st["activated_blocks"]
+        out["backward"] = {
+            "ms_per_step": round(msg, 3), "steps": stepsg, "dtype": "f32 (bf16 inputs)",
+            "algorithmic_tflop": round(bflops / 1e12, 4),
+            "roofline": {"bound": "alu", "achieved": round(bflops / (msg / 1e3) / 1e12, 2),
+                         "peak": PEAK_FP32_VECTOR / 1e12, "unit": "TFLOP/s",
+                         "frac": round(bflops / (msg / 1e3) / PEAK_FP32_VECTOR, 4)}}
+        del wsg, gr, dYd
+        torch.cuda.empty_cache()
     if args.copy_calibration_mb > 0:
         nbytes = args.copy_calibration_mb << 20
         src = torch.ones(nbytes, dtype=torch.uint8, device=dev.device)

@@ -261,7 +261,7 @@ int32_t unif_moe_block_forward(const unif_moe_config* cfg, const unif_moe_block*
 
 /* Workspace needed by unif_moe_layer_backward (bytes). Host only. It holds
  * the forward's workspace plus fp32 per-pair intermediates sized for the
- * worst case: 4 (2 H + d + 1) N (K+1) bytes and the forward output. */
+ * worst case: 4 (2 H + d + 2) N (K+1) bytes and the forward output. */
 int32_t unif_moe_layer_backward_workspace_size(const unif_moe_config* cfg, size_t* bytes);
 
 /* Backward pass of the layer for a training step: the gradients of
@@ -280,10 +280,10 @@ int32_t unif_moe_layer_backward_workspace_size(const unif_moe_config* cfg, size_
  *   dW_down    [K+1, d, H] fp32, written (layout of W_down)
  *   dW_router  [K+1, d] fp32, written (layout of W_router)
  * All arithmetic is fp32 (bf16 inputs are exact in fp32). A first
- * implementation on the vector units: per-pair recompute of the activations,
- * tiled fp32 reductions for the weight gradients. Requires what
- * unif_moe_layer_forward requires and 4 (2 d + 2 H + 16) <= 160 KB (LDS of
- * the per-pair kernel); otherwise UNIF_EUNSUPPORTED. Errors as
+ * implementation on the vector units: tiled fp32 GEMMs over each expert's
+ * pairs (activations recomputed, dense over H and masked to the pair's
+ * blocks) and for the weight gradients. Requires what unif_moe_layer_forward
+ * requires and N <= 4,194,240; otherwise UNIF_EUNSUPPORTED. Errors as
  * unif_moe_layer_forward. The Gram diversity loss of Eq. diversity-loss is a
  * (K+1) x (K+1) product of the router with itself and is left to the caller. */
 int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const uint8_t* valid,

@@ -6,16 +6,20 @@
 // residual-router-score) to W_1..W_K and x, and through the expert FFNs of
 // Eq. block-expert-output. The prototypes get none (they only enter TopK).
 //
-// A first, plain implementation (scalar fp32 FMA, no matrix cores):
-//   bwd_pair      per (token, expert) pair: a = x K over the pair's active
-//                 channels, act = GELU(a), E = act V, dcoef = dy . E,
-//                 dE = w dy, dh = dE V^T, da = dh GELU'(a), dx_pair = da K^T
+// A first implementation on the vector units (fp32 FMA, no matrix cores),
+// as tiled fp32 GEMMs over each expert's segment of pairs (rows gathered by
+// token; dense over the H channels, masked to the pair's blocks):
+//   bwd_seg<0>    a = x K^T; act = GELU(a), gp = GELU'(a) on active channels
+//   bwd_seg<1>    E = act V^T                        (per-pair expert output)
+//   bwd_dcoef     dcoef = dy . E                     (d loss / d pair weight)
+//   bwd_seg<2>    dh = dE V, dE = w dy; da = dh gp
+//   bwd_seg<3>    dx_pair = da K
 //   bwd_token     per token: dx = sum of its pairs' dx_pair, plus the router
 //                 terms dz0 W_shr + sum_j dl_j W_j
 //   bwd_wgrad     dW_up[e] = DA_e^T X_e and dW_down[e] = dE_e^T ACT_e over
-//                 the pairs of expert e (tiled fp32 GEMMs, one 64 x 64 output
-//                 tile per workgroup)
-//   bwd_router    dW_router[j] = sum_t dz[t, j] x_t
+//                 the pairs of expert e
+//   bwd_router    dW_router[j] = sum_t dz[t, j] x_t (token slices, then
+//                 their sum)
 #pragma once
 #include "common.hpp"
 
@@ -41,10 +45,12 @@ struct BwdParams {
     const int* seg_off;       // [K+2] first pair of each expert segment
     const int* totals;        // [0]: pairs
     float* act;               // [pairs, H] GELU(a), zero on inactive channels
-    float* da;                // [pairs, H] dL/da, zero on inactive channels
+    float* da;                // [pairs, H] GELU'(a), then dL/da; zero on inactive channels
     float* dcoef;             // [pairs] dy . E_pair
-    float* dxp;               // [pairs, d]
+    float* pw;                // [pairs] pair weight (alpha or p_i)
+    float* dxp;               // [pairs, d] E_pair, then dx_pair
     float* dz;                // [N, K+1]: dz0, then dl_1..dl_K
+    float* rpart;             // [kRouterChunks, K+1, d] partial router gradients
     float* dX;                // [N, d]
     float* dWup;              // [K+1, H, d]
     float* dWdown;            // [K+1, d, H]
@@ -72,74 +78,119 @@ __device__ __forceinline__ float pair_weight(const BwdParams& p, int t, int e) {
     return 0.f;
 }
 
-__device__ __forceinline__ float block_sum(float v, float* red) {
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    __syncthreads();
-    if ((threadIdx.x & 63) == 0) red[w] = v;
-    __syncthreads();
-    float s = 0.f;
-    for (int i = 0; i < nw; ++i) s += red[i];
-    return s;
+// Pair weights: alpha for the shared expert, p_i for residual expert q_i.
+__global__ __launch_bounds__(256) void bwd_weight_kernel(BwdParams p) {
+    const int P = p.totals[0];
+    for (int pr = blockIdx.x * blockDim.x + threadIdx.x; pr < P; pr += gridDim.x * blockDim.x)
+        p.pw[pr] = pair_weight(p, p.pair_token[pr], p.pair_expert[pr]);
 }
 
-// One workgroup per pair (grid-stride). LDS: x, dE (d floats each), act and
-// da (H floats each), 16 floats for reductions.
+// dcoef[pr] = dy_{tok(pr)} . E_pr, one wave per pair.
 template <bool BF16>
-__global__ __launch_bounds__(256) void bwd_pair_kernel(BwdParams p) {
-    extern __shared__ float lds_b[];
-    float* xs = lds_b;
-    float* dEs = xs + p.d;
-    float* acts = dEs + p.d;
-    float* das = acts + p.H;
-    float* red = das + p.H;
-    const int P = p.totals[0];
-    for (int pr = blockIdx.x; pr < P; pr += gridDim.x) {
-        const int t = p.pair_token[pr], e = p.pair_expert[pr];
-        const uint64_t mask = p.pair_mask[pr];
-        const float w = pair_weight(p, t, e);
-        __syncthreads();
-        for (int n = threadIdx.x; n < p.d; n += blockDim.x) {
-            xs[n] = ld_val<BF16>(p.X, (size_t)t * p.d + n);
-            dEs[n] = w * ld_val<BF16>(p.dY, (size_t)t * p.d + n);
-        }
-        __syncthreads();
-        // Channels: a, act, dh, da.
-        for (int h = threadIdx.x; h < p.H; h += blockDim.x) {
-            float act = 0.f, dah = 0.f;
-            if ((mask >> (h / p.M)) & 1ull) {
-                const size_t urow = ((size_t)e * p.H + h) * p.d;
-                float a = 0.f;
-                for (int n = 0; n < p.d; ++n) a = fmaf(ld_val<BF16>(p.Wup, urow + n), xs[n], a);
-                act = gelu_erf(a);
-                float dh = 0.f;
-                const size_t dbase = (size_t)e * p.d * p.H + h;
-                for (int n = 0; n < p.d; ++n) dh = fmaf(ld_val<BF16>(p.Wdown, dbase + (size_t)n * p.H), dEs[n], dh);
-                dah = dh * gelu_grad_erf(a);
+__global__ __launch_bounds__(256) void bwd_dcoef_kernel(BwdParams p) {
+    const int pr = blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (pr >= p.totals[0]) return;
+    const int t = p.pair_token[pr];
+    float s = 0.f;
+    for (int n = lane_id(); n < p.d; n += kWave)
+        s = fmaf(ld_val<BF16>(p.dY, (size_t)t * p.d + n), p.dxp[(size_t)pr * p.d + n], s);
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    if (lane_id() == 0) p.dcoef[pr] = s;
+}
+
+// C[pr][col] = sum_k L(pr, k) R(k, col) over the pairs of expert e =
+// blockIdx.z, one 64 x 64 tile per workgroup (blockIdx.y: pair tile,
+// blockIdx.x: column tile; tiles past the segment exit), 16 k per LDS step,
+// 4 x 4 outputs per thread.
+//   MODE 0: L = x (k over d), R = K^T (col = channel h)      -> act, gp
+//   MODE 1: L = act (k over H), R = V^T (col = output n)      -> E
+//   MODE 2: L = w dy (k over d), R = V (col = channel h)      -> da = dh gp
+//   MODE 3: L = da (k over H), R = K (col = output n)         -> dx_pair
+template <bool BF16, int MODE>
+__global__ __launch_bounds__(256) void bwd_seg_kernel(BwdParams p) {
+    __shared__ float Ls[16][64 + 1];
+    __shared__ float Rs[16][64 + 1];
+    constexpr bool CH = (MODE == 0 || MODE == 2);   // columns are channels
+    constexpr bool KD = (MODE == 0 || MODE == 2);   // contraction over d
+    const int e = blockIdx.z;
+    const int p0 = p.seg_off[e], p1 = p.seg_off[e + 1];
+    const int r0 = p0 + (int)blockIdx.y * 64;
+    const int cols = CH ? p.H : p.d, kdim = KD ? p.d : p.H;
+    const int c0 = (int)blockIdx.x * 64;
+    if (r0 >= p1 || c0 >= cols) return;
+    const size_t wu = (size_t)e * p.H * p.d, wd = (size_t)e * p.d * p.H;
+    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+    float acc[4][4] = {};
+    for (int k0 = 0; k0 < kdim; k0 += 16) {
+        for (int i = threadIdx.x; i < 16 * 64; i += blockDim.x) {
+            // L: 64 pair rows x 16 k, consecutive threads along k.
+            {
+                const int r = i / 16, kk = i % 16, pr = r0 + r, k = k0 + kk;
+                float v = 0.f;
+                if (pr < p1 && k < kdim) {
+                    if constexpr (MODE == 0) v = ld_val<BF16>(p.X, (size_t)p.pair_token[pr] * p.d + k);
+                    else if constexpr (MODE == 1) v = p.act[(size_t)pr * p.H + k];
+                    else if constexpr (MODE == 2) v = p.pw[pr] * ld_val<BF16>(p.dY, (size_t)p.pair_token[pr] * p.d + k);
+                    else v = p.da[(size_t)pr * p.H + k];
+                }
+                Ls[kk][r] = v;
             }
-            acts[h] = act;
-            das[h] = dah;
-            p.act[(size_t)pr * p.H + h] = act;
-            p.da[(size_t)pr * p.H + h] = dah;
-        }
-        __syncthreads();
-        // Outputs: E (for dcoef) and dx_pair.
-        float dc = 0.f;
-        for (int n = threadIdx.x; n < p.d; n += blockDim.x) {
-            const size_t drow = ((size_t)e * p.d + n) * p.H;
-            float E = 0.f, dx = 0.f;
-            for (int c = 0; c < p.B; ++c) {
-                if (!((mask >> c) & 1ull)) continue;
-                for (int h = c * p.M; h < (c + 1) * p.M; ++h) {
-                    E = fmaf(ld_val<BF16>(p.Wdown, drow + h), acts[h], E);
-                    dx = fmaf(ld_val<BF16>(p.Wup, ((size_t)e * p.H + h) * p.d + n), das[h], dx);
+            // R: 16 k x 64 columns, consecutive threads along the weight's
+            // contiguous index.
+            {
+                float v = 0.f;
+                if constexpr (MODE == 0 || MODE == 1) {
+                    const int c = i / 16, kk = i % 16, col = c0 + c, k = k0 + kk;
+                    if (col < cols && k < kdim)
+                        v = MODE == 0 ? ld_val<BF16>(p.Wup, wu + (size_t)col * p.d + k)       // K_e[h = col][n = k]
+                                      : ld_val<BF16>(p.Wdown, wd + (size_t)col * p.H + k);    // V_e[n = col][h = k]
+                    Rs[kk][c] = v;
+                } else {
+                    const int kk = i / 64, c = i % 64, col = c0 + c, k = k0 + kk;
+                    if (col < cols && k < kdim)
+                        v = MODE == 2 ? ld_val<BF16>(p.Wdown, wd + (size_t)k * p.H + col)     // V_e[n = k][h = col]
+                                      : ld_val<BF16>(p.Wup, wu + (size_t)k * p.d + col);      // K_e[h = k][n = col]
+                    Rs[kk][c] = v;
                 }
             }
-            dc = fmaf(ld_val<BF16>(p.dY, (size_t)t * p.d + n), E, dc);
-            p.dxp[(size_t)pr * p.d + n] = dx;
         }
-        dc = block_sum(dc, red);
-        if (threadIdx.x == 0) p.dcoef[pr] = dc;
+        __syncthreads();
+#pragma unroll 4
+        for (int kk = 0; kk < 16; ++kk) {
+            float l[4], r[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                l[u] = Ls[kk][ty * 4 + u];
+                r[u] = Rs[kk][tx * 4 + u];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(l[u], r[v], acc[u][v]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int pr = r0 + ty * 4 + u;
+        if (pr >= p1) continue;
+        const uint64_t mask = p.pair_mask[pr];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int col = c0 + tx * 4 + v;
+            if (col >= cols) continue;
+            const float a = acc[u][v];
+            if constexpr (MODE == 0) {
+                const bool on = (mask >> (col / p.M)) & 1ull;
+                p.act[(size_t)pr * p.H + col] = on ? gelu_erf(a) : 0.f;
+                p.da[(size_t)pr * p.H + col] = on ? gelu_grad_erf(a) : 0.f;
+            } else if constexpr (MODE == 2) {
+                float* g = p.da + (size_t)pr * p.H + col;
+                *g = a * *g;
+            } else {
+                p.dxp[(size_t)pr * p.d + col] = a;
+            }
+        }
     }
 }
 
@@ -187,14 +238,29 @@ __global__ __launch_bounds__(256) void bwd_token_kernel(BwdParams p) {
     }
 }
 
-// dW_router[j][n] = sum_t dz[t][j] x_t[n]: one thread per (j, n).
+// dW_router[j][n] = sum_t dz[t][j] x_t[n] in two passes: partial sums over
+// kRouterChunks slices of the tokens (blockIdx.y), then their sum in slice
+// order. One thread per (j, n).
+constexpr int kRouterChunks = 64;
+
 template <bool BF16>
 __global__ __launch_bounds__(256) void bwd_router_kernel(BwdParams p) {
     const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (item >= (size_t)(p.K + 1) * p.d) return;
     const int j = (int)(item / p.d), n = (int)(item - (size_t)j * p.d);
+    const int c = blockIdx.y;
+    const int t0 = (int)((int64_t)c * p.N / kRouterChunks), t1 = (int)((int64_t)(c + 1) * p.N / kRouterChunks);
     float s = 0.f;
-    for (int t = 0; t < p.N; ++t) s = fmaf(p.dz[(size_t)t * (p.K + 1) + j], ld_val<BF16>(p.X, (size_t)t * p.d + n), s);
+    for (int t = t0; t < t1; ++t) s = fmaf(p.dz[(size_t)t * (p.K + 1) + j], ld_val<BF16>(p.X, (size_t)t * p.d + n), s);
+    p.rpart[(size_t)c * (p.K + 1) * p.d + item] = s;
+}
+
+__global__ __launch_bounds__(256) void bwd_router_sum_kernel(BwdParams p) {
+    const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t n = (size_t)(p.K + 1) * p.d;
+    if (item >= n) return;
+    float s = 0.f;
+    for (int c = 0; c < kRouterChunks; ++c) s += p.rpart[(size_t)c * n + item];
     p.dWr[item] = s;
 }
 
@@ -228,8 +294,7 @@ __global__ __launch_bounds__(256) void bwd_wgrad_kernel(BwdParams p, int tiles_h
                     if (r0 + x < rows) lv = p.da[(size_t)pr * p.H + r0 + x];
                     if (c0 + x < cols) rv = ld_val<BF16>(p.X, (size_t)t * p.d + c0 + x);
                 } else {
-                    const float w = pair_weight(p, t, e);
-                    if (r0 + x < rows) lv = w * ld_val<BF16>(p.dY, (size_t)t * p.d + r0 + x);
+                    if (r0 + x < rows) lv = p.pw[pr] * ld_val<BF16>(p.dY, (size_t)t * p.d + r0 + x);
                     if (c0 + x < cols) rv = p.act[(size_t)pr * p.H + c0 + x];
                 }
             }

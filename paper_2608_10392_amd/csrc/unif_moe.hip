@@ -829,7 +829,7 @@ namespace {
 // Backward workspace: the forward's (record and pair tables kept), then the
 // forward output and the per-pair intermediates.
 struct BwdPlan {
-    size_t fwd, y, act, da, dcoef, dxp, dz, total;
+    size_t fwd, y, act, da, dcoef, pw, dxp, dz, rpart, total;
 };
 
 BwdPlan plan_backward(const Dims& m) {
@@ -842,20 +842,21 @@ BwdPlan plan_backward(const Dims& m) {
     b.act = cv.take(pmax * m.H * sizeof(float));
     b.da = cv.take(pmax * m.H * sizeof(float));
     b.dcoef = cv.take(pmax * sizeof(float));
+    b.pw = cv.take(pmax * sizeof(float));
     b.dxp = cv.take(pmax * m.d * sizeof(float));
     b.dz = cv.take((size_t)m.N * m.K1 * sizeof(float));
+    b.rpart = cv.take((size_t)kRouterChunks * m.K1 * m.d * sizeof(float));
     b.total = cv.cur + 256;
     return b;
 }
-
-size_t bwd_pair_lds(const Dims& m) { return (size_t)(2 * m.d + 2 * m.H + 16) * sizeof(float); }
 
 int32_t check_backward_shape(const unif_moe_config* c) {
     int32_t s = check_config(c);
     if (s != UNIF_OK) return s;
     s = check_forward_shape(c);
     if (s != UNIF_OK) return s;
-    if (bwd_pair_lds(dims_of(c)) > kLdsLimit) return UNIF_EUNSUPPORTED;
+    // Pair tiles of an expert segment index grid dimension y.
+    if (ceil_div(c->n_tokens, 64) > 65535) return UNIF_EUNSUPPORTED;
     return UNIF_OK;
 }
 
@@ -929,6 +930,8 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
     p.act = reinterpret_cast<float*>(ws + bp.act);
     p.da = reinterpret_cast<float*>(ws + bp.da);
     p.dcoef = reinterpret_cast<float*>(ws + bp.dcoef);
+    p.pw = reinterpret_cast<float*>(ws + bp.pw);
+    p.rpart = reinterpret_cast<float*>(ws + bp.rpart);
     p.dxp = reinterpret_cast<float*>(ws + bp.dxp);
     p.dz = reinterpret_cast<float*>(ws + bp.dz);
     if (m.N == 0) {
@@ -942,26 +945,39 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
         }
         return UNIF_OK;
     }
-    // 2. per pair, 3. per token, 4. router and expert weight gradients
-    const size_t lds = bwd_pair_lds(m);
+    // 2. per pair (segment GEMMs), 3. per token, 4. router and expert weight gradients
+    const unsigned ptiles = (unsigned)ceil_div(m.N, 64);
+    const dim3 g_ch((unsigned)tiles_h, ptiles, (unsigned)m.K1), g_out((unsigned)tiles_d, ptiles, (unsigned)m.K1);
+    const unsigned gp = (unsigned)ceil_div(m.N * m.K1, 4);
+    bwd_weight_kernel<<<(unsigned)cus * 4, 256, 0, st>>>(p);
+    UNIF_LAUNCH_CHECK();
     if (m.bf16) {
-        if (allow_lds(bwd_pair_kernel<true>, lds) != UNIF_OK) return UNIF_EDEVICE;
-        bwd_pair_kernel<true><<<cus * 4, 256, lds, st>>>(p);
+        bwd_seg_kernel<true, 0><<<g_ch, 256, 0, st>>>(p);
+        bwd_seg_kernel<true, 1><<<g_out, 256, 0, st>>>(p);
+        bwd_dcoef_kernel<true><<<gp, 256, 0, st>>>(p);
+        bwd_seg_kernel<true, 2><<<g_ch, 256, 0, st>>>(p);
+        bwd_seg_kernel<true, 3><<<g_out, 256, 0, st>>>(p);
     } else {
-        if (allow_lds(bwd_pair_kernel<false>, lds) != UNIF_OK) return UNIF_EDEVICE;
-        bwd_pair_kernel<false><<<cus * 4, 256, lds, st>>>(p);
+        bwd_seg_kernel<false, 0><<<g_ch, 256, 0, st>>>(p);
+        bwd_seg_kernel<false, 1><<<g_out, 256, 0, st>>>(p);
+        bwd_dcoef_kernel<false><<<gp, 256, 0, st>>>(p);
+        bwd_seg_kernel<false, 2><<<g_ch, 256, 0, st>>>(p);
+        bwd_seg_kernel<false, 3><<<g_out, 256, 0, st>>>(p);
     }
     UNIF_LAUNCH_CHECK();
     bwd_token_kernel<<<(unsigned)ceil_div(m.N, 4), 256, 0, st>>>(p);
     UNIF_LAUNCH_CHECK();
     const unsigned rg = (unsigned)ceil_div(m.K1 * m.d, 256);
+    const dim3 rgrid(rg, kRouterChunks);
     if (m.bf16) {
-        bwd_router_kernel<true><<<rg, 256, 0, st>>>(p);
+        bwd_router_kernel<true><<<rgrid, 256, 0, st>>>(p);
         bwd_wgrad_kernel<true><<<wg_grid, 256, 0, st>>>(p, tiles_h, tiles_d);
     } else {
-        bwd_router_kernel<false><<<rg, 256, 0, st>>>(p);
+        bwd_router_kernel<false><<<rgrid, 256, 0, st>>>(p);
         bwd_wgrad_kernel<false><<<wg_grid, 256, 0, st>>>(p, tiles_h, tiles_d);
     }
+    UNIF_LAUNCH_CHECK();
+    bwd_router_sum_kernel<<<rg, 256, 0, st>>>(p);
     UNIF_LAUNCH_CHECK();
     return UNIF_OK;
 }
