@@ -283,7 +283,7 @@ int32_t unif_moe_layer_backward_workspace_size(const unif_moe_config* cfg, size_
  * implementation on the vector units: tiled fp32 GEMMs over each expert's
  * pairs (activations recomputed, dense over H and masked to the pair's
  * blocks) and for the weight gradients. Requires what unif_moe_layer_forward
- * requires and N <= 4,194,240; otherwise UNIF_EUNSUPPORTED. Errors as
+ * requires and N <= 8,388,480; otherwise UNIF_EUNSUPPORTED. Errors as
  * unif_moe_layer_forward. The Gram diversity loss of Eq. diversity-loss is a
  * (K+1) x (K+1) product of the router with itself and is left to the caller. */
 int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const uint8_t* valid,

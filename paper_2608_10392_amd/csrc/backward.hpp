@@ -98,32 +98,35 @@ __global__ __launch_bounds__(256) void bwd_dcoef_kernel(BwdParams p) {
     if (lane_id() == 0) p.dcoef[pr] = s;
 }
 
+// Output tile of the backward GEMMs: kBT x kBT per workgroup of 256
+// threads, kBU x kBU per thread, 16 k per LDS step.
+constexpr int kBT = 128, kBU = kBT / 16;
+
 // C[pr][col] = sum_k L(pr, k) R(k, col) over the pairs of expert e =
-// blockIdx.z, one 64 x 64 tile per workgroup (blockIdx.y: pair tile,
-// blockIdx.x: column tile; tiles past the segment exit), 16 k per LDS step,
-// 4 x 4 outputs per thread.
+// blockIdx.z, one kBT x kBT tile per workgroup (blockIdx.y: pair tile,
+// blockIdx.x: column tile; tiles past the segment exit).
 //   MODE 0: L = x (k over d), R = K^T (col = channel h)      -> act, gp
 //   MODE 1: L = act (k over H), R = V^T (col = output n)      -> E
 //   MODE 2: L = w dy (k over d), R = V (col = channel h)      -> da = dh gp
 //   MODE 3: L = da (k over H), R = K (col = output n)         -> dx_pair
 template <bool BF16, int MODE>
 __global__ __launch_bounds__(256) void bwd_seg_kernel(BwdParams p) {
-    __shared__ float Ls[16][64 + 1];
-    __shared__ float Rs[16][64 + 1];
+    __shared__ float Ls[16][kBT + 1];
+    __shared__ float Rs[16][kBT + 1];
     constexpr bool CH = (MODE == 0 || MODE == 2);   // columns are channels
     constexpr bool KD = (MODE == 0 || MODE == 2);   // contraction over d
     const int e = blockIdx.z;
     const int p0 = p.seg_off[e], p1 = p.seg_off[e + 1];
-    const int r0 = p0 + (int)blockIdx.y * 64;
+    const int r0 = p0 + (int)blockIdx.y * kBT;
     const int cols = CH ? p.H : p.d, kdim = KD ? p.d : p.H;
-    const int c0 = (int)blockIdx.x * 64;
+    const int c0 = (int)blockIdx.x * kBT;
     if (r0 >= p1 || c0 >= cols) return;
     const size_t wu = (size_t)e * p.H * p.d, wd = (size_t)e * p.d * p.H;
     const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-    float acc[4][4] = {};
+    float acc[kBU][kBU] = {};
     for (int k0 = 0; k0 < kdim; k0 += 16) {
-        for (int i = threadIdx.x; i < 16 * 64; i += blockDim.x) {
-            // L: 64 pair rows x 16 k, consecutive threads along k.
+        for (int i = threadIdx.x; i < 16 * kBT; i += blockDim.x) {
+            // L: kBT pair rows x 16 k, consecutive threads along k.
             {
                 const int r = i / 16, kk = i % 16, pr = r0 + r, k = k0 + kk;
                 float v = 0.f;
@@ -135,7 +138,7 @@ __global__ __launch_bounds__(256) void bwd_seg_kernel(BwdParams p) {
                 }
                 Ls[kk][r] = v;
             }
-            // R: 16 k x 64 columns, consecutive threads along the weight's
+            // R: 16 k x kBT columns, consecutive threads along the weight's
             // contiguous index.
             {
                 float v = 0.f;
@@ -146,7 +149,7 @@ __global__ __launch_bounds__(256) void bwd_seg_kernel(BwdParams p) {
                                       : ld_val<BF16>(p.Wdown, wd + (size_t)col * p.H + k);    // V_e[n = col][h = k]
                     Rs[kk][c] = v;
                 } else {
-                    const int kk = i / 64, c = i % 64, col = c0 + c, k = k0 + kk;
+                    const int kk = i / kBT, c = i % kBT, col = c0 + c, k = k0 + kk;
                     if (col < cols && k < kdim)
                         v = MODE == 2 ? ld_val<BF16>(p.Wdown, wd + (size_t)k * p.H + col)     // V_e[n = k][h = col]
                                       : ld_val<BF16>(p.Wup, wu + (size_t)k * p.d + col);      // K_e[h = k][n = col]
@@ -157,27 +160,27 @@ __global__ __launch_bounds__(256) void bwd_seg_kernel(BwdParams p) {
         __syncthreads();
 #pragma unroll 4
         for (int kk = 0; kk < 16; ++kk) {
-            float l[4], r[4];
+            float l[kBU], r[kBU];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                l[u] = Ls[kk][ty * 4 + u];
-                r[u] = Rs[kk][tx * 4 + u];
+            for (int u = 0; u < kBU; ++u) {
+                l[u] = Ls[kk][ty * kBU + u];
+                r[u] = Rs[kk][tx * kBU + u];
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < kBU; ++u)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(l[u], r[v], acc[u][v]);
+                for (int v = 0; v < kBU; ++v) acc[u][v] = fmaf(l[u], r[v], acc[u][v]);
         }
         __syncthreads();
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int pr = r0 + ty * 4 + u;
+    for (int u = 0; u < kBU; ++u) {
+        const int pr = r0 + ty * kBU + u;
         if (pr >= p1) continue;
         const uint64_t mask = p.pair_mask[pr];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int col = c0 + tx * 4 + v;
+        for (int v = 0; v < kBU; ++v) {
+            const int col = c0 + tx * kBU + v;
             if (col >= cols) continue;
             const float a = acc[u][v];
             if constexpr (MODE == 0) {
@@ -267,26 +270,26 @@ __global__ __launch_bounds__(256) void bwd_router_sum_kernel(BwdParams p) {
 // Weight gradients of expert e as two fp32 GEMMs over its pair segment:
 //   dW_up[e][h][n]   = sum_pr da[pr][h] x_{tok(pr)}[n]
 //   dW_down[e][n][h] = sum_pr w_pr dy_{tok(pr)}[n] act[pr][h]
-// blockIdx.z = e, blockIdx.y picks the product (0: up, 1: down); one 64 x 64
-// output tile per workgroup (rows: h for up, n for down), 16 pairs per LDS
-// step, 4 x 4 outputs per thread.
+// blockIdx.z = e, blockIdx.y picks the product (0: up, 1: down); one
+// kBT x kBT output tile per workgroup (rows: h for up, n for down), 16 pairs
+// per LDS step.
 template <bool BF16>
 __global__ __launch_bounds__(256) void bwd_wgrad_kernel(BwdParams p, int tiles_h, int tiles_d) {
-    __shared__ float Ls[16][64 + 1];   // pair x output-row operand
-    __shared__ float Rs[16][64 + 1];   // pair x output-column operand
+    __shared__ float Ls[16][kBT + 1];   // pair x output-row operand
+    __shared__ float Rs[16][kBT + 1];   // pair x output-column operand
     const int e = blockIdx.z, up = blockIdx.y == 0;
     const int rows = up ? p.H : p.d, cols = up ? p.d : p.H;
     const int tr = up ? tiles_h : tiles_d, tc = up ? tiles_d : tiles_h;
     const int tile = blockIdx.x;
     if (tile >= tr * tc) return;
-    const int r0 = (tile / tc) * 64, c0 = (tile % tc) * 64;
+    const int r0 = (tile / tc) * kBT, c0 = (tile % tc) * kBT;
     const int p0 = p.seg_off[e], p1 = p.seg_off[e + 1];
     const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-    float acc[4][4] = {};
+    float acc[kBU][kBU] = {};
     for (int q0 = p0; q0 < p1; q0 += 16) {
-        // Stage 16 pairs x 64 rows and 16 pairs x 64 columns.
-        for (int i = threadIdx.x; i < 16 * 64; i += blockDim.x) {
-            const int pi = i / 64, x = i % 64, pr = q0 + pi;
+        // Stage 16 pairs x kBT rows and 16 pairs x kBT columns.
+        for (int i = threadIdx.x; i < 16 * kBT; i += blockDim.x) {
+            const int pi = i / kBT, x = i % kBT, pr = q0 + pi;
             float lv = 0.f, rv = 0.f;
             if (pr < p1) {
                 const int t = p.pair_token[pr];
@@ -304,27 +307,27 @@ __global__ __launch_bounds__(256) void bwd_wgrad_kernel(BwdParams p, int tiles_h
         __syncthreads();
 #pragma unroll 4
         for (int pi = 0; pi < 16; ++pi) {
-            float l[4], r[4];
+            float l[kBU], r[kBU];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                l[u] = Ls[pi][ty * 4 + u];
-                r[u] = Rs[pi][tx * 4 + u];
+            for (int u = 0; u < kBU; ++u) {
+                l[u] = Ls[pi][ty * kBU + u];
+                r[u] = Rs[pi][tx * kBU + u];
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < kBU; ++u)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(l[u], r[v], acc[u][v]);
+                for (int v = 0; v < kBU; ++v) acc[u][v] = fmaf(l[u], r[v], acc[u][v]);
         }
         __syncthreads();
     }
     float* out = up ? p.dWup + (size_t)e * p.H * p.d : p.dWdown + (size_t)e * p.d * p.H;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int r = r0 + ty * 4 + u;
+    for (int u = 0; u < kBU; ++u) {
+        const int r = r0 + ty * kBU + u;
         if (r >= rows) continue;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int c = c0 + tx * 4 + v;
+        for (int v = 0; v < kBU; ++v) {
+            const int c = c0 + tx * kBU + v;
             if (c < cols) out[(size_t)r * cols + c] = acc[u][v];
         }
     }

@@ -856,7 +856,7 @@ int32_t check_backward_shape(const unif_moe_config* c) {
     s = check_forward_shape(c);
     if (s != UNIF_OK) return s;
     // Pair tiles of an expert segment index grid dimension y.
-    if (ceil_div(c->n_tokens, 64) > 65535) return UNIF_EUNSUPPORTED;
+    if (ceil_div(c->n_tokens, kBT) > 65535) return UNIF_EUNSUPPORTED;
     return UNIF_OK;
 }
 
@@ -906,7 +906,7 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
     p.dWup = dW_up;
     p.dWdown = dW_down;
     p.dWr = dW_router;
-    const int tiles_h = ceil_div(m.H, 64), tiles_d = ceil_div(m.d, 64);
+    const int tiles_h = ceil_div(m.H, kBT), tiles_d = ceil_div(m.d, kBT);
     const dim3 wg_grid((unsigned)(tiles_h * tiles_d), 2, (unsigned)m.K1);
     // 1. the forward (routing record, pair tables) into the front of the workspace
     char* ws = align_base(workspace);
@@ -946,7 +946,7 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
         return UNIF_OK;
     }
     // 2. per pair (segment GEMMs), 3. per token, 4. router and expert weight gradients
-    const unsigned ptiles = (unsigned)ceil_div(m.N, 64);
+    const unsigned ptiles = (unsigned)ceil_div(m.N, kBT);
     const dim3 g_ch((unsigned)tiles_h, ptiles, (unsigned)m.K1), g_out((unsigned)tiles_d, ptiles, (unsigned)m.K1);
     const unsigned gp = (unsigned)ceil_div(m.N * m.K1, 4);
     bwd_weight_kernel<<<(unsigned)cus * 4, 256, 0, st>>>(p);

@@ -216,8 +216,8 @@ def test_backward_workspace_and_validation(L):
     assert L.unif_moe_layer_backward(ctypes.byref(cc), 1, None, 1, 1, 1, 1, None, 1, 1, 1, 1, 1, big, None) == _lib.EINVAL
     assert L.unif_moe_layer_backward(ctypes.byref(cc), 1, None, 1, 1, 1, 1, 1, 1, None, 1, 1, 1, big, None) == _lib.EINVAL
     assert L.unif_moe_layer_backward(ctypes.byref(cc), 1, None, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 16, None) == _lib.EWORKSPACE
-    # pair tiles of an expert segment index grid dimension y (at most 65535 tiles of 64)
-    assert _lib.layer_backward_workspace_size(base_cfg(n_tokens=64 * 65535)) > 0
+    # pair tiles of an expert segment index grid dimension y (at most 65535 tiles of 128)
+    assert _lib.layer_backward_workspace_size(base_cfg(n_tokens=128 * 65535)) > 0
     with pytest.raises(_lib.UnifMoeError) as e:
-        _lib.layer_backward_workspace_size(base_cfg(n_tokens=64 * 65535 + 1))
+        _lib.layer_backward_workspace_size(base_cfg(n_tokens=128 * 65535 + 1))
     assert e.value.status == _lib.EUNSUPPORTED
