@@ -279,6 +279,10 @@ int32_t unif_moe_layer_backward_workspace_size(const unif_moe_config* cfg, size_
  *   dW_up      [K+1, H, d] fp32, written (layout of W_up)
  *   dW_down    [K+1, d, H] fp32, written (layout of W_down)
  *   dW_router  [K+1, d] fp32, written (layout of W_router)
+ * dX and dW_router are bitwise repeatable; dW_up and dW_down sum over each
+ * expert's pairs in the forward's permutation order, which within equal
+ * block-mask keys depends on the arrival order of atomics, so repeated calls
+ * agree to fp32 rounding.
  * All arithmetic is fp32 (bf16 inputs are exact in fp32). A first
  * implementation on the vector units: tiled fp32 GEMMs over each expert's
  * pairs (activations recomputed, dense over H and masked to the pair's
