@@ -63,6 +63,28 @@ __device__ __forceinline__ float ld_val(const void* p, size_t i) {
     else return static_cast<const float*>(p)[i];
 }
 
+// 8 consecutive values from a bf16 row (one 16-byte load) or an fp32 row
+// (two), as floats; the caller guarantees alignment (8-element chunks).
+template <bool SRC_BF16>
+__device__ __forceinline__ void ld8(const void* base, size_t i, float (&v)[8]) {
+    if constexpr (SRC_BF16) {
+        const u32x4 q = ld16(static_cast<const u16*>(base) + i);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[2 * j] = __uint_as_float(q[j] << 16);
+            v[2 * j + 1] = __uint_as_float(q[j] & 0xffff0000u);
+        }
+    } else {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(static_cast<const float*>(base) + i);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(static_cast<const float*>(base) + i + 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            v[j] = a[j];
+            v[4 + j] = b[j];
+        }
+    }
+}
+
 // d GELU / da = Phi(a) + a phi(a).
 __device__ __forceinline__ float gelu_grad_erf(float a) {
     return 0.5f * (1.0f + erff(a * 0.7071067811865475244f)) + a * 0.3989422804014327f * expf(-0.5f * a * a);
@@ -125,6 +147,57 @@ __global__ __launch_bounds__(256) void bwd_seg_kernel(BwdParams p) {
     const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
     float acc[kBU][kBU] = {};
     for (int k0 = 0; k0 < kdim; k0 += 16) {
+        if constexpr (BF16) {
+            // bf16 layers: d % 128 == 0 and H % 64 == 0, so every 8-chunk
+            // below is whole and 16-byte aligned. L: kBT rows x 2 chunks
+            // (pairs past the segment read zeros).
+            for (int i = threadIdx.x; i < kBT * 2; i += blockDim.x) {
+                const int r = i >> 1, kc = (i & 1) * 8, pr = r0 + r;
+                float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+                if (pr < p1) {
+                    if constexpr (MODE == 0) ld8<true>(p.X, (size_t)p.pair_token[pr] * p.d + k0 + kc, v);
+                    else if constexpr (MODE == 1) ld8<false>(p.act, (size_t)pr * p.H + k0 + kc, v);
+                    else if constexpr (MODE == 2) {
+                        ld8<true>(p.dY, (size_t)p.pair_token[pr] * p.d + k0 + kc, v);
+                        const float w = p.pw[pr];
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) v[j] *= w;
+                    } else {
+                        ld8<false>(p.da, (size_t)pr * p.H + k0 + kc, v);
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) Ls[kc + j][r] = v[j];
+            }
+            // R: 16 k x kBT columns, in 8-chunks along the weight's
+            // contiguous index (k for K^T and V^T, the column for V and K).
+            for (int i = threadIdx.x; i < kBT * 2; i += blockDim.x) {
+                float v[8];
+                if constexpr (MODE == 0 || MODE == 1) {
+                    const int c = i >> 1, kc = (i & 1) * 8, col = c0 + c;
+                    if (col < cols) {
+                        if constexpr (MODE == 0) ld8<true>(p.Wup, wu + (size_t)col * p.d + k0 + kc, v);
+                        else ld8<true>(p.Wdown, wd + (size_t)col * p.H + k0 + kc, v);
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) v[j] = 0.f;
+                    }
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) Rs[kc + j][c] = v[j];
+                } else {
+                    const int kk = i / (kBT / 8), c = (i % (kBT / 8)) * 8, col = c0 + c;
+                    if (col < cols) {
+                        if constexpr (MODE == 2) ld8<true>(p.Wdown, wd + (size_t)(k0 + kk) * p.H + col, v);
+                        else ld8<true>(p.Wup, wu + (size_t)(k0 + kk) * p.d + col, v);
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) v[j] = 0.f;
+                    }
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) Rs[kk][c + j] = v[j];
+                }
+            }
+        } else
         for (int i = threadIdx.x; i < 16 * kBT; i += blockDim.x) {
             // L: kBT pair rows x 16 k, consecutive threads along k.
             {
@@ -287,7 +360,35 @@ __global__ __launch_bounds__(256) void bwd_wgrad_kernel(BwdParams p, int tiles_h
     const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
     float acc[kBU][kBU] = {};
     for (int q0 = p0; q0 < p1; q0 += 16) {
-        // Stage 16 pairs x kBT rows and 16 pairs x kBT columns.
+        // Stage 16 pairs x kBT rows and 16 pairs x kBT columns (bf16 layers:
+        // 8-chunks, whole and aligned since H % 64 == 0 and d % 128 == 0).
+        if constexpr (BF16) {
+            for (int i = threadIdx.x; i < 16 * (kBT / 8); i += blockDim.x) {
+                const int pi = i / (kBT / 8), x = (i % (kBT / 8)) * 8, pr = q0 + pi;
+                float lv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+                float rv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+                if (pr < p1) {
+                    const int t = p.pair_token[pr];
+                    if (up) {
+                        if (r0 + x < rows) ld8<false>(p.da, (size_t)pr * p.H + r0 + x, lv);
+                        if (c0 + x < cols) ld8<true>(p.X, (size_t)t * p.d + c0 + x, rv);
+                    } else {
+                        if (r0 + x < rows) {
+                            ld8<true>(p.dY, (size_t)t * p.d + r0 + x, lv);
+                            const float w = p.pw[pr];
+#pragma unroll
+                            for (int j = 0; j < 8; ++j) lv[j] *= w;
+                        }
+                        if (c0 + x < cols) ld8<false>(p.act, (size_t)pr * p.H + c0 + x, rv);
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    Ls[pi][x + j] = lv[j];
+                    Rs[pi][x + j] = rv[j];
+                }
+            }
+        } else
         for (int i = threadIdx.x; i < 16 * kBT; i += blockDim.x) {
             const int pi = i / kBT, x = i % kBT, pr = q0 + pi;
             float lv = 0.f, rv = 0.f;
