@@ -157,7 +157,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the layer forward shards by tokens with no "
-              "communication, and this build runs on a single MI355X (use --gpus 1).",
+              "communication; run it with --gpus 1 (one MI355X).",
               file=sys.stderr)
         sys.exit(2)
 

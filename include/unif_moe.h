@@ -54,7 +54,7 @@ extern "C" {
 #define UNIF_EINVAL       (-1) /* invalid argument: NULL pointer, bad size/mode  */
 #define UNIF_EWORKSPACE   (-2) /* workspace smaller than the reported size       */
 #define UNIF_EDEVICE      (-3) /* a HIP launch or runtime call failed            */
-#define UNIF_EUNSUPPORTED (-4) /* valid layer this build does not implement     */
+#define UNIF_EUNSUPPORTED (-4) /* valid layer the library does not implement   */
 
 /* Element type of X, W_up, W_down and Y. */
 #define UNIF_F32  0
