@@ -85,6 +85,13 @@ __device__ __forceinline__ void ld8(const void* base, size_t i, float (&v)[8]) {
     }
 }
 
+// Blocks (bit c) that channels [h0, h1) touch, h0 < h1.
+__device__ __forceinline__ uint64_t channel_blocks(int h0, int h1, int M) {
+    const int b0 = h0 / M, b1 = (h1 - 1) / M;
+    const uint64_t hi = (b1 >= 63) ? ~0ull : ((1ull << (b1 + 1)) - 1);
+    return hi & ~((1ull << b0) - 1);
+}
+
 // d GELU / da = Phi(a) + a phi(a).
 __device__ __forceinline__ float gelu_grad_erf(float a) {
     return 0.5f * (1.0f + erff(a * 0.7071067811865475244f)) + a * 0.3989422804014327f * expf(-0.5f * a * a);
@@ -145,8 +152,41 @@ __global__ __launch_bounds__(256) void bwd_seg_kernel(BwdParams p) {
     if (r0 >= p1 || c0 >= cols) return;
     const size_t wu = (size_t)e * p.H * p.d, wd = (size_t)e * p.d * p.H;
     const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+    // Union of the block masks of the tile's pairs. Pairs are sorted by mask
+    // key, so a tile's pairs mostly agree on a block, and a block none of
+    // them runs contributes exact zeros: channel tiles of such blocks are
+    // skipped (MODE 0 writes zeros), and so are k steps inside them.
+    __shared__ uint64_t un_w[kBT / 64];
+    if (threadIdx.x < kBT) {
+        const int pr = r0 + threadIdx.x;
+        uint64_t m = pr < p1 ? p.pair_mask[pr] : 0ull;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) m |= shfl_xor64(m, o);
+        if (lane_id() == 0) un_w[threadIdx.x >> 6] = m;
+    }
+    __syncthreads();
+    uint64_t un = 0;
+#pragma unroll
+    for (int w = 0; w < kBT / 64; ++w) un |= un_w[w];
+    if constexpr (CH) {
+        if ((un & channel_blocks(c0, min(c0 + kBT, cols), p.M)) == 0) {
+            if constexpr (MODE == 0) {
+                for (int i = threadIdx.x; i < kBT * kBT; i += blockDim.x) {
+                    const int pr = r0 + i / kBT, col = c0 + i % kBT;
+                    if (pr < p1 && col < cols) {
+                        p.act[(size_t)pr * p.H + col] = 0.f;
+                        p.da[(size_t)pr * p.H + col] = 0.f;
+                    }
+                }
+            }
+            return;
+        }
+    }
     float acc[kBU][kBU] = {};
     for (int k0 = 0; k0 < kdim; k0 += 16) {
+        if constexpr (!KD) {
+            if (!((un >> (k0 / p.M)) & 1ull)) continue;   // a 16-channel step lies in one block
+        }
         if constexpr (BF16) {
             // bf16 layers: d % 128 == 0 and H % 64 == 0, so every 8-chunk
             // below is whole and 16-byte aligned. L: kBT rows x 2 chunks
@@ -358,8 +398,16 @@ __global__ __launch_bounds__(256) void bwd_wgrad_kernel(BwdParams p, int tiles_h
     const int r0 = (tile / tc) * kBT, c0 = (tile % tc) * kBT;
     const int p0 = p.seg_off[e], p1 = p.seg_off[e + 1];
     const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+    // Channel blocks of this tile (rows h for up, columns h for down): a
+    // 16-pair step whose pairs run none of them adds exact zeros and is
+    // skipped.
+    const uint64_t tmask = up ? channel_blocks(r0, min(r0 + kBT, rows), p.M)
+                              : channel_blocks(c0, min(c0 + kBT, cols), p.M);
     float acc[kBU][kBU] = {};
     for (int q0 = p0; q0 < p1; q0 += 16) {
+        uint64_t cu = 0;
+        for (int j = 0; j < 16 && q0 + j < p1; ++j) cu |= p.pair_mask[q0 + j];
+        if ((cu & tmask) == 0) continue;
         // Stage 16 pairs x kBT rows and 16 pairs x kBT columns (bf16 layers:
         // 8-chunks, whole and aligned since H % 64 == 0 and d % 128 == 0).
         if constexpr (BF16) {
