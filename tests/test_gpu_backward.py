@@ -115,3 +115,15 @@ def test_backward_full_size_properties(name):
     del dev, g1, g2
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+
+
+def test_backward_all_padded():
+    """No valid token: no pairs, and every gradient is exactly zero."""
+    g = generate(get_config("vit_s16", n_tokens=200, d_model=128, n_experts=4, n_blocks=4,
+                            block_width=64, max_shared=4))
+    from paper_2608_10392_amd.layer import DeviceLayer
+    dev = DeviceLayer(layer_config(g["cfg"]), g["X"], np.zeros(200, np.uint8), g["W_router"],
+                      g["prototypes"], g["W_up"], g["W_down"])
+    grads = dev.backward(upstream_grad(g))
+    for k, v in grads.items():
+        assert bool((v == 0).all()), k
