@@ -334,7 +334,10 @@ def to_format(v, dtype):
 def rounding_slack(v, dtype):
     """Distance (float64) of each value to the nearest point where its
     rounding to the layer's format changes (a midpoint between two
-    neighbours)."""
+    neighbours). Midpoints are taken within the value's own binade, so the
+    result is exact whenever it is below a quarter of the format's spacing
+    at the value (the only range the near-tie checks use); larger results
+    can overstate the distance to a midpoint just below a power of two."""
     v = np.asarray(v, F64)
     bits = 8 if dtype == "bf16" else 24
     m, e = np.frexp(v)

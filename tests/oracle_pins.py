@@ -123,6 +123,15 @@ def pin_gelu(O):
 def pin_tau(O):
     for B, num, den in ((2, 1, 4), (4, 3, 16), (8, 7, 64), (16, 15, 256), (32, 31, 1024)):
         assert float(O.shared_offset(dict(n_blocks=B, tau=None))) == num / den, B
+        assert float(O.shared_offset(dict(n_blocks=B, tau=float("nan")))) == num / den, B
+    # A given tau replaces (B-1)/B^2: with x W_shr = ln 3, sigma = 3/4 and
+    # alpha = tau + (1 - 2 tau) 3/4 = 0.1 + 0.8 * 0.75 = 0.7 for tau = 0.1.
+    assert O.shared_offset(dict(n_blocks=4, tau=0.1)) == np.float32(0.1)
+    L = dict(X=np.array([[1.0, 0.0]], np.float32), prototypes=np.eye(2, dtype=np.float32),
+             W_router=np.array([[math.log(3.0), 0.0], [0.0, 0.0], [0.0, 0.0]], np.float32),
+             W_up=np.zeros((3, 2, 2), np.float32), W_down=np.zeros((3, 2, 2), np.float32))
+    _, rec = _forward(O, layer_cfg(2, 2, 2, 1, tau=0.1), L)
+    assert abs(float(rec["alpha"][0]) - 0.7) < 1e-6, float(rec["alpha"][0])
 
 
 def pin_round_half_even(O):
@@ -171,6 +180,19 @@ def pin_rank_order(O):
     assert np.array_equal(r, expect)
 
 
+def pin_softmax_large_logits(O):
+    """Router logits far beyond float32's exp range (|l| ~ 300): the
+    affinities of Eq. residual-router-score stay finite and equal the
+    float64 textbook softmax."""
+    rng = np.random.default_rng(8)
+    d, K, B, M, N = 4, 5, 2, 1, 40
+    L = random_layer(rng, N, d, K, B, M, logit_scale=300.0)
+    _, rec = _forward(O, layer_cfg(d, K, B, M), L)
+    s = tb_softmax(L["X"].astype(float) @ L["W_router"][1:].astype(float).T)
+    assert np.all(np.isfinite(rec["s"]))
+    assert np.abs(rec["s"] - s).max() < 1e-5, np.abs(rec["s"] - s).max()
+
+
 def _bf_token(x, L, cfg):
     """Brute-force float64 decisions and output of one token (tiny sizes)."""
     d, K, B, M = cfg["d_model"], cfg["n_experts"], cfg["n_blocks"], cfg["block_width"]
@@ -185,7 +207,11 @@ def _bf_token(x, L, cfg):
     b = min(max(b, 1), B - 1)
     b = min(b, cfg["max_shared"])
     u = [dot(x, Mu[c]) for c in range(B)]
-    S = max(itertools.combinations(range(B), b), key=lambda s: sum(u[c] for c in s))
+    prefix = cfg.get("select_mode", "prototype") == "prefix"
+    if prefix:
+        S = tuple(range(b))
+    else:
+        S = max(itertools.combinations(range(B), b), key=lambda s: sum(u[c] for c in s))
     l = [dot(x, Wr[j]) for j in range(1, K + 1)]
     mx = max(l)
     e = [math.exp(t - mx) for t in l]
@@ -214,7 +240,8 @@ def _bf_token(x, L, cfg):
     P = list(itertools.accumulate(ss))
     fb = lambda r: min(min(max(r, 1), B - 1), cfg["max_shared"])
     marg = [abs(v - (h + 0.5)) for h in range(-1, B + 1) if fb(h) != fb(h + 1)]
-    if 0 < b < B:
+    margin_b = min(marg, default=math.inf)
+    if 0 < b < B and not prefix:
         marg.append(us[b - 1] - us[b])
     if k < K:
         marg.append(ss[k - 1] - ss[k])
@@ -224,7 +251,7 @@ def _bf_token(x, L, cfg):
     return dict(alpha=alpha, b=b, S=tuple(sorted(S)), k=k, experts=set(j + 1 for j in best),
                 order=[j + 1 for j in sorted(range(K), key=lambda j: (-s[j], j))],
                 order_gap=min([ss[i] - ss[i + 1] for i in range(K - 1)], default=1.0),
-                y=np.array(y), margin=min(marg))
+                y=np.array(y), margin=min(marg), margin_b=margin_b)
 
 
 def pin_bruteforce(O, n_layers=60, n_tok=6, seed=11):
@@ -400,6 +427,11 @@ def pin_stats(O):
     cb = b + k * (B - b)
     assert st["activated_blocks"] == cb.sum() and np.all(cb >= B)
     assert st["activated_gemm_flops"] == 4 * d * M * cb.sum()
+    for i in range(65):
+        assert st["hist_b"][i] == int(np.sum(b == i)) and st["hist_k"][i] == int(np.sum(k == i)), i
+    assert st["routing_flops"] == 2 * d * (1 + K + B) * v.sum()
+    assert abs(st["mean_b"] - b.mean()) < 1e-12 and abs(st["mean_k"] - k.mean()) < 1e-12
+    assert abs(st["mean_cb"] - cb.mean()) < 1e-12
 
 
 def pin_margins(O):
@@ -414,6 +446,120 @@ def pin_margins(O):
         for t in range(8):
             ref = _bf_token(L["X"][t], L, cfg)["margin"]
             assert abs(m[t] - ref) < 1e-5, (m[t], ref)
+
+
+def pin_margins_capped(O):
+    """Margins where the cap S_max binds below B - 1 (the breakpoints of b
+    move or vanish) and in prefix mode (no selection margin), against the
+    brute-force float64 distances; the b-margin is compared on its own."""
+    rng = np.random.default_rng(21)
+    cases = [(4, 0, "prototype"), (4, 1, "prototype"), (4, 2, "prototype"), (5, 2, "prototype"),
+             (5, 3, "prototype"), (4, 4, "prefix"), (5, 2, "prefix")]
+    for B, S_max, sel in cases:
+        for _ in range(6):
+            d, K, M = 3, 3, 1
+            cfg = layer_cfg(d, K, B, M, mass_threshold=0.8, max_shared=S_max, select_mode=sel)
+            L = random_layer(rng, 8, d, K, B, M, logit_scale=2.0)
+            L["W_router"][0] *= np.float32(3.0)       # spread alpha over the whole range
+            _, rec = _forward(O, cfg, L)
+            m, parts = O.margins(cfg, rec)
+            for t in range(8):
+                ref = _bf_token(L["X"][t], L, cfg)
+                assert abs(m[t] - ref["margin"]) < 1e-5, (B, S_max, sel, m[t], ref["margin"])
+                mb, rb = float(parts["m_b"][t]), ref["margin_b"]
+                assert (math.isinf(mb) and math.isinf(rb)) or abs(mb - rb) < 1e-5, (B, S_max, sel, mb, rb)
+                if sel == "prefix":
+                    assert math.isinf(float(parts["m_sel"][t]))
+
+
+def pin_forced_hand(O):
+    """Outputs under given decisions (the near-tie check of the parity
+    tests): cases derived by hand from Eq. output and block-expert-output
+    on the worked example (tests/golden/hand_example.json, "forced")."""
+    with open(os.path.join(GOLDEN, "hand_example.json")) as f:
+        g = json.load(f)
+    f32 = np.float32
+    cfg = dict(g["config"])
+    X = np.array(g["X"], f32)
+    L = dict(X=X, W_router=np.array(g["W_router"], f32), prototypes=np.array(g["prototypes"], f32),
+             W_up=np.array(g["W_up"], f32), W_down=np.array(g["W_down"], f32))
+    _, rec = _forward(O, cfg, L)
+    W = O.ExpertWeights(cfg, L["W_up"], L["W_down"])
+    for e in g["forced"]:
+        y = O.forced_forward(cfg, X, rec, e["token"], e["shared_blocks"], e["experts"], W)
+        assert np.allclose(y, e["y"], rtol=1e-6, atol=1e-9), ("forced", e["token"], y, e["y"])
+
+
+def _bf16_bits(v):
+    """bfloat16 bit pattern of a float that bfloat16 represents exactly."""
+    import struct
+    w = struct.unpack(">I", struct.pack(">f", v))[0]
+    assert w & 0xFFFF == 0, v
+    return w >> 16
+
+
+def pin_bf16_inputs(O):
+    """bf16 inputs: bit patterns of known value decode exactly, and a tiny
+    bf16 layer (values rounded to bf16 by exact rational rounding, passed
+    as bit patterns) matches the brute force on those values."""
+    known = [(0x3F80, 1.0), (0xBF80, -1.0), (0x4049, 3.140625), (0x3F81, 1.0 + 2.0 ** -7),
+             (0xC2F7, -123.5), (0x0080, 2.0 ** -126), (0x0001, 2.0 ** -133),
+             (0x7F7F, (2.0 - 2.0 ** -7) * 2.0 ** 127), (0x0000, 0.0), (0x3E20, 0.15625)]
+    got = O._as_f32(np.array([b for b, _ in known], np.uint16), "bf16")
+    assert got.dtype == np.float32
+    for (bits, val), gv in zip(known, got):
+        assert float(gv) == val, (hex(bits), float(gv), val)
+    rng = np.random.default_rng(22)
+    checked = 0
+    for _ in range(25):
+        d, K, B, M = 3, 3, 4, 2
+        cfg = layer_cfg(d, K, B, M, mass_threshold=0.7, dtype="bf16")
+        L = random_layer(rng, 5, d, K, B, M, logit_scale=3.0)
+        for key in ("X", "W_up", "W_down"):
+            L[key] = np.vectorize(tb_bf16, otypes=[np.float64])(L[key].astype(np.float64)).astype(np.float32)
+        Lb = dict(L)
+        for key in ("X", "W_up", "W_down"):
+            Lb[key] = np.vectorize(_bf16_bits, otypes=[np.uint16])(L[key].astype(np.float64))
+        Y, rec = _forward(O, cfg, Lb)
+        for t in range(5):
+            ref = _bf_token(L["X"][t], L, cfg)
+            if ref["margin"] < 1e-4:
+                continue
+            b, S, k, q = O.decisions(rec, t)
+            assert (b, S, k, set(q)) == (ref["b"], ref["S"], ref["k"], ref["experts"]), "bf16 decisions"
+            scale = max(1e-12, float(np.abs(ref["y"]).max()))
+            assert float(np.abs(Y[t] - ref["y"]).max()) / scale < 1e-5, "bf16 output"
+            checked += 1
+    assert checked >= 60, checked
+
+
+def pin_rounding_slack(O):
+    """Distance to the nearest rounding midpoint of the format, at values a
+    known dyadic offset from a midpoint (exact), and as a property: no
+    midpoint lies within the slack, one lies just beyond it."""
+    cases = [  # (value, format, exact slack)
+        (1.0 + 2.0 ** -8, "bf16", 0.0),
+        (1.0 + 2.0 ** -8 + 2.0 ** -30, "bf16", 2.0 ** -30),
+        (1.0 + 3 * 2.0 ** -8 - 2.0 ** -20, "bf16", 2.0 ** -20),
+        (-(3.0 + 2.0 ** -7 + 2.0 ** -25), "bf16", 2.0 ** -25),
+        (2.0 ** -100 * (1.0 + 2.0 ** -8) + 2.0 ** -131, "bf16", 2.0 ** -131),
+        (1.5 + 2.0 ** -24, "f32", 0.0),
+        (1.0 + 2.0 ** -24 + 2.0 ** -50, "f32", 2.0 ** -50),
+        (-(7.0 + 2.0 ** -22 - 2.0 ** -45), "f32", 2.0 ** -45),
+    ]
+    for v, fmt, want in cases:
+        got = float(O.rounding_slack(np.array([v]), fmt)[0])
+        assert got == want, (v, fmt, got, want)
+    rng = np.random.default_rng(23)
+    vals = rng.standard_normal(400) * 10.0 ** rng.integers(-5, 5, 400)
+    for fmt, rel in (("bf16", 2.0 ** -8), ("f32", 2.0 ** -24)):
+        sl = O.rounding_slack(vals, fmt)
+        for v, dlt in zip(vals, sl):
+            if not (0 < dlt < abs(v) * rel / 4):
+                continue
+            r = lambda z: O.to_format(np.array([z]), fmt)[0]
+            assert r(v - 0.5 * dlt) == r(v + 0.5 * dlt), (fmt, v, dlt)
+            assert r(v - 1.5 * dlt) != r(v + 1.5 * dlt), (fmt, v, dlt)
 
 
 # ------------------------------------------------ the block around it ---
@@ -510,6 +656,22 @@ def pin_block_dense(O):
     ref = L["X"].astype(float) + _gelu_vec(a) @ L["W_down"][0].astype(float).T + blk["b_down"][0]
     _close(Y, ref, 1e-9, "pre-LN dense block")
     assert np.array_equal(Xin, xn)
+
+
+def pin_block_pre_ln_bf16(O):
+    """bf16 pre-LN block: the FFN input is LN(x) rounded once to bf16
+    (exact rational rounding of the plain-Python LayerNorm)."""
+    rng = np.random.default_rng(36)
+    d, K, B, M, N = 6, 3, 4, 2, 12
+    cfg = layer_cfg(d, K, B, M, dtype="bf16", n_tokens=N)
+    x = (3.0 * rng.standard_normal((N, d)) + 1.0)
+    xr = np.vectorize(tb_bf16, otypes=[np.float64])(x)
+    Xb = np.vectorize(_bf16_bits, otypes=[np.uint16])(xr)
+    blk = _block(d, K, B, M, rng, "pre", True)
+    got = O.block_input(cfg, blk, Xb)
+    ref = tb_layer_norm(xr, blk["ln_gamma"], blk["ln_beta"], blk["ln_eps"])
+    want = np.vectorize(lambda v: _bf16_bits(tb_bf16(v)), otypes=[np.uint16])(ref)
+    assert got.dtype == np.uint16 and np.array_equal(got, want)
 
 
 def pin_block_bias_split(O):
@@ -697,9 +859,10 @@ def pin_diversity_loss(O):
 
 
 ALL_PINS = [pin_hand_example, pin_gelu, pin_tau, pin_round_half_even, pin_alpha_range,
-            pin_rank_order, pin_bruteforce, pin_topk_moe, pin_dense_ffn, pin_soft_moe,
+            pin_rank_order, pin_softmax_large_logits, pin_bruteforce, pin_topk_moe, pin_dense_ffn, pin_soft_moe,
             pin_identical_experts, pin_prefix_selection, pin_mass_bound, pin_padding,
-            pin_stats, pin_margins, pin_layer_norm, pin_bf16_rounding, pin_block_dense,
-            pin_block_bias_split, pin_block_post_ln, pin_block_padding,
+            pin_stats, pin_margins, pin_margins_capped, pin_forced_hand, pin_bf16_inputs,
+            pin_rounding_slack, pin_layer_norm, pin_bf16_rounding, pin_block_dense,
+            pin_block_pre_ln_bf16, pin_block_bias_split, pin_block_post_ln, pin_block_padding,
             pin_backward_finite_differences, pin_backward_dense_torch, pin_backward_soft_moe_torch,
             pin_diversity_loss]

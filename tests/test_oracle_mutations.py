@@ -60,6 +60,17 @@ MUTANTS = {
     "dWup_transposed_input": ("dWup[j, h] += np.outer(da, x)", "dWup[j, h] += np.outer(da, x[::-1])"),
     "div_grad_factor": ("(2.0 / L) * (D @ Wr)", "(1.0 / L) * (D @ Wr)"),
     "div_squared": ("L = math.sqrt(float(np.sum(D * D)))", "L = float(np.sum(D * D))"),
+    "forced_weight_lookup": ('residual = [(j, rec["s"][t, j - 1]) for j in experts]',
+                             'residual = [(j, rec["s"][t, j % rec["s"].shape[1]]) for j in experts]'),
+    "bf16_decode_shift": ("(a.astype(np.uint32) << 16)", "(a.astype(np.uint32) << 15)"),
+    "slack_bf16_7_bits": ('bits = 8 if dtype == "bf16" else 24', 'bits = 7 if dtype == "bf16" else 24'),
+    "margins_cap_ignored": ('return min(bb, cfg["max_shared"])', "return bb"),
+    "stats_hist_k_from_b": ("hist_k = np.bincount(k, minlength=65)[:65]", "hist_k = np.bincount(b, minlength=65)[:65]"),
+    "routing_flops_no_shr": ("routing_flops=2.0 * d * (1 + K + B) * nv", "routing_flops=2.0 * d * (K + B) * nv"),
+    "softmax_min_shift": ("e = np.exp(l - l.max(axis=1, keepdims=True))", "e = np.exp(l - l.min(axis=1, keepdims=True))"),
+    "tau_ignored": ("    return F32(t)\n", "    return F32((B - 1) / (B * B))\n"),
+    "pre_ln_input_unrounded": ('return to_format(layer_norm(x, blk["ln_gamma"], blk["ln_beta"], blk["ln_eps"]), cfg["dtype"])',
+                               'return layer_norm(x, blk["ln_gamma"], blk["ln_beta"], blk["ln_eps"]).astype(F32)'),
 }
 
 
