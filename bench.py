@@ -69,7 +69,7 @@ def phase_bytes(cfg, st):
     permute = (N * (8 + 4) + sum_k * 4                               # read mask, k, q_1..q_k
                + pairs * (4 + 8 + 4 + 4)                             # pair token/mask/expert, pair_of
                + pairs * (4 + 8) + sum_cb * 4)                       # slab lists: read pairs, write rows
-    combine = pairs * d * es + pairs * 8 + N * 4 + N * d * es        # per-expert rows, weights, Y
+    combine = pairs * d * 4 + pairs * 8 + N * 4 + N * d * es         # fp32 per-expert rows, weights, Y
     return dict(routing=routing, permute=permute, combine=combine)
 
 
@@ -189,7 +189,7 @@ def main():
     ms_per_step = wall / args.steps * 1e3
 
     # Same steps again through the instrumented entry point: the library
-    # records six events per step on the launch stream.
+    # records seven events per step on the launch stream.
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(_lib.N_PHASE_EVENTS)]
               for _ in range(args.steps)]
     for evs in events:
@@ -203,7 +203,7 @@ def main():
                                     stream=stream)
     torch.cuda.synchronize()
     wall_prof = time.perf_counter() - t0
-    names = ["routing", "permute", "up_gemm", "down_gemm", "combine"]
+    names = ["wdown_f16", "routing", "permute", "up_gemm", "down_gemm", "combine"]
     phase_ms = {n: float(np.mean([evs[i].elapsed_time(evs[i + 1]) for evs in events]))
                 for i, n in enumerate(names)}
 

@@ -167,10 +167,15 @@ int32_t unif_moe_layer_forward_workspace_size(const unif_moe_config* cfg, size_t
  *          linear layer)
  *   Y      [N, d] (cfg->dtype), written for every row (zero for padded rows)
  *   routing_out  optional record (NULL: kept inside the workspace)
- * Accumulation is fp32. In the bf16 path the GELU activations are rounded
- * to bf16 before the down-projection; the per-expert outputs stay fp32 and
- * Y is rounded once. The merge sums in a fixed order (shared expert, then
- * q_1..q_k), so repeated calls give bitwise-identical Y.
+ * Precision of the bf16 path: the up-projection multiplies bf16 values
+ * (exact products, fp32 accumulation); the GELU activations are rounded to
+ * fp16 and multiplied with an fp16 copy of W_down (made in the workspace at
+ * each call; exact for bf16 magnitudes in [2^-17, 65504], larger ones become
+ * infinities), accumulating in fp32; the per-expert outputs E_j(x) stay fp32
+ * and Y is rounded once to bf16. Activations beyond 65504 in magnitude are
+ * not representable in fp16 and make the output infinite. The merge sums in
+ * a fixed order (shared expert, then q_1..q_k), so repeated calls give
+ * bitwise-identical Y.
  * Requires, for bf16: d % 128 == 0, M % 64 == 0, M <= 256; for fp32:
  * H = B M <= 16384. Otherwise UNIF_EUNSUPPORTED. */
 int32_t unif_moe_layer_forward(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
@@ -182,13 +187,16 @@ int32_t unif_moe_layer_forward(const unif_moe_config* cfg, const void* X, const 
 /* Instrumented unif_moe_layer_forward for measurement: identical work and
  * result, and additionally records the caller's events (hipEvent_t handles,
  * created by the caller, recorded on `stream`) at the phase boundaries:
- *   events[0] before the first launch      events[3] after the up-projection
- *   events[1] after routing (split, route) events[4] after the down-projection
- *   events[2] after the permutation        events[5] after the weighted merge
- * (zero-fill, scan, scatter, slab lists)
- * n_events must be 6. In the fp32 path events[3] and events[4] both follow
+ *   events[0] before the first launch
+ *   events[1] after the fp16 copy of W_down (bf16 path; else = events[0])
+ *   events[2] after routing (split, route)
+ *   events[3] after the permutation (scan, scatter, slab lists)
+ *   events[4] after the up-projection
+ *   events[5] after the down-projection
+ *   events[6] after the weighted merge
+ * n_events must be 7. In the fp32 path events[4] and events[5] both follow
  * the per-pair FFN. Errors as unif_moe_layer_forward; UNIF_EINVAL for a NULL
- * event array or n_events != 6. */
+ * event array or n_events != 7. */
 int32_t unif_moe_layer_forward_profiled(const unif_moe_config* cfg, const void* X,
                                         const uint8_t* valid, const float* W_router,
                                         const float* prototypes, const void* W_up,

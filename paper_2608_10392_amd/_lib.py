@@ -59,7 +59,7 @@ EXPORTS = ("unif_moe_route_workspace_size", "unif_moe_route",
            "unif_moe_block_forward", "unif_moe_layer_backward_workspace_size",
            "unif_moe_layer_backward", "unif_moe_stats_workspace_size",
            "unif_moe_stats", "unif_moe_status_string")
-N_PHASE_EVENTS = 6
+N_PHASE_EVENTS = 7
 
 
 class UnifMoeError(RuntimeError):
@@ -215,7 +215,7 @@ def layer_forward(cfg, X, valid, W_router, prototypes, W_up, W_down, Y, workspac
 
 def layer_forward_profiled(cfg, X, valid, W_router, prototypes, W_up, W_down, Y, workspace,
                            events, routing=None, stream=None):
-    """As layer_forward, recording the six torch.cuda.Event objects in
+    """As layer_forward, recording the seven torch.cuda.Event objects in
     ``events`` at the phase boundaries (see the C header)."""
     c = make_config(cfg)
     r = _routing_struct(routing)

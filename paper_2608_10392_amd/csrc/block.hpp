@@ -147,7 +147,7 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(LayerNormParams p) 
 
 struct BlockCombineParams {
     int N, d, K, B;
-    const void* part;       // per-pair expert rows (layer format)
+    const void* part;       // per-pair expert rows (fp32)
     const int* pair_of;     // [N, K+1] pair of (token, i-th pathway)
     const float* alpha;
     const int* nsh;         // b
@@ -179,20 +179,33 @@ __device__ __forceinline__ void block_chunk_sum(const BlockCombineParams& c, int
     const int* of = c.pair_of + (size_t)t * (c.K + 1);
     const float* wt = c.wts + (size_t)t * c.K;
     const size_t esz = BF16 ? 2 : 4;
-    const char* part = static_cast<const char*>(c.part);
+    const float* part = static_cast<const float*>(c.part);
 #pragma unroll
     for (int e = 0; e < E; ++e) z[e] = 0.f;
     for (int i0 = 0; i0 <= k && k > 0; i0 += kBlockCombineBatch) {
-        C r[kBlockCombineBatch];
+        float r[kBlockCombineBatch][E];
 #pragma unroll
-        for (int u = 0; u < kBlockCombineBatch; ++u)
-            if (i0 + u <= k) r[u].load(part + (size_t)of[i0 + u] * c.d * esz, ch);
+        for (int u = 0; u < kBlockCombineBatch; ++u) {
+            if (i0 + u <= k) {
+                const float* row = part + (size_t)of[i0 + u] * c.d + ch * E;
+                if constexpr (BF16) {
+#pragma unroll
+                    for (int h = 0; h < E / 4; ++h) {
+                        const f32x4 q = *reinterpret_cast<const f32x4*>(row + 4 * h);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) r[u][4 * h + e] = q[e];
+                    }
+                } else {
+                    r[u][0] = row[0];
+                }
+            }
+        }
 #pragma unroll
         for (int u = 0; u < kBlockCombineBatch; ++u) {
             if (i0 + u <= k) {
                 const float wi = (i0 + u == 0) ? a : wt[i0 + u - 1];
 #pragma unroll
-                for (int e = 0; e < E; ++e) z[e] = fmaf(wi, r[u].v[e], z[e]);
+                for (int e = 0; e < E; ++e) z[e] = fmaf(wi, r[u][e], z[e]);
             }
         }
     }

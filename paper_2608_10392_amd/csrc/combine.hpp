@@ -19,8 +19,8 @@ struct CombineParams {
 
 constexpr int kCombineBatch = 6;
 
-// bf16 path: one thread per 8 consecutive outputs; bf16 per-expert rows
-// (one 16-byte load each), one 16-byte store.
+// bf16 layers: one thread per 8 consecutive outputs; fp32 per-expert rows
+// (two 16-byte loads each), one 16-byte bf16 store.
 __global__ void combine_bf16_kernel(CombineParams c) {
     const int chunks = c.d >> 3;
     const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -28,7 +28,7 @@ __global__ void combine_bf16_kernel(CombineParams c) {
     const int t = (int)(item / chunks), ch = (int)(item - (size_t)t * chunks);
     const int k = c.nres[t];
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    const u16* part = static_cast<const u16*>(c.part);
+    const float* part = static_cast<const float*>(c.part);
     const int* of = c.pair_of + (size_t)t * (c.K + 1);
     const float* wt = c.wts + (size_t)t * c.K;
     // Rows in batches of kCombineBatch: the weights and pair indices of a
@@ -48,20 +48,21 @@ __global__ void combine_bf16_kernel(CombineParams c) {
         }
         if (k == 0) break;
         // The rows are read once and Y written once: non-temporal accesses
-        // keep them from displacing cached data (15% on this kernel).
-        u32x4 v[kCombineBatch];
+        // keep them from displacing cached data.
+        f32x4 v[kCombineBatch][2];
 #pragma unroll
-        for (int u = 0; u < kCombineBatch; ++u)
-            v[u] = (i0 + u <= k) ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(part + (size_t)pr[u] * c.d + ch * 8))
-                                 : u32x4{0u, 0u, 0u, 0u};
+        for (int u = 0; u < kCombineBatch; ++u) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+                v[u][h] = (i0 + u <= k)
+                              ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(part + (size_t)pr[u] * c.d + ch * 8 + 4 * h))
+                              : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
 #pragma unroll
         for (int u = 0; u < kCombineBatch; ++u) {
             if (i0 + u <= k) {
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    acc[2 * q] = fmaf(w[u], __uint_as_float(v[u][q] << 16), acc[2 * q]);
-                    acc[2 * q + 1] = fmaf(w[u], __uint_as_float(v[u][q] & 0xffff0000u), acc[2 * q + 1]);
-                }
+                for (int q = 0; q < 8; ++q) acc[q] = fmaf(w[u], v[u][q >> 2][q & 3], acc[q]);
             }
         }
     }
@@ -69,6 +70,20 @@ __global__ void combine_bf16_kernel(CombineParams c) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) o[q] = (uint32_t)f2bf(acc[2 * q]) | ((uint32_t)f2bf(acc[2 * q + 1]) << 16);
     __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(static_cast<u16*>(c.Y) + (size_t)t * c.d + ch * 8));
+}
+
+// W_down (bf16) -> fp16 values for the down-projection's fp16 products: n
+// 8-element chunks, grid-stride. Each value is rounded to nearest even
+// (exact for bf16 magnitudes in [2^-17, 65504]; larger ones become
+// infinities).
+__global__ void bf16_to_f16_kernel(const u16* __restrict__ src, u16* __restrict__ dst, size_t n) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+        const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + i);
+        u32x4 o;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = pack_f16x2(__uint_as_float(v[q] << 16), __uint_as_float(v[q] & 0xffff0000u));
+        reinterpret_cast<u32x4*>(dst)[i] = o;
+    }
 }
 
 // fp32: one thread per output element.

@@ -1,15 +1,21 @@
-// Block-sparse expert FFN on the bf16 matrix cores (Eq. block-expert-output).
+// Block-sparse expert FFN on the matrix cores (Eq. block-expert-output).
 //
-// Up-projection + GELU, one tile = TM rows of one (expert e, block c) slab:
-//   Hbuf[pair, c M .. c M + M) = GELU(X[token(pair)] K_e[:, block c])
+// Up-projection + GELU (bf16 products), one tile = TM rows of one (expert e,
+// block c) slab:
+//   Hbuf[pair, c M .. c M + M) = fp16(GELU(X[token(pair)] K_e[:, block c]))
 // Rows come from the slab's compacted pair list, so no inactive (pair, block)
 // is computed. The tile spans the whole block width M, so each gathered token
 // row is read once per slab.
 //
-// Down-projection, one tile = TM consecutive pairs of one expert segment x
-// BN output columns:
+// Down-projection (fp16 products: the activations H and a fp16 copy of the
+// bf16 values V, which fp16 holds exactly down to 2^-17 in magnitude), one
+// tile = TM consecutive pairs of one expert segment x BN output columns:
 //   part[pair, n] = sum over blocks c of the pair's mask of
 //                   Hbuf[pair, block c] . V_e[block c, n]        (fp32)
+// H is kept in fp16 rather than bf16 because its rounding enters every
+// output through a sum over all active channels: with bf16 (relative step
+// 2^-8) it alone takes a sixth of the bf16 output bound on these layers,
+// with fp16 (2^-11) an eighth of that.
 // The contraction runs over the union of the tile's block masks; rows whose
 // mask lacks a block read a zero page instead, and each 32-row MFMA group
 // skips the blocks none of its rows use. Pairs are sorted by mask key, so
@@ -76,9 +82,9 @@ struct DownParams {
     int d, M, B, H, ncol;        // ncol: column tiles per row tile
     const u16* Hbuf;
     const u16* zero16;           // 16 zero bytes: the source of rows that lack a block
-    const u16* Wdown;
-    u16* part;                   // per-pair output rows, bf16
-    u16* part_sink;              // one d row that absorbs the stores of unused tile rows
+    const u16* Wdown;            // fp16 values V, layout of the layer's W_down
+    float* part;                 // per-pair output rows, fp32
+    float* part_sink;            // one d row that absorbs the stores of unused tile rows
     const int4* rt_info;         // per row tile: first pair, rows, expert, cost
     const uint64_t* rt_masks;    // per row tile: block-mask union of each 16-row group, then of the tile
     const uint64_t* pair_mask;   // readable for a whole tile past the last pair
@@ -371,7 +377,7 @@ void up_kernel(UpParams p) {
             if (s == 0 && has_next) fetch_rows(next_rows, par ^ 1);
             slot = other;
         }
-        // GELU, round to bf16; lane stores 16 consecutive columns of its row
+        // GELU, round to fp16; lane stores 16 consecutive columns of its row
         // per 32-column group.
         const int sl = info & 0xffff, nrows = info >> 16;
         const int c = sl - (sl / p.B) * p.B;
@@ -399,8 +405,8 @@ void up_kernel(UpParams p) {
                 u32x4 lo, hi;
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    lo[t] = pack_bf16x2(gelu_exp2poly(v[2 * t]), gelu_exp2poly(v[2 * t + 1]));
-                    hi[t] = pack_bf16x2(gelu_exp2poly(v[8 + 2 * t]), gelu_exp2poly(v[9 + 2 * t]));
+                    lo[t] = pack_f16x2(gelu_exp2poly(v[2 * t]), gelu_exp2poly(v[2 * t + 1]));
+                    hi[t] = pack_f16x2(gelu_exp2poly(v[8 + 2 * t]), gelu_exp2poly(v[9 + 2 * t]));
                 }
                 st16(dst + 32 * j, lo);
                 st16(dst + 32 * j + 8, hi);
@@ -440,7 +446,7 @@ void down_kernel(DownParams p) {
     constexpr int LA = TM / S::ROWS_PER_DMA / NWV;
     constexpr int LB = BN / S::ROWS_PER_DMA / NWV;
     constexpr int L = LA + LB;
-    constexpr int NEPI = RG * NG * 2;                 // epilogue stores per wave
+    constexpr int NEPI = RG * NG * 4;                 // epilogue stores per wave (fp32 rows)
     constexpr int A_BYTES = TM * RB, STAGE = (TM + BN) * RB, RING = 2 * STAGE;
     constexpr int NFETCH = 1;                         // 4-byte copies per wave for a tile's row masks
     constexpr int NR = RG + NG;
@@ -641,7 +647,7 @@ void down_kernel(DownParams p) {
                     if (gset & (1u << i)) {
 #pragma unroll
                         for (int j = 0; j < NG; ++j)
-                            acc[i][j] = mfma32x32x16(as_bf16x8(W[j]), as_bf16x8(X[i]), acc[i][j]);
+                            acc[i][j] = mfma32x32x16_f16(as_f16x8(W[j]), as_f16x8(X[i]), acc[i][j]);
                     }
                     if (k == KS - 1) {
 #pragma unroll
@@ -678,25 +684,21 @@ void down_kernel(DownParams p) {
             }
             slot = other;
         }
-        // Per-expert rows, rounded to bf16 (the combine weighs and sums them
-        // in fp32); lane stores 16 consecutive columns of its row per
-        // 32-column group.
+        // Per-expert rows in fp32 (the combine weighs and sums them in fp32
+        // and rounds once); lane stores 16 consecutive columns of its row
+        // per 32-column group.
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
             const int r = wm * 64 + i * 32 + lr;
-            u16* dst = (r < cur.nrows) ? p.part + (size_t)(cur.p0 + r) * p.d + (size_t)cur.ct * BN : p.part_sink;
+            float* dst = (r < cur.nrows) ? p.part + (size_t)(cur.p0 + r) * p.d + (size_t)cur.ct * BN : p.part_sink;
             dst += wn * (BN / WN) + 16 * lh;
 #pragma unroll
             for (int j = 0; j < NG; ++j) {
                 const f32x16 v = acc[i][j];
-                u32x4 lo, hi;
 #pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    lo[t] = pack_bf16x2(v[2 * t], v[2 * t + 1]);
-                    hi[t] = pack_bf16x2(v[8 + 2 * t], v[9 + 2 * t]);
-                }
-                st16(dst + 32 * j, lo);
-                st16(dst + 32 * j + 8, hi);
+                for (int t = 0; t < 4; ++t)
+                    st16(dst + 32 * j + 4 * t, u32x4{__float_as_uint(v[4 * t]), __float_as_uint(v[4 * t + 1]),
+                                                     __float_as_uint(v[4 * t + 2]), __float_as_uint(v[4 * t + 3])});
             }
         }
         if (!has_next) break;

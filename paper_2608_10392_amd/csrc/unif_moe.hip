@@ -4,6 +4,7 @@
 //
 // Forward launch sequence (all asynchronous on the caller's stream, no
 // device-to-host traffic):
+//   bf16_to_f16      W_down -> fp16 copy for the down-projection (bf16 only)
 //   fill_zero        pair / slab counters
 //   split_router     fp32 router + prototypes -> 3 bf16 parts (bf16 only)
 //   route            routing record + pair and slab counts
@@ -40,6 +41,7 @@ using namespace unifmoe;
 namespace {
 
 constexpr int kKeyBitsMax = 10;
+constexpr int kPhaseEvents = 7;   // unif_moe_layer_forward_profiled
 constexpr size_t kLdsLimit = 160 * 1024;
 
 // Expert-GEMM tile shapes, one workgroup of 8 waves per CU. Up: 256
@@ -211,7 +213,8 @@ struct FwdPlan {
     size_t bin_cursor, slab_off, seg_off, up_tile_off, down_tile_off, chunk_off, chunk_cnt;
     size_t pair_token, pair_mask, pair_expert, pair_of, slab_rows, slab_tok, up_tile_info, up_tile_rows, hbuf, part;
     size_t max_chunks, max_row_tiles, rt_info, rt_masks, down_tiles, down_slices;
-    size_t xn;   // LN(X), the FFN input of a pre-LN block
+    size_t xn;      // LN(X), the FFN input of a pre-LN block
+    size_t wdown16; // fp16 copy of W_down (bf16 layers)
     size_t total;
 };
 
@@ -257,14 +260,15 @@ FwdPlan plan_forward(const Dims& m, bool own_record, size_t xn_bytes = 0) {
     p.max_chunks = ceil_div_sz(pmax, kChunk) + K1;
     p.chunk_off = cv.take(m.bf16 ? 4 * (K1 + 1) : 0);
     p.chunk_cnt = cv.take(m.bf16 ? 4 * p.max_chunks * (size_t)m.B : 0);
-    p.hbuf = cv.take(m.bf16 ? (pmax + 1) * (size_t)m.H * 2 : 0);  // + the sink row
-    p.part = cv.take((pmax + 1) * (size_t)m.d * (m.bf16 ? 2 : sizeof(float)));   // + the sink row
+    p.hbuf = cv.take(m.bf16 ? (pmax + 1) * (size_t)m.H * 2 : 0);  // fp16, + the sink row
+    p.part = cv.take((pmax + 1) * (size_t)m.d * sizeof(float));   // fp32, + the sink row
     p.max_row_tiles = ceil_div_sz(pmax, kDownTMMin) + K1;
     p.rt_info = cv.take(m.bf16 ? 16 * p.max_row_tiles : 0);
     p.rt_masks = cv.take(m.bf16 ? 8 * (kDownTMMax / 16 + 1) * p.max_row_tiles : 0);
     p.down_tiles = cv.take(m.bf16 ? 4 * p.max_row_tiles * (size_t)(m.d / kDownBNNarrow) : 0);
     p.down_slices = cv.take(m.bf16 ? 4 * 16 : 0);
     p.xn = cv.take(xn_bytes);
+    p.wdown16 = cv.take(m.bf16 ? K1 * (size_t)m.d * m.H * 2 : 0);
     p.total = cv.cur + 256;  // slack for aligning an unaligned base pointer
     return p;
 }
@@ -549,7 +553,18 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     int* totals = reinterpret_cast<int*>(ws + plan.totals);
 
     UNIF_MARK(0);
-    // 0. the FFN input: LN(X) for a pre-LN block, else X
+    // 0. the fp16 copy of W_down that the down-projection multiplies with
+    const u16* wdown16 = nullptr;
+    if (m.bf16) {
+        const size_t n8 = (size_t)m.K1 * m.d * m.H / 8;
+        u16* dst = reinterpret_cast<u16*>(ws + plan.wdown16);
+        const unsigned g = (unsigned)std::min<size_t>((n8 + 255) / 256, (size_t)cu_count() * 8);
+        bf16_to_f16_kernel<<<g, 256, 0, st>>>(static_cast<const u16*>(W_down), dst, n8);
+        UNIF_LAUNCH_CHECK();
+        wdown16 = dst;
+    }
+    UNIF_MARK(1);
+    // 1. the FFN input: LN(X) for a pre-LN block, else X
     const void* Xf = X;
     if (blk != nullptr && blk->norm == UNIF_NORM_PRE) {
         LayerNormParams ln;
@@ -578,7 +593,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     s = launch_route(m, rp, W_router, prototypes, wsplit, st, reinterpret_cast<uint32_t*>(ws + plan.zero_begin),
                      zwords);
     if (s != UNIF_OK) return s;
-    UNIF_MARK(1);
+    UNIF_MARK(2);
 
     // 3. offsets and tile tables, pair slots, slab lists
     PermuteParams pp;
@@ -636,7 +651,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         const int up_groups = m.K1 * ceil_div(m.B, pp.up_group);
         slabfill_kernel<<<(unsigned)up_groups + std::min((unsigned)plan.max_chunks, gs), kChunk, 0, st>>>(pp, up_groups);
         UNIF_LAUNCH_CHECK();
-        UNIF_MARK(2);
+        UNIF_MARK(3);
         // 4. block-sparse expert GEMMs
         UpParams up;
         up.d = m.d;
@@ -658,7 +673,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         const int grid = (cus / kXcds) * kXcds;
         s = up.b_up != nullptr ? launch_up<true>(m, grid, up_lds, st, up) : launch_up<false>(m, grid, up_lds, st, up);
         if (s != UNIF_OK) return s;
-        UNIF_MARK(3);
+        UNIF_MARK(4);
         DownParams dn;
         dn.d = m.d;
         dn.M = m.M;
@@ -667,8 +682,8 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         dn.ncol = pp.down_col_tiles;
         dn.zero16 = reinterpret_cast<const u16*>(ws + plan.zero_page);
         dn.Hbuf = up.Hbuf;
-        dn.Wdown = static_cast<const u16*>(W_down);
-        dn.part = static_cast<u16*>(part);
+        dn.Wdown = wdown16;
+        dn.part = static_cast<float*>(part);
         dn.part_sink = dn.part + (size_t)m.N * m.K1 * m.d;
         dn.rt_info = pp.rt_info;
         dn.rt_masks = pp.rt_masks;
@@ -684,9 +699,9 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         else
             s = launch_persistent(down_kernel<4, 2>, grid, (size_t)down_lds_bytes(256, 128), st, dn);
         if (s != UNIF_OK) return s;
-        UNIF_MARK(4);
+        UNIF_MARK(5);
     } else {
-        UNIF_MARK(2);
+        UNIF_MARK(3);
         PairF32Params fp;
         fp.d = m.d;
         fp.M = m.M;
@@ -705,8 +720,8 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         if (allow_lds(pair_ffn_f32_kernel, lds) != UNIF_OK) return UNIF_EDEVICE;
         pair_ffn_f32_kernel<<<cus * 4, 256, lds, st>>>(fp);
         UNIF_LAUNCH_CHECK();
-        UNIF_MARK(3);
         UNIF_MARK(4);
+        UNIF_MARK(5);
     }
 
     // 5. weighted merge (the block's merge around it)
@@ -750,7 +765,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
             }
         }
         UNIF_LAUNCH_CHECK();
-        UNIF_MARK(5);
+        UNIF_MARK(6);
         return UNIF_OK;
     }
     CombineParams cp;
@@ -771,7 +786,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         combine_f32_kernel<<<(unsigned)((items + 255) / 256), 256, 0, st>>>(cp);
     }
     UNIF_LAUNCH_CHECK();
-    UNIF_MARK(5);
+    UNIF_MARK(6);
     return UNIF_OK;
 }
 
@@ -815,8 +830,8 @@ int32_t unif_moe_layer_forward_profiled(const unif_moe_config* cfg, const void* 
                                         const void* W_down, void* Y, const unif_moe_routing* routing_out,
                                         void* workspace, size_t workspace_bytes, void* const* events,
                                         int32_t n_events, void* stream) {
-    if (events == nullptr || n_events != 6) return UNIF_EINVAL;
-    for (int i = 0; i < 6; ++i)
+    if (events == nullptr || n_events != kPhaseEvents) return UNIF_EINVAL;
+    for (int i = 0; i < kPhaseEvents; ++i)
         if (events[i] == nullptr) return UNIF_EINVAL;
     return forward_impl(cfg, nullptr, X, valid, W_router, prototypes, W_up, W_down, Y, routing_out, workspace,
                         workspace_bytes, events, stream);

@@ -8,14 +8,18 @@ decisions differ, each differing decision must lie within 1e-4 of its
 boundary, and their outputs are checked against the oracle evaluated under
 the GPU's decisions (oracle.forced_forward).
 
-Outputs: max over the checked tokens and all features of
-    |y_gpu - y_ref| - ulp_out(y_ref) / 2   <=   tol * RMS(y_ref),
-with tol = 2e-2 for bf16 and 1e-4 for fp32, y_ref the float64 oracle output
-and ulp_out the spacing of the output format at y_ref. The half-ulp term is
-the representation error that any output in that format carries (for bf16
-it alone reaches ~1.8e-2 x RMS at the 6-sigma tails of these layers); the
-bound applies to the error the computation adds on top of it. The raw
-max |y_gpu - y_ref| / RMS is reported as well.
+Outputs, over the checked tokens and all features, against y_ref, the
+float64 oracle output:
+  raw     max |y_gpu - y_ref| / RMS(y_ref) <= TOL (2e-2 bf16, 1e-4 fp32), the
+          bound as stated;
+  excess  max (|y_gpu - y_ref| - ulp_out(y_ref) / 2) / RMS(y_ref) <= KERNEL_TOL,
+          the error the computation adds beyond rounding y_ref once to the
+          output format (ulp_out: the format's spacing at y_ref), so that the
+          kernels' own error cannot grow unseen below the raw bound.
+Only where rounding y_ref once to nearest (RNE) already exceeds TOL (bf16
+outputs of 8 x RMS and more) is the raw bound replaced by RNE + KERNEL_TOL,
+and the message says so; every message carries the raw, RNE and excess
+figures.
 """
 import numpy as np
 
@@ -24,6 +28,7 @@ from synth.generate import bf16_bits_to_f32
 
 MARGIN = 1e-4
 TOL = {"bf16": 2e-2, "f32": 1e-4}
+KERNEL_TOL = {"bf16": 5e-3, "f32": 5e-5}
 
 
 def _decision_parts(rec, t, B):
@@ -141,15 +146,31 @@ def gpu_output_f64(Y, dtype):
     return (bf16_bits_to_f32(Y) if dtype == "bf16" else np.asarray(Y, np.float32)).astype(np.float64)
 
 
+def rne_format(y, dtype):
+    """y (float64) rounded once to the output format, to nearest even."""
+    if dtype == "f32":
+        return np.asarray(y, np.float64).astype(np.float32).astype(np.float64)
+    return gpu_output_f64(O.to_format(y, "bf16"), "bf16")
+
+
 def _output_error(cfg, Yg, ref):
+    dt = cfg["dtype"]
     rms = float(np.sqrt(np.mean(ref ** 2)))
-    raw = float(np.abs(Yg - ref).max())
-    excess = float(np.maximum(np.abs(Yg - ref) - half_ulp(ref, cfg["dtype"]), 0.0).max())
-    rel = excess / rms if rms > 0 else excess
-    raw_rel = raw / rms if rms > 0 else raw
-    assert rel <= TOL[cfg["dtype"]], (f"output error beyond the output format's half ulp "
-                                      f"{excess:.3e} = {rel:.3e} x RMS {rms:.3e} (raw {raw_rel:.3e})")
-    return rel, raw_rel
+    scale = rms if rms > 0 else 1.0
+    raw = float(np.abs(Yg - ref).max()) / scale
+    rne = float(np.abs(rne_format(ref, dt) - ref).max()) / scale
+    excess = float(np.maximum(np.abs(Yg - ref) - half_ulp(ref, dt), 0.0).max()) / scale
+    bound = TOL[dt]
+    note = ""
+    if rne > TOL[dt]:
+        bound = rne + KERNEL_TOL[dt]
+        note = " (format-limited case: rounding y_ref once already exceeds the bound)"
+    msg = (f"output error: raw {raw:.3e} x RMS (bound {bound:.1e}{note}), rounding y_ref once "
+           f"{rne:.3e}, beyond the half ulp {excess:.3e} (bound {KERNEL_TOL[dt]:.0e}); RMS {rms:.3e}")
+    print(msg)
+    assert raw <= bound, msg
+    assert excess <= KERNEL_TOL[dt], msg
+    return raw, excess
 
 
 # ------------------------------------------------ the block around it ---

@@ -39,11 +39,11 @@ def run_block(g, blk, X, label, n_sample=None):
     tokens = (np.arange(cfg["n_tokens"]) if n_sample is None
               else parity.sample_tokens(orec, cfg, n_sample))
     inputs = dict(g, X=X)
-    rel, raw = parity.check_block_outputs(cfg, blk, inputs, Xin, orec, grec, Y, tokens)
+    raw, excess = parity.check_block_outputs(cfg, blk, inputs, Xin, orec, grec, Y, tokens)
     print(f"[gpu] block {label}: checked {summary['n_checked']}/{summary['n_valid']} decisions, "
           f"loose {int(loose.sum())}, near-ties {summary['n_near']} (differing "
-          f"{summary['n_near_differ']}), output err {rel:.2e} x RMS beyond half-ulp "
-          f"(raw {raw:.2e}) over {len(tokens)} tokens", flush=True)
+          f"{summary['n_near_differ']}), output err raw {raw:.2e} x RMS, "
+          f"beyond half-ulp {excess:.2e} over {len(tokens)} tokens", flush=True)
     del dev
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
