@@ -278,17 +278,13 @@ char* align_base(void* ws) {
     return reinterpret_cast<char*>((a + 255) & ~(uintptr_t)255);
 }
 
-int g_cu_count[64];
-
+// Compute units of the current device (queried at each call; the grids of
+// the persistent kernels are sized by it).
 int cu_count() {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (g_cu_count[dev] == 0) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-        g_cu_count[dev] = n;
-    }
-    return g_cu_count[dev];
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 256;
+    return n;
 }
 
 #define UNIF_LAUNCH_CHECK()                              \
