@@ -304,6 +304,29 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
                                 float* dW_down, float* dW_router, void* workspace,
                                 size_t workspace_bytes, void* stream);
 
+/* Scratch memory of unif_moe_layer_forward_static on each GPU (bytes). */
+#define UNIF_MOE_STATIC_WORKSPACE_BYTES ((size_t)128 << 20)
+
+/* unif_moe_layer_forward for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc. Same arguments, work and result as unif_moe_layer_forward, but
+ * no caller workspace: the scratch memory is a file-scope device array of
+ * UNIF_MOE_STATIC_WORKSPACE_BYTES held by each GPU that the library's code is
+ * loaded on until the process ends. The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); its first call on a device looks
+ * up the array's device address once (hipGetSymbolAddress).
+ * All calls on one GPU share that GPU's array and every call clears what it
+ * needs zeroed; calls that overlap in time on one GPU (other streams or host
+ * threads) race on it and must be ordered by the caller.
+ * Errors: as unif_moe_layer_forward; UNIF_EWORKSPACE when the layer needs
+ * more scratch than UNIF_MOE_STATIC_WORKSPACE_BYTES (the size reported by
+ * unif_moe_layer_forward_workspace_size; checked on the host before any HIP
+ * call); UNIF_EDEVICE when the array's address cannot be obtained. */
+int32_t unif_moe_layer_forward_static(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
+                                      const float* W_router, const float* prototypes, const void* W_up,
+                                      const void* W_down, void* Y, const unif_moe_routing* routing_out,
+                                      void* stream);
+
 /* Workspace needed by unif_moe_stats (bytes). Host only. */
 int32_t unif_moe_stats_workspace_size(const unif_moe_config* cfg, size_t* bytes);
 

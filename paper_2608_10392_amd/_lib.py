@@ -58,7 +58,7 @@ EXPORTS = ("unif_moe_route_workspace_size", "unif_moe_route",
            "unif_moe_layer_forward_profiled", "unif_moe_block_forward_workspace_size",
            "unif_moe_block_forward", "unif_moe_layer_backward_workspace_size",
            "unif_moe_layer_backward", "unif_moe_stats_workspace_size",
-           "unif_moe_stats", "unif_moe_status_string")
+           "unif_moe_stats", "unif_moe_layer_forward_static", "unif_moe_status_string")
 N_PHASE_EVENTS = 7
 
 
@@ -99,6 +99,8 @@ def lib():
         L.unif_moe_block_forward_workspace_size.argtypes = [cfgp, blkp, ctypes.POINTER(sz)]
         L.unif_moe_block_forward.argtypes = [cfgp, blkp, vp, vp, vp, vp, vp, vp, vp,
                                              ctypes.POINTER(Routing), vp, sz, vp]
+        L.unif_moe_layer_forward_static.argtypes = [cfgp, vp, vp, vp, vp, vp, vp, vp,
+                                                    ctypes.POINTER(Routing), vp]
         L.unif_moe_status_string.argtypes = [ctypes.c_int32]
         L.unif_moe_status_string.restype = ctypes.c_char_p
         for name in EXPORTS[:-1]:
@@ -211,6 +213,22 @@ def layer_forward(cfg, X, valid, W_router, prototypes, W_up, W_down, Y, workspac
                                         ctypes.byref(r) if r is not None else None,
                                         _ptr(workspace), ws_bytes, _stream(stream)),
            "unif_moe_layer_forward")
+
+
+STATIC_WORKSPACE_BYTES = 128 << 20   # UNIF_MOE_STATIC_WORKSPACE_BYTES
+
+
+def layer_forward_static(cfg, X, valid, W_router, prototypes, W_up, W_down, Y, routing=None,
+                         stream=None):
+    """layer_forward with the library's static per-GPU scratch instead of a
+    caller workspace (unif_moe_layer_forward_static)."""
+    c = make_config(cfg)
+    r = _routing_struct(routing)
+    _check(lib().unif_moe_layer_forward_static(ctypes.byref(c), _ptr(X), _ptr(valid), _ptr(W_router),
+                                               _ptr(prototypes), _ptr(W_up), _ptr(W_down), _ptr(Y),
+                                               ctypes.byref(r) if r is not None else None,
+                                               _stream(stream)),
+           "unif_moe_layer_forward_static")
 
 
 def layer_forward_profiled(cfg, X, valid, W_router, prototypes, W_up, W_down, Y, workspace,

@@ -24,6 +24,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "../../include/unif_moe.h"
 #include "backward.hpp"
@@ -1046,6 +1047,56 @@ int32_t unif_moe_stats(const unif_moe_config* cfg, const unif_moe_routing* routi
     host_out->activated_gemm_flops = 4.0 * m.d * m.M * (double)h[kStSumCB];
     host_out->routing_flops = 2.0 * m.d * (1.0 + m.K + m.B) * nv;
     return UNIF_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The layer forward without a caller workspace (unif_moe_layer_forward_static):
+// its scratch memory is this file-scope device array, one copy per GPU the
+// library's code is loaded on, held until the process ends.
+namespace {
+
+constexpr size_t kStaticScratchBytes = UNIF_MOE_STATIC_WORKSPACE_BYTES;
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+// Device address of `scratch` on each GPU, looked up once per device with that
+// device current (the array's name is a host-side stand-in in host code and
+// must never be passed to a kernel or a copy).
+constexpr int kMaxDevices = 64;
+void* g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+int32_t static_scratch(void** out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return UNIF_EDEVICE;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return UNIF_EDEVICE;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return UNIF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t unif_moe_layer_forward_static(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
+                                      const float* W_router, const float* prototypes, const void* W_up,
+                                      const void* W_down, void* Y, const unif_moe_routing* routing_out,
+                                      void* stream) {
+    size_t need = 0;
+    const int32_t s = unif_moe_layer_forward_workspace_size(cfg, &need);
+    if (s != UNIF_OK) return s;
+    if (need > kStaticScratchBytes) return UNIF_EWORKSPACE;
+    void* ws = nullptr;
+    const int32_t e = static_scratch(&ws);
+    if (e != UNIF_OK) return e;
+    return forward_impl(cfg, nullptr, X, valid, W_router, prototypes, W_up, W_down, Y, routing_out, ws,
+                        kStaticScratchBytes, nullptr, stream);
 }
 
 }  // extern "C"

@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 12, names
+    assert len(names) == 13, names
     assert set(names) == set(_lib.EXPORTS)
     out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True, text=True).stdout
     for n in names:
@@ -221,3 +221,12 @@ def test_backward_workspace_and_validation(L):
     with pytest.raises(_lib.UnifMoeError) as e:
         _lib.layer_backward_workspace_size(base_cfg(n_tokens=128 * 65535 + 1))
     assert e.value.status == _lib.EUNSUPPORTED
+
+
+def test_static_forward_rejects_layers_beyond_its_scratch(L):
+    """The forward without a workspace rejects, on the host before any HIP
+    call, a layer that needs more than the static scratch."""
+    c = _lib.make_config(layer_config(get_config("vit_b16")))
+    assert _lib.layer_forward_workspace_size(c) > _lib.STATIC_WORKSPACE_BYTES
+    assert L.unif_moe_layer_forward_static(ctypes.byref(c), 1, None, 1, 1, 1, 1, 1, None, None) == _lib.EWORKSPACE
+    assert L.unif_moe_layer_forward_static(None, 1, None, 1, 1, 1, 1, 1, None, None) == _lib.EINVAL
