@@ -12,10 +12,15 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
-// Copies of the per-(expert, block) row counts that the routing kernel's
-// workgroups add into (spreading same-address atomics); the permutation
-// sums them.
-constexpr int kSlabCopies = 8;
+// Copies of the per-expert pair totals that the routing tiles add into
+// (spreading same-address atomics); the permutation sums them.
+constexpr int kExpCopies = 16;
+// Copies of each (expert, mask key) bin of the pair sort: token tile q counts
+// its pairs and takes their slots in copy q % kBinCopies, so that no counter
+// sees more than a share of its bin's atomics (same-address atomics serialize
+// at the device's coherence point); a bin's slots are its copies' ranges in
+// copy order.
+constexpr int kBinCopies = 8;
 
 __device__ __forceinline__ float bf2f(u16 v) { return __uint_as_float(((uint32_t)v) << 16); }
 
@@ -139,6 +144,23 @@ __device__ __forceinline__ int mask_key(uint64_t mask, int B, int kb) {
     v ^= v >> 4;
     v ^= v >> 8;
     return (int)v;
+}
+
+// put(i, get(i)) for i in [0, n), the workgroup's threads striding over i;
+// each thread issues a batch of 8 gets (global loads) before any put, so the
+// loads' latencies overlap instead of adding up one per iteration.
+template <class Get, class Put>
+__device__ __forceinline__ void batched_copy(int n, Get get, Put put) {
+    const int T = blockDim.x;
+    for (int i0 = threadIdx.x; i0 < n; i0 += 8 * T) {
+        decltype(get(0)) v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (i0 + u * T < n) v[u] = get(i0 + u * T);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (i0 + u * T < n) put(i0 + u * T, v[u]);
+    }
 }
 
 // Largest i in [0, n) with off[i] <= x (off ascending, off[0] = 0 <= x).

@@ -85,12 +85,10 @@ struct DownParams {
     const u16* Wdown;            // fp16 values V, layout of the layer's W_down
     float* part;                 // per-pair output rows, fp32
     float* part_sink;            // one d row that absorbs the stores of unused tile rows
-    const int4* rt_info;         // per row tile: first pair, rows, expert, cost
-    const uint64_t* rt_masks;    // per row tile: block-mask union of each 16-row group, then of the tile
+    const int4* rt_info;         // per row tile: first pair, rows, expert
+    const uint64_t* rt_masks;    // per row tile: block-mask union of each 32-row group, then of the tile
     const uint64_t* pair_mask;   // readable for a whole tile past the last pair
-    const int* tiles;            // per down tile: row tile << 8 | column tile
-    const int* totals;           // [2]: down tiles
-    const int* slices;           // [9]: first tile of each XCD's slice, then the count
+    const int* totals;           // [2]: down tiles (row tiles x column tiles)
     int* queue;                  // 8 per-XCD tile counters, zero at launch
 };
 
@@ -442,7 +440,6 @@ void down_kernel(DownParams p) {
     constexpr int TM = WM * 64;
     constexpr int BN = WN * NG * 32;                  // NG 32-column groups per wave
     constexpr int RG = 2;                             // 32-row groups per wave
-    constexpr int G16 = TM / 16;                      // 16-row mask groups per tile
     constexpr int LA = TM / S::ROWS_PER_DMA / NWV;
     constexpr int LB = BN / S::ROWS_PER_DMA / NWV;
     constexpr int L = LA + LB;
@@ -459,7 +456,7 @@ void down_kernel(DownParams p) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WN, wn = wave % WN;
     const int kcpb = p.M / S::SK;   // stages per block
-    const TileQueue tq(p.queue, p.slices);
+    const TileQueue tq(p.queue, ld_uniform(p.totals + 2));
     // ctl as in the up kernel.
     int* ctl = reinterpret_cast<int*>(lds_dn + RING + 16 * TM);
     if (tid == 0) {
@@ -499,28 +496,26 @@ void down_kernel(DownParams p) {
         vA[j] = (uint32_t)rA[j] * hrow + ch * 16;
     }
 
-    // Uniform description of a tile; gm[i]: block mask of this wave's
-    // 32-row group i.
+    // Uniform description of a tile: tiles are listed row tile by row tile
+    // (the column tiles of one row tile run side by side on one XCD and
+    // share its H rows in L2), row tiles expert by expert; gm[i]: the block
+    // mask of this wave's 32-row group i, all: the tile's.
     struct Desc {
         int p0, nrows, e, ct, nst, nreal;
         uint64_t all, gm[RG];
     };
     auto describe = [&](int t) {
         Desc D;
-        const int rc = ld_uniform(p.tiles + t);
-        const int rt = rc >> 8;
-        D.ct = rc & 255;
+        const int rt = t / p.ncol;
+        D.ct = t - rt * p.ncol;
         const int* inf = reinterpret_cast<const int*>(p.rt_info + rt);
         D.p0 = ld_uniform(inf);
         D.nrows = ld_uniform(inf + 1);
         D.e = ld_uniform(inf + 2);
-        const uint64_t* ms = p.rt_masks + (size_t)rt * (G16 + 1);
-        D.all = ld_uniform64(ms + G16);
+        const uint64_t* ms = p.rt_masks + (size_t)rt * (TM / 32 + 1);
+        D.all = ld_uniform64(ms + TM / 32);
 #pragma unroll
-        for (int i = 0; i < RG; ++i) {
-            const int g = 2 * (wm * RG + i);
-            D.gm[i] = ld_uniform64(ms + g) | ld_uniform64(ms + g + 1);
-        }
+        for (int i = 0; i < RG; ++i) D.gm[i] = ld_uniform64(ms + wm * RG + i);
         D.nreal = __popcll(D.all) * kcpb;
         D.nst = max(D.nreal, 4);
         return D;

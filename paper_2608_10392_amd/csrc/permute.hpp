@@ -6,63 +6,61 @@
 // grouped by expert and, inside an expert, by the Gray-code rank of the top
 // key_bits bits of their block mask (a counting sort, see mask_key), so that
 // pairs that share blocks sit next to each other for the down-projection
-// tiles. Each (expert, block) "slab" gets the list of pairs that use it,
-// which the up-projection tiles read.
+// tiles. Each (expert, block) "slab" gets the list of pairs that use it, in
+// token order, which the up-projection tiles read (and the backward's weight
+// gradients sum over, in that order).
 //
-//   route_kernel       counts pairs per (expert, key), taking each pair's slot
-//                      in its bin, and rows per slab
-//   scan_kernel        one workgroup per expert and one more: LDS-staged
-//                      exclusive prefix sums -> bin cursors, expert segment
-//                      offsets, slab offsets, chunk offsets, tile offsets
-//   scatter_kernel     one thread per token writes its pairs at their slots
-//   tables_kernel      down row tiles (per row tile), and per chunk of
-//                      kChunk pairs of one expert: pairs per block
-//   chunk_scan_kernel  per slab: exclusive scan of its chunk counts
-//   slabfill_kernel    per chunk: each pair writes itself into the slabs of
-//                      its blocks, in pair order (deterministic); per
-//                      (expert, block group): the up tile table
+//   route kernels  per pair, its slot in its (expert, key) bin copy; per
+//                  tile of 64 tokens, rows per slab and pairs per expert
+//                  (tile_cnt), and the pairs per expert
+//   scan_kernel    one workgroup per expert: pairs per expert, segments,
+//                  bin cursors; one per slab: the exclusive prefix of its
+//                  rows over the token tiles, and its total
+//   scatter_kernel one workgroup per token tile: pairs at their slots, and
+//                  every slab row (the tile's first row in the slab plus the
+//                  token's rank among the tile's tokens that use the slab,
+//                  from a ballot); one workgroup per (expert, block group):
+//                  the up tile table
 //
 // Each slab's row list starts at a multiple of the up-projection tile height
-// bm_up and holds the slab's pairs in pair order, with their tokens beside
-// them, so a tile's gather needs no dependent lookups. Up tiles are listed
-// expert by expert, and inside an expert by groups of blocks, then by the
-// stretch of the expert's pairs they cover (see up_tiles_of_group).
+// bm_up and holds the slab's pairs with their tokens beside them, so a
+// tile's gather needs no dependent lookups. Up tiles are listed expert by
+// expert, and inside an expert by groups of blocks, then by the token tile
+// in which they start (see up_tiles_of_group). Down tiles are described by
+// the down kernel itself from the expert segments.
 #pragma once
 #include "common.hpp"
 
 namespace unifmoe {
 
 constexpr int kScanThreads = 1024;
-constexpr int kChunk = 256;   // pairs per chunk of the ordered slab fill
-constexpr int kXcdSlices = 8; // the down tile table is split into one slice per XCD
+constexpr int kPermTok = 64;     // tokens per tile of the counts and the scatter (one wave)
 
 struct PermuteParams {
-    int N, K, B, key_bits, bm_up, bm_down, down_col_tiles, up_group;
+    int N, K, B, key_bits, bm_up, bm_down, down_col_tiles, up_group, ntile;
     const uint64_t* mask;
     const int* nres;
     const int* eids;
     const int* bin_count;
     int* bin_cursor;
-    const int* slab_count;
-    int* slab_off;
+    int* slab_count;    // [nslab] rows per slab (the scan's column sums)
+    int* tile_cnt;      // [ntile][nslab + K + 1] per-tile counts; the scan turns each slab column into
+                        // the tile's first row in the slab (exclusive prefix over tiles)
+    const int* exp_total;   // [kExpCopies][K + 1] pairs per expert
+    const int* pair_rank;   // [N][K + 1] slot of each pair within its bin copy
     int* seg_off;
-    int* up_tile_off;
     int* down_tile_off;  // [K+2] first down row tile of each expert segment
-    int* totals;  // [0] pairs P, [1] up tiles, [2] down tiles, [3] fill chunks, [4] down row tiles
+    int* totals;  // [0] pairs P, [1] up tiles, [2] down tiles, [4] down row tiles
     int* pair_token;
     uint64_t* pair_mask;
     int* pair_expert;
-    int* pair_of;  // [N][K+1]: pair of the shared expert, then of q_1..q_k
+    int* pair_of;  // [N][K+1]: the pairs of the shared expert and of q_1..q_k
     int* slab_rows;     // pair of each slab row (entries past a slab's count are unused)
     int* slab_tok;      // token of each slab row
     int* up_tile_info;  // per up tile: slab | rows << 16
     int* up_tile_rows;  // per up tile: first entry in slab_rows / slab_tok
-    int* chunk_off;     // [K+2] first chunk of each expert's pair segment
-    int* chunk_cnt;     // [chunks][B] pairs per block, then (scanned) first slab row
-    int4* rt_info;      // per down row tile: first pair, rows, expert, cost (see down_rowtile)
-    uint64_t* rt_masks; // per down row tile: mask union of each 16-row group, then of the tile
-    int* down_tiles;    // per down tile: row tile << 8 | column tile
-    int* down_slices;   // [9]: first down tile of each XCD's slice of the table, then the count
+    int4* rt_info;      // per down row tile: first pair, rows, expert
+    uint64_t* rt_masks; // per down row tile: mask union of each 32-row group, then of the tile
 };
 
 __global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n) {
@@ -78,22 +76,44 @@ __device__ int block_exclusive_scan(int n, Get get, Put put, int* lds) {
     const int tid = threadIdx.x, T = blockDim.x;
     const int per = ceil_div(n, T);
     const int beg = min(n, tid * per), end = min(n, beg + per);
+    // Up to 8 values per thread are loaded together into registers (their
+    // latencies overlap), longer chunks are read twice.
+    constexpr int R = 8;
+    int v[R];
+    if (per <= R) {
+#pragma unroll
+        for (int u = 0; u < R; ++u) v[u] = (beg + u < end) ? get(beg + u) : 0;
+    }
     int s = 0;
-    for (int i = beg; i < end; ++i) s += get(i);
+    if (per <= R) {
+#pragma unroll
+        for (int u = 0; u < R; ++u) s += v[u];
+    } else {
+        for (int i = beg; i < end; ++i) s += get(i);
+    }
     lds[tid] = s;
     __syncthreads();
     for (int off = 1; off < T; off <<= 1) {
-        const int v = (tid >= off) ? lds[tid - off] : 0;
+        const int x = (tid >= off) ? lds[tid - off] : 0;
         __syncthreads();
-        lds[tid] += v;
+        lds[tid] += x;
         __syncthreads();
     }
     int run = lds[tid] - s;
     const int total = lds[T - 1];
-    for (int i = beg; i < end; ++i) {
-        const int c = get(i);
-        put(i, run);
-        run += c;
+    if (per <= R) {
+#pragma unroll
+        for (int u = 0; u < R; ++u)
+            if (beg + u < end) {
+                put(beg + u, run);
+                run += v[u];
+            }
+    } else {
+        for (int i = beg; i < end; ++i) {
+            const int c = get(i);
+            put(i, run);
+            run += c;
+        }
     }
     __syncthreads();
     return total;
@@ -147,356 +167,287 @@ __device__ int staged_exclusive_scan(int n, Get get, Put put, int* stage, int* l
     return carry;
 }
 
-// One workgroup per expert, and one more. The routing kernel leaves the row
-// counts per slab and the pair counts per expert in kSlabCopies copies
-// (slab_count: [copy][nslab + K + 1]). Every workgroup sums the expert
-// counts into the segment offsets; workgroup e <= K scans its expert's bins
-// from its segment start; workgroup K + 1 builds the slab offsets and the
-// tile offsets meanwhile.
+// Workgroups [0, K]: expert segments (from the routing tiles' pair totals),
+// then expert e's bin cursors (its segment start plus the
+// exclusive prefix of its bins); workgroup 0 also writes the segments, the
+// down row-tile offsets and the totals. Workgroups past them: slab
+// sl = blockIdx.x - K - 1, its rows per token tile turned into each tile's
+// first row in the slab, and its total.
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
     __shared__ int lds[kScanThreads];
     __shared__ int stage[kScanStage];
     __shared__ int segs[66];   // K + 2 <= 66
     const int K1 = p.K + 1, nslab = K1 * p.B, ncnt = nslab + K1, nb = 1 << p.key_bits;
-    const int e = blockIdx.x;
-    int* cnt = const_cast<int*>(p.slab_count);
-    if ((int)threadIdx.x < K1) {
-        int v[kSlabCopies];
-#pragma unroll
-        for (int c = 0; c < kSlabCopies; ++c) v[c] = cnt[(size_t)c * ncnt + nslab + threadIdx.x];
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x, T = blockDim.x;
+    if (b >= K1) {
+        const int sl = b - K1;
+        const int total = block_exclusive_scan(
+            p.ntile, [&](int i) { return p.tile_cnt[(size_t)i * ncnt + sl]; },
+            [&](int i, int v) { p.tile_cnt[(size_t)i * ncnt + sl] = v; }, lds);
+        if (tid == 0) p.slab_count[sl] = total;
+        return;
+    }
+    // Pairs per expert: the routing tiles' totals.
+    if (tid < K1) {
         int n = 0;
 #pragma unroll
-        for (int c = 0; c < kSlabCopies; ++c) n += v[c];
-        lds[threadIdx.x] = n;
+        for (int c = 0; c < kExpCopies; ++c) n += p.exp_total[c * K1 + tid];
+        segs[tid] = n;
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
         int run = 0;
         for (int x = 0; x < K1; ++x) {
+            const int n = segs[x];
             segs[x] = run;
-            run += lds[x];
+            run += n;
         }
         segs[K1] = run;
     }
     __syncthreads();
-    if (e < K1) {
-        const int base = segs[e];
-        staged_exclusive_scan(
-            nb, [&](int i) { return p.bin_count[(size_t)e * nb + i]; },
-            [&](int i, int v) { p.bin_cursor[(size_t)e * nb + i] = base + v; }, stage, lds);
-        return;
+    if (b == 0) {
+        for (int x = tid; x <= K1; x += T) p.seg_off[x] = segs[x];
+        if (tid == 0) {
+            int run = 0;
+            for (int x = 0; x < K1; ++x) {
+                p.down_tile_off[x] = run;
+                run += ceil_div(segs[x + 1] - segs[x], p.bm_down);
+            }
+            p.down_tile_off[K1] = run;
+            p.totals[0] = segs[K1];
+            p.totals[2] = run * p.down_col_tiles;
+            p.totals[4] = run;
+        }
     }
-    for (int x = threadIdx.x; x <= K1; x += blockDim.x) p.seg_off[x] = segs[x];
-    const int P = segs[K1];
-    // Row counts per slab: sum the copies into the first.
-    for (int i = threadIdx.x; i < nslab; i += blockDim.x) {
-        int v[kSlabCopies];
-#pragma unroll
-        for (int c = 0; c < kSlabCopies; ++c) v[c] = cnt[(size_t)c * ncnt + i];
-        int n = 0;
-#pragma unroll
-        for (int c = 0; c < kSlabCopies; ++c) n += v[c];
-        cnt[i] = n;
-    }
-    __syncthreads();
-    const int bm = p.bm_up;
-    const int nup = staged_exclusive_scan(
+    // Expert b's bins, each as kBinCopies consecutive counters.
+    const int base = segs[b];
+    const size_t off = (size_t)b * nb * kBinCopies;
+    staged_exclusive_scan(
+        nb * kBinCopies, [&](int i) { return p.bin_count[off + i]; },
+        [&](int i, int v) { p.bin_cursor[off + i] = base + v; }, stage, lds);
+}
+
+// Slab offsets, in LDS (each scatter workgroup computes them): slab sl
+// starts at so[sl] (a multiple of bm_up) and its up tiles at uo[sl]
+// (so[nslab], uo[nslab]: the totals). Workgroup 0 records the up tile count.
+__device__ __forceinline__ void slab_offsets(const PermuteParams& p, int* so, int* uo, int* lds) {
+    const int nslab = (p.K + 1) * p.B, bm = p.bm_up;
+    const int nup = block_exclusive_scan(
         nslab, [&](int i) { return ceil_div(p.slab_count[i], bm); },
         [&](int i, int v) {
-            p.up_tile_off[i] = v;
-            p.slab_off[i] = v * bm;
+            uo[i] = v;
+            so[i] = v * bm;
         },
-        stage, lds);
+        lds);
     if (threadIdx.x == 0) {
-        p.slab_off[nslab] = nup * bm;
-        p.up_tile_off[nslab] = nup;
-        if (p.chunk_off != nullptr) {
-            int q = 0;
-            for (int x = 0; x < K1; ++x) {
-                p.chunk_off[x] = q;
-                q += ceil_div(segs[x + 1] - segs[x], kChunk);
-            }
-            p.chunk_off[K1] = q;
-            p.totals[3] = q;
-        }
-        int run = 0;
-        for (int x = 0; x < K1; ++x) {
-            p.down_tile_off[x] = run;
-            run += ceil_div(segs[x + 1] - segs[x], p.bm_down);
-        }
-        p.down_tile_off[K1] = run;
-        p.totals[0] = P;
-        p.totals[1] = nup;
-        p.totals[2] = run * p.down_col_tiles;
-        p.totals[4] = run;
+        uo[nslab] = nup;
+        so[nslab] = nup * bm;
+        if (blockIdx.x == 0) p.totals[1] = nup;
     }
+    __syncthreads();
 }
 
-// One thread per token writes its pairs at bin start + the slot the routing
-// kernel took for each (stored in pair_of, overwritten here with the pair).
-__global__ void scatter_kernel(PermuteParams p) {
-    const int t = blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= p.N) return;
-    const int k = p.nres[t];
-    if (k == 0) return;  // padded token (valid tokens have k >= 1)
-    const int B = p.B, kb = p.key_bits, K1 = p.K + 1;
-    const uint64_t full = (B == 64) ? ~0ull : ((1ull << B) - 1ull);
-    const uint64_t m = p.mask[t], rm = ~m & full;
-    const int ks = mask_key(m, B, kb);
-    const int kr = mask_key(rm, B, kb);
-    int* of = p.pair_of + (size_t)t * K1;
-    const int* eid = p.eids + (size_t)t * p.K;
-    const int pr = p.bin_cursor[ks] + of[0];
-    // Residual pairs in batches: every load of a batch (experts, slots, bin
-    // cursors) is issued before its stores, which the compiler may not move
-    // loads across.
-    constexpr int kBatch = 8;
-    for (int i0 = 0; i0 < k; i0 += kBatch) {
-        int e[kBatch], q[kBatch];
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            e[u] = (i0 + u < k) ? eid[i0 + u] : 0;
-            q[u] = (i0 + u < k) ? of[1 + i0 + u] : 0;
-        }
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u)
-            if (i0 + u < k) q[u] += p.bin_cursor[(e[u] << kb) + kr];
-        if (i0 == 0) {
-            p.pair_token[pr] = t;
-            p.pair_mask[pr] = m;
-            p.pair_expert[pr] = 0;
-            of[0] = pr;
-        }
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            if (i0 + u < k) {
-                p.pair_token[q[u]] = t;
-                p.pair_mask[q[u]] = rm;
-                p.pair_expert[q[u]] = e[u];
-                of[1 + i0 + u] = q[u];
-            }
-        }
-    }
-}
-
-// Up tile table, built once the slab rows of every chunk are known. Tiles
-// are listed expert by expert; inside an expert the blocks are taken in
-// groups of up_group, and inside a group tile j of block c is placed by the
-// chunk q of the expert's pairs in which its first row falls, then by c,
-// then by j. Tiles that run close together in this order gather the token
-// rows of the same stretch of the expert's pairs, which a group's weight
-// slabs share in L2. One workgroup per (expert, group); each thread takes a
-// contiguous range of the expert's chunks. tile_lo(i, c) is the first tile
-// of slab c whose first row is at or after chunk i's first slab row.
-__device__ __forceinline__ void up_tiles_of_group(const PermuteParams& p, int grp, int* lds) {
+// Up tile table. Tiles are listed expert by expert; inside an expert the
+// blocks are taken in groups of up_group, and inside a group tile j of block
+// c is placed by the chunk of token tiles in which its first row falls, then
+// by c, then by j. Tiles that run close together in this order gather the
+// token rows of the same stretch of tokens, which a group's weight slabs
+// share in L2. One workgroup per (expert, group). A chunk is CH token tiles,
+// CH chosen so that the group's first up tile of every chunk,
+// tl[i][c] = ceil(first row of chunk i in slab c / bm_up), fits in
+// kUpTableWords words of LDS; these are loaded first (coalesced), then each
+// thread takes a contiguous range of chunks.
+constexpr int kUpTableWords = 8192;
+__device__ __forceinline__ void up_tiles_of_group(const PermuteParams& p, int grp, const int* so, const int* uo,
+                                                  int* lds) {
     const int ngr = ceil_div(p.B, p.up_group);
     const int e = grp / ngr, g = grp - e * ngr;
-    const int c0 = g * p.up_group, c1 = min(p.B, c0 + p.up_group);
-    const int q0 = p.chunk_off[e], nq = p.chunk_off[e + 1] - q0;
+    const int c0 = g * p.up_group, c1 = min(p.B, c0 + p.up_group), ng = c1 - c0;
+    const int ncnt = (p.K + 1) * (p.B + 1);
     const int bm = p.bm_up, sl0 = e * p.B;
-    auto tile_lo = [&](int i, int c) {
-        const int sl = sl0 + c;
-        const int r = (i < nq) ? p.chunk_cnt[(size_t)(q0 + i) * p.B + c] - p.slab_off[sl] : p.slab_count[sl];
-        return ceil_div(r, bm);
-    };
+    // (nq + 1) ng <= (ntile / CH + 2) ng < kUpTableWords, since ng <= 64)
+    const int CH = max(1, ceil_div((p.ntile + 1) * ng, kUpTableWords - 256));
+    const int nq = ceil_div(p.ntile, CH);
+    int* tl = lds;                           // [nq + 1][ng]
+    int* scan = lds + kUpTableWords;         // blockDim.x words
+    batched_copy(
+        (nq + 1) * ng,
+        [&](int x) {
+            const int i = x / ng, sl = sl0 + c0 + x - i * ng;
+            return (i < nq) ? p.tile_cnt[(size_t)i * CH * ncnt + sl] : p.slab_count[sl];
+        },
+        [&](int x, int r) { tl[x] = ceil_div(r, bm); });
+    __syncthreads();
     const int tid = threadIdx.x, T = blockDim.x;
     const int per = ceil_div(nq, T);
     const int qa = min(nq, tid * per), qb = min(nq, qa + per);
     int n = 0;
-    for (int c = c0; c < c1; ++c) n += tile_lo(qb, c) - tile_lo(qa, c);
-    lds[tid] = n;
+    for (int c = 0; c < ng; ++c) n += tl[qb * ng + c] - tl[qa * ng + c];
+    scan[tid] = n;
     __syncthreads();
     for (int off = 1; off < T; off <<= 1) {
-        const int v = (tid >= off) ? lds[tid - off] : 0;
+        const int v = (tid >= off) ? scan[tid - off] : 0;
         __syncthreads();
-        lds[tid] += v;
+        scan[tid] += v;
         __syncthreads();
     }
-    int pos = p.up_tile_off[sl0 + c0] + lds[tid] - n;
+    int pos = uo[sl0 + c0] + scan[tid] - n;
     for (int i = qa; i < qb; ++i)
-        for (int c = c0; c < c1; ++c) {
-            const int sl = sl0 + c, cnt = p.slab_count[sl];
-            for (int j = tile_lo(i, c), je = tile_lo(i + 1, c); j < je; ++j, ++pos) {
+        for (int c = 0; c < ng; ++c) {
+            const int sl = sl0 + c0 + c, cnt = p.slab_count[sl], s0 = so[sl];
+            for (int j = tl[i * ng + c], je = tl[(i + 1) * ng + c]; j < je; ++j, ++pos) {
                 p.up_tile_info[pos] = sl | (min(bm, cnt - j * bm) << 16);
-                p.up_tile_rows[pos] = p.slab_off[sl] + j * bm;
+                p.up_tile_rows[pos] = s0 + j * bm;
             }
         }
     __syncthreads();
 }
 
-// Down row tiles: bm_down consecutive pairs of one expert segment. One wave
-// per row tile records its first pair, row count and expert, and the union
-// of the block masks of each 16-row group and of the whole tile. Down tiles
-// (row tile x column tile of d) are listed row tile by row tile: the column
-// tiles of one row tile run side by side on one XCD and read its H rows
-// from HBM once.
-__device__ __forceinline__ void down_rowtile(const PermuteParams& p, int rt) {
-    const int e = upper_index(p.down_tile_off, p.K + 1, rt);
-    const int p0 = p.seg_off[e] + (rt - p.down_tile_off[e]) * p.bm_down;
-    const int nrows = min(p.bm_down, p.seg_off[e + 1] - p0);
-    const int lane = threadIdx.x & 63, G = p.bm_down / 16;
-    uint64_t* out = p.rt_masks + (size_t)rt * (G + 1);
-    uint64_t all = 0;
-    int groups = 0;   // blocks summed over the 32-row MFMA groups (lanes 0 and 32)
-    for (int h = 0; h * 64 < p.bm_down; ++h) {
-        const int r = h * 64 + lane;
-        uint64_t m = r < nrows ? p.pair_mask[p0 + r] : 0ull;
-        for (int o = 1; o < 16; o <<= 1) m |= shfl_xor64(m, o);
-        if ((lane & 15) == 0) out[h * 4 + (lane >> 4)] = m;
-        all |= m;
-        const uint64_t m32 = m | shfl_xor64(m, 16);
-        if ((lane & 31) == 0) groups += __popcll(m32);
-    }
-    for (int o = 16; o < 64; o <<= 1) all |= shfl_xor64(all, o);
-    groups += __shfl_xor(groups, 32);
-    if (lane == 0) {
-        out[G] = all;
-        // Cost estimate for balancing the XCD slices: the MFMA work (blocks
-        // over the 32-row groups) plus a per-stage share for the copies
-        // every stage of the tile's union makes.
-        p.rt_info[rt] = make_int4(p0, nrows, e, groups + 4 * __popcll(all));
-    }
-    for (int ct = lane; ct < p.down_col_tiles; ct += 64)
-        p.down_tiles[(size_t)rt * p.down_col_tiles + ct] = (rt << 8) | ct;
-}
-
-
-
-// Chunk q of expert e covers pairs [seg_off[e] + (q - chunk_off[e]) kChunk, ...)
-// of the expert's segment. One workgroup of kChunk threads per chunk, one
-// thread per pair; workgroups past the chunk count exit.
-struct ChunkView {
-    int e, lo, hi;
-};
-__device__ __forceinline__ ChunkView chunk_view(const PermuteParams& p, int q) {
-    ChunkView v;
-    v.e = upper_index(p.chunk_off, p.K + 1, q);
-    v.lo = p.seg_off[v.e] + (q - p.chunk_off[v.e]) * kChunk;
-    v.hi = min(v.lo + kChunk, p.seg_off[v.e + 1]);
-    return v;
-}
-
-// Pairs of the workgroup's waves that use each block (wave ballots).
-__device__ __forceinline__ void chunk_wave_counts(int B, uint64_t m, int (*wc)[64]) {
-    const int w = threadIdx.x >> 6;
-    for (int c = 0; c < B; ++c) {
-        const uint64_t bits = ballot(((m >> c) & 1ull) != 0ull);
-        if (lane_id() == 0) wc[w][c] = __popcll(bits);
-    }
-}
-
-// The two tables that only need the scatter's output, in one launch (each
-// is small; a kernel launch costs more than their work): workgroups [0, g1)
-// build the down row tiles (one wave per row tile), the rest count the
-// chunks' rows per block.
-__global__ __launch_bounds__(256) void tables_kernel(PermuteParams p, int g1) {
-    static_assert(kChunk == 256, "one thread per chunk pair");
-    __shared__ int wc[kChunk / 64][64];
-    const int b = blockIdx.x;
-    if (b < g1) {
-        const int nrt = p.totals[4];
-        for (int rt = b * 4 + (threadIdx.x >> 6); rt < nrt; rt += g1 * 4) down_rowtile(p, rt);
-    } else {
-        const int g2 = gridDim.x - g1, nq = p.totals[3];
-        for (int q = b - g1; q < nq; q += g2) {
-            const ChunkView v = chunk_view(p, q);
-            const int pr = v.lo + (int)threadIdx.x;
-            chunk_wave_counts(p.B, pr < v.hi ? p.pair_mask[pr] : 0ull, wc);
-            __syncthreads();
-            if ((int)threadIdx.x < p.B) {
-                int n = 0;
-                for (int w = 0; w < kChunk / 64; ++w) n += wc[w][threadIdx.x];
-                p.chunk_cnt[(size_t)q * p.B + threadIdx.x] = n;
+// One workgroup of kScatterWaves waves per token tile (lane = token). Each
+// pair goes to its bin copy's cursor plus the slot the routing kernel took.
+// Wave w takes the residual pairs i = w, w + kScatterWaves, .. of the tile's
+// tokens (wave 0 also the shared pairs). Then, slab by slab, the tile's
+// tokens that use the slab take consecutive rows from the tile's first row
+// in it, in token order (ballot ranks), so every slab lists its tokens in
+// token order; wave w takes experts w, w + kScatterWaves, .. The tokens'
+// pairs per expert and the tile's first rows are staged in LDS.
+constexpr int kScatterWaves = 4;
+__device__ __forceinline__ void scatter_tile(const PermuteParams& p, int q, const int* so, int* pidx, int* first) {
+    const int lane = lane_id(), t = q * kPermTok + lane;
+    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    const int K = p.K, K1 = K + 1, B = p.B, kb = p.key_bits, nslab = K1 * B;
+    const int ncnt = nslab + K1;
+    const bool in = t < p.N;
+    const int k = in ? p.nres[t] : 0;   // 0 for padded tokens (valid tokens have k >= 1)
+    const bool v = k > 0;
+    const uint64_t full = (B == 64) ? ~0ull : ((1ull << B) - 1ull);
+    const uint64_t m = v ? p.mask[t] : 0ull, rm = ~m & full;
+    int* of = p.pair_of + (size_t)(v ? t : 0) * K1;
+    const int* eid = p.eids + (size_t)(v ? t : 0) * K;
+    const bool slabs = p.slab_rows != nullptr;   // no slab lists for fp32 layers
+    // The tile's first row in each slab (absolute), read while the pairs'
+    // atomics are in flight.
+    const int* tfirst = p.tile_cnt + (size_t)q * ncnt;
+    if (slabs)
+        batched_copy(nslab, [&](int sl) { return tfirst[sl]; }, [&](int sl, int v) { first[sl] = so[sl] + v; });
+    uint64_t sel = 0;
+    const int bc = q % kBinCopies;   // the bin copy of this token tile
+    if (v) {
+        const int kr = mask_key(rm, B, kb);
+        // This wave's residual pairs, in batches: every atomic of a batch is
+        // issued before its results are used.
+        constexpr int kBatch = 4;
+        const int* rank = p.pair_rank + (size_t)t * K1;
+        for (int i0 = wave; i0 < k; i0 += kBatch * kScatterWaves) {
+            int e[kBatch], r[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int i = i0 + u * kScatterWaves;
+                e[u] = (i < k) ? eid[i] : 0;
+                r[u] = (i < k) ? rank[1 + i] : 0;
             }
-            __syncthreads();
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u)
+                if (i0 + u * kScatterWaves < k) r[u] += p.bin_cursor[((e[u] << kb) + kr) * kBinCopies + bc];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int i = i0 + u * kScatterWaves;
+                if (i < k) {
+                    p.pair_token[r[u]] = t;
+                    p.pair_mask[r[u]] = rm;
+                    p.pair_expert[r[u]] = e[u];
+                    of[1 + i] = r[u];
+                    pidx[lane * K1 + e[u]] = r[u];
+                }
+            }
         }
+        if (wave == 0) {
+            const int pr = p.bin_cursor[mask_key(m, B, kb) * kBinCopies + bc] + p.pair_rank[(size_t)t * K1];
+            p.pair_token[pr] = t;
+            p.pair_mask[pr] = m;
+            p.pair_expert[pr] = 0;
+            of[0] = pr;
+            pidx[lane * K1] = pr;
+        }
+        for (int i = 0; i < k; ++i) sel |= 1ull << (eid[i] - 1);
     }
-}
-
-// The down tile table is split into one contiguous slice per XCD with equal
-// estimated cost (rt_info[].w per tile of a row tile), not equal tile
-// counts: the shared expert's row tiles, listed first, are cheaper. Slice x
-// starts at the first tile whose preceding cost reaches x/8 of the total.
-__device__ __forceinline__ void down_slices(const PermuteParams& p, int* lds) {
-    const int nrt = p.totals[4], ncol = p.down_col_tiles;
-    const int total = block_exclusive_scan(
-        nrt, [&](int i) { return p.rt_info[i].w * ncol; }, [&](int, int) {}, lds);
-    if (threadIdx.x == 0) {
-        p.down_slices[0] = 0;
-        p.down_slices[kXcdSlices] = nrt * ncol;
-        for (int x = 1; x < kXcdSlices; ++x)
-            if ((int64_t)x * total / kXcdSlices == 0) p.down_slices[x] = 0;
-    }
-    block_exclusive_scan(
-        nrt, [&](int i) { return p.rt_info[i].w * ncol; },
-        [&](int i, int v) {
-            const int c = p.rt_info[i].w;
-            for (int x = 1; x < kXcdSlices; ++x) {
-                const int target = (int)((int64_t)x * total / kXcdSlices);
-                if (target > v && target <= v + ncol * c)
-                    p.down_slices[x] = i * ncol + (target - v + c - 1) / c;
-            }
-        },
-        lds);
-}
-
-// One workgroup per slab: its chunks' counts become the slab row at which
-// each chunk's pairs start. One more workgroup splits the down tile table
-// into the XCD slices.
-__global__ __launch_bounds__(256) void chunk_scan_kernel(PermuteParams p) {
-    __shared__ int lds[256];
-    if ((int)blockIdx.x == (p.K + 1) * p.B) {
-        down_slices(p, lds);
-        return;
-    }
-    const int sl = blockIdx.x;
-    const int e = sl / p.B, c = sl - e * p.B;
-    const int q0 = p.chunk_off[e], nq = p.chunk_off[e + 1] - q0;
-    const int base = p.slab_off[sl];
-    int* cnt = p.chunk_cnt + (size_t)q0 * p.B + c;
-    block_exclusive_scan(
-        nq, [&](int i) { return cnt[(size_t)i * p.B]; }, [&](int i, int v) { cnt[(size_t)i * p.B] = base + v; },
-        lds);
-}
-
-// first[c]: the chunk's first row in slab c, staged in LDS so that the
-// store loop below carries no global loads.
-__device__ __forceinline__ void slabfill_chunk(const PermuteParams& p, int q, int (*wc)[64], int* first) {
-    const ChunkView v = chunk_view(p, q);
-    const int pr = v.lo + (int)threadIdx.x;
-    const bool act = pr < v.hi;
-    const uint64_t m = act ? p.pair_mask[pr] : 0ull;
-    const int tok = act ? p.pair_token[pr] : 0;
-    if ((int)threadIdx.x < p.B) first[threadIdx.x] = p.chunk_cnt[(size_t)q * p.B + threadIdx.x];
-    chunk_wave_counts(p.B, m, wc);
+    if (!slabs) return;
     __syncthreads();
-    const int w = threadIdx.x >> 6;
-    for (int c = 0; c < p.B; ++c) {
-        const bool use = ((m >> c) & 1ull) != 0ull;
-        const uint64_t bits = ballot(use);
-        if (use) {
-            int at = first[c] + __popcll(bits & lanes_below());
-            for (int w2 = 0; w2 < w; ++w2) at += wc[w2][c];
-            p.slab_rows[at] = pr;
-            p.slab_tok[at] = tok;
+    // Slab rows of this wave's experts (an expert none of the tile's tokens
+    // uses is skipped whole).
+    const uint64_t below = lanes_below();
+    for (int e = wave; e <= K; e += kScatterWaves) {
+        const bool he = (e == 0) ? v : ((sel >> (e - 1)) & 1ull) != 0ull;
+        if (!ballot(he)) continue;
+        const uint64_t me = (e == 0) ? m : rm;
+        const int pr = he ? pidx[lane * K1 + e] : 0;
+        for (int c = 0; c < B; ++c) {
+            const bool has = he && ((me >> c) & 1ull);
+            const uint64_t bits = ballot(has);
+            if (!bits) continue;
+            if (has) {
+                const int at = first[e * B + c] + __popcll(bits & below);
+                p.slab_rows[at] = pr;
+                p.slab_tok[at] = t;
+            }
         }
     }
 }
 
 // Workgroups [0, n_groups) build the up tile table of one (expert, block
-// group) each; the rest fill the chunks' slab rows.
-__global__ __launch_bounds__(kChunk) void slabfill_kernel(PermuteParams p, int n_groups) {
-    __shared__ int wc[kChunk / 64][64];
-    __shared__ int first[64];
+// group) each; the rest scatter one token tile each.
+__global__ __launch_bounds__(kScatterWaves * 64) void scatter_kernel(PermuteParams p, int n_groups) {
+    // LDS: slab and up tile offsets ([nslab + 1] each), then the role's
+    // words: the tokens' pairs [64][K+1] and the tile's first rows [nslab],
+    // or the up table's inputs.
+    extern __shared__ int lds_sc[];
+    const int nslab = (p.K + 1) * p.B;
+    int* so = lds_sc;
+    int* uo = so + nslab + 1;
+    int* rest = uo + nslab + 1;
+    if (p.slab_rows != nullptr) slab_offsets(p, so, uo, rest);
     const int b = blockIdx.x;
     if (b < n_groups) {
-        up_tiles_of_group(p, b, &wc[0][0]);
+        up_tiles_of_group(p, b, so, uo, rest);
         return;
     }
-    const int nq = p.totals[3];
-    for (int q = b - n_groups; q < nq; q += gridDim.x - n_groups) {
-        slabfill_chunk(p, q, wc, first);
-        __syncthreads();
+    scatter_tile(p, b - n_groups, so, rest, rest + 64 * (p.K + 1));
+}
+
+// Down row tiles: bm_down consecutive pairs of one expert segment. One wave
+// per row tile records its first pair, row count and expert, and the union
+// of the block masks of each 32-row group and of the whole tile (the down
+// kernel contracts over the tile's union and skips, per 32-row MFMA group,
+// the blocks none of its rows use).
+__global__ __launch_bounds__(256) void down_tables_kernel(PermuteParams p) {
+    const int nrt = p.totals[4], G = p.bm_down / 32;
+    const int lane = lane_id();
+    for (int rt = blockIdx.x * 4 + ((int)threadIdx.x >> 6); rt < nrt; rt += gridDim.x * 4) {
+        const int e = upper_index(p.down_tile_off, p.K + 1, rt);
+        const int p0 = p.seg_off[e] + (rt - p.down_tile_off[e]) * p.bm_down;
+        const int nrows = min(p.bm_down, p.seg_off[e + 1] - p0);
+        uint64_t* out = p.rt_masks + (size_t)rt * (G + 1);
+        uint64_t m[4];   // bm_down <= 256: rows h * 64 + lane
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+            const int r = h * 64 + lane;
+            m[h] = (h * 64 < p.bm_down && r < nrows) ? p.pair_mask[p0 + r] : 0ull;
+        }
+        uint64_t all = 0;
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+            uint64_t g = m[h];
+#pragma unroll
+            for (int o = 1; o < 32; o <<= 1) g |= shfl_xor64(g, o);
+            if ((lane & 31) == 0 && h * 64 < p.bm_down) out[h * 2 + (lane >> 5)] = g;
+            all |= g;
+        }
+        all |= shfl_xor64(all, 32);
+        if (lane == 0) {
+            out[G] = all;
+            p.rt_info[rt] = make_int4(p0, nrows, e, 0);
+        }
     }
 }
 

@@ -1,21 +1,24 @@
 // Fused routing kernel (Sec. III-B and III-C): router logits, shared demand,
 // shared block count and prototype selection, residual softmax, sort,
-// cumulative-mass expert count, and the per-(expert, block) counts that the
+// cumulative-mass expert count, and the per-tile counts that the
 // permutation needs.
 //
-// One workgroup of two waves routes 128 tokens. Phase 1 computes the
-// 1 + K + B logits of each token (x W_shr, x W_1..x W_K, x mu_1..x mu_B)
-// into LDS:
+// Phase 1 computes the 1 + K + B logits of each token (x W_shr, x W_1..x W_K,
+// x mu_1..x mu_B) into LDS:
 //   * bf16 tokens: x W_1.., x mu_1.. on the matrix cores. The fp32 router
 //     and prototype weights are pre-split into three bf16 parts (hi + mid +
 //     lo carries all 24 significand bits), so every bf16 x bf16 product is
 //     exact and only the fp32 accumulation order differs from a sequential
 //     dot product. x W_shr is an fp32 dot product on the vector units.
 //   * fp32 tokens: sequential fp32 FMA dot products.
-// Phase 2 takes one token per lane and runs the decisions in the paper's
-// order in fp32 with explicitly rounded operations; ties break toward the
-// lower index. The per-(expert, block) row counts are gathered with wave
-// ballots into LDS, then added to global memory once per workgroup.
+// Phase 2 decides each token with a group of 16, 32 or 64 lanes (one lane
+// per expert and per block) using wave-level exchanges: a butterfly maximum
+// and index-order broadcast sums for the softmax, broadcast comparisons for
+// the rankings (ties toward the lower index), a lane permute for the sort
+// and an in-order prefix with a ballot for the cumulative-mass count. Every
+// step is the paper's order in fp32 with explicitly rounded operations.
+// Per tile of 64 tokens, the rows per (expert, block) slab and the pairs per
+// expert are counted in LDS and written out for the permutation.
 #pragma once
 #include "common.hpp"
 
@@ -23,12 +26,11 @@ namespace unifmoe {
 
 constexpr int kRouteTok = 128;
 // 4 waves: in the logits, wave w takes tokens 64 (w & 1).. and half (w >> 1)
-// of the k range; then waves 0 and 1 take one token per thread.
+// of the k range; then all four share each tile's decisions.
 constexpr int kRouteThreads = 256;
 
 struct RouteParams {
     int N, d, K, B, NL, NLP, lstride, key_bits;
-    int key_stride;     // words per token of the LDS ranking keys, 0 if none
     float tau, one_minus_2tau, t_mass, alpha_fixed;
     int max_shared, alpha_mode, mass_mode, fixed_k, select_mode;
     const void* X;
@@ -42,9 +44,11 @@ struct RouteParams {
     int* nres;
     int* eids;
     float* wts;
-    int* bin_count;   // [(K+1) << key_bits] pairs per (expert, mask key), or null
-    int* slab_count;  // [kSlabCopies][(K+1) B + K+1]: rows per (expert, block), then pairs per expert; or null
-    int* pair_rank;   // [N][K+1]: slot of each pair within its (expert, key) bin (with bin_count)
+    int* bin_count;   // [(K+1) << key_bits][kBinCopies] pairs per (expert, mask key), or null
+    int* tile_cnt;    // [ceil(N / kTileTok)][(K+1) B + K+1]: per tile of tokens, rows per (expert, block)
+                      // slab, then pairs per expert; or null
+    int* exp_total;   // [kExpCopies][K+1] pairs per expert (tile i adds into copy i % kExpCopies)
+    int* pair_rank;   // [N][K+1]: slot of each pair within its bin copy
 };
 
 // Exact three-way split of an fp32 value into bf16 parts, in workgroups
@@ -205,9 +209,6 @@ __device__ __forceinline__ void route_logits_f32(const RouteParams& p, float* L,
     }
 }
 
-// Words per token of the ranking keys: max(K, B) rounded up to 4.
-__host__ __device__ __forceinline__ int key_row(int K, int B) { return ((K > B ? K : B) + 3) & ~3; }
-
 // Total-order key of a float for ranking: for non-NaN values it orders as
 // the float comparison does (-0 is first mapped to +0, so the two tie), and
 // a NaN gets a fixed place, so ranks computed with it always form a
@@ -217,335 +218,261 @@ __device__ __forceinline__ uint32_t rank_key(float f) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Rank of entry j among the n keys of a row (16-byte aligned, zero-padded to
-// a multiple of 4): the number of entries that come before it in decreasing
-// key order, ties to the lower index. Padding keys are 0 and sit at indices
-// >= n, so they never come first.
-__device__ __forceinline__ int rank_in_row(const uint32_t* keys, int n, int j) {
-    const uint32_t kj = keys[j];
-    int rank = 0;
-    for (int c = 0; c < n; c += 4) {
-        const u32x4 k4 = *reinterpret_cast<const u32x4*>(keys + c);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) rank += (k4[q] > kj) || (k4[q] == kj && c + q < j);
-    }
-    return rank;
+// Tokens are decided in tiles of kTileTok (one wave's ballot); the
+// permutation's per-tile counts use the same tiles.
+constexpr int kTileTok = 64;
+
+// Lanes per token in the decisions: the smallest power of two >= max(K, B),
+// at least 16.
+__host__ __device__ __forceinline__ int decide_lanes(int K, int B) {
+    const int n = K > B ? K : B;
+    return n <= 16 ? 16 : (n <= 32 ? 32 : 64);
 }
 
-// The same from the float values (no key row).
-__device__ __forceinline__ int rank_in_values(const float* v, int n, int j) {
-    const uint32_t kj = rank_key(v[j]);
-    int rank = 0;
-    for (int c = 0; c < n; ++c) {
-        const uint32_t kc = rank_key(v[c]);
-        rank += (kc > kj) || (kc == kj && c < j);
-    }
-    return rank;
-}
-
-constexpr int kRankBatch = 8;   // residual-pair atomics in flight per token
-
-// Rankings of at most this many entries run on registers.
-constexpr int kSmallRank = 16;
-
-// Decisions for token tok0 + tid, one token per lane of whole waves (the
-// counting below merges the lanes of a wave).
-__device__ __forceinline__ void route_decide(const RouteParams& p, float* L, float* PS, int* QS, uint32_t* KEYS,
-                                             int* slab_lds, int tok0, int tid) {
-    const int K = p.K, B = p.B, tok = tok0 + tid;
-    const bool in_range = tok < p.N;
+// Decisions of Sec. III-B and III-C for 64 / L tokens of one tile per call,
+// L lanes per token (lane j of a token's group stands for expert j + 1 and
+// block j), with wave-level exchanges instead of per-token loops:
+//   alpha, b          every lane of the group, from the shared logit
+//   I_shr             lane c ranks x mu_c against the other B priorities
+//                     (broadcasts in index order, ties to the lower index)
+//   softmax           group maximum (butterfly), then the sum of the
+//                     exponentials in index order (broadcasts), fp32
+//   q, p              lane j ranks s_j; a permute sends (s_j, j + 1) to lane
+//                     rank(j), so lane r then holds p_r and q_r
+//   P_r, k            lane r sums p_0..p_r in order; k is the first lane
+//                     whose prefix reaches the target (ballot), else K
+// All arithmetic is the paper's order in fp32 with explicitly rounded
+// operations. `row` is the token's logit row in LDS (shared logit, K expert
+// logits, B priorities); `t` the token's index in the tile (tokens at or past
+// `ntok` are outside the layer and write nothing); `cnt` the tile's LDS
+// counters (rows per (expert, block) slab, then pairs per expert), or null.
+template <int L>
+__device__ __forceinline__ void decide_group(const RouteParams& p, const float* row, int tok0, int t, int ntok,
+                                             int* cnt) {
+    static_assert(L == 16 || L == 32 || L == 64, "lane groups");
+    const int K = p.K, B = p.B;
+    const int lane = lane_id(), j = lane & (L - 1), gbase = lane - j;
+    const int tok = tok0 + t;
+    const bool in_range = t < ntok;
     const bool v = in_range && (p.valid == nullptr || p.valid[tok] != 0);
-    float* row = L + tid * p.lstride;
-    float* ps = PS + tid * (K + 1);
-    int* qs = QS + tid * (K + 1);
-    // Ranking keys: a 16-byte-aligned row per token when the workgroup's
-    // LDS has room for them (kp > 0), else ranked straight from the values.
-    const int kp = p.key_stride;
-    uint32_t* keys = KEYS + tid * kp;
-    uint64_t mask = 0, sel = 0;
-    int k = 0;
-    if (v) {
-        // Eq. alpha (adaptive) or the fixed-alpha ablation.
-        float alpha;
-        if (p.alpha_mode == 0) {
-            const float sig = __fdiv_rn(1.0f, __fadd_rn(1.0f, expf(-row[0])));
-            alpha = __fadd_rn(p.tau, __fmul_rn(p.one_minus_2tau, sig));
-        } else {
-            alpha = p.alpha_fixed;
+    const uint64_t gmask = (L == 64) ? ~0ull : ((1ull << L) - 1ull);
+    auto group_bits = [&](bool pred) { return (ballot(pred) >> gbase) & gmask; };
+
+    // Eq. alpha (adaptive) or the fixed-alpha ablation.
+    float alpha;
+    if (p.alpha_mode == 0) {
+        const float sig = __fdiv_rn(1.0f, __fadd_rn(1.0f, expf(-row[0])));
+        alpha = __fadd_rn(p.tau, __fmul_rn(p.one_minus_2tau, sig));
+    } else {
+        alpha = p.alpha_fixed;
+    }
+    // Eq. block-count, half to even; clamp to [1, B-1] (adaptive), cap.
+    // (fminf/fmaxf drop a NaN alpha, so b stays in range for any input.)
+    int b = (int)rintf(fminf(fmaxf(__fmul_rn((float)B, alpha), 0.0f), (float)B));
+    if (p.alpha_mode == 0) b = min(max(b, 1), B - 1);
+    b = min(b, p.max_shared);
+
+    // Eq. block-priority / shared-indices: block j is shared when fewer than
+    // b priorities come before it (decreasing, ties to the lower index).
+    bool shared;
+    if (p.select_mode == 0) {
+        const uint32_t uk = j < B ? rank_key(row[1 + K + j]) : 0u;
+        int ru = 0;
+#pragma unroll 16
+        for (int c = 0; c < L; ++c) {
+            const uint32_t o = (uint32_t)__shfl((int)uk, gbase + c);
+            ru += (o > uk) || (o == uk && c < j);
         }
-        // Eq. block-count, half to even; clamp to [1, B-1] (adaptive), cap.
-        // (fminf/fmaxf drop a NaN alpha, so b stays in range for any input.)
-        int b = (int)rintf(fminf(fmaxf(__fmul_rn((float)B, alpha), 0.0f), (float)B));
-        if (p.alpha_mode == 0) b = min(max(b, 1), B - 1);
-        b = min(b, p.max_shared);
-        // Eq. block-priority / shared-indices: the b largest x mu_c.
-        if (p.select_mode == 0) {
-            const float* u = row + 1 + K;
-            if (B <= kSmallRank) {
-                // All keys in registers; padding keys 0 never come first.
-                uint32_t uk[kSmallRank];
+        shared = j < B && ru < b;
+    } else {
+        shared = j < b;
+    }
+    const uint64_t mask = group_bits(shared);
+
+    // Eq. residual-router-score: max-subtracted softmax, index-order sum.
+    const float l = j < K ? row[1 + j] : -INFINITY;
+    float m = l;
 #pragma unroll
-                for (int c = 0; c < kSmallRank; ++c) uk[c] = c < B ? rank_key(u[c]) : 0u;
-#pragma unroll
-                for (int c = 0; c < kSmallRank; ++c) {
-                    int rank = 0;
-#pragma unroll
-                    for (int c2 = 0; c2 < kSmallRank; ++c2) rank += (uk[c2] > uk[c]) || (uk[c2] == uk[c] && c2 < c);
-                    if (c < B && rank < b) mask |= 1ull << c;
-                }
-            } else if (kp > 0) {
-                for (int c = 0; c < kp; ++c) keys[c] = c < B ? rank_key(u[c]) : 0u;
-                for (int c = 0; c < B; ++c)
-                    if (rank_in_row(keys, B, c) < b) mask |= 1ull << c;
-            } else {
-                for (int c = 0; c < B; ++c)
-                    if (rank_in_values(u, B, c) < b) mask |= 1ull << c;
-            }
-        } else {
-            mask = (b >= 64) ? ~0ull : ((1ull << b) - 1ull);
+    for (int o = L / 2; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    const float e = j < K ? expf(__fsub_rn(l, m)) : 0.f;
+    float S = 0.f;
+#pragma unroll 16
+    for (int c = 0; c < L; ++c) {
+        const float o = __shfl(e, gbase + c);
+        if (c < K) S = __fadd_rn(S, o);
+    }
+    const float s = __fdiv_rn(e, S);
+    // Eq. sorted-affinity: ranks by decreasing affinity, ties to the lower
+    // index; padding lanes (j >= K) rank after every expert, so the ranks of
+    // the group are a permutation of 0..L-1.
+    const uint32_t sk = j < K ? rank_key(s) : 0u;
+    int rs = 0;
+#pragma unroll 16
+    for (int c = 0; c < L; ++c) {
+        const uint32_t o = (uint32_t)__shfl((int)sk, gbase + c);
+        rs += (o > sk) || (o == sk && c < j);
+    }
+    const int dst = (gbase + rs) << 2;
+    const float ps = __int_as_float(__builtin_amdgcn_ds_permute(dst, __float_as_int(s)));
+    const int qs = __builtin_amdgcn_ds_permute(dst, j + 1);
+    // Eq. beta / expert-count: the smallest prefix reaching the target.
+    int k;
+    if (p.mass_mode == 2) {
+        k = p.fixed_k;
+    } else {
+        const float beta = __fsub_rn(1.0f, alpha);
+        const float target = (p.mass_mode == 0) ? fminf(beta, p.t_mass) : p.t_mass;
+        float P = 0.f;
+#pragma unroll 16
+        for (int c = 0; c < L; ++c) {
+            const float o = __shfl(ps, gbase + c);
+            if (c <= j && c < K) P = __fadd_rn(P, o);
         }
-        // Eq. residual-router-score: max-subtracted softmax, index-order sum.
-        float* l = row + 1;
-        if (K <= kSmallRank) {
-            // The same steps on registers: softmax, ranks, then the sorted
-            // weights back from LDS for the prefix of Eq. expert-count.
-            float lv[kSmallRank];
-#pragma unroll
-            for (int j = 0; j < kSmallRank; ++j) lv[j] = j < K ? l[j] : 0.f;
-            float m = lv[0];
-#pragma unroll
-            for (int j = 1; j < kSmallRank; ++j) m = j < K ? fmaxf(m, lv[j]) : m;
-            float S = 0.f;
-#pragma unroll
-            for (int j = 0; j < kSmallRank; ++j) {
-                lv[j] = j < K ? expf(__fsub_rn(lv[j], m)) : 0.f;
-                S = j < K ? __fadd_rn(S, lv[j]) : S;
-            }
-            uint32_t ek[kSmallRank];
-#pragma unroll
-            for (int j = 0; j < kSmallRank; ++j) {
-                lv[j] = __fdiv_rn(lv[j], S);
-                ek[j] = j < K ? rank_key(lv[j]) : 0u;
-            }
-            int rk[kSmallRank];
-#pragma unroll
-            for (int j = 0; j < kSmallRank; ++j) {
-                int rank = 0;
-#pragma unroll
-                for (int j2 = 0; j2 < kSmallRank; ++j2) rank += (ek[j2] > ek[j]) || (ek[j2] == ek[j] && j2 < j);
-                rk[j] = rank;
-                if (j < K) {
-                    ps[rank] = lv[j];
-                    qs[rank] = j + 1;
-                }
-            }
-            if (p.mass_mode == 2) {
-                k = p.fixed_k;
-            } else {
-                const float beta = __fsub_rn(1.0f, alpha);
-                const float target = (p.mass_mode == 0) ? fminf(beta, p.t_mass) : p.t_mass;
-                float sv[kSmallRank];
-#pragma unroll
-                for (int n = 0; n < kSmallRank; ++n) sv[n] = n < K ? ps[n] : 0.f;
-                float P = 0.f;
-                k = K;
-                bool found = false;
-#pragma unroll
-                for (int n = 0; n < kSmallRank; ++n) {
-                    if (n < K && !found) {
-                        P = __fadd_rn(P, sv[n]);
-                        if (P >= target) {
-                            k = n + 1;
-                            found = true;
-                        }
-                    }
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < kSmallRank; ++j)
-                if (j < K && rk[j] < k) sel |= 1ull << j;
-        } else {
-        float m = l[0];
-        for (int j = 1; j < K; ++j) m = fmaxf(m, l[j]);
-        float S = 0.f;
-        for (int j = 0; j < K; ++j) {
-            const float e = expf(__fsub_rn(l[j], m));
-            l[j] = e;
-            S = __fadd_rn(S, e);
+        const uint64_t reached = group_bits(j < K && P >= target);
+        k = reached ? __builtin_ctzll(reached) + 1 : K;
+    }
+
+    if (in_range) {
+        if (j == 0) {
+            p.alpha[tok] = v ? alpha : 0.f;
+            p.nsh[tok] = v ? b : 0;
+            p.mask[tok] = v ? mask : 0ull;
+            p.nres[tok] = v ? k : 0;
         }
-        for (int j = 0; j < K; ++j) l[j] = __fdiv_rn(l[j], S);
-        // Eq. sorted-affinity: rank by decreasing affinity, ties to lower index.
-        for (int j = 0; j < kp; ++j) keys[j] = j < K ? rank_key(l[j]) : 0u;
-        for (int j = 0; j < K; ++j) {
-            const int rank = kp > 0 ? rank_in_row(keys, K, j) : rank_in_values(l, K, j);
-            ps[rank] = l[j];
-            qs[rank] = j + 1;
-        }
-        // Eq. beta / expert-count: smallest prefix reaching the target.
-        if (p.mass_mode == 2) {
-            k = p.fixed_k;
-        } else {
-            const float beta = __fsub_rn(1.0f, alpha);
-            const float target = (p.mass_mode == 0) ? fminf(beta, p.t_mass) : p.t_mass;
-            float P = 0.f;
-            k = K;
-            for (int n = 0; n < K; ++n) {
-                P = __fadd_rn(P, ps[n]);
-                if (P >= target) {
-                    k = n + 1;
-                    break;
-                }
-            }
-        }
-        for (int i = 0; i < k; ++i) sel |= 1ull << (qs[i] - 1);
-        }
-        p.alpha[tok] = alpha;
-        p.nsh[tok] = b;
-        p.mask[tok] = mask;
-        p.nres[tok] = k;
-    } else if (in_range) {
-        p.alpha[tok] = 0.f;
-        p.nsh[tok] = 0;
-        p.mask[tok] = 0;
-        p.nres[tok] = 0;
-        for (int j = 0; j < K; ++j) {
-            ps[j] = 0.f;
-            qs[j] = -1;
+        if (j < K) {
+            p.eids[(size_t)tok * K + j] = v ? qs : -1;
+            p.wts[(size_t)tok * K + j] = v ? ps : 0.f;
         }
     }
     if (p.bin_count == nullptr) return;
 
     // Pairs per (expert, key of the pair's block mask): one shared pair and
-    // k residual pairs per valid token.
+    // k residual pairs per valid token. The count a bin copy had before a
+    // pair adds itself is the pair's slot within that copy (pair_rank), so
+    // the scatter needs no atomics; slots inside a bin follow the order the
+    // atomics land in, and no result depends on it (every GEMM row is
+    // computed from its own pair).
     const uint64_t full = (B == 64) ? ~0ull : ((1ull << B) - 1ull);
     const int kb = p.key_bits;
-    const int lane = lane_id();
-    const uint64_t rmask = ~mask & full;
-    const int ks = mask_key(mask, B, kb);
-    const int kr = mask_key(rmask, B, kb);
-    // The count of a bin taken before a pair adds itself is the pair's slot
-    // within the bin (pair_rank), so the scatter needs no atomics. The order
-    // of the slots inside a bin is whatever order the atomics land in; no
-    // result depends on it (every GEMM row is computed from its own pair).
-    // The shared pair's atomic and those of the first kRankBatch residual
-    // pairs are issued before any result is used, so their latencies overlap.
+    const int ks = mask_key(mask, B, kb), kr = mask_key(~mask & full, B, kb);
+    const int bc = (tok / kTileTok) % kBinCopies;
     int* rank = p.pair_rank + (size_t)(v ? tok : 0) * (K + 1);
-    const int r0 = v ? atomicAdd(&p.bin_count[ks], 1) : 0;
-    for (int i0 = 0; i0 < K; i0 += kRankBatch) {
-        if (!ballot(v && i0 < k)) break;
-        int r[kRankBatch];
+    if (v && j == 0) rank[0] = atomicAdd(&p.bin_count[ks * kBinCopies + bc], 1);
+    if (v && j < k) rank[1 + j] = atomicAdd(&p.bin_count[((qs << kb) + kr) * kBinCopies + bc], 1);
+    if (cnt == nullptr) return;
+    // The tile's counts: pairs per expert, and rows per slab (the shared
+    // expert on I_shr, each selected residual expert on I_res). Lane c adds
+    // block c's rows.
+    int* ecnt = cnt + (K + 1) * B;
+    if (v && j == 0) atomicAdd(&ecnt[0], 1);
+    if (v && j < k) atomicAdd(&ecnt[qs], 1);
+    if (v && j < B && shared) atomicAdd(&cnt[j], 1);
+    int kmax = v ? k : 0;
 #pragma unroll
-        for (int u = 0; u < kRankBatch; ++u)
-            r[u] = (v && i0 + u < k) ? atomicAdd(&p.bin_count[(qs[i0 + u] << kb) + kr], 1) : 0;
-#pragma unroll
-        for (int u = 0; u < kRankBatch; ++u)
-            if (v && i0 + u < k) rank[1 + i0 + u] = r[u];
+    for (int o = 32; o > 0; o >>= 1) kmax = max(kmax, __shfl_xor(kmax, o));
+    for (int i = 0; i < kmax; ++i) {
+        const int ei = __shfl(qs, gbase + i);
+        if (v && i < k && j < B && !shared) atomicAdd(&cnt[ei * B + j], 1);
     }
-    if (v) rank[0] = r0;
-    // Pairs per expert and rows per (expert, block), after the row counts in
-    // slab_lds: lane c (< B) holds the ballot of the tokens whose shared
-    // blocks include c, so expert e's rows on block c (the shared expert on
-    // I_shr, a residual expert on I_res) are one popcount, and each expert
-    // needs one LDS add per block lane.
-    int* ecnt = slab_lds + (K + 1) * B;
-    uint64_t mb = 0;
-    for (int c = 0; c < B; ++c) {
-        const uint64_t bits = ballot(v && ((mask >> c) & 1ull));
-        if (lane == c) mb = bits;
+}
+
+// Every token of a tile of kTileTok tokens whose logit rows are at `rows`
+// (stride lstride): the waves [w0, w0 + nw) of the workgroup share the
+// tile's tokens, 64 / L per pass.
+template <int L>
+__device__ __forceinline__ void decide_tile(const RouteParams& p, const float* rows, int tok0, int ntok, int wave,
+                                            int w0, int nw, int* cnt) {
+    constexpr int TPP = 64 / L;   // tokens per wave pass
+    const int g = lane_id() / L;
+    for (int t0 = (wave - w0) * TPP; t0 < kTileTok; t0 += nw * TPP) {
+        const int t = t0 + g;
+        decide_group<L>(p, rows + (size_t)(t < ntok ? t : 0) * p.lstride, tok0, t, ntok, cnt);
     }
-    const uint64_t vb = ballot(v);
-    if (!vb) return;
-    if (lane == 0) atomicAdd(&ecnt[0], __popcll(vb));
-    if (lane < B) {
-        const int n = __popcll(mb);
-        if (n) atomicAdd(&slab_lds[lane], n);
-    }
-    for (int e = 1; e <= K; ++e) {
-        const uint64_t hb = ballot(v && ((sel >> (e - 1)) & 1ull));
-        if (!hb) continue;
-        if (lane == 0) atomicAdd(&ecnt[e], __popcll(hb));
-        if (lane < B) {
-            const int n = __popcll(hb & ~mb);
-            if (n) atomicAdd(&slab_lds[e * B + lane], n);
+}
+
+// The workgroup's tile counters (ncnt words per tile, in LDS) out to memory
+// once its tiles are decided: tile i of the workgroup is layer tile
+// tile0 + i * stride. Called by every thread after a barrier.
+__device__ __forceinline__ void flush_counts(const RouteParams& p, const int* cnt, int ntiles, int ncnt, int tile0,
+                                             int stride) {
+    const int nslab = (p.K + 1) * p.B;
+    for (int x = threadIdx.x; x < ncnt; x += blockDim.x)
+        for (int i = 0; i < ntiles; ++i) {
+            const int tile = tile0 + i * stride, c = cnt[i * ncnt + x];
+            p.tile_cnt[(size_t)tile * ncnt + x] = c;
+            // Pairs per expert also into the totals (few atomics, spread).
+            if (x >= nslab && c) atomicAdd(&p.exp_total[(tile % kExpCopies) * (p.K + 1) + x - nslab], c);
         }
+}
+
+// The decisions of one tile with the lane count of the layer (see
+// decide_lanes).
+__device__ __forceinline__ void decide_tile_any(const RouteParams& p, const float* rows, int tok0, int ntok,
+                                                int wave, int w0, int nw, int* cnt) {
+    switch (decide_lanes(p.K, p.B)) {
+        case 16: decide_tile<16>(p, rows, tok0, ntok, wave, w0, nw, cnt); break;
+        case 32: decide_tile<32>(p, rows, tok0, ntok, wave, w0, nw, cnt); break;
+        default: decide_tile<64>(p, rows, tok0, ntok, wave, w0, nw, cnt); break;
     }
 }
 
 // NCT: 16-column logit tiles of the bf16 path (1 + K + B <= 16 NCT); 0 for
-// fp32 tokens.
+// fp32 tokens. One workgroup of 4 waves per kRouteTok tokens (two tiles):
+// the logits of all of them, then the two tiles' decisions, all 4 waves on
+// each tile.
 template <int NCT>
 __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteParams p) {
+    constexpr int NT = kRouteTok / kTileTok;
     extern __shared__ float lds_route[];
     float* L = lds_route;
-    float* PS = L + kRouteTok * p.lstride;
-    int* QS = reinterpret_cast<int*>(PS + kRouteTok * (p.K + 1));
-    uint32_t* KEYS = reinterpret_cast<uint32_t*>(QS + kRouteTok * (p.K + 1));   // 16-byte aligned
-    int* slab_lds = reinterpret_cast<int*>(KEYS + kRouteTok * p.key_stride);
+    int* cnt = reinterpret_cast<int*>(L + kRouteTok * p.lstride);   // [NT][ncnt]
     const int tok0 = blockIdx.x * kRouteTok;
-    const int nslab = (p.K + 1) * p.B;
-    // slab_lds: rows per slab, then pairs per expert.
-    const int ncnt = nslab + p.K + 1;
-    if (p.slab_count)
-        for (int i = threadIdx.x; i < ncnt; i += blockDim.x) slab_lds[i] = 0;
+    const int ncnt = (p.K + 1) * p.B + p.K + 1;
+    const bool counting = p.tile_cnt != nullptr;
+    if (counting)
+        for (int i = threadIdx.x; i < NT * ncnt; i += blockDim.x) cnt[i] = 0;
     if constexpr (NCT > 0) route_logits_bf16<NCT>(p, L, tok0);
     else route_logits_f32(p, L, tok0);
     __syncthreads();
-    if (threadIdx.x < kRouteTok) route_decide(p, L, PS, QS, KEYS, slab_lds, tok0, threadIdx.x);
-    __syncthreads();
-    // Sorted expert ids and weights of the workgroup's tokens: one contiguous
-    // range of each output, written from LDS with consecutive addresses.
-    {
-        const int K = p.K, ntok = min(kRouteTok, p.N - tok0);
-        const size_t base = (size_t)tok0 * K;
-        for (int i = threadIdx.x; i < ntok * K; i += blockDim.x) {
-            const int t = i / K, r = i - t * K;
-            p.eids[base + i] = QS[t * (K + 1) + r];
-            p.wts[base + i] = PS[t * (K + 1) + r];
-        }
+    const int wave = threadIdx.x >> 6;
+    int nt = 0;
+    for (int h = 0; h < NT; ++h) {
+        const int t0 = tok0 + h * kTileTok;
+        if (t0 >= p.N) break;
+        decide_tile_any(p, L + (size_t)h * kTileTok * p.lstride, t0, min(kTileTok, p.N - t0), wave, 0,
+                        kRouteThreads / 64, counting ? cnt + h * ncnt : nullptr);
+        ++nt;
     }
-    // Workgroup totals go to one of kSlabCopies copies of the counts, which
-    // spreads the same-address atomics; the permutation sums the copies.
-    if (p.slab_count) {
-        int* dst = p.slab_count + (size_t)(blockIdx.x % kSlabCopies) * ncnt;
-        for (int i = threadIdx.x; i < ncnt; i += blockDim.x)
-            if (slab_lds[i]) atomicAdd(&dst[i], slab_lds[i]);
+    if (counting) {
+        __syncthreads();
+        flush_counts(p, cnt, nt, ncnt, tok0 / kTileTok, 1);
     }
 }
 
-// Persistent routing for bf16 tokens when the router fits in registers
-// (1 + K + B <= 32 columns, d <= 768, K, B <= 16). One workgroup of 8 waves
-// takes the 64-token tiles blockIdx.x, blockIdx.x + gridDim.x, ... (at most
-// kRpMaxTiles). Wave w owns k steps [w nks / 8, (w + 1) nks / 8) of the
-// logits and keeps the router's three bf16 parts and W_shr for them in
-// registers for all its tiles, so only token rows stream from memory; each
-// tile's partial logits go to LDS and are summed over the 8 k slices in a
-// fixed order. Then wave i takes the decisions of tile i (one token per lane),
-// the tiles' decisions running side by side.
-constexpr int kRpTok = 64;
+// Logits of bf16 tokens when the router fits in registers (1 + K + B <= 32
+// columns, d <= 768), persistent: one workgroup of 8 waves takes the 64-token
+// tiles blockIdx.x, blockIdx.x + gridDim.x, ... Wave w owns k steps
+// [w nks / 8, (w + 1) nks / 8) and keeps the router's three bf16 parts and
+// W_shr for them in registers for all its tiles, so only token rows stream
+// from memory (the next tile's rows load while this tile's partial logits
+// are reduced); the 8 partial sets are summed in a fixed order and each
+// token's 1 + 16 NCT logits written to logits[N][1 + 16 NCT]. The decisions
+// run in route_decide_kernel.
+constexpr int kRpTok = kTileTok;
 constexpr int kRpWaves = 8;
 constexpr int kRpThreads = kRpWaves * 64;
-constexpr int kRpMaxTiles = 4;
 
 template <int NCT, int KPW>
-__global__ __launch_bounds__(kRpThreads) void route_persist_kernel(RouteParams p) {
+__global__ __launch_bounds__(kRpThreads) void route_logits_kernel(RouteParams p, float* __restrict__ logits) {
     constexpr int RT = kRpTok / 16;          // 16-row fragments per tile
+    constexpr int ncols = 1 + 16 * NCT;
     extern __shared__ float lds_route[];
-    const int K = p.K, ls = p.lstride;
-    const int ncols = 1 + 16 * NCT;
-    float* Lb = lds_route;                                       // [kRpMaxTiles][64][ls]
-    float* U = Lb + kRpMaxTiles * kRpTok * ls;                   // union: partials, then PS/QS
-    float* Pbuf = U;                                             // [8][64][ls]
-    float* PS = U;                                               // [kRpMaxTiles][64][K+1]
-    int* QS = reinterpret_cast<int*>(PS + kRpMaxTiles * kRpTok * (K + 1));
-    const int ufloats = max(kRpWaves * kRpTok * ls, 2 * kRpMaxTiles * kRpTok * (K + 1));
-    int* slab_lds = reinterpret_cast<int*>(U + ufloats);
-    const int nslab = (K + 1) * p.B, ncnt = nslab + K + 1;
+    const int ls = p.lstride;
+    float* Pbuf = lds_route;                                     // [8][64][ls] partial logits
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int ntile_all = (p.N + kRpTok - 1) / kRpTok;
-    const int nt = min(kRpMaxTiles, (ntile_all - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x);
-    if (p.slab_count)
-        for (int i = tid; i < ncnt; i += blockDim.x) slab_lds[i] = 0;
+    const int nt = (ntile_all - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;
 
     // This wave's k steps (32 deep) and the router parts for them.
     const int nks = p.d / 32;
@@ -570,7 +497,7 @@ __global__ __launch_bounds__(kRpThreads) void route_persist_kernel(RouteParams p
         const int tok0 = ((int)blockIdx.x + i * (int)gridDim.x) * kRpTok;
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
-            // Rows past N read row N - 1; their logits are never used.
+            // Rows past N read row N - 1; their logits are never written.
             const u16* xr = X + (size_t)min(tok0 + r * 16 + (lane & 15), p.N - 1) * p.d + kof;
 #pragma unroll
             for (int j = 0; j < KPW; ++j) xa[j][r] = ld16(xr + (kb + (j < kn ? j : 0)) * 32);
@@ -578,6 +505,7 @@ __global__ __launch_bounds__(kRpThreads) void route_persist_kernel(RouteParams p
     };
     if (nt > 0) load_x(0);
     for (int i = 0; i < nt; ++i) {
+        const int tok0 = ((int)blockIdx.x + i * (int)gridDim.x) * kRpTok;
         f32x4 acc[RT][NCT];
         float sh[RT];
 #pragma unroll
@@ -610,7 +538,8 @@ __global__ __launch_bounds__(kRpThreads) void route_persist_kernel(RouteParams p
         // The next tile's rows are in flight during the reduction.
         if (i + 1 < nt) load_x(i + 1);
         // This wave's partial logits: column 0 the shared demand, columns
-        // 1.. the MFMA tiles.
+        // 1.. the MFMA tiles. (The barrier after the previous tile's sum
+        // orders its reads of Pbuf before these writes.)
         float* P = Pbuf + wave * kRpTok * ls;
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
@@ -625,40 +554,46 @@ __global__ __launch_bounds__(kRpThreads) void route_persist_kernel(RouteParams p
                     P[(r * 16 + (lane >> 4) * 4 + e) * ls + 1 + ct * 16 + (lane & 15)] = acc[r][ct][e];
         }
         lds_barrier();
-        // Sum of the 8 k slices, in wave order.
-        float* L = Lb + i * kRpTok * ls;
-        for (int e = tid; e < kRpTok * ncols; e += blockDim.x) {
+        // Sum of the 8 k slices, in wave order, straight to memory.
+        const int ntok = min(kRpTok, p.N - tok0);
+        for (int e = tid; e < ntok * ncols; e += blockDim.x) {
             const int t = e / ncols, c = e - t * ncols;
             float v = 0.f;
 #pragma unroll
             for (int w = 0; w < kRpWaves; ++w) v += Pbuf[(w * kRpTok + t) * ls + c];
-            L[t * ls + c] = v;
+            logits[(size_t)tok0 * ncols + e] = v;
         }
         lds_barrier();
     }
-    // Decisions: wave i takes tile i (the partial buffer is reused as PS/QS).
-    if (wave < nt) {
-        const int tok0 = ((int)blockIdx.x + wave * (int)gridDim.x) * kRpTok;
-        route_decide(p, Lb + wave * kRpTok * ls, PS + wave * kRpTok * (K + 1), QS + wave * kRpTok * (K + 1),
-                     nullptr, slab_lds, tok0, lane);
-    }
+}
+
+// Decisions of one 64-token tile per workgroup of 4 waves (L lanes per
+// token, see decide_lanes), from the logits route_logits_kernel wrote (ncols
+// per token), staged in LDS rows; then the tile's counters out to memory.
+constexpr int kDecideThreads = 256;
+template <int L>
+__global__ __launch_bounds__(kDecideThreads) void route_decide_kernel(RouteParams p, const float* __restrict__ logits,
+                                                                      int ncols) {
+    extern __shared__ float lds_dec[];
+    const int ls = p.lstride;
+    float* rows = lds_dec;                                       // [64][ls]
+    int* cnt = reinterpret_cast<int*>(rows + kTileTok * ls);     // the tile's counters
+    const int ncnt = (p.K + 1) * p.B + p.K + 1;
+    const bool counting = p.tile_cnt != nullptr;
+    const int tile = blockIdx.x, tok0 = tile * kTileTok, ntok = min(kTileTok, p.N - tok0);
+    batched_copy(
+        ntok * ncols, [&](int e) { return logits[(size_t)tok0 * ncols + e]; },
+        [&](int e, float v) {
+            const int t = e / ncols;
+            rows[t * ls + e - t * ncols] = v;
+        });
+    if (counting)
+        for (int i = threadIdx.x; i < ncnt; i += blockDim.x) cnt[i] = 0;
     __syncthreads();
-    for (int i = 0; i < nt; ++i) {
-        const int tok0 = ((int)blockIdx.x + i * (int)gridDim.x) * kRpTok;
-        const int ntok = min(kRpTok, p.N - tok0);
-        const size_t base = (size_t)tok0 * K;
-        const float* ps = PS + i * kRpTok * (K + 1);
-        const int* qs = QS + i * kRpTok * (K + 1);
-        for (int e = tid; e < ntok * K; e += blockDim.x) {
-            const int t = e / K, r = e - t * K;
-            p.eids[base + e] = qs[t * (K + 1) + r];
-            p.wts[base + e] = ps[t * (K + 1) + r];
-        }
-    }
-    if (p.slab_count) {
-        int* dst = p.slab_count + (size_t)(blockIdx.x % kSlabCopies) * ncnt;
-        for (int i = tid; i < ncnt; i += blockDim.x)
-            if (slab_lds[i]) atomicAdd(&dst[i], slab_lds[i]);
+    decide_tile<L>(p, rows, tok0, ntok, (int)threadIdx.x >> 6, 0, kDecideThreads / 64, counting ? cnt : nullptr);
+    if (counting) {
+        __syncthreads();
+        flush_counts(p, cnt, 1, ncnt, tile, 1);
     }
 }
 

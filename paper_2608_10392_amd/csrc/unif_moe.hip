@@ -7,11 +7,12 @@
 //   bf16_to_f16      W_down -> fp16 copy for the down-projection (bf16 only)
 //   fill_zero        pair / slab counters
 //   split_router     fp32 router + prototypes -> 3 bf16 parts (bf16 only)
-//   route            routing record + pair and slab counts
-//   scan             LDS prefix sums -> offsets and tile tables
-//   scatter          pair slots (expert segments sorted by block-mask key)
-//   tables, chunk_scan, slabfill
-//                    tile tables, per-(expert, block) pair lists  (bf16)
+//   route            routing record, pair slots in their bins, per-tile
+//                    slab and expert counts
+//   scan             prefix sums -> segment, bin, slab and tile offsets
+//   scatter          pairs (expert segments sorted by block-mask key), the
+//                    per-(expert, block) row lists in token order and the
+//                    up tile table                               (bf16)
 //   up, down         block-sparse MFMA grouped GEMMs              (bf16)
 //   pair_ffn_f32     per-pair fp32 FFN                            (fp32)
 //   combine          weighted merge in fixed order
@@ -106,16 +107,33 @@ Dims dims_of(const unif_moe_config* c) {
     return m;
 }
 
-// Routing LDS: logits, sorted weights and ids, ranking keys (16-byte
-// aligned; left out when they would not fit), row counts.
-size_t route_lds_bytes_with(const Dims& m, int key_stride) {
-    const size_t head = (size_t)kRouteTok * m.lstride + (size_t)kRouteTok * (m.K + 1) * 2;
-    return sizeof(float) * (((head + 3) & ~(size_t)3) + (size_t)kRouteTok * key_stride + (size_t)m.K1 * m.B + m.K1);
+// Counters per tile of the permutation: rows per slab, then pairs per expert.
+size_t tile_counters(const Dims& m) { return (size_t)m.nslab + m.K1; }
+// Routing LDS (route_kernel): the logit rows of its tokens, then its two
+// tiles' counters.
+size_t route_lds_bytes(const Dims& m) {
+    return sizeof(float) * ((size_t)kRouteTok * m.lstride + (kRouteTok / kTileTok) * tile_counters(m));
 }
-int route_key_stride(const Dims& m) {
-    return route_lds_bytes_with(m, key_row(m.K, m.B)) <= kLdsLimit ? key_row(m.K, m.B) : 0;
+// The persistent logits kernel: 8 partial logit sets of a tile. The
+// decisions kernel: a tile's logit rows and counters.
+size_t route_logits_lds_bytes(const Dims& m) { return sizeof(float) * (size_t)kRpWaves * kRpTok * m.lstride; }
+size_t route_decide_lds_bytes(const Dims& m) {
+    return sizeof(float) * ((size_t)kTileTok * m.lstride + tile_counters(m));
 }
-size_t route_lds_bytes(const Dims& m) { return route_lds_bytes_with(m, route_key_stride(m)); }
+// Logits of the split routing path (bf16 routers of <= 32 columns, d <= 768):
+// 1 + 16 NCT fp32 values per token, or 0 when the path does not apply.
+int split_route_cols(const Dims& m) {
+    const int nct = m.NLP / 16, kpw = ceil_div(m.d / 32, kRpWaves);
+    return (m.bf16 && nct <= 2 && kpw <= 3) ? 1 + 16 * nct : 0;
+}
+// The scatter kernel: the tile's tokens' pairs per expert and its first row
+// in every slab, or the up tile table's inputs.
+size_t scatter_lds_bytes(const Dims& m) {
+    const size_t offsets = 2 * ((size_t)m.nslab + 1);
+    const size_t token_role = 64 * (size_t)m.K1 + (size_t)m.nslab;
+    const size_t table_role = (size_t)kUpTableWords + kScatterWaves * 64;
+    return sizeof(int) * (offsets + std::max(token_role, table_role));
+}
 
 // Checks shared by every entry point (host only, no HIP call).
 int32_t check_config(const unif_moe_config* c) {
@@ -147,8 +165,8 @@ int32_t check_forward_shape(const unif_moe_config* c) {
     const Dims m = dims_of(c);
     if (m.bf16) {
         if (m.d % 128 != 0 || m.M % 64 != 0 || m.M > 256) return UNIF_EUNSUPPORTED;
-        // Down tiles are encoded as row tile << 8 | column tile.
-        if (m.d / kDownBNNarrow > 255 || (int64_t)m.N * m.K1 / kDownTMMin + m.K1 >= ((int64_t)1 << 23))
+        // Down tile indices (row tiles x column tiles) fit an int.
+        if (((int64_t)m.N * m.K1 / kDownTMMin + m.K1) * (m.d / kDownBNNarrow) >= ((int64_t)1 << 31))
             return UNIF_EUNSUPPORTED;
         if ((int64_t)m.H * m.d * 2 > ((int64_t)1 << 40)) return UNIF_EUNSUPPORTED;
     } else {
@@ -195,25 +213,25 @@ struct Carver {
 };
 
 struct RoutePlan {
-    size_t wsplit, total;
+    size_t wsplit, logits, total;
 };
 
 RoutePlan plan_route(const Dims& m) {
     Carver cv;
     RoutePlan p;
     p.wsplit = cv.take(m.bf16 ? (size_t)3 * m.NLP * m.d * sizeof(u16) : 0);
+    p.logits = cv.take((size_t)m.N * split_route_cols(m) * sizeof(float));
     p.total = cv.cur;
     return p;
 }
 
 struct FwdPlan {
     size_t alpha, nsh, mask, nres, eids, wts;
-    size_t wsplit;
+    size_t wsplit, logits;
     size_t zero_begin, zero_end;  // bin_count, slab_count, totals, zero page
-    size_t bin_count, slab_count, totals, queues, zero_page;
-    size_t bin_cursor, slab_off, seg_off, up_tile_off, down_tile_off, chunk_off, chunk_cnt;
-    size_t pair_token, pair_mask, pair_expert, pair_of, slab_rows, slab_tok, up_tile_info, up_tile_rows, hbuf, part;
-    size_t max_chunks, max_row_tiles, rt_info, rt_masks, down_tiles, down_slices;
+    size_t bin_count, slab_count, exp_total, totals, queues, zero_page;
+    size_t bin_cursor, seg_off, down_tile_off, tile_cnt, max_row_tiles, rt_info, rt_masks;
+    size_t pair_token, pair_mask, pair_expert, pair_of, pair_rank, slab_rows, slab_tok, up_tile_info, up_tile_rows, hbuf, part;
     size_t xn;      // LN(X), the FFN input of a pre-LN block
     size_t wdown16; // fp16 copy of W_down (bf16 layers)
     size_t total;
@@ -233,22 +251,27 @@ FwdPlan plan_forward(const Dims& m, bool own_record, size_t xn_bytes = 0) {
     p.eids = cv.take(own_record ? 4 * N * K : 0);
     p.wts = cv.take(own_record ? 4 * N * K : 0);
     p.wsplit = cv.take(m.bf16 ? (size_t)3 * m.NLP * m.d * sizeof(u16) : 0);
-    p.bin_count = cv.take(4 * (size_t)m.nbin);
+    p.logits = cv.take((size_t)N * split_route_cols(m) * sizeof(float));
+    p.bin_count = cv.take(4 * (size_t)m.nbin * kBinCopies);
     p.zero_begin = p.bin_count;
-    p.slab_count = cv.take(4 * ((size_t)m.nslab + K1) * kSlabCopies);
+    p.slab_count = cv.take(4 * (size_t)m.nslab);
+    p.exp_total = cv.take(4 * (size_t)kExpCopies * K1);
     p.totals = cv.take(4 * 8);
     p.queues = cv.take(4 * 16);   // per-XCD tile counters: up, then down
     p.zero_page = cv.take(256);
     p.zero_end = cv.cur;
-    p.bin_cursor = cv.take(4 * (size_t)m.nbin);
-    p.slab_off = cv.take(4 * ((size_t)m.nslab + 1));
+    p.bin_cursor = cv.take(4 * (size_t)m.nbin * kBinCopies);
     p.seg_off = cv.take(4 * (K1 + 1));
-    p.up_tile_off = cv.take(4 * ((size_t)m.nslab + 1));
     p.down_tile_off = cv.take(4 * (K1 + 1));
+    p.tile_cnt = cv.take(4 * ceil_div_sz(N, kTileTok) * tile_counters(m));
+    p.max_row_tiles = ceil_div_sz(pmax, kDownTMMin) + K1;
+    p.rt_info = cv.take(m.bf16 ? 16 * p.max_row_tiles : 0);
+    p.rt_masks = cv.take(m.bf16 ? 8 * (kDownTMMax / 32 + 1) * p.max_row_tiles : 0);
     p.pair_token = cv.take(4 * pmax);
     p.pair_mask = cv.take(8 * (pmax + kDownTMMax));   // a whole down tile is readable past the last pair
     p.pair_expert = cv.take(4 * pmax);
     p.pair_of = cv.take(4 * N * K1);
+    p.pair_rank = cv.take(4 * N * K1);
     // Slab row lists: at most K B rows per token (b + k (B - b) <= K B), each
     // slab padded to whole up tiles.
     const size_t tm = (size_t)up_tm(m.M, m.d);
@@ -257,17 +280,8 @@ FwdPlan plan_forward(const Dims& m, bool own_record, size_t xn_bytes = 0) {
     p.slab_tok = cv.take(m.bf16 ? 4 * up_tiles * tm : 0);
     p.up_tile_info = cv.take(m.bf16 ? 4 * up_tiles : 0);
     p.up_tile_rows = cv.take(m.bf16 ? 4 * up_tiles : 0);
-    // Ordered slab fill: chunks of kChunk pairs inside each expert segment.
-    p.max_chunks = ceil_div_sz(pmax, kChunk) + K1;
-    p.chunk_off = cv.take(m.bf16 ? 4 * (K1 + 1) : 0);
-    p.chunk_cnt = cv.take(m.bf16 ? 4 * p.max_chunks * (size_t)m.B : 0);
     p.hbuf = cv.take(m.bf16 ? (pmax + 1) * (size_t)m.H * 2 : 0);  // fp16, + the sink row
     p.part = cv.take((pmax + 1) * (size_t)m.d * sizeof(float));   // fp32, + the sink row
-    p.max_row_tiles = ceil_div_sz(pmax, kDownTMMin) + K1;
-    p.rt_info = cv.take(m.bf16 ? 16 * p.max_row_tiles : 0);
-    p.rt_masks = cv.take(m.bf16 ? 8 * (kDownTMMax / 16 + 1) * p.max_row_tiles : 0);
-    p.down_tiles = cv.take(m.bf16 ? 4 * p.max_row_tiles * (size_t)(m.d / kDownBNNarrow) : 0);
-    p.down_slices = cv.take(m.bf16 ? 4 * 16 : 0);
     p.xn = cv.take(xn_bytes);
     p.wdown16 = cv.take(m.bf16 ? K1 * (size_t)m.d * m.H * 2 : 0);
     p.total = cv.cur + 256;  // slack for aligning an unaligned base pointer
@@ -320,7 +334,6 @@ RouteParams route_params(const unif_moe_config* c, const Dims& m, const void* X,
     r.NL = m.NL;
     r.NLP = m.NLP;
     r.lstride = m.lstride;
-    r.key_stride = route_key_stride(m);
     r.key_bits = m.key_bits;
     r.tau = m.tau;
     r.one_minus_2tau = m.one_minus_2tau;
@@ -343,7 +356,8 @@ RouteParams route_params(const unif_moe_config* c, const Dims& m, const void* X,
     r.eids = eids;
     r.wts = wts;
     r.bin_count = nullptr;
-    r.slab_count = nullptr;
+    r.tile_cnt = nullptr;
+    r.exp_total = nullptr;
     r.pair_rank = nullptr;
     return r;
 }
@@ -352,7 +366,7 @@ RouteParams route_params(const unif_moe_config* c, const Dims& m, const void* X,
 // The forward's counters (zwords words at zero) are cleared in the launch
 // that splits the router weights.
 int32_t launch_route(const Dims& m, const RouteParams& rp, const float* Wr, const float* mu, u16* wsplit,
-                     hipStream_t st, uint32_t* zero = nullptr, size_t zwords = 0) {
+                     float* logits, hipStream_t st, uint32_t* zero = nullptr, size_t zwords = 0) {
     if (m.N == 0) return UNIF_OK;
     const int nsplit = m.bf16 ? ceil_div(m.NLP * m.d, 256) : 0;
     const int nzero = zwords ? (int)std::min<size_t>(ceil_div_sz(zwords, 256), 1024) : 0;
@@ -361,35 +375,34 @@ int32_t launch_route(const Dims& m, const RouteParams& rp, const float* Wr, cons
                                                            zwords);
         UNIF_LAUNCH_CHECK();
     }
-    // Persistent routing with the router in registers where it fits.
-    const int nct = m.NLP / 16, kpw = ceil_div(m.d / 32, kRpWaves);
-    if (m.bf16 && nct <= 2 && kpw <= 3 && m.K <= kSmallRank && m.B <= kSmallRank) {
-        const size_t ls = (size_t)m.lstride, K1 = (size_t)m.K1;
-        const size_t lds = sizeof(float) * (kRpMaxTiles * kRpTok * ls +
-                                            std::max(kRpWaves * kRpTok * ls, 2 * kRpMaxTiles * kRpTok * K1) +
-                                            (size_t)m.nslab + K1);
-        if (lds <= kLdsLimit) {
-            void (*pk)(RouteParams) = nullptr;
-            switch (nct * 4 + kpw) {
-                case 5: pk = route_persist_kernel<1, 1>; break;
-                case 6: pk = route_persist_kernel<1, 2>; break;
-                case 7: pk = route_persist_kernel<1, 3>; break;
-                case 9: pk = route_persist_kernel<2, 1>; break;
-                case 10: pk = route_persist_kernel<2, 2>; break;
-                case 11: pk = route_persist_kernel<2, 3>; break;
-                default: break;
-            }
-            if (pk != nullptr) {
-                RouteParams rq = rp;
-                rq.key_stride = 0;   // rankings of <= 16 entries run on registers
-                const int ntiles = ceil_div(m.N, kRpTok);
-                const int grid = std::max(std::min(cu_count(), ntiles), ceil_div(ntiles, kRpMaxTiles));
-                if (allow_lds(pk, lds) != UNIF_OK) return UNIF_EDEVICE;
-                pk<<<grid, kRpThreads, lds, st>>>(rq);
-                UNIF_LAUNCH_CHECK();
-                return UNIF_OK;
-            }
+    // Small bf16 routers: logits (router in registers), then decisions.
+    const int ncols = split_route_cols(m);
+    if (ncols > 0 && logits != nullptr) {
+        void (*lk)(RouteParams, float*) = nullptr;
+        const int nct = m.NLP / 16, kpw = ceil_div(m.d / 32, kRpWaves);
+        switch (nct * 4 + kpw) {
+            case 5: lk = route_logits_kernel<1, 1>; break;
+            case 6: lk = route_logits_kernel<1, 2>; break;
+            case 7: lk = route_logits_kernel<1, 3>; break;
+            case 9: lk = route_logits_kernel<2, 1>; break;
+            case 10: lk = route_logits_kernel<2, 2>; break;
+            case 11: lk = route_logits_kernel<2, 3>; break;
+            default: return UNIF_EUNSUPPORTED;
         }
+        void (*dk)(RouteParams, const float*, int) = nullptr;
+        switch (decide_lanes(m.K, m.B)) {
+            case 16: dk = route_decide_kernel<16>; break;
+            case 32: dk = route_decide_kernel<32>; break;
+            default: dk = route_decide_kernel<64>; break;
+        }
+        const int ntiles = ceil_div(m.N, kRpTok);
+        const size_t l1 = route_logits_lds_bytes(m), l2 = route_decide_lds_bytes(m);
+        if (allow_lds(lk, l1) != UNIF_OK || allow_lds(dk, l2) != UNIF_OK) return UNIF_EDEVICE;
+        lk<<<std::min(cu_count(), ntiles), kRpThreads, l1, st>>>(rp, logits);
+        UNIF_LAUNCH_CHECK();
+        dk<<<ntiles, kDecideThreads, l2, st>>>(rp, logits, ncols);
+        UNIF_LAUNCH_CHECK();
+        return UNIF_OK;
     }
     const size_t lds = route_lds_bytes(m);
     const int grid = ceil_div(m.N, kRouteTok);
@@ -458,7 +471,8 @@ int32_t unif_moe_route(const unif_moe_config* cfg, const void* X, const uint8_t*
     const RouteParams rp = route_params(cfg, m, X, valid, W_router, prototypes, wsplit, out->alpha,
                                         out->n_shared, out->shared_mask, out->n_res, out->expert_ids,
                                         out->weights);
-    return launch_route(m, rp, W_router, prototypes, wsplit, static_cast<hipStream_t>(stream));
+    float* logits = need ? reinterpret_cast<float*>(ws + plan.logits) : nullptr;
+    return launch_route(m, rp, W_router, prototypes, wsplit, logits, static_cast<hipStream_t>(stream));
 }
 
 int32_t unif_moe_layer_forward_workspace_size(const unif_moe_config* cfg, size_t* bytes) {
@@ -585,10 +599,11 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     RouteParams rp = route_params(cfg, m, Xf, valid, W_router, prototypes, wsplit, alpha, nsh, mask, nres, eids,
                                   wts);
     rp.bin_count = bin_count;
-    rp.slab_count = slab_count;
-    rp.pair_rank = reinterpret_cast<int*>(ws + plan.pair_of);
-    s = launch_route(m, rp, W_router, prototypes, wsplit, st, reinterpret_cast<uint32_t*>(ws + plan.zero_begin),
-                     zwords);
+    rp.tile_cnt = reinterpret_cast<int*>(ws + plan.tile_cnt);
+    rp.exp_total = reinterpret_cast<int*>(ws + plan.exp_total);
+    rp.pair_rank = reinterpret_cast<int*>(ws + plan.pair_rank);
+    s = launch_route(m, rp, W_router, prototypes, wsplit, reinterpret_cast<float*>(ws + plan.logits), st,
+                     reinterpret_cast<uint32_t*>(ws + plan.zero_begin), zwords);
     if (s != UNIF_OK) return s;
     UNIF_MARK(2);
 
@@ -609,9 +624,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     pp.bin_count = bin_count;
     pp.bin_cursor = reinterpret_cast<int*>(ws + plan.bin_cursor);
     pp.slab_count = slab_count;
-    pp.slab_off = reinterpret_cast<int*>(ws + plan.slab_off);
     pp.seg_off = reinterpret_cast<int*>(ws + plan.seg_off);
-    pp.up_tile_off = reinterpret_cast<int*>(ws + plan.up_tile_off);
     pp.down_tile_off = reinterpret_cast<int*>(ws + plan.down_tile_off);
     pp.totals = totals;
     pp.pair_token = reinterpret_cast<int*>(ws + plan.pair_token);
@@ -622,31 +635,33 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     pp.slab_tok = m.bf16 ? reinterpret_cast<int*>(ws + plan.slab_tok) : nullptr;
     pp.up_tile_info = m.bf16 ? reinterpret_cast<int*>(ws + plan.up_tile_info) : nullptr;
     pp.up_tile_rows = m.bf16 ? reinterpret_cast<int*>(ws + plan.up_tile_rows) : nullptr;
-    pp.chunk_off = m.bf16 ? reinterpret_cast<int*>(ws + plan.chunk_off) : nullptr;
-    pp.chunk_cnt = m.bf16 ? reinterpret_cast<int*>(ws + plan.chunk_cnt) : nullptr;
+    pp.tile_cnt = reinterpret_cast<int*>(ws + plan.tile_cnt);
+    pp.exp_total = rp.exp_total;
     pp.rt_info = m.bf16 ? reinterpret_cast<int4*>(ws + plan.rt_info) : nullptr;
     pp.rt_masks = m.bf16 ? reinterpret_cast<uint64_t*>(ws + plan.rt_masks) : nullptr;
-    pp.down_tiles = m.bf16 ? reinterpret_cast<int*>(ws + plan.down_tiles) : nullptr;
-    pp.down_slices = m.bf16 ? reinterpret_cast<int*>(ws + plan.down_slices) : nullptr;
-    scan_kernel<<<m.K1 + 1, kScanThreads, 0, st>>>(pp);
+    pp.pair_rank = rp.pair_rank;
+    pp.ntile = ceil_div(m.N, kTileTok);
+    // Expert segments and bin cursors; per slab (bf16), its rows per token
+    // tile as first rows.
+    scan_kernel<<<(unsigned)(m.K1 + (m.bf16 ? m.nslab : 0)), kScanThreads, 0, st>>>(pp);
     UNIF_LAUNCH_CHECK();
-    scatter_kernel<<<ceil_div(m.N, 256), 256, 0, st>>>(pp);
-    UNIF_LAUNCH_CHECK();
+    // Pairs and slab rows; the up tile table (bf16).
+    const int up_groups = m.bf16 ? m.K1 * ceil_div(m.B, pp.up_group) : 0;
+    {
+        const size_t lds = scatter_lds_bytes(m);
+        if (allow_lds(scatter_kernel, lds) != UNIF_OK) return UNIF_EDEVICE;
+        scatter_kernel<<<(unsigned)(up_groups + pp.ntile), kScatterWaves * 64, lds, st>>>(
+            pp, up_groups);
+        UNIF_LAUNCH_CHECK();
+    }
 
     const int cus = cu_count();
     void* part = ws + plan.part;
     if (m.bf16) {
-        // The grid-stride loops below are sized for the worst case only up to
-        // a few workgroups per CU; the real counts are on the device.
-        const unsigned gs = (unsigned)(4 * cus);
-        const unsigned g1 = std::min((unsigned)ceil_div_sz(plan.max_row_tiles, 4), gs);
-        const unsigned g2 = std::min((unsigned)plan.max_chunks, gs);
-        tables_kernel<<<g1 + g2, 256, 0, st>>>(pp, (int)g1);
-        UNIF_LAUNCH_CHECK();
-        chunk_scan_kernel<<<m.nslab + 1, 256, 0, st>>>(pp);   // + the down slices
-        UNIF_LAUNCH_CHECK();
-        const int up_groups = m.K1 * ceil_div(m.B, pp.up_group);
-        slabfill_kernel<<<(unsigned)up_groups + std::min((unsigned)plan.max_chunks, gs), kChunk, 0, st>>>(pp, up_groups);
+        // Down row-tile descriptions (the grid-stride loop is sized for the
+        // worst case only up to a few workgroups per CU).
+        down_tables_kernel<<<(unsigned)std::min<size_t>(ceil_div_sz(plan.max_row_tiles, 4), (size_t)cus * 4), 256, 0,
+                             st>>>(pp);
         UNIF_LAUNCH_CHECK();
         UNIF_MARK(3);
         // 4. block-sparse expert GEMMs
@@ -684,9 +699,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         dn.part_sink = dn.part + (size_t)m.N * m.K1 * m.d;
         dn.rt_info = pp.rt_info;
         dn.rt_masks = pp.rt_masks;
-        dn.slices = pp.down_slices;
         dn.pair_mask = pp.pair_mask;
-        dn.tiles = pp.down_tiles;
         dn.totals = totals;
         dn.queue = reinterpret_cast<int*>(ws + plan.queues) + 8;
         if (dsh.bn == 384)
