@@ -2,39 +2,44 @@
 """Throughput of the forward pass of one UniF-MoE feed-forward layer on one
 MI355X (bf16 expert FFNs, fp32 router), on seeded synthetic tokens.
 
-Workload: the ViT-B/16-shaped layer - 256 images x 197 tokens = 50,432 tokens,
-d = 768, K = 16 residual experts plus the shared expert, all upcycled from a
-d_ff = 3072 GELU FFN and split into B = 16 blocks of M = 192 channels,
-cumulative-mass threshold 0.6.
+Headline workload: the ViT-B/16-shaped layer - 256 images x 197 tokens =
+50,432 tokens, d = 768, K = 16 residual experts plus the shared expert, all
+upcycled from a d_ff = 3072 GELU FFN and split into B = 16 blocks of M = 192
+channels, cumulative-mass threshold 0.6.
 
 One step = one unif_moe_layer_forward call (routing, permutation, the
 block-sparse expert GEMMs and the weighted merge) with inputs already
-resident in HBM. Prints one JSON line. Per-phase kernel durations come from
-HIP events recorded by the library itself on the launch stream during a
-second pass over the same number of steps (unif_moe_layer_forward_profiled).
+resident in HBM. `value` is valid tokens / wall-clock seconds over exactly
+`steps` synchronized steps; the median of per-step HIP events on the launch
+stream is reported beside it. Per-phase kernel durations come from HIP events
+the library records on the launch stream (unif_moe_layer_forward_profiled),
+medians over the steps. Prints one JSON line.
 
     python bench.py [--steps 20] [--warmup 3] [--workload vit_b16] [--no-cpu-baseline]
-                    [--no-paper-exact] [--no-block] [--no-backward]
+                    [--no-configs] [--no-paper-exact] [--no-block] [--no-backward]
 
-Unless --no-paper-exact, a second, shorter run repeats the workload with the
-cumulative target exactly Eq. beta (t = 1) and reports it under
-"paper_exact_t1" (whole-step time only). Unless --no-block, a third repeats
-it as the pre-LN transformer block around the layer (LayerNorm, FFN biases,
-residual add; unif_moe_block_forward) and reports it under "block_pre_ln".
-Unless --no-backward, the training step's backward pass (unif_moe_layer_backward,
-a first fp32 version on the vector units) is timed on the same workload and
-reported under "backward" against the fp32 vector peak.
+Also, unless switched off: "configs" - the other workloads (ViT-S/16, BERT-base
+with padding, the skewed 131k-token layer, the paper's DeiT-S and BERT-large
+operating points), each with tokens/s, phases, MFMA utilisation and roofline;
+"paper_exact_t1" - the headline tokens with the cumulative target exactly
+Eq. beta (t = 1); "block_pre_ln" - the DeiT-style pre-LN block around the
+layer; "backward" - the training step's backward pass; "cpu_baseline" - the
+CPU oracle timed on a sample of the headline workload, with the GPU output
+on the same sample checked against it ("parity_on_sample").
 """
 import argparse
 import json
 import os
+import subprocess
 import sys
+import threading
 import time
 
-PEAK_BF16_FLOPS = 2.5e15   # MI355X dense bf16 matrix-core peak
+PEAK_BF16_FLOPS = 2.5e15   # MI355X dense bf16/fp16 matrix-core peak
 PEAK_HBM_BYTES = 8.0e12    # MI355X HBM3E bandwidth
-PEAK_FP32_VECTOR = 157.3e12  # MI355X fp32 vector peak
 METRIC = "UniF-MoE layer fwd tokens/s (bf16); MFMA util of activated FLOPs vs peak"
+PHASES = ["wdown_f16", "routing", "permute", "up_gemm", "down_gemm", "combine"]
+OTHER_CONFIGS = ["vit_s16", "bert_base_padded", "zipf_stress", "paper_vision", "paper_language"]
 
 
 def parse():
@@ -44,12 +49,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="vit_b16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true", help="skip the other workloads")
     ap.add_argument("--no-paper-exact", action="store_true",
                     help="skip the second, shorter run at cumulative target t = 1")
-    ap.add_argument("--no-block", action="store_true",
-                    help="skip the pre-LN block run")
-    ap.add_argument("--no-backward", action="store_true",
-                    help="skip the backward-pass run")
+    ap.add_argument("--no-block", action="store_true", help="skip the pre-LN block run")
+    ap.add_argument("--no-backward", action="store_true", help="skip the backward-pass run")
     ap.add_argument("--cpu-sample", type=int, default=2048)
     ap.add_argument("--cpu-repeats", type=int, default=3)
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
@@ -61,16 +65,17 @@ def parse():
 def phase_bytes(cfg, st):
     """Algorithmic HBM bytes of the non-GEMM phases (minimum traffic of each
     step as defined, not counter readings)."""
-    N, d, K = cfg["n_tokens"], cfg["d_model"], cfg["n_experts"]
+    N, d, K, H = cfg["n_tokens"], cfg["d_model"], cfg["n_experts"], cfg["n_blocks"] * cfg["block_width"]
     nv, sum_k, sum_cb = st["n_valid"], st["mean_k"] * st["n_valid"], st["activated_blocks"]
     pairs = nv + sum_k
     es = 2 if cfg["dtype"] == "bf16" else 4
+    wdown = (K + 1) * d * H * (2 + 2) if cfg["dtype"] == "bf16" else 0   # read bf16, write fp16
     routing = N * d * es + N * (4 + 4 + 8 + 4 + 8 * K)             # read X, write the record
     permute = (N * (8 + 4) + sum_k * 4                               # read mask, k, q_1..q_k
                + pairs * (4 + 8 + 4 + 4)                             # pair token/mask/expert, pair_of
-               + pairs * (4 + 8) + sum_cb * 4)                       # slab lists: read pairs, write rows
+               + sum_cb * 8)                                         # slab lists: pair and token per row
     combine = pairs * d * 4 + pairs * 8 + N * 4 + N * d * es         # fp32 per-expert rows, weights, Y
-    return dict(routing=routing, permute=permute, combine=combine)
+    return dict(wdown_f16=wdown, routing=routing, permute=permute, combine=combine)
 
 
 COUNTERS_PROFILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
@@ -110,11 +115,118 @@ def committed_traffic(kernel):
         return None
 
 
-def cpu_baseline(g, n_sample, repeats):
-    """The CPU oracle timed on a seeded sample of the same workload."""
+def median(v):
+    v = sorted(v)
+    n = len(v)
+    return v[n // 2] if n % 2 else 0.5 * (v[n // 2 - 1] + v[n // 2])
+
+
+class ClockSampler:
+    """Shader clock samples (rocm-smi) taken while the GPU runs; best effort."""
+
+    def __init__(self):
+        self.samples = []
+        self._stop = threading.Event()
+        self._t = None
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                out = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True,
+                                     timeout=10).stdout
+                for card in json.loads(out).values():
+                    for key, v in card.items():
+                        if key.lower().startswith("sclk"):
+                            self.samples.append(int("".join(ch for ch in str(v) if ch.isdigit())))
+            except Exception:
+                return
+            self._stop.wait(0.5)
+
+    def start(self):
+        self._t = threading.Thread(target=self._run, daemon=True)
+        self._t.start()
+
+    def stop(self):
+        self._stop.set()
+        if self._t is not None:
+            self._t.join(timeout=15)
+        s = sorted(self.samples)
+        return {"samples": len(s), "max_mhz": s[-1] if s else None,
+                "median_mhz": s[len(s) // 2] if s else None,
+                "note": "rocm-smi samples every 0.5 s during the per-workload runs"}
+
+
+def measure(torch, _lib, dev, cfg, steps, warmup, stream):
+    """Wall-clock and event timing of `steps` forwards, then the same steps
+    through the profiled entry point (phase events)."""
+    for _ in range(warmup):
+        dev.forward(stream=stream)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a, b in ev:
+        a.record(stream)
+        dev.forward(stream=stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = [a.elapsed_time(b) for a, b in ev]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(_lib.N_PHASE_EVENTS)] for _ in range(steps)]
+    for evs in events:
+        for e in evs:
+            e.record(stream)          # creates the underlying HIP event
+    torch.cuda.synchronize()
+    for evs in events:
+        _lib.layer_forward_profiled(cfg, dev.X, dev.valid, dev.W_router, dev.prototypes, dev.W_up,
+                                    dev.W_down, dev.Y, dev.ws_forward, evs, routing=dev.routing,
+                                    stream=stream)
+    torch.cuda.synchronize()
+    phase_ms = {n: median([evs[i].elapsed_time(evs[i + 1]) for evs in events]) for i, n in enumerate(PHASES)}
+    return wall / steps * 1e3, median(step_ms), phase_ms
+
+
+def summarize(cfg, st, work, ms_event, phase_ms):
+    """Throughput, MFMA utilisation, roofline of the dominant GEMM and HBM
+    fractions of the other phases."""
+    nv = st["n_valid"]
+    act = st["activated_gemm_flops"]
+    gemm_ms = phase_ms["up_gemm"] + phase_ms["down_gemm"]
+    dom = "up_gemm" if phase_ms["up_gemm"] >= phase_ms["down_gemm"] else "down_gemm"
+    achieved = act / 2.0 / (phase_ms[dom] / 1e3)       # each projection is half of 4 d M C_B
+    pb = phase_bytes(cfg, st)
+    rpc = ["routing", "permute", "combine"]
+    out = {
+        "tokens_per_s": round(nv / (ms_event / 1e3), 1), "ms_per_step_event_median": round(ms_event, 4),
+        "n_valid": nv, "mean_b": round(st["mean_b"], 3), "mean_k": round(st["mean_k"], 3),
+        "mean_cb": round(st["mean_cb"], 3), "activated_gemm_tflop": round(act / 1e12, 4),
+        "phases_ms": {n: round(v, 4) for n, v in phase_ms.items()},
+        "mfma_util_activated": round(act / (gemm_ms / 1e3) / PEAK_BF16_FLOPS, 4),
+        "roofline_dominant_gemm": {"bound": "mfma", "kernel": dom, "achieved": round(achieved / 1e12, 2),
+                                   "peak": PEAK_BF16_FLOPS / 1e12, "unit": "TFLOP/s",
+                                   "frac": round(achieved / PEAK_BF16_FLOPS, 4)},
+        "hbm_frac": {n: round(pb[n] / (phase_ms[n] / 1e3) / PEAK_HBM_BYTES, 4) for n in pb if phase_ms[n] > 0},
+        "hbm_frac_routing_permute_combine": round(
+            sum(pb[n] for n in rpc) / (sum(phase_ms[n] for n in rpc) / 1e3) / PEAK_HBM_BYTES, 4),
+    }
+    if work is not None:
+        out["executed_vs_activated"] = {
+            "up": round(work["up_mfma_flops"] / (act / 2.0), 4),
+            "down": round(work["down_mfma_flops"] / (act / 2.0), 4),
+            "mfma_util_executed": round((work["up_mfma_flops"] + work["down_mfma_flops"]) / (gemm_ms / 1e3)
+                                        / PEAK_BF16_FLOPS, 4)}
+    return out
+
+
+def cpu_baseline_and_sample_check(g, Y_gpu, rec_gpu, n_sample, repeats):
+    """The CPU oracle timed on a seeded sample of the same workload; the GPU
+    output on the sample checked against it (raw and beyond-half-ulp error
+    x RMS over the tokens whose decisions the two agree on and whose margins
+    are at least 1e-4; near-tie tokens counted)."""
     import numpy as np
     from threadpoolctl import threadpool_info
     import oracle.unif_moe_oracle as O
+    from synth.generate import bf16_bits_to_f32
 
     cfg = dict(g["cfg"])
     valid_idx = np.arange(cfg["n_tokens"]) if g["valid"] is None else np.nonzero(g["valid"])[0]
@@ -124,21 +236,37 @@ def cpu_baseline(g, n_sample, repeats):
     Xs = g["X"][sample]
     weights = O.ExpertWeights(cfg, g["W_up"], g["W_down"])   # one-time weight preparation
     times, cpu = [], []
+    Yref = rec = None
     for _ in range(repeats):
         w0, c0 = time.perf_counter(), time.process_time()
-        O.forward(sub, Xs, None, g["W_router"], g["prototypes"], None, None, weights=weights)
+        Yref, rec = O.forward(sub, Xs, None, g["W_router"], g["prototypes"], None, None, weights=weights)
         times.append(time.perf_counter() - w0)
         cpu.append(time.process_time() - c0)
     med = float(np.median(times))
     blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
     threads = int(blas[0]["num_threads"]) if blas else 1
-    return {"value": round(sample.size / med, 2), "unit": "tokens/s", "cores": threads,
-            "kind": "oracle",
+    base = {"value": round(sample.size / med, 2), "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{sample.size} seeded valid tokens of the same workload, routing + "
                       f"per-token expert evaluation, median of {repeats} runs "
                       f"({med:.2f} s each; numpy BLAS threads {threads}, "
                       f"CPU/wall {float(np.median(cpu)) / med:.2f}; weights converted once, untimed)",
             "host_cpu": _cpu_model(), "nproc": os.cpu_count()}
+    m, _ = O.margins(sub, rec)
+    same = np.ones(sample.size, bool)
+    for key in ("n_shared", "shared_mask", "n_res"):
+        same &= rec_gpu[key][sample] == rec[key]
+    sure = (m >= 1e-4) & same
+    yg = bf16_bits_to_f32(Y_gpu[sample][sure]).astype(np.float64)
+    ref = Yref[sure]
+    rms = float(np.sqrt(np.mean(ref ** 2))) if ref.size else 1.0
+    err = np.abs(yg - ref)
+    half = np.where(ref == 0, 0.0, 2.0 ** (np.floor(np.log2(np.maximum(np.abs(ref), 1e-300))) - 8))
+    check = {"tokens": int(sample.size), "near_ties": int(np.sum(m < 1e-4)),
+             "decisions_differ_beyond_margin": int(np.sum((m >= 1e-4) & ~same)),
+             "max_raw_error_x_rms": round(float(err.max() / rms), 5) if err.size else 0.0,
+             "max_error_beyond_half_ulp_x_rms": round(float(np.maximum(err - half, 0).max() / rms), 5)
+             if err.size else 0.0}
+    return base, check
 
 
 def _cpu_model():
@@ -173,54 +301,19 @@ def main():
     dev = DeviceLayer(cfg, g["X"], g["valid"], g["W_router"], g["prototypes"], g["W_up"], g["W_down"])
     stream = torch.cuda.current_stream()
 
-    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        dev.forward()
-    torch.cuda.synchronize()
+    print(f"[bench] warmup {args.warmup}, timing {args.steps} steps", file=sys.stderr, flush=True)
+    ms_per_step, ms_event, phase_ms = measure(torch, _lib, dev, cfg, args.steps, args.warmup, stream)
     st = dev.stats()
-
-    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        dev.forward()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = wall / args.steps * 1e3
-
-    # Same steps again through the instrumented entry point: the library
-    # records seven events per step on the launch stream.
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(_lib.N_PHASE_EVENTS)]
-              for _ in range(args.steps)]
-    for evs in events:
-        for ev in evs:
-            ev.record(stream)          # creates the underlying HIP event
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for evs in events:
-        _lib.layer_forward_profiled(cfg, dev.X, dev.valid, dev.W_router, dev.prototypes, dev.W_up,
-                                    dev.W_down, dev.Y, dev.ws_forward, evs, routing=dev.routing,
-                                    stream=stream)
-    torch.cuda.synchronize()
-    wall_prof = time.perf_counter() - t0
-    names = ["wdown_f16", "routing", "permute", "up_gemm", "down_gemm", "combine"]
-    phase_ms = {n: float(np.mean([evs[i].elapsed_time(evs[i + 1]) for evs in events]))
-                for i, n in enumerate(names)}
-
+    work = _lib.forward_work(cfg, dev.ws_forward) if cfg["dtype"] == "bf16" else None
+    Y_head = dev.output_numpy()
+    rec_head = dev.routing_numpy()
+    head = summarize(cfg, st, work, ms_event, phase_ms)
     nv = st["n_valid"]
-    value = nv / (ms_per_step / 1e3)
-    act = st["activated_gemm_flops"]
-    gemm_ms = phase_ms["up_gemm"] + phase_ms["down_gemm"]
-    dom = "up_gemm" if phase_ms["up_gemm"] >= phase_ms["down_gemm"] else "down_gemm"
-    dom_flops = act / 2.0                       # each projection is half of 4 d M C_B
-    achieved = dom_flops / (phase_ms[dom] / 1e3)
-    pb = phase_bytes(cfg, st)
-    hbm = {n: pb[n] / (phase_ms[n] / 1e3) / PEAK_HBM_BYTES for n in pb}
-    hbm_all = sum(pb.values()) / ((phase_ms["routing"] + phase_ms["permute"] + phase_ms["combine"]) / 1e3)
-
+    rf = head["roofline_dominant_gemm"]
     out = {
-        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "metric": METRIC, "value": round(nv / (ms_per_step / 1e3), 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step_event_median": head["ms_per_step_event_median"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"{args.workload}: {cfg['n_tokens']} tokens x d={cfg['d_model']}, "
@@ -229,54 +322,62 @@ def main():
                    "n_tokens": cfg["n_tokens"], "n_valid": nv, "d_model": cfg["d_model"],
                    "n_experts": cfg["n_experts"], "n_blocks": cfg["n_blocks"],
                    "block_width": cfg["block_width"], "mass_threshold": cfg["mass_threshold"]},
-        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved / 1e12, 2),
-                     "peak": PEAK_BF16_FLOPS / 1e12, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_FLOPS, 4), "traffic": committed_traffic(dom)},
-        "mfma_util_activated": round(act / (gemm_ms / 1e3) / PEAK_BF16_FLOPS, 4),
-        "hbm_frac": {n: round(v, 4) for n, v in hbm.items()},
-        "hbm_frac_routing_permute_combine": round(hbm_all / PEAK_HBM_BYTES, 4),
-        "phases_ms": {n: round(v, 4) for n, v in phase_ms.items()},
-        "profiled_ms_per_step": round(wall_prof / args.steps * 1e3, 4),
-        "routing_stats": {"mean_b": round(st["mean_b"], 3), "mean_k": round(st["mean_k"], 3),
-                          "mean_cb": round(st["mean_cb"], 3),
-                          "activated_gemm_tflop": round(act / 1e12, 4)},
+        "roofline": {"bound": "mfma", "kernel": rf["kernel"], "achieved": rf["achieved"], "peak": rf["peak"],
+                     "unit": "TFLOP/s", "frac": rf["frac"], "traffic": committed_traffic(rf["kernel"])},
     }
+    for k in ("mfma_util_activated", "executed_vs_activated", "hbm_frac", "hbm_frac_routing_permute_combine",
+              "phases_ms"):
+        if k in head:
+            out[k] = head[k]
+    out["routing_stats"] = {k: head[k] for k in ("mean_b", "mean_k", "mean_cb", "activated_gemm_tflop")}
+
+    clock = ClockSampler()
+    clock.start()
     if not args.no_paper_exact and cfg["mass_threshold"] != 1.0:
         # The same tokens and weights with the target exactly Eq. beta
         # (t = 1): more residual experts per token, so more activated work.
+        print("[bench] paper-exact target t = 1", file=sys.stderr, flush=True)
         cfg1 = dict(cfg, mass_threshold=1.0)
         dev1 = DeviceLayer(cfg1, g["X"], g["valid"], g["W_router"], g["prototypes"], g["W_up"], g["W_down"])
-        steps1 = max(1, args.steps // 2)
-        for _ in range(args.warmup):
-            dev1.forward()
-        torch.cuda.synchronize()
+        steps1 = max(2, args.steps // 2)
+        ms1, ev1, ph1 = measure(torch, _lib, dev1, cfg1, steps1, args.warmup, stream)
         st1 = dev1.stats()
-        t0 = time.perf_counter()
-        for _ in range(steps1):
-            dev1.forward()
-        torch.cuda.synchronize()
-        ms1 = (time.perf_counter() - t0) / steps1 * 1e3
-        out["paper_exact_t1"] = {
-            "ms_per_step": round(ms1, 4), "tokens_per_s": round(st1["n_valid"] / (ms1 / 1e3), 1),
-            "steps": steps1, "mean_k": round(st1["mean_k"], 3), "mean_cb": round(st1["mean_cb"], 3),
-            "activated_gemm_tflop": round(st1["activated_gemm_flops"] / 1e12, 4),
-            "activated_tflops_per_s": round(st1["activated_gemm_flops"] / (ms1 / 1e3) / 1e12, 1)}
+        s1 = summarize(cfg1, st1, _lib.forward_work(cfg1, dev1.ws_forward), ev1, ph1)
+        out["paper_exact_t1"] = dict(s1, steps=steps1, ms_per_step=round(ms1, 4))
         del dev1
+        torch.cuda.empty_cache()
+    if not args.no_configs:
+        out["configs"] = {}
+        for name in OTHER_CONFIGS:
+            print(f"[bench] workload {name}", file=sys.stderr, flush=True)
+            gc = generate(name)
+            cc = layer_config(gc["cfg"])
+            dc = DeviceLayer(cc, gc["X"], gc["valid"], gc["W_router"], gc["prototypes"], gc["W_up"], gc["W_down"])
+            sc = max(2, args.steps // 2) if cc["n_tokens"] > 100000 else args.steps
+            msc, evc, phc = measure(torch, _lib, dc, cc, sc, args.warmup, stream)
+            stc = dc.stats()
+            entry = summarize(cc, stc, _lib.forward_work(cc, dc.ws_forward), evc, phc)
+            entry.update(steps=sc, ms_per_step=round(msc, 4),
+                         shape=f"{cc['n_tokens']} tokens x d={cc['d_model']}, K={cc['n_experts']}, "
+                               f"B={cc['n_blocks']} x M={cc['block_width']}, t={cc['mass_threshold']}")
+            out["configs"][name] = entry
+            del dc, gc
+            torch.cuda.empty_cache()
+    out["sclk"] = clock.stop()
     if not args.no_block:
         # The pre-LN block (as in DeiT) around the same layer: LN(x) feeds
         # routing and experts, b1 and b2 are added, and x is added back.
+        print("[bench] pre-LN block", file=sys.stderr, flush=True)
         from synth import block_inputs
         blk, Xb = block_inputs(g, "pre", residual=True, eps=1e-6)
-        dev.X = None
-        torch.cuda.empty_cache()
         Xd = torch.from_numpy(Xb.view(np.int16)).view(torch.bfloat16).to(dev.device)
         bd = dict(norm="pre", residual=True, ln_eps=float(blk["ln_eps"]))
         for k in ("ln_gamma", "ln_beta", "b_up", "b_down"):
             bd[k] = torch.from_numpy(blk[k]).to(dev.device)
-        wsb = _lib.alloc_workspace(_lib.block_forward_workspace_size(cfg, bd), dev.device)
         dev.ws_forward = None
         torch.cuda.empty_cache()
-        stepsb = max(1, args.steps // 2)
+        wsb = _lib.alloc_workspace(_lib.block_forward_workspace_size(cfg, bd), dev.device)
+        stepsb = max(2, args.steps // 2)
 
         def block_step():
             _lib.block_forward(cfg, bd, Xd, dev.valid, dev.W_router, dev.prototypes, dev.W_up,
@@ -295,13 +396,15 @@ def main():
             "steps": stepsb, "mean_cb": round(stb["mean_cb"], 3),
             "over_layer_ms": round(msb - ms_per_step, 4)}
         del Xd, wsb, bd
+        torch.cuda.empty_cache()
     if not args.no_backward:
         # Gradients of sum(dY * Y) for the layer (forward recomputed inside).
         # Algorithmic work: four products of 2 d M per activated block (dh,
         # dx, dW_up, dW_down), i.e. 8 d M sum(C_B).
+        print("[bench] backward", file=sys.stderr, flush=True)
         from synth import upstream_grad
-        if dev.X is None:
-            dev.X = torch.from_numpy(g["X"].view(np.int16)).view(torch.bfloat16).to(dev.device)
+        dev.ws_forward = None
+        torch.cuda.empty_cache()
         dY = upstream_grad(g)
         dYd = torch.from_numpy(dY.view(np.int16)).view(torch.bfloat16).to(dev.device)
         N, d, K = cfg["n_tokens"], cfg["d_model"], cfg["n_experts"]
@@ -315,22 +418,22 @@ def main():
             _lib.layer_backward(cfg, dev.X, dev.valid, dev.W_router, dev.prototypes, dev.W_up,
                                 dev.W_down, dYd, gr["dX"], gr["dW_up"], gr["dW_down"],
                                 gr["dW_router"], wsg, stream=stream)
-        print("[bench] backward", file=sys.stderr, flush=True)
         bwd_step()
         torch.cuda.synchronize()
-        stepsg = 2
-        t0 = time.perf_counter()
-        for _ in range(stepsg):
+        stepsg = 3
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(stepsg)]
+        for a, b in ev:
+            a.record(stream)
             bwd_step()
+            b.record(stream)
         torch.cuda.synchronize()
-        msg = (time.perf_counter() - t0) / stepsg * 1e3
+        msg = median([a.elapsed_time(b) for a, b in ev])
         bflops = 8.0 * cfg["d_model"] * cfg["block_width"] * st["activated_blocks"]
         out["backward"] = {
-            "ms_per_step": round(msg, 3), "steps": stepsg, "dtype": "f32 (bf16 inputs)",
+            "ms_per_step": round(msg, 3), "steps": stepsg, "over_forward": round(msg / ms_event, 2),
             "algorithmic_tflop": round(bflops / 1e12, 4),
-            "roofline": {"bound": "alu", "achieved": round(bflops / (msg / 1e3) / 1e12, 2),
-                         "peak": PEAK_FP32_VECTOR / 1e12, "unit": "TFLOP/s",
-                         "frac": round(bflops / (msg / 1e3) / PEAK_FP32_VECTOR, 4)}}
+            "achieved_tflops": round(bflops / (msg / 1e3) / 1e12, 2),
+            "workspace_gb": round(wsg.numel() / 1e9, 2)}
         del wsg, gr, dYd
         torch.cuda.empty_cache()
     if args.copy_calibration_mb > 0:
@@ -343,7 +446,9 @@ def main():
         del src, dst
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(g, args.cpu_sample, args.cpu_repeats)
+        base, check = cpu_baseline_and_sample_check(g, Y_head, rec_head, args.cpu_sample, args.cpu_repeats)
+        out["cpu_baseline"] = base
+        out["parity_on_sample"] = check
     print(json.dumps(out), flush=True)
 
 

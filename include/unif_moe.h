@@ -339,6 +339,27 @@ int32_t unif_moe_stats(const unif_moe_config* cfg, const unif_moe_routing* routi
                        const uint8_t* valid, unif_moe_stats_t* host_out,
                        void* workspace, size_t workspace_bytes, void* stream);
 
+/* Work that a bf16 forward executed (host structure filled by
+ * unif_moe_forward_work): the up-projection computes whole tiles of its
+ * slabs' rows, the down-projection each 32-row group over the blocks any of
+ * its rows uses (the activated work is 4 d M sum C_B, unif_moe_stats). */
+typedef struct unif_moe_work_t {
+    int64_t pairs;            /* (token, expert) pairs                            */
+    int64_t up_tiles;         /* up-projection tiles                              */
+    int64_t down_tiles;       /* down-projection tiles (row tiles x column tiles) */
+    double  up_mfma_flops;    /* matrix-core FLOPs the up-projection executed     */
+    double  down_mfma_flops;  /* matrix-core FLOPs the down-projection executed   */
+} unif_moe_work_t;
+
+/* Reads the tile tables that the last unif_moe_layer_forward (or
+ * _profiled / _static: the latter's workspace is not reachable here) left in
+ * `workspace` for this cfg and fills *host_out; synchronises `stream`.
+ * bf16 layers only (UNIF_EUNSUPPORTED otherwise). Errors: UNIF_EINVAL,
+ * UNIF_EWORKSPACE, UNIF_EUNSUPPORTED, UNIF_EDEVICE. Follows the shape rules
+ * of unif_moe_layer_forward. */
+int32_t unif_moe_forward_work(const unif_moe_config* cfg, const void* workspace, size_t workspace_bytes,
+                              unif_moe_work_t* host_out, void* stream);
+
 /* Static text for a status code ("unknown status" for other values). */
 const char* unif_moe_status_string(int32_t status);
 

@@ -58,8 +58,14 @@ EXPORTS = ("unif_moe_route_workspace_size", "unif_moe_route",
            "unif_moe_layer_forward_profiled", "unif_moe_block_forward_workspace_size",
            "unif_moe_block_forward", "unif_moe_layer_backward_workspace_size",
            "unif_moe_layer_backward", "unif_moe_stats_workspace_size",
-           "unif_moe_stats", "unif_moe_layer_forward_static", "unif_moe_status_string")
+           "unif_moe_stats", "unif_moe_layer_forward_static", "unif_moe_forward_work",
+           "unif_moe_status_string")
 N_PHASE_EVENTS = 7
+
+
+class Work(ctypes.Structure):
+    _fields_ = [("pairs", ctypes.c_int64), ("up_tiles", ctypes.c_int64), ("down_tiles", ctypes.c_int64),
+                ("up_mfma_flops", ctypes.c_double), ("down_mfma_flops", ctypes.c_double)]
 
 
 class UnifMoeError(RuntimeError):
@@ -101,6 +107,7 @@ def lib():
                                              ctypes.POINTER(Routing), vp, sz, vp]
         L.unif_moe_layer_forward_static.argtypes = [cfgp, vp, vp, vp, vp, vp, vp, vp,
                                                     ctypes.POINTER(Routing), vp]
+        L.unif_moe_forward_work.argtypes = [cfgp, vp, sz, ctypes.POINTER(Work), vp]
         L.unif_moe_status_string.argtypes = [ctypes.c_int32]
         L.unif_moe_status_string.restype = ctypes.c_char_p
         for name in EXPORTS[:-1]:
@@ -304,3 +311,15 @@ def stats(cfg, routing, valid, workspace, stream=None):
                 expert_tokens=list(s.expert_tokens), activated_blocks=s.activated_blocks,
                 mean_b=s.mean_b, mean_k=s.mean_k, mean_cb=s.mean_cb,
                 activated_gemm_flops=s.activated_gemm_flops, routing_flops=s.routing_flops)
+
+
+def forward_work(cfg, workspace, stream=None):
+    """Work the last forward in ``workspace`` executed (unif_moe_forward_work)."""
+    c = make_config(cfg)
+    w = Work()
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().unif_moe_forward_work(ctypes.byref(c), _ptr(workspace), ws_bytes, ctypes.byref(w),
+                                       _stream(stream)), "unif_moe_forward_work")
+    return dict(pairs=w.pairs, up_tiles=w.up_tiles, down_tiles=w.down_tiles,
+                up_mfma_flops=w.up_mfma_flops, down_mfma_flops=w.down_mfma_flops)
+

@@ -51,4 +51,17 @@ __global__ __launch_bounds__(256) void stats_kernel(StatsParams s) {
     }
 }
 
+// Work a bf16 forward executed, from its workspace tables: out[0] the block
+// count of every 32-row MFMA group of the down-projection's row tiles, summed
+// (each counts 32 rows x M x d x 2 FLOPs). One thread per row tile.
+__global__ __launch_bounds__(256) void work_kernel(const uint64_t* __restrict__ rt_masks, const int* __restrict__ totals,
+                                                   int groups, unsigned long long* out) {
+    const int nrt = totals[4];
+    unsigned long long n = 0;
+    for (int rt = blockIdx.x * blockDim.x + threadIdx.x; rt < nrt; rt += gridDim.x * blockDim.x)
+        for (int g = 0; g < groups; ++g) n += (unsigned long long)__popcll(rt_masks[(size_t)rt * (groups + 1) + g]);
+    for (int o = 32; o > 0; o >>= 1) n += __shfl_xor(n, o);
+    if ((threadIdx.x & 63) == 0 && n) atomicAdd(out, n);
+}
+
 }  // namespace unifmoe

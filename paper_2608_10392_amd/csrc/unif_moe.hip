@@ -229,7 +229,7 @@ struct FwdPlan {
     size_t alpha, nsh, mask, nres, eids, wts;
     size_t wsplit, logits;
     size_t zero_begin, zero_end;  // bin_count, slab_count, totals, zero page
-    size_t bin_count, slab_count, exp_total, totals, queues, zero_page;
+    size_t bin_count, slab_count, exp_total, totals, queues, zero_page, work;
     size_t bin_cursor, seg_off, down_tile_off, tile_cnt, max_row_tiles, rt_info, rt_masks;
     size_t pair_token, pair_mask, pair_expert, pair_of, pair_rank, slab_rows, slab_tok, up_tile_info, up_tile_rows, hbuf, part;
     size_t xn;      // LN(X), the FFN input of a pre-LN block
@@ -239,17 +239,20 @@ struct FwdPlan {
 
 size_t ceil_div_sz(size_t a, size_t b) { return (a + b - 1) / b; }
 
-FwdPlan plan_forward(const Dims& m, bool own_record, size_t xn_bytes = 0) {
+// The routing record's region is reserved whether or not the caller passes
+// its own record, so every other offset is the same for both kinds of call
+// (unif_moe_forward_work reads the workspace a forward left behind).
+FwdPlan plan_forward(const Dims& m, size_t xn_bytes = 0) {
     Carver cv;
     FwdPlan p;
     const size_t N = (size_t)m.N, K = (size_t)m.K, K1 = (size_t)m.K1;
     const size_t pmax = N * K1;
-    p.alpha = cv.take(own_record ? 4 * N : 0);
-    p.nsh = cv.take(own_record ? 4 * N : 0);
-    p.mask = cv.take(own_record ? 8 * N : 0);
-    p.nres = cv.take(own_record ? 4 * N : 0);
-    p.eids = cv.take(own_record ? 4 * N * K : 0);
-    p.wts = cv.take(own_record ? 4 * N * K : 0);
+    p.alpha = cv.take(4 * N);
+    p.nsh = cv.take(4 * N);
+    p.mask = cv.take(8 * N);
+    p.nres = cv.take(4 * N);
+    p.eids = cv.take(4 * N * K);
+    p.wts = cv.take(4 * N * K);
     p.wsplit = cv.take(m.bf16 ? (size_t)3 * m.NLP * m.d * sizeof(u16) : 0);
     p.logits = cv.take((size_t)N * split_route_cols(m) * sizeof(float));
     p.bin_count = cv.take(4 * (size_t)m.nbin * kBinCopies);
@@ -260,6 +263,7 @@ FwdPlan plan_forward(const Dims& m, bool own_record, size_t xn_bytes = 0) {
     p.queues = cv.take(4 * 16);   // per-XCD tile counters: up, then down
     p.zero_page = cv.take(256);
     p.zero_end = cv.cur;
+    p.work = cv.take(16);   // unif_moe_forward_work's counter
     p.bin_cursor = cv.take(4 * (size_t)m.nbin * kBinCopies);
     p.seg_off = cv.take(4 * (K1 + 1));
     p.down_tile_off = cv.take(4 * (K1 + 1));
@@ -481,7 +485,7 @@ int32_t unif_moe_layer_forward_workspace_size(const unif_moe_config* cfg, size_t
     if (s != UNIF_OK) return s;
     s = check_forward_shape(cfg);
     if (s != UNIF_OK) return s;
-    *bytes = plan_forward(dims_of(cfg), true).total;
+    *bytes = plan_forward(dims_of(cfg)).total;
     return UNIF_OK;
 }
 
@@ -542,7 +546,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         return UNIF_EINVAL;
     const Dims m = dims_of(cfg);
     const bool own = routing_out == nullptr;
-    const FwdPlan plan = plan_forward(m, own, block_xn_bytes(cfg, blk));
+    const FwdPlan plan = plan_forward(m, block_xn_bytes(cfg, blk));
     // The size reported by the query always includes the internal record.
     size_t need = 0;
     if (blk != nullptr) unif_moe_block_forward_workspace_size(cfg, blk, &need);
@@ -821,7 +825,7 @@ int32_t unif_moe_block_forward_workspace_size(const unif_moe_config* cfg, const 
     if (s != UNIF_OK) return s;
     s = check_block_shape(cfg, blk);
     if (s != UNIF_OK) return s;
-    *bytes = plan_forward(dims_of(cfg), true, block_xn_bytes(cfg, blk)).total;
+    *bytes = plan_forward(dims_of(cfg), block_xn_bytes(cfg, blk)).total;
     return UNIF_OK;
 }
 
@@ -859,7 +863,7 @@ struct BwdPlan {
 
 BwdPlan plan_backward(const Dims& m) {
     BwdPlan b;
-    b.fwd = plan_forward(m, true).total;   // includes its own 256 bytes of alignment slack
+    b.fwd = plan_forward(m).total;   // includes its own 256 bytes of alignment slack
     const size_t pmax = (size_t)m.N * m.K1;
     Carver cv;
     cv.cur = b.fwd;
@@ -935,7 +939,7 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
     const dim3 wg_grid((unsigned)(tiles_h * tiles_d), 2, (unsigned)m.K1);
     // 1. the forward (routing record, pair tables) into the front of the workspace
     char* ws = align_base(workspace);
-    const FwdPlan fp = plan_forward(m, true);
+    const FwdPlan fp = plan_forward(m);
     void* Yscratch = ws + bp.y;
     if (m.N > 0) {
         s = forward_impl(cfg, nullptr, X, valid, W_router, prototypes, W_up, W_down, Yscratch, nullptr, ws,
@@ -1113,3 +1117,47 @@ int32_t unif_moe_layer_forward_static(const unif_moe_config* cfg, const void* X,
 }
 
 }  // extern "C"
+
+extern "C" {
+
+int32_t unif_moe_forward_work(const unif_moe_config* cfg, const void* workspace, size_t workspace_bytes,
+                              unif_moe_work_t* host_out, void* stream) {
+    int32_t s = check_config(cfg);
+    if (s != UNIF_OK) return s;
+    s = check_forward_shape(cfg);
+    if (s != UNIF_OK) return s;
+    if (host_out == nullptr) return UNIF_EINVAL;
+    if (cfg->dtype != UNIF_BF16) return UNIF_EUNSUPPORTED;
+    size_t need = 0;
+    unif_moe_layer_forward_workspace_size(cfg, &need);
+    if (workspace == nullptr || workspace_bytes < need) return UNIF_EWORKSPACE;
+    std::memset(host_out, 0, sizeof(*host_out));
+    const Dims m = dims_of(cfg);
+    if (m.N == 0) return UNIF_OK;
+    const FwdPlan plan = plan_forward(m);
+    char* ws = align_base(const_cast<void*>(workspace));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    unsigned long long* cnt = reinterpret_cast<unsigned long long*>(ws + plan.work);
+    const int* totals = reinterpret_cast<const int*>(ws + plan.totals);
+    fill_zero_kernel<<<1, 64, 0, st>>>(reinterpret_cast<uint32_t*>(cnt), 2);
+    UNIF_LAUNCH_CHECK();
+    const DownShape dsh = down_shape(m.d);
+    work_kernel<<<(unsigned)std::min<size_t>(ceil_div_sz(plan.max_row_tiles, 256), 1024), 256, 0, st>>>(
+        reinterpret_cast<const uint64_t*>(ws + plan.rt_masks), totals, dsh.tm / 32, cnt);
+    UNIF_LAUNCH_CHECK();
+    int32_t t[8];
+    unsigned long long g = 0;
+    if (hipMemcpyAsync(t, totals, sizeof(t), hipMemcpyDeviceToHost, st) != hipSuccess) return UNIF_EDEVICE;
+    if (hipMemcpyAsync(&g, cnt, sizeof(g), hipMemcpyDeviceToHost, st) != hipSuccess) return UNIF_EDEVICE;
+    if (hipStreamSynchronize(st) != hipSuccess) return UNIF_EDEVICE;
+    const double dM = (double)m.M, dd = (double)m.d;
+    host_out->pairs = t[0];
+    host_out->up_tiles = t[1];
+    host_out->down_tiles = t[2];
+    host_out->up_mfma_flops = (double)t[1] * up_tm(m.M, m.d) * dM * dd * 2.0;
+    host_out->down_mfma_flops = (double)g * 32.0 * dM * dd * 2.0;
+    return UNIF_OK;
+}
+
+}  // extern "C"
+

@@ -220,3 +220,54 @@ def test_full_workload(name):
     run_case(g, f"workload {name}", n_sample=FULL_SAMPLE[name],
              near_cap=64 if name == "zipf_stress" else 256)
     _free()
+
+
+@pytest.mark.parametrize("routing_passed", [False, True])
+def test_forward_work_counts(routing_passed):
+    """unif_moe_forward_work on the workspace of the last forward: the pair
+    count is n_valid + sum k; the up-projection ran sum over (expert, block)
+    slabs of ceil(rows / tile) tiles, where a slab's rows are the tokens whose
+    I_shr holds the block (shared expert) or that selected the expert
+    (residual, every block); executed MFMA work is at least the activated
+    work. Holds with the routing record in the workspace or passed in."""
+    from paper_2608_10392_amd import _lib
+    g = generate(get_config("vit_s16", n_tokens=2500, d_model=384, n_experts=8, n_blocks=8,
+                            block_width=192, max_shared=8))
+    cfg = layer_config(g["cfg"])
+    dev = _device_layer(g)
+    if routing_passed:
+        dev.forward()
+    else:
+        dev.ws_forward = _lib.alloc_workspace(_lib.layer_forward_workspace_size(cfg), dev.device)
+        _lib.layer_forward(cfg, dev.X, dev.valid, dev.W_router, dev.prototypes, dev.W_up,
+                           dev.W_down, dev.Y, dev.ws_forward)
+        dev.route()   # the same decisions, into dev.routing, for the tie check
+    torch.cuda.synchronize()
+    w = _lib.forward_work(cfg, dev.ws_forward)
+    orec = O.route(g["cfg"], g["X"], g["valid"], g["W_router"], g["prototypes"])
+    if parity.check_routing(g["cfg"], orec, dev.routing_numpy())["n_near_differ"]:
+        pytest.skip("a near-tie decision differs; counts are then not fixed by the oracle")
+    N, K, B, M, d = cfg["n_tokens"], cfg["n_experts"], cfg["n_blocks"], cfg["block_width"], cfg["d_model"]
+    rows = np.zeros((K + 1, B), np.int64)
+    pairs = 0
+    act_blocks = 0
+    for t in range(N):
+        if not orec["valid"][t]:
+            continue
+        b, shr, k, q = O.decisions(orec, t)
+        pairs += 1 + k
+        act_blocks += b + k * B
+        for c in shr:
+            rows[0, c] += 1
+        for e in q:
+            rows[e, :] += 1
+    assert w["pairs"] == pairs
+    per_tile = 2.0 * M * d
+    tm = w["up_mfma_flops"] / (w["up_tiles"] * per_tile)
+    assert tm in (32.0, 64.0, 128.0, 256.0), tm
+    assert w["up_tiles"] == int(np.sum(-(-rows // int(tm))))
+    act_half = 2.0 * d * M * act_blocks
+    assert act_half <= w["up_mfma_flops"] and act_half <= w["down_mfma_flops"]
+    # each 32-row group of a down tile runs at most every block once
+    assert w["down_mfma_flops"] <= (pairs + 32 * (K + 1)) * B * 2.0 * M * d
+    _free()
