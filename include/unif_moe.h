@@ -268,41 +268,66 @@ int32_t unif_moe_block_forward(const unif_moe_config* cfg, const unif_moe_block*
                                size_t workspace_bytes, void* stream);
 
 /* Workspace needed by unif_moe_layer_backward (bytes). Host only. It holds
- * the forward's workspace plus fp32 per-pair intermediates sized for the
- * worst case: 4 (2 H + d + 2) N (K+1) bytes and the forward output. */
+ * the forward's workspace (routing record, pair tables, the H buffer and
+ * the fp32 per-pair rows, which take dx per pair), and, for bf16 layers, a
+ * second H-shaped buffer ((N(K+1) + 1) H bf16 values), a transposed copy of
+ * W_down and 8 B N(K+1) bytes of per-block partial sums; for fp32 layers
+ * 8 H N(K+1) bytes of fp32 intermediates. */
 int32_t unif_moe_layer_backward_workspace_size(const unif_moe_config* cfg, size_t* bytes);
 
 /* Backward pass of the layer for a training step: the gradients of
  * sum(dY * Y) with Y the output of unif_moe_layer_forward for the same
- * arguments. The forward is recomputed inside (same kernels, so the same
- * discrete decisions). Readings, since the paper gives no gradients: the
- * decisions b, I_shr, the expert order q and k are held fixed (they are
- * piecewise constant); gradients flow through alpha (Eq. alpha) to W_shr and
- * x, through the selected affinities p_i (softmax of Eq.
- * residual-router-score) to W_1..W_K and x, and through the expert FFNs of
- * Eq. block-expert-output; the prototypes get none. Padded tokens get
+ * arguments. Routing and the permutation are recomputed inside (same
+ * kernels, so the same discrete decisions). Readings, since the paper gives
+ * no gradients: the decisions b, I_shr, the expert order q and k are held
+ * fixed (they are piecewise constant); gradients flow through alpha (Eq.
+ * alpha) to W_shr and x, through the selected affinities p_i (softmax of
+ * Eq. residual-router-score) to W_1..W_K and x, and through the expert FFNs
+ * of Eq. block-expert-output; the prototypes get none. Padded tokens get
  * dX = 0 and contribute nothing.
  *   dY         [N, d] (cfg->dtype)
  *   dX         [N, d] fp32, written
  *   dW_up      [K+1, H, d] fp32, written (layout of W_up)
  *   dW_down    [K+1, d, H] fp32, written (layout of W_down)
  *   dW_router  [K+1, d] fp32, written (layout of W_router)
- * dX and dW_router are bitwise repeatable; dW_up and dW_down sum over each
- * expert's pairs in the forward's permutation order, which within equal
- * block-mask keys depends on the arrival order of atomics, so repeated calls
- * agree to fp32 rounding.
- * All arithmetic is fp32 (bf16 inputs are exact in fp32). A first
- * implementation on the vector units: tiled fp32 GEMMs over each expert's
- * pairs (activations recomputed, dense over H and masked to the pair's
- * blocks) and for the weight gradients. Requires what unif_moe_layer_forward
- * requires and N <= 8,388,480; otherwise UNIF_EUNSUPPORTED. Errors as
- * unif_moe_layer_forward. The Gram diversity loss of Eq. diversity-loss is a
- * (K+1) x (K+1) product of the router with itself and is left to the caller. */
+ * Every gradient is bitwise repeatable: each sum runs in a fixed order (the
+ * expert weight gradients over each (expert, block)'s rows in token order).
+ * bf16 layers run on the matrix cores over the (pair, block) rows the
+ * forward runs, never over inactive blocks: a = x K^T with GELU(a) and
+ * GELU'(a) kept in fp16; dy V (bf16 products, fp32 sums) gives the pair's
+ * d loss / d weight (sum of GELU(a) . dy V over its blocks, fp32), then
+ * d loss / da = w (dy V) GELU'(a) and w GELU(a), both rounded to bf16, which
+ * feed dx = sum over blocks of (d loss / da) K and the weight gradients
+ * (bf16 products, fp32 sums). fp32 layers run on the vector units in fp32
+ * (tiled GEMMs over each expert's pairs, dense over H and masked to the
+ * pair's blocks) and require N <= 8,388,480. Requires what
+ * unif_moe_layer_forward requires; otherwise UNIF_EUNSUPPORTED. Errors as
+ * unif_moe_layer_forward. */
 int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
                                 const float* W_router, const float* prototypes, const void* W_up,
                                 const void* W_down, const void* dY, float* dX, float* dW_up,
                                 float* dW_down, float* dW_router, void* workspace,
                                 size_t workspace_bytes, void* stream);
+
+/* Workspace needed by unif_moe_diversity_loss (bytes): 8 ((K+1)^2 + 1)
+ * bytes plus alignment. Host only. */
+int32_t unif_moe_diversity_loss_workspace_size(const unif_moe_config* cfg, size_t* bytes);
+
+/* Gram diversity loss of the augmented router (Eq. diversity-loss, part of
+ * the training objective of Eq. loss): with W* the d x (K+1) matrix whose
+ * columns are the rows of W_router (W_shr, W_1..W_K),
+ *   *loss = L_div = || W*^T W* - I_{K+1} ||_F          (device fp32, written)
+ *   dW_router += lambda * dL_div / dW_router             (device fp32 [K+1, d], updated)
+ * where dL_div / dW_router = (2 / L_div) (G - I) W_router, G = W_router
+ * W_router^T, and nothing is added when L_div = 0 or lambda = 0 (so a
+ * training step calls it after unif_moe_layer_backward with the loss
+ * weight lambda). Arithmetic in fp64 with fixed summation orders (bitwise
+ * repeatable); the outputs are rounded to fp32 once. Only K and d of cfg
+ * are read (cfg is validated as for the layer).
+ * Errors: UNIF_EINVAL (NULL W_router, loss or dW_router, non-finite
+ * lambda), UNIF_EWORKSPACE, UNIF_EDEVICE. */
+int32_t unif_moe_diversity_loss(const unif_moe_config* cfg, const float* W_router, float lambda, float* loss,
+                                float* dW_router, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Scratch memory of unif_moe_layer_forward_static on each GPU (bytes). */
 #define UNIF_MOE_STATIC_WORKSPACE_BYTES ((size_t)128 << 20)

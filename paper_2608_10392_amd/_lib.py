@@ -59,6 +59,7 @@ EXPORTS = ("unif_moe_route_workspace_size", "unif_moe_route",
            "unif_moe_block_forward", "unif_moe_layer_backward_workspace_size",
            "unif_moe_layer_backward", "unif_moe_stats_workspace_size",
            "unif_moe_stats", "unif_moe_layer_forward_static", "unif_moe_forward_work",
+           "unif_moe_diversity_loss_workspace_size", "unif_moe_diversity_loss",
            "unif_moe_status_string")
 N_PHASE_EVENTS = 7
 
@@ -108,6 +109,8 @@ def lib():
         L.unif_moe_layer_forward_static.argtypes = [cfgp, vp, vp, vp, vp, vp, vp, vp,
                                                     ctypes.POINTER(Routing), vp]
         L.unif_moe_forward_work.argtypes = [cfgp, vp, sz, ctypes.POINTER(Work), vp]
+        L.unif_moe_diversity_loss_workspace_size.argtypes = [cfgp, ctypes.POINTER(sz)]
+        L.unif_moe_diversity_loss.argtypes = [cfgp, vp, ctypes.c_float, vp, vp, vp, sz, vp]
         L.unif_moe_status_string.argtypes = [ctypes.c_int32]
         L.unif_moe_status_string.restype = ctypes.c_char_p
         for name in EXPORTS[:-1]:
@@ -298,6 +301,19 @@ def layer_backward(cfg, X, valid, W_router, prototypes, W_up, W_down, dY, dX, dW
                                          _ptr(dX), _ptr(dW_up), _ptr(dW_down), _ptr(dW_router),
                                          _ptr(workspace), ws_bytes, _stream(stream)),
            "unif_moe_layer_backward")
+
+
+def diversity_loss_workspace_size(cfg):
+    return _size("unif_moe_diversity_loss_workspace_size", cfg)
+
+
+def diversity_loss(cfg, W_router, lam, loss, dW_router, workspace, stream=None):
+    """L_div into ``loss`` (1 fp32) and dW_router += lam * dL_div/dW_router."""
+    c = make_config(cfg)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().unif_moe_diversity_loss(ctypes.byref(c), _ptr(W_router), float(lam), _ptr(loss),
+                                         _ptr(dW_router), _ptr(workspace), ws_bytes, _stream(stream)),
+           "unif_moe_diversity_loss")
 
 
 def stats(cfg, routing, valid, workspace, stream=None):

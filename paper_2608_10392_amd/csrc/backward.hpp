@@ -1,4 +1,4 @@
-// Backward pass of the layer (gradients of sum(dY * Y)), fp32 throughout.
+// Backward pass of the layer (gradients of sum(dY * Y)).
 //
 // The discrete decisions (b, I_shr, q, k) are those of the forward and are
 // held fixed; gradients flow through alpha (Eq. alpha) to W_shr and x,
@@ -6,9 +6,14 @@
 // residual-router-score) to W_1..W_K and x, and through the expert FFNs of
 // Eq. block-expert-output. The prototypes get none (they only enter TopK).
 //
-// A first implementation on the vector units (fp32 FMA, no matrix cores),
-// as tiled fp32 GEMMs over each expert's segment of pairs (rows gathered by
-// token; dense over the H channels, masked to the pair's blocks):
+// bf16 layers run on the matrix cores (the up and down engines of
+// ffn_bf16.hpp with backward epilogues, and wgrad.hpp); the kernels here
+// serve them for the per-pair and per-token scalars (bwd_weight_kernel,
+// bwd_dcoef_sum_kernel, bwd_token_kernel, the router kernels).
+//
+// fp32 layers run on the vector units (fp32 FMA) as tiled fp32 GEMMs over
+// each expert's segment of pairs (rows gathered by token; dense over the H
+// channels, masked to the pair's blocks):
 //   bwd_seg<0>    a = x K^T; act = GELU(a), gp = GELU'(a) on active channels
 //   bwd_seg<1>    E = act V^T                        (per-pair expert output)
 //   bwd_dcoef     dcoef = dy . E                     (d loss / d pair weight)
@@ -57,32 +62,12 @@ struct BwdParams {
     float* dWr;               // [K+1, d]
 };
 
+__device__ __forceinline__ float ld_f32(const void* p, size_t i) { return static_cast<const float*>(p)[i]; }
+
 template <bool BF16>
 __device__ __forceinline__ float ld_val(const void* p, size_t i) {
     if constexpr (BF16) return bf2f(static_cast<const u16*>(p)[i]);
     else return static_cast<const float*>(p)[i];
-}
-
-// 8 consecutive values from a bf16 row (one 16-byte load) or an fp32 row
-// (two), as floats; the caller guarantees alignment (8-element chunks).
-template <bool SRC_BF16>
-__device__ __forceinline__ void ld8(const void* base, size_t i, float (&v)[8]) {
-    if constexpr (SRC_BF16) {
-        const u32x4 q = ld16(static_cast<const u16*>(base) + i);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            v[2 * j] = __uint_as_float(q[j] << 16);
-            v[2 * j + 1] = __uint_as_float(q[j] & 0xffff0000u);
-        }
-    } else {
-        const f32x4 a = *reinterpret_cast<const f32x4*>(static_cast<const float*>(base) + i);
-        const f32x4 b = *reinterpret_cast<const f32x4*>(static_cast<const float*>(base) + i + 4);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            v[j] = a[j];
-            v[4 + j] = b[j];
-        }
-    }
 }
 
 // Blocks (bit c) that channels [h0, h1) touch, h0 < h1.
@@ -90,11 +75,6 @@ __device__ __forceinline__ uint64_t channel_blocks(int h0, int h1, int M) {
     const int b0 = h0 / M, b1 = (h1 - 1) / M;
     const uint64_t hi = (b1 >= 63) ? ~0ull : ((1ull << (b1 + 1)) - 1);
     return hi & ~((1ull << b0) - 1);
-}
-
-// d GELU / da = Phi(a) + a phi(a).
-__device__ __forceinline__ float gelu_grad_erf(float a) {
-    return 0.5f * (1.0f + erff(a * 0.7071067811865475244f)) + a * 0.3989422804014327f * expf(-0.5f * a * a);
 }
 
 // Weight of pair (t, e): alpha for the shared expert, else the affinity p_i
@@ -114,15 +94,32 @@ __global__ __launch_bounds__(256) void bwd_weight_kernel(BwdParams p) {
         p.pw[pr] = pair_weight(p, p.pair_token[pr], p.pair_expert[pr]);
 }
 
-// dcoef[pr] = dy_{tok(pr)} . E_pr, one wave per pair.
-template <bool BF16>
+// dcoef[pr] = dy_{tok(pr)} . E_pr from the partial sums the bf16 path's
+// second up-projection leaves per (pair, block, column half): summed over
+// the blocks of the pair's mask in increasing order (a pair with no block
+// gets 0).
+__global__ __launch_bounds__(256) void bwd_dcoef_sum_kernel(BwdParams p, const float* __restrict__ dcp) {
+    const int P = p.totals[0];
+    for (int pr = blockIdx.x * blockDim.x + threadIdx.x; pr < P; pr += gridDim.x * blockDim.x) {
+        uint64_t m = p.pair_mask[pr];
+        float s = 0.f;
+        while (m) {
+            const float* q = dcp + ((size_t)pr * p.B + __builtin_ctzll(m)) * 2;
+            s += q[0] + q[1];
+            m &= m - 1;
+        }
+        p.dcoef[pr] = s;
+    }
+}
+
+// dcoef[pr] = dy_{tok(pr)} . E_pr, one wave per pair (fp32 path).
 __global__ __launch_bounds__(256) void bwd_dcoef_kernel(BwdParams p) {
     const int pr = blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (pr >= p.totals[0]) return;
     const int t = p.pair_token[pr];
     float s = 0.f;
     for (int n = lane_id(); n < p.d; n += kWave)
-        s = fmaf(ld_val<BF16>(p.dY, (size_t)t * p.d + n), p.dxp[(size_t)pr * p.d + n], s);
+        s = fmaf(ld_f32(p.dY, (size_t)t * p.d + n), p.dxp[(size_t)pr * p.d + n], s);
     for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
     if (lane_id() == 0) p.dcoef[pr] = s;
 }
@@ -138,7 +135,7 @@ constexpr int kBT = 128, kBU = kBT / 16;
 //   MODE 1: L = act (k over H), R = V^T (col = output n)      -> E
 //   MODE 2: L = w dy (k over d), R = V (col = channel h)      -> da = dh gp
 //   MODE 3: L = da (k over H), R = K (col = output n)         -> dx_pair
-template <bool BF16, int MODE>
+template <int MODE>
 __global__ __launch_bounds__(256) void bwd_seg_kernel(BwdParams p) {
     __shared__ float Ls[16][kBT + 1];
     __shared__ float Rs[16][kBT + 1];
@@ -185,68 +182,19 @@ __global__ __launch_bounds__(256) void bwd_seg_kernel(BwdParams p) {
     float acc[kBU][kBU] = {};
     for (int k0 = 0; k0 < kdim; k0 += 16) {
         if constexpr (!KD) {
-            if (!((un >> (k0 / p.M)) & 1ull)) continue;   // a 16-channel step lies in one block
+            // skip a 16-channel step only if no pair of the tile runs any
+            // block it touches (with M % 16 != 0 a step spans two blocks)
+            if ((un & channel_blocks(k0, min(k0 + 16, kdim), p.M)) == 0) continue;
         }
-        if constexpr (BF16) {
-            // bf16 layers: d % 128 == 0 and H % 64 == 0, so every 8-chunk
-            // below is whole and 16-byte aligned. L: kBT rows x 2 chunks
-            // (pairs past the segment read zeros).
-            for (int i = threadIdx.x; i < kBT * 2; i += blockDim.x) {
-                const int r = i >> 1, kc = (i & 1) * 8, pr = r0 + r;
-                float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-                if (pr < p1) {
-                    if constexpr (MODE == 0) ld8<true>(p.X, (size_t)p.pair_token[pr] * p.d + k0 + kc, v);
-                    else if constexpr (MODE == 1) ld8<false>(p.act, (size_t)pr * p.H + k0 + kc, v);
-                    else if constexpr (MODE == 2) {
-                        ld8<true>(p.dY, (size_t)p.pair_token[pr] * p.d + k0 + kc, v);
-                        const float w = p.pw[pr];
-#pragma unroll
-                        for (int j = 0; j < 8; ++j) v[j] *= w;
-                    } else {
-                        ld8<false>(p.da, (size_t)pr * p.H + k0 + kc, v);
-                    }
-                }
-#pragma unroll
-                for (int j = 0; j < 8; ++j) Ls[kc + j][r] = v[j];
-            }
-            // R: 16 k x kBT columns, in 8-chunks along the weight's
-            // contiguous index (k for K^T and V^T, the column for V and K).
-            for (int i = threadIdx.x; i < kBT * 2; i += blockDim.x) {
-                float v[8];
-                if constexpr (MODE == 0 || MODE == 1) {
-                    const int c = i >> 1, kc = (i & 1) * 8, col = c0 + c;
-                    if (col < cols) {
-                        if constexpr (MODE == 0) ld8<true>(p.Wup, wu + (size_t)col * p.d + k0 + kc, v);
-                        else ld8<true>(p.Wdown, wd + (size_t)col * p.H + k0 + kc, v);
-                    } else {
-#pragma unroll
-                        for (int j = 0; j < 8; ++j) v[j] = 0.f;
-                    }
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) Rs[kc + j][c] = v[j];
-                } else {
-                    const int kk = i / (kBT / 8), c = (i % (kBT / 8)) * 8, col = c0 + c;
-                    if (col < cols) {
-                        if constexpr (MODE == 2) ld8<true>(p.Wdown, wd + (size_t)(k0 + kk) * p.H + col, v);
-                        else ld8<true>(p.Wup, wu + (size_t)(k0 + kk) * p.d + col, v);
-                    } else {
-#pragma unroll
-                        for (int j = 0; j < 8; ++j) v[j] = 0.f;
-                    }
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) Rs[kk][c + j] = v[j];
-                }
-            }
-        } else
         for (int i = threadIdx.x; i < 16 * kBT; i += blockDim.x) {
             // L: kBT pair rows x 16 k, consecutive threads along k.
             {
                 const int r = i / 16, kk = i % 16, pr = r0 + r, k = k0 + kk;
                 float v = 0.f;
                 if (pr < p1 && k < kdim) {
-                    if constexpr (MODE == 0) v = ld_val<BF16>(p.X, (size_t)p.pair_token[pr] * p.d + k);
+                    if constexpr (MODE == 0) v = ld_f32(p.X, (size_t)p.pair_token[pr] * p.d + k);
                     else if constexpr (MODE == 1) v = p.act[(size_t)pr * p.H + k];
-                    else if constexpr (MODE == 2) v = p.pw[pr] * ld_val<BF16>(p.dY, (size_t)p.pair_token[pr] * p.d + k);
+                    else if constexpr (MODE == 2) v = p.pw[pr] * ld_f32(p.dY, (size_t)p.pair_token[pr] * p.d + k);
                     else v = p.da[(size_t)pr * p.H + k];
                 }
                 Ls[kk][r] = v;
@@ -258,14 +206,14 @@ __global__ __launch_bounds__(256) void bwd_seg_kernel(BwdParams p) {
                 if constexpr (MODE == 0 || MODE == 1) {
                     const int c = i / 16, kk = i % 16, col = c0 + c, k = k0 + kk;
                     if (col < cols && k < kdim)
-                        v = MODE == 0 ? ld_val<BF16>(p.Wup, wu + (size_t)col * p.d + k)       // K_e[h = col][n = k]
-                                      : ld_val<BF16>(p.Wdown, wd + (size_t)col * p.H + k);    // V_e[n = col][h = k]
+                        v = MODE == 0 ? ld_f32(p.Wup, wu + (size_t)col * p.d + k)       // K_e[h = col][n = k]
+                                      : ld_f32(p.Wdown, wd + (size_t)col * p.H + k);    // V_e[n = col][h = k]
                     Rs[kk][c] = v;
                 } else {
                     const int kk = i / kBT, c = i % kBT, col = c0 + c, k = k0 + kk;
                     if (col < cols && k < kdim)
-                        v = MODE == 2 ? ld_val<BF16>(p.Wdown, wd + (size_t)k * p.H + col)     // V_e[n = k][h = col]
-                                      : ld_val<BF16>(p.Wup, wu + (size_t)k * p.d + col);      // K_e[h = k][n = col]
+                        v = MODE == 2 ? ld_f32(p.Wdown, wd + (size_t)k * p.H + col)     // V_e[n = k][h = col]
+                                      : ld_f32(p.Wup, wu + (size_t)k * p.d + col);      // K_e[h = k][n = col]
                     Rs[kk][c] = v;
                 }
             }
@@ -386,7 +334,6 @@ __global__ __launch_bounds__(256) void bwd_router_sum_kernel(BwdParams p) {
 // blockIdx.z = e, blockIdx.y picks the product (0: up, 1: down); one
 // kBT x kBT output tile per workgroup (rows: h for up, n for down), 16 pairs
 // per LDS step.
-template <bool BF16>
 __global__ __launch_bounds__(256) void bwd_wgrad_kernel(BwdParams p, int tiles_h, int tiles_d) {
     __shared__ float Ls[16][kBT + 1];   // pair x output-row operand
     __shared__ float Rs[16][kBT + 1];   // pair x output-column operand
@@ -410,33 +357,6 @@ __global__ __launch_bounds__(256) void bwd_wgrad_kernel(BwdParams p, int tiles_h
         if ((cu & tmask) == 0) continue;
         // Stage 16 pairs x kBT rows and 16 pairs x kBT columns (bf16 layers:
         // 8-chunks, whole and aligned since H % 64 == 0 and d % 128 == 0).
-        if constexpr (BF16) {
-            for (int i = threadIdx.x; i < 16 * (kBT / 8); i += blockDim.x) {
-                const int pi = i / (kBT / 8), x = (i % (kBT / 8)) * 8, pr = q0 + pi;
-                float lv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-                float rv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-                if (pr < p1) {
-                    const int t = p.pair_token[pr];
-                    if (up) {
-                        if (r0 + x < rows) ld8<false>(p.da, (size_t)pr * p.H + r0 + x, lv);
-                        if (c0 + x < cols) ld8<true>(p.X, (size_t)t * p.d + c0 + x, rv);
-                    } else {
-                        if (r0 + x < rows) {
-                            ld8<true>(p.dY, (size_t)t * p.d + r0 + x, lv);
-                            const float w = p.pw[pr];
-#pragma unroll
-                            for (int j = 0; j < 8; ++j) lv[j] *= w;
-                        }
-                        if (c0 + x < cols) ld8<false>(p.act, (size_t)pr * p.H + c0 + x, rv);
-                    }
-                }
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    Ls[pi][x + j] = lv[j];
-                    Rs[pi][x + j] = rv[j];
-                }
-            }
-        } else
         for (int i = threadIdx.x; i < 16 * kBT; i += blockDim.x) {
             const int pi = i / kBT, x = i % kBT, pr = q0 + pi;
             float lv = 0.f, rv = 0.f;
@@ -444,9 +364,9 @@ __global__ __launch_bounds__(256) void bwd_wgrad_kernel(BwdParams p, int tiles_h
                 const int t = p.pair_token[pr];
                 if (up) {
                     if (r0 + x < rows) lv = p.da[(size_t)pr * p.H + r0 + x];
-                    if (c0 + x < cols) rv = ld_val<BF16>(p.X, (size_t)t * p.d + c0 + x);
+                    if (c0 + x < cols) rv = ld_f32(p.X, (size_t)t * p.d + c0 + x);
                 } else {
-                    if (r0 + x < rows) lv = p.pw[pr] * ld_val<BF16>(p.dY, (size_t)t * p.d + r0 + x);
+                    if (r0 + x < rows) lv = p.pw[pr] * ld_f32(p.dY, (size_t)t * p.d + r0 + x);
                     if (c0 + x < cols) rv = p.act[(size_t)pr * p.H + c0 + x];
                 }
             }
@@ -480,6 +400,80 @@ __global__ __launch_bounds__(256) void bwd_wgrad_kernel(BwdParams p, int tiles_h
             if (c < cols) out[(size_t)r * cols + c] = acc[u][v];
         }
     }
+}
+
+// Gram diversity loss of the augmented router (Eq. diversity-loss):
+// L_div = || W W^T - I ||_F over the K+1 router rows W (W_shr, W_1..W_K),
+// and dW += lambda (2 / L_div) (W W^T - I) W (none when L_div = 0). fp64
+// throughout (the products of fp32 values are exact), every sum in a fixed
+// order, so the result is the same on every call.
+struct DivParams {
+    int K1, d;
+    const float* W;      // [K+1, d]
+    double* G;           // [K+1, K+1] workspace
+    double* Ls;          // [1] workspace: L_div
+    float* loss;         // [1]
+    float* dW;           // [K+1, d], updated
+    float lambda;
+};
+
+// G[i][j] = W_i . W_j, one wave per pair i <= j (lanes take n = lane + 64 t,
+// then a fixed shuffle tree).
+__global__ __launch_bounds__(256) void div_gram_kernel(DivParams p) {
+    const int w = blockIdx.x * 4 + (int)(threadIdx.x >> 6);
+    const int npair = p.K1 * (p.K1 + 1) / 2;
+    if (w >= npair) return;
+    int i = 0, rem = w;
+    while (rem >= p.K1 - i) {
+        rem -= p.K1 - i;
+        ++i;
+    }
+    const int j = i + rem;
+    const float* a = p.W + (size_t)i * p.d;
+    const float* b = p.W + (size_t)j * p.d;
+    double s = 0.0;
+    for (int n = lane_id(); n < p.d; n += kWave) s = fma((double)a[n], (double)b[n], s);
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    if (lane_id() == 0) {
+        p.G[(size_t)i * p.K1 + j] = s;
+        p.G[(size_t)j * p.K1 + i] = s;
+    }
+}
+
+// L_div from G (one workgroup of 256: strided partial sums, then a fixed
+// tree in LDS).
+__global__ __launch_bounds__(256) void div_loss_kernel(DivParams p) {
+    __shared__ double part[256];
+    const int n = p.K1 * p.K1;
+    double s = 0.0;
+    for (int x = threadIdx.x; x < n; x += 256) {
+        const double v = p.G[x] - ((x / p.K1 == x % p.K1) ? 1.0 : 0.0);
+        s = fma(v, v, s);
+    }
+    part[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) part[threadIdx.x] += part[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const double L = sqrt(part[0]);
+        *p.Ls = L;
+        *p.loss = (float)L;
+    }
+}
+
+// dW[i][n] += lambda (2 / L) sum_j (G - I)[i][j] W[j][n], one thread per (i, n).
+__global__ __launch_bounds__(256) void div_grad_kernel(DivParams p) {
+    const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (item >= (size_t)p.K1 * p.d) return;
+    const double L = *p.Ls;
+    if (L == 0.0 || p.lambda == 0.0f) return;
+    const int i = (int)(item / p.d), n = (int)(item - (size_t)i * p.d);
+    double g = 0.0;
+    for (int j = 0; j < p.K1; ++j)
+        g = fma(p.G[(size_t)i * p.K1 + j] - (i == j ? 1.0 : 0.0), (double)p.W[(size_t)j * p.d + n], g);
+    p.dW[item] = (float)((double)p.dW[item] + (double)p.lambda * (2.0 / L) * g);
 }
 
 }  // namespace unifmoe

@@ -90,6 +90,26 @@ __device__ __forceinline__ float gelu_exp2poly(float a) {
     return fmaf(fabsf(a), 0.5f - __builtin_amdgcn_exp2f(q), 0.5f * a);
 }
 
+// GELU(a) as gelu_exp2poly and its derivative Phi(a) + a phi(a) from the
+// same fitted Phi(-|a|) = 2^Q(|a|): Phi(a) = 1 - Phi(-a) for a >= 0, and
+// phi(a) = 2^(-a^2 log2(e) / 2) / sqrt(2 pi). In fp32 the derivative is
+// within 5e-6 of the exact one (the fit's error at 0, where Phi(-0) = 1/2
+// comes out 4.5e-6 high), far below the fp16 rounding it then gets.
+__device__ __forceinline__ void gelu_exp2poly_grad(float a, float& g, float& gp) {
+    const float y = __builtin_amdgcn_fmed3f(fabsf(a), 0.0f, kGeluQMax);
+    float q = fmaf(kGeluQ[7], y, kGeluQ[6]);
+    q = fmaf(q, y, kGeluQ[5]);
+    q = fmaf(q, y, kGeluQ[4]);
+    q = fmaf(q, y, kGeluQ[3]);
+    q = fmaf(q, y, kGeluQ[2]);
+    q = fmaf(q, y, kGeluQ[1]);
+    q = fmaf(q, y, kGeluQ[0]);
+    const float P = __builtin_amdgcn_exp2f(q);
+    g = fmaf(fabsf(a), 0.5f - P, 0.5f * a);
+    const float phi2 = __builtin_amdgcn_exp2f((-0.7213475204444817f * a) * a);
+    gp = fmaf(a * 0.3989422804014327f, phi2, a >= 0.0f ? 1.0f - P : P);
+}
+
 // Two fp32 -> packed bf16 pair (round to nearest even, one gfx950
 // v_cvt_pk_bf16_f32); `lo` lands in the low half.
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -108,6 +128,31 @@ __device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
     v[0] = (_Float16)lo;
     v[1] = (_Float16)hi;
     return __builtin_bit_cast(uint32_t, v);
+}
+
+// A packed fp16 pair (pack_f16x2's layout) as two fp32 values (exact).
+__device__ __forceinline__ void unpack_f16x2(uint32_t v, float& lo, float& hi) {
+    const f16x2 h = __builtin_bit_cast(f16x2, v);
+    lo = (float)h[0];
+    hi = (float)h[1];
+}
+
+// Column j of an 8 x 8 block of 16-bit values held as eight rows of 16
+// bytes (v[q] = row q): the eight values of rows 0..7 at position j, as one
+// 16-byte row (row q in half q % 2 of word q / 2).
+__device__ __forceinline__ u32x4 column8(const u32x4 (&v)[8], int j) {
+    u32x4 o;
+    const int w = j >> 1;
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+        o[m] = (j & 1) ? ((v[2 * m][w] >> 16) | (v[2 * m + 1][w] & 0xffff0000u))
+                       : ((v[2 * m][w] & 0xffffu) | (v[2 * m + 1][w] << 16));
+    return o;
+}
+
+// d GELU / da = Phi(a) + a phi(a) (library erff and expf).
+__device__ __forceinline__ float gelu_grad_erf(float a) {
+    return 0.5f * (1.0f + erff(a * 0.7071067811865475244f)) + a * 0.3989422804014327f * expf(-0.5f * a * a);
 }
 
 // Load of a wave-uniform address through the constant address space, so it

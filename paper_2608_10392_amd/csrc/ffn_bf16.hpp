@@ -63,10 +63,22 @@ constexpr int kFfnWaves = 8;
 constexpr int kFfnTM = 256;   // rows per tile (4 waves x 2 groups of 32)
 constexpr int kXcds = 8;
 
+// What the up kernel does with its fp32 tile a (rows x the block's M
+// channels) of one (expert, block) slab:
+//   kEpiGelu      H = fp16(GELU(a))                       (forward)
+//   kEpiGeluBias  H = fp16(GELU(a + b1))                   (block forward)
+//   kEpiActGrad   H = fp16(GELU(a)), G = fp16(GELU'(a))    (backward, a = x K^T)
+//   kEpiDa        with a = dy V (rows read from dY, weights V^T) and w the
+//                 pair weight: dcp = partial sums of H . a (the pair's
+//                 d loss / d w = dy . E restricted to the block), then
+//                 G = bf16(w a G) = d loss / d(x K^T) and H = bf16(w H), in
+//                 place                                  (backward)
+constexpr int kEpiGelu = 0, kEpiGeluBias = 1, kEpiActGrad = 2, kEpiDa = 3;
+
 struct UpParams {
     int d, M, B, H;
-    const u16* X;
-    const u16* Wup;
+    const u16* X;            // token rows (dY for kEpiDa)
+    const u16* Wup;          // [K+1, H, d] (V^T for kEpiDa)
     u16* Hbuf;
     u16* Hsink;              // one H row that absorbs the stores of a tile's unused rows
     const int* slab_rows;    // pair of each slab row
@@ -75,14 +87,19 @@ struct UpParams {
     const int* tile_rows;    // first entry of the tile's rows in slab_rows / slab_tok
     const int* totals;
     int* queue;              // 8 per-XCD tile counters, zero at launch
-    const float* b_up;       // [K+1, H] fp32 biases added before the GELU (BIAS kernels only)
+    const float* b_up;       // [K+1, H] fp32 biases added before the GELU (kEpiGeluBias only)
+    u16* Gbuf;               // backward: layout of Hbuf, with its own sink row Gsink
+    u16* Gsink;
+    const float* pw;         // kEpiDa: weight of each pair
+    float* dcp;              // kEpiDa: [pairs, B, 2] partial sums (block, column half)
+    float* dcp_sink;         // kEpiDa: 2 floats for a tile's unused rows
 };
 
 struct DownParams {
     int d, M, B, H, ncol;        // ncol: column tiles per row tile
-    const u16* Hbuf;
+    const u16* Hbuf;             // fp16 (F16 kernels) or bf16
     const u16* zero16;           // 16 zero bytes: the source of rows that lack a block
-    const u16* Wdown;            // fp16 values V, layout of the layer's W_down
+    const u16* Wdown;            // values V in Hbuf's format, layout of the layer's W_down
     float* part;                 // per-pair output rows, fp32
     float* part_sink;            // one d row that absorbs the stores of unused tile rows
     const int4* rt_info;         // per row tile: first pair, rows, expert
@@ -178,7 +195,7 @@ __device__ __forceinline__ void wait_stage(int s, bool after_epi, bool has_next)
 //    with stages that re-read k = 0.. and run no MFMAs (the row-list copy of
 //    stage 0 is waited for at the barrier of stage 2). PAD: whether d < 256
 //    (else no stage is padding and the MFMAs need no per-stage test).
-template <int MG, bool PAD, int TM, bool BIAS = false>
+template <int MG, bool PAD, int TM, int EPI = kEpiGelu>
 __global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void up_kernel(UpParams p) {
     using S = Stage;
@@ -189,7 +206,11 @@ void up_kernel(UpParams p) {
     constexpr int LA = TM / S::ROWS_PER_DMA / NWV;    // token-row copies per wave per stage
     constexpr int LB = M / S::ROWS_PER_DMA / NWV;     // weight-row copies per wave per stage
     constexpr int L = LA + LB;
-    constexpr int NEPI = RG * MG * 2;                 // epilogue stores per wave
+    // Epilogue stores per wave: H (two per 32-column group), and G for the
+    // backward epilogues. kEpiDa also stores its partial sums and first loads
+    // H and G, whose waits (placed by the compiler) drain the copies in
+    // flight; so NEPI is a lower bound of what follows the copies there.
+    constexpr int NEPI = RG * MG * (EPI >= kEpiActGrad ? 4 : 2);
     constexpr int A_BYTES = TM * RB, STAGE = (TM + M) * RB, RING = 2 * STAGE;
     // 4-byte copies per wave for a tile's row lists (2 TM ints): one of 64
     // ints per wave, and for TM = 384 one more of 32.
@@ -379,6 +400,67 @@ void up_kernel(UpParams p) {
         // per 32-column group.
         const int sl = info & 0xffff, nrows = info >> 16;
         const int c = sl - (sl / p.B) * p.B;
+        if constexpr (EPI >= kEpiActGrad) {
+#pragma unroll
+            for (int i = 0; i < RG; ++i) {
+                const int r = wm * (TM / 4) + i * 32 + lr;
+                const bool live = r < nrows;
+                const int pr = live ? rows[(par * 2 + 1) * TM + r] : 0;
+                const size_t off = (live ? (size_t)pr * p.H + (size_t)c * M : 0) + wn * (M / 2) + 16 * lh;
+                u16* ha = (live ? p.Hbuf : p.Hsink) + off;
+                u16* hg = (live ? p.Gbuf : p.Gsink) + off;
+                if constexpr (EPI == kEpiActGrad) {
+#pragma unroll
+                    for (int j = 0; j < MG; ++j) {
+                        const f32x16 v = acc[i][j];
+                        u32x4 alo, ahi, glo, ghi;
+#pragma unroll
+                        for (int t = 0; t < 8; ++t) {
+                            float g0, g1, d0, d1;
+                            gelu_exp2poly_grad(v[2 * t], g0, d0);
+                            gelu_exp2poly_grad(v[2 * t + 1], g1, d1);
+                            (t < 4 ? alo : ahi)[t & 3] = pack_f16x2(g0, g1);
+                            (t < 4 ? glo : ghi)[t & 3] = pack_f16x2(d0, d1);
+                        }
+                        st16(ha + 32 * j, alo);
+                        st16(ha + 32 * j + 8, ahi);
+                        st16(hg + 32 * j, glo);
+                        st16(hg + 32 * j + 8, ghi);
+                    }
+                } else {
+                    const float w = live ? p.pw[pr] : 0.f;
+                    float dc = 0.f;
+#pragma unroll
+                    for (int j = 0; j < MG; ++j) {
+                        const f32x16 v = acc[i][j];
+                        const u32x4 a4[2] = {ld16(ha + 32 * j), ld16(ha + 32 * j + 8)};
+                        const u32x4 g4[2] = {ld16(hg + 32 * j), ld16(hg + 32 * j + 8)};
+                        u32x4 wo[2], dq[2];
+#pragma unroll
+                        for (int h = 0; h < 2; ++h)
+#pragma unroll
+                            for (int t = 0; t < 4; ++t) {
+                                float a0, a1, g0, g1;
+                                unpack_f16x2(a4[h][t], a0, a1);
+                                unpack_f16x2(g4[h][t], g0, g1);
+                                const float v0 = v[8 * h + 2 * t], v1 = v[8 * h + 2 * t + 1];
+                                dc = fmaf(a0, v0, dc);
+                                dc = fmaf(a1, v1, dc);
+                                wo[h][t] = pack_bf16x2(w * a0, w * a1);
+                                dq[h][t] = pack_bf16x2(w * v0 * g0, w * v1 * g1);
+                            }
+                        st16(ha + 32 * j, wo[0]);
+                        st16(ha + 32 * j + 8, wo[1]);
+                        st16(hg + 32 * j, dq[0]);
+                        st16(hg + 32 * j + 8, dq[1]);
+                    }
+                    // lanes l and l + 32 hold the two 16-column halves of a row
+                    dc += __shfl_xor(dc, 32);
+                    float* dd = live ? p.dcp + ((size_t)pr * p.B + c) * 2 + wn : p.dcp_sink + wn;
+                    if (lh == 0) *dd = dc;
+                }
+            }
+        } else
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
             const int r = wm * (TM / 4) + i * 32 + lr;
@@ -387,7 +469,7 @@ void up_kernel(UpParams p) {
 #pragma unroll
             for (int j = 0; j < MG; ++j) {
                 f32x16 v = acc[i][j];
-                if constexpr (BIAS) {
+                if constexpr (EPI == kEpiGeluBias) {
                     // b1 of the lane's 16 columns (Eq. block-expert-output
                     // with the FFN's first bias). The compiler's wait for
                     // these loads also covers the copies in flight: an
@@ -431,7 +513,7 @@ void up_kernel(UpParams p) {
 // lacks the stage's block reads the zero page, and a 32-row MFMA group whose
 // rows all lack it skips its MFMAs. Tiles are padded to at least 4 stages
 // with empty stages (no MFMAs).
-template <int WM, int NG>
+template <int WM, int NG, bool F16 = true>
 __global__ __launch_bounds__(kFfnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void down_kernel(DownParams p) {
     using S = Stage;
@@ -642,7 +724,8 @@ void down_kernel(DownParams p) {
                     if (gset & (1u << i)) {
 #pragma unroll
                         for (int j = 0; j < NG; ++j)
-                            acc[i][j] = mfma32x32x16_f16(as_f16x8(W[j]), as_f16x8(X[i]), acc[i][j]);
+                            acc[i][j] = F16 ? mfma32x32x16_f16(as_f16x8(W[j]), as_f16x8(X[i]), acc[i][j])
+                                            : mfma32x32x16(as_bf16x8(W[j]), as_bf16x8(X[i]), acc[i][j]);
                     }
                     if (k == KS - 1) {
 #pragma unroll

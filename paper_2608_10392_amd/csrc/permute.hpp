@@ -44,6 +44,7 @@ struct PermuteParams {
     const int* bin_count;
     int* bin_cursor;
     int* slab_count;    // [nslab] rows per slab (the scan's column sums)
+    int* slab_off;      // [nslab + 1] first entry of each slab in the row lists (bf16)
     int* tile_cnt;      // [ntile][nslab + K + 1] per-tile counts; the scan turns each slab column into
                         // the tile's first row in the slab (exclusive prefix over tiles)
     const int* exp_total;   // [kExpCopies][K + 1] pairs per expert
@@ -246,6 +247,8 @@ __device__ __forceinline__ void slab_offsets(const PermuteParams& p, int* so, in
         if (blockIdx.x == 0) p.totals[1] = nup;
     }
     __syncthreads();
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i <= nslab; i += blockDim.x) p.slab_off[i] = so[i];
 }
 
 // Up tile table. Tiles are listed expert by expert; inside an expert the

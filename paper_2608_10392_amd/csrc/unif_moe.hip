@@ -37,6 +37,7 @@
 #include "permute.hpp"
 #include "route.hpp"
 #include "stats.hpp"
+#include "wgrad.hpp"
 
 using namespace unifmoe;
 
@@ -230,7 +231,7 @@ struct FwdPlan {
     size_t wsplit, logits;
     size_t zero_begin, zero_end;  // bin_count, slab_count, totals, zero page
     size_t bin_count, slab_count, exp_total, totals, queues, zero_page, work;
-    size_t bin_cursor, seg_off, down_tile_off, tile_cnt, max_row_tiles, rt_info, rt_masks;
+    size_t bin_cursor, seg_off, slab_off, down_tile_off, tile_cnt, max_row_tiles, rt_info, rt_masks;
     size_t pair_token, pair_mask, pair_expert, pair_of, pair_rank, slab_rows, slab_tok, up_tile_info, up_tile_rows, hbuf, part;
     size_t xn;      // LN(X), the FFN input of a pre-LN block
     size_t wdown16; // fp16 copy of W_down (bf16 layers)
@@ -266,6 +267,7 @@ FwdPlan plan_forward(const Dims& m, size_t xn_bytes = 0) {
     p.work = cv.take(16);   // unif_moe_forward_work's counter
     p.bin_cursor = cv.take(4 * (size_t)m.nbin * kBinCopies);
     p.seg_off = cv.take(4 * (K1 + 1));
+    p.slab_off = cv.take(4 * ((size_t)m.nslab + 1));
     p.down_tile_off = cv.take(4 * (K1 + 1));
     p.tile_cnt = cv.take(4 * ceil_div_sz(N, kTileTok) * tile_counters(m));
     p.max_row_tiles = ceil_div_sz(pmax, kDownTMMin) + K1;
@@ -503,23 +505,23 @@ int32_t record_event(void* const* events, int i, hipStream_t st) {
         if (record_event(events, (i), st) != UNIF_OK) return UNIF_EDEVICE; \
     } while (0)
 
-// Up-projection launch for the layer's block width (BIAS: b1 before GELU).
-template <bool BIAS>
+// Up-projection launch for the layer's block width, with epilogue EPI.
+template <int EPI>
 int32_t launch_up(const Dims& m, int grid, size_t lds, hipStream_t st, const UpParams& up) {
-    const bool pad = m.d / 64 < 4;   // tiles padded to 4 stages
+    const bool pad = m.d < 256;
     switch (m.M / 64) {
         case 1:
-            return pad ? launch_persistent(up_kernel<1, true, 256, BIAS>, grid, lds, st, up)
-                       : launch_persistent(up_kernel<1, false, 384, BIAS>, grid, lds, st, up);
+            return pad ? launch_persistent(up_kernel<1, true, 256, EPI>, grid, lds, st, up)
+                       : launch_persistent(up_kernel<1, false, 384, EPI>, grid, lds, st, up);
         case 2:
-            return pad ? launch_persistent(up_kernel<2, true, 256, BIAS>, grid, lds, st, up)
-                       : launch_persistent(up_kernel<2, false, 384, BIAS>, grid, lds, st, up);
+            return pad ? launch_persistent(up_kernel<2, true, 256, EPI>, grid, lds, st, up)
+                       : launch_persistent(up_kernel<2, false, 384, EPI>, grid, lds, st, up);
         case 3:
-            return pad ? launch_persistent(up_kernel<3, true, 256, BIAS>, grid, lds, st, up)
-                       : launch_persistent(up_kernel<3, false, 384, BIAS>, grid, lds, st, up);
+            return pad ? launch_persistent(up_kernel<3, true, 256, EPI>, grid, lds, st, up)
+                       : launch_persistent(up_kernel<3, false, 384, EPI>, grid, lds, st, up);
         case 4:
-            return pad ? launch_persistent(up_kernel<4, true, 256, BIAS>, grid, lds, st, up)
-                       : launch_persistent(up_kernel<4, false, 256, BIAS>, grid, lds, st, up);
+            return pad ? launch_persistent(up_kernel<4, true, 256, EPI>, grid, lds, st, up)
+                       : launch_persistent(up_kernel<4, false, 256, EPI>, grid, lds, st, up);
         default: return UNIF_EUNSUPPORTED;
     }
 }
@@ -529,7 +531,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
                      const uint8_t* valid, const float* W_router, const float* prototypes,
                      const void* W_up, const void* W_down, void* Y,
                      const unif_moe_routing* routing_out, void* workspace, size_t workspace_bytes,
-                     void* const* events, void* stream) {
+                     void* const* events, void* stream, bool tables_only = false) {
     int32_t s = check_config(cfg);
     if (s != UNIF_OK) return s;
     s = check_forward_shape(cfg);
@@ -542,7 +544,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     }
     if (routing_out != nullptr && !record_complete(routing_out)) return UNIF_EINVAL;
     if (cfg->n_tokens > 0 && (X == nullptr || W_router == nullptr || prototypes == nullptr ||
-                              W_up == nullptr || W_down == nullptr || Y == nullptr))
+                              W_up == nullptr || W_down == nullptr || (Y == nullptr && !tables_only)))
         return UNIF_EINVAL;
     const Dims m = dims_of(cfg);
     const bool own = routing_out == nullptr;
@@ -570,7 +572,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     UNIF_MARK(0);
     // 0. the fp16 copy of W_down that the down-projection multiplies with
     const u16* wdown16 = nullptr;
-    if (m.bf16) {
+    if (m.bf16 && !tables_only) {
         const size_t n8 = (size_t)m.K1 * m.d * m.H / 8;
         u16* dst = reinterpret_cast<u16*>(ws + plan.wdown16);
         const unsigned g = (unsigned)std::min<size_t>((n8 + 255) / 256, (size_t)cu_count() * 8);
@@ -628,6 +630,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     pp.bin_count = bin_count;
     pp.bin_cursor = reinterpret_cast<int*>(ws + plan.bin_cursor);
     pp.slab_count = slab_count;
+    pp.slab_off = reinterpret_cast<int*>(ws + plan.slab_off);
     pp.seg_off = reinterpret_cast<int*>(ws + plan.seg_off);
     pp.down_tile_off = reinterpret_cast<int*>(ws + plan.down_tile_off);
     pp.totals = totals;
@@ -668,6 +671,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
                              st>>>(pp);
         UNIF_LAUNCH_CHECK();
         UNIF_MARK(3);
+        if (tables_only) return UNIF_OK;
         // 4. block-sparse expert GEMMs
         UpParams up;
         up.d = m.d;
@@ -687,7 +691,8 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         up.b_up = blk != nullptr ? blk->b_up : nullptr;
         const size_t up_lds = (size_t)up_lds_bytes(m.M, up_tm(m.M, m.d));
         const int grid = (cus / kXcds) * kXcds;
-        s = up.b_up != nullptr ? launch_up<true>(m, grid, up_lds, st, up) : launch_up<false>(m, grid, up_lds, st, up);
+        s = up.b_up != nullptr ? launch_up<kEpiGeluBias>(m, grid, up_lds, st, up)
+                                : launch_up<kEpiGelu>(m, grid, up_lds, st, up);
         if (s != UNIF_OK) return s;
         UNIF_MARK(4);
         DownParams dn;
@@ -716,6 +721,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         UNIF_MARK(5);
     } else {
         UNIF_MARK(3);
+        if (tables_only) return UNIF_OK;
         PairF32Params fp;
         fp.d = m.d;
         fp.M = m.M;
@@ -855,10 +861,14 @@ int32_t unif_moe_layer_forward_profiled(const unif_moe_config* cfg, const void* 
 
 namespace {
 
-// Backward workspace: the forward's (record and pair tables kept), then the
-// forward output and the per-pair intermediates.
+// Backward workspace: the forward's (routing record, pair tables, slab
+// lists; for bf16 layers its H buffer holds GELU(a), then w GELU(a), and its
+// fp16 W_down region the transposed W_up; its per-pair rows receive dx_pair),
+// then for bf16 layers a second H-shaped buffer (GELU'(a), then d loss / da),
+// V^T and the per-(pair, block) partial sums of dy . E, for fp32 layers the
+// per-pair fp32 intermediates, and the per-pair and per-token scalars.
 struct BwdPlan {
-    size_t fwd, y, act, da, dcoef, pw, dxp, dz, rpart, total;
+    size_t fwd, act, da, gbuf, wdnT, dcp, dcoef, pw, dz, rpart, queues, total;
 };
 
 BwdPlan plan_backward(const Dims& m) {
@@ -867,14 +877,16 @@ BwdPlan plan_backward(const Dims& m) {
     const size_t pmax = (size_t)m.N * m.K1;
     Carver cv;
     cv.cur = b.fwd;
-    b.y = cv.take((size_t)m.N * m.d * m.elem);
-    b.act = cv.take(pmax * m.H * sizeof(float));
-    b.da = cv.take(pmax * m.H * sizeof(float));
+    b.act = cv.take(m.bf16 ? 0 : pmax * m.H * sizeof(float));
+    b.da = cv.take(m.bf16 ? 0 : pmax * m.H * sizeof(float));
+    b.gbuf = cv.take(m.bf16 ? (pmax + 1) * (size_t)m.H * 2 : 0);   // + the sink row
+    b.wdnT = cv.take(m.bf16 ? (size_t)m.K1 * m.d * m.H * 2 : 0);
+    b.dcp = cv.take(m.bf16 ? (pmax * m.B + 1) * 2 * sizeof(float) : 0);
     b.dcoef = cv.take(pmax * sizeof(float));
     b.pw = cv.take(pmax * sizeof(float));
-    b.dxp = cv.take(pmax * m.d * sizeof(float));
     b.dz = cv.take((size_t)m.N * m.K1 * sizeof(float));
     b.rpart = cv.take((size_t)kRouterChunks * m.K1 * m.d * sizeof(float));
+    b.queues = cv.take(4 * 32);
     b.total = cv.cur + 256;
     return b;
 }
@@ -884,9 +896,37 @@ int32_t check_backward_shape(const unif_moe_config* c) {
     if (s != UNIF_OK) return s;
     s = check_forward_shape(c);
     if (s != UNIF_OK) return s;
-    // Pair tiles of an expert segment index grid dimension y.
-    if (ceil_div(c->n_tokens, kBT) > 65535) return UNIF_EUNSUPPORTED;
+    // fp32 layers: pair tiles of an expert segment index grid dimension y.
+    if (c->dtype == UNIF_F32 && ceil_div(c->n_tokens, kBT) > 65535) return UNIF_EUNSUPPORTED;
     return UNIF_OK;
+}
+
+// The weight-gradient launch for block width M and n tiles of TN columns.
+template <bool UP, int GQ, int GP, int WQ>
+int32_t launch_wgrad1(const WgradParams& w, int nslab, hipStream_t st) {
+    constexpr int TQ = WQ * GQ * 32, TP = (8 / WQ) * GP * 32;
+    const size_t lds = (size_t)wgrad_lds_bytes(TQ, TP);
+    if (allow_lds(wgrad_kernel<UP, GQ, GP, WQ>, lds) != UNIF_OK) return UNIF_EDEVICE;
+    wgrad_kernel<UP, GQ, GP, WQ><<<(unsigned)(nslab * w.ntn), 512, lds, st>>>(w);
+    return hipGetLastError() == hipSuccess ? UNIF_OK : UNIF_EDEVICE;
+}
+
+template <bool UP, int GN>
+int32_t launch_wgrad_m(const WgradParams& w, int nslab, hipStream_t st) {
+    // dW_up: Q = h (2 waves x M / 64 groups), P = n (4 waves x GN groups);
+    // dW_down: Q = n (4 waves x GN groups), P = h (2 waves x M / 64 groups).
+    switch (w.M / 64) {
+        case 1: return UP ? launch_wgrad1<true, 1, GN, 2>(w, nslab, st) : launch_wgrad1<false, GN, 1, 4>(w, nslab, st);
+        case 2: return UP ? launch_wgrad1<true, 2, GN, 2>(w, nslab, st) : launch_wgrad1<false, GN, 2, 4>(w, nslab, st);
+        case 3: return UP ? launch_wgrad1<true, 3, GN, 2>(w, nslab, st) : launch_wgrad1<false, GN, 3, 4>(w, nslab, st);
+        case 4: return UP ? launch_wgrad1<true, 4, GN, 2>(w, nslab, st) : launch_wgrad1<false, GN, 4, 4>(w, nslab, st);
+        default: return UNIF_EUNSUPPORTED;
+    }
+}
+
+template <bool UP>
+int32_t launch_wgrad(const WgradParams& w, int nslab, hipStream_t st) {
+    return w.ntn * 256 == w.d ? launch_wgrad_m<UP, 2>(w, nslab, st) : launch_wgrad_m<UP, 1>(w, nslab, st);
 }
 
 }  // namespace
@@ -935,15 +975,12 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
     p.dWup = dW_up;
     p.dWdown = dW_down;
     p.dWr = dW_router;
-    const int tiles_h = ceil_div(m.H, kBT), tiles_d = ceil_div(m.d, kBT);
-    const dim3 wg_grid((unsigned)(tiles_h * tiles_d), 2, (unsigned)m.K1);
-    // 1. the forward (routing record, pair tables) into the front of the workspace
+    // 1. routing and the permutation's tables into the front of the workspace
     char* ws = align_base(workspace);
     const FwdPlan fp = plan_forward(m);
-    void* Yscratch = ws + bp.y;
     if (m.N > 0) {
-        s = forward_impl(cfg, nullptr, X, valid, W_router, prototypes, W_up, W_down, Yscratch, nullptr, ws,
-                         bp.fwd, nullptr, stream);
+        s = forward_impl(cfg, nullptr, X, valid, W_router, prototypes, W_up, W_down, nullptr, nullptr, ws,
+                         bp.fwd, nullptr, stream, true);
         if (s != UNIF_OK) return s;
     }
     p.alpha = reinterpret_cast<const float*>(ws + fp.alpha);
@@ -961,7 +998,7 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
     p.dcoef = reinterpret_cast<float*>(ws + bp.dcoef);
     p.pw = reinterpret_cast<float*>(ws + bp.pw);
     p.rpart = reinterpret_cast<float*>(ws + bp.rpart);
-    p.dxp = reinterpret_cast<float*>(ws + bp.dxp);
+    p.dxp = reinterpret_cast<float*>(ws + fp.part);
     p.dz = reinterpret_cast<float*>(ws + bp.dz);
     if (m.N == 0) {
         // No tokens: the forward built no tables; the weight gradients are zero.
@@ -974,39 +1011,174 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
         }
         return UNIF_OK;
     }
-    // 2. per pair (segment GEMMs), 3. per token, 4. router and expert weight gradients
-    const unsigned ptiles = (unsigned)ceil_div(m.N, kBT);
-    const dim3 g_ch((unsigned)tiles_h, ptiles, (unsigned)m.K1), g_out((unsigned)tiles_d, ptiles, (unsigned)m.K1);
-    const unsigned gp = (unsigned)ceil_div(m.N * m.K1, 4);
     bwd_weight_kernel<<<(unsigned)cus * 4, 256, 0, st>>>(p);
     UNIF_LAUNCH_CHECK();
+    const size_t pmax = (size_t)m.N * m.K1;
+    u16* const abuf = reinterpret_cast<u16*>(ws + fp.hbuf);
+    u16* const gbuf = reinterpret_cast<u16*>(ws + bp.gbuf);
     if (m.bf16) {
-        bwd_seg_kernel<true, 0><<<g_ch, 256, 0, st>>>(p);
-        bwd_seg_kernel<true, 1><<<g_out, 256, 0, st>>>(p);
-        bwd_dcoef_kernel<true><<<gp, 256, 0, st>>>(p);
-        bwd_seg_kernel<true, 2><<<g_ch, 256, 0, st>>>(p);
-        bwd_seg_kernel<true, 3><<<g_out, 256, 0, st>>>(p);
+        // 2. V^T [K+1, H, d] (rows of dy V as the up kernel's weights) and
+        //    K^T [K+1, d, H] (dx_pair = da K as the down kernel's weights)
+        int* queues = reinterpret_cast<int*>(ws + bp.queues);
+        fill_zero_kernel<<<1, 64, 0, st>>>(reinterpret_cast<uint32_t*>(queues), 32);
+        UNIF_LAUNCH_CHECK();
+        u16* const wdnT = reinterpret_cast<u16*>(ws + bp.wdnT);
+        u16* const wupT = reinterpret_cast<u16*>(ws + fp.wdown16);
+        const int nt = m.K1 * (m.d / 64) * (m.H / 64);
+        transpose16_kernel<<<(unsigned)ceil_div(nt, 4), 256, 0, st>>>(static_cast<const u16*>(W_down), wdnT, m.d,
+                                                                       m.H, nt);
+        transpose16_kernel<<<(unsigned)ceil_div(nt, 4), 256, 0, st>>>(static_cast<const u16*>(W_up), wupT, m.H,
+                                                                       m.d, nt);
+        UNIF_LAUNCH_CHECK();
+        // 3. a = x K^T over the slabs: GELU(a) and GELU'(a); then dy V: the
+        //    dy . E partials, da and w GELU(a)
+        UpParams up;
+        up.d = m.d;
+        up.M = m.M;
+        up.B = m.B;
+        up.H = m.H;
+        up.X = static_cast<const u16*>(X);
+        up.Wup = static_cast<const u16*>(W_up);
+        up.Hbuf = abuf;
+        up.Hsink = abuf + pmax * m.H;
+        up.slab_rows = reinterpret_cast<const int*>(ws + fp.slab_rows);
+        up.slab_tok = reinterpret_cast<const int*>(ws + fp.slab_tok);
+        up.tile_info = reinterpret_cast<const int*>(ws + fp.up_tile_info);
+        up.tile_rows = reinterpret_cast<const int*>(ws + fp.up_tile_rows);
+        up.totals = p.totals;
+        up.queue = queues;
+        up.b_up = nullptr;
+        up.Gbuf = gbuf;
+        up.Gsink = gbuf + pmax * m.H;
+        up.pw = p.pw;
+        float* const dcp = reinterpret_cast<float*>(ws + bp.dcp);
+        up.dcp = dcp;
+        up.dcp_sink = dcp + pmax * m.B * 2;
+        const size_t up_lds = (size_t)up_lds_bytes(m.M, up_tm(m.M, m.d));
+        const int grid = (cus / kXcds) * kXcds;
+        s = launch_up<kEpiActGrad>(m, grid, up_lds, st, up);
+        if (s != UNIF_OK) return s;
+        up.X = static_cast<const u16*>(dY);
+        up.Wup = wdnT;
+        up.queue = queues + 8;
+        s = launch_up<kEpiDa>(m, grid, up_lds, st, up);
+        if (s != UNIF_OK) return s;
+        bwd_dcoef_sum_kernel<<<(unsigned)cus * 4, 256, 0, st>>>(p, dcp);
+        UNIF_LAUNCH_CHECK();
+        // 4. dx_pair = da K over each pair's blocks
+        const DownShape dsh = down_shape(m.d);
+        DownParams dn;
+        dn.d = m.d;
+        dn.M = m.M;
+        dn.B = m.B;
+        dn.H = m.H;
+        dn.ncol = m.d / dsh.bn;
+        dn.Hbuf = gbuf;
+        dn.zero16 = reinterpret_cast<const u16*>(ws + fp.zero_page);
+        dn.Wdown = wupT;
+        dn.part = p.dxp;
+        dn.part_sink = p.dxp + pmax * m.d;
+        dn.rt_info = reinterpret_cast<const int4*>(ws + fp.rt_info);
+        dn.rt_masks = reinterpret_cast<const uint64_t*>(ws + fp.rt_masks);
+        dn.pair_mask = p.pair_mask;
+        dn.totals = p.totals;
+        dn.queue = queues + 16;
+        if (dsh.bn == 384)
+            s = launch_persistent(down_kernel<2, 3, false>, grid, (size_t)down_lds_bytes(128, 384), st, dn);
+        else if (dsh.bn == 256)
+            s = launch_persistent(down_kernel<4, 4, false>, grid, (size_t)down_lds_bytes(256, 256), st, dn);
+        else
+            s = launch_persistent(down_kernel<4, 2, false>, grid, (size_t)down_lds_bytes(256, 128), st, dn);
+        if (s != UNIF_OK) return s;
     } else {
-        bwd_seg_kernel<false, 0><<<g_ch, 256, 0, st>>>(p);
-        bwd_seg_kernel<false, 1><<<g_out, 256, 0, st>>>(p);
-        bwd_dcoef_kernel<false><<<gp, 256, 0, st>>>(p);
-        bwd_seg_kernel<false, 2><<<g_ch, 256, 0, st>>>(p);
-        bwd_seg_kernel<false, 3><<<g_out, 256, 0, st>>>(p);
+        // 2. per pair: tiled fp32 GEMMs over each expert's segment
+        const int tiles_h = ceil_div(m.H, kBT), tiles_d = ceil_div(m.d, kBT);
+        const unsigned ptiles = (unsigned)ceil_div(m.N, kBT);
+        const dim3 g_ch((unsigned)tiles_h, ptiles, (unsigned)m.K1), g_out((unsigned)tiles_d, ptiles, (unsigned)m.K1);
+        const unsigned gp = (unsigned)ceil_div(m.N * m.K1, 4);
+        bwd_seg_kernel<0><<<g_ch, 256, 0, st>>>(p);
+        bwd_seg_kernel<1><<<g_out, 256, 0, st>>>(p);
+        bwd_dcoef_kernel<<<gp, 256, 0, st>>>(p);
+        bwd_seg_kernel<2><<<g_ch, 256, 0, st>>>(p);
+        bwd_seg_kernel<3><<<g_out, 256, 0, st>>>(p);
+        UNIF_LAUNCH_CHECK();
     }
-    UNIF_LAUNCH_CHECK();
+    // 5. per token: dX and the router-logit gradients; the router's weight gradient
     bwd_token_kernel<<<(unsigned)ceil_div(m.N, 4), 256, 0, st>>>(p);
     UNIF_LAUNCH_CHECK();
     const unsigned rg = (unsigned)ceil_div(m.K1 * m.d, 256);
     const dim3 rgrid(rg, kRouterChunks);
-    if (m.bf16) {
-        bwd_router_kernel<true><<<rgrid, 256, 0, st>>>(p);
-        bwd_wgrad_kernel<true><<<wg_grid, 256, 0, st>>>(p, tiles_h, tiles_d);
-    } else {
-        bwd_router_kernel<false><<<rgrid, 256, 0, st>>>(p);
-        bwd_wgrad_kernel<false><<<wg_grid, 256, 0, st>>>(p, tiles_h, tiles_d);
-    }
+    if (m.bf16) bwd_router_kernel<true><<<rgrid, 256, 0, st>>>(p);
+    else bwd_router_kernel<false><<<rgrid, 256, 0, st>>>(p);
     UNIF_LAUNCH_CHECK();
     bwd_router_sum_kernel<<<rg, 256, 0, st>>>(p);
+    UNIF_LAUNCH_CHECK();
+    // 6. expert weight gradients
+    if (m.bf16) {
+        WgradParams w;
+        w.d = m.d;
+        w.M = m.M;
+        w.B = m.B;
+        w.H = m.H;
+        w.ntn = (m.d % 256 == 0) ? m.d / 256 : m.d / 128;
+        w.slab_rows = reinterpret_cast<const int*>(ws + fp.slab_rows);
+        w.slab_tok = reinterpret_cast<const int*>(ws + fp.slab_tok);
+        w.slab_off = reinterpret_cast<const int*>(ws + fp.slab_off);
+        w.slab_count = reinterpret_cast<const int*>(ws + fp.slab_count);
+        w.Psrc = static_cast<const u16*>(X);
+        w.Qsrc = gbuf;
+        w.out = dW_up;
+        s = launch_wgrad<true>(w, m.nslab, st);
+        if (s != UNIF_OK) return s;
+        w.Psrc = abuf;
+        w.Qsrc = static_cast<const u16*>(dY);
+        w.out = dW_down;
+        s = launch_wgrad<false>(w, m.nslab, st);
+        if (s != UNIF_OK) return s;
+    } else {
+        const int tiles_h = ceil_div(m.H, kBT), tiles_d = ceil_div(m.d, kBT);
+        const dim3 wg_grid((unsigned)(tiles_h * tiles_d), 2, (unsigned)m.K1);
+        bwd_wgrad_kernel<<<wg_grid, 256, 0, st>>>(p, tiles_h, tiles_d);
+        UNIF_LAUNCH_CHECK();
+    }
+    return UNIF_OK;
+}
+
+int32_t unif_moe_diversity_loss_workspace_size(const unif_moe_config* cfg, size_t* bytes) {
+    if (bytes == nullptr) return UNIF_EINVAL;
+    const int32_t s = check_config(cfg);
+    if (s != UNIF_OK) return s;
+    const size_t k1 = (size_t)cfg->n_experts + 1;
+    *bytes = 8 * (k1 * k1 + 1) + 256;
+    return UNIF_OK;
+}
+
+int32_t unif_moe_diversity_loss(const unif_moe_config* cfg, const float* W_router, float lambda, float* loss,
+                                float* dW_router, void* workspace, size_t workspace_bytes, void* stream) {
+    const int32_t s = check_config(cfg);
+    if (s != UNIF_OK) return s;
+    if (W_router == nullptr || loss == nullptr || dW_router == nullptr || !std::isfinite(lambda))
+        return UNIF_EINVAL;
+    size_t need = 0;
+    unif_moe_diversity_loss_workspace_size(cfg, &need);
+    if (workspace == nullptr || workspace_bytes < need) return UNIF_EWORKSPACE;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    DivParams dp;
+    dp.K1 = cfg->n_experts + 1;
+    dp.d = cfg->d_model;
+    dp.W = W_router;
+    char* ws = align_base(workspace);
+    dp.G = reinterpret_cast<double*>(ws);
+    dp.Ls = dp.G + (size_t)dp.K1 * dp.K1;
+    dp.loss = loss;
+    dp.dW = dW_router;
+    dp.lambda = lambda;
+    const int npair = dp.K1 * (dp.K1 + 1) / 2;
+    div_gram_kernel<<<(unsigned)ceil_div(npair, 4), 256, 0, st>>>(dp);
+    UNIF_LAUNCH_CHECK();
+    div_loss_kernel<<<1, 256, 0, st>>>(dp);
+    UNIF_LAUNCH_CHECK();
+    div_grad_kernel<<<(unsigned)ceil_div(dp.K1 * dp.d, 256), 256, 0, st>>>(dp);
     UNIF_LAUNCH_CHECK();
     return UNIF_OK;
 }

@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 14, names
+    assert len(names) == 16, names
     assert set(names) == set(_lib.EXPORTS)
     out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True, text=True).stdout
     for n in names:
@@ -208,19 +208,28 @@ def test_block_calls_fail_before_touching_the_device(L):
 def test_backward_workspace_and_validation(L):
     c = base_cfg(n_tokens=1000)
     N, d, K, H = 1000, 768, 16, 3072
+    B = 16
     ws = _lib.layer_backward_workspace_size(c)
-    assert ws >= _lib.layer_forward_workspace_size(c) + 4 * (2 * H + d + 1) * N * (K + 1)
+    # bf16: a second H buffer (bf16), the transposed W_down, the per-block partial sums
+    assert ws >= (_lib.layer_forward_workspace_size(c) + 2 * (N * (K + 1) + 1) * H + 2 * (K + 1) * d * H
+                  + 8 * B * N * (K + 1))
+    # fp32: the per-pair fp32 intermediates
+    cf = base_cfg(n_tokens=1000, dtype="f32")
+    assert (_lib.layer_backward_workspace_size(cf)
+            >= _lib.layer_forward_workspace_size(cf) + 4 * 2 * H * N * (K + 1))
     cc = _lib.make_config(c)
     big = 1 << 45
     # NULL dY, NULL gradient outputs, small workspace: rejected before any HIP call
     assert L.unif_moe_layer_backward(ctypes.byref(cc), 1, None, 1, 1, 1, 1, None, 1, 1, 1, 1, 1, big, None) == _lib.EINVAL
     assert L.unif_moe_layer_backward(ctypes.byref(cc), 1, None, 1, 1, 1, 1, 1, 1, None, 1, 1, 1, big, None) == _lib.EINVAL
     assert L.unif_moe_layer_backward(ctypes.byref(cc), 1, None, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 16, None) == _lib.EWORKSPACE
-    # pair tiles of an expert segment index grid dimension y (at most 65535 tiles of 128)
-    assert _lib.layer_backward_workspace_size(base_cfg(n_tokens=128 * 65535)) > 0
+    # fp32 layers: pair tiles of an expert segment index grid dimension y
+    # (at most 65535 tiles of 128); bf16 layers have no such limit
+    assert _lib.layer_backward_workspace_size(base_cfg(n_tokens=128 * 65535, dtype="f32")) > 0
     with pytest.raises(_lib.UnifMoeError) as e:
-        _lib.layer_backward_workspace_size(base_cfg(n_tokens=128 * 65535 + 1))
+        _lib.layer_backward_workspace_size(base_cfg(n_tokens=128 * 65535 + 1, dtype="f32"))
     assert e.value.status == _lib.EUNSUPPORTED
+    assert _lib.layer_backward_workspace_size(base_cfg(n_tokens=128 * 65535 + 1)) > 0
 
 
 def test_static_forward_rejects_layers_beyond_its_scratch(L):
@@ -230,3 +239,31 @@ def test_static_forward_rejects_layers_beyond_its_scratch(L):
     assert _lib.layer_forward_workspace_size(c) > _lib.STATIC_WORKSPACE_BYTES
     assert L.unif_moe_layer_forward_static(ctypes.byref(c), 1, None, 1, 1, 1, 1, 1, None, None) == _lib.EWORKSPACE
     assert L.unif_moe_layer_forward_static(None, 1, None, 1, 1, 1, 1, 1, None, None) == _lib.EINVAL
+
+
+def test_diversity_loss_rejects_bad_arguments(L):
+    """unif_moe_diversity_loss validates before any device call: the
+    pointers below are never dereferenced."""
+    cfg = layer_config(get_config("vit_b16"))
+    c = _lib.make_config(cfg)
+    n = ctypes.c_size_t(0)
+    assert L.unif_moe_diversity_loss_workspace_size(ctypes.byref(c), ctypes.byref(n)) == 0
+    K1 = cfg["n_experts"] + 1
+    assert n.value >= 8 * (K1 * K1 + 1)
+    assert L.unif_moe_diversity_loss_workspace_size(ctypes.byref(c), None) == _lib.EINVAL
+    p = ctypes.c_void_p(4096)
+    args = dict(W=p, lam=1.0, loss=p, dW=p, ws=p, nbytes=n.value)
+
+    def call(**over):
+        a = dict(args, **over)
+        return L.unif_moe_diversity_loss(ctypes.byref(c), a["W"], a["lam"], a["loss"], a["dW"], a["ws"],
+                                          a["nbytes"], None)
+    assert call(W=None) == _lib.EINVAL
+    assert call(loss=None) == _lib.EINVAL
+    assert call(dW=None) == _lib.EINVAL
+    assert call(lam=float("nan")) == _lib.EINVAL
+    assert call(lam=float("inf")) == _lib.EINVAL
+    assert call(ws=None) == _lib.EWORKSPACE
+    assert call(nbytes=n.value - 1) == _lib.EWORKSPACE
+    bad = _lib.make_config(dict(cfg, n_experts=0))
+    assert L.unif_moe_diversity_loss(ctypes.byref(bad), p, 1.0, p, p, p, n.value, None) == _lib.EINVAL

@@ -1,12 +1,19 @@
-"""Parity of the backward pass (unif_moe_layer_backward) with the CPU
-oracle's backward (MI355X only).
+"""Parity of the backward pass (unif_moe_layer_backward) and of the Gram
+diversity loss (unif_moe_diversity_loss) with the CPU oracle (MI355X only).
 
-The gradients of sum(dY * Y) are compared tensor by tensor: max |g_gpu -
-g_ref| <= 1e-4 x max |g_ref| (the library computes in fp32 from inputs that
-are exact in fp32; the oracle in fp64). The decisions are held fixed, so
-tokens whose routing margin is below 1e-4 (where the two sides may take
-different decisions) are marked padded in the input; padded tokens must get
-dX = 0.
+The gradients of sum(dY * Y) are compared tensor by tensor as max |g_gpu -
+g_ref| / max |g_ref|:
+  * fp32 layers: <= 1e-4 (fp32 arithmetic on inputs exact in fp32; the
+    oracle in fp64);
+  * bf16 layers: <= 1e-2. The matrix-core path rounds d loss / da and
+    w GELU(a) to bf16 (relative step 2^-8, so at most 2^-9 = 1.95e-3 per
+    value) before the products that give dx, dW_up and dW_down, and GELU(a),
+    GELU'(a) to fp16; each gradient element is a sum of such rounded terms,
+    whose error is at most 2^-9 of the sum of their magnitudes. The bound
+    allows that sum to reach five times the largest gradient element.
+The decisions are held fixed, so tokens whose routing margin is below 1e-4
+(where the two sides may take different decisions) are marked padded in the
+input; padded tokens must get dX = 0.
 """
 import numpy as np
 import pytest
@@ -19,7 +26,7 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-TOL = 1e-4
+TOL = {"f32": 1e-4, "bf16": 1e-2}
 
 
 def run_backward(g, label):
@@ -43,7 +50,7 @@ def run_backward(g, label):
         scale = float(np.abs(ref[k]).max())
         err = float(np.abs(got[k] - ref[k]).max()) / scale
         errs[k] = err
-        assert err <= TOL, f"{k}: error {err:.2e} x max |ref| ({scale:.3e})"
+        assert err <= TOL[cfg["dtype"]], f"{k}: error {err:.2e} x max |ref| ({scale:.3e})"
     assert np.all(got["dX"][valid == 0] == 0)
     print(f"[gpu] backward {label}: " + ", ".join(f"{k} {v:.1e}" for k, v in errs.items())
           + " x max |ref|", flush=True)
@@ -64,6 +71,10 @@ CASES = {
                                              block_width=64, max_shared=8)),
     "f32": ("tiny_f32", dict(n_tokens=200, d_model=64, n_experts=4, n_blocks=4, block_width=32,
                              max_shared=4)),
+    # a block width that is not a multiple of the fp32 kernels' 16-channel
+    # steps: a step then spans two blocks
+    "f32_m24": ("tiny_f32", dict(n_tokens=200, d_model=64, n_experts=4, n_blocks=4, block_width=24,
+                                 max_shared=4)),
     # edge shapes: one token; two blocks of the widest kernel; 64 experts x 64 blocks
     "n1": ("vit_s16", dict(n_tokens=1, d_model=128, n_experts=4, n_blocks=4, block_width=64,
                            max_shared=4)),
@@ -83,13 +94,12 @@ def test_backward(name):
 @pytest.mark.parametrize("name", ["vit_b16", "bert_base_padded"])
 def test_backward_full_size_properties(name):
     """At the full workload sizes, where the oracle's gradient sums are out of
-    reach: every gradient is linear in dY and scaling by 2 is exact in fp32,
-    so backward(2 dY) equals 2 backward(dY) bit for bit for dX and dW_router
-    (sums in token order). The expert weight gradients sum over an expert's
-    pairs in the order of the forward's permutation, which within equal
-    block-mask keys follows the arrival order of the routing kernel's
-    atomics, so they agree to fp32 rounding (1e-5 of their scale). Padded
-    tokens get dX = 0; all gradients are finite."""
+    reach: every gradient is linear in dY, and scaling dY by 2 scales every
+    intermediate the backward rounds (to bf16 or fp16, away from the
+    formats' range limits) by exactly 2, so backward(2 dY) equals
+    2 backward(dY) bit for bit, for all four gradients, since every sum runs
+    in a fixed order. A repeated call gives the same bits. Padded tokens get
+    dX = 0; all gradients are finite."""
     g = generate(name)
     cfg = g["cfg"]
     print(f"\n[gpu] backward properties {name}: N={cfg['n_tokens']}", flush=True)
@@ -101,18 +111,16 @@ def test_backward_full_size_properties(name):
     dY2 = O._as_f32(dY, cfg["dtype"]) * np.float32(2.0)
     dY2 = (dY2.view(np.uint32) >> 16).astype(np.uint16) if cfg["dtype"] == "bf16" else dY2
     g2 = dev.backward(dY2)
+    g3 = dev.backward(dY)
     for k in g1:
         a, b = g1[k], g2[k]
         assert bool(torch.isfinite(a).all()), k
-        if k in ("dX", "dW_router"):
-            assert torch.equal(b, 2.0 * a), f"{k}: backward(2 dY) != 2 backward(dY)"
-        else:
-            err = float((b - 2.0 * a).abs().max() / (2.0 * a).abs().max())
-            assert err <= 1e-5, f"{k}: backward(2 dY) - 2 backward(dY) = {err:.2e} of its scale"
+        assert torch.equal(g3[k], a), f"{k}: a repeated backward differs"
+        assert torch.equal(b, 2.0 * a), f"{k}: backward(2 dY) != 2 backward(dY)"
     if g["valid"] is not None:
         pad = torch.from_numpy(g["valid"] == 0).to(g1["dX"].device)
         assert bool((g1["dX"][pad] == 0).all())
-    del dev, g1, g2
+    del dev, g1, g2, g3
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
 
@@ -127,3 +135,37 @@ def test_backward_all_padded():
     grads = dev.backward(upstream_grad(g))
     for k, v in grads.items():
         assert bool((v == 0).all()), k
+
+
+@pytest.mark.parametrize("shape", [(17, 768), (65, 128), (2, 40), (7, 384)])
+def test_diversity_loss(shape):
+    """L_div (Eq. diversity-loss) and lambda times its gradient added to
+    dW_router, against oracle.diversity_loss (fp64): the loss to 1e-6
+    relative, the update to 1e-6 of its largest element; a zero lambda
+    leaves dW_router untouched, and a repeated call gives the same bits."""
+    from paper_2608_10392_amd import _lib
+    K1, d = shape
+    cfg = layer_config(get_config("tiny_f32", n_experts=K1 - 1, d_model=d, fixed_k=1))
+    rng = np.random.default_rng(K1 * 1000 + d)
+    W = (rng.standard_normal((K1, d)) / np.sqrt(d)).astype(np.float32)
+    print(f"\n[gpu] diversity loss K+1={K1} d={d}", flush=True)
+    L_ref, g_ref = O.diversity_loss(W)
+    dev = torch.device("cuda:0")
+    Wd = torch.from_numpy(W).to(dev)
+    loss = torch.zeros(1, dtype=torch.float32, device=dev)
+    base = torch.from_numpy(rng.standard_normal((K1, d)).astype(np.float32)).to(dev)
+    ws = _lib.alloc_workspace(_lib.diversity_loss_workspace_size(cfg), dev)
+    lam = 0.25
+    dW = base.clone()
+    _lib.diversity_loss(cfg, Wd, lam, loss, dW, ws)
+    torch.cuda.synchronize()
+    assert abs(float(loss.item()) - L_ref) <= 1e-6 * L_ref
+    upd = (dW.double() - base.double()).cpu().numpy()
+    scale = float(np.abs(lam * g_ref).max())
+    assert np.abs(upd - lam * g_ref).max() <= 1e-6 * scale + 2.0 ** -23 * float(base.abs().max())
+    dW2 = base.clone()
+    _lib.diversity_loss(cfg, Wd, lam, loss, dW2, ws)
+    dW0 = base.clone()
+    _lib.diversity_loss(cfg, Wd, 0.0, loss, dW0, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(dW2, dW) and torch.equal(dW0, base)

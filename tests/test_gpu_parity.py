@@ -264,7 +264,7 @@ def test_forward_work_counts(routing_passed):
     assert w["pairs"] == pairs
     per_tile = 2.0 * M * d
     tm = w["up_mfma_flops"] / (w["up_tiles"] * per_tile)
-    assert tm in (32.0, 64.0, 128.0, 256.0), tm
+    assert tm in (256.0, 384.0), tm   # the up kernel's tile heights
     assert w["up_tiles"] == int(np.sum(-(-rows // int(tm))))
     act_half = 2.0 * d * M * act_blocks
     assert act_half <= w["up_mfma_flops"] and act_half <= w["down_mfma_flops"]

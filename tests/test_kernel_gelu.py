@@ -82,3 +82,41 @@ def test_infinities_and_nan():
     with np.errstate(invalid="ignore"):
         v = gelu_kernel(np.array([np.inf, np.nan]), c, ymax)
     assert v[0] == np.inf and np.isnan(v[1])
+
+
+def gelu_grad_kernel(x, c, ymax):
+    """gelu_exp2poly_grad's derivative in fp32 steps: the fitted
+    Phi(-|x|) = 2^Q(|x|) gives Phi(x), and phi(x) = 2^(-x^2 log2(e)/2) / sqrt(2 pi)."""
+    x = f32(x)
+    y = np.minimum(np.abs(x), ymax)
+    q = fma32(c[7], y, c[6])
+    for i in range(5, -1, -1):
+        q = fma32(q, y, c[i])
+    P = f32(np.exp2(q))
+    Phi = np.where(x >= 0, f32(1.0 - P), P)
+    phi2 = f32(np.exp2(f32(f32(np.float32(-0.7213475204444817) * x) * x)))
+    return fma32(f32(x * np.float32(0.3989422804014327)), phi2, Phi)
+
+
+def test_derivative_error_bound():
+    """d GELU/dx = Phi(x) + x phi(x) within 5e-6 (absolute) of the exact
+    derivative everywhere, as the header states; the backward rounds it to
+    fp16 (spacing 2^-11 near 1) right after."""
+    c, ymax = header_coefficients()
+    x = f32(np.concatenate([np.linspace(-14, 14, 560001), [0.0, 1e-30, -1e-30, 6.0, -6.0, 40.0, -40.0]]))
+    exact = special.ndtr(x) + x * np.exp(-0.5 * x * x) / np.sqrt(2.0 * np.pi)
+    got = gelu_grad_kernel(x, c, ymax)
+    assert np.abs(got - exact).max() < 5e-6
+    # the limits: 1 for large x, 0 for very negative x, 1/2 at 0 (to the fit)
+    assert abs(gelu_grad_kernel(np.array([40.0]), c, ymax)[0] - 1.0) < 1e-8
+    assert abs(gelu_grad_kernel(np.array([-40.0]), c, ymax)[0]) < 1e-8
+    assert abs(gelu_grad_kernel(np.array([0.0]), c, ymax)[0] - 0.5) < 5e-6
+
+
+def test_derivative_matches_header_formula():
+    """The constants the host model uses are the ones in the header."""
+    text = open(os.path.join(CSRC, "common.hpp")).read()
+    body = text[text.index("void gelu_exp2poly_grad"):]
+    body = body[:body.index("\n}\n")]
+    assert "-0.7213475204444817f" in body and "0.3989422804014327f" in body
+    assert "a >= 0.0f ? 1.0f - P : P" in body
