@@ -293,14 +293,14 @@ int32_t unif_moe_layer_backward_workspace_size(const unif_moe_config* cfg, size_
  * Every gradient is bitwise repeatable: each sum runs in a fixed order (the
  * expert weight gradients over each (expert, block)'s rows in token order).
  * bf16 layers run on the matrix cores over the (pair, block) rows the
- * forward runs, never over inactive blocks: a = x K^T with GELU(a) and
- * GELU'(a) kept in fp16; dy V (bf16 products, fp32 sums) gives the pair's
- * d loss / d weight (sum of GELU(a) . dy V over its blocks, fp32), then
+ * forward runs, never over inactive blocks: a = x K^T kept in fp16; dy V
+ * (bf16 products, fp32 sums) gives the pair's d loss / d weight (sum of
+ * GELU(a) . dy V over its blocks, fp32), then
  * d loss / da = w (dy V) GELU'(a) and w GELU(a), both rounded to bf16, which
  * feed dx = sum over blocks of (d loss / da) K and the weight gradients
  * (bf16 products, fp32 sums). fp32 layers run on the vector units in fp32
  * (tiled GEMMs over each expert's pairs, dense over H and masked to the
- * pair's blocks) and require N <= 8,388,480. Requires what
+ * pair's blocks) and require N <= 8,388,480. Requires d % 8 == 0 and what
  * unif_moe_layer_forward requires; otherwise UNIF_EUNSUPPORTED. Errors as
  * unif_moe_layer_forward. */
 int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const uint8_t* valid,

@@ -258,65 +258,167 @@ __global__ __launch_bounds__(256) void bwd_seg_kernel(BwdParams p) {
     }
 }
 
-// One wave per token: router terms and the sum of the token's pairs.
+// Per token: the router-logit gradients dz (dz0 for W_shr through alpha,
+// dl_j for W_j through the softmax) and dX = the sum of the token's dx_pair
+// plus sum_j dz_j W_j. A workgroup takes kTokTile tokens: their dz first
+// (one thread per (token, slot)), kept in LDS and written out for the
+// router's weight gradient; then each thread takes columns n, holds W_j[n]
+// for 16 j at a time in registers and adds their terms to all the tile's
+// tokens. Fixed summation order: the pairs in slot order, then j = 0..K.
+constexpr int kTokTile = 16;
+constexpr int kDzRow = 80;   // K+1 <= 65, rounded up to whole groups of 16
+
 __global__ __launch_bounds__(256) void bwd_token_kernel(BwdParams p) {
-    const int t = blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    if (t >= p.N) return;
-    const int lane = lane_id();
-    const int k = p.nres[t];
-    const int* of = p.pair_of + (size_t)t * (p.K + 1);
-    float* dz = p.dz + (size_t)t * (p.K + 1);
-    if (k == 0) {   // padded token
-        for (int j = lane; j <= p.K; j += kWave) dz[j] = 0.f;
-        for (int n = lane; n < p.d; n += kWave) p.dX[(size_t)t * p.d + n] = 0.f;
-        return;
+    __shared__ float dzs[kTokTile][kDzRow];
+    __shared__ float sdp_s[kTokTile];
+    const int K1 = p.K + 1;
+    const int t0 = blockIdx.x * kTokTile;
+    const int nt = min(kTokTile, p.N - t0);
+    for (int x = threadIdx.x; x < kTokTile * kDzRow; x += blockDim.x) dzs[x / kDzRow][x % kDzRow] = 0.f;
+    // sum_m p_m dp_m with dp nonzero for the k selected experts
+    if ((int)threadIdx.x < nt) {
+        const int t = t0 + threadIdx.x;
+        const int k = p.nres[t];
+        const int* of = p.pair_of + (size_t)t * K1;
+        float sdp = 0.f;
+        for (int i = 0; i < k; ++i) sdp = fmaf(p.wts[(size_t)t * p.K + i], p.dcoef[of[1 + i]], sdp);
+        sdp_s[threadIdx.x] = sdp;
     }
-    // alpha = tau + (1 - 2 tau) sigma(z0): dz0 = dcoef_shr (1 - 2 tau) sigma (1 - sigma),
-    // sigma recovered from alpha.
-    float dz0 = 0.f;
-    if (p.alpha_adaptive) {
-        const float sg = (p.alpha[t] - p.tau) / p.one_minus_2tau;
-        dz0 = p.dcoef[of[0]] * p.one_minus_2tau * sg * (1.f - sg);
-    }
-    // p_i = s_{q_i}; dl_{q_i} = p_i (dp_{q_i} - sum_m p_m dp_{q_m}), dp nonzero for i < k.
-    float sdp = 0.f;
-    for (int i = 0; i < k; ++i) sdp = fmaf(p.wts[(size_t)t * p.K + i], p.dcoef[of[1 + i]], sdp);
-    // dz (for the router's weight gradient, a later kernel) and dX: every
-    // lane recomputes the K values dl_j it needs rather than reading dz back.
-    if (lane == 0) dz[0] = dz0;
-    for (int i = lane; i < p.K; i += kWave) {
-        const float pi = p.wts[(size_t)t * p.K + i];
-        const float dpi = (i < k) ? p.dcoef[of[1 + i]] : 0.f;
-        dz[p.eids[(size_t)t * p.K + i]] = pi * (dpi - sdp);
-    }
-    for (int n = lane; n < p.d; n += kWave) {
+    __syncthreads();
+    // Slot 0: alpha = tau + (1 - 2 tau) sigma(z0), so dz0 = dcoef_shr (1 - 2
+    // tau) sigma (1 - sigma), sigma recovered from alpha. Slot i + 1: p_i =
+    // s_{q_i}, dl_{q_i} = p_i (dp_{q_i} - sum_m p_m dp_{q_m}). Padded tokens
+    // get zeros (slot i then stands for j = i).
+    for (int x = threadIdx.x; x < nt * K1; x += blockDim.x) {
+        const int tt = x / K1, i = x - tt * K1, t = t0 + tt;
+        const int k = p.nres[t];
         float v = 0.f;
-        for (int i = 0; i <= k; ++i) v += p.dxp[(size_t)of[i] * p.d + n];
-        v = fmaf(dz0, p.Wr[n], v);
-        for (int i = 0; i < p.K; ++i) {
-            const float pi = p.wts[(size_t)t * p.K + i];
-            const float dpi = (i < k) ? p.dcoef[of[1 + i]] : 0.f;
-            v = fmaf(pi * (dpi - sdp), p.Wr[(size_t)p.eids[(size_t)t * p.K + i] * p.d + n], v);
+        int j = i;
+        if (k > 0) {
+            const int* of = p.pair_of + (size_t)t * K1;
+            if (i == 0) {
+                if (p.alpha_adaptive) {
+                    const float sg = (p.alpha[t] - p.tau) / p.one_minus_2tau;
+                    v = p.dcoef[of[0]] * p.one_minus_2tau * sg * (1.f - sg);
+                }
+            } else {
+                const float pi = p.wts[(size_t)t * p.K + i - 1];
+                const float dpi = (i - 1 < k) ? p.dcoef[of[i]] : 0.f;
+                v = pi * (dpi - sdp_s[tt]);
+                j = p.eids[(size_t)t * p.K + i - 1];
+            }
         }
-        p.dX[(size_t)t * p.d + n] = v;
+        dzs[tt][j] = v;
+        p.dz[(size_t)t * K1 + j] = v;
+    }
+    __syncthreads();
+    // dX, 4 columns per thread: the pair rows slot by slot across the tile's
+    // tokens (the loads of one slot are independent), then the router terms
+    // 8 j at a time with W_j[n..n+3] in registers.
+    int kk[kTokTile];
+    int kmax = 0;
+#pragma unroll
+    for (int tt = 0; tt < kTokTile; ++tt) {
+        kk[tt] = tt < nt ? p.nres[t0 + tt] : 0;
+        kmax = max(kmax, kk[tt]);
+    }
+    for (int n = 4 * (int)threadIdx.x; n < p.d; n += 4 * (int)blockDim.x) {
+        f32x4 acc[kTokTile];
+#pragma unroll
+        for (int tt = 0; tt < kTokTile; ++tt) acc[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i <= kmax; ++i) {
+#pragma unroll
+            for (int tt = 0; tt < kTokTile; ++tt)
+                if (kk[tt] > 0 && i <= kk[tt]) {
+                    const int pr = p.pair_of[(size_t)(t0 + tt) * K1 + i];
+                    acc[tt] += *reinterpret_cast<const f32x4*>(p.dxp + (size_t)pr * p.d + n);
+                }
+        }
+        for (int j0 = 0; j0 < K1; j0 += 8) {
+            f32x4 w[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                w[u] = (j0 + u < K1) ? *reinterpret_cast<const f32x4*>(p.Wr + (size_t)(j0 + u) * p.d + n)
+                                     : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int tt = 0; tt < kTokTile; ++tt)
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const float z = dzs[tt][j0 + u];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) acc[tt][q] = fmaf(z, w[u][q], acc[tt][q]);
+                }
+        }
+#pragma unroll
+        for (int tt = 0; tt < kTokTile; ++tt)
+            if (tt < nt)
+                *reinterpret_cast<f32x4*>(p.dX + (size_t)(t0 + tt) * p.d + n) =
+                    kk[tt] > 0 ? acc[tt] : f32x4{0.f, 0.f, 0.f, 0.f};
     }
 }
 
 // dW_router[j][n] = sum_t dz[t][j] x_t[n] in two passes: partial sums over
 // kRouterChunks slices of the tokens (blockIdx.y), then their sum in slice
-// order. One thread per (j, n).
-constexpr int kRouterChunks = 64;
+// order. A thread takes 8 consecutive columns of one slice (one 16-byte load
+// of a bf16 row, two of an fp32 one) and 8 j at a time in registers; the
+// slice's dz rows are staged through LDS kRouterStage tokens at a time.
+constexpr int kRouterChunks = 256;
+constexpr int kRouterStage = 64;
+constexpr int kRouterThreads = 64;
 
 template <bool BF16>
-__global__ __launch_bounds__(256) void bwd_router_kernel(BwdParams p) {
-    const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (item >= (size_t)(p.K + 1) * p.d) return;
-    const int j = (int)(item / p.d), n = (int)(item - (size_t)j * p.d);
+__global__ __launch_bounds__(kRouterThreads) void bwd_router_kernel(BwdParams p) {
+    __shared__ float dzs[kRouterStage][8];
+    const int K1 = p.K + 1;
+    const int n = 8 * (blockIdx.x * kRouterThreads + (int)threadIdx.x);
     const int c = blockIdx.y;
     const int t0 = (int)((int64_t)c * p.N / kRouterChunks), t1 = (int)((int64_t)(c + 1) * p.N / kRouterChunks);
-    float s = 0.f;
-    for (int t = t0; t < t1; ++t) s = fmaf(p.dz[(size_t)t * (p.K + 1) + j], ld_val<BF16>(p.X, (size_t)t * p.d + n), s);
-    p.rpart[(size_t)c * (p.K + 1) * p.d + item] = s;
+    for (int j0 = 0; j0 < K1; j0 += 8) {
+        float acc[8][8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+            for (int q = 0; q < 8; ++q) acc[u][q] = 0.f;
+        for (int s0 = t0; s0 < t1; s0 += kRouterStage) {
+            const int ns = min(kRouterStage, t1 - s0);
+            __syncthreads();
+            for (int x = threadIdx.x; x < kRouterStage * 8; x += kRouterThreads) {
+                const int tt = x >> 3, u = x & 7;
+                dzs[tt][u] = (tt < ns && j0 + u < K1) ? p.dz[(size_t)(s0 + tt) * K1 + j0 + u] : 0.f;
+            }
+            __syncthreads();
+            if (n < p.d)
+                for (int tt = 0; tt < ns; ++tt) {
+                    float xv[8];
+                    const size_t o = (size_t)(s0 + tt) * p.d + n;
+                    if constexpr (BF16) {
+                        const u32x4 q4 = ld16(static_cast<const u16*>(p.X) + o);
+#pragma unroll
+                        for (int h = 0; h < 4; ++h) {
+                            xv[2 * h] = __uint_as_float(q4[h] << 16);
+                            xv[2 * h + 1] = __uint_as_float(q4[h] & 0xffff0000u);
+                        }
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) xv[q] = static_cast<const float*>(p.X)[o + q];
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        const float z = dzs[tt][u];
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) acc[u][q] = fmaf(z, xv[q], acc[u][q]);
+                    }
+                }
+        }
+        if (n < p.d)
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (j0 + u < K1) {
+                    float* dst = p.rpart + ((size_t)c * K1 + j0 + u) * p.d + n;
+                    *reinterpret_cast<f32x4*>(dst) = f32x4{acc[u][0], acc[u][1], acc[u][2], acc[u][3]};
+                    *reinterpret_cast<f32x4*>(dst + 4) = f32x4{acc[u][4], acc[u][5], acc[u][6], acc[u][7]};
+                }
+    }
 }
 
 __global__ __launch_bounds__(256) void bwd_router_sum_kernel(BwdParams p) {

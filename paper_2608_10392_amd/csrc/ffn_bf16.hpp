@@ -67,13 +67,13 @@ constexpr int kXcds = 8;
 // channels) of one (expert, block) slab:
 //   kEpiGelu      H = fp16(GELU(a))                       (forward)
 //   kEpiGeluBias  H = fp16(GELU(a + b1))                   (block forward)
-//   kEpiActGrad   H = fp16(GELU(a)), G = fp16(GELU'(a))    (backward, a = x K^T)
-//   kEpiDa        with a = dy V (rows read from dY, weights V^T) and w the
-//                 pair weight: dcp = partial sums of H . a (the pair's
-//                 d loss / d w = dy . E restricted to the block), then
-//                 G = bf16(w a G) = d loss / d(x K^T) and H = bf16(w H), in
-//                 place                                  (backward)
-constexpr int kEpiGelu = 0, kEpiGeluBias = 1, kEpiActGrad = 2, kEpiDa = 3;
+//   kEpiPre       H = fp16(a)                              (backward, a = x K^T)
+//   kEpiDa        with g = dy V (rows read from dY, weights V^T), w the
+//                 pair weight and a = H: dcp = partial sums of GELU(a) . g
+//                 (the pair's d loss / d w = dy . E restricted to the
+//                 block), G = bf16(w g GELU'(a)) = d loss / d(x K^T) and
+//                 H = bf16(w GELU(a)), in place          (backward)
+constexpr int kEpiGelu = 0, kEpiGeluBias = 1, kEpiPre = 2, kEpiDa = 3;
 
 struct UpParams {
     int d, M, B, H;
@@ -88,7 +88,7 @@ struct UpParams {
     const int* totals;
     int* queue;              // 8 per-XCD tile counters, zero at launch
     const float* b_up;       // [K+1, H] fp32 biases added before the GELU (kEpiGeluBias only)
-    u16* Gbuf;               // backward: layout of Hbuf, with its own sink row Gsink
+    u16* Gbuf;               // kEpiDa: layout of Hbuf, with its own sink row Gsink
     u16* Gsink;
     const float* pw;         // kEpiDa: weight of each pair
     float* dcp;              // kEpiDa: [pairs, B, 2] partial sums (block, column half)
@@ -206,11 +206,11 @@ void up_kernel(UpParams p) {
     constexpr int LA = TM / S::ROWS_PER_DMA / NWV;    // token-row copies per wave per stage
     constexpr int LB = M / S::ROWS_PER_DMA / NWV;     // weight-row copies per wave per stage
     constexpr int L = LA + LB;
-    // Epilogue stores per wave: H (two per 32-column group), and G for the
-    // backward epilogues. kEpiDa also stores its partial sums and first loads
-    // H and G, whose waits (placed by the compiler) drain the copies in
-    // flight; so NEPI is a lower bound of what follows the copies there.
-    constexpr int NEPI = RG * MG * (EPI >= kEpiActGrad ? 4 : 2);
+    // Epilogue stores per wave: H (two per 32-column group), and G for
+    // kEpiDa, which also stores its partial sums and first loads H, whose
+    // waits (placed by the compiler) drain the copies in flight; so NEPI is
+    // a lower bound of what follows the copies there.
+    constexpr int NEPI = RG * MG * (EPI == kEpiDa ? 4 : 2);
     constexpr int A_BYTES = TM * RB, STAGE = (TM + M) * RB, RING = 2 * STAGE;
     // 4-byte copies per wave for a tile's row lists (2 TM ints): one of 64
     // ints per wave, and for TM = 384 one more of 32.
@@ -400,7 +400,7 @@ void up_kernel(UpParams p) {
         // per 32-column group.
         const int sl = info & 0xffff, nrows = info >> 16;
         const int c = sl - (sl / p.B) * p.B;
-        if constexpr (EPI >= kEpiActGrad) {
+        if constexpr (EPI >= kEpiPre) {
 #pragma unroll
             for (int i = 0; i < RG; ++i) {
                 const int r = wm * (TM / 4) + i * 32 + lr;
@@ -408,45 +408,40 @@ void up_kernel(UpParams p) {
                 const int pr = live ? rows[(par * 2 + 1) * TM + r] : 0;
                 const size_t off = (live ? (size_t)pr * p.H + (size_t)c * M : 0) + wn * (M / 2) + 16 * lh;
                 u16* ha = (live ? p.Hbuf : p.Hsink) + off;
-                u16* hg = (live ? p.Gbuf : p.Gsink) + off;
-                if constexpr (EPI == kEpiActGrad) {
+                if constexpr (EPI == kEpiPre) {
 #pragma unroll
                     for (int j = 0; j < MG; ++j) {
                         const f32x16 v = acc[i][j];
-                        u32x4 alo, ahi, glo, ghi;
+                        u32x4 lo, hi;
 #pragma unroll
-                        for (int t = 0; t < 8; ++t) {
-                            float g0, g1, d0, d1;
-                            gelu_exp2poly_grad(v[2 * t], g0, d0);
-                            gelu_exp2poly_grad(v[2 * t + 1], g1, d1);
-                            (t < 4 ? alo : ahi)[t & 3] = pack_f16x2(g0, g1);
-                            (t < 4 ? glo : ghi)[t & 3] = pack_f16x2(d0, d1);
+                        for (int t = 0; t < 4; ++t) {
+                            lo[t] = pack_f16x2(v[2 * t], v[2 * t + 1]);
+                            hi[t] = pack_f16x2(v[8 + 2 * t], v[9 + 2 * t]);
                         }
-                        st16(ha + 32 * j, alo);
-                        st16(ha + 32 * j + 8, ahi);
-                        st16(hg + 32 * j, glo);
-                        st16(hg + 32 * j + 8, ghi);
+                        st16(ha + 32 * j, lo);
+                        st16(ha + 32 * j + 8, hi);
                     }
                 } else {
+                    u16* hg = (live ? p.Gbuf : p.Gsink) + off;
                     const float w = live ? p.pw[pr] : 0.f;
                     float dc = 0.f;
 #pragma unroll
                     for (int j = 0; j < MG; ++j) {
                         const f32x16 v = acc[i][j];
                         const u32x4 a4[2] = {ld16(ha + 32 * j), ld16(ha + 32 * j + 8)};
-                        const u32x4 g4[2] = {ld16(hg + 32 * j), ld16(hg + 32 * j + 8)};
                         u32x4 wo[2], dq[2];
 #pragma unroll
                         for (int h = 0; h < 2; ++h)
 #pragma unroll
                             for (int t = 0; t < 4; ++t) {
-                                float a0, a1, g0, g1;
+                                float a0, a1, e0, e1, g0, g1;
                                 unpack_f16x2(a4[h][t], a0, a1);
-                                unpack_f16x2(g4[h][t], g0, g1);
+                                gelu_exp2poly_grad(a0, e0, g0);
+                                gelu_exp2poly_grad(a1, e1, g1);
                                 const float v0 = v[8 * h + 2 * t], v1 = v[8 * h + 2 * t + 1];
-                                dc = fmaf(a0, v0, dc);
-                                dc = fmaf(a1, v1, dc);
-                                wo[h][t] = pack_bf16x2(w * a0, w * a1);
+                                dc = fmaf(e0, v0, dc);
+                                dc = fmaf(e1, v1, dc);
+                                wo[h][t] = pack_bf16x2(w * e0, w * e1);
                                 dq[h][t] = pack_bf16x2(w * v0 * g0, w * v1 * g1);
                             }
                         st16(ha + 32 * j, wo[0]);

@@ -898,6 +898,8 @@ int32_t check_backward_shape(const unif_moe_config* c) {
     if (s != UNIF_OK) return s;
     // fp32 layers: pair tiles of an expert segment index grid dimension y.
     if (c->dtype == UNIF_F32 && ceil_div(c->n_tokens, kBT) > 65535) return UNIF_EUNSUPPORTED;
+    // the per-token and router-gradient kernels take 4 and 8 columns at a time
+    if (c->d_model % 8 != 0) return UNIF_EUNSUPPORTED;
     return UNIF_OK;
 }
 
@@ -1030,8 +1032,8 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
         transpose16_kernel<<<(unsigned)ceil_div(nt, 4), 256, 0, st>>>(static_cast<const u16*>(W_up), wupT, m.H,
                                                                        m.d, nt);
         UNIF_LAUNCH_CHECK();
-        // 3. a = x K^T over the slabs: GELU(a) and GELU'(a); then dy V: the
-        //    dy . E partials, da and w GELU(a)
+        // 3. a = x K^T over the slabs (kept in fp16); then dy V: the dy . E
+        //    partials, da and w GELU(a)
         UpParams up;
         up.d = m.d;
         up.M = m.M;
@@ -1056,7 +1058,7 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
         up.dcp_sink = dcp + pmax * m.B * 2;
         const size_t up_lds = (size_t)up_lds_bytes(m.M, up_tm(m.M, m.d));
         const int grid = (cus / kXcds) * kXcds;
-        s = launch_up<kEpiActGrad>(m, grid, up_lds, st, up);
+        s = launch_up<kEpiPre>(m, grid, up_lds, st, up);
         if (s != UNIF_OK) return s;
         up.X = static_cast<const u16*>(dY);
         up.Wup = wdnT;
@@ -1104,14 +1106,13 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
         UNIF_LAUNCH_CHECK();
     }
     // 5. per token: dX and the router-logit gradients; the router's weight gradient
-    bwd_token_kernel<<<(unsigned)ceil_div(m.N, 4), 256, 0, st>>>(p);
+    bwd_token_kernel<<<(unsigned)ceil_div(m.N, kTokTile), 256, 0, st>>>(p);
     UNIF_LAUNCH_CHECK();
-    const unsigned rg = (unsigned)ceil_div(m.K1 * m.d, 256);
-    const dim3 rgrid(rg, kRouterChunks);
-    if (m.bf16) bwd_router_kernel<true><<<rgrid, 256, 0, st>>>(p);
-    else bwd_router_kernel<false><<<rgrid, 256, 0, st>>>(p);
+    const dim3 rgrid((unsigned)ceil_div(m.d, 8 * kRouterThreads), kRouterChunks);
+    if (m.bf16) bwd_router_kernel<true><<<rgrid, kRouterThreads, 0, st>>>(p);
+    else bwd_router_kernel<false><<<rgrid, kRouterThreads, 0, st>>>(p);
     UNIF_LAUNCH_CHECK();
-    bwd_router_sum_kernel<<<rg, 256, 0, st>>>(p);
+    bwd_router_sum_kernel<<<(unsigned)ceil_div(m.K1 * m.d, 256), 256, 0, st>>>(p);
     UNIF_LAUNCH_CHECK();
     // 6. expert weight gradients
     if (m.bf16) {

@@ -267,3 +267,14 @@ def test_diversity_loss_rejects_bad_arguments(L):
     assert call(nbytes=n.value - 1) == _lib.EWORKSPACE
     bad = _lib.make_config(dict(cfg, n_experts=0))
     assert L.unif_moe_diversity_loss(ctypes.byref(bad), p, 1.0, p, p, p, n.value, None) == _lib.EINVAL
+
+
+def test_backward_needs_whole_column_groups():
+    """The backward's per-token and router kernels take 8 columns at a time:
+    an fp32 layer with d % 8 != 0 is rejected by the size query."""
+    ok = layer_config(get_config("tiny_f32", d_model=64))
+    assert _lib.layer_backward_workspace_size(ok) > 0
+    with pytest.raises(_lib.UnifMoeError) as e:
+        _lib.layer_backward_workspace_size(dict(ok, d_model=60))
+    assert e.value.status == _lib.EUNSUPPORTED
+    assert _lib.layer_forward_workspace_size(dict(ok, d_model=60)) > 0

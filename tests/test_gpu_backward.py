@@ -7,8 +7,8 @@ g_ref| / max |g_ref|:
     oracle in fp64);
   * bf16 layers: <= 1e-2. The matrix-core path rounds d loss / da and
     w GELU(a) to bf16 (relative step 2^-8, so at most 2^-9 = 1.95e-3 per
-    value) before the products that give dx, dW_up and dW_down, and GELU(a),
-    GELU'(a) to fp16; each gradient element is a sum of such rounded terms,
+    value) before the products that give dx, dW_up and dW_down, and the
+    pre-activation a to fp16; each gradient element is a sum of such terms,
     whose error is at most 2^-9 of the sum of their magnitudes. The bound
     allows that sum to reach five times the largest gradient element.
 The decisions are held fixed, so tokens whose routing margin is below 1e-4

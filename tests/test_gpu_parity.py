@@ -227,9 +227,10 @@ def test_forward_work_counts(routing_passed):
     """unif_moe_forward_work on the workspace of the last forward: the pair
     count is n_valid + sum k; the up-projection ran sum over (expert, block)
     slabs of ceil(rows / tile) tiles, where a slab's rows are the tokens whose
-    I_shr holds the block (shared expert) or that selected the expert
-    (residual, every block); executed MFMA work is at least the activated
-    work. Holds with the routing record in the workspace or passed in."""
+    I_shr holds the block (shared expert) or that selected the expert and
+    whose I_shr lacks the block (residual: the B - b other blocks); executed
+    MFMA work is at least the activated work. Holds with the routing record
+    in the workspace or passed in."""
     from paper_2608_10392_amd import _lib
     g = generate(get_config("vit_s16", n_tokens=2500, d_model=384, n_experts=8, n_blocks=8,
                             block_width=192, max_shared=8))
@@ -256,11 +257,12 @@ def test_forward_work_counts(routing_passed):
             continue
         b, shr, k, q = O.decisions(orec, t)
         pairs += 1 + k
-        act_blocks += b + k * B
+        act_blocks += b + k * (B - b)
+        rest = [c for c in range(B) if c not in shr]
         for c in shr:
             rows[0, c] += 1
         for e in q:
-            rows[e, :] += 1
+            rows[e, rest] += 1
     assert w["pairs"] == pairs
     per_tile = 2.0 * M * d
     tm = w["up_mfma_flops"] / (w["up_tiles"] * per_tile)
