@@ -430,40 +430,63 @@ __global__ __launch_bounds__(256) void bwd_router_sum_kernel(BwdParams p) {
     p.dWr[item] = s;
 }
 
-// Weight gradients of expert e as two fp32 GEMMs over its pair segment:
+// Weight gradients of expert e as two fp32 GEMMs over its pairs:
 //   dW_up[e][h][n]   = sum_pr da[pr][h] x_{tok(pr)}[n]
 //   dW_down[e][n][h] = sum_pr w_pr dy_{tok(pr)}[n] act[pr][h]
 // blockIdx.z = e, blockIdx.y picks the product (0: up, 1: down); one
-// kBT x kBT output tile per workgroup (rows: h for up, n for down), 16 pairs
-// per LDS step.
+// kBT x kBT output tile per workgroup (rows: h for up, n for down). The sum
+// runs over the tokens in order, 16 per LDS step, each step taking the
+// step's pairs with expert e (a token has at most one), so it is the same on
+// every call (the segment order of the pairs follows the routing kernel's
+// atomics).
 __global__ __launch_bounds__(256) void bwd_wgrad_kernel(BwdParams p, int tiles_h, int tiles_d) {
     __shared__ float Ls[16][kBT + 1];   // pair x output-row operand
     __shared__ float Rs[16][kBT + 1];   // pair x output-column operand
+    __shared__ int prs[16];             // the step's pairs with expert e (-1: none)
     const int e = blockIdx.z, up = blockIdx.y == 0;
     const int rows = up ? p.H : p.d, cols = up ? p.d : p.H;
     const int tr = up ? tiles_h : tiles_d, tc = up ? tiles_d : tiles_h;
     const int tile = blockIdx.x;
     if (tile >= tr * tc) return;
     const int r0 = (tile / tc) * kBT, c0 = (tile % tc) * kBT;
-    const int p0 = p.seg_off[e], p1 = p.seg_off[e + 1];
     const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
     // Channel blocks of this tile (rows h for up, columns h for down): a
-    // 16-pair step whose pairs run none of them adds exact zeros and is
+    // 16-token step whose pairs run none of them adds exact zeros and is
     // skipped.
     const uint64_t tmask = up ? channel_blocks(r0, min(r0 + kBT, rows), p.M)
                               : channel_blocks(c0, min(c0 + kBT, cols), p.M);
     float acc[kBU][kBU] = {};
-    for (int q0 = p0; q0 < p1; q0 += 16) {
+    for (int q0 = 0; q0 < p.N; q0 += 16) {
+        if (threadIdx.x < 16) {
+            const int t = q0 + threadIdx.x;
+            int pr = -1;
+            const int k = t < p.N ? p.nres[t] : 0;
+            if (k > 0) {
+                if (e == 0) {
+                    pr = p.pair_of[(size_t)t * (p.K + 1)];
+                } else {
+                    for (int i = 0; i < k; ++i)
+                        if (p.eids[(size_t)t * p.K + i] == e) {
+                            pr = p.pair_of[(size_t)t * (p.K + 1) + 1 + i];
+                            break;
+                        }
+                }
+            }
+            prs[threadIdx.x] = pr;
+        }
+        __syncthreads();
         uint64_t cu = 0;
-        for (int j = 0; j < 16 && q0 + j < p1; ++j) cu |= p.pair_mask[q0 + j];
-        if ((cu & tmask) == 0) continue;
-        // Stage 16 pairs x kBT rows and 16 pairs x kBT columns (bf16 layers:
-        // 8-chunks, whole and aligned since H % 64 == 0 and d % 128 == 0).
+        for (int j = 0; j < 16; ++j)
+            if (prs[j] >= 0) cu |= p.pair_mask[prs[j]];
+        if ((cu & tmask) == 0) {
+            __syncthreads();   // every thread has read prs before it is rewritten
+            continue;
+        }
         for (int i = threadIdx.x; i < 16 * kBT; i += blockDim.x) {
-            const int pi = i / kBT, x = i % kBT, pr = q0 + pi;
+            const int pi = i / kBT, x = i % kBT, pr = prs[pi];
             float lv = 0.f, rv = 0.f;
-            if (pr < p1) {
-                const int t = p.pair_token[pr];
+            if (pr >= 0) {
+                const int t = q0 + pi;
                 if (up) {
                     if (r0 + x < rows) lv = p.da[(size_t)pr * p.H + r0 + x];
                     if (c0 + x < cols) rv = ld_f32(p.X, (size_t)t * p.d + c0 + x);
