@@ -30,7 +30,6 @@ on the same sample checked against it ("parity_on_sample").
 import argparse
 import json
 import os
-import subprocess
 import sys
 import threading
 import time
@@ -79,7 +78,7 @@ def phase_bytes(cfg, st):
 
 
 COUNTERS_PROFILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
-                                "gemm_vit_b16_hbm_counters.md")
+                                "vit_b16_forward_hbm_counters.md")
 
 
 def library_source_hash():
@@ -99,18 +98,21 @@ def library_source_hash():
     return h.hexdigest()
 
 
-def committed_traffic(kernel):
-    """HBM bytes per launch of `kernel` from the committed counter summary
-    (FETCH_SIZE and WRITE_SIZE scaled by a same-run copy of known size), or
-    None when the summary is missing or the sources changed since."""
+def committed_phase_bytes():
+    """HBM bytes per forward of each phase (sum over its kernels) from the
+    committed counter summary of the headline workload (FETCH_SIZE and
+    WRITE_SIZE scaled by a same-run copy of known size), or None when the
+    summary is missing or the sources changed since."""
     try:
         with open(COUNTERS_PROFILE) as f:
             line = next(l for l in f if l.startswith("counters-json:"))
         c = json.loads(line.split(":", 1)[1])
         if c.get("source_sha256") != library_source_hash():
             return None
-        k = c["kernels"][kernel]
-        return int(k["read_bytes_per_launch"] + k["write_bytes_per_launch"])
+        out = {}
+        for k in c["kernels"].values():
+            out[k["phase"]] = out.get(k["phase"], 0) + int(k["read_bytes_per_launch"] + k["write_bytes_per_launch"])
+        return out
     except (OSError, StopIteration, ValueError, KeyError):
         return None
 
@@ -122,25 +124,41 @@ def median(v):
 
 
 class ClockSampler:
-    """Shader clock samples (rocm-smi) taken while the GPU runs; best effort."""
+    """Shader clock samples read from sysfs while the GPU runs (the current
+    level of pp_dpm_sclk, else the hwmon frequency); best effort, no child
+    processes."""
 
     def __init__(self):
+        import glob
         self.samples = []
         self._stop = threading.Event()
         self._t = None
+        self._dpm = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self._hwmon = sorted(glob.glob("/sys/class/drm/card*/device/hwmon/hwmon*/freq1_input"))
+
+    def _read(self):
+        for path in self._dpm:
+            try:
+                with open(path) as f:
+                    for line in f:
+                        if line.rstrip().endswith("*"):
+                            return int("".join(ch for ch in line.split(":", 1)[1] if ch.isdigit()))
+            except (OSError, ValueError, IndexError):
+                pass
+        for path in self._hwmon:
+            try:
+                with open(path) as f:
+                    return int(f.read().strip()) // 1000000
+            except (OSError, ValueError):
+                pass
+        return None
 
     def _run(self):
         while not self._stop.is_set():
-            try:
-                out = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True,
-                                     timeout=10).stdout
-                for card in json.loads(out).values():
-                    for key, v in card.items():
-                        if key.lower().startswith("sclk"):
-                            self.samples.append(int("".join(ch for ch in str(v) if ch.isdigit())))
-            except Exception:
-                return
-            self._stop.wait(0.5)
+            v = self._read()
+            if v:
+                self.samples.append(v)
+            self._stop.wait(0.05)
 
     def start(self):
         self._t = threading.Thread(target=self._run, daemon=True)
@@ -149,11 +167,11 @@ class ClockSampler:
     def stop(self):
         self._stop.set()
         if self._t is not None:
-            self._t.join(timeout=15)
+            self._t.join(timeout=5)
         s = sorted(self.samples)
         return {"samples": len(s), "max_mhz": s[-1] if s else None,
                 "median_mhz": s[len(s) // 2] if s else None,
-                "note": "rocm-smi samples every 0.5 s during the per-workload runs"}
+                "note": "sysfs current shader-clock level every 50 ms from the headline run to the end of the other workloads"}
 
 
 def measure(torch, _lib, dev, cfg, steps, warmup, stream):
@@ -302,6 +320,8 @@ def main():
     stream = torch.cuda.current_stream()
 
     print(f"[bench] warmup {args.warmup}, timing {args.steps} steps", file=sys.stderr, flush=True)
+    clock = ClockSampler()
+    clock.start()
     ms_per_step, ms_event, phase_ms = measure(torch, _lib, dev, cfg, args.steps, args.warmup, stream)
     st = dev.stats()
     work = _lib.forward_work(cfg, dev.ws_forward) if cfg["dtype"] == "bf16" else None
@@ -323,16 +343,22 @@ def main():
                    "n_experts": cfg["n_experts"], "n_blocks": cfg["n_blocks"],
                    "block_width": cfg["block_width"], "mass_threshold": cfg["mass_threshold"]},
         "roofline": {"bound": "mfma", "kernel": rf["kernel"], "achieved": rf["achieved"], "peak": rf["peak"],
-                     "unit": "TFLOP/s", "frac": rf["frac"], "traffic": committed_traffic(rf["kernel"])},
+                     "unit": "TFLOP/s", "frac": rf["frac"], "traffic": None},
     }
+    counted = committed_phase_bytes() if args.workload == "vit_b16" else None
+    if counted is not None:
+        out["roofline"]["traffic"] = counted.get(rf["kernel"])
+        rpc = [n for n in ("routing", "permute", "combine") if n in counted]
+        out["hbm_frac_counters"] = {n: round(counted[n] / (phase_ms[n] / 1e3) / PEAK_HBM_BYTES, 4) for n in rpc}
+        out["hbm_frac_counters"]["routing_permute_combine"] = round(
+            sum(counted[n] for n in rpc) / (sum(phase_ms[n] for n in rpc) / 1e3) / PEAK_HBM_BYTES, 4)
+        out["counted_bytes"] = counted
     for k in ("mfma_util_activated", "executed_vs_activated", "hbm_frac", "hbm_frac_routing_permute_combine",
               "phases_ms"):
         if k in head:
             out[k] = head[k]
     out["routing_stats"] = {k: head[k] for k in ("mean_b", "mean_k", "mean_cb", "activated_gemm_tflop")}
 
-    clock = ClockSampler()
-    clock.start()
     if not args.no_paper_exact and cfg["mass_threshold"] != 1.0:
         # The same tokens and weights with the target exactly Eq. beta
         # (t = 1): more residual experts per token, so more activated work.
