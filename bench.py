@@ -55,6 +55,9 @@ def parse():
     ap.add_argument("--no-backward", action="store_true", help="skip the backward-pass run")
     ap.add_argument("--cpu-sample", type=int, default=2048)
     ap.add_argument("--cpu-repeats", type=int, default=3)
+    ap.add_argument("--vendor-reference", action="store_true",
+                    help="also time dense bf16 GEMMs of the workload's FFN shapes and one expert slab "
+                         "through torch.matmul (hipBLASLt), and a device copy, as a vendor reference")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after the timed steps, copy a buffer of this many MiB device to "
                          "device (a known-size reference for HBM byte counters)")
@@ -233,6 +236,51 @@ def summarize(cfg, st, work, ms_event, phase_ms):
             "down": round(work["down_mfma_flops"] / (act / 2.0), 4),
             "mfma_util_executed": round((work["up_mfma_flops"] + work["down_mfma_flops"]) / (gemm_ms / 1e3)
                                         / PEAK_BF16_FLOPS, 4)}
+    return out
+
+
+def vendor_reference(torch, cfg, st):
+    """Dense bf16 GEMMs of the layer's FFN shapes (all N tokens through all H
+    channels: [N, d] x [d, H] and [N, H] x [H, d]) and of one expert-block
+    slab's shape (its mean row count x d x M) through torch.matmul, which
+    dispatches to hipBLASLt; medians of 20 HIP-event timings after 3 warmups,
+    against the 2.5 PFLOP/s bf16 peak. Also a device-to-device copy of 1 GiB
+    (bytes read + written per second)."""
+    N, d, H, M = cfg["n_tokens"], cfg["d_model"], cfg["n_blocks"] * cfg["block_width"], cfg["block_width"]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    out = {}
+
+    def timed(fn, reps=20):
+        for _ in range(3):
+            fn()
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return median(ts)
+
+    def gemm(name, m, k, n):
+        A = torch.randn(m, k, device="cuda", dtype=torch.bfloat16, generator=g)
+        B = torch.randn(k, n, device="cuda", dtype=torch.bfloat16, generator=g)
+        ms = timed(lambda: A @ B)
+        fl = 2.0 * m * k * n
+        out[name] = {"shape": f"{m}x{k}x{n}", "ms": round(ms, 4), "tflops": round(fl / ms / 1e9, 1),
+                     "frac": round(fl / ms / 1e9 / (PEAK_BF16_FLOPS / 1e12), 4)}
+
+    gemm("dense_up", N, d, H)
+    gemm("dense_down", N, H, d)
+    rows = max(1, int(round(st["activated_blocks"] / ((cfg["n_experts"] + 1) * cfg["n_blocks"]))))
+    gemm("slab_up", rows, d, M)
+    src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    ms = timed(lambda: dst.copy_(src), reps=10)
+    out["copy_1gib"] = {"ms": round(ms, 4), "TBps": round(2 * src.numel() * 4 / ms / 1e9, 2)}
+    out["note"] = "torch.matmul (hipBLASLt) and torch copy, HIP-event medians"
     return out
 
 
@@ -461,6 +509,10 @@ def main():
             "achieved_tflops": round(bflops / (msg / 1e3) / 1e12, 2),
             "workspace_gb": round(wsg.numel() / 1e9, 2)}
         del wsg, gr, dYd
+        torch.cuda.empty_cache()
+    if args.vendor_reference:
+        print("[bench] vendor reference GEMMs", file=sys.stderr, flush=True)
+        out["vendor_reference"] = vendor_reference(torch, cfg, st)
         torch.cuda.empty_cache()
     if args.copy_calibration_mb > 0:
         nbytes = args.copy_calibration_mb << 20
