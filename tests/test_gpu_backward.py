@@ -80,6 +80,8 @@ CASES = {
                            max_shared=4)),
     "b2_m256": ("vit_s16", dict(n_tokens=260, d_model=256, n_experts=3, n_blocks=2,
                                 block_width=256, max_shared=2)),
+    "m128_d512": ("vit_s16", dict(n_tokens=450, d_model=512, n_experts=5, n_blocks=4,
+                                  block_width=128, max_shared=4)),
     "k64_b64": ("vit_s16", dict(n_tokens=200, d_model=128, n_experts=64, n_blocks=64,
                                 block_width=64, max_shared=64, mass_threshold=0.9)),
 }
@@ -91,7 +93,7 @@ def test_backward(name):
     run_backward(generate(get_config(base, **over)), name)
 
 
-@pytest.mark.parametrize("name", ["vit_b16", "bert_base_padded"])
+@pytest.mark.parametrize("name", ["vit_b16", "bert_base_padded", "zipf_stress"])
 def test_backward_full_size_properties(name):
     """At the full workload sizes, where the oracle's gradient sums are out of
     reach: every gradient is linear in dY, and scaling dY by 2 scales every
