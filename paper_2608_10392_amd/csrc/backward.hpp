@@ -359,65 +359,49 @@ __global__ __launch_bounds__(256) void bwd_token_kernel(BwdParams p) {
 
 // dW_router[j][n] = sum_t dz[t][j] x_t[n] in two passes: partial sums over
 // kRouterChunks slices of the tokens (blockIdx.y), then their sum in slice
-// order. A thread takes 8 consecutive columns of one slice (one 16-byte load
-// of a bf16 row, two of an fp32 one) and 8 j at a time in registers; the
-// slice's dz rows are staged through LDS kRouterStage tokens at a time.
+// order. A thread takes one column n of one slice with 16 j at a time in
+// registers (x_t[n] is read once per 16 j, four tokens' loads in flight);
+// the slice's dz rows are staged through LDS kRouterStage tokens at a time.
 constexpr int kRouterChunks = 256;
 constexpr int kRouterStage = 64;
-constexpr int kRouterThreads = 64;
 
 template <bool BF16>
-__global__ __launch_bounds__(kRouterThreads) void bwd_router_kernel(BwdParams p) {
-    __shared__ float dzs[kRouterStage][8];
+__global__ __launch_bounds__(256) void bwd_router_kernel(BwdParams p) {
+    __shared__ float dzs[kRouterStage][16];
     const int K1 = p.K + 1;
-    const int n = 8 * (blockIdx.x * kRouterThreads + (int)threadIdx.x);
+    const int n = blockIdx.x * blockDim.x + threadIdx.x;
     const int c = blockIdx.y;
     const int t0 = (int)((int64_t)c * p.N / kRouterChunks), t1 = (int)((int64_t)(c + 1) * p.N / kRouterChunks);
-    for (int j0 = 0; j0 < K1; j0 += 8) {
-        float acc[8][8];
+    for (int j0 = 0; j0 < K1; j0 += 16) {
+        float acc[16];
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-#pragma unroll
-            for (int q = 0; q < 8; ++q) acc[u][q] = 0.f;
+        for (int u = 0; u < 16; ++u) acc[u] = 0.f;
         for (int s0 = t0; s0 < t1; s0 += kRouterStage) {
             const int ns = min(kRouterStage, t1 - s0);
             __syncthreads();
-            for (int x = threadIdx.x; x < kRouterStage * 8; x += kRouterThreads) {
-                const int tt = x >> 3, u = x & 7;
+            for (int x = threadIdx.x; x < kRouterStage * 16; x += blockDim.x) {
+                const int tt = x >> 4, u = x & 15;
                 dzs[tt][u] = (tt < ns && j0 + u < K1) ? p.dz[(size_t)(s0 + tt) * K1 + j0 + u] : 0.f;
             }
             __syncthreads();
-            if (n < p.d)
-                for (int tt = 0; tt < ns; ++tt) {
-                    float xv[8];
-                    const size_t o = (size_t)(s0 + tt) * p.d + n;
-                    if constexpr (BF16) {
-                        const u32x4 q4 = ld16(static_cast<const u16*>(p.X) + o);
+            if (n < p.d) {
+                // rows past the slice read x = 0 against dz = 0
+                for (int tt = 0; tt < ns; tt += 4) {
+                    float xv[4];
 #pragma unroll
-                        for (int h = 0; h < 4; ++h) {
-                            xv[2 * h] = __uint_as_float(q4[h] << 16);
-                            xv[2 * h + 1] = __uint_as_float(q4[h] & 0xffff0000u);
-                        }
-                    } else {
+                    for (int q = 0; q < 4; ++q)
+                        xv[q] = (tt + q < ns) ? ld_val<BF16>(p.X, (size_t)(s0 + tt + q) * p.d + n) : 0.f;
 #pragma unroll
-                        for (int q = 0; q < 8; ++q) xv[q] = static_cast<const float*>(p.X)[o + q];
-                    }
+                    for (int q = 0; q < 4; ++q)
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) {
-                        const float z = dzs[tt][u];
-#pragma unroll
-                        for (int q = 0; q < 8; ++q) acc[u][q] = fmaf(z, xv[q], acc[u][q]);
-                    }
+                        for (int u = 0; u < 16; ++u) acc[u] = fmaf(dzs[tt + q][u], xv[q], acc[u]);
                 }
+            }
         }
         if (n < p.d)
 #pragma unroll
-            for (int u = 0; u < 8; ++u)
-                if (j0 + u < K1) {
-                    float* dst = p.rpart + ((size_t)c * K1 + j0 + u) * p.d + n;
-                    *reinterpret_cast<f32x4*>(dst) = f32x4{acc[u][0], acc[u][1], acc[u][2], acc[u][3]};
-                    *reinterpret_cast<f32x4*>(dst + 4) = f32x4{acc[u][4], acc[u][5], acc[u][6], acc[u][7]};
-                }
+            for (int u = 0; u < 16; ++u)
+                if (j0 + u < K1) p.rpart[((size_t)c * K1 + j0 + u) * p.d + n] = acc[u];
     }
 }
 
