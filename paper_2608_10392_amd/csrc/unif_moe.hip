@@ -1,24 +1,29 @@
 // Host side of the UniF-MoE layer library: argument validation, workspace
-// planning and the launch sequence of the forward pass. See include/unif_moe.h
-// for the contract of every entry point.
+// planning and the launch sequences. See include/unif_moe.h for the contract
+// of every entry point.
 //
 // Forward launch sequence (all asynchronous on the caller's stream, no
 // device-to-host traffic):
 //   bf16_to_f16      W_down -> fp16 copy for the down-projection (bf16 only)
-//   fill_zero        pair / slab counters
-//   split_router     fp32 router + prototypes -> 3 bf16 parts (bf16 only)
-//   route            routing record, pair slots in their bins, per-tile
-//                    slab and expert counts
-//   scan             prefix sums -> segment, bin, slab and tile offsets
+//   split_router     fp32 router + prototypes -> 3 bf16 parts (bf16 only);
+//                    the same launch clears the counters and tile queues
+//   route_logits +   logits with the router held in registers, then the
+//   route_decide     decisions, bin slots and per-tile counts (bf16 routers
+//                    of at most 32 columns); otherwise one fused route kernel
+//   scan             segment offsets, bin cursors, per-slab first rows
 //   scatter          pairs (expert segments sorted by block-mask key), the
 //                    per-(expert, block) row lists in token order and the
-//                    up tile table                               (bf16)
+//                    up tile table
+//   down_tables      down row tiles and their block-mask unions (bf16)
 //   up, down         block-sparse MFMA grouped GEMMs              (bf16)
 //   pair_ffn_f32     per-pair fp32 FFN                            (fp32)
 //   combine          weighted merge in fixed order
 // The block forward adds a LayerNorm pass before routing (pre-LN) and
 // replaces the merge by the block's merge (biases, residual, post-LN). The
-// backward runs the forward into its workspace, then the backward kernels.
+// backward runs routing and the permutation into its workspace, then its
+// own kernels (bf16: weight transposes, the x K^T and dy V passes of the up
+// engine, the dx pass of the down engine, per-token and router kernels and
+// the weight-gradient GEMMs; fp32: vector-unit GEMMs).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -47,9 +52,8 @@ constexpr int kKeyBitsMax = 10;
 constexpr int kPhaseEvents = 7;   // unif_moe_layer_forward_profiled
 constexpr size_t kLdsLimit = 160 * 1024;
 
-// Expert-GEMM tile shapes, one workgroup of 8 waves per CU. Up: 256
-// gathered rows x the whole block width M. Down: 256 pairs x 256 output
-// columns (128 when d is not a multiple of 256).
+// Expert-GEMM tile shapes, one workgroup of 8 waves per CU. Up: 256 or 384
+// gathered rows x the whole block width M. Down: see down_shape.
 // Up tiles are 384 rows when the block is at most 192 wide and no stage is
 // padding (d >= 256): their accumulators and fragments then still fit two
 // waves per SIMD without spills. Else 256.
