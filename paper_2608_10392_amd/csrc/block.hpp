@@ -147,6 +147,8 @@ __global__ __launch_bounds__(256) void layernorm_rows_kernel(LayerNormParams p) 
 
 struct BlockCombineParams {
     int N, d, K, B;
+    int nsplit;             // row buffers per pair (bf16: the down-projection's parts), summed in order
+    size_t split_stride;    // floats between them
     const void* part;       // per-pair expert rows (fp32)
     const int* pair_of;     // [N, K+1] pair of (token, i-th pathway)
     const float* alpha;
@@ -191,7 +193,9 @@ __device__ __forceinline__ void block_chunk_sum(const BlockCombineParams& c, int
                 if constexpr (BF16) {
 #pragma unroll
                     for (int h = 0; h < E / 4; ++h) {
-                        const f32x4 q = *reinterpret_cast<const f32x4*>(row + 4 * h);
+                        f32x4 q = *reinterpret_cast<const f32x4*>(row + 4 * h);
+                        for (int sp = 1; sp < c.nsplit; ++sp)
+                            q += *reinterpret_cast<const f32x4*>(row + sp * c.split_stride + 4 * h);
 #pragma unroll
                         for (int e = 0; e < 4; ++e) r[u][4 * h + e] = q[e];
                     }

@@ -9,6 +9,8 @@ namespace unifmoe {
 
 struct CombineParams {
     int N, d, K;
+    int nsplit;            // row buffers per pair (the down-projection's parts), summed in order
+    size_t split_stride;   // floats between them
     const void* part;
     const int* pair_of;
     const float* alpha;
@@ -20,7 +22,8 @@ struct CombineParams {
 constexpr int kCombineBatch = 6;
 
 // bf16 layers: one thread per 8 consecutive outputs; fp32 per-expert rows
-// (two 16-byte loads each), one 16-byte bf16 store.
+// (two 16-byte loads each, per part with SPLIT), one 16-byte bf16 store.
+template <bool SPLIT>
 __global__ void combine_bf16_kernel(CombineParams c) {
     const int chunks = c.d >> 3;
     const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -57,6 +60,16 @@ __global__ void combine_bf16_kernel(CombineParams c) {
                 v[u][h] = (i0 + u <= k)
                               ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(part + (size_t)pr[u] * c.d + ch * 8 + 4 * h))
                               : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        for (int sp = 1; SPLIT && sp < c.nsplit; ++sp) {
+#pragma unroll
+            for (int u = 0; u < kCombineBatch; ++u) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+                    if (i0 + u <= k)
+                        v[u][h] += __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(
+                            part + sp * c.split_stride + (size_t)pr[u] * c.d + ch * 8 + 4 * h));
+            }
         }
 #pragma unroll
         for (int u = 0; u < kCombineBatch; ++u) {

@@ -107,6 +107,8 @@ struct DownParams {
     const uint64_t* pair_mask;   // readable for a whole tile past the last pair
     const int* totals;           // [2]: down tiles (row tiles x column tiles)
     int* queue;                  // 8 per-XCD tile counters, zero at launch
+    int nsplit;                  // parts each tile's block union is split into (1: none)
+    size_t split_stride;         // floats between the parts' row buffers in part
 };
 
 // Staged-row geometry: one 128-byte line (64 bf16 of k) per row and stage.
@@ -533,7 +535,7 @@ void down_kernel(DownParams p) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WN, wn = wave % WN;
     const int kcpb = p.M / S::SK;   // stages per block
-    const TileQueue tq(p.queue, ld_uniform(p.totals + 2));
+    const TileQueue tq(p.queue, ld_uniform(p.totals + 2) * p.nsplit);
     // ctl as in the up kernel.
     int* ctl = reinterpret_cast<int*>(lds_dn + RING + 16 * TM);
     if (tid == 0) {
@@ -577,20 +579,31 @@ void down_kernel(DownParams p) {
     // (the column tiles of one row tile run side by side on one XCD and
     // share its H rows in L2), row tiles expert by expert; gm[i]: the block
     // mask of this wave's 32-row group i, all: the tile's.
+    // With nsplit > 1, tile t is part t % nsplit of row-and-column tile
+    // t / nsplit: every nsplit-th block of the union, in order, written to
+    // that part's row buffer (the merge adds the parts in order).
     struct Desc {
-        int p0, nrows, e, ct, nst, nreal;
+        int p0, nrows, e, ct, nst, nreal, sp;
         uint64_t all, gm[RG];
     };
     auto describe = [&](int t) {
         Desc D;
-        const int rt = t / p.ncol;
-        D.ct = t - rt * p.ncol;
+        const int tt = t / p.nsplit;
+        D.sp = t - tt * p.nsplit;
+        const int rt = tt / p.ncol;
+        D.ct = tt - rt * p.ncol;
         const int* inf = reinterpret_cast<const int*>(p.rt_info + rt);
         D.p0 = ld_uniform(inf);
         D.nrows = ld_uniform(inf + 1);
         D.e = ld_uniform(inf + 2);
         const uint64_t* ms = p.rt_masks + (size_t)rt * (TM / 32 + 1);
         D.all = ld_uniform64(ms + TM / 32);
+        if (p.nsplit > 1) {
+            uint64_t keep = 0, rem = D.all;
+            for (int i = 0; rem; ++i, rem &= rem - 1)
+                if (i % p.nsplit == D.sp) keep |= rem & (0ull - rem);
+            D.all = keep;
+        }
 #pragma unroll
         for (int i = 0; i < RG; ++i) D.gm[i] = ld_uniform64(ms + wm * RG + i);
         D.nreal = __popcll(D.all) * kcpb;
@@ -763,7 +776,8 @@ void down_kernel(DownParams p) {
 #pragma unroll
         for (int i = 0; i < RG; ++i) {
             const int r = wm * 64 + i * 32 + lr;
-            float* dst = (r < cur.nrows) ? p.part + (size_t)(cur.p0 + r) * p.d + (size_t)cur.ct * BN : p.part_sink;
+            float* dst = (r < cur.nrows) ? p.part + cur.sp * p.split_stride + (size_t)(cur.p0 + r) * p.d + (size_t)cur.ct * BN
+                                         : p.part_sink;
             dst += wn * (BN / WN) + 16 * lh;
 #pragma unroll
             for (int j = 0; j < NG; ++j) {

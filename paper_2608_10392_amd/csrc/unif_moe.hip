@@ -244,6 +244,21 @@ struct FwdPlan {
 
 size_t ceil_div_sz(size_t a, size_t b) { return (a + b - 1) / b; }
 
+// Parts each down tile's block union is split into (the parts' partial rows
+// are added by the merge in order). The down kernel runs each tile's blocks
+// one after another, so when a workload has no more tiles than a 256-CU
+// device has compute units, the chip idles while those chains run: such
+// workloads get enough parts for about two tiles per compute unit. The tile
+// count is estimated from N with 4 pairs per token (a function of cfg only,
+// since it sizes the workspace).
+int down_splits(const Dims& m) {
+    if (!m.bf16) return 1;
+    const DownShape dsh = down_shape(m.d);
+    const size_t est_pairs = (size_t)m.N * (size_t)std::min(m.K1, 4);
+    const size_t tiles = std::max<size_t>(1, ceil_div_sz(est_pairs, dsh.tm) * (size_t)(m.d / dsh.bn));
+    return tiles > 256 ? 1 : (int)std::min<size_t>(4, ceil_div_sz(2 * 256, tiles));
+}
+
 // The routing record's region is reserved whether or not the caller passes
 // its own record, so every other offset is the same for both kinds of call
 // (unif_moe_forward_work reads the workspace a forward left behind).
@@ -291,7 +306,7 @@ FwdPlan plan_forward(const Dims& m, size_t xn_bytes = 0) {
     p.up_tile_info = cv.take(m.bf16 ? 4 * up_tiles : 0);
     p.up_tile_rows = cv.take(m.bf16 ? 4 * up_tiles : 0);
     p.hbuf = cv.take(m.bf16 ? (pmax + 1) * (size_t)m.H * 2 : 0);  // fp16, + the sink row
-    p.part = cv.take((pmax + 1) * (size_t)m.d * sizeof(float));   // fp32, + the sink row
+    p.part = cv.take((pmax + 1) * (size_t)m.d * sizeof(float) * down_splits(m));   // fp32, + the sink row, per part
     p.xn = cv.take(xn_bytes);
     p.wdown16 = cv.take(m.bf16 ? K1 * (size_t)m.d * m.H * 2 : 0);
     p.total = cv.cur + 256;  // slack for aligning an unaligned base pointer
@@ -715,6 +730,8 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         dn.pair_mask = pp.pair_mask;
         dn.totals = totals;
         dn.queue = reinterpret_cast<int*>(ws + plan.queues) + 8;
+        dn.nsplit = down_splits(m);
+        dn.split_stride = ((size_t)m.N * m.K1 + 1) * m.d;
         if (dsh.bn == 384)
             s = launch_persistent(down_kernel<2, 3>, grid, (size_t)down_lds_bytes(128, 384), st, dn);
         else if (dsh.bn == 256)
@@ -751,6 +768,8 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     // 5. weighted merge (the block's merge around it)
     if (blk != nullptr) {
         BlockCombineParams bc;
+        bc.nsplit = down_splits(m);
+        bc.split_stride = ((size_t)m.N * m.K1 + 1) * m.d;
         bc.N = m.N;
         bc.d = m.d;
         bc.K = m.K;
@@ -793,6 +812,8 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         return UNIF_OK;
     }
     CombineParams cp;
+    cp.nsplit = down_splits(m);
+    cp.split_stride = ((size_t)m.N * m.K1 + 1) * m.d;
     cp.N = m.N;
     cp.d = m.d;
     cp.K = m.K;
@@ -804,7 +825,8 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     cp.Y = Y;
     if (m.bf16) {
         const size_t items = (size_t)m.N * (m.d / 8);
-        combine_bf16_kernel<<<(unsigned)((items + 255) / 256), 256, 0, st>>>(cp);
+        if (cp.nsplit > 1) combine_bf16_kernel<true><<<(unsigned)((items + 255) / 256), 256, 0, st>>>(cp);
+        else combine_bf16_kernel<false><<<(unsigned)((items + 255) / 256), 256, 0, st>>>(cp);
     } else {
         const size_t items = (size_t)m.N * m.d;
         combine_f32_kernel<<<(unsigned)((items + 255) / 256), 256, 0, st>>>(cp);
@@ -1089,6 +1111,8 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const
         dn.pair_mask = p.pair_mask;
         dn.totals = p.totals;
         dn.queue = queues + 16;
+        dn.nsplit = 1;
+        dn.split_stride = 0;
         if (dsh.bn == 384)
             s = launch_persistent(down_kernel<2, 3, false>, grid, (size_t)down_lds_bytes(128, 384), st, dn);
         else if (dsh.bn == 256)
