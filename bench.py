@@ -17,15 +17,20 @@ medians over the steps. Prints one JSON line.
 
     python bench.py [--steps 20] [--warmup 3] [--workload vit_b16] [--no-cpu-baseline]
                     [--no-configs] [--no-paper-exact] [--no-block] [--no-backward]
+                    [--no-ablations] [--vendor-reference]
 
 Also, unless switched off: "configs" - the other workloads (ViT-S/16, BERT-base
 with padding, the skewed 131k-token layer, the paper's DeiT-S and BERT-large
 operating points), each with tokens/s, phases, MFMA utilisation and roofline;
 "paper_exact_t1" - the headline tokens with the cumulative target exactly
-Eq. beta (t = 1); "block_pre_ln" - the DeiT-style pre-LN block around the
-layer; "backward" - the training step's backward pass; "cpu_baseline" - the
-CPU oracle timed on a sample of the headline workload, with the GPU output
-on the same sample checked against it ("parity_on_sample").
+Eq. beta (t = 1); "ablations" - the headline tokens under the ablation
+table's routing variants (fixed alpha, top-2 residual, prefix blocks);
+"block_pre_ln" - the DeiT-style pre-LN block around the layer;
+"block_post_ln" - the BERT-style post-LN block on the paper's BERT-large
+shape; "backward" - the training step's backward pass and the Gram
+diversity loss; "cpu_baseline" - the CPU oracle timed on a sample of the
+headline workload, with the GPU output on the same sample checked against it
+("parity_on_sample").
 """
 import argparse
 import json
@@ -53,6 +58,8 @@ def parse():
                     help="skip the second, shorter run at cumulative target t = 1")
     ap.add_argument("--no-block", action="store_true", help="skip the pre-LN block run")
     ap.add_argument("--no-backward", action="store_true", help="skip the backward-pass run")
+    ap.add_argument("--no-ablations", action="store_true",
+                    help="skip the routing ablation modes and the post-LN block")
     ap.add_argument("--cpu-sample", type=int, default=2048)
     ap.add_argument("--cpu-repeats", type=int, default=3)
     ap.add_argument("--vendor-reference", action="store_true",
@@ -444,6 +451,62 @@ def main():
             out["configs"][name] = entry
             del dc, gc
             torch.cuda.empty_cache()
+    if not args.no_ablations and args.workload == "vit_b16":
+        # The routing variants of the ablation table on the same tokens and
+        # weights: a fixed shared demand alpha = 0.4, top-2 residual experts,
+        # prefix instead of prototype block selection.
+        out["ablations"] = {}
+        for name, over in (("fixed_alpha_0.4", dict(alpha_mode="fixed", alpha_fixed=0.4)),
+                           ("top2_residual", dict(mass_mode="topk", fixed_k=2)),
+                           ("prefix_selection", dict(select_mode="prefix"))):
+            print(f"[bench] ablation {name}", file=sys.stderr, flush=True)
+            ca = dict(cfg, **over)
+            da = DeviceLayer(ca, g["X"], g["valid"], g["W_router"], g["prototypes"], g["W_up"], g["W_down"])
+            sa = max(2, args.steps // 2)
+            msa, eva, pha = measure(torch, _lib, da, ca, sa, args.warmup, stream)
+            sta = da.stats()
+            ea = summarize(ca, sta, _lib.forward_work(ca, da.ws_forward), eva, pha)
+            out["ablations"][name] = {k: ea[k] for k in ("tokens_per_s", "ms_per_step_event_median", "mean_b",
+                                                         "mean_k", "mean_cb", "activated_gemm_tflop",
+                                                         "mfma_util_activated", "executed_vs_activated",
+                                                         "phases_ms")}
+            del da
+            torch.cuda.empty_cache()
+        # The post-LN block (as in BERT) on the paper's BERT-large shape:
+        # the FFN input is the previous LayerNorm's output; LN(x + F(x)).
+        print("[bench] post-LN block (paper_language)", file=sys.stderr, flush=True)
+        from synth import block_inputs
+        gl = generate("paper_language")
+        cl = layer_config(gl["cfg"])
+        dl = DeviceLayer(cl, gl["X"], gl["valid"], gl["W_router"], gl["prototypes"], gl["W_up"], gl["W_down"])
+        msl, evl, _ = measure(torch, _lib, dl, cl, args.steps, args.warmup, stream)
+        blkl, Xl = block_inputs(gl, "post", residual=True, eps=1e-12)
+        bl = dict(norm="post", residual=True, ln_eps=float(blkl["ln_eps"]))
+        for k in ("ln_gamma", "ln_beta", "b_up", "b_down"):
+            bl[k] = torch.from_numpy(blkl[k]).to(dl.device)
+        Xld = torch.from_numpy(Xl.view(np.int16)).view(torch.bfloat16).to(dl.device)
+        wsl = _lib.alloc_workspace(_lib.block_forward_workspace_size(cl, bl), dl.device)
+
+        def post_step():
+            _lib.block_forward(cl, bl, Xld, dl.valid, dl.W_router, dl.prototypes, dl.W_up, dl.W_down, dl.Y, wsl,
+                               routing=dl.routing, stream=stream)
+        for _ in range(args.warmup):
+            post_step()
+        torch.cuda.synchronize()
+        evp = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        for a, b in evp:
+            a.record(stream)
+            post_step()
+            b.record(stream)
+        torch.cuda.synchronize()
+        msp = median([a.elapsed_time(b) for a, b in evp])
+        stl = dl.stats()
+        out["block_post_ln"] = {"workload": "paper_language (4096 slots, d=1024, K=16, B=16 x M=256, t=1)",
+                                "ms_per_step_event_median": round(msp, 4),
+                                "tokens_per_s": round(stl["n_valid"] / (msp / 1e3), 1),
+                                "layer_ms_event_median": round(evl, 4), "over_layer_ms": round(msp - evl, 4)}
+        del dl, gl, wsl, Xld, bl
+        torch.cuda.empty_cache()
     out["clocks"] = clock.stop()
     if not args.no_block:
         # The pre-LN block (as in DeiT) around the same layer: LN(x) feeds
@@ -510,12 +573,25 @@ def main():
         torch.cuda.synchronize()
         msg = median([a.elapsed_time(b) for a, b in ev])
         bflops = 8.0 * cfg["d_model"] * cfg["block_width"] * st["activated_blocks"]
+        # The Gram diversity loss of the router (Eq. diversity-loss) and its
+        # gradient added to dW_router, as in a training step.
+        wsd = _lib.alloc_workspace(_lib.diversity_loss_workspace_size(cfg), dev.device)
+        lossd = torch.zeros(1, dtype=torch.float32, device=dev.device)
+        _lib.diversity_loss(cfg, dev.W_router, 0.01, lossd, gr["dW_router"], wsd, stream=stream)
+        evd = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(5)]
+        for a, b in evd:
+            a.record(stream)
+            _lib.diversity_loss(cfg, dev.W_router, 0.01, lossd, gr["dW_router"], wsd, stream=stream)
+            b.record(stream)
+        torch.cuda.synchronize()
+        msd = median([a.elapsed_time(b) for a, b in evd])
         out["backward"] = {
             "ms_per_step": round(msg, 3), "steps": stepsg, "over_forward": round(msg / ms_event, 2),
+            "diversity_loss_ms": round(msd, 4), "diversity_loss": round(float(lossd.item()), 6),
             "algorithmic_tflop": round(bflops / 1e12, 4),
             "achieved_tflops": round(bflops / (msg / 1e3) / 1e12, 2),
             "workspace_gb": round(wsg.numel() / 1e9, 2)}
-        del wsg, gr, dYd
+        del wsg, gr, dYd, wsd
         torch.cuda.empty_cache()
     if args.vendor_reference:
         print("[bench] vendor reference GEMMs", file=sys.stderr, flush=True)
