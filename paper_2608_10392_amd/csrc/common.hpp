@@ -17,10 +17,16 @@ constexpr int kWave = 64;
 constexpr int kExpCopies = 16;
 // Copies of each (expert, mask key) bin of the pair sort: token tile q counts
 // its pairs and takes their slots in copy q % kBinCopies, so that no counter
-// sees more than a share of its bin's atomics (same-address atomics serialize
-// at the device's coherence point); a bin's slots are its copies' ranges in
-// copy order.
+// sees more than a share of its bin's atomics (atomics on one cache line
+// serialize at the L2); a bin's slots are its copies' ranges in copy order.
 constexpr int kBinCopies = 8;
+
+// The counter of copy c of bin `bin` among nbin bins: the copies of a bin lie
+// nbin counters apart, on different cache lines (and L2 channels), so a bin
+// that many pairs share spreads its atomics over kBinCopies lines.
+__host__ __device__ __forceinline__ size_t bin_counter(int bin, int c, int nbin) {
+    return (size_t)c * (size_t)nbin + (size_t)bin;
+}
 
 __device__ __forceinline__ float bf2f(u16 v) { return __uint_as_float(((uint32_t)v) << 16); }
 

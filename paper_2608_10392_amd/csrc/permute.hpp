@@ -41,8 +41,8 @@ struct PermuteParams {
     const uint64_t* mask;
     const int* nres;
     const int* eids;
-    const int* bin_count;
-    int* bin_cursor;
+    const int* bin_count;   // [kBinCopies][(K+1) << key_bits] (bin_counter)
+    int* bin_cursor;        // [(K+1) << key_bits][kBinCopies]
     int* slab_count;    // [nslab] rows per slab (the scan's column sums)
     int* slab_off;      // [nslab + 1] first entry of each slab in the row lists (bf16)
     int* tile_cnt;      // [ntile][nslab + K + 1] per-tile counts; the scan turns each slab column into
@@ -221,11 +221,13 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
             p.totals[4] = run;
         }
     }
-    // Expert b's bins, each as kBinCopies consecutive counters.
-    const int base = segs[b];
+    // Expert b's bins in key order, each bin's copies in copy order; the
+    // cursors keep this order (a bin's kBinCopies cursors are consecutive).
+    const int base = segs[b], nbin = K1 * nb;
     const size_t off = (size_t)b * nb * kBinCopies;
     staged_exclusive_scan(
-        nb * kBinCopies, [&](int i) { return p.bin_count[off + i]; },
+        nb * kBinCopies,
+        [&](int i) { return p.bin_count[bin_counter(b * nb + i / kBinCopies, i % kBinCopies, nbin)]; },
         [&](int i, int v) { p.bin_cursor[off + i] = base + v; }, stage, lds);
 }
 

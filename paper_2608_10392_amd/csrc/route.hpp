@@ -44,7 +44,7 @@ struct RouteParams {
     int* nres;
     int* eids;
     float* wts;
-    int* bin_count;   // [(K+1) << key_bits][kBinCopies] pairs per (expert, mask key), or null
+    int* bin_count;   // [kBinCopies][(K+1) << key_bits] pairs per (expert, mask key), or null
     int* tile_cnt;    // [ceil(N / kTileTok)][(K+1) B + K+1]: per tile of tokens, rows per (expert, block)
                       // slab, then pairs per expert; or null
     int* exp_total;   // [kExpCopies][K+1] pairs per expert (tile i adds into copy i % kExpCopies)
@@ -355,10 +355,10 @@ __device__ __forceinline__ void decide_group(const RouteParams& p, const float* 
     const uint64_t full = (B == 64) ? ~0ull : ((1ull << B) - 1ull);
     const int kb = p.key_bits;
     const int ks = mask_key(mask, B, kb), kr = mask_key(~mask & full, B, kb);
-    const int bc = (tok / kTileTok) % kBinCopies;
+    const int bc = (tok / kTileTok) % kBinCopies, nbin = (K + 1) << kb;
     int* rank = p.pair_rank + (size_t)(v ? tok : 0) * (K + 1);
-    if (v && j == 0) rank[0] = atomicAdd(&p.bin_count[ks * kBinCopies + bc], 1);
-    if (v && j < k) rank[1 + j] = atomicAdd(&p.bin_count[((qs << kb) + kr) * kBinCopies + bc], 1);
+    if (v && j == 0) rank[0] = atomicAdd(&p.bin_count[bin_counter(ks, bc, nbin)], 1);
+    if (v && j < k) rank[1 + j] = atomicAdd(&p.bin_count[bin_counter((qs << kb) + kr, bc, nbin)], 1);
     if (cnt == nullptr) return;
     // The tile's counts: pairs per expert, and rows per slab (the shared
     // expert on I_shr, each selected residual expert on I_res). Lane c adds
