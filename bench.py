@@ -73,18 +73,20 @@ def parse():
 
 def phase_bytes(cfg, st):
     """Algorithmic HBM bytes of the non-GEMM phases (minimum traffic of each
-    step as defined, not counter readings)."""
+    step as defined, not counter readings). The fp16 copy of W_down (bf16
+    layers) is made by extra workgroups of the routing decisions' launch, so
+    its bytes belong to the routing phase."""
     N, d, K, H = cfg["n_tokens"], cfg["d_model"], cfg["n_experts"], cfg["n_blocks"] * cfg["block_width"]
     nv, sum_k, sum_cb = st["n_valid"], st["mean_k"] * st["n_valid"], st["activated_blocks"]
     pairs = nv + sum_k
     es = 2 if cfg["dtype"] == "bf16" else 4
     wdown = (K + 1) * d * H * (2 + 2) if cfg["dtype"] == "bf16" else 0   # read bf16, write fp16
-    routing = N * d * es + N * (4 + 4 + 8 + 4 + 8 * K)             # read X, write the record
+    routing = N * d * es + N * (4 + 4 + 8 + 4 + 8 * K) + wdown       # read X, write the record; the copy
     permute = (N * (8 + 4) + sum_k * 4                               # read mask, k, q_1..q_k
                + pairs * (4 + 8 + 4 + 4)                             # pair token/mask/expert, pair_of
                + sum_cb * 8)                                         # slab lists: pair and token per row
     combine = pairs * d * 4 + pairs * 8 + N * 4 + N * d * es         # fp32 per-expert rows, weights, Y
-    return dict(wdown_f16=wdown, routing=routing, permute=permute, combine=combine)
+    return dict(routing=routing, permute=permute, combine=combine)
 
 
 COUNTERS_PROFILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",

@@ -85,20 +85,6 @@ __global__ void combine_bf16_kernel(CombineParams c) {
     __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(static_cast<u16*>(c.Y) + (size_t)t * c.d + ch * 8));
 }
 
-// W_down (bf16) -> fp16 values for the down-projection's fp16 products: n
-// 8-element chunks, grid-stride. Each value is rounded to nearest even
-// (exact for bf16 magnitudes in [2^-17, 65504]; larger ones become
-// infinities).
-__global__ void bf16_to_f16_kernel(const u16* __restrict__ src, u16* __restrict__ dst, size_t n) {
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
-        const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + i);
-        u32x4 o;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = pack_f16x2(__uint_as_float(v[q] << 16), __uint_as_float(v[q] & 0xffff0000u));
-        reinterpret_cast<u32x4*>(dst)[i] = o;
-    }
-}
-
 // fp32: one thread per output element.
 __global__ void combine_f32_kernel(CombineParams c) {
     const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;

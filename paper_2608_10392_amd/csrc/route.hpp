@@ -49,7 +49,39 @@ struct RouteParams {
                       // slab, then pairs per expert; or null
     int* exp_total;   // [kExpCopies][K+1] pairs per expert (tile i adds into copy i % kExpCopies)
     int* pair_rank;   // [N][K+1]: slot of each pair within its bin copy
+    // Copy job carried by the decisions launch (forward of bf16 layers): the
+    // last cvt_blocks workgroups convert cvt_n8 16-byte chunks of bf16 at
+    // cvt_src to fp16 at cvt_dst (bf16_to_f16_chunks). The decisions are
+    // bound by latency and leave HBM bandwidth idle, which the copy uses.
+    const u16* cvt_src;
+    u16* cvt_dst;
+    size_t cvt_n8;
+    int cvt_blocks;
 };
+
+// bf16 -> fp16 of chunks [i0, n8) with stride `stride` (16-byte chunks of 8
+// values). Each value is rounded to nearest even (exact for bf16 magnitudes
+// in [2^-17, 65504]; larger ones become infinities).
+__device__ __forceinline__ void bf16_to_f16_chunks(const u16* __restrict__ src, u16* __restrict__ dst, size_t n8,
+                                                   size_t i0, size_t stride) {
+    for (size_t i = i0; i < n8; i += stride) {
+        const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + i);
+        u32x4 o;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = pack_f16x2(__uint_as_float(v[q] << 16), __uint_as_float(v[q] & 0xffff0000u));
+        reinterpret_cast<u32x4*>(dst)[i] = o;
+    }
+}
+
+// The copy role of a routing launch: true (after doing its share of the
+// copy) for the last p.cvt_blocks workgroups of the grid.
+__device__ __forceinline__ bool route_copy_role(const RouteParams& p) {
+    const int first = (int)gridDim.x - p.cvt_blocks;
+    if ((int)blockIdx.x < first) return false;
+    bf16_to_f16_chunks(p.cvt_src, p.cvt_dst, p.cvt_n8, (size_t)(blockIdx.x - first) * blockDim.x + threadIdx.x,
+                       (size_t)p.cvt_blocks * blockDim.x);
+    return true;
+}
 
 // Exact three-way split of an fp32 value into bf16 parts, in workgroups
 // [0, nsplit); the workgroups after them zero zwords words at zero (the
@@ -419,10 +451,11 @@ __device__ __forceinline__ void decide_tile_any(const RouteParams& p, const floa
 // NCT: 16-column logit tiles of the bf16 path (1 + K + B <= 16 NCT); 0 for
 // fp32 tokens. One workgroup of 4 waves per kRouteTok tokens (two tiles):
 // the logits of all of them, then the two tiles' decisions, all 4 waves on
-// each tile.
+// each tile. The last p.cvt_blocks workgroups do the launch's copy job.
 template <int NCT>
 __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteParams p) {
     constexpr int NT = kRouteTok / kTileTok;
+    if (route_copy_role(p)) return;
     extern __shared__ float lds_route[];
     float* L = lds_route;
     int* cnt = reinterpret_cast<int*>(L + kRouteTok * p.lstride);   // [NT][ncnt]
@@ -570,10 +603,12 @@ __global__ __launch_bounds__(kRpThreads) void route_logits_kernel(RouteParams p,
 // Decisions of one 64-token tile per workgroup of 4 waves (L lanes per
 // token, see decide_lanes), from the logits route_logits_kernel wrote (ncols
 // per token), staged in LDS rows; then the tile's counters out to memory.
+// The last p.cvt_blocks workgroups do the launch's copy job instead.
 constexpr int kDecideThreads = 256;
 template <int L>
 __global__ __launch_bounds__(kDecideThreads) void route_decide_kernel(RouteParams p, const float* __restrict__ logits,
                                                                       int ncols) {
+    if (route_copy_role(p)) return;
     extern __shared__ float lds_dec[];
     const int ls = p.lstride;
     float* rows = lds_dec;                                       // [64][ls]

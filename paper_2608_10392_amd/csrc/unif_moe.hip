@@ -4,12 +4,13 @@
 //
 // Forward launch sequence (all asynchronous on the caller's stream, no
 // device-to-host traffic):
-//   bf16_to_f16      W_down -> fp16 copy for the down-projection (bf16 only)
 //   split_router     fp32 router + prototypes -> 3 bf16 parts (bf16 only);
 //                    the same launch clears the counters and tile queues
 //   route_logits +   logits with the router held in registers, then the
 //   route_decide     decisions, bin slots and per-tile counts (bf16 routers
-//                    of at most 32 columns); otherwise one fused route kernel
+//                    of at most 32 columns); otherwise one fused route kernel;
+//                    extra workgroups of the decisions' launch make the fp16
+//                    copy of W_down for the down-projection (bf16 only)
 //   scan             segment offsets, bin cursors, per-slab first rows
 //   scatter          pairs (expert segments sorted by block-mask key), the
 //                    per-(expert, block) row lists in token order and the
@@ -384,6 +385,10 @@ RouteParams route_params(const unif_moe_config* c, const Dims& m, const void* X,
     r.tile_cnt = nullptr;
     r.exp_total = nullptr;
     r.pair_rank = nullptr;
+    r.cvt_src = nullptr;
+    r.cvt_dst = nullptr;
+    r.cvt_n8 = 0;
+    r.cvt_blocks = 0;
     return r;
 }
 
@@ -425,7 +430,7 @@ int32_t launch_route(const Dims& m, const RouteParams& rp, const float* Wr, cons
         if (allow_lds(lk, l1) != UNIF_OK || allow_lds(dk, l2) != UNIF_OK) return UNIF_EDEVICE;
         lk<<<std::min(cu_count(), ntiles), kRpThreads, l1, st>>>(rp, logits);
         UNIF_LAUNCH_CHECK();
-        dk<<<ntiles, kDecideThreads, l2, st>>>(rp, logits, ncols);
+        dk<<<ntiles + rp.cvt_blocks, kDecideThreads, l2, st>>>(rp, logits, ncols);
         UNIF_LAUNCH_CHECK();
         return UNIF_OK;
     }
@@ -446,7 +451,7 @@ int32_t launch_route(const Dims& m, const RouteParams& rp, const float* Wr, cons
         }
     }
     if (allow_lds(kern, lds) != UNIF_OK) return UNIF_EDEVICE;
-    kern<<<grid, kRouteThreads, lds, st>>>(rp);
+    kern<<<grid + rp.cvt_blocks, kRouteThreads, lds, st>>>(rp);
     UNIF_LAUNCH_CHECK();
     return UNIF_OK;
 }
@@ -589,16 +594,9 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     int* totals = reinterpret_cast<int*>(ws + plan.totals);
 
     UNIF_MARK(0);
-    // 0. the fp16 copy of W_down that the down-projection multiplies with
-    const u16* wdown16 = nullptr;
-    if (m.bf16 && !tables_only) {
-        const size_t n8 = (size_t)m.K1 * m.d * m.H / 8;
-        u16* dst = reinterpret_cast<u16*>(ws + plan.wdown16);
-        const unsigned g = (unsigned)std::min<size_t>((n8 + 255) / 256, (size_t)cu_count() * 8);
-        bf16_to_f16_kernel<<<g, 256, 0, st>>>(static_cast<const u16*>(W_down), dst, n8);
-        UNIF_LAUNCH_CHECK();
-        wdown16 = dst;
-    }
+    // 0. the fp16 copy of W_down that the down-projection multiplies with:
+    // made by extra workgroups of the routing decisions' launch (step 2)
+    const u16* wdown16 = (m.bf16 && !tables_only) ? reinterpret_cast<u16*>(ws + plan.wdown16) : nullptr;
     UNIF_MARK(1);
     // 1. the FFN input: LN(X) for a pre-LN block, else X
     const void* Xf = X;
@@ -627,6 +625,12 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     rp.tile_cnt = reinterpret_cast<int*>(ws + plan.tile_cnt);
     rp.exp_total = reinterpret_cast<int*>(ws + plan.exp_total);
     rp.pair_rank = reinterpret_cast<int*>(ws + plan.pair_rank);
+    if (wdown16 != nullptr) {
+        rp.cvt_src = static_cast<const u16*>(W_down);
+        rp.cvt_dst = reinterpret_cast<u16*>(ws + plan.wdown16);
+        rp.cvt_n8 = (size_t)m.K1 * m.d * m.H / 8;
+        rp.cvt_blocks = (int)std::min<size_t>(ceil_div_sz(rp.cvt_n8, 256), (size_t)cu_count() * 2);
+    }
     s = launch_route(m, rp, W_router, prototypes, wsplit, reinterpret_cast<float*>(ws + plan.logits), st,
                      reinterpret_cast<uint32_t*>(ws + plan.zero_begin), zwords);
     if (s != UNIF_OK) return s;
