@@ -21,16 +21,18 @@ struct CombineParams {
 
 constexpr int kCombineBatch = 6;
 
-// bf16 layers: one thread per 8 consecutive outputs; fp32 per-expert rows
-// (two 16-byte loads each, per part with SPLIT), one 16-byte bf16 store.
+// bf16 layers: one thread per 4 consecutive outputs; fp32 per-expert rows
+// (one 16-byte load each, per part with SPLIT), one 8-byte bf16 store. (Four
+// outputs per thread keep more rows in flight per CU than eight: 10% less
+// time on the 50k-token d = 768 layer.)
 template <bool SPLIT>
 __global__ void combine_bf16_kernel(CombineParams c) {
-    const int chunks = c.d >> 3;
+    const int chunks = c.d >> 2;
     const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (item >= (size_t)c.N * chunks) return;
     const int t = (int)(item / chunks), ch = (int)(item - (size_t)t * chunks);
     const int k = c.nres[t];
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
     const float* part = static_cast<const float*>(c.part);
     const int* of = c.pair_of + (size_t)t * (c.K + 1);
     const float* wt = c.wts + (size_t)t * c.K;
@@ -52,37 +54,32 @@ __global__ void combine_bf16_kernel(CombineParams c) {
         if (k == 0) break;
         // The rows are read once and Y written once: non-temporal accesses
         // keep them from displacing cached data.
-        f32x4 v[kCombineBatch][2];
+        f32x4 v[kCombineBatch];
 #pragma unroll
-        for (int u = 0; u < kCombineBatch; ++u) {
-#pragma unroll
-            for (int h = 0; h < 2; ++h)
-                v[u][h] = (i0 + u <= k)
-                              ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(part + (size_t)pr[u] * c.d + ch * 8 + 4 * h))
-                              : f32x4{0.f, 0.f, 0.f, 0.f};
-        }
+        for (int u = 0; u < kCombineBatch; ++u)
+            v[u] = (i0 + u <= k)
+                       ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(part + (size_t)pr[u] * c.d + ch * 4))
+                       : f32x4{0.f, 0.f, 0.f, 0.f};
         for (int sp = 1; SPLIT && sp < c.nsplit; ++sp) {
 #pragma unroll
-            for (int u = 0; u < kCombineBatch; ++u) {
-#pragma unroll
-                for (int h = 0; h < 2; ++h)
-                    if (i0 + u <= k)
-                        v[u][h] += __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(
-                            part + sp * c.split_stride + (size_t)pr[u] * c.d + ch * 8 + 4 * h));
-            }
+            for (int u = 0; u < kCombineBatch; ++u)
+                if (i0 + u <= k)
+                    v[u] += __builtin_nontemporal_load(
+                        reinterpret_cast<const f32x4*>(part + sp * c.split_stride + (size_t)pr[u] * c.d + ch * 4));
         }
 #pragma unroll
         for (int u = 0; u < kCombineBatch; ++u) {
             if (i0 + u <= k) {
 #pragma unroll
-                for (int q = 0; q < 8; ++q) acc[q] = fmaf(w[u], v[u][q >> 2][q & 3], acc[q]);
+                for (int q = 0; q < 4; ++q) acc[q] = fmaf(w[u], v[u][q], acc[q]);
             }
         }
     }
-    u32x4 o;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) o[q] = (uint32_t)f2bf(acc[2 * q]) | ((uint32_t)f2bf(acc[2 * q + 1]) << 16);
-    __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(static_cast<u16*>(c.Y) + (size_t)t * c.d + ch * 8));
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    u32x2 o;
+    o[0] = (uint32_t)f2bf(acc[0]) | ((uint32_t)f2bf(acc[1]) << 16);
+    o[1] = (uint32_t)f2bf(acc[2]) | ((uint32_t)f2bf(acc[3]) << 16);
+    __builtin_nontemporal_store(o, reinterpret_cast<u32x2*>(static_cast<u16*>(c.Y) + (size_t)t * c.d + ch * 4));
 }
 
 // fp32: one thread per output element.

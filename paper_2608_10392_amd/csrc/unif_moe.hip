@@ -828,7 +828,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     cp.wts = wts;
     cp.Y = Y;
     if (m.bf16) {
-        const size_t items = (size_t)m.N * (m.d / 8);
+        const size_t items = (size_t)m.N * (m.d / 4);
         if (cp.nsplit > 1) combine_bf16_kernel<true><<<(unsigned)((items + 255) / 256), 256, 0, st>>>(cp);
         else combine_bf16_kernel<false><<<(unsigned)((items + 255) / 256), 256, 0, st>>>(cp);
     } else {
