@@ -107,7 +107,7 @@ struct DownParams {
     const uint64_t* pair_mask;   // readable for a whole tile past the last pair
     const int* totals;           // [2]: down tiles (row tiles x column tiles)
     int* queue;                  // 8 per-XCD tile counters, zero at launch
-    int nsplit;                  // parts each tile's block union is split into (1: none)
+    int nsplit;                  // parts each tile's block union is split into by block index mod nsplit (1: none)
     size_t split_stride;         // floats between the parts' row buffers in part
 };
 
@@ -580,8 +580,12 @@ void down_kernel(DownParams p) {
     // share its H rows in L2), row tiles expert by expert; gm[i]: the block
     // mask of this wave's 32-row group i, all: the tile's.
     // With nsplit > 1, tile t is part t % nsplit of row-and-column tile
-    // t / nsplit: every nsplit-th block of the union, in order, written to
-    // that part's row buffer (the merge adds the parts in order).
+    // t / nsplit: the blocks c of the union with c % nsplit equal to the
+    // part, in order, written to that part's row buffer (the merge adds the
+    // parts in order). A row's part sums then cover a fixed set of its own
+    // blocks, whichever rows share its tile (the order of pairs inside a
+    // mask-key bin follows the arrival of atomics), so the result does not
+    // depend on the tile's composition.
     struct Desc {
         int p0, nrows, e, ct, nst, nreal, sp;
         uint64_t all, gm[RG];
@@ -599,10 +603,9 @@ void down_kernel(DownParams p) {
         const uint64_t* ms = p.rt_masks + (size_t)rt * (TM / 32 + 1);
         D.all = ld_uniform64(ms + TM / 32);
         if (p.nsplit > 1) {
-            uint64_t keep = 0, rem = D.all;
-            for (int i = 0; rem; ++i, rem &= rem - 1)
-                if (i % p.nsplit == D.sp) keep |= rem & (0ull - rem);
-            D.all = keep;
+            uint64_t keep = 0;
+            for (int c = D.sp; c < 64; c += p.nsplit) keep |= 1ull << c;
+            D.all &= keep;
         }
 #pragma unroll
         for (int i = 0; i < RG; ++i) D.gm[i] = ld_uniform64(ms + wm * RG + i);

@@ -61,15 +61,26 @@ struct RouteParams {
 
 // bf16 -> fp16 of chunks [i0, n8) with stride `stride` (16-byte chunks of 8
 // values). Each value is rounded to nearest even (exact for bf16 magnitudes
-// in [2^-17, 65504]; larger ones become infinities).
+// in [2^-17, 65504]; larger ones become infinities). Four chunks per pass are
+// loaded before any is converted, so each thread keeps four loads in flight.
 __device__ __forceinline__ void bf16_to_f16_chunks(const u16* __restrict__ src, u16* __restrict__ dst, size_t n8,
                                                    size_t i0, size_t stride) {
-    for (size_t i = i0; i < n8; i += stride) {
-        const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + i);
-        u32x4 o;
+    constexpr int U = 4;
+    for (size_t i = i0; i < n8; i += U * stride) {
+        u32x4 v[U];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = pack_f16x2(__uint_as_float(v[q] << 16), __uint_as_float(v[q] & 0xffff0000u));
-        reinterpret_cast<u32x4*>(dst)[i] = o;
+        for (int u = 0; u < U; ++u)
+            if (i + u * stride < n8) v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + i + u * stride);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (i + u * stride < n8) {
+                u32x4 o;
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    o[q] = pack_f16x2(__uint_as_float(v[u][q] << 16), __uint_as_float(v[u][q] & 0xffff0000u));
+                reinterpret_cast<u32x4*>(dst)[i + u * stride] = o;
+            }
+        }
     }
 }
 
