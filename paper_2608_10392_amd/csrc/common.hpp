@@ -72,19 +72,21 @@ __device__ __forceinline__ float gelu_erf(float a) {
 
 // GELU(a) = a Phi(a) = a / 2 + |a| (1/2 - Phi(-|a|)), with Phi(-y) = 2^Q(y) and
 // Q(y) = log2 Phi(-y) replaced by a degree-7 polynomial fitted on [0, 6]
-// (gelu_coeffs.py prints kGeluQ), evaluated at min(|a|, 6): one exp2 and
-// eleven other vector instructions. In fp32 the error is below 1e-5 |GELU(a)|
-// + 3e-8 |a| for |a| < 6 (the second term, from rounding 1/2 - Phi(-|a|),
-// matters only in the far negative tail) and below 5e-7 everywhere (|a|
-// Phi(-6) bounds it past 6); used where the result is rounded to bf16
-// (relative spacing 2^-8), far above that.
+// (gelu_coeffs.py prints kGeluQ), evaluated at |a|: one exp2 and ten other
+// vector instructions. Past the fit range the polynomial keeps falling
+// (Q(6) = -29.9, its leading coefficient is negative, and in fp32 it reaches
+// -inf for huge |a|), so 2^Q stays below 2^-29.9 there, as Phi(-|a|) does.
+// In fp32 the error is below 1e-5 |GELU(a)| + 3e-8 |a| for |a| < 6 (the
+// second term, from rounding 1/2 - Phi(-|a|), matters only in the far
+// negative tail) and below 5e-7 everywhere (|a| 2^-29.9 bounds it past 6);
+// used where the result is rounded to fp16 (relative spacing 2^-11), far
+// above that.
 constexpr float kGeluQ[8] = {-9.999869466e-01f, -1.151324511e+00f, -4.582976401e-01f, -5.411815643e-02f,
                              8.582305163e-03f,  -9.488553624e-04f, 6.385870802e-05f,  -1.944835731e-06f};
 constexpr float kGeluQMax = 6.0f;
 __device__ __forceinline__ float gelu_exp2poly(float a) {
-    // med3(|a|, 0, Y) = min(|a|, Y) in one instruction (fminf would first
-    // quiet a signalling NaN); a NaN input still yields NaN through the fma.
-    const float y = __builtin_amdgcn_fmed3f(fabsf(a), 0.0f, kGeluQMax);
+    // |a| is a source modifier of the first fma; a NaN input yields NaN.
+    const float y = fabsf(a);
     float q = fmaf(kGeluQ[7], y, kGeluQ[6]);
     q = fmaf(q, y, kGeluQ[5]);
     q = fmaf(q, y, kGeluQ[4]);

@@ -35,8 +35,9 @@ def fma32(a, b, c):
 
 
 def gelu_kernel(x, c, ymax):
+    """gelu_exp2poly in fp32 steps: Q evaluated at |x| (no clamp)."""
     x = f32(x)
-    y = np.minimum(np.abs(x), ymax)
+    y = np.abs(x)
     q = fma32(c[7], y, c[6])
     for i in range(5, -1, -1):
         q = fma32(q, y, c[i])
@@ -75,6 +76,21 @@ def test_error_bounds():
     # GELU(0) = 0 and the signs of the two branches.
     assert gelu_kernel(np.array([0.0]), c, ymax)[0] == 0.0
     assert (got[x > 0] > 0).all() and (got[x < 0] <= 0).all()
+
+
+def test_polynomial_falls_past_the_fit_range():
+    """The forward evaluates Q at |x| without clamping: past the fit range
+    the fp32 Horner value must stay at or below Q(Y) (so 2^Q <= Phi(-Y)-sized
+    values) and reach -inf for huge |x|."""
+    c, ymax = header_coefficients()
+    y = f32(np.concatenate([np.linspace(ymax, 200.0, 200001), np.geomspace(200.0, 3e38, 4000)]))
+    with np.errstate(over="ignore", invalid="ignore"):
+        q = fma32(c[7], y, c[6])
+        for i in range(5, -1, -1):
+            q = fma32(q, y, c[i])
+    assert (q <= q[0]).all() and q[0] < -29.0
+    assert np.all(np.diff(q[np.isfinite(q)]) <= 0)
+    assert q[-1] == -np.inf
 
 
 def test_infinities_and_nan():
