@@ -188,8 +188,10 @@ int32_t unif_moe_layer_forward(const unif_moe_config* cfg, const void* X, const 
  * result, and additionally records the caller's events (hipEvent_t handles,
  * created by the caller, recorded on `stream`) at the phase boundaries:
  *   events[0] before the first launch
- *   events[1] after the fp16 copy of W_down (bf16 path; else = events[0])
- *   events[2] after routing (split, route)
+ *   events[1] right after events[0] (kept for the layout of the array: the
+ *             fp16 copy of W_down runs inside the routing launches)
+ *   events[2] after routing (split, route, and the fp16 copy of W_down on
+ *             the bf16 path)
  *   events[3] after the permutation (scan, scatter, slab lists)
  *   events[4] after the up-projection
  *   events[5] after the down-projection
