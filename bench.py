@@ -425,6 +425,15 @@ def main():
         if k in head:
             out[k] = head[k]
     out["routing_stats"] = {k: head[k] for k in ("mean_b", "mean_k", "mean_cb", "activated_gemm_tflop")}
+    # Workspace of the timed forward (sized for the worst case, every token on
+    # all K experts) against one sized by the pair capacity cfg max_pairs for
+    # the pairs this routing produced (what a caller that knows its routing
+    # statistics allocates; unif_moe_forward_status reports an overflow).
+    _, pairs = _lib.forward_status(cfg, dev.ws_forward)
+    out["workspace_gb"] = {
+        "worst_case": round(_lib.layer_forward_workspace_size(cfg) / 1e9, 3),
+        "at_capacity": round(_lib.layer_forward_workspace_size(dict(cfg, max_pairs=pairs)) / 1e9, 3),
+        "pairs": pairs, "worst_case_pairs": cfg["n_tokens"] * (cfg["n_experts"] + 1)}
 
     if not args.no_paper_exact and cfg["mass_threshold"] != 1.0:
         # The same tokens and weights with the target exactly Eq. beta

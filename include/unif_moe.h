@@ -55,6 +55,8 @@ extern "C" {
 #define UNIF_EWORKSPACE   (-2) /* workspace smaller than the reported size       */
 #define UNIF_EDEVICE      (-3) /* a HIP launch or runtime call failed            */
 #define UNIF_EUNSUPPORTED (-4) /* valid layer the library does not implement   */
+#define UNIF_ECAPACITY    (-5) /* the routing needs more (token, expert) pairs
+                                  than cfg->max_pairs (unif_moe_forward_status) */
 
 /* Element type of X, W_up, W_down and Y. */
 #define UNIF_F32  0
@@ -97,6 +99,12 @@ typedef struct unif_moe_config {
     int32_t mass_mode;      /* UNIF_MASS_*                                         */
     int32_t fixed_k;        /* k in [1, K] when mass_mode == TOPK                  */
     int32_t select_mode;    /* UNIF_SELECT_*                                       */
+    int32_t max_pairs;      /* >= 0: capacity of the forward's workspace in (token,
+                               expert) pairs, sum over valid tokens of 1 + k; 0 (or
+                               at least N (K+1)) sizes it for the worst case
+                               N (K+1). Read by the forward entry points only (see
+                               unif_moe_layer_forward); the backward always sizes
+                               for the worst case.                                 */
 } unif_moe_config;
 
 /* Per-token routing record, device arrays written by the library. Residual
@@ -151,9 +159,13 @@ int32_t unif_moe_route(const unif_moe_config* cfg, const void* X, const uint8_t*
                        const unif_moe_routing* out, void* workspace, size_t workspace_bytes,
                        void* stream);
 
-/* Workspace needed by unif_moe_layer_forward (bytes). Host only. The size
- * covers the worst case (every token routed to all K residual experts), so
- * the forward never reads counts back to the host. */
+/* Workspace needed by unif_moe_layer_forward (bytes). Host only. With
+ * cfg->max_pairs = 0 the size covers the worst case (every token routed to
+ * all K residual experts), so the forward never reads counts back to the
+ * host; a capacity max_pairs > 0 sizes the pair-indexed buffers (the fp16
+ * activations, the per-expert rows, the pair and slab lists, the down-tile
+ * tables) for that many pairs instead, which shrinks the workspace by about
+ * N (K+1) / max_pairs for large layers. */
 int32_t unif_moe_layer_forward_workspace_size(const unif_moe_config* cfg, size_t* bytes);
 
 /* Forward pass of the layer: routing, token permutation, block-sparse expert
@@ -176,6 +188,12 @@ int32_t unif_moe_layer_forward_workspace_size(const unif_moe_config* cfg, size_t
  * not representable in fp16 and make the output infinite. The merge sums in
  * a fixed order (shared expert, then q_1..q_k), so repeated calls give
  * bitwise-identical Y.
+ * Capacity: when cfg->max_pairs > 0 and the routing of this call needs more
+ * (token, expert) pairs than that, the call still writes the routing record
+ * but runs no expert FFN and writes Y = 0; the overflow is detected on the
+ * device (nothing is read back) and reported afterwards by
+ * unif_moe_forward_status. The result never depends on the capacity
+ * otherwise.
  * Requires, for bf16: d % 128 == 0, M % 64 == 0, M <= 256; for fp32:
  * H = B M <= 16384. Otherwise UNIF_EUNSUPPORTED. */
 int32_t unif_moe_layer_forward(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
@@ -386,6 +404,16 @@ typedef struct unif_moe_work_t {
  * of unif_moe_layer_forward. */
 int32_t unif_moe_forward_work(const unif_moe_config* cfg, const void* workspace, size_t workspace_bytes,
                               unif_moe_work_t* host_out, void* stream);
+
+/* Outcome of the last forward (unif_moe_layer_forward, _profiled or
+ * unif_moe_block_forward) that used `workspace` with this cfg: UNIF_OK, or
+ * UNIF_ECAPACITY when its routing needed more pairs than cfg->max_pairs (its
+ * Y is then zero). *pairs_needed (host, may be NULL) receives the number of
+ * (token, expert) pairs that routing produced. Copies two words to the host
+ * and synchronises `stream`. Errors: UNIF_EINVAL, UNIF_EWORKSPACE,
+ * UNIF_EUNSUPPORTED, UNIF_EDEVICE, as unif_moe_layer_forward. */
+int32_t unif_moe_forward_status(const unif_moe_config* cfg, const void* workspace, size_t workspace_bytes,
+                                int64_t* pairs_needed, void* stream);
 
 /* Static text for a status code ("unknown status" for other values). */
 const char* unif_moe_status_string(int32_t status);

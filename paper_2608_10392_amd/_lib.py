@@ -12,7 +12,7 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libunifmoe.so")
 
-OK, EINVAL, EWORKSPACE, EDEVICE, EUNSUPPORTED = 0, -1, -2, -3, -4
+OK, EINVAL, EWORKSPACE, EDEVICE, EUNSUPPORTED, ECAPACITY = 0, -1, -2, -3, -4, -5
 DTYPES = {"f32": 0, "bf16": 1}
 ALPHA_MODES = {"adaptive": 0, "fixed": 1}
 MASS_MODES = {"coupled": 0, "fixed": 1, "topk": 2}
@@ -26,7 +26,8 @@ class Config(ctypes.Structure):
                 ("tau", ctypes.c_float), ("mass_threshold", ctypes.c_float),
                 ("max_shared", ctypes.c_int32), ("alpha_mode", ctypes.c_int32),
                 ("alpha_fixed", ctypes.c_float), ("mass_mode", ctypes.c_int32),
-                ("fixed_k", ctypes.c_int32), ("select_mode", ctypes.c_int32)]
+                ("fixed_k", ctypes.c_int32), ("select_mode", ctypes.c_int32),
+                ("max_pairs", ctypes.c_int32)]
 
 
 class Routing(ctypes.Structure):
@@ -60,7 +61,7 @@ EXPORTS = ("unif_moe_route_workspace_size", "unif_moe_route",
            "unif_moe_layer_backward", "unif_moe_stats_workspace_size",
            "unif_moe_stats", "unif_moe_layer_forward_static", "unif_moe_forward_work",
            "unif_moe_diversity_loss_workspace_size", "unif_moe_diversity_loss",
-           "unif_moe_status_string")
+           "unif_moe_forward_status", "unif_moe_status_string")
 N_PHASE_EVENTS = 7
 
 
@@ -109,6 +110,7 @@ def lib():
         L.unif_moe_layer_forward_static.argtypes = [cfgp, vp, vp, vp, vp, vp, vp, vp,
                                                     ctypes.POINTER(Routing), vp]
         L.unif_moe_forward_work.argtypes = [cfgp, vp, sz, ctypes.POINTER(Work), vp]
+        L.unif_moe_forward_status.argtypes = [cfgp, vp, sz, ctypes.POINTER(ctypes.c_int64), vp]
         L.unif_moe_diversity_loss_workspace_size.argtypes = [cfgp, ctypes.POINTER(sz)]
         L.unif_moe_diversity_loss.argtypes = [cfgp, vp, ctypes.c_float, vp, vp, vp, sz, vp]
         L.unif_moe_status_string.argtypes = [ctypes.c_int32]
@@ -138,7 +140,8 @@ def make_config(cfg):
         alpha_fixed=float(cfg.get("alpha_fixed", 0.0)),
         mass_mode=MASS_MODES[cfg.get("mass_mode", "coupled")],
         fixed_k=int(cfg.get("fixed_k", 1)),
-        select_mode=SELECT_MODES[cfg.get("select_mode", "prototype")])
+        select_mode=SELECT_MODES[cfg.get("select_mode", "prototype")],
+        max_pairs=int(cfg.get("max_pairs", 0) or 0))
 
 
 def _ptr(t):
@@ -339,3 +342,17 @@ def forward_work(cfg, workspace, stream=None):
     return dict(pairs=w.pairs, up_tiles=w.up_tiles, down_tiles=w.down_tiles,
                 up_mfma_flops=w.up_mfma_flops, down_mfma_flops=w.down_mfma_flops)
 
+
+
+def forward_status(cfg, workspace, stream=None):
+    """(status, pairs) of the last forward in ``workspace``
+    (unif_moe_forward_status): status is OK or ECAPACITY (the routing needed
+    more pairs than cfg's max_pairs); other codes raise."""
+    c = make_config(cfg)
+    n = ctypes.c_int64(0)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    s = lib().unif_moe_forward_status(ctypes.byref(c), _ptr(workspace), ws_bytes, ctypes.byref(n),
+                                      _stream(stream))
+    if s not in (OK, ECAPACITY):
+        _check(s, "unif_moe_forward_status")
+    return s, n.value

@@ -163,6 +163,7 @@ struct BlockCombineParams {
     const float* beta;
     double eps;
     void* Y;
+    const int* totals;      // totals[5] != 0: the routing overflowed the pair capacity (Y = 0)
 };
 
 constexpr int kBlockCombineBatch = 4;
@@ -251,7 +252,13 @@ __global__ __launch_bounds__(256) void combine_block_flat_kernel(BlockCombinePar
     if (item >= (size_t)c.N * nch) return;
     const int t = (int)(item / nch), ch = (int)(item - (size_t)t * nch);
     float z[E];
-    block_chunk_sum<BF16>(c, t, ch, z);
+    if (ld_uniform(c.totals + 5) != 0) {
+        // past the pair capacity no expert row exists: Y = 0
+#pragma unroll
+        for (int e = 0; e < E; ++e) z[e] = 0.f;
+    } else {
+        block_chunk_sum<BF16>(c, t, ch, z);
+    }
     // One rounding from fp32 (what f64_to_bf16 gives for an fp32 value).
     if constexpr (BF16) {
         u32x4 o;
@@ -275,6 +282,14 @@ __global__ __launch_bounds__(256) void combine_block_post_kernel(BlockCombinePar
     float* zrow = zrow_all + (size_t)w * c.d;
     const int lane = lane_id(), nch = c.d / E;
     char* yr = static_cast<char*>(c.Y) + (size_t)t * c.d * (BF16 ? 2 : 4);
+    if (ld_uniform(c.totals + 5) != 0) {
+        // past the pair capacity no expert row exists: Y = 0
+        double y0[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) y0[e] = 0.0;
+        for (int ch = lane; ch < nch; ch += kWave) store_chunk<BF16>(yr, ch, y0);
+        return;
+    }
     double s = 0.0;
     for (int ch = lane; ch < nch; ch += kWave) {
         float z[E];

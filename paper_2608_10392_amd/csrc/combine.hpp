@@ -17,6 +17,7 @@ struct CombineParams {
     const int* nres;
     const float* wts;
     void* Y;
+    const int* totals;     // totals[5] != 0: the routing overflowed the pair capacity (Y = 0)
 };
 
 constexpr int kCombineBatch = 6;
@@ -31,7 +32,8 @@ __global__ void combine_bf16_kernel(CombineParams c) {
     const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (item >= (size_t)c.N * chunks) return;
     const int t = (int)(item / chunks), ch = (int)(item - (size_t)t * chunks);
-    const int k = c.nres[t];
+    // past the pair capacity no expert row exists: Y = 0
+    const int k = ld_uniform(c.totals + 5) ? 0 : c.nres[t];
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
     const float* part = static_cast<const float*>(c.part);
     const int* of = c.pair_of + (size_t)t * (c.K + 1);
@@ -87,7 +89,7 @@ __global__ void combine_f32_kernel(CombineParams c) {
     const size_t item = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (item >= (size_t)c.N * c.d) return;
     const int t = (int)(item / c.d), j = (int)(item - (size_t)t * c.d);
-    const int k = c.nres[t];
+    const int k = ld_uniform(c.totals + 5) ? 0 : c.nres[t];   // past the pair capacity: Y = 0
     const float* part = static_cast<const float*>(c.part);
     float acc = 0.f;
     for (int i = 0; i <= k && k > 0; ++i) {

@@ -18,13 +18,13 @@ struct PairF32Params {
     const int* pair_token;
     const int* pair_expert;
     const uint64_t* pair_mask;
-    const int* totals;
+    const int* totals;   // [0] pairs, [5] nonzero: more pairs than the buffers hold (nothing to run)
     const float* b_up;   // [K+1][H] biases added before the GELU, or null
 };
 
 __global__ __launch_bounds__(256) void pair_ffn_f32_kernel(PairF32Params p) {
     extern __shared__ float g_act[];
-    const int P = p.totals[0];
+    const int P = p.totals[5] ? 0 : p.totals[0];
     for (int pr = blockIdx.x; pr < P; pr += gridDim.x) {
         const int e = p.pair_expert[pr], t = p.pair_token[pr];
         const uint64_t m = p.pair_mask[pr];

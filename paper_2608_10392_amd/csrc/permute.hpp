@@ -38,6 +38,7 @@ constexpr int kPermTok = 64;     // tokens per tile of the counts and the scatte
 
 struct PermuteParams {
     int N, K, B, key_bits, bm_up, bm_down, down_col_tiles, up_group, ntile;
+    int max_pairs;      // pairs the pair-indexed buffers hold (the workspace's capacity)
     const uint64_t* mask;
     const int* nres;
     const int* eids;
@@ -51,7 +52,7 @@ struct PermuteParams {
     const int* pair_rank;   // [N][K + 1] slot of each pair within its bin copy
     int* seg_off;
     int* down_tile_off;  // [K+2] first down row tile of each expert segment
-    int* totals;  // [0] pairs P, [1] up tiles, [2] down tiles, [4] down row tiles
+    int* totals;  // [0] pairs P, [1] up tiles, [2] down tiles, [4] down row tiles, [5] P > max_pairs
     int* pair_token;
     uint64_t* pair_mask;
     int* pair_expert;
@@ -216,9 +217,14 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(PermuteParams p) {
                 run += ceil_div(segs[x + 1] - segs[x], p.bm_down);
             }
             p.down_tile_off[K1] = run;
+            // More pairs than the buffers hold: no down tiles, and the flag
+            // that makes the scatter, the fp32 FFN and the merge stand down
+            // (the up tile count stays at its cleared 0).
+            const bool over = segs[K1] > p.max_pairs;
             p.totals[0] = segs[K1];
-            p.totals[2] = run * p.down_col_tiles;
-            p.totals[4] = run;
+            p.totals[2] = over ? 0 : run * p.down_col_tiles;
+            p.totals[4] = over ? 0 : run;
+            p.totals[5] = over ? 1 : 0;
         }
     }
     // Expert b's bins in key order, each bin's copies in copy order; the
@@ -403,6 +409,8 @@ __device__ __forceinline__ void scatter_tile(const PermuteParams& p, int q, cons
 // Workgroups [0, n_groups) build the up tile table of one (expert, block
 // group) each; the rest scatter one token tile each.
 __global__ __launch_bounds__(kScatterWaves * 64) void scatter_kernel(PermuteParams p, int n_groups) {
+    // Routing needed more pairs than the buffers hold: nothing to place.
+    if (ld_uniform(p.totals + 5) != 0) return;
     // LDS: slab and up tile offsets ([nslab + 1] each), then the role's
     // words: the tokens' pairs [64][K+1] and the tile's first rows [nslab],
     // or the up table's inputs.

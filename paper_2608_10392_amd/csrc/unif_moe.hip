@@ -86,6 +86,7 @@ static_assert(down_lds_bytes(128, 384) <= 160 * 1024 && down_lds_bytes(256, 256)
 
 struct Dims {
     int N, d, K, B, M, H, K1, NL, NLP, lstride, key_bits, nslab, nbin;
+    size_t pcap;   // (token, expert) pairs the forward's workspace holds (cfg max_pairs, else N (K+1))
     bool bf16;
     size_t elem;
     float tau, one_minus_2tau;
@@ -106,11 +107,19 @@ Dims dims_of(const unif_moe_config* c) {
     m.key_bits = m.B < kKeyBitsMax ? m.B : kKeyBitsMax;
     m.nslab = m.K1 * m.B;
     m.nbin = m.K1 << m.key_bits;
+    const size_t worst = (size_t)m.N * (size_t)m.K1;
+    m.pcap = (c->max_pairs > 0 && (size_t)c->max_pairs < worst) ? (size_t)c->max_pairs : worst;
     m.bf16 = c->dtype == UNIF_BF16;
     m.elem = m.bf16 ? 2 : 4;
     m.tau = std::isnan(c->tau) ? (float)((double)(m.B - 1) / ((double)m.B * (double)m.B)) : c->tau;
     m.one_minus_2tau = 1.0f - 2.0f * m.tau;
     return m;
+}
+
+// cfg without a pair capacity (workspaces sized for the worst case).
+unif_moe_config worst_case(unif_moe_config c) {
+    c.max_pairs = 0;
+    return c;
 }
 
 // Counters per tile of the permutation: rows per slab, then pairs per expert.
@@ -146,6 +155,7 @@ int32_t check_config(const unif_moe_config* c) {
     if (c == nullptr) return UNIF_EINVAL;
     if (c->n_tokens < 0 || c->d_model <= 0 || c->n_experts < 1 || c->n_blocks < 1 || c->block_width < 1)
         return UNIF_EINVAL;
+    if (c->max_pairs < 0) return UNIF_EINVAL;
     if (c->dtype != UNIF_F32 && c->dtype != UNIF_BF16) return UNIF_EINVAL;
     if (c->alpha_mode != UNIF_ALPHA_ADAPTIVE && c->alpha_mode != UNIF_ALPHA_FIXED) return UNIF_EINVAL;
     if (c->mass_mode != UNIF_MASS_COUPLED && c->mass_mode != UNIF_MASS_FIXED && c->mass_mode != UNIF_MASS_TOPK)
@@ -267,7 +277,7 @@ FwdPlan plan_forward(const Dims& m, size_t xn_bytes = 0) {
     Carver cv;
     FwdPlan p;
     const size_t N = (size_t)m.N, K = (size_t)m.K, K1 = (size_t)m.K1;
-    const size_t pmax = N * K1;
+    const size_t pmax = m.pcap;   // pairs the pair-indexed buffers hold
     p.alpha = cv.take(4 * N);
     p.nsh = cv.take(4 * N);
     p.mask = cv.take(8 * N);
@@ -298,10 +308,10 @@ FwdPlan plan_forward(const Dims& m, size_t xn_bytes = 0) {
     p.pair_expert = cv.take(4 * pmax);
     p.pair_of = cv.take(4 * N * K1);
     p.pair_rank = cv.take(4 * N * K1);
-    // Slab row lists: at most K B rows per token (b + k (B - b) <= K B), each
-    // slab padded to whole up tiles.
+    // Slab row lists: at most K B rows per token (b + k (B - b) <= K B) and
+    // at most B per pair, each slab padded to whole up tiles.
     const size_t tm = (size_t)up_tm(m.M, m.d);
-    const size_t up_tiles = ceil_div_sz(N * K * (size_t)m.B, tm) + (size_t)m.nslab;
+    const size_t up_tiles = ceil_div_sz(std::min(N * K, pmax) * (size_t)m.B, tm) + (size_t)m.nslab;
     p.slab_rows = cv.take(m.bf16 ? 4 * up_tiles * tm : 0);
     p.slab_tok = cv.take(m.bf16 ? 4 * up_tiles * tm : 0);
     p.up_tile_info = cv.take(m.bf16 ? 4 * up_tiles : 0);
@@ -471,6 +481,7 @@ const char* unif_moe_status_string(int32_t s) {
         case UNIF_EWORKSPACE: return "workspace too small";
         case UNIF_EDEVICE: return "HIP device error";
         case UNIF_EUNSUPPORTED: return "unsupported layer shape";
+        case UNIF_ECAPACITY: return "routing needs more pairs than the capacity";
         default: return "unknown status";
     }
 }
@@ -671,6 +682,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     pp.rt_masks = m.bf16 ? reinterpret_cast<uint64_t*>(ws + plan.rt_masks) : nullptr;
     pp.pair_rank = rp.pair_rank;
     pp.ntile = ceil_div(m.N, kTileTok);
+    pp.max_pairs = (int)m.pcap;
     // Expert segments and bin cursors; per slab (bf16), its rows per token
     // tile as first rows.
     scan_kernel<<<(unsigned)(m.K1 + (m.bf16 ? m.nslab : 0)), kScanThreads, 0, st>>>(pp);
@@ -704,7 +716,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         up.X = static_cast<const u16*>(Xf);
         up.Wup = static_cast<const u16*>(W_up);
         up.Hbuf = reinterpret_cast<u16*>(ws + plan.hbuf);
-        up.Hsink = up.Hbuf + (size_t)m.N * m.K1 * m.H;
+        up.Hsink = up.Hbuf + m.pcap * m.H;
         up.slab_rows = pp.slab_rows;
         up.slab_tok = pp.slab_tok;
         up.tile_info = pp.up_tile_info;
@@ -728,14 +740,14 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         dn.Hbuf = up.Hbuf;
         dn.Wdown = wdown16;
         dn.part = static_cast<float*>(part);
-        dn.part_sink = dn.part + (size_t)m.N * m.K1 * m.d;
+        dn.part_sink = dn.part + m.pcap * m.d;
         dn.rt_info = pp.rt_info;
         dn.rt_masks = pp.rt_masks;
         dn.pair_mask = pp.pair_mask;
         dn.totals = totals;
         dn.queue = reinterpret_cast<int*>(ws + plan.queues) + 8;
         dn.nsplit = down_splits(m);
-        dn.split_stride = ((size_t)m.N * m.K1 + 1) * m.d;
+        dn.split_stride = (m.pcap + 1) * m.d;
         if (dsh.bn == 384)
             s = launch_persistent(down_kernel<2, 3>, grid, (size_t)down_lds_bytes(128, 384), st, dn);
         else if (dsh.bn == 256)
@@ -773,7 +785,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     if (blk != nullptr) {
         BlockCombineParams bc;
         bc.nsplit = down_splits(m);
-        bc.split_stride = ((size_t)m.N * m.K1 + 1) * m.d;
+        bc.split_stride = (m.pcap + 1) * m.d;
         bc.N = m.N;
         bc.d = m.d;
         bc.K = m.K;
@@ -792,6 +804,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         bc.beta = blk->ln_beta;
         bc.eps = (double)blk->ln_eps;
         bc.Y = Y;
+        bc.totals = totals;
         if (!bc.post) {
             const int nch = m.bf16 ? m.d / 8 : m.d;
             const unsigned g = (unsigned)(((size_t)m.N * nch + 255) / 256);
@@ -817,7 +830,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     }
     CombineParams cp;
     cp.nsplit = down_splits(m);
-    cp.split_stride = ((size_t)m.N * m.K1 + 1) * m.d;
+    cp.split_stride = (m.pcap + 1) * m.d;
     cp.N = m.N;
     cp.d = m.d;
     cp.K = m.K;
@@ -827,6 +840,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     cp.nres = nres;
     cp.wts = wts;
     cp.Y = Y;
+    cp.totals = totals;
     if (m.bf16) {
         const size_t items = (size_t)m.N * (m.d / 4);
         if (cp.nsplit > 1) combine_bf16_kernel<true><<<(unsigned)((items + 255) / 256), 256, 0, st>>>(cp);
@@ -969,16 +983,19 @@ int32_t unif_moe_layer_backward_workspace_size(const unif_moe_config* cfg, size_
     if (bytes == nullptr) return UNIF_EINVAL;
     const int32_t s = check_backward_shape(cfg);
     if (s != UNIF_OK) return s;
-    *bytes = plan_backward(dims_of(cfg)).total;
+    const unif_moe_config cw = worst_case(*cfg);
+    *bytes = plan_backward(dims_of(&cw)).total;
     return UNIF_OK;
 }
 
-int32_t unif_moe_layer_backward(const unif_moe_config* cfg, const void* X, const uint8_t* valid,
+int32_t unif_moe_layer_backward(const unif_moe_config* cfg_in, const void* X, const uint8_t* valid,
                                 const float* W_router, const float* prototypes, const void* W_up,
                                 const void* W_down, const void* dY, float* dX, float* dW_up, float* dW_down,
                                 float* dW_router, void* workspace, size_t workspace_bytes, void* stream) {
-    int32_t s = check_backward_shape(cfg);
+    int32_t s = check_backward_shape(cfg_in);
     if (s != UNIF_OK) return s;
+    const unif_moe_config cfg_worst = worst_case(*cfg_in);   // the backward sizes for the worst case
+    const unif_moe_config* cfg = &cfg_worst;
     if (cfg->n_tokens > 0 && (X == nullptr || W_router == nullptr || prototypes == nullptr || W_up == nullptr ||
                               W_down == nullptr || dY == nullptr || dX == nullptr))
         return UNIF_EINVAL;
@@ -1324,6 +1341,29 @@ int32_t unif_moe_layer_forward_static(const unif_moe_config* cfg, const void* X,
 }  // extern "C"
 
 extern "C" {
+
+int32_t unif_moe_forward_status(const unif_moe_config* cfg, const void* workspace, size_t workspace_bytes,
+                                int64_t* pairs_needed, void* stream) {
+    int32_t s = check_config(cfg);
+    if (s != UNIF_OK) return s;
+    s = check_forward_shape(cfg);
+    if (s != UNIF_OK) return s;
+    size_t need = 0;
+    unif_moe_layer_forward_workspace_size(cfg, &need);
+    if (workspace == nullptr || workspace_bytes < need) return UNIF_EWORKSPACE;
+    if (pairs_needed != nullptr) *pairs_needed = 0;
+    const Dims m = dims_of(cfg);
+    if (m.N == 0) return UNIF_OK;
+    // The totals sit at the same offset in the layer's and the block's plans.
+    const FwdPlan plan = plan_forward(m);
+    const char* ws = align_base(const_cast<void*>(workspace));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    int32_t t[8];
+    if (hipMemcpyAsync(t, ws + plan.totals, sizeof(t), hipMemcpyDeviceToHost, st) != hipSuccess) return UNIF_EDEVICE;
+    if (hipStreamSynchronize(st) != hipSuccess) return UNIF_EDEVICE;
+    if (pairs_needed != nullptr) *pairs_needed = t[0];
+    return t[5] != 0 ? UNIF_ECAPACITY : UNIF_OK;
+}
 
 int32_t unif_moe_forward_work(const unif_moe_config* cfg, const void* workspace, size_t workspace_bytes,
                               unif_moe_work_t* host_out, void* stream) {

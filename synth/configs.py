@@ -16,12 +16,15 @@ Layer fields mirror the C structure ``unif_moe_config``:
                   alpha, Table mechanism-ablation).
   mass_mode       "coupled", "fixed" or "topk" (top-k residual activation).
   select_mode     "prototype" (Eq. shared-indices) or "prefix" (ablation).
+  max_pairs       capacity of the forward's workspace in (token, expert)
+                  pairs; 0 sizes it for the worst case N (K+1).
 """
 import copy
 
 _LAYER_DEFAULTS = dict(
     tau=None, mass_threshold=1.0, max_shared=None, alpha_mode="adaptive",
     alpha_fixed=0.0, mass_mode="coupled", fixed_k=1, select_mode="prototype",
+    max_pairs=0,
 )
 
 CONFIGS = {
@@ -82,7 +85,7 @@ for _c in CONFIGS.values():
 
 LAYER_KEYS = ("n_tokens", "d_model", "n_experts", "n_blocks", "block_width",
               "dtype", "tau", "mass_threshold", "max_shared", "alpha_mode",
-              "alpha_fixed", "mass_mode", "fixed_k", "select_mode")
+              "alpha_fixed", "mass_mode", "fixed_k", "select_mode", "max_pairs")
 
 
 def config_names():

@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 16, names
+    assert len(names) == 17, names
     assert set(names) == set(_lib.EXPORTS)
     out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True, text=True).stdout
     for n in names:
@@ -45,7 +45,7 @@ def test_struct_layout_matches_header(tmp_path):
         "int main(void) {\n"
         ' printf("config %zu\\nrouting %zu\\nstats %zu\\nblock %zu\\n", sizeof(unif_moe_config),'
         " sizeof(unif_moe_routing), sizeof(unif_moe_stats_t), sizeof(unif_moe_block));\n"
-        " F(unif_moe_config, tau); F(unif_moe_config, select_mode);"
+        " F(unif_moe_config, tau); F(unif_moe_config, select_mode); F(unif_moe_config, max_pairs);"
         " F(unif_moe_routing, weights); F(unif_moe_stats_t, expert_tokens);"
         " F(unif_moe_stats_t, activated_blocks); F(unif_moe_stats_t, routing_flops);\n"
         " F(unif_moe_block, ln_eps); F(unif_moe_block, ln_gamma); F(unif_moe_block, b_down);\n"
@@ -58,6 +58,7 @@ def test_struct_layout_matches_header(tmp_path):
     assert int(got["stats"]) == ctypes.sizeof(_lib.Stats)
     assert int(got["unif_moe_config.tau"]) == _lib.Config.tau.offset
     assert int(got["unif_moe_config.select_mode"]) == _lib.Config.select_mode.offset
+    assert int(got["unif_moe_config.max_pairs"]) == _lib.Config.max_pairs.offset
     assert int(got["unif_moe_routing.weights"]) == _lib.Routing.weights.offset
     assert int(got["unif_moe_stats_t.expert_tokens"]) == _lib.Stats.expert_tokens.offset
     assert int(got["unif_moe_stats_t.activated_blocks"]) == _lib.Stats.activated_blocks.offset
@@ -71,6 +72,7 @@ def test_struct_layout_matches_header(tmp_path):
 def test_status_strings(L):
     assert _lib.status_string(0) == "ok"
     assert _lib.status_string(-2) == "workspace too small"
+    assert _lib.status_string(_lib.ECAPACITY) == "routing needs more pairs than the capacity"
     assert _lib.status_string(12345) == "unknown status"
 
 
@@ -85,7 +87,7 @@ def base_cfg(**kw):
     dict(mass_threshold=0.0), dict(mass_threshold=1.5), dict(mass_threshold=math.nan),
     dict(max_shared=-1), dict(max_shared=17), dict(n_blocks=1, max_shared=1),
     dict(alpha_mode="fixed", alpha_fixed=1.5), dict(mass_mode="topk", fixed_k=0),
-    dict(mass_mode="topk", fixed_k=17), dict(tau=0.5), dict(tau=-0.1),
+    dict(mass_mode="topk", fixed_k=17), dict(tau=0.5), dict(tau=-0.1), dict(max_pairs=-1),
 ])
 def test_invalid_config_rejected(bad):
     with pytest.raises(_lib.UnifMoeError) as e:
@@ -278,3 +280,23 @@ def test_backward_needs_whole_column_groups():
         _lib.layer_backward_workspace_size(dict(ok, d_model=60))
     assert e.value.status == _lib.EUNSUPPORTED
     assert _lib.layer_forward_workspace_size(dict(ok, d_model=60)) > 0
+
+
+@pytest.mark.parametrize("name", ["vit_b16", "zipf_stress", "tiny_f32"])
+def test_capacity_sizes_the_forward_workspace(name):
+    """max_pairs sizes the pair-indexed buffers: the workspace shrinks with
+    the capacity (by the activations and per-expert rows of the pairs left
+    out), equals the worst case at or above N (K+1), and the backward's
+    workspace ignores it."""
+    c = layer_config(get_config(name))
+    N, d, K, H = c["n_tokens"], c["d_model"], c["n_experts"], c["n_blocks"] * c["block_width"]
+    worst = N * (K + 1)
+    full = _lib.layer_forward_workspace_size(c)
+    assert _lib.layer_forward_workspace_size(dict(c, max_pairs=worst)) == full
+    assert _lib.layer_forward_workspace_size(dict(c, max_pairs=worst + 12345)) == full
+    per_pair = d * 4 + (H * 2 if c["dtype"] == "bf16" else 0)   # per-expert row (+ fp16 activations)
+    sizes = [_lib.layer_forward_workspace_size(dict(c, max_pairs=p)) for p in (worst // 2, worst // 4, worst // 8)]
+    assert full > sizes[0] > sizes[1] > sizes[2]
+    assert full - sizes[0] >= (worst - worst // 2) * per_pair
+    if d % 8 == 0:   # a shape the backward takes
+        assert _lib.layer_backward_workspace_size(dict(c, max_pairs=1000)) == _lib.layer_backward_workspace_size(c)
