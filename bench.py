@@ -15,7 +15,7 @@ stream is reported beside it. Per-phase kernel durations come from HIP events
 the library records on the launch stream (unif_moe_layer_forward_profiled),
 medians over the steps. Prints one JSON line.
 
-    python bench.py [--steps 20] [--warmup 3] [--workload vit_b16] [--no-cpu-baseline]
+    python bench.py [--steps 50] [--warmup 3] [--workload vit_b16] [--no-cpu-baseline]
                     [--no-configs] [--no-paper-exact] [--no-block] [--no-backward]
                     [--no-ablations] [--vendor-reference]
 
@@ -51,7 +51,7 @@ OTHER_CONFIGS = ["vit_s16", "bert_base_padded", "zipf_stress", "paper_vision", "
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="vit_b16")
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -494,7 +494,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteParams p) {
 }
 
 // Logits of bf16 tokens when the router fits in registers (1 + K + B <= 32
-// columns, d <= 768), persistent: one workgroup of 8 waves takes the 64-token
+// columns, d <= 1024), persistent: one workgroup of 8 waves takes the 64-token
 // tiles blockIdx.x, blockIdx.x + gridDim.x, ... Wave w owns k steps
 // [w nks / 8, (w + 1) nks / 8) and keeps the router's three bf16 parts and
 // W_shr for them in registers for all its tiles, so only token rows stream

@@ -135,11 +135,11 @@ size_t route_logits_lds_bytes(const Dims& m) { return sizeof(float) * (size_t)kR
 size_t route_decide_lds_bytes(const Dims& m) {
     return sizeof(float) * ((size_t)kTileTok * m.lstride + tile_counters(m));
 }
-// Logits of the split routing path (bf16 routers of <= 32 columns, d <= 768):
+// Logits of the split routing path (bf16 routers of <= 32 columns, d <= 1024):
 // 1 + 16 NCT fp32 values per token, or 0 when the path does not apply.
 int split_route_cols(const Dims& m) {
     const int nct = m.NLP / 16, kpw = ceil_div(m.d / 32, kRpWaves);
-    return (m.bf16 && nct <= 2 && kpw <= 3) ? 1 + 16 * nct : 0;
+    return (m.bf16 && nct <= 2 && kpw <= 4) ? 1 + 16 * nct : 0;
 }
 // The scatter kernel: the tile's tokens' pairs per expert and its first row
 // in every slab, or the up tile table's inputs.
@@ -427,6 +427,8 @@ int32_t launch_route(const Dims& m, const RouteParams& rp, const float* Wr, cons
             case 9: lk = route_logits_kernel<2, 1>; break;
             case 10: lk = route_logits_kernel<2, 2>; break;
             case 11: lk = route_logits_kernel<2, 3>; break;
+            case 8: lk = route_logits_kernel<1, 4>; break;
+            case 12: lk = route_logits_kernel<2, 4>; break;
             default: return UNIF_EUNSUPPORTED;
         }
         void (*dk)(RouteParams, const float*, int) = nullptr;
