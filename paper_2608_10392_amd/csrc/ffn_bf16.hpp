@@ -88,11 +88,11 @@ struct UpParams {
     const int* totals;
     int* queue;              // 8 per-XCD tile counters, zero at launch
     const float* b_up;       // [K+1, H] fp32 biases added before the GELU (kEpiGeluBias only)
-    u16* Gbuf;               // kEpiDa: layout of Hbuf, with its own sink row Gsink
-    u16* Gsink;
+    u16* Gbuf;               // kEpiDa: layout of Hbuf (its sink row included)
     const float* pw;         // kEpiDa: weight of each pair
-    float* dcp;              // kEpiDa: [pairs, B, 2] partial sums (block, column half)
-    float* dcp_sink;         // kEpiDa: 2 floats for a tile's unused rows
+    float* dcp;              // kEpiDa: [pairs + 1, B, 2] partial sums (block, column half)
+    int sink_row;            // kEpiDa: the pair slot whose rows of Hbuf, Gbuf and dcp absorb a
+                             // tile's unused rows (Hsink's row)
 };
 
 struct DownParams {
@@ -402,7 +402,7 @@ void up_kernel(UpParams p) {
         // per 32-column group.
         const int sl = info & 0xffff, nrows = info >> 16;
         const int c = sl - (sl / p.B) * p.B;
-        if constexpr (EPI >= kEpiPre) {
+        if constexpr (EPI == kEpiPre) {
 #pragma unroll
             for (int i = 0; i < RG; ++i) {
                 const int r = wm * (TM / 4) + i * 32 + lr;
@@ -410,52 +410,72 @@ void up_kernel(UpParams p) {
                 const int pr = live ? rows[(par * 2 + 1) * TM + r] : 0;
                 const size_t off = (live ? (size_t)pr * p.H + (size_t)c * M : 0) + wn * (M / 2) + 16 * lh;
                 u16* ha = (live ? p.Hbuf : p.Hsink) + off;
-                if constexpr (EPI == kEpiPre) {
 #pragma unroll
-                    for (int j = 0; j < MG; ++j) {
-                        const f32x16 v = acc[i][j];
-                        u32x4 lo, hi;
+                for (int j = 0; j < MG; ++j) {
+                    const f32x16 v = acc[i][j];
+                    u32x4 lo, hi;
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        lo[t] = pack_f16x2(v[2 * t], v[2 * t + 1]);
+                        hi[t] = pack_f16x2(v[8 + 2 * t], v[9 + 2 * t]);
+                    }
+                    st16(ha + 32 * j, lo);
+                    st16(ha + 32 * j + 8, hi);
+                }
+            }
+        } else if constexpr (EPI == kEpiDa) {
+            // A row group's loads (a, the pair weight) are all issued before
+            // its first store: the wave's memory counter retires loads and
+            // stores in order, so a load issued after a store would also wait
+            // for that store. Unused rows go to the sink row of each buffer
+            // (one address formula for every lane). The lane's row and column
+            // offsets are derived here from an opaque copy of the lane index,
+            // so they are not kept in registers through the stage loop.
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+            const int elr = ln & 31, elh = ln >> 5;
+#pragma unroll
+            for (int i = 0; i < RG; ++i) {
+                const int r = wm * (TM / 4) + i * 32 + elr;
+                const bool live = r < nrows;
+                const int pr = live ? rows[(par * 2 + 1) * TM + r] : p.sink_row;
+                const size_t off = (size_t)pr * p.H + (size_t)c * M + wn * (M / 2) + 16 * elh;
+                u16* const hw = p.Hbuf + off;
+                u16* const hg = p.Gbuf + off;
+                const float w = live ? p.pw[pr] : 0.f;
+                u32x4 a4[MG][2];
+#pragma unroll
+                for (int j = 0; j < MG; ++j) {
+                    a4[j][0] = ld16(hw + 32 * j);
+                    a4[j][1] = ld16(hw + 32 * j + 8);
+                }
+                float dc = 0.f;
+#pragma unroll
+                for (int j = 0; j < MG; ++j) {
+                    const f32x16 v = acc[i][j];
+                    u32x4 wo[2], dq[2];
+#pragma unroll
+                    for (int h = 0; h < 2; ++h)
 #pragma unroll
                         for (int t = 0; t < 4; ++t) {
-                            lo[t] = pack_f16x2(v[2 * t], v[2 * t + 1]);
-                            hi[t] = pack_f16x2(v[8 + 2 * t], v[9 + 2 * t]);
+                            float a0, a1, e0, e1, g0, g1;
+                            unpack_f16x2(a4[j][h][t], a0, a1);
+                            gelu_exp2poly_grad(a0, e0, g0);
+                            gelu_exp2poly_grad(a1, e1, g1);
+                            const float v0 = v[8 * h + 2 * t], v1 = v[8 * h + 2 * t + 1];
+                            dc = fmaf(e0, v0, dc);
+                            dc = fmaf(e1, v1, dc);
+                            wo[h][t] = pack_bf16x2(w * e0, w * e1);
+                            dq[h][t] = pack_bf16x2(w * v0 * g0, w * v1 * g1);
                         }
-                        st16(ha + 32 * j, lo);
-                        st16(ha + 32 * j + 8, hi);
-                    }
-                } else {
-                    u16* hg = (live ? p.Gbuf : p.Gsink) + off;
-                    const float w = live ? p.pw[pr] : 0.f;
-                    float dc = 0.f;
-#pragma unroll
-                    for (int j = 0; j < MG; ++j) {
-                        const f32x16 v = acc[i][j];
-                        const u32x4 a4[2] = {ld16(ha + 32 * j), ld16(ha + 32 * j + 8)};
-                        u32x4 wo[2], dq[2];
-#pragma unroll
-                        for (int h = 0; h < 2; ++h)
-#pragma unroll
-                            for (int t = 0; t < 4; ++t) {
-                                float a0, a1, e0, e1, g0, g1;
-                                unpack_f16x2(a4[h][t], a0, a1);
-                                gelu_exp2poly_grad(a0, e0, g0);
-                                gelu_exp2poly_grad(a1, e1, g1);
-                                const float v0 = v[8 * h + 2 * t], v1 = v[8 * h + 2 * t + 1];
-                                dc = fmaf(e0, v0, dc);
-                                dc = fmaf(e1, v1, dc);
-                                wo[h][t] = pack_bf16x2(w * e0, w * e1);
-                                dq[h][t] = pack_bf16x2(w * v0 * g0, w * v1 * g1);
-                            }
-                        st16(ha + 32 * j, wo[0]);
-                        st16(ha + 32 * j + 8, wo[1]);
-                        st16(hg + 32 * j, dq[0]);
-                        st16(hg + 32 * j + 8, dq[1]);
-                    }
-                    // lanes l and l + 32 hold the two 16-column halves of a row
-                    dc += __shfl_xor(dc, 32);
-                    float* dd = live ? p.dcp + ((size_t)pr * p.B + c) * 2 + wn : p.dcp_sink + wn;
-                    if (lh == 0) *dd = dc;
+                    st16(hw + 32 * j, wo[0]);
+                    st16(hw + 32 * j + 8, wo[1]);
+                    st16(hg + 32 * j, dq[0]);
+                    st16(hg + 32 * j + 8, dq[1]);
                 }
+                // lanes l and l + 32 hold the two 16-column halves of a row
+                dc += __shfl_xor(dc, 32);
+                if (elh == 0) p.dcp[((size_t)pr * p.B + c) * 2 + wn] = dc;
             }
         } else
 #pragma unroll

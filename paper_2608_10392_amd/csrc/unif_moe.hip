@@ -719,6 +719,10 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         up.Wup = static_cast<const u16*>(W_up);
         up.Hbuf = reinterpret_cast<u16*>(ws + plan.hbuf);
         up.Hsink = up.Hbuf + m.pcap * m.H;
+        up.sink_row = m.pcap;
+        up.Gbuf = nullptr;
+        up.pw = nullptr;
+        up.dcp = nullptr;
         up.slab_rows = pp.slab_rows;
         up.slab_tok = pp.slab_tok;
         up.tile_info = pp.up_tile_info;
@@ -927,7 +931,7 @@ BwdPlan plan_backward(const Dims& m) {
     b.da = cv.take(m.bf16 ? 0 : pmax * m.H * sizeof(float));
     b.gbuf = cv.take(m.bf16 ? (pmax + 1) * (size_t)m.H * 2 : 0);   // + the sink row
     b.wdnT = cv.take(m.bf16 ? (size_t)m.K1 * m.d * m.H * 2 : 0);
-    b.dcp = cv.take(m.bf16 ? (pmax * m.B + 1) * 2 * sizeof(float) : 0);
+    b.dcp = cv.take(m.bf16 ? (pmax + 1) * m.B * 2 * sizeof(float) : 0);
     b.dcoef = cv.take(pmax * sizeof(float));
     b.pw = cv.take(pmax * sizeof(float));
     b.dz = cv.take((size_t)m.N * m.K1 * sizeof(float));
@@ -1100,11 +1104,10 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg_in, const void* X, co
         up.queue = queues;
         up.b_up = nullptr;
         up.Gbuf = gbuf;
-        up.Gsink = gbuf + pmax * m.H;
         up.pw = p.pw;
         float* const dcp = reinterpret_cast<float*>(ws + bp.dcp);
         up.dcp = dcp;
-        up.dcp_sink = dcp + pmax * m.B * 2;
+        up.sink_row = (int)pmax;
         const size_t up_lds = (size_t)up_lds_bytes(m.M, up_tm(m.M, m.d));
         const int grid = (cus / kXcds) * kXcds;
         s = launch_up<kEpiPre>(m, grid, up_lds, st, up);
