@@ -271,6 +271,7 @@ constexpr int kDzRow = 80;   // K+1 <= 65, rounded up to whole groups of 16
 __global__ __launch_bounds__(256) void bwd_token_kernel(BwdParams p) {
     __shared__ float dzs[kTokTile][kDzRow];
     __shared__ float sdp_s[kTokTile];
+    __shared__ int pofs[kTokTile][kDzRow];   // the tile's pairs by slot (0 past a token's k)
     const int K1 = p.K + 1;
     const int t0 = blockIdx.x * kTokTile;
     const int nt = min(kTokTile, p.N - t0);
@@ -313,8 +314,10 @@ __global__ __launch_bounds__(256) void bwd_token_kernel(BwdParams p) {
     }
     __syncthreads();
     // dX, 4 columns per thread: the pair rows slot by slot across the tile's
-    // tokens (the loads of one slot are independent), then the router terms
-    // 8 j at a time with W_j[n..n+3] in registers.
+    // tokens, then the router terms 8 j at a time with W_j[n..n+3] in
+    // registers. The tile's pair indices are staged in LDS and a slot's 16
+    // row loads are issued unconditionally (slots a token lacks re-read pair
+    // 0 and add nothing), so they are all in flight together.
     int kk[kTokTile];
     int kmax = 0;
 #pragma unroll
@@ -322,17 +325,25 @@ __global__ __launch_bounds__(256) void bwd_token_kernel(BwdParams p) {
         kk[tt] = tt < nt ? p.nres[t0 + tt] : 0;
         kmax = max(kmax, kk[tt]);
     }
+    for (int x = threadIdx.x; x < kTokTile * K1; x += blockDim.x) {
+        const int tt = x / K1, i = x - tt * K1;
+        const int k = tt < nt ? p.nres[t0 + tt] : 0;
+        pofs[tt][i] = (k > 0 && i <= k) ? p.pair_of[(size_t)(t0 + tt) * K1 + i] : 0;
+    }
+    __syncthreads();
+    const int nslot = (kmax > 0) ? kmax + 1 : 0;   // kmax = 0: every token of the tile is padded
     for (int n = 4 * (int)threadIdx.x; n < p.d; n += 4 * (int)blockDim.x) {
         f32x4 acc[kTokTile];
 #pragma unroll
         for (int tt = 0; tt < kTokTile; ++tt) acc[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int i = 0; i <= kmax; ++i) {
+        for (int i = 0; i < nslot; ++i) {
+            f32x4 v[kTokTile];
 #pragma unroll
             for (int tt = 0; tt < kTokTile; ++tt)
-                if (kk[tt] > 0 && i <= kk[tt]) {
-                    const int pr = p.pair_of[(size_t)(t0 + tt) * K1 + i];
-                    acc[tt] += *reinterpret_cast<const f32x4*>(p.dxp + (size_t)pr * p.d + n);
-                }
+                v[tt] = *reinterpret_cast<const f32x4*>(p.dxp + (size_t)pofs[tt][i] * p.d + n);
+#pragma unroll
+            for (int tt = 0; tt < kTokTile; ++tt)
+                if (i <= kk[tt] && kk[tt] > 0) acc[tt] += v[tt];
         }
         for (int j0 = 0; j0 < K1; j0 += 8) {
             f32x4 w[8];
@@ -358,51 +369,91 @@ __global__ __launch_bounds__(256) void bwd_token_kernel(BwdParams p) {
 }
 
 // dW_router[j][n] = sum_t dz[t][j] x_t[n] in two passes: partial sums over
-// kRouterChunks slices of the tokens (blockIdx.y), then their sum in slice
-// order. A thread takes one column n of one slice with 16 j at a time in
-// registers (x_t[n] is read once per 16 j, four tokens' loads in flight);
-// the slice's dz rows are staged through LDS kRouterStage tokens at a time.
+// kRouterChunks slices of the tokens (blockIdx.z), then their sum in slice
+// order. One wave per (128 columns, 32 j, slice), on the matrix cores in
+// fp32 (v_mfma_f32_32x32x2_f32, two tokens per step, four products side by
+// side): lane l brings dz[t + l / 32][j0 + l % 32] as its A value and
+// x_{t + l / 32}[n0 + 4 (l % 32) + b] as its B value of product b, so column
+// cc of product b stands for n = n0 + 4 cc + b and one load gives a lane its
+// four B values. The loads of the next 16 tokens are in flight while the
+// current 16 are multiplied.
 constexpr int kRouterChunks = 256;
-constexpr int kRouterStage = 64;
+constexpr int kRouterCols = 128;
+
+// Four consecutive values of a layer-format tensor: the raw bytes (8 for
+// bf16, 16 for fp32), then as floats.
+template <bool BF16>
+using raw4_t = typename std::conditional<BF16, uint2, f32x4>::type;
 
 template <bool BF16>
-__global__ __launch_bounds__(256) void bwd_router_kernel(BwdParams p) {
-    __shared__ float dzs[kRouterStage][16];
+__device__ __forceinline__ raw4_t<BF16> ld_raw4(const void* p, size_t i) {
+    if constexpr (BF16) return *reinterpret_cast<const uint2*>(static_cast<const u16*>(p) + i);
+    else return *reinterpret_cast<const f32x4*>(static_cast<const float*>(p) + i);
+}
+
+template <bool BF16>
+__device__ __forceinline__ f32x4 raw4_f32(raw4_t<BF16> r) {
+    if constexpr (BF16)
+        return f32x4{__uint_as_float(r.x << 16), __uint_as_float(r.x & 0xffff0000u), __uint_as_float(r.y << 16),
+                     __uint_as_float(r.y & 0xffff0000u)};
+    else return r;
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(64) void bwd_router_kernel(BwdParams p) {
+    constexpr int U = 8;   // steps (two tokens each) per batch of loads
     const int K1 = p.K + 1;
-    const int n = blockIdx.x * blockDim.x + threadIdx.x;
-    const int c = blockIdx.y;
+    const int lane = (int)threadIdx.x, lr = lane & 31, lh = lane >> 5;
+    const int n0 = (int)blockIdx.x * kRouterCols, j0 = (int)blockIdx.y * 32, c = (int)blockIdx.z;
     const int t0 = (int)((int64_t)c * p.N / kRouterChunks), t1 = (int)((int64_t)(c + 1) * p.N / kRouterChunks);
-    for (int j0 = 0; j0 < K1; j0 += 16) {
-        float acc[16];
+    const int j = j0 + lr, n = n0 + 4 * lr;
+    const bool jok = j < K1, nok = n < p.d;   // d % 4 == 0: a lane's 4 columns are all in or all out
+    // Loads are issued for every lane and step (out-of-range ones read a
+    // valid element of the slice, row t1 - 1, and are zeroed afterwards), so
+    // a batch's loads are all in flight together.
+    const int jc = jok ? j : 0, nc = nok ? n : 0;
+    f32x16 acc[4];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) acc[u] = 0.f;
-        for (int s0 = t0; s0 < t1; s0 += kRouterStage) {
-            const int ns = min(kRouterStage, t1 - s0);
-            __syncthreads();
-            for (int x = threadIdx.x; x < kRouterStage * 16; x += blockDim.x) {
-                const int tt = x >> 4, u = x & 15;
-                dzs[tt][u] = (tt < ns && j0 + u < K1) ? p.dz[(size_t)(s0 + tt) * K1 + j0 + u] : 0.f;
-            }
-            __syncthreads();
-            if (n < p.d) {
-                // rows past the slice read x = 0 against dz = 0
-                for (int tt = 0; tt < ns; tt += 4) {
-                    float xv[4];
+    for (int q = 0; q < 4; ++q) acc[q] = f32x16{};
+    float a[2][U];
+    raw4_t<BF16> x[2][U];
+    auto load = [&](int t, int set) {
 #pragma unroll
-                    for (int q = 0; q < 4; ++q)
-                        xv[q] = (tt + q < ns) ? ld_val<BF16>(p.X, (size_t)(s0 + tt + q) * p.d + n) : 0.f;
-#pragma unroll
-                    for (int q = 0; q < 4; ++q)
-#pragma unroll
-                        for (int u = 0; u < 16; ++u) acc[u] = fmaf(dzs[tt + q][u], xv[q], acc[u]);
-                }
-            }
+        for (int u = 0; u < U; ++u) {
+            const int tt = min(t + 2 * u + lh, t1 - 1);
+            a[set][u] = p.dz[(size_t)tt * K1 + jc];
+            x[set][u] = ld_raw4<BF16>(p.X, (size_t)tt * p.d + nc);
         }
-        if (n < p.d)
+    };
+    auto multiply = [&](int t, int set) {
 #pragma unroll
-            for (int u = 0; u < 16; ++u)
-                if (j0 + u < K1) p.rpart[((size_t)c * K1 + j0 + u) * p.d + n] = acc[u];
+        for (int u = 0; u < U; ++u) {
+            const bool ok = t + 2 * u + lh < t1;
+            const float av = (ok && jok) ? a[set][u] : 0.f;
+            const f32x4 xv = raw4_f32<BF16>(x[set][u]);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                acc[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, nok ? xv[q] : 0.f, acc[q], 0, 0, 0);
+        }
+    };
+    if (t0 < t1) load(t0, 0);
+    for (int t = t0; t < t1; t += 4 * U) {
+        if (t + 2 * U < t1) load(t + 2 * U, 1);
+        multiply(t, 0);
+        if (t + 2 * U >= t1) break;
+        if (t + 4 * U < t1) load(t + 4 * U, 0);
+        multiply(t + 2 * U, 1);
     }
+    // Lane l holds rows (v / 4) 8 + 4 (l / 32) + v % 4 of column l % 32 of
+    // each product.
+    if (nok)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int r = j0 + (v >> 2) * 8 + lh * 4 + (v & 3);
+            if (r < K1)
+                *reinterpret_cast<f32x4*>(p.rpart + ((size_t)c * K1 + r) * p.d + n) =
+                    f32x4{acc[0][v], acc[1][v], acc[2][v], acc[3][v]};
+        }
 }
 
 __global__ __launch_bounds__(256) void bwd_router_sum_kernel(BwdParams p) {

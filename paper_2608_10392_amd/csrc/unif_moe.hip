@@ -1162,9 +1162,9 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg_in, const void* X, co
     // 5. per token: dX and the router-logit gradients; the router's weight gradient
     bwd_token_kernel<<<(unsigned)ceil_div(m.N, kTokTile), 256, 0, st>>>(p);
     UNIF_LAUNCH_CHECK();
-    const dim3 rgrid((unsigned)ceil_div(m.d, 256), kRouterChunks);
-    if (m.bf16) bwd_router_kernel<true><<<rgrid, 256, 0, st>>>(p);
-    else bwd_router_kernel<false><<<rgrid, 256, 0, st>>>(p);
+    const dim3 rgrid((unsigned)ceil_div(m.d, kRouterCols), (unsigned)ceil_div(m.K1, 32), kRouterChunks);
+    if (m.bf16) bwd_router_kernel<true><<<rgrid, 64, 0, st>>>(p);
+    else bwd_router_kernel<false><<<rgrid, 64, 0, st>>>(p);
     UNIF_LAUNCH_CHECK();
     bwd_router_sum_kernel<<<(unsigned)ceil_div(m.K1 * m.d, 256), 256, 0, st>>>(p);
     UNIF_LAUNCH_CHECK();
