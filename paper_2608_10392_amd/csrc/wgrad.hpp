@@ -12,10 +12,10 @@
 // row, while the MFMA takes 8 consecutive r per lane. Each thread loads an
 // 8 x 8 block (8 rows, one 16-byte column chunk each), transposes it in
 // registers and writes 8 index rows of 8 r to LDS, where a stage is laid out
-// index-major: one 128-byte line of 64 r per index, in the up kernel's
-// swizzle, so the fragment reads are the up kernel's. Two stage slots
-// alternate; the loads of stage s + 1 are in flight while stage s is
-// multiplied.
+// index-major: one 128-byte line of 64 r per index (wg_off's swizzle), so
+// the fragment reads are the up kernel's. Two stage slots alternate; while
+// stage s is multiplied, the rows of stage s + 2 and the list indices of
+// stage s + 3 are in flight.
 //
 // Output tile TQ x TP per workgroup of 8 waves (WQ x WP), where P is the
 // output's contiguous index (n for dW_up, h for dW_down) and Q the other.
@@ -45,6 +45,16 @@ __device__ __forceinline__ int wcol_pos(int i) { return (i & 3) | ((i >> 4) << 2
 
 __host__ __device__ constexpr int wgrad_lds_bytes(int TQ, int TP) { return 2 * (TQ + TP) * Stage::RB; }
 
+// Byte offset of 16-byte chunk c of stage row r. The chunk is rotated by
+// bits 1-3, 2-4 and 3-5 of the row: the fragment reads (rows r..r+15 of one
+// chunk per 16 lanes) stay free of bank conflicts as with the up kernel's
+// layout, and the 16 lanes of a store, whose rows are 8 apart (one index row
+// of each lane's 8 x 8 block, all of one parity), fall on 8 distinct bank
+// groups, two lanes each (the fewest a single row parity allows).
+__device__ __forceinline__ uint32_t wg_off(int r, int c) {
+    return (uint32_t)r * Stage::RB + ((c ^ (((r >> 1) ^ (r >> 2) ^ (r >> 3)) & 7)) << 4);
+}
+
 template <bool UP, int GQ, int GP, int WQ>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void wgrad_kernel(WgradParams p) {
@@ -66,8 +76,10 @@ void wgrad_kernel(WgradParams p) {
 
     // This thread's unit: rows 8 ro .. 8 ro + 7 of each stage, 16-byte chunk
     // ch of the stage's index range (P indices first, then Q).
+    // Threads past the units (whole waves) load like thread 0 and store
+    // nothing.
     const bool active = tid < NU;
-    const int ro = tid / NCH, ch = tid - (tid / NCH) * NCH;
+    const int ro = active ? tid / NCH : 0, ch = active ? tid - (tid / NCH) * NCH : 0;
     const bool isP = ch < TP / 8;
     const int idx0 = isP ? 8 * ch : 8 * (ch - TP / 8);
     const bool tokrows = (UP == isP);            // X and dY rows are tokens; G and Hw rows pairs
@@ -79,31 +91,44 @@ void wgrad_kernel(WgradParams p) {
     for (int j = 0; j < 8; ++j) {
         const int idx = idx0 + j;
         const int row = isP ? 32 * (idx >> 5) + wcol_pos(idx & 31) : TP + idx;
-        wofs[j] = S::off(row, ro);
+        wofs[j] = wg_off(row, ro);
     }
 
     const int nst = (cnt + 63) / 64;
-    int ri[8];
-    u32x4 v[8];
-    auto load_idx = [&](int st) {
-        if (!active) return;
+    // Row loads are issued one stage ahead of their LDS store and the list
+    // indices two stages ahead, indices first: the memory counter retires in
+    // order, so the wait for a stage's indices then never includes the row
+    // loads issued after them. No load sits behind a branch (the compiler
+    // would then count conservatively): rows past the slab's count read row
+    // 0 of the list's buffer and are zeroed before the store, and loads for
+    // stages past the last re-read the last one.
+    const char* const srcb = reinterpret_cast<const char*>(src);
+    const uint32_t row_bytes = (uint32_t)(stride * 2);
+    auto load_idx = [&](int st, uint32_t (&ri)[8]) {
+        st = min(st, nst - 1);
         const u32x4 a = ld16(list + st * 64), b = ld16(list + st * 64 + 4);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            ri[q] = (int)a[q];
-            ri[4 + q] = (int)b[q];
+            ri[q] = a[q];
+            ri[4 + q] = b[q];
         }
     };
-    auto load_data = [&](int st) {
+    auto load_data = [&](int st, const uint32_t (&ri)[8], u32x4 (&v)[8]) {
+        st = min(st, nst - 1);
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            const int r = st * 64 + 8 * ro + q;
-            v[q] = (active && r < cnt) ? ld16(src + (size_t)ri[q] * stride) : u32x4{0u, 0u, 0u, 0u};
+            const uint32_t rr = (st * 64 + 8 * ro + q < cnt) ? ri[q] : 0u;
+            v[q] = ld16(srcb + (uint64_t)rr * row_bytes);
         }
     };
-    auto store_lds = [&](int slot) {
+    auto store_lds = [&](int st, u32x4 (&v)[8]) {
         if (!active) return;
-        char* base = lds_wg + slot * STAGE;
+        if (st * 64 + 64 > cnt) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                if (st * 64 + 8 * ro + q >= cnt) v[q] = u32x4{0u, 0u, 0u, 0u};
+        }
+        char* base = lds_wg + (st & 1) * STAGE;
 #pragma unroll
         for (int j = 0; j < 8; ++j) st16(base + wofs[j], column8(v, j));
     };
@@ -118,30 +143,63 @@ void wgrad_kernel(WgradParams p) {
         for (int kk = 0; kk < S::KSTEPS; ++kk) {
             u32x4 fp[GP], fq[GQ];
 #pragma unroll
-            for (int j = 0; j < GP; ++j) fp[j] = ld16(base + S::off(wp * GP * 32 + j * 32 + lr, 2 * kk + lh));
+            for (int j = 0; j < GP; ++j) fp[j] = ld16(base + wg_off(wp * GP * 32 + j * 32 + lr, 2 * kk + lh));
 #pragma unroll
-            for (int i = 0; i < GQ; ++i) fq[i] = ld16(base + S::off(TP + wq * GQ * 32 + i * 32 + lr, 2 * kk + lh));
+            for (int i = 0; i < GQ; ++i) fq[i] = ld16(base + wg_off(TP + wq * GQ * 32 + i * 32 + lr, 2 * kk + lh));
 #pragma unroll
             for (int i = 0; i < GQ; ++i)
 #pragma unroll
                 for (int j = 0; j < GP; ++j) acc[i][j] = mfma32x32x16(as_bf16x8(fp[j]), as_bf16x8(fq[i]), acc[i][j]);
         }
     };
+    // Tiles of up to 6 MFMA groups per wave keep two row sets in registers:
+    // at stage st the indices of st + 3 and the rows of st + 2 are issued,
+    // stage st is multiplied and the rows of st + 1 go to LDS (indices and
+    // rows of stage s in set s & 1). Larger tiles keep one row set: the
+    // indices of st + 2 and the rows of st + 1 are issued, stage st is
+    // multiplied and the rows of st + 1 go to LDS.
+    constexpr bool kTwoSets = GQ * GP <= 6;
+    uint32_t i0[8], i1[8];
+    u32x4 d0[8], d1[8];
     if (nst > 0) {
-        load_idx(0);
-        load_data(0);
-        if (nst > 1) load_idx(1);
-        store_lds(0);
+        load_idx(0, i0);
+        load_idx(1, i1);
+        load_data(0, i0, d0);
+        if constexpr (kTwoSets) {
+            load_idx(2, i0);
+            load_data(1, i1, d1);
+        }
+        store_lds(0, d0);
         __syncthreads();
-        for (int st = 0; st < nst; ++st) {
-            const bool more = st + 1 < nst;
-            if (more) {
-                load_data(st + 1);
-                if (st + 2 < nst) load_idx(st + 2);
+        if constexpr (kTwoSets) {
+            auto step = [&](int st, uint32_t (&in)[8], uint32_t (&ic)[8], u32x4 (&dn)[8], u32x4 (&dc)[8]) {
+                load_idx(st + 3, in);
+                load_data(st + 2, ic, dn);
+                compute(st & 1);
+                if (st + 1 < nst) store_lds(st + 1, dc);
+                __syncthreads();
+            };
+            int st = 0;
+            for (; st + 1 < nst; st += 2) {
+                step(st, i1, i0, d0, d1);
+                step(st + 1, i0, i1, d1, d0);
             }
-            compute(st & 1);
-            if (more) store_lds((st + 1) & 1);
-            __syncthreads();
+            if (st < nst) step(st, i1, i0, d0, d1);
+        } else {
+            // in: the set of st + 2 (st & 1), ic: the indices of st + 1.
+            auto step = [&](int st, uint32_t (&in)[8], uint32_t (&ic)[8]) {
+                load_idx(st + 2, in);
+                load_data(st + 1, ic, d0);
+                compute(st & 1);
+                if (st + 1 < nst) store_lds(st + 1, d0);
+                __syncthreads();
+            };
+            int st = 0;
+            for (; st + 1 < nst; st += 2) {
+                step(st, i0, i1);
+                step(st + 1, i1, i0);
+            }
+            if (st < nst) step(st, i0, i1);
         }
     }
     // Lane: Q index wq GQ 32 + 32 i + lr, P indices wp GP 32 + 32 j + 16 lh + 0..15.
