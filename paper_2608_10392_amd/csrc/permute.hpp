@@ -82,9 +82,17 @@ __device__ int block_exclusive_scan(int n, Get get, Put put, int* lds) {
     // latencies overlap), longer chunks are read twice.
     constexpr int R = 8;
     int v[R];
-    if (per <= R) {
+    if (per <= R && n > 0) {
+        // Every load is issued (past the chunk: the last element again, then
+        // dropped), so none waits behind a branch for the previous one.
 #pragma unroll
-        for (int u = 0; u < R; ++u) v[u] = (beg + u < end) ? get(beg + u) : 0;
+        for (int u = 0; u < R; ++u) {
+            const int x = get(min(beg + u, n - 1));
+            v[u] = (beg + u < end) ? x : 0;
+        }
+    } else if (per <= R) {
+#pragma unroll
+        for (int u = 0; u < R; ++u) v[u] = 0;
     }
     int s = 0;
     if (per <= R) {
@@ -136,7 +144,7 @@ __device__ int staged_exclusive_scan(int n, Get get, Put put, int* stage, int* l
         for (int i0 = tid; i0 < cnt; i0 += 8 * T) {
             int v[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = (i0 + u * T < cnt) ? get(base + i0 + u * T) : 0;
+            for (int u = 0; u < 8; ++u) v[u] = get(base + min(i0 + u * T, cnt - 1));
 #pragma unroll
             for (int u = 0; u < 8; ++u)
                 if (i0 + u * T < cnt) stage[i0 + u * T] = v[u];
@@ -282,13 +290,17 @@ __device__ __forceinline__ void up_tiles_of_group(const PermuteParams& p, int gr
     const int nq = ceil_div(p.ntile, CH);
     int* tl = lds;                           // [nq + 1][ng]
     int* scan = lds + kUpTableWords;         // blockDim.x words
+    int* cn = scan + blockDim.x;             // [ng] rows of the group's slabs
     batched_copy(
         (nq + 1) * ng,
         [&](int x) {
             const int i = x / ng, sl = sl0 + c0 + x - i * ng;
             return (i < nq) ? p.tile_cnt[(size_t)i * CH * ncnt + sl] : p.slab_count[sl];
         },
-        [&](int x, int r) { tl[x] = ceil_div(r, bm); });
+        [&](int x, int r) {
+            tl[x] = ceil_div(r, bm);
+            if (x >= nq * ng) cn[x - nq * ng] = r;
+        });
     __syncthreads();
     const int tid = threadIdx.x, T = blockDim.x;
     const int per = ceil_div(nq, T);
@@ -306,7 +318,7 @@ __device__ __forceinline__ void up_tiles_of_group(const PermuteParams& p, int gr
     int pos = uo[sl0 + c0] + scan[tid] - n;
     for (int i = qa; i < qb; ++i)
         for (int c = 0; c < ng; ++c) {
-            const int sl = sl0 + c0 + c, cnt = p.slab_count[sl], s0 = so[sl];
+            const int sl = sl0 + c0 + c, cnt = cn[c], s0 = so[sl];
             for (int j = tl[i * ng + c], je = tl[(i + 1) * ng + c]; j < je; ++j, ++pos) {
                 p.up_tile_info[pos] = sl | (min(bm, cnt - j * bm) << 16);
                 p.up_tile_rows[pos] = s0 + j * bm;

@@ -146,7 +146,7 @@ int split_route_cols(const Dims& m) {
 size_t scatter_lds_bytes(const Dims& m) {
     const size_t offsets = 2 * ((size_t)m.nslab + 1);
     const size_t token_role = 64 * (size_t)m.K1 + (size_t)m.nslab;
-    const size_t table_role = (size_t)kUpTableWords + kScatterWaves * 64;
+    const size_t table_role = (size_t)kUpTableWords + kScatterWaves * 64 + 64;
     return sizeof(int) * (offsets + std::max(token_role, table_role));
 }
 
