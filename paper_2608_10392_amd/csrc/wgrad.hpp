@@ -45,14 +45,14 @@ __device__ __forceinline__ int wcol_pos(int i) { return (i & 3) | ((i >> 4) << 2
 
 __host__ __device__ constexpr int wgrad_lds_bytes(int TQ, int TP) { return 2 * (TQ + TP) * Stage::RB; }
 
-// Byte offset of 16-byte chunk c of stage row r. The chunk is rotated by
-// bits 1-3, 2-4 and 3-5 of the row: the fragment reads (rows r..r+15 of one
+// Byte offset of 16-byte chunk c of stage row r: the chunk is rotated by
+// bits 1-3, 2-4 and 4-6 of the row. The fragment reads (rows r..r+15 of one
 // chunk per 16 lanes) stay free of bank conflicts as with the up kernel's
-// layout, and the 16 lanes of a store, whose rows are 8 apart (one index row
-// of each lane's 8 x 8 block, all of one parity), fall on 8 distinct bank
-// groups, two lanes each (the fewest a single row parity allows).
+// layout, and the stores, whose 16 lanes write rows 8 apart with both
+// parities (odd chunks store their block's columns in the order j ^ 1),
+// fall on nearly all 16 bank groups.
 __device__ __forceinline__ uint32_t wg_off(int r, int c) {
-    return (uint32_t)r * Stage::RB + ((c ^ (((r >> 1) ^ (r >> 2) ^ (r >> 3)) & 7)) << 4);
+    return (uint32_t)r * Stage::RB + ((c ^ (((r >> 1) ^ (r >> 2) ^ (r >> 4)) & 7)) << 4);
 }
 
 template <bool UP, int GQ, int GP, int WQ>
@@ -86,10 +86,16 @@ void wgrad_kernel(WgradParams p) {
     const int* list = (tokrows ? p.slab_tok : p.slab_rows) + so + 8 * ro;
     const u16* src = (isP ? p.Psrc : p.Qsrc) + (tokrows ? n0 : c * p.M) + idx0;
     const size_t stride = tokrows ? (size_t)p.d : (size_t)p.H;
-    uint32_t wofs[8];                            // LDS byte offset of index row idx0 + j, chunk ro
+    // Store j of an odd chunk writes column j ^ 1 of the thread's block:
+    // wofs[j] is the LDS byte offset of index row idx0 + (j ^ (ch & 1)),
+    // chunk ro, and sel_even / sel_odd (for even and odd j) pick the 16-bit
+    // halves that form that column.
+    const int jx = ch & 1;
+    const uint32_t sel_even = jx ? 0x07060302u : 0x05040100u, sel_odd = jx ? 0x05040100u : 0x07060302u;
+    uint32_t wofs[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-        const int idx = idx0 + j;
+        const int idx = idx0 + (j ^ jx);
         const int row = isP ? 32 * (idx >> 5) + wcol_pos(idx & 31) : TP + idx;
         wofs[j] = wg_off(row, ro);
     }
@@ -130,7 +136,14 @@ void wgrad_kernel(WgradParams p) {
         }
         char* base = lds_wg + (st & 1) * STAGE;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) st16(base + wofs[j], column8(v, j));
+        for (int j = 0; j < 8; ++j) {
+            // column j ^ jx: 16-bit half (j ^ jx) & 1 of word j / 2 of the 8 rows
+            const uint32_t sel = (j & 1) ? sel_odd : sel_even;
+            u32x4 o;
+#pragma unroll
+            for (int m = 0; m < 4; ++m) o[m] = __builtin_amdgcn_perm(v[2 * m + 1][j >> 1], v[2 * m][j >> 1], sel);
+            st16(base + wofs[j], o);
+        }
     };
     f32x16 acc[GQ][GP];
 #pragma unroll
