@@ -26,6 +26,8 @@
 //   bwd_router    dW_router[j] = sum_t dz[t, j] x_t (token slices, then
 //                 their sum)
 #pragma once
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace unifmoe {
@@ -64,11 +66,6 @@ struct BwdParams {
 
 __device__ __forceinline__ float ld_f32(const void* p, size_t i) { return static_cast<const float*>(p)[i]; }
 
-template <bool BF16>
-__device__ __forceinline__ float ld_val(const void* p, size_t i) {
-    if constexpr (BF16) return bf2f(static_cast<const u16*>(p)[i]);
-    else return static_cast<const float*>(p)[i];
-}
 
 // Blocks (bit c) that channels [h0, h1) touch, h0 < h1.
 __device__ __forceinline__ uint64_t channel_blocks(int h0, int h1, int M) {
