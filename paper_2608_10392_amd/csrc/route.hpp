@@ -291,13 +291,13 @@ __host__ __device__ __forceinline__ int decide_lanes(int K, int B) {
 // counters (rows per (expert, block) slab, then pairs per expert), or null.
 template <int L>
 __device__ __forceinline__ void decide_group(const RouteParams& p, const float* row, int tok0, int t, int ntok,
-                                             int* cnt) {
+                                             bool tok_valid, int* cnt) {
     static_assert(L == 16 || L == 32 || L == 64, "lane groups");
     const int K = p.K, B = p.B;
     const int lane = lane_id(), j = lane & (L - 1), gbase = lane - j;
     const int tok = tok0 + t;
     const bool in_range = t < ntok;
-    const bool v = in_range && (p.valid == nullptr || p.valid[tok] != 0);
+    const bool v = in_range && tok_valid;
     const uint64_t gmask = (L == 64) ? ~0ull : ((1ull << L) - 1ull);
     auto group_bits = [&](bool pred) { return (ballot(pred) >> gbase) & gmask; };
 
@@ -399,9 +399,13 @@ __device__ __forceinline__ void decide_group(const RouteParams& p, const float* 
     const int kb = p.key_bits;
     const int ks = mask_key(mask, B, kb), kr = mask_key(~mask & full, B, kb);
     const int bc = (tok / kTileTok) % kBinCopies, nbin = (K + 1) << kb;
+    // Both atomics are issued before either slot is stored (one round trip).
     int* rank = p.pair_rank + (size_t)(v ? tok : 0) * (K + 1);
-    if (v && j == 0) rank[0] = atomicAdd(&p.bin_count[bin_counter(ks, bc, nbin)], 1);
-    if (v && j < k) rank[1 + j] = atomicAdd(&p.bin_count[bin_counter((qs << kb) + kr, bc, nbin)], 1);
+    int r0 = 0, r1 = 0;
+    if (v && j == 0) r0 = atomicAdd(&p.bin_count[bin_counter(ks, bc, nbin)], 1);
+    if (v && j < k) r1 = atomicAdd(&p.bin_count[bin_counter((qs << kb) + kr, bc, nbin)], 1);
+    if (v && j == 0) rank[0] = r0;
+    if (v && j < k) rank[1 + j] = r1;
     if (cnt == nullptr) return;
     // The tile's counts: pairs per expert, and rows per slab (the shared
     // expert on I_shr, each selected residual expert on I_res). Lane c adds
@@ -423,13 +427,23 @@ __device__ __forceinline__ void decide_group(const RouteParams& p, const float* 
 // (stride lstride): the waves [w0, w0 + nw) of the workgroup share the
 // tile's tokens, 64 / L per pass.
 template <int L>
-__device__ __forceinline__ void decide_tile(const RouteParams& p, const float* rows, int tok0, int ntok, int wave,
-                                            int w0, int nw, int* cnt) {
+__device__ __forceinline__ void decide_tile(const RouteParams& p, const float* rows, const int* vflags, int tok0,
+                                            int ntok, int wave, int w0, int nw, int* cnt) {
     constexpr int TPP = 64 / L;   // tokens per wave pass
     const int g = lane_id() / L;
     for (int t0 = (wave - w0) * TPP; t0 < kTileTok; t0 += nw * TPP) {
         const int t = t0 + g;
-        decide_group<L>(p, rows + (size_t)(t < ntok ? t : 0) * p.lstride, tok0, t, ntok, cnt);
+        decide_group<L>(p, rows + (size_t)(t < ntok ? t : 0) * p.lstride, tok0, t, ntok, vflags[t] != 0, cnt);
+    }
+}
+
+// The valid flags of a tile's tokens into LDS (1 for every token without a
+// mask; tokens past the layer read 0): the decisions then read them without
+// a global load in each pass. Called by every thread; a barrier follows.
+__device__ __forceinline__ void stage_valid(const RouteParams& p, int tok0, int* vflags) {
+    for (int t = threadIdx.x; t < kTileTok; t += blockDim.x) {
+        const int tok = tok0 + t;
+        vflags[t] = (tok < p.N) ? (p.valid == nullptr ? 1 : (int)p.valid[tok]) : 0;
     }
 }
 
@@ -450,12 +464,12 @@ __device__ __forceinline__ void flush_counts(const RouteParams& p, const int* cn
 
 // The decisions of one tile with the lane count of the layer (see
 // decide_lanes).
-__device__ __forceinline__ void decide_tile_any(const RouteParams& p, const float* rows, int tok0, int ntok,
-                                                int wave, int w0, int nw, int* cnt) {
+__device__ __forceinline__ void decide_tile_any(const RouteParams& p, const float* rows, const int* vflags, int tok0,
+                                                int ntok, int wave, int w0, int nw, int* cnt) {
     switch (decide_lanes(p.K, p.B)) {
-        case 16: decide_tile<16>(p, rows, tok0, ntok, wave, w0, nw, cnt); break;
-        case 32: decide_tile<32>(p, rows, tok0, ntok, wave, w0, nw, cnt); break;
-        default: decide_tile<64>(p, rows, tok0, ntok, wave, w0, nw, cnt); break;
+        case 16: decide_tile<16>(p, rows, vflags, tok0, ntok, wave, w0, nw, cnt); break;
+        case 32: decide_tile<32>(p, rows, vflags, tok0, ntok, wave, w0, nw, cnt); break;
+        default: decide_tile<64>(p, rows, vflags, tok0, ntok, wave, w0, nw, cnt); break;
     }
 }
 
@@ -469,12 +483,14 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteParams p) {
     if (route_copy_role(p)) return;
     extern __shared__ float lds_route[];
     float* L = lds_route;
-    int* cnt = reinterpret_cast<int*>(L + kRouteTok * p.lstride);   // [NT][ncnt]
-    const int tok0 = blockIdx.x * kRouteTok;
     const int ncnt = (p.K + 1) * p.B + p.K + 1;
+    int* cnt = reinterpret_cast<int*>(L + kRouteTok * p.lstride);   // [NT][ncnt]
+    int* vflags = cnt + NT * ncnt;                                   // [NT][kTileTok]
+    const int tok0 = blockIdx.x * kRouteTok;
     const bool counting = p.tile_cnt != nullptr;
     if (counting)
         for (int i = threadIdx.x; i < NT * ncnt; i += blockDim.x) cnt[i] = 0;
+    for (int h = 0; h < NT; ++h) stage_valid(p, tok0 + h * kTileTok, vflags + h * kTileTok);
     if constexpr (NCT > 0) route_logits_bf16<NCT>(p, L, tok0);
     else route_logits_f32(p, L, tok0);
     __syncthreads();
@@ -483,8 +499,8 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(RouteParams p) {
     for (int h = 0; h < NT; ++h) {
         const int t0 = tok0 + h * kTileTok;
         if (t0 >= p.N) break;
-        decide_tile_any(p, L + (size_t)h * kTileTok * p.lstride, t0, min(kTileTok, p.N - t0), wave, 0,
-                        kRouteThreads / 64, counting ? cnt + h * ncnt : nullptr);
+        decide_tile_any(p, L + (size_t)h * kTileTok * p.lstride, vflags + h * kTileTok, t0, min(kTileTok, p.N - t0),
+                        wave, 0, kRouteThreads / 64, counting ? cnt + h * ncnt : nullptr);
         ++nt;
     }
     if (counting) {
@@ -611,32 +627,42 @@ __global__ __launch_bounds__(kRpThreads) void route_logits_kernel(RouteParams p,
     }
 }
 
-// Decisions of one 64-token tile per workgroup of 4 waves (L lanes per
+// Decisions of one 64-token tile per workgroup of NW waves (L lanes per
 // token, see decide_lanes), from the logits route_logits_kernel wrote (ncols
 // per token), staged in LDS rows; then the tile's counters out to memory.
-// The last p.cvt_blocks workgroups do the launch's copy job instead.
-constexpr int kDecideThreads = 256;
-template <int L>
-__global__ __launch_bounds__(kDecideThreads) void route_decide_kernel(RouteParams p, const float* __restrict__ logits,
-                                                                      int ncols) {
+// The last p.cvt_blocks workgroups do the launch's copy job instead. With
+// few tiles (up to two per compute unit) 8 waves share a tile, so each wave
+// runs half the passes of dependent lane exchanges; with more tiles 4 do,
+// which leaves room on each compute unit for more tiles and the copy.
+template <int L, int NW>
+__global__ __launch_bounds__(NW * 64) void route_decide_kernel(RouteParams p, const float* __restrict__ logits,
+                                                               int ncols) {
     if (route_copy_role(p)) return;
     extern __shared__ float lds_dec[];
     const int ls = p.lstride;
     float* rows = lds_dec;                                       // [64][ls]
-    int* cnt = reinterpret_cast<int*>(rows + kTileTok * ls);     // the tile's counters
     const int ncnt = (p.K + 1) * p.B + p.K + 1;
+    int* cnt = reinterpret_cast<int*>(rows + kTileTok * ls);     // the tile's counters
+    int* vflags = cnt + ncnt;                                    // [kTileTok] valid flags
     const bool counting = p.tile_cnt != nullptr;
     const int tile = blockIdx.x, tok0 = tile * kTileTok, ntok = min(kTileTok, p.N - tok0);
+    // The tokens' valid flags are loaded first and stored after the logit
+    // rows' batch, so their latencies overlap.
+    const int tv = (int)threadIdx.x;
+    uint32_t vb = 1u;
+    if (tv < ntok && p.valid != nullptr) vb = p.valid[tok0 + tv];
     batched_copy(
         ntok * ncols, [&](int e) { return logits[(size_t)tok0 * ncols + e]; },
         [&](int e, float v) {
             const int t = e / ncols;
             rows[t * ls + e - t * ncols] = v;
         });
+    asm volatile("" : "+v"(vb));   // the byte is first used here, after the rows' batch
+    if (tv < kTileTok) vflags[tv] = (tv < ntok && vb != 0u) ? 1 : 0;
     if (counting)
         for (int i = threadIdx.x; i < ncnt; i += blockDim.x) cnt[i] = 0;
     __syncthreads();
-    decide_tile<L>(p, rows, tok0, ntok, (int)threadIdx.x >> 6, 0, kDecideThreads / 64, counting ? cnt : nullptr);
+    decide_tile<L>(p, rows, vflags, tok0, ntok, (int)threadIdx.x >> 6, 0, NW, counting ? cnt : nullptr);
     if (counting) {
         __syncthreads();
         flush_counts(p, cnt, 1, ncnt, tile, 1);

@@ -125,15 +125,15 @@ unif_moe_config worst_case(unif_moe_config c) {
 // Counters per tile of the permutation: rows per slab, then pairs per expert.
 size_t tile_counters(const Dims& m) { return (size_t)m.nslab + m.K1; }
 // Routing LDS (route_kernel): the logit rows of its tokens, then its two
-// tiles' counters.
+// tiles' counters and their tokens' valid flags.
 size_t route_lds_bytes(const Dims& m) {
-    return sizeof(float) * ((size_t)kRouteTok * m.lstride + (kRouteTok / kTileTok) * tile_counters(m));
+    return sizeof(float) * ((size_t)kRouteTok * m.lstride + (kRouteTok / kTileTok) * (tile_counters(m) + kTileTok));
 }
 // The persistent logits kernel: 8 partial logit sets of a tile. The
-// decisions kernel: a tile's logit rows and counters.
+// decisions kernel: a tile's logit rows, counters and valid flags.
 size_t route_logits_lds_bytes(const Dims& m) { return sizeof(float) * (size_t)kRpWaves * kRpTok * m.lstride; }
 size_t route_decide_lds_bytes(const Dims& m) {
-    return sizeof(float) * ((size_t)kTileTok * m.lstride + tile_counters(m));
+    return sizeof(float) * ((size_t)kTileTok * m.lstride + tile_counters(m) + kTileTok);
 }
 // Logits of the split routing path (bf16 routers of <= 32 columns, d <= 1024):
 // 1 + 16 NCT fp32 values per token, or 0 when the path does not apply.
@@ -432,17 +432,18 @@ int32_t launch_route(const Dims& m, const RouteParams& rp, const float* Wr, cons
             default: return UNIF_EUNSUPPORTED;
         }
         void (*dk)(RouteParams, const float*, int) = nullptr;
-        switch (decide_lanes(m.K, m.B)) {
-            case 16: dk = route_decide_kernel<16>; break;
-            case 32: dk = route_decide_kernel<32>; break;
-            default: dk = route_decide_kernel<64>; break;
-        }
         const int ntiles = ceil_div(m.N, kRpTok);
+        const bool wide = ntiles <= 2 * cu_count();   // 8 waves per tile
+        switch (decide_lanes(m.K, m.B)) {
+            case 16: dk = wide ? route_decide_kernel<16, 8> : route_decide_kernel<16, 4>; break;
+            case 32: dk = wide ? route_decide_kernel<32, 8> : route_decide_kernel<32, 4>; break;
+            default: dk = wide ? route_decide_kernel<64, 8> : route_decide_kernel<64, 4>; break;
+        }
         const size_t l1 = route_logits_lds_bytes(m), l2 = route_decide_lds_bytes(m);
         if (allow_lds(lk, l1) != UNIF_OK || allow_lds(dk, l2) != UNIF_OK) return UNIF_EDEVICE;
         lk<<<std::min(cu_count(), ntiles), kRpThreads, l1, st>>>(rp, logits);
         UNIF_LAUNCH_CHECK();
-        dk<<<ntiles + rp.cvt_blocks, kDecideThreads, l2, st>>>(rp, logits, ncols);
+        dk<<<ntiles + rp.cvt_blocks, wide ? 512 : 256, l2, st>>>(rp, logits, ncols);
         UNIF_LAUNCH_CHECK();
         return UNIF_OK;
     }
