@@ -150,13 +150,6 @@ struct TileQueue {
         lo = (int)((int64_t)x * n_tiles / kXcds);
         hi = (int)((int64_t)(x + 1) * n_tiles / kXcds);
     }
-    // Slices given by the table: XCD x owns [slices[x], slices[x + 1]).
-    __device__ TileQueue(int* queue, const int* slices) {
-        const int x = blockIdx.x % kXcds;
-        ctr = queue + x;
-        lo = ld_uniform(slices + x);
-        hi = ld_uniform(slices + x + 1);
-    }
     // One lane only (a vector atomic with return); the result is an offset
     // from lo.
     __device__ int take(int n) const { return atomicAdd(ctr, n); }
