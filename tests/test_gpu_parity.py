@@ -61,6 +61,11 @@ SMALL = {
     "k64_b64": dict(n_tokens=300, d_model=128, n_experts=64, n_blocks=64, block_width=64,
                     max_shared=64, mass_threshold=0.9),
     "n1": dict(n_tokens=1, d_model=256, n_experts=4, n_blocks=4, block_width=64, max_shared=4),
+    # d = 640: down tiles of 256 pairs x 128 columns, five column tiles
+    "d640": dict(n_tokens=900, d_model=640, n_experts=5, n_blocks=8, block_width=128, max_shared=8),
+    # d = 1152: down tiles of 128 pairs x 384 columns, three column tiles;
+    # routing on the fused path (the split path takes d <= 1024)
+    "d1152": dict(n_tokens=700, d_model=1152, n_experts=4, n_blocks=4, block_width=192, max_shared=4),
 }
 
 
