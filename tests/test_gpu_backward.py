@@ -82,6 +82,10 @@ CASES = {
                                 block_width=256, max_shared=2)),
     "m128_d512": ("vit_s16", dict(n_tokens=450, d_model=512, n_experts=5, n_blocks=4,
                                   block_width=128, max_shared=4)),
+    # d = 640: five 128-column n tiles of the weight gradients, the down
+    # projection's 256 x 128 tiles
+    "m192_d640": ("vit_s16", dict(n_tokens=500, d_model=640, n_experts=4, n_blocks=4,
+                                  block_width=192, max_shared=4)),
     "k64_b64": ("vit_s16", dict(n_tokens=200, d_model=128, n_experts=64, n_blocks=64,
                                 block_width=64, max_shared=64, mass_threshold=0.9)),
 }
