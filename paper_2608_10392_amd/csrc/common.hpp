@@ -20,6 +20,9 @@ constexpr int kExpCopies = 16;
 // sees more than a share of its bin's atomics (atomics on one cache line
 // serialize at the L2); a bin's slots are its copies' ranges in copy order.
 constexpr int kBinCopies = 8;
+// XCDs of an MI355X (each with its own L2); the persistent GEMMs keep one
+// tile queue per XCD.
+constexpr int kXcds = 8;
 
 // The counter of copy c of bin `bin` among nbin bins: the copies of a bin lie
 // nbin counters apart, on different cache lines (and L2 channels), so a bin

@@ -61,7 +61,6 @@ namespace unifmoe {
 constexpr int kFfnThreads = 512;
 constexpr int kFfnWaves = 8;
 constexpr int kFfnTM = 256;   // rows per tile (4 waves x 2 groups of 32)
-constexpr int kXcds = 8;
 
 // What the up kernel does with its fp32 tile a (rows x the block's M
 // channels) of one (expert, block) slab:
@@ -105,7 +104,7 @@ struct DownParams {
     const int4* rt_info;         // per row tile: first pair, rows, expert
     const uint64_t* rt_masks;    // per row tile: block-mask union of each 32-row group, then of the tile
     const uint64_t* pair_mask;   // readable for a whole tile past the last pair
-    const int* totals;           // [2]: down tiles (row tiles x column tiles)
+    const int* slices;           // [kXcds + 1]: the tiles (row tile x column tile x part) of each XCD's queue
     int* queue;                  // 8 per-XCD tile counters, zero at launch
     int nsplit;                  // parts each tile's block union is split into by block index mod nsplit (1: none)
     size_t split_stride;         // floats between the parts' row buffers in part
@@ -149,6 +148,13 @@ struct TileQueue {
         ctr = queue + x;
         lo = (int)((int64_t)x * n_tiles / kXcds);
         hi = (int)((int64_t)(x + 1) * n_tiles / kXcds);
+    }
+    // Slices given by a table: XCD x owns [slices[x], slices[x + 1]).
+    __device__ TileQueue(int* queue, const int* slices) {
+        const int x = blockIdx.x % kXcds;
+        ctr = queue + x;
+        lo = ld_uniform(slices + x);
+        hi = ld_uniform(slices + x + 1);
     }
     // One lane only (a vector atomic with return); the result is an offset
     // from lo.
@@ -548,7 +554,7 @@ void down_kernel(DownParams p) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WN, wn = wave % WN;
     const int kcpb = p.M / S::SK;   // stages per block
-    const TileQueue tq(p.queue, ld_uniform(p.totals + 2) * p.nsplit);
+    const TileQueue tq(p.queue, p.slices);
     // ctl as in the up kernel.
     int* ctl = reinterpret_cast<int*>(lds_dn + RING + 16 * TM);
     if (tid == 0) {

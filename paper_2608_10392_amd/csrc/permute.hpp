@@ -61,8 +61,11 @@ struct PermuteParams {
     int* slab_tok;      // token of each slab row
     int* up_tile_info;  // per up tile: slab | rows << 16
     int* up_tile_rows;  // per up tile: first entry in slab_rows / slab_tok
-    int4* rt_info;      // per down row tile: first pair, rows, expert
+    int4* rt_info;      // per down row tile: first pair, rows, expert, blocks in its union
     uint64_t* rt_masks; // per down row tile: mask union of each 32-row group, then of the tile
+    int* down_slices;   // [kXcds + 1]: the down tiles each XCD's queue owns (down_tables)
+    int down_stages;    // stages per block of the down-projection (M / 64)
+    int down_splits;    // parts each down row tile is split into (DownParams::nsplit)
 };
 
 __global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n) {
@@ -471,9 +474,47 @@ __global__ __launch_bounds__(256) void down_tables_kernel(PermuteParams p) {
         all |= shfl_xor64(all, 32);
         if (lane == 0) {
             out[G] = all;
-            p.rt_info[rt] = make_int4(p0, nrows, e, 0);
+            p.rt_info[rt] = make_int4(p0, nrows, e, __popcll(all));
         }
     }
+}
+
+// The down tiles split over the XCDs' queues by cost instead of by count
+// (one workgroup, after down_tables): a row tile's tiles cost about its
+// stages (at least 4) plus 2 for each tile's epilogue and hand-over, per
+// column tile and part. XCD x takes the row tiles from the first whose
+// exclusive cost prefix reaches x / kXcds of the total.
+constexpr int kSliceThreads = 1024;
+__global__ __launch_bounds__(kSliceThreads) void down_slices_kernel(PermuteParams p) {
+    __shared__ int part[kSliceThreads];
+    __shared__ int bound[kXcds + 1];
+    const int nrt = p.totals[4], ns = p.down_splits;
+    const int T = blockDim.x, tid = threadIdx.x;
+    const int per = ceil_div(nrt, T), r0 = min(nrt, tid * per), r1 = min(nrt, r0 + per);
+    auto cost = [&](int rt) { return p.down_col_tiles * (max(p.rt_info[rt].w * p.down_stages, 4) + 2 * ns); };
+    int sum = 0;
+    for (int r = r0; r < r1; ++r) sum += cost(r);
+    part[tid] = sum;
+    if (tid <= kXcds) bound[tid] = nrt;
+    __syncthreads();
+    for (int off = 1; off < T; off <<= 1) {
+        const int v = (tid >= off) ? part[tid - off] : 0;
+        __syncthreads();
+        part[tid] += v;
+        __syncthreads();
+    }
+    const long long total = part[T - 1];
+    long long run = part[tid] - sum;
+    for (int r = r0; r < r1; ++r) {
+        const int c = cost(r);
+        for (int x = 1; x < kXcds; ++x) {
+            const long long target = total * x / kXcds;
+            if (run >= target && run - c < target) bound[x] = r;   // the first row tile at or past the target
+        }
+        run += c;
+    }
+    __syncthreads();
+    if (tid <= kXcds) p.down_slices[tid] = ((tid == 0) ? 0 : bound[tid]) * p.down_col_tiles * ns;
 }
 
 }  // namespace unifmoe

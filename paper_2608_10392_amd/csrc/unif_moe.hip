@@ -250,6 +250,7 @@ struct FwdPlan {
     size_t pair_token, pair_mask, pair_expert, pair_of, pair_rank, slab_rows, slab_tok, up_tile_info, up_tile_rows, hbuf, part;
     size_t xn;      // LN(X), the FFN input of a pre-LN block
     size_t wdown16; // fp16 copy of W_down (bf16 layers)
+    size_t down_slices; // [kXcds + 1] down tiles per XCD queue
     size_t total;
 };
 
@@ -291,6 +292,7 @@ FwdPlan plan_forward(const Dims& m, size_t xn_bytes = 0) {
     p.slab_count = cv.take(4 * (size_t)m.nslab);
     p.exp_total = cv.take(4 * (size_t)kExpCopies * K1);
     p.totals = cv.take(4 * 8);
+    p.down_slices = cv.take(4 * (kXcds + 1));
     p.queues = cv.take(4 * 16);   // per-XCD tile counters: up, then down
     p.zero_page = cv.take(256);
     p.zero_end = cv.cur;
@@ -686,6 +688,10 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
     pp.pair_rank = rp.pair_rank;
     pp.ntile = ceil_div(m.N, kTileTok);
     pp.max_pairs = (int)m.pcap;
+    pp.down_slices = reinterpret_cast<int*>(ws + plan.down_slices);
+    pp.down_stages = m.M / 64;
+    // The backward (tables_only) runs its down-projection unsplit.
+    pp.down_splits = tables_only ? 1 : down_splits(m);
     // Expert segments and bin cursors; per slab (bf16), its rows per token
     // tile as first rows.
     scan_kernel<<<(unsigned)(m.K1 + (m.bf16 ? m.nslab : 0)), kScanThreads, 0, st>>>(pp);
@@ -707,6 +713,9 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         // worst case only up to a few workgroups per CU).
         down_tables_kernel<<<(unsigned)std::min<size_t>(ceil_div_sz(plan.max_row_tiles, 4), (size_t)cus * 4), 256, 0,
                              st>>>(pp);
+        UNIF_LAUNCH_CHECK();
+        // The down tiles of each XCD's queue, split by cost.
+        down_slices_kernel<<<1, kSliceThreads, 0, st>>>(pp);
         UNIF_LAUNCH_CHECK();
         UNIF_MARK(3);
         if (tables_only) return UNIF_OK;
@@ -751,7 +760,7 @@ int32_t forward_impl(const unif_moe_config* cfg, const unif_moe_block* blk, cons
         dn.rt_info = pp.rt_info;
         dn.rt_masks = pp.rt_masks;
         dn.pair_mask = pp.pair_mask;
-        dn.totals = totals;
+        dn.slices = pp.down_slices;
         dn.queue = reinterpret_cast<int*>(ws + plan.queues) + 8;
         dn.nsplit = down_splits(m);
         dn.split_stride = (m.pcap + 1) * m.d;
@@ -1136,7 +1145,7 @@ int32_t unif_moe_layer_backward(const unif_moe_config* cfg_in, const void* X, co
         dn.rt_info = reinterpret_cast<const int4*>(ws + fp.rt_info);
         dn.rt_masks = reinterpret_cast<const uint64_t*>(ws + fp.rt_masks);
         dn.pair_mask = p.pair_mask;
-        dn.totals = p.totals;
+        dn.slices = reinterpret_cast<const int*>(ws + fp.down_slices);
         dn.queue = queues + 16;
         dn.nsplit = 1;
         dn.split_stride = 0;
