@@ -394,6 +394,10 @@ typedef struct unif_moe_work_t {
     int64_t down_tiles;       /* down-projection tiles (row tiles x column tiles) */
     double  up_mfma_flops;    /* matrix-core FLOPs the up-projection executed     */
     double  down_mfma_flops;  /* matrix-core FLOPs the down-projection executed   */
+    int64_t down_parts;       /* parts each down tile's block union is split into */
+    int64_t down_queued;      /* down tiles the per-XCD queues hold, summed over  */
+                              /* the queues: down_tiles x down_parts when each    */
+                              /* tile is queued exactly once                      */
 } unif_moe_work_t;
 
 /* Reads the tile tables that the last unif_moe_layer_forward (or

@@ -67,7 +67,8 @@ N_PHASE_EVENTS = 7
 
 class Work(ctypes.Structure):
     _fields_ = [("pairs", ctypes.c_int64), ("up_tiles", ctypes.c_int64), ("down_tiles", ctypes.c_int64),
-                ("up_mfma_flops", ctypes.c_double), ("down_mfma_flops", ctypes.c_double)]
+                ("up_mfma_flops", ctypes.c_double), ("down_mfma_flops", ctypes.c_double),
+                ("down_parts", ctypes.c_int64), ("down_queued", ctypes.c_int64)]
 
 
 class UnifMoeError(RuntimeError):
@@ -340,7 +341,8 @@ def forward_work(cfg, workspace, stream=None):
     _check(lib().unif_moe_forward_work(ctypes.byref(c), _ptr(workspace), ws_bytes, ctypes.byref(w),
                                        _stream(stream)), "unif_moe_forward_work")
     return dict(pairs=w.pairs, up_tiles=w.up_tiles, down_tiles=w.down_tiles,
-                up_mfma_flops=w.up_mfma_flops, down_mfma_flops=w.down_mfma_flops)
+                up_mfma_flops=w.up_mfma_flops, down_mfma_flops=w.down_mfma_flops,
+                down_parts=w.down_parts, down_queued=w.down_queued)
 
 
 

@@ -483,7 +483,10 @@ __global__ __launch_bounds__(256) void down_tables_kernel(PermuteParams p) {
 // (one workgroup, after down_tables): a row tile's tiles cost about its
 // stages (at least 4) plus 2 for each tile's epilogue and hand-over, per
 // column tile and part. XCD x takes the row tiles from the first whose
-// exclusive cost prefix reaches x / kXcds of the total.
+// exclusive cost prefix reaches x / kXcds of the total: r + 1 for the one
+// row tile r whose cost interval (prefix(r), prefix(r) + cost(r)] holds that
+// target (costs are positive, so the intervals tile (0, total] and the
+// boundaries never decrease), 0 for a target of 0.
 constexpr int kSliceThreads = 1024;
 __global__ __launch_bounds__(kSliceThreads) void down_slices_kernel(PermuteParams p) {
     __shared__ int part[kSliceThreads];
@@ -495,7 +498,7 @@ __global__ __launch_bounds__(kSliceThreads) void down_slices_kernel(PermuteParam
     int sum = 0;
     for (int r = r0; r < r1; ++r) sum += cost(r);
     part[tid] = sum;
-    if (tid <= kXcds) bound[tid] = nrt;
+    if (tid <= kXcds) bound[tid] = (tid == kXcds) ? nrt : 0;
     __syncthreads();
     for (int off = 1; off < T; off <<= 1) {
         const int v = (tid >= off) ? part[tid - off] : 0;
@@ -509,12 +512,12 @@ __global__ __launch_bounds__(kSliceThreads) void down_slices_kernel(PermuteParam
         const int c = cost(r);
         for (int x = 1; x < kXcds; ++x) {
             const long long target = total * x / kXcds;
-            if (run >= target && run - c < target) bound[x] = r;   // the first row tile at or past the target
+            if (run < target && run + c >= target) bound[x] = r + 1;
         }
         run += c;
     }
     __syncthreads();
-    if (tid <= kXcds) p.down_slices[tid] = ((tid == 0) ? 0 : bound[tid]) * p.down_col_tiles * ns;
+    if (tid <= kXcds) p.down_slices[tid] = bound[tid] * p.down_col_tiles * ns;
 }
 
 }  // namespace unifmoe

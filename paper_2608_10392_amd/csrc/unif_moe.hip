@@ -1405,10 +1405,12 @@ int32_t unif_moe_forward_work(const unif_moe_config* cfg, const void* workspace,
     work_kernel<<<(unsigned)std::min<size_t>(ceil_div_sz(plan.max_row_tiles, 256), 1024), 256, 0, st>>>(
         reinterpret_cast<const uint64_t*>(ws + plan.rt_masks), totals, dsh.tm / 32, cnt);
     UNIF_LAUNCH_CHECK();
-    int32_t t[8];
+    int32_t t[8], sl[kXcds + 1];
     unsigned long long g = 0;
     if (hipMemcpyAsync(t, totals, sizeof(t), hipMemcpyDeviceToHost, st) != hipSuccess) return UNIF_EDEVICE;
     if (hipMemcpyAsync(&g, cnt, sizeof(g), hipMemcpyDeviceToHost, st) != hipSuccess) return UNIF_EDEVICE;
+    if (hipMemcpyAsync(sl, ws + plan.down_slices, sizeof(sl), hipMemcpyDeviceToHost, st) != hipSuccess)
+        return UNIF_EDEVICE;
     if (hipStreamSynchronize(st) != hipSuccess) return UNIF_EDEVICE;
     const double dM = (double)m.M, dd = (double)m.d;
     host_out->pairs = t[0];
@@ -1416,6 +1418,8 @@ int32_t unif_moe_forward_work(const unif_moe_config* cfg, const void* workspace,
     host_out->down_tiles = t[2];
     host_out->up_mfma_flops = (double)t[1] * up_tm(m.M, m.d) * dM * dd * 2.0;
     host_out->down_mfma_flops = (double)g * 32.0 * dM * dd * 2.0;
+    host_out->down_parts = down_splits(m);
+    for (int x = 0; x < kXcds; ++x) host_out->down_queued += std::max(0, sl[x + 1] - sl[x]);
     return UNIF_OK;
 }
 

@@ -35,6 +35,11 @@ def run_case(g, label, n_sample=None, near_cap=256):
     dev = _device_layer(g)
     dev.forward()
     torch.cuda.synchronize()
+    if cfg["dtype"] == "bf16":
+        # the per-XCD queues of the down-projection hold every tile once
+        from paper_2608_10392_amd import _lib
+        w = _lib.forward_work(layer_config(cfg), dev.ws_forward)
+        assert w["down_queued"] == w["down_tiles"] * w["down_parts"], w
     grec, Y = dev.routing_numpy(), dev.output_numpy()
     orec = O.route(cfg, g["X"], g["valid"], g["W_router"], g["prototypes"])
     summary = parity.check_routing(cfg, orec, grec)
@@ -198,6 +203,11 @@ def test_nonfinite_tokens_keep_routing_in_range():
     dev = _device_layer(g)
     dev.forward()
     torch.cuda.synchronize()
+    if cfg["dtype"] == "bf16":
+        # the per-XCD queues of the down-projection hold every tile once
+        from paper_2608_10392_amd import _lib
+        w = _lib.forward_work(layer_config(cfg), dev.ws_forward)
+        assert w["down_queued"] == w["down_tiles"] * w["down_parts"], w
     grec, Y = dev.routing_numpy(), dev.output_numpy()
     for t in bad:
         ids = grec["expert_ids"][t]
@@ -250,6 +260,7 @@ def test_forward_work_counts(routing_passed):
         dev.route()   # the same decisions, into dev.routing, for the tie check
     torch.cuda.synchronize()
     w = _lib.forward_work(cfg, dev.ws_forward)
+    assert w["down_queued"] == w["down_tiles"] * w["down_parts"], w
     orec = O.route(g["cfg"], g["X"], g["valid"], g["W_router"], g["prototypes"])
     if parity.check_routing(g["cfg"], orec, dev.routing_numpy())["n_near_differ"]:
         pytest.skip("a near-tie decision differs; counts are then not fixed by the oracle")
