@@ -43,12 +43,13 @@ def test_struct_layout_matches_header(tmp_path):
         '#include <stdio.h>\n#include <stddef.h>\n#include "unif_moe.h"\n'
         "#define F(T, m) printf(#T \".\" #m \" %zu\\n\", offsetof(T, m))\n"
         "int main(void) {\n"
-        ' printf("config %zu\\nrouting %zu\\nstats %zu\\nblock %zu\\n", sizeof(unif_moe_config),'
-        " sizeof(unif_moe_routing), sizeof(unif_moe_stats_t), sizeof(unif_moe_block));\n"
+        ' printf("config %zu\\nrouting %zu\\nstats %zu\\nblock %zu\\nwork %zu\\n", sizeof(unif_moe_config),'
+        " sizeof(unif_moe_routing), sizeof(unif_moe_stats_t), sizeof(unif_moe_block), sizeof(unif_moe_work_t));\n"
         " F(unif_moe_config, tau); F(unif_moe_config, select_mode); F(unif_moe_config, max_pairs);"
         " F(unif_moe_routing, weights); F(unif_moe_stats_t, expert_tokens);"
         " F(unif_moe_stats_t, activated_blocks); F(unif_moe_stats_t, routing_flops);\n"
         " F(unif_moe_block, ln_eps); F(unif_moe_block, ln_gamma); F(unif_moe_block, b_down);\n"
+        " F(unif_moe_work_t, down_mfma_flops); F(unif_moe_work_t, down_queued);\n"
         " return 0; }\n")
     exe = tmp_path / "layout"
     subprocess.run(["gcc", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
@@ -67,6 +68,9 @@ def test_struct_layout_matches_header(tmp_path):
     assert int(got["unif_moe_block.ln_eps"]) == _lib.Block.ln_eps.offset
     assert int(got["unif_moe_block.ln_gamma"]) == _lib.Block.ln_gamma.offset
     assert int(got["unif_moe_block.b_down"]) == _lib.Block.b_down.offset
+    assert int(got["work"]) == ctypes.sizeof(_lib.Work)
+    assert int(got["unif_moe_work_t.down_mfma_flops"]) == _lib.Work.down_mfma_flops.offset
+    assert int(got["unif_moe_work_t.down_queued"]) == _lib.Work.down_queued.offset
 
 
 def test_status_strings(L):
