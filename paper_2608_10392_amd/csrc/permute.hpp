@@ -361,7 +361,7 @@ __device__ __forceinline__ void scatter_tile(const PermuteParams& p, int q, cons
     const int bc = q % kBinCopies;   // the bin copy of this token tile
     if (v) {
         const int kr = mask_key(rm, B, kb);
-        // This wave's residual pairs, in batches: every atomic of a batch is
+        // This wave's residual pairs, in batches: every load of a batch is
         // issued before its results are used.
         constexpr int kBatch = 4;
         const int* rank = p.pair_rank + (size_t)t * K1;
@@ -408,12 +408,15 @@ __device__ __forceinline__ void scatter_tile(const PermuteParams& p, int q, cons
         if (!ballot(he)) continue;
         const uint64_t me = (e == 0) ? m : rm;
         const int pr = he ? pidx[lane * K1 + e] : 0;
+        // The expert's first rows, one slab per lane (B <= 64), read back
+        // per slab from a register instead of LDS.
+        const int fe = (lane < B) ? first[e * B + lane] : 0;
         for (int c = 0; c < B; ++c) {
             const bool has = he && ((me >> c) & 1ull);
             const uint64_t bits = ballot(has);
             if (!bits) continue;
             if (has) {
-                const int at = first[e * B + c] + __popcll(bits & below);
+                const int at = __builtin_amdgcn_readlane(fe, c) + __popcll(bits & below);
                 p.slab_rows[at] = pr;
                 p.slab_tok[at] = t;
             }
