@@ -73,6 +73,32 @@ __global__ void fill_zero_kernel(uint32_t* __restrict__ p, size_t n) {
         p[i] = 0u;
 }
 
+// Exclusive prefix over the workgroup (thread order) of each thread's s, and
+// the total in every thread: an inclusive scan inside each wave with
+// shuffles, then the wave totals through lds (at least blockDim.x / 64
+// words). Two barriers instead of two per doubling step; lds is free again
+// on return. blockDim.x is a multiple of 64, at most 1024.
+__device__ __forceinline__ int block_prefix(int s, int* lds, int& total) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    int x = s;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) lds[w] = x;
+    __syncthreads();
+    int base = 0, tot = 0;
+    for (int i = 0; i < nw; ++i) {
+        const int v = lds[i];
+        base += (i < w) ? v : 0;
+        tot += v;
+    }
+    __syncthreads();
+    total = tot;
+    return base + x - s;
+}
+
 // Exclusive prefix sum of get(0..n-1) by one workgroup: each thread sums a
 // contiguous chunk, the chunk sums are scanned in LDS, then each thread
 // writes its chunk. Returns the total (same value in every thread).
@@ -104,16 +130,8 @@ __device__ int block_exclusive_scan(int n, Get get, Put put, int* lds) {
     } else {
         for (int i = beg; i < end; ++i) s += get(i);
     }
-    lds[tid] = s;
-    __syncthreads();
-    for (int off = 1; off < T; off <<= 1) {
-        const int x = (tid >= off) ? lds[tid - off] : 0;
-        __syncthreads();
-        lds[tid] += x;
-        __syncthreads();
-    }
-    int run = lds[tid] - s;
-    const int total = lds[T - 1];
+    int total;
+    int run = block_prefix(s, lds, total);
     if (per <= R) {
 #pragma unroll
         for (int u = 0; u < R; ++u)
@@ -157,16 +175,8 @@ __device__ int staged_exclusive_scan(int n, Get get, Put put, int* stage, int* l
         const int beg = min(cnt, tid * per), end = min(cnt, beg + per);
         int s = 0;
         for (int i = beg; i < end; ++i) s += stage[i];
-        lds[tid] = s;
-        __syncthreads();
-        for (int off = 1; off < T; off <<= 1) {
-            const int v = (tid >= off) ? lds[tid - off] : 0;
-            __syncthreads();
-            lds[tid] += v;
-            __syncthreads();
-        }
-        int run = carry + lds[tid] - s;
-        const int total = lds[T - 1];
+        int total;
+        int run = carry + block_prefix(s, lds, total);
         for (int i = beg; i < end; ++i) {
             const int c = stage[i];
             stage[i] = run;
@@ -310,15 +320,8 @@ __device__ __forceinline__ void up_tiles_of_group(const PermuteParams& p, int gr
     const int qa = min(nq, tid * per), qb = min(nq, qa + per);
     int n = 0;
     for (int c = 0; c < ng; ++c) n += tl[qb * ng + c] - tl[qa * ng + c];
-    scan[tid] = n;
-    __syncthreads();
-    for (int off = 1; off < T; off <<= 1) {
-        const int v = (tid >= off) ? scan[tid - off] : 0;
-        __syncthreads();
-        scan[tid] += v;
-        __syncthreads();
-    }
-    int pos = uo[sl0 + c0] + scan[tid] - n;
+    int ntot;
+    int pos = uo[sl0 + c0] + block_prefix(n, scan, ntot);
     for (int i = qa; i < qb; ++i)
         for (int c = 0; c < ng; ++c) {
             const int sl = sl0 + c0 + c, cnt = cn[c], s0 = so[sl];
@@ -492,7 +495,7 @@ __global__ __launch_bounds__(256) void down_tables_kernel(PermuteParams p) {
 // boundaries never decrease), 0 for a target of 0.
 constexpr int kSliceThreads = 1024;
 __global__ __launch_bounds__(kSliceThreads) void down_slices_kernel(PermuteParams p) {
-    __shared__ int part[kSliceThreads];
+    __shared__ int part[kSliceThreads / 64];
     __shared__ int bound[kXcds + 1];
     const int nrt = p.totals[4], ns = p.down_splits;
     const int T = blockDim.x, tid = threadIdx.x;
@@ -500,17 +503,10 @@ __global__ __launch_bounds__(kSliceThreads) void down_slices_kernel(PermuteParam
     auto cost = [&](int rt) { return p.down_col_tiles * (max(p.rt_info[rt].w * p.down_stages, 4) + 2 * ns); };
     int sum = 0;
     for (int r = r0; r < r1; ++r) sum += cost(r);
-    part[tid] = sum;
     if (tid <= kXcds) bound[tid] = (tid == kXcds) ? nrt : 0;
-    __syncthreads();
-    for (int off = 1; off < T; off <<= 1) {
-        const int v = (tid >= off) ? part[tid - off] : 0;
-        __syncthreads();
-        part[tid] += v;
-        __syncthreads();
-    }
-    const long long total = part[T - 1];
-    long long run = part[tid] - sum;
+    int itotal;
+    long long run = block_prefix(sum, part, itotal);
+    const long long total = itotal;
     for (int r = r0; r < r1; ++r) {
         const int c = cost(r);
         for (int x = 1; x < kXcds; ++x) {
